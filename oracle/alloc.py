@@ -1,0 +1,159 @@
+"""Joint Lagrangian allocation of Tucker ranks and residual bits (fp64 oracle).
+
+Section 4, "Joint Lagrangian allocation":
+
+* eq. (1) byte cost of a cell at (r_T, r_d, b):
+  s = (m r_T r_d + T r_T + d r_d) c + (b/8) m T d, plus - in this library's
+  reading - 2 bytes per quantiser group for the fp16 scales the paper calls a
+  negligible per-row term (switchable);
+* eq. (2) error model e = eps^2(b) * tau(r_T, r_d), with eps^2(0) = 1 and
+  eps^2(b) calibrated once on a Gaussian round trip; tau is the relative
+  Frobenius mass the truncation discards, read here as
+  min(1, tau_T(r_T) + tau_d(r_d)) from the mode spectra of the original cell
+  (the ST-HOSVD upper bound; (0, 0) discards everything, tau = 1);
+* eq. (3) minimise the summed error subject to the summed cost <= B;
+* eq. (4) Lagrangian relaxation: for fixed lambda each cell minimises
+  e + lambda s over its finite grid independently, and one bisection on
+  lambda drives the total cost to the budget.
+
+Section 5, "Cap selection": q_cap = min(max(q_min(R), ceil(T/32)), 512) with
+q_min = 32 for R <= 4 and 64 otherwise.
+
+Deterministic conventions (so that two independent implementations agree
+bit for bit on the same spectra):
+
+* grid: r_T in {0} U {k*step <= r_T_max}, r_d in {k*step <= d} (r_d = 0 only
+  with r_T = 0), b in the bit grid; optional floors restrict it;
+* grid points are ordered by (cost, bits, r_T, r_d) and a cell takes the first
+  point of minimal e + lambda s in that order (ties go to the cheaper point);
+* e = eps2[b] * min(1, tau_T[r_T] + tau_d[r_d]); value = e + lambda * s, all in
+  IEEE double without fused multiply-add;
+* bisection on lambda in [0, 1e3]: if the lambda = 0 allocation fits, it is
+  returned; if even lambda = 1e3 (the cheapest allocation) does not fit, that
+  allocation is returned with the infeasible flag set; otherwise
+  mid = 0.5 (lo + hi) replaces hi when S(mid) <= B and lo otherwise, until
+  hi - lo <= 1e-15 hi or 200 halvings, and the allocation at hi is returned.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from .philox import calibration_samples, rotation_signs
+from .residual import residual_roundtrip
+from .tucker import tail_fractions
+
+BIT_GRID = (0, 2, 4, 8)
+LAMBDA_HI = 1e3
+MAX_HALVINGS = 200
+
+
+def q_cap(T: int, R: float) -> int:
+    q_min = 32 if R <= 4 else 64
+    return int(min(max(q_min, math.ceil(T / 32)), 512))
+
+
+def byte_cost(m: int, T: int, d: int, r_T: int, r_d: int, b: int, c: int, g: int,
+              count_scales: bool = True) -> int:
+    s = (m * r_T * r_d + T * r_T + d * r_d) * c
+    if b > 0:
+        s += (b * m * T * d) // 8
+        if count_scales:
+            s += 2 * ((m * T * d) // g)
+    return int(s)
+
+
+@dataclass
+class CellSpectrum:
+    m: int
+    T: int
+    d: int
+    c: int                 # bytes per stored factor scalar
+    g: int                 # quantiser group size
+    E: float
+    lam_T: np.ndarray      # token-mode eigenvalues (flash: q_eff values + tail)
+    lam_d: np.ndarray      # feature-mode eigenvalues (d values)
+    rT_max: int            # largest admissible token rank
+    extra: dict = field(default_factory=dict)
+
+
+def allocate(cells, budget: float, eps2: dict, *, bits=BIT_GRID, step: int = 8,
+             floors=(0, 0, 0), count_scales: bool = True):
+    """Solve eq. (3) through eq. (4); returns dict(alloc=[(r_T, r_d, b)], ...)."""
+    grids = []
+    for cell in cells:
+        tau_T = tail_fractions(cell.lam_T, cell.E)
+        tau_d = tail_fractions(cell.lam_d, cell.E)
+        fT, fd, fb = floors
+        rTs = [0] + list(range(step, cell.rT_max + 1, step))
+        rds = list(range(step, cell.d + 1, step))
+        pts = []
+        for b in bits:
+            if b < fb:
+                continue
+            for rT in rTs:
+                if rT < fT:
+                    continue
+                for rd in ([0] if rT == 0 else rds):
+                    if rT > 0 and rd < fd:
+                        continue
+                    pts.append((byte_cost(cell.m, cell.T, cell.d, rT, rd, b, cell.c,
+                                          cell.g, count_scales), b, rT, rd))
+        if not pts:
+            raise ValueError("empty allocation grid (floors exclude every point)")
+        pts.sort()
+        P = np.array(pts, dtype=np.int64)
+        s = P[:, 0].astype(np.float64)
+        eb = np.array([float(eps2[int(x)]) for x in P[:, 1]])
+        e = eb * np.minimum(1.0, tau_T[P[:, 2]] + tau_d[P[:, 3]])
+        grids.append((s, e, P))
+
+    def choose(lam):
+        idx = [int(np.argmin(e + lam * s)) for (s, e, _) in grids]
+        total = float(sum(g[0][i] for g, i in zip(grids, idx)))
+        return idx, total
+
+    def result(idx, lam, infeasible):
+        alloc = [tuple(int(v) for v in g[2][i][[2, 3, 1]]) for g, i in zip(grids, idx)]
+        total = float(sum(g[0][i] for g, i in zip(grids, idx)))
+        err = float(sum(g[1][i] for g, i in zip(grids, idx)))
+        return dict(alloc=alloc, lam=lam, total_bytes=total, model_error=err,
+                    infeasible=infeasible)
+
+    idx0, S0 = choose(0.0)
+    if S0 <= budget:
+        return result(idx0, 0.0, False)
+    lo, hi = 0.0, LAMBDA_HI
+    idx_hi, S_hi = choose(hi)
+    if S_hi > budget:
+        return result(idx_hi, hi, True)
+    for _ in range(MAX_HALVINGS):
+        if hi - lo <= 1e-15 * hi:
+            break
+        mid = 0.5 * (lo + hi)
+        idx_mid, S_mid = choose(mid)
+        if S_mid <= budget:
+            hi, idx_hi = mid, idx_mid
+        else:
+            lo = mid
+    return result(idx_hi, hi, False)
+
+
+def allocation_cost(cells, alloc, *, count_scales=True) -> float:
+    return float(sum(byte_cost(c.m, c.T, c.d, rT, rd, b, c.c, c.g, count_scales)
+                     for c, (rT, rd, b) in zip(cells, alloc)))
+
+
+def calibrate_eps2(*, group: int, d: int, seed: int = 0, n_samples: int = 1 << 20,
+                   bits=(2, 4, 8)) -> dict:
+    """eps^2(b) = ||x^ - x||^2 / ||x||^2 of a Gaussian round trip (eq. (2) calibration)."""
+    x = calibration_samples(seed, n_samples).reshape(-1, d)
+    signs = rotation_signs(seed, d)
+    out = {0: 1.0}
+    den = float(np.sum(x * x))
+    for b in bits:
+        xh = residual_roundtrip(x, signs, b, group)
+        out[b] = float(np.sum((xh - x) ** 2)) / den
+    return out

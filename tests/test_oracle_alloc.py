@@ -1,0 +1,104 @@
+"""Pins of the oracle's byte model, cap policy and Lagrangian allocator (sections 4, 5, 8)."""
+import itertools
+
+import numpy as np
+import pytest
+
+from conftest import golden, lowrank_cell
+from oracle import alloc, pipeline, tucker as tk
+
+
+def test_byte_model_matches_paper_footprint():
+    """Section 8: Mistral-7B at ctx-2048 occupies 268.4 MB uncompressed, and the
+    compressed footprints at 2/3/4/8x land at the printed sizes (1.99-7.98x)."""
+    g = golden("paper_memory_footprint.json")
+    mdl = g["model"]
+    total = 2 * mdl["layers"] * mdl["kv_heads"] * mdl["ctx"] * mdl["head_dim"] * mdl["bytes_per_scalar"]
+    assert round(total / 1e6, 1) == g["uncompressed_MB"]
+    lo, hi = g["achieved_ratio_range"]
+    for R, mb in g["compressed_MB"].items():
+        achieved = total / (mb * 1e6)
+        assert lo - 0.005 <= achieved <= hi + 0.005
+        assert abs(achieved / float(R) - 1) < 0.005     # meets each target to 0.5%
+
+
+def test_byte_cost_eq1_terms():
+    """eq. (1): core m r_T r_d, token factor T r_T, feature factor d r_d scalars at
+    c bytes, plus b/8 bytes per cached entry; scales add 2 bytes per group."""
+    m, T, d = 8, 256, 128
+    assert alloc.byte_cost(m, T, d, 0, 0, 0, 2, 64) == 0
+    assert alloc.byte_cost(m, T, d, 64, 64, 0, 4, 64) == (8 * 64 * 64 + 256 * 64 + 128 * 64) * 4
+    assert alloc.byte_cost(m, T, d, 0, 0, 4, 2, 64, count_scales=False) == m * T * d // 2
+    assert alloc.byte_cost(m, T, d, 64, 64, 2, 4, 64) == 229376 + 65536 + 8192
+    # doubling every rank roughly quadruples the core term only
+    a = alloc.byte_cost(m, T, d, 16, 16, 0, 2, 64)
+    b = alloc.byte_cost(m, T, d, 32, 32, 0, 2, 64)
+    assert b - 2 * a == 2 * m * 16 * 16 * 2
+
+
+def test_cap_policy_matches_paper():
+    for c in golden("paper_cap_policy.json")["cases"]:
+        assert alloc.q_cap(c["T"], c["R"]) == c["q"], c
+    for T in (64, 256, 512, 1000, 1024):       # "a no-op for T <= 1024"
+        assert alloc.q_cap(T, 2) == 32 and alloc.q_cap(T, 6) == 64
+    qs = [alloc.q_cap(T, 3) for T in range(1, 40000, 97)]
+    assert (np.diff(qs) >= 0).all() and max(qs) == 512
+
+
+def _cells(rng, n, m=2, T=24, d=16):
+    out = []
+    for i in range(n):
+        X = lowrank_cell(rng, m, T, d, 4, noise=0.2 + 0.3 * i, decay=0.5 + i)
+        sp = pipeline.spectrum(X)
+        out.append(alloc.CellSpectrum(m=m, T=T, d=d, c=2, g=8, E=sp["E"], lam_T=sp["lam_T"],
+                                      lam_d=sp["lam_d"], rT_max=T))
+    return out
+
+
+def _enumerate(cells, eps2, step):
+    per = []
+    for c in cells:
+        opts = [(0, 0, b) for b in alloc.BIT_GRID]
+        opts += [(rT, rd, b) for rT in range(step, c.rT_max + 1, step)
+                 for rd in range(step, c.d + 1, step) for b in alloc.BIT_GRID]
+        tauT = tk.tail_fractions(c.lam_T, c.E)
+        taud = tk.tail_fractions(c.lam_d, c.E)
+        per.append([(alloc.byte_cost(c.m, c.T, c.d, rT, rd, b, c.c, c.g),
+                     eps2[b] * min(1.0, tauT[rT] + taud[rd]), (rT, rd, b)) for rT, rd, b in opts])
+    return per
+
+
+def test_everett_optimality_against_brute_force(rng):                 # P11
+    eps2 = {0: 1.0, 2: 0.26, 4: 0.0101, 8: 3.5e-5}
+    cells = _cells(rng, 3)
+    per = _enumerate(cells, eps2, 8)
+    total_in = sum(c.m * c.T * c.d * 2 for c in cells)
+    for ratio in (1.5, 2.0, 3.0, 5.0, 9.0):
+        res = alloc.allocate(cells, total_in / ratio, eps2)
+        S = res["total_bytes"]
+        assert S <= total_in / ratio
+        # no allocation that spends at most S bytes has a smaller summed model error
+        best = min(sum(p[1] for p in combo) for combo in itertools.product(*per)
+                   if sum(p[0] for p in combo) <= S)
+        assert res["model_error"] <= best + 1e-15
+
+
+def test_spend_nonincreasing_in_lambda(rng):
+    eps2 = {0: 1.0, 2: 0.26, 4: 0.0101, 8: 3.5e-5}
+    cells = _cells(rng, 4)
+    total_in = sum(c.m * c.T * c.d * 2 for c in cells)
+    spends = []
+    for ratio in (1.2, 1.5, 2, 3, 4, 6, 10, 20):
+        spends.append(alloc.allocate(cells, total_in / ratio, eps2)["total_bytes"])
+    assert (np.diff(spends) <= 0).all()
+
+
+def test_generous_budget_gives_min_error_and_tiny_budget_flags(rng):
+    eps2 = {0: 1.0, 2: 0.26, 4: 0.0101, 8: 3.5e-5}
+    cells = _cells(rng, 2)
+    res = alloc.allocate(cells, 1e12, eps2)
+    assert res["lam"] == 0.0 and res["model_error"] <= 1e-12
+    tiny = alloc.allocate(cells, 1.0, eps2, floors=(8, 8, 0))
+    assert tiny["infeasible"] and all(a[0] >= 8 for a in tiny["alloc"])
+    zero = alloc.allocate(cells, 0.0, eps2)
+    assert not zero["infeasible"] and zero["alloc"] == [(0, 0, 0)] * 2
