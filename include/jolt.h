@@ -1,0 +1,196 @@
+/*
+ * jolt.h - C ABI of the MI355X (gfx950) implementation of the JoLT / FlashJoLT
+ * KV-cache compression path ("A JoLT for the KV Cache", arXiv 2607.12550).
+ *
+ * What is computed (one "cell" = one layer group's keys or values, section 4):
+ *   X in R^{m x T x d}, m = layers_in_group * heads, slice s = layer * n_heads + head.
+ *   jolt_spectrum   : energy E = ||X||_F^2, token-mode spectrum (exact Gram
+ *                     eigenvalues, section 4 "Partial Tucker backbone", or the
+ *                     FlashJoLT randomized SVD with tail-mass accounting,
+ *                     section 5) and feature-mode spectrum.
+ *   jolt_allocate   : eq. (1)-(4): byte model, error model, Lagrangian
+ *                     bisection choosing (r_T, r_d, b) per cell under a budget.
+ *   jolt_compress   : ST-HOSVD truncation at (r_T, r_d), fp16 factor
+ *                     serialisation (section 9), residual R = X - X~ against the
+ *                     stored factors, randomized Hadamard rotation and b-bit
+ *                     group quantisation (section 4 "Rotated residual").
+ *   jolt_decompress : X^ = X~ + rotation^-1(dequantised residual).
+ *
+ * Conventions shared by every entry point:
+ *   - Return JOLT_OK (0) or a negative JOLT_E_* code; jolt_last_error() gives a
+ *     thread-local message for the last failure.  No C++ exception crosses the ABI.
+ *   - Every argument is validated on the host before any device work is queued.
+ *   - Device memory is owned by the caller: input tensors, blobs, outputs and the
+ *     workspace.  The library never allocates device memory.
+ *   - Device work is queued on the caller's stream (a hipStream_t passed as
+ *     jolt_stream; NULL = the default stream).  jolt_spectrum synchronises that
+ *     stream because it returns host arrays; the other calls are asynchronous.
+ *   - A call processes n_cells cells of one shape (one jolt_cell_desc) together:
+ *     their kernels are batched, so per-cell host arrays have n_cells entries.
+ *   - Pointer arrays (X, blobs, Xhat) are host arrays of device pointers.
+ */
+#ifndef JOLT_H
+#define JOLT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct jolt_ctx jolt_ctx;
+typedef void *jolt_stream; /* hipStream_t */
+
+enum {
+  JOLT_OK = 0,
+  JOLT_E_INVAL = -1,       /* bad argument (null pointer, out-of-range value) */
+  JOLT_E_UNSUPPORTED = -2, /* valid but not supported (e.g. d not a power of two) */
+  JOLT_E_WORKSPACE = -3,   /* workspace or blob buffer too small */
+  JOLT_E_BLOB = -4,        /* corrupt or mismatched blob header */
+  JOLT_E_HIP = -5,         /* HIP runtime error (message has the HIP error string) */
+  JOLT_E_NONFINITE = -6,   /* input contains NaN or Inf */
+  JOLT_E_STATE = -7        /* call sequence error (e.g. stale spectrum reuse) */
+};
+
+enum { JOLT_F32 = 0, JOLT_BF16 = 1 };            /* element types of caches and outputs */
+enum { JOLT_EXACT = 0, JOLT_FLASH = 1 };         /* token-mode method */
+enum { JOLT_FACTOR_F32 = 0, JOLT_FACTOR_F16 = 1 };/* stored factor precision (c = 4 / 2) */
+
+/* Shape and memory layout of one cell; cells passed together share it.
+ * Element (slice s, token t, feature f) of a cell whose base pointer is P lives at
+ *   P + (s / n_heads) * stride_layer + (s % n_heads) * stride_head + t * stride_token + f
+ * (strides in elements).  Features are contiguous. */
+typedef struct {
+  int32_t dtype;        /* JOLT_F32 or JOLT_BF16 */
+  int32_t n_layers;     /* layers in the group (>= 1) */
+  int32_t n_heads;      /* heads per layer (>= 1); m = n_layers * n_heads */
+  int32_t T;            /* tokens (>= 1) */
+  int32_t d;            /* features: power of two, 32 <= d <= 256 */
+  int32_t reserved;
+  int64_t stride_layer;
+  int64_t stride_head;
+  int64_t stride_token; /* >= d */
+} jolt_cell_desc;
+
+/* Options of the token-mode spectrum (section 5 for the FlashJoLT fields). */
+typedef struct {
+  int32_t method;      /* JOLT_EXACT or JOLT_FLASH */
+  int32_t q;           /* FlashJoLT kept directions; 0 = cap policy jolt_q_cap(T, ratio) */
+  double ratio;        /* target compression ratio R read by the cap policy */
+  int32_t oversample;  /* p: sketch width l = min(q + p, T, m*d) */
+  int32_t power_iters; /* power (subspace) iterations of the range finder */
+} jolt_spectrum_opts;
+
+/* Per-cell compression parameters. */
+typedef struct {
+  int32_t r_T, r_d;     /* Tucker ranks; r_T = 0 iff r_d = 0 (no backbone) */
+  int32_t bits;         /* residual bits b in {0, 2, 4, 8}; 0 stores no residual */
+  int32_t group;        /* quantiser group size g: divides d, multiple of 8 */
+  int32_t factor_dtype; /* JOLT_FACTOR_F16 (c = 2) or JOLT_FACTOR_F32 (c = 4) */
+  int32_t reserved;
+  uint64_t seed;        /* rotation signs; for FlashJoLT also the sketch (must equal
+                           the seed given to jolt_spectrum when its result is reused) */
+} jolt_params;
+
+/* Host-side description of one cell's spectra for the allocator. */
+typedef struct {
+  int32_t m, T, d;
+  int32_t c;             /* bytes per stored factor scalar */
+  int32_t g;             /* quantiser group size */
+  int32_t n_lam_T;       /* entries of lam_T */
+  int32_t rT_max;        /* largest admissible r_T */
+  int32_t reserved;
+  double E;              /* ||X||_F^2 */
+  const double *lam_T;   /* token-mode eigenvalues, descending (FlashJoLT: q_eff values
+                            followed by the synthetic tail) */
+  const double *lam_d;   /* d feature-mode eigenvalues, descending */
+} jolt_cell_spectrum;
+
+typedef struct {
+  double budget_bytes;
+  double eps2[4];        /* eps^2(b) for b = 0, 2, 4, 8 (eps2[0] is 1) */
+  int32_t bit_mask;      /* allowed b: bit 0 -> 0, bit 1 -> 2, bit 2 -> 4, bit 3 -> 8 */
+  int32_t step;          /* rank grid step (ranks are multiples of step) */
+  int32_t floor_rT, floor_rd, floor_bits; /* per-cell floors (0 = none) */
+  int32_t count_scale_bytes;              /* 1: add 2 bytes per quantiser group to s */
+} jolt_alloc_opts;
+
+const char *jolt_last_error(void);
+
+/* Context: device properties only.  device < 0 uses the current device. */
+int jolt_create(jolt_ctx **ctx, int device);
+int jolt_destroy(jolt_ctx *ctx);
+
+/* Section 5 "Cap selection": min(max(q_min(R), ceil(T / 32)), 512),
+ * q_min = 32 for R <= 4 else 64.  Returns q (>= 1) or JOLT_E_INVAL. */
+int jolt_q_cap(int T, double ratio);
+
+/* Length of the lam_T array jolt_spectrum returns per cell (T for the exact
+ * method, q_eff + 1 for FlashJoLT) and the largest admissible r_T. */
+int jolt_spectrum_len(const jolt_cell_desc *desc, const jolt_spectrum_opts *opts,
+                      int32_t *n_lam_T, int32_t *rT_max);
+
+/* Device workspace needed by jolt_spectrum / jolt_compress / jolt_decompress
+ * for n_cells cells of this shape (opts NULL = exact method). */
+int jolt_workspace_size(const jolt_cell_desc *desc, int n_cells, const jolt_spectrum_opts *opts,
+                        size_t *bytes);
+
+/* a2-a4: E[n_cells], lam_T[n_cells * n_lam_T], lam_d[n_cells * d] (host arrays).
+ * seeds[n_cells] seed the FlashJoLT sketch (may be NULL for JOLT_EXACT).
+ * The workspace keeps the factors; a following jolt_compress on the same cells,
+ * workspace and options reuses them. */
+int jolt_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_cells, const void *const *X,
+                  const uint64_t *seeds, const jolt_spectrum_opts *opts, void *ws, size_t ws_bytes,
+                  double *E, double *lam_T, double *lam_d, jolt_stream stream);
+
+/* Blob size for one cell: 128-byte header + sections (see the blob format in the
+ * oracle / design notes): U_T (T x r_T), U_d (d x r_d), G (m x r_T x r_d) at c bytes,
+ * m int8 core exponents, fp16 scales (m*T*d/g), packed codes (m*T*d*b/8). */
+int jolt_compressed_size(const jolt_cell_desc *desc, const jolt_params *params, size_t *bytes);
+
+/* a6-a9 for every cell: writes blob i (device memory of blob_bytes[i] bytes).
+ * opts gives the token-mode method; when the workspace holds the spectrum of the
+ * same cells from the preceding jolt_spectrum call it is reused, otherwise the
+ * spectrum is recomputed on the device. */
+int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_cells, const void *const *X,
+                  const jolt_params *params, const jolt_spectrum_opts *opts, void *ws,
+                  size_t ws_bytes, void *const *blobs, const size_t *blob_bytes,
+                  jolt_stream stream);
+
+/* a10: reconstructs every blob into Xhat[i] laid out by out_desc (its dtype is the
+ * output type: JOLT_BF16 rounds to nearest even, JOLT_F32 keeps fp32).  The blobs'
+ * shapes must equal out_desc's.  hdr_host (optional, may be NULL) is a host copy of
+ * the n_cells 128-byte headers; without it the headers are copied device->host,
+ * which synchronises the stream. */
+int jolt_decompress(jolt_ctx *ctx, int n_cells, const void *const *blobs, const size_t *blob_bytes,
+                    const void *hdr_host, const jolt_cell_desc *out_desc, void *const *Xhat,
+                    void *ws, size_t ws_bytes, jolt_stream stream);
+
+/* a5 (host only, no device work): eq. (3) through eq. (4).  Outputs per cell
+ * r_T, r_d, bits; lambda_star, total bytes and summed model error; *infeasible is
+ * 1 when even the cheapest grid point of every cell exceeds the budget (the
+ * cheapest allocation is then returned). */
+int jolt_allocate(const jolt_cell_spectrum *cells, int n_cells, const jolt_alloc_opts *opts,
+                  int32_t *r_T, int32_t *r_d, int32_t *bits, double *lambda_star,
+                  double *total_bytes, double *model_error, int32_t *infeasible);
+
+/* eq. (2) calibration: eps^2(b) for b = 0, 2, 4, 8 from a round trip of n_samples
+ * Gaussian samples (rows of d, group g, Philox seed).  n_samples must be a
+ * multiple of d.  ws: at least jolt_eps2_workspace_size bytes. */
+int jolt_eps2_workspace_size(int d, int n_samples, size_t *bytes);
+int jolt_eps2_calibrate(jolt_ctx *ctx, int group, int d, uint64_t seed, int n_samples,
+                        double eps2_out[4], void *ws, size_t ws_bytes, jolt_stream stream);
+
+/* Test hook: copies an intermediate of the most recent jolt_compress on this
+ * context for cell `cell` into dst (device memory, dst_bytes): 0 = U_T (T x r_T fp32),
+ * 1 = U_d (d x r_d fp32), 2 = X~ (m x T x d fp32 from the stored factors),
+ * 3 = FlashJoLT sketch Omega (m*d x l, bf16 bits).  Requires the workspace of that
+ * call to be untouched since. */
+int jolt_debug_export(jolt_ctx *ctx, int what, int cell, void *dst, size_t dst_bytes,
+                      jolt_stream stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* JOLT_H */

@@ -1,0 +1,144 @@
+// Joint Lagrangian allocation of Tucker ranks and residual bits (section 4,
+// eq. (1)-(4)); host only.
+//
+// Cost (eq. (1)):  s = (m r_T r_d + T r_T + d r_d) c + [b > 0] (b m T d / 8 + 2 m T d / g)
+//                  (the scale term is optional: the paper treats it as negligible).
+// Error (eq. (2)): e = eps2(b) * min(1, tau_T(r_T) + tau_d(r_d)), tau from the mode
+//                  spectra of the cell, tau(r) = (sum of eigenvalues past r) / E.
+// Problem (eq. (3)) is solved through the relaxation of eq. (4): for a fixed lambda
+// every cell independently takes the grid point minimising e + lambda s, and one
+// bisection on lambda drives the total cost to the budget.
+//
+// Determinism: grid points are ordered by (cost, bits, r_T, r_d) and the first
+// point of minimal value wins; tails are suffix sums accumulated from the smallest
+// eigenvalue upward; the bisection halves [0, 1e3] until hi - lo <= 1e-15 hi (at
+// most 200 halvings) and returns the allocation at hi.  This file is compiled
+// without floating-point contraction so the arithmetic is plain IEEE double.
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <tuple>
+#include <vector>
+
+#include "../../include/jolt.h"
+#include "host_util.h"
+
+namespace {
+
+struct Point {
+  int64_t s;
+  int32_t b, rT, rd;
+  double e;
+};
+
+std::vector<double> tail_fractions(const double *lam, int n, double E) {
+  std::vector<double> suf(n + 1, 0.0);
+  double acc = 0.0;
+  for (int i = n - 1; i >= 0; --i) {
+    acc += lam[i];
+    suf[i] = acc;
+  }
+  if (!(E > 0.0)) return std::vector<double>(n + 1, 0.0);
+  for (int i = 0; i <= n; ++i) suf[i] = suf[i] / E;
+  return suf;
+}
+
+int64_t byte_cost(int64_t m, int64_t T, int64_t d, int64_t rT, int64_t rd, int64_t b, int64_t c,
+                  int64_t g, bool scales) {
+  int64_t s = (m * rT * rd + T * rT + d * rd) * c;
+  if (b > 0) {
+    s += (b * m * T * d) / 8;
+    if (scales) s += 2 * ((m * T * d) / g);
+  }
+  return s;
+}
+
+}  // namespace
+
+extern "C" int jolt_allocate(const jolt_cell_spectrum *cells, int n_cells, const jolt_alloc_opts *o,
+                             int32_t *r_T, int32_t *r_d, int32_t *bits, double *lambda_star,
+                             double *total_bytes, double *model_error, int32_t *infeasible) {
+  if (!cells || !o || !r_T || !r_d || !bits || n_cells < 0)
+    return jolt_fail(JOLT_E_INVAL, "jolt_allocate: null argument or negative cell count");
+  if (o->step < 1) return jolt_fail(JOLT_E_INVAL, "jolt_allocate: step must be >= 1");
+  if (!(o->budget_bytes >= 0.0)) return jolt_fail(JOLT_E_INVAL, "jolt_allocate: budget must be >= 0");
+  const int bit_values[4] = {0, 2, 4, 8};
+  std::vector<std::vector<Point>> grids(n_cells);
+  for (int ci = 0; ci < n_cells; ++ci) {
+    const jolt_cell_spectrum &c = cells[ci];
+    if (c.m < 1 || c.T < 1 || c.d < 1 || (c.c != 2 && c.c != 4) || c.g < 1 || c.n_lam_T < 1 ||
+        c.rT_max < 0 || c.rT_max > c.n_lam_T || !c.lam_T || !c.lam_d)
+      return jolt_fail(JOLT_E_INVAL, "jolt_allocate: malformed cell spectrum %d", ci);
+    const std::vector<double> tT = tail_fractions(c.lam_T, c.n_lam_T, c.E);
+    const std::vector<double> td = tail_fractions(c.lam_d, c.d, c.E);
+    std::vector<Point> &pts = grids[ci];
+    for (int bi = 0; bi < 4; ++bi) {
+      if (!(o->bit_mask & (1 << bi))) continue;
+      const int b = bit_values[bi];
+      if (b < o->floor_bits) continue;
+      std::vector<int> rTs{0};
+      for (int r = o->step; r <= c.rT_max; r += o->step) rTs.push_back(r);
+      for (int rT : rTs) {
+        if (rT < o->floor_rT) continue;
+        if (rT == 0) {
+          Point p{byte_cost(c.m, c.T, c.d, 0, 0, b, c.c, c.g, o->count_scale_bytes != 0), b, 0, 0, 0.0};
+          const double tau = std::min(1.0, tT[0] + td[0]);
+          p.e = o->eps2[bi] * tau;
+          pts.push_back(p);
+          continue;
+        }
+        for (int rd = o->step; rd <= c.d; rd += o->step) {
+          if (rd < o->floor_rd) continue;
+          Point p{byte_cost(c.m, c.T, c.d, rT, rd, b, c.c, c.g, o->count_scale_bytes != 0), b, rT, rd, 0.0};
+          const double tau = std::min(1.0, tT[rT] + td[rd]);
+          p.e = o->eps2[bi] * tau;
+          pts.push_back(p);
+        }
+      }
+    }
+    if (pts.empty()) return jolt_fail(JOLT_E_INVAL, "jolt_allocate: empty grid for cell %d", ci);
+    std::sort(pts.begin(), pts.end(), [](const Point &a, const Point &b) {
+      return std::make_tuple(a.s, a.b, a.rT, a.rd) < std::make_tuple(b.s, b.b, b.rT, b.rd);
+    });
+  }
+  std::vector<int> idx(n_cells), idx_hi(n_cells);
+  auto choose = [&](double lam, std::vector<int> &out) {
+    double total = 0.0;
+    for (int ci = 0; ci < n_cells; ++ci) {
+      const std::vector<Point> &pts = grids[ci];
+      int best = 0;
+      double bv = pts[0].e + lam * (double)pts[0].s;
+      for (int k = 1; k < (int)pts.size(); ++k) {
+        const double v = pts[k].e + lam * (double)pts[k].s;
+        if (v < bv) { bv = v; best = k; }
+      }
+      out[ci] = best;
+      total += (double)pts[best].s;
+    }
+    return total;
+  };
+  auto emit = [&](const std::vector<int> &sel, double lam, int infeas) {
+    double tb = 0.0, te = 0.0;
+    for (int ci = 0; ci < n_cells; ++ci) {
+      const Point &p = grids[ci][sel[ci]];
+      r_T[ci] = p.rT; r_d[ci] = p.rd; bits[ci] = p.b;
+      tb += (double)p.s; te += p.e;
+    }
+    if (lambda_star) *lambda_star = lam;
+    if (total_bytes) *total_bytes = tb;
+    if (model_error) *model_error = te;
+    if (infeasible) *infeasible = infeas;
+    return JOLT_OK;
+  };
+  const double B = o->budget_bytes;
+  if (choose(0.0, idx) <= B) return emit(idx, 0.0, 0);
+  double lo = 0.0, hi = 1e3;
+  if (choose(hi, idx_hi) > B) return emit(idx_hi, hi, 1);
+  for (int it = 0; it < 200; ++it) {
+    if (hi - lo <= 1e-15 * hi) break;
+    const double mid = 0.5 * (lo + hi);
+    if (choose(mid, idx) <= B) { hi = mid; idx_hi = idx; }
+    else lo = mid;
+  }
+  return emit(idx_hi, hi, 0);
+}

@@ -1,0 +1,62 @@
+// Internal host-side declarations of the C-ABI implementation.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <vector>
+
+#include "../../include/jolt.h"
+#include "kernels.h"
+
+constexpr int kHeaderBytes = 128;
+
+struct SpecShape {
+  int m = 0, T = 0, d = 0, N = 0, method = 0;
+  int n_lam_T = 0, rT_max = 0, q = 0, ell = 0;
+};
+
+struct BlobLayout {
+  int64_t UT = 0, Ud = 0, G = 0, gexp = 0, scales = 0, codes = 0, total = 0;
+};
+
+struct BlobInfo {
+  uint32_t in_bf16, f16, m, T, d, rT, rd, bits, group, method, heads;
+  uint64_t seed;
+  BlobLayout L;
+};
+
+// State a jolt_compress call may reuse from the preceding jolt_spectrum call.
+struct SpecKey {
+  bool valid = false;
+  const void *ws = nullptr;
+  size_t ws_bytes = 0;
+  jolt_cell_desc desc{};
+  jolt_spectrum_opts opts{};
+  std::vector<const void *> X;
+  std::vector<uint64_t> seeds;
+};
+
+struct DebugState {
+  bool valid = false;
+  int n_cells = 0, T = 0, d = 0, m = 0, N = 0, ell = 0;
+  std::vector<int> rT, rd;
+  const float *U = nullptr, *Ud = nullptr, *Xt = nullptr;
+  const uint16_t *Omega = nullptr;
+  int64_t u_stride = 0, ldu = 0, ud_stride = 0, xt_stride = 0, om_stride = 0;
+};
+
+struct jolt_ctx {
+  int device = 0;
+  hipDeviceProp_t prop{};
+  SpecKey spec;
+  DebugState dbg;
+  std::vector<GemmProblem> tab_host;
+};
+
+int validate_desc(const jolt_cell_desc *d);
+int resolve_spectrum(const jolt_cell_desc *d, const jolt_spectrum_opts *o, SpecShape *sh);
+int validate_params(const jolt_cell_desc *d, const jolt_params *p, int rT_max);
+BlobLayout blob_layout(int64_t m, int64_t T, int64_t d, int64_t rT, int64_t rd, int64_t bits,
+                       int64_t group, int64_t fb);
+void fill_header(uint8_t *h, const jolt_cell_desc *d, const jolt_params *p, int method);
+int parse_header(const uint8_t *h, size_t blob_bytes, BlobInfo *bi);

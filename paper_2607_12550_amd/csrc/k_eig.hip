@@ -1,0 +1,415 @@
+// Batched symmetric eigensolver for the mode Gram matrices (token Gram C = X_(2) X_(2)^T,
+// feature Grams, FlashJoLT's B B^T).  Section 4 takes the token- and feature-mode
+// singular vectors of the cell; they are the eigenvectors of these Grams.
+//
+//   1. Householder tridiagonalisation A = Q T Q^T (fp32, lower reflectors,
+//      Q = H_0 H_1 ... H_{n-2}, H_i = I - tau_i v_i v_i^T, v_i(i+1) = 1).
+//   2. All eigenvalues of T by Sturm-count bisection in fp64 (one thread each).
+//   3. The top-k eigenvectors of T by inverse iteration in fp64 (one thread each,
+//      tridiagonal LU with partial pivoting), re-orthogonalised (modified
+//      Gram-Schmidt, two passes) inside clusters of nearly equal eigenvalues.
+//   4. U = Q Z applied as blocked WY reflectors (I - V T V^T) with GEMMs.
+// fp64 in steps 2-3 costs little on CDNA (full-rate fp64) and makes the
+// tridiagonal eigenvectors orthogonal to ~1e-12 even for close eigenvalues.
+#include <algorithm>
+#include <cfloat>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr int SYTD2_THREADS = 1024;
+
+JOLT_DEV double block_sum(double v, double *red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  v = wave_sum(v);
+  __syncthreads();
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  double s = 0.0;
+  for (int w = 0; w < nw; ++w) s += red[w];
+  return s;
+}
+
+// One workgroup per matrix; full symmetric storage in global memory (L2-resident for
+// the sizes this kernel serves).  Writes d, e, tau and leaves v_i in column i of A
+// (rows i+1..n-1, v_i(i+1) = 1) with zeros above, the dense form the blocked
+// back-transformation multiplies by.
+__global__ void __launch_bounds__(SYTD2_THREADS) k_sytd2(EigBatch b) {
+  const int mat = blockIdx.x, n = b.n;
+  float *A = b.A + (int64_t)mat * b.mat_stride;
+  double *dd = b.d + (int64_t)mat * n, *ee = b.e + (int64_t)mat * n;
+  float *tau = b.tau + (int64_t)mat * n;
+  extern __shared__ float sh[];
+  float *v = sh, *w = sh + n;
+  __shared__ double red[SYTD2_THREADS / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = SYTD2_THREADS / 64;
+  for (int i = 0; i < n - 1; ++i) {
+    const int L = n - 1 - i;
+    for (int t = tid; t < L; t += SYTD2_THREADS) v[t] = A[(int64_t)(i + 1 + t) * n + i];
+    __syncthreads();
+    double part = 0.0;
+    for (int t = 1 + tid; t < L; t += SYTD2_THREADS) part += (double)v[t] * (double)v[t];
+    const double sigma = block_sum(part, red);
+    const double alpha = v[0];
+    double beta, tv, scal;
+    if (sigma == 0.0) {
+      tv = 0.0; beta = alpha; scal = 0.0;
+    } else {
+      beta = -copysign(sqrt(alpha * alpha + sigma), alpha);
+      tv = (beta - alpha) / beta;
+      scal = 1.0 / (alpha - beta);
+    }
+    __syncthreads();
+    for (int t = tid; t < L; t += SYTD2_THREADS) {
+      float vt = (t == 0) ? 1.f : (float)((double)v[t] * scal);
+      if (tv == 0.0) vt = (t == 0) ? 1.f : 0.f;
+      v[t] = vt;
+      A[(int64_t)(i + 1 + t) * n + i] = vt;
+    }
+    if (tid == 0) { ee[i] = beta; tau[i] = (float)tv; }
+    __syncthreads();
+    if (tv == 0.0) continue;
+    const float tf = (float)tv;
+    // w = tau * A22 v  (one wavefront per row, lanes along the row)
+    for (int r = wave; r < L; r += nw) {
+      const float *row = A + (int64_t)(i + 1 + r) * n + (i + 1);
+      float s = 0.f;
+      for (int c = lane; c < L; c += 64) s = fmaf(row[c], v[c], s);
+      s = wave_sum(s);
+      if (lane == 0) w[r] = tf * s;
+    }
+    __syncthreads();
+    part = 0.0;
+    for (int t = tid; t < L; t += SYTD2_THREADS) part += (double)w[t] * (double)v[t];
+    const float K = (float)(-0.5 * tv * block_sum(part, red));
+    for (int t = tid; t < L; t += SYTD2_THREADS) w[t] = fmaf(K, v[t], w[t]);
+    __syncthreads();
+    // A22 -= v w^T + w v^T
+    for (int r = wave; r < L; r += nw) {
+      float *row = A + (int64_t)(i + 1 + r) * n + (i + 1);
+      const float vr = v[r], wr = w[r];
+      for (int c = lane; c < L; c += 64) row[c] -= vr * w[c] + wr * v[c];
+    }
+    __syncthreads();
+  }
+  // diagonal of T, then zero the strictly upper part and diagonal of the reflector block
+  for (int i = tid; i < n; i += SYTD2_THREADS) dd[i] = A[(int64_t)i * n + i];
+  if (tid == 0) { ee[n - 1] = 0.0; tau[n - 1] = 0.f; }
+  __syncthreads();
+  for (int r = wave; r < n; r += nw) {
+    float *row = A + (int64_t)r * n;
+    for (int c = lane; c < n; c += 64)
+      if (c >= r || c == n - 1) row[c] = 0.f;
+  }
+  if (n == 1 && tid == 0) A[0] = 0.f;
+}
+
+JOLT_DEV int sturm_count(const double *d, const double *e, int n, double x, double pivmin) {
+  double q = d[0] - x;
+  if (fabs(q) <= pivmin) q = -pivmin;
+  int cnt = q < 0.0;
+  for (int j = 1; j < n; ++j) {
+    const double ej = e[j - 1];
+    q = d[j] - x - ej * ej / q;
+    if (fabs(q) <= pivmin) q = -pivmin;
+    cnt += q < 0.0;
+  }
+  return cnt;
+}
+
+JOLT_DEV void gershgorin(const double *d, const double *e, int n, double &gl, double &gu,
+                         double &pivmin) {
+  gl = DBL_MAX; gu = -DBL_MAX;
+  double emax2 = 0.0;
+  for (int i = 0; i < n; ++i) {
+    const double r = (i > 0 ? fabs(e[i - 1]) : 0.0) + (i < n - 1 ? fabs(e[i]) : 0.0);
+    gl = fmin(gl, d[i] - r);
+    gu = fmax(gu, d[i] + r);
+    if (i < n - 1) emax2 = fmax(emax2, e[i] * e[i]);
+  }
+  pivmin = DBL_MIN * fmax(1.0, emax2);
+  const double tnorm = fmax(fabs(gl), fabs(gu));
+  gl -= 2.0 * DBL_EPSILON * tnorm + 2.0 * pivmin;
+  gu += 2.0 * DBL_EPSILON * tnorm + 2.0 * pivmin;
+}
+
+__global__ void k_tri_eigvals(EigBatch b) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int n = b.n;
+  if (idx >= (int64_t)b.n_mat * n) return;
+  const int mat = (int)(idx / n), k = (int)(idx % n);
+  const double *d = b.d + (int64_t)mat * n, *e = b.e + (int64_t)mat * n;
+  double lo, hi, pivmin;
+  gershgorin(d, e, n, lo, hi, pivmin);
+  for (int it = 0; it < 200; ++it) {
+    const double mid = 0.5 * (lo + hi);
+    if (hi - lo <= 2.0 * DBL_EPSILON * fmax(fabs(lo), fabs(hi)) + 4.0 * pivmin || mid == lo || mid == hi)
+      break;
+    if (sturm_count(d, e, n, mid, pivmin) > k) hi = mid; else lo = mid;
+  }
+  b.lam[(int64_t)mat * n + (n - 1 - k)] = 0.5 * (lo + hi);
+}
+
+// inverse iteration on (T - lam I) with partial pivoting; per-thread vectors are laid
+// out [array][i][column] so neighbouring threads touch neighbouring addresses.
+__global__ void k_tri_eigvecs(EigBatch b, InvitWork w, int j0) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int n = b.n;
+  if (idx >= (int64_t)b.n_mat * w.ldlu) return;
+  const int mat = (int)(idx / w.ldlu), jj = (int)(idx % w.ldlu), j = j0 + jj;
+  if (j >= w.k[mat]) return;
+  const double *d = b.d + (int64_t)mat * n, *e = b.e + (int64_t)mat * n;
+  const double lam = b.lam[(int64_t)mat * n + j];
+  const int64_t ld = w.ldz;
+  double *x = w.Z + (int64_t)mat * n * ld + j;
+  const int64_t ll = w.ldlu;
+  double *u0 = w.lu + ((int64_t)mat * 3 + 0) * n * ll + jj;
+  double *u1 = w.lu + ((int64_t)mat * 3 + 1) * n * ll + jj;
+  double *u2 = w.lu + ((int64_t)mat * 3 + 2) * n * ll + jj;
+  double gl, gu, pivmin;
+  gershgorin(d, e, n, gl, gu, pivmin);
+  const double tnorm = fmax(fmax(fabs(gl), fabs(gu)), DBL_MIN);
+  const double tiny = DBL_EPSILON * tnorm;
+  // deterministic start vector in [-1, 1]
+  for (int i = 0; i < n; ++i) {
+    u32x4 r = philox4x32_10(u32x4{(uint32_t)i, (uint32_t)j, (uint32_t)mat, 4u}, 0x6a6f6c74u, 0u);
+    x[(int64_t)i * ld] = ((double)r.x + 0.5) * 0x1p-31 - 1.0;
+  }
+  for (int it = 0; it < 3; ++it) {
+    // forward: factor T - lam I = P L U while transforming the right-hand side in x
+    double p = d[0] - lam, q = (n > 1) ? e[0] : 0.0;
+    double y = x[0];
+    for (int i = 0; i < n - 1; ++i) {
+      const double c = e[i];                       // sub-diagonal entry of row i+1
+      const double a1 = d[i + 1] - lam;
+      const double b1 = (i + 1 < n - 1) ? e[i + 1] : 0.0;
+      double y1 = x[(int64_t)(i + 1) * ld];
+      if (fabs(p) >= fabs(c)) {
+        if (fabs(p) < tiny) p = copysign(tiny, p == 0.0 ? 1.0 : p);
+        const double l = c / p;
+        u0[(int64_t)(i) * ll] = p; u1[(int64_t)(i) * ll] = q; u2[(int64_t)(i) * ll] = 0.0;
+        x[(int64_t)i * ld] = y;
+        y = y1 - l * y;
+        p = a1 - l * q;
+        q = b1;
+      } else {
+        const double l = p / c;
+        u0[(int64_t)(i) * ll] = c; u1[(int64_t)(i) * ll] = a1; u2[(int64_t)(i) * ll] = b1;
+        x[(int64_t)i * ld] = y1;
+        const double ynew = y - l * y1;
+        const double pnew = q - l * a1;
+        q = -l * b1;
+        p = pnew;
+        y = ynew;
+      }
+    }
+    if (fabs(p) < tiny) p = copysign(tiny, p == 0.0 ? 1.0 : p);
+    u0[(int64_t)(n - 1) * ll] = p;
+    x[(int64_t)(n - 1) * ld] = y;
+    // back substitution
+    double xn1 = x[(int64_t)(n - 1) * ld] / p, xn2 = 0.0;
+    x[(int64_t)(n - 1) * ld] = xn1;
+    double amax = fabs(xn1);
+    for (int i = n - 2; i >= 0; --i) {
+      const double xi = (x[(int64_t)i * ld] - u1[(int64_t)(i) * ll] * xn1 - u2[(int64_t)(i) * ll] * xn2) /
+                        u0[(int64_t)(i) * ll];
+      x[(int64_t)i * ld] = xi;
+      xn2 = xn1; xn1 = xi;
+      amax = fmax(amax, fabs(xi));
+    }
+    const double s = amax > 0.0 ? 1.0 / amax : 1.0;
+    for (int i = 0; i < n; ++i) x[(int64_t)i * ld] *= s;
+  }
+  double nrm = 0.0;
+  for (int i = 0; i < n; ++i) nrm += x[(int64_t)i * ld] * x[(int64_t)i * ld];
+  nrm = nrm > 0.0 ? 1.0 / sqrt(nrm) : 0.0;
+  for (int i = 0; i < n; ++i) x[(int64_t)i * ld] *= nrm;
+}
+
+// Modified Gram-Schmidt (two passes) over each cluster of eigenvalues whose
+// consecutive gaps are below tol * ||T||; one workgroup per cluster start.
+__global__ void __launch_bounds__(256) k_cluster_mgs(EigBatch b, InvitWork w, int kmax, double rtol) {
+  const int mat = blockIdx.y, j0 = blockIdx.x, n = b.n;
+  const int k = w.k[mat];
+  if (j0 >= k) return;
+  const double *lam = b.lam + (int64_t)mat * n;
+  const double scale = fmax(fabs(lam[0]), fabs(lam[n - 1]));
+  const double tol = rtol * scale;
+  auto close = [&](int a) { return lam[a] - lam[a + 1] <= tol; };   // a, a+1 in cluster
+  if (j0 > 0 && close(j0 - 1)) return;            // not a cluster start
+  int j1 = j0;
+  while (j1 + 1 < k && close(j1)) ++j1;
+  if (j1 == j0) return;
+  __shared__ double red[4];
+  const int64_t ld = w.ldz;
+  double *Z = w.Z + (int64_t)mat * n * ld;
+  for (int c = j0; c <= j1; ++c) {
+    for (int pass = 0; pass < 2; ++pass) {
+      for (int p = j0; p < c; ++p) {
+        double part = 0.0;
+        for (int i = threadIdx.x; i < n; i += 256) part += Z[(int64_t)i * ld + p] * Z[(int64_t)i * ld + c];
+        const double dot = block_sum(part, red);
+        for (int i = threadIdx.x; i < n; i += 256) Z[(int64_t)i * ld + c] -= dot * Z[(int64_t)i * ld + p];
+        __syncthreads();
+      }
+    }
+    double part = 0.0;
+    for (int i = threadIdx.x; i < n; i += 256) part += Z[(int64_t)i * ld + c] * Z[(int64_t)i * ld + c];
+    const double nr = block_sum(part, red);
+    const double s = nr > 0.0 ? 1.0 / sqrt(nr) : 0.0;
+    for (int i = threadIdx.x; i < n; i += 256) Z[(int64_t)i * ld + c] *= s;
+    __syncthreads();
+  }
+}
+
+__global__ void k_z_to_f32(EigBatch b, InvitWork w, int kmax, float *U, int64_t ldu, int64_t u_stride) {
+  const int mat = blockIdx.y;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int n = b.n;
+  if (idx >= (int64_t)n * kmax) return;
+  const int i = (int)(idx / kmax), j = (int)(idx % kmax);
+  const int k = w.k[mat];
+  float v = 0.f;
+  if (j < k) v = (float)w.Z[(int64_t)mat * n * w.ldz + (int64_t)i * w.ldz + j];
+  if (j < ldu) U[(int64_t)mat * u_stride + (int64_t)i * ldu + j] = v;
+}
+
+// T factor of the block reflector of panel p (columns i0 .. i0+pw-1 of A):
+// H_i0 ... H_{i0+pw-1} = I - V T V^T with T upper triangular, built by the forward
+// recurrence T[0:j, j] = -tau_j T[0:j, 0:j] (V^T V)[0:j, j] from the precomputed Gram S.
+constexpr int NB = 64;
+__global__ void __launch_bounds__(64) k_larft(EigBatch b, const float *S_all, float *Tout) {
+  const int mat = blockIdx.y, p = blockIdx.x, n = b.n;
+  const int panels = (n + NB - 1) / NB;
+  const int i0 = p * NB;
+  const int pw = min(NB, n - 1 - i0);
+  const float *tau = b.tau + (int64_t)mat * n;
+  const float *S = S_all + ((int64_t)mat * panels + p) * NB * NB;
+  __shared__ float T[NB][NB + 1];
+  const int a = threadIdx.x;
+  for (int c = 0; c < NB; ++c) T[a][c] = 0.f;
+  __syncthreads();
+  for (int j = 0; j < pw; ++j) {
+    const float tj = tau[i0 + j];
+    float s = 0.f;
+    if (a < j)
+      for (int c = a; c < j; ++c) s = fmaf(T[a][c], S[c * NB + j], s);
+    __syncthreads();
+    if (a < j) T[a][j] = -tj * s;
+    if (a == j) T[j][j] = tj;
+    __syncthreads();
+  }
+  float *To = Tout + ((int64_t)mat * panels + p) * NB * NB;
+  for (int c = 0; c < NB; ++c) To[a * NB + c] = T[a][c];
+}
+
+}  // namespace
+
+hipError_t launch_sytrd_small(const EigBatch &b, hipStream_t st) {
+  size_t shm = (size_t)2 * b.n * sizeof(float);
+  hipLaunchKernelGGL(k_sytd2, dim3(b.n_mat), dim3(SYTD2_THREADS), shm, st, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_tridiag_eigvals(const EigBatch &b, hipStream_t st) {
+  int64_t total = (int64_t)b.n_mat * b.n;
+  hipLaunchKernelGGL(k_tri_eigvals, dim3((unsigned)((total + 127) / 128)), dim3(128), 0, st, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_tridiag_eigvecs(const EigBatch &b, const InvitWork &w, int kmax, hipStream_t st) {
+  if (kmax <= 0) return hipSuccess;
+  const int64_t total = (int64_t)b.n_mat * w.ldlu;
+  hipError_t err = hipSuccess;
+  for (int j0 = 0; j0 < kmax; j0 += w.ldlu) {
+    hipLaunchKernelGGL(k_tri_eigvecs, dim3((unsigned)((total + 63) / 64)), dim3(64), 0, st, b, w, j0);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
+  hipLaunchKernelGGL(k_cluster_mgs, dim3(kmax, b.n_mat), dim3(256), 0, st, b, w, kmax, 1e-10);
+  return hipGetLastError();
+}
+
+int backtransform_nb() { return NB; }
+
+size_t backtransform_scratch_floats(int n_mat, int n, int kmax) {
+  const size_t panels = (n + NB - 1) / NB;
+  return 2 * (size_t)n_mat * panels * NB * NB        // S = V^T V and T per panel
+         + 2 * (size_t)n_mat * NB * kmax;             // W1, W2
+}
+
+size_t backtransform_table_entries(int n_mat, int n) {
+  const size_t panels = (n + NB - 1) / NB;
+  return 4 * panels * (size_t)n_mat;
+}
+
+hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax, float *U,
+                                int64_t ldu, int64_t u_stride, float *scratch, GemmProblem *tab_dev,
+                                GemmProblem *tab_host, hipStream_t st) {
+  const int n = b.n, panels = (n + NB - 1) / NB, nm = b.n_mat;
+  {
+    dim3 g((unsigned)(((int64_t)n * kmax + 255) / 256), nm);
+    hipLaunchKernelGGL(k_z_to_f32, g, dim3(256), 0, st, b, w, kmax, U, ldu, u_stride);
+  }
+  float *Sf = scratch;
+  float *Tf = Sf + (size_t)nm * panels * NB * NB;
+  float *W1 = Tf + (size_t)nm * panels * NB * NB;
+  float *W2 = W1 + (size_t)nm * NB * kmax;
+  // table layout: [S problems: panel-major x mat] then per panel [W1 | W2 | U] x mat
+  GemmProblem *gS = tab_host;
+  for (int p = 0; p < panels; ++p) {
+    const int i0 = p * NB, pw = std::min(NB, n - 1 - i0), rows = n - (i0 + 1);
+    for (int m = 0; m < nm; ++m) {
+      const float *A = b.A + (int64_t)m * b.mat_stride;
+      GemmProblem S{};
+      S.A = GemmOperand{A + (int64_t)(i0 + 1) * n + i0, n, 0, 0, 0, 1};
+      S.B = GemmOperand{A + (int64_t)(i0 + 1) * n + i0, n, 0, 0, 0, 1};
+      S.C = Sf + ((size_t)m * panels + p) * NB * NB; S.ldc = NB;
+      S.M = std::max(pw, 0); S.N = std::max(pw, 0); S.K = rows; S.alpha = 1.f; S.beta = 0.f;
+      gS[(size_t)p * nm + m] = S;
+      GemmProblem *g = tab_host + (size_t)panels * nm + (size_t)p * 3 * nm;
+      GemmProblem P{};
+      P.A = GemmOperand{A + (int64_t)(i0 + 1) * n + i0, n, 0, 0, 0, 1};
+      P.B = GemmOperand{U + (int64_t)m * u_stride + (int64_t)(i0 + 1) * ldu, ldu, 0, 0, 0, 1};
+      P.C = W1 + (size_t)m * NB * kmax; P.ldc = kmax;
+      P.M = pw; P.N = kmax; P.K = rows; P.alpha = 1.f; P.beta = 0.f;
+      g[m] = P;
+      GemmProblem Q{};
+      Q.A = GemmOperand{Tf + ((size_t)m * panels + p) * NB * NB, NB, 0, 0, 0, 1};
+      Q.B = GemmOperand{W1 + (size_t)m * NB * kmax, kmax, 0, 0, 0, 1};
+      Q.C = W2 + (size_t)m * NB * kmax; Q.ldc = kmax;
+      Q.M = pw; Q.N = kmax; Q.K = pw; Q.alpha = 1.f; Q.beta = 0.f;
+      g[nm + m] = Q;
+      GemmProblem R{};
+      R.A = GemmOperand{A + (int64_t)(i0 + 1) * n + i0, n, 0, 0, 0, 1};
+      R.B = GemmOperand{W2 + (size_t)m * NB * kmax, kmax, 0, 0, 0, 1};
+      R.C = U + (int64_t)m * u_stride + (int64_t)(i0 + 1) * ldu; R.ldc = ldu;
+      R.M = rows; R.N = kmax; R.K = pw; R.alpha = -1.f; R.beta = 1.f;
+      g[2 * nm + m] = R;
+    }
+  }
+  hipError_t err = hipMemcpyAsync(tab_dev, tab_host, sizeof(GemmProblem) * 4 * nm * panels,
+                                  hipMemcpyHostToDevice, st);
+  if (err != hipSuccess) return err;
+  // S = V^T V for every (matrix, panel): A = V^T is m-contiguous, B = V is n-contiguous
+  err = launch_gemm(tab_dev, nm * panels, NB, NB, 1, GT_F32, GT_F32, false, false, st);
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(k_larft, dim3(panels, nm), dim3(64), 0, st, b, Sf, Tf);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  for (int p = panels - 1; p >= 0; --p) {
+    const int i0 = p * NB, pw = std::min(NB, n - 1 - i0);
+    if (pw <= 0) continue;
+    const int rows = n - (i0 + 1);
+    GemmProblem *g = tab_dev + (size_t)panels * nm + (size_t)p * 3 * nm;
+    err = launch_gemm(g, nm, pw, kmax, 1, GT_F32, GT_F32, false, false, st);
+    if (err != hipSuccess) return err;
+    err = launch_gemm(g + nm, nm, pw, kmax, 1, GT_F32, GT_F32, true, false, st);
+    if (err != hipSuccess) return err;
+    err = launch_gemm(g + 2 * nm, nm, rows, kmax, 1, GT_F32, GT_F32, true, false, st);
+    if (err != hipSuccess) return err;
+  }
+  return hipSuccess;
+}

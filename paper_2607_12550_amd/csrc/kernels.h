@@ -1,0 +1,173 @@
+// Launch interface of the gfx950 kernels (host side).  Each launcher queues work on
+// the given stream and returns the launch status; argument validation is the
+// caller's job (the C-ABI layer checks every shape before calling in here).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+// ----------------------------------------------------------------- residual / decode
+struct ResidCell {
+  const void *x;        // cell base pointer (bf16 or fp32)
+  const float *xt;      // X~ (m x T x d fp32, contiguous) or null (no backbone)
+  uint16_t *scales;     // fp16 bits, one per group
+  uint8_t *codes;       // packed codes
+  int32_t bits;
+  int32_t pad;
+};
+
+struct ResidArgs {
+  const ResidCell *cells;   // device array [n_cells]
+  const float *signs;       // device [n_cells][d]
+  int32_t n_cells, m, T, heads, group;
+  int64_t s_layer, s_head, s_tok;
+  float inv_sqrt_d;
+};
+
+struct DecodeCell {
+  const uint8_t *codes;
+  const uint16_t *scales;
+  const float *xt;          // X~ or null
+  void *out;                // output cell base (bf16 or fp32)
+  int32_t bits;
+  int32_t pad;
+};
+
+struct DecodeArgs {
+  const DecodeCell *cells;
+  const float *signs;
+  int32_t n_cells, m, T, heads, group;
+  int64_t s_layer, s_head, s_tok;
+  float inv_sqrt_d;
+};
+
+struct Eps2Args {
+  uint64_t seed;
+  int64_t n_samples;
+  int32_t group;
+  float inv_sqrt_d;
+  double *partials;         // [blocks][4]
+};
+
+hipError_t launch_residual_quant(const ResidArgs &a, int d, int in_dtype, hipStream_t st);
+hipError_t launch_decode(const DecodeArgs &a, int d, int out_dtype, hipStream_t st);
+hipError_t launch_rotation_signs(const uint64_t *seeds_dev, int n_cells, int d, float *signs,
+                                 hipStream_t st);
+int eps2_blocks();
+hipError_t launch_eps2_partial(const Eps2Args &a, int d, hipStream_t st);
+
+// ----------------------------------------------------------------- generic MFMA GEMM
+// C[b] = alpha * op(A[b]) op(B[b]) + beta * C[b] for a table of problems b.
+// An operand is a 2-D view with element (row, col) at
+//   ptr + seg_off(col / seg_len) + row * ld + (col % seg_len)
+// where seg_off(s) = (s / seg_heads) * seg_hi + (s % seg_heads) * seg_lo (no segmentation
+// when seg_len = 0).  A is M x K: "k-contiguous" (row = m, col = k) or
+// "m-contiguous" (row = k, col = m).  B is K x N: "k-contiguous" (row = n, col = k)
+// or "n-contiguous" (row = k, col = n).
+enum GemmType { GT_BF16 = 0, GT_F16 = 1, GT_F32 = 2, GT_F64 = 3 };
+
+struct GemmOperand {
+  const void *ptr;
+  int64_t ld;
+  int64_t seg_hi, seg_lo;
+  int32_t seg_len, seg_heads;
+};
+
+struct GemmProblem {
+  GemmOperand A, B;
+  float *C;              // fp32 output (row-major M x N with ldc)
+  int64_t ldc;
+  int32_t M, N, K;
+  float alpha, beta;
+  int32_t lower_only;    // compute only tiles with tile_m >= tile_n (symmetric outputs)
+  int32_t pad;
+  const int8_t *alpha_exp2;  // optional: alpha is multiplied by 2^(*alpha_exp2)
+};
+
+// mode: 0 = bf16 x bf16 inputs on bf16 MFMA; 1 = fp32 MFMA with A/B of types ta/tb
+// converted exactly to fp32 (bf16, fp16 or fp32 inputs).
+hipError_t launch_gemm(const GemmProblem *probs_dev, int n_probs, int max_M, int max_N,
+                       int mode, int ta, int tb, bool a_kcontig, bool b_kcontig, hipStream_t st);
+
+// ----------------------------------------------------------------- feature Gram / energy
+// F[cell] = sum over rows of x^T x for the row set {(s, r) : s < nseg, r < rows_per_seg}
+// with row (s, r) at base + seg_off(s) + r * row_stride; also sum x^2 (fp64) and a
+// non-finite flag.  Partials are reduced by launch_feature_gram_reduce.
+struct FGramCell {
+  const void *base;
+  int32_t rows_per_seg;     // rows of each segment for this cell
+  int32_t pad;
+};
+struct FGramArgs {
+  const FGramCell *cells;
+  int32_t n_cells, nseg, seg_heads;
+  int64_t seg_hi, seg_lo, row_stride;
+  int32_t chunks_per_cell;  // work items per cell (each a contiguous run of rows)
+  float *partial_F;         // [n_cells][chunks][d][d]
+  double *partial_E;        // [n_cells][chunks]
+  int32_t *nonfinite;       // [n_cells]
+};
+hipError_t launch_feature_gram(const FGramArgs &a, int d, int dtype, hipStream_t st);
+// F_out[cell] (fp32, d x d) and E_out[cell] (fp64) from the partials
+hipError_t launch_feature_gram_reduce(const FGramArgs &a, int d, float *F_out, double *E_out,
+                                      hipStream_t st);
+
+// ----------------------------------------------------------------- eigensolver
+struct EigBatch {
+  float *A;              // [n_mat][n][n] row-major; lower triangle read, overwritten with
+                         // the Householder vectors
+  int64_t mat_stride;    // elements between matrices
+  int32_t n_mat, n;
+  double *d, *e;         // tridiagonal [n_mat][n]
+  float *tau;            // [n_mat][n]
+  double *lam;           // eigenvalues, descending [n_mat][n]
+};
+// Householder tridiagonalisation (lower): small n in one workgroup per matrix.
+hipError_t launch_sytrd_small(const EigBatch &b, hipStream_t st);
+// all eigenvalues of the tridiagonal (fp64 bisection), descending
+hipError_t launch_tridiag_eigvals(const EigBatch &b, hipStream_t st);
+// top-k eigenvectors of the tridiagonal by fp64 inverse iteration, orthogonalised
+// within clusters; Z [n_mat][n][kmax] fp64 row-major (ldz = kmax); k per matrix.
+struct InvitWork {
+  double *Z;             // [n_mat][n][ldz]
+  double *lu;            // scratch [n_mat][3][n][ldlu], columns processed ldlu at a time
+  int32_t ldz, ldlu;
+  const int32_t *k;      // device [n_mat] vectors wanted per matrix
+};
+hipError_t launch_tridiag_eigvecs(const EigBatch &b, const InvitWork &w, int kmax,
+                                  hipStream_t st);
+// U = Q Z for the Householder vectors stored in A (Q = H_0 ... H_{n-2}), blocked into
+// panels of backtransform_nb() reflectors applied as I - V T V^T with GEMMs.  U fp32
+// [n_mat] x (n x ldu) at u_stride, first k[mat] columns written.  Needs
+// backtransform_scratch_floats() device floats and backtransform_table_entries()
+// GemmProblem slots on device (tab_dev) and host (tab_host).
+int backtransform_nb();
+size_t backtransform_scratch_floats(int n_mat, int n, int kmax);
+size_t backtransform_table_entries(int n_mat, int n);
+hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax, float *U,
+                                int64_t ldu, int64_t u_stride, float *scratch, GemmProblem *tab_dev,
+                                GemmProblem *tab_host, hipStream_t st);
+
+// ----------------------------------------------------------------- serialisation
+struct SerCell {
+  const float *G;          // core, slice s at G + s * g_slice_stride, row r at + r * g_ld
+  int64_t g_slice_stride, g_ld;
+  void *G_out;             // blob core section (m x r_T x r_d, fp16 or fp32)
+  int8_t *gexp;            // blob exponent section (m)
+  int32_t r_T, r_d, f16, pad;
+};
+struct SerCore {
+  const SerCell *cells;
+  int32_t m;
+};
+hipError_t launch_core_pack(const SerCore &a, int n_cells, hipStream_t st);
+
+struct SerFactorCell {
+  const float *src;
+  int64_t ld;
+  void *dst;
+  int32_t rows, cols, f16, pad;
+};
+struct SerFactor {
+  const SerFactorCell *cells;
+};
+hipError_t launch_factor_pack(const SerFactor &a, int n_cells, int64_t max_elems, hipStream_t st);

@@ -1,0 +1,744 @@
+// Orchestration of the compression path on the device: workspace layout, the
+// spectral stage (section 4 partial Tucker spectra; section 5 FlashJoLT), the codec
+// stage (ST-HOSVD truncation, fp16 serialisation, closed-loop residual, rotation,
+// quantisation) and the decoder.  All cells of a call share one shape and are
+// batched into the same kernel launches.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "host_util.h"
+#include "jolt_internal.h"
+
+namespace {
+
+constexpr int KC = 256;   // inverse-iteration columns per launch (bounds its scratch)
+
+struct Carver {
+  uint8_t *base;
+  size_t off = 0;
+  explicit Carver(void *b) : base(static_cast<uint8_t *>(b)) {}
+  template <class T>
+  T *take(size_t n) {
+    off = (off + 255) / 256 * 256;
+    T *p = base ? reinterpret_cast<T *>(base + off) : nullptr;
+    off += n * sizeof(T);
+    return p;
+  }
+};
+
+struct EigWs {
+  EigBatch b{};
+  double *Z = nullptr, *lu = nullptr;
+  int32_t *k = nullptr;
+  float *bt = nullptr;
+  int kmax = 0;
+};
+
+struct Ws {
+  // tables
+  GemmProblem *tab = nullptr;
+  size_t tab_n = 0;
+  ResidCell *rcell = nullptr;
+  DecodeCell *dcell = nullptr;
+  FGramCell *fcell = nullptr;
+  SerCell *scell = nullptr;
+  SerFactorCell *sfcell = nullptr;
+  uint64_t *seeds = nullptr;
+  int32_t *nonfinite = nullptr;
+  float *signs = nullptr;
+  // feature Gram
+  int chunks = 1;
+  float *fpart = nullptr, *F = nullptr;
+  double *epart = nullptr, *E = nullptr;
+  EigWs feig;          // feature Gram of X (eigenvalues) and of Y (eigenvectors)
+  float *Ud = nullptr;
+  // token
+  float *C = nullptr;  // exact: token Gram, flash: B B^T
+  EigWs teig;
+  float *U = nullptr;  // token factor, T x kmaxT per cell
+  int kmaxT = 0;
+  // ST-HOSVD / reconstruction
+  float *Y = nullptr, *G = nullptr, *W = nullptr, *Xt = nullptr;
+  // FlashJoLT
+  uint16_t *Om = nullptr;
+  float *Ysk = nullptr, *Zsk = nullptr, *Bsk = nullptr;
+  double *gram64 = nullptr;
+  float *Rinv = nullptr;
+  // eps2
+  double *eps_part = nullptr;
+};
+
+size_t eig_bt_floats(int nmat, int n, int kmax) { return backtransform_scratch_floats(nmat, n, kmax); }
+
+void carve_eig(Carver &cv, EigWs &e, int nmat, int n, int kmax, float *A) {
+  e.b.A = A;
+  e.b.mat_stride = (int64_t)n * n;
+  e.b.n_mat = nmat;
+  e.b.n = n;
+  e.b.d = cv.take<double>((size_t)nmat * n);
+  e.b.e = cv.take<double>((size_t)nmat * n);
+  e.b.lam = cv.take<double>((size_t)nmat * n);
+  e.b.tau = cv.take<float>((size_t)nmat * n);
+  e.kmax = kmax;
+  e.k = cv.take<int32_t>(nmat);
+  if (kmax > 0) {
+    e.Z = cv.take<double>((size_t)nmat * n * kmax);
+    e.lu = cv.take<double>((size_t)nmat * 3 * n * std::min(kmax, KC));
+    e.bt = cv.take<float>(eig_bt_floats(nmat, n, kmax));
+  }
+}
+
+void plan(Carver &cv, Ws &w, const SpecShape &sh, int nc) {
+  const int m = sh.m, T = sh.T, d = sh.d, N = sh.N;
+  const int nmax = std::max({T, d, sh.ell});
+  w.tab_n = 8192 + backtransform_table_entries(nc, nmax) + 4 * (size_t)nc * m;
+  w.tab = cv.take<GemmProblem>(w.tab_n);
+  w.rcell = cv.take<ResidCell>(nc);
+  w.dcell = cv.take<DecodeCell>(nc);
+  w.fcell = cv.take<FGramCell>(nc);
+  w.scell = cv.take<SerCell>(nc);
+  w.sfcell = cv.take<SerFactorCell>(2 * nc);
+  w.seeds = cv.take<uint64_t>(nc);
+  w.nonfinite = cv.take<int32_t>(nc);
+  w.signs = cv.take<float>((size_t)nc * d);
+  w.chunks = (int)std::min<int64_t>(64, std::max<int64_t>(1, (int64_t)m * T / 2048));
+  w.fpart = cv.take<float>((size_t)nc * w.chunks * d * d);
+  w.epart = cv.take<double>((size_t)nc * w.chunks);
+  w.F = cv.take<float>((size_t)nc * d * d);
+  w.E = cv.take<double>(nc);
+  carve_eig(cv, w.feig, nc, d, d, w.F);
+  w.Ud = cv.take<float>((size_t)nc * d * d);
+  w.kmaxT = sh.rT_max;
+  if (sh.method == JOLT_EXACT) {
+    w.C = cv.take<float>((size_t)nc * T * T);
+    carve_eig(cv, w.teig, nc, T, w.kmaxT, w.C);
+  } else {
+    const int l = sh.ell;
+    w.C = cv.take<float>((size_t)nc * l * l);
+    carve_eig(cv, w.teig, nc, l, sh.q, w.C);
+    w.Om = cv.take<uint16_t>((size_t)nc * N * l);
+    w.Ysk = cv.take<float>((size_t)nc * T * l);
+    w.Zsk = cv.take<float>((size_t)nc * N * l);
+    w.Bsk = cv.take<float>((size_t)nc * l * N);
+    w.gram64 = cv.take<double>((size_t)nc * l * l);
+    w.Rinv = cv.take<float>((size_t)nc * l * l);
+  }
+  w.U = cv.take<float>((size_t)nc * T * std::max(w.kmaxT, 1));
+  w.Y = cv.take<float>((size_t)nc * std::max(w.kmaxT, 1) * N);
+  w.G = cv.take<float>((size_t)nc * m * std::max(w.kmaxT, 1) * d);
+  w.W = cv.take<float>((size_t)nc * m * std::max(w.kmaxT, 1) * d);
+  w.Xt = cv.take<float>((size_t)nc * m * T * d);
+}
+
+int dtype_gt(int dt) { return dt == JOLT_BF16 ? GT_BF16 : GT_F32; }
+
+GemmOperand cell_operand(const void *x, const jolt_cell_desc *d) {
+  GemmOperand o{};
+  o.ptr = x;
+  o.ld = d->stride_token;
+  o.seg_len = d->d;
+  o.seg_heads = d->n_heads;
+  o.seg_hi = d->stride_layer;
+  o.seg_lo = d->stride_head;
+  return o;
+}
+
+GemmOperand plain(const void *p, int64_t ld) {
+  GemmOperand o{};
+  o.ptr = p;
+  o.ld = ld;
+  o.seg_heads = 1;
+  return o;
+}
+
+struct Run {
+  jolt_ctx *ctx;
+  hipStream_t st;
+  Ws w;
+  size_t tab_used = 0;
+
+  // upload a problem table into the next slice of the device table area, then launch
+  int gemm(const std::vector<GemmProblem> &probs, int mode, int ta, int tb, bool ak, bool bk) {
+    if (probs.empty()) return JOLT_OK;
+    if (tab_used + probs.size() > w.tab_n)
+      return jolt_fail(JOLT_E_WORKSPACE, "GEMM problem table overflow");
+    GemmProblem *dst = w.tab + tab_used;
+    tab_used += probs.size();
+    HIP_OK(hipMemcpyAsync(dst, probs.data(), probs.size() * sizeof(GemmProblem),
+                          hipMemcpyHostToDevice, st));
+    int maxM = 0, maxN = 0;
+    for (auto &p : probs) { maxM = std::max(maxM, p.M); maxN = std::max(maxN, p.N); }
+    HIP_OK(launch_gemm(dst, (int)probs.size(), maxM, maxN, mode, ta, tb, ak, bk, st));
+    return JOLT_OK;
+  }
+
+  GemmProblem *tab_slice(size_t n) {
+    if (tab_used + n > w.tab_n) return nullptr;
+    GemmProblem *p = w.tab + tab_used;
+    tab_used += n;
+    return p;
+  }
+};
+
+// symmetric eigenvalues (all) of the n x n matrices in e.b.A
+int eig_values(Run &R, EigWs &e) {
+  HIP_OK(launch_sytrd_small(e.b, R.st));
+  HIP_OK(launch_tridiag_eigvals(e.b, R.st));
+  return JOLT_OK;
+}
+
+// top-k[mat] eigenvectors into U (fp32, n x ldu per matrix at u_stride); requires eig_values first
+int eig_vectors(Run &R, EigWs &e, const std::vector<int> &k, float *U, int64_t ldu, int64_t u_stride) {
+  int kmax = 0;
+  for (int v : k) kmax = std::max(kmax, v);
+  if (kmax == 0) return JOLT_OK;
+  if (kmax > e.kmax) return jolt_fail(JOLT_E_WORKSPACE, "eigenvector count %d exceeds workspace %d", kmax, e.kmax);
+  HIP_OK(hipMemcpyAsync(e.k, k.data(), k.size() * sizeof(int32_t), hipMemcpyHostToDevice, R.st));
+  InvitWork iw{e.Z, e.lu, kmax, std::min(kmax, KC), e.k};
+  HIP_OK(launch_tridiag_eigvecs(e.b, iw, kmax, R.st));
+  const size_t nt = backtransform_table_entries(e.b.n_mat, e.b.n);
+  GemmProblem *tab = R.tab_slice(nt);
+  if (!tab) return jolt_fail(JOLT_E_WORKSPACE, "GEMM problem table overflow");
+  R.ctx->tab_host.resize(std::max(R.ctx->tab_host.size(), nt));
+  HIP_OK(launch_backtransform(e.b, iw, kmax, U, ldu, u_stride, e.bt, tab, R.ctx->tab_host.data(), R.st));
+  return JOLT_OK;
+}
+
+int upload_seeds_and_signs(Run &R, const uint64_t *seeds, int nc, int d) {
+  HIP_OK(hipMemcpyAsync(R.w.seeds, seeds, nc * sizeof(uint64_t), hipMemcpyHostToDevice, R.st));
+  HIP_OK(launch_rotation_signs(R.w.seeds, nc, d, R.w.signs, R.st));
+  return JOLT_OK;
+}
+
+// E, feature Gram F (and its eigenvalues) of every cell
+int feature_stage(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc,
+                  const void *const *X) {
+  std::vector<FGramCell> fc(nc);
+  for (int c = 0; c < nc; ++c) fc[c] = FGramCell{X[c], sh.T, 0};
+  HIP_OK(hipMemcpyAsync(R.w.fcell, fc.data(), nc * sizeof(FGramCell), hipMemcpyHostToDevice, R.st));
+  HIP_OK(hipMemsetAsync(R.w.nonfinite, 0, nc * sizeof(int32_t), R.st));
+  FGramArgs a{};
+  a.cells = R.w.fcell;
+  a.n_cells = nc;
+  a.nseg = sh.m;
+  a.seg_heads = desc->n_heads;
+  a.seg_hi = desc->stride_layer;
+  a.seg_lo = desc->stride_head;
+  a.row_stride = desc->stride_token;
+  a.chunks_per_cell = R.w.chunks;
+  a.partial_F = R.w.fpart;
+  a.partial_E = R.w.epart;
+  a.nonfinite = R.w.nonfinite;
+  HIP_OK(launch_feature_gram(a, sh.d, desc->dtype, R.st));
+  HIP_OK(launch_feature_gram_reduce(a, sh.d, R.w.F, R.w.E, R.st));
+  return eig_values(R, R.w.feig);
+}
+
+// exact token-mode spectrum: C = X_(2) X_(2)^T, tridiagonalise, all eigenvalues
+int token_exact(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc, const void *const *X) {
+  std::vector<GemmProblem> P(nc);
+  for (int c = 0; c < nc; ++c) {
+    GemmProblem &p = P[c];
+    p = GemmProblem{};
+    p.A = cell_operand(X[c], desc);
+    p.B = cell_operand(X[c], desc);
+    p.C = R.w.C + (size_t)c * sh.T * sh.T;
+    p.ldc = sh.T;
+    p.M = sh.T; p.N = sh.T; p.K = sh.N;
+    p.alpha = 1.f; p.beta = 0.f;
+  }
+  const int mode = desc->dtype == JOLT_BF16 ? 0 : 1;
+  int rc = R.gemm(P, mode, dtype_gt(desc->dtype), dtype_gt(desc->dtype), true, true);
+  if (rc) return rc;
+  return eig_values(R, R.w.teig);
+}
+
+int spectrum_device(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc,
+                    const void *const *X, const uint64_t *seeds, const jolt_spectrum_opts *o);
+
+}  // namespace
+
+// ------------------------------------------------------------------------ sizes
+extern "C" int jolt_workspace_size(const jolt_cell_desc *desc, int n_cells,
+                                   const jolt_spectrum_opts *opts, size_t *bytes) {
+  SpecShape sh;
+  int rc = resolve_spectrum(desc, opts, &sh);
+  if (rc) return rc;
+  if (n_cells < 1 || !bytes) return jolt_fail(JOLT_E_INVAL, "jolt_workspace_size: n_cells >= 1 and bytes required");
+  Carver cv(nullptr);
+  Ws w;
+  plan(cv, w, sh, n_cells);
+  *bytes = cv.off + 256;
+  return JOLT_OK;
+}
+
+static int check_common(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_cells, const void *const *X,
+                        void *ws) {
+  if (!ctx) return jolt_fail(JOLT_E_INVAL, "ctx is null");
+  if (n_cells < 1) return jolt_fail(JOLT_E_INVAL, "n_cells must be >= 1");
+  if (!X) return jolt_fail(JOLT_E_INVAL, "X is null");
+  for (int c = 0; c < n_cells; ++c) {
+    if (!X[c]) return jolt_fail(JOLT_E_INVAL, "X[%d] is null", c);
+    if (reinterpret_cast<uintptr_t>(X[c]) & 15) return jolt_fail(JOLT_E_INVAL, "X[%d] not 16-byte aligned", c);
+  }
+  if (!ws) return jolt_fail(JOLT_E_INVAL, "workspace is null");
+  if (reinterpret_cast<uintptr_t>(ws) & 255) return jolt_fail(JOLT_E_INVAL, "workspace must be 256-byte aligned");
+  (void)desc;
+  return JOLT_OK;
+}
+
+static bool same_desc(const jolt_cell_desc &a, const jolt_cell_desc &b) {
+  return std::memcmp(&a, &b, sizeof a) == 0;
+}
+
+static bool same_opts(const jolt_spectrum_opts &a, const jolt_spectrum_opts &b) {
+  return a.method == b.method && a.q == b.q && a.ratio == b.ratio && a.oversample == b.oversample &&
+         a.power_iters == b.power_iters;
+}
+
+namespace {
+
+int spectrum_device(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc,
+                    const void *const *X, const uint64_t *seeds, const jolt_spectrum_opts *o) {
+  int rc = feature_stage(R, sh, desc, nc, X);
+  if (rc) return rc;
+  if (sh.method == JOLT_EXACT) return token_exact(R, sh, desc, nc, X);
+  (void)seeds; (void)o;
+  return jolt_fail(JOLT_E_UNSUPPORTED, "FlashJoLT path not available in this build");
+}
+
+}  // namespace
+
+extern "C" int jolt_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_cells, const void *const *X,
+                             const uint64_t *seeds, const jolt_spectrum_opts *opts, void *ws,
+                             size_t ws_bytes, double *E, double *lam_T, double *lam_d,
+                             jolt_stream stream) {
+  SpecShape sh;
+  int rc = resolve_spectrum(desc, opts, &sh);
+  if (rc) return rc;
+  rc = check_common(ctx, desc, n_cells, X, ws);
+  if (rc) return rc;
+  if (sh.method == JOLT_FLASH && !seeds) return jolt_fail(JOLT_E_INVAL, "FlashJoLT needs seeds");
+  if (!E || !lam_T || !lam_d) return jolt_fail(JOLT_E_INVAL, "output arrays are null");
+  size_t need = 0;
+  jolt_workspace_size(desc, n_cells, opts, &need);
+  if (ws_bytes < need) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  HIP_OK(hipSetDevice(ctx->device));
+  Run R{ctx, (hipStream_t)stream, {}};
+  Carver cv(ws);
+  plan(cv, R.w, sh, n_cells);
+  ctx->spec.valid = false;
+  rc = spectrum_device(R, sh, desc, n_cells, X, seeds, opts);
+  if (rc) return rc;
+  std::vector<double> lt((size_t)n_cells * sh.T), ld((size_t)n_cells * sh.d);
+  HIP_OK(hipMemcpyAsync(E, R.w.E, n_cells * sizeof(double), hipMemcpyDeviceToHost, R.st));
+  HIP_OK(hipMemcpyAsync(ld.data(), R.w.feig.b.lam, ld.size() * sizeof(double), hipMemcpyDeviceToHost, R.st));
+  if (sh.method == JOLT_EXACT)
+    HIP_OK(hipMemcpyAsync(lt.data(), R.w.teig.b.lam, lt.size() * sizeof(double), hipMemcpyDeviceToHost, R.st));
+  std::vector<int32_t> bad(n_cells);
+  HIP_OK(hipMemcpyAsync(bad.data(), R.w.nonfinite, n_cells * sizeof(int32_t), hipMemcpyDeviceToHost, R.st));
+  HIP_OK(hipStreamSynchronize(R.st));
+  for (int c = 0; c < n_cells; ++c)
+    if (bad[c]) return jolt_fail(JOLT_E_NONFINITE, "cell %d contains NaN or Inf", c);
+  // eigenvalues are clipped at 0 (the Grams are positive semi-definite)
+  for (int c = 0; c < n_cells; ++c) {
+    for (int i = 0; i < sh.d; ++i) lam_d[(size_t)c * sh.d + i] = std::max(0.0, ld[(size_t)c * sh.d + i]);
+    if (sh.method == JOLT_EXACT)
+      for (int i = 0; i < sh.T; ++i) lam_T[(size_t)c * sh.T + i] = std::max(0.0, lt[(size_t)c * sh.T + i]);
+  }
+  SpecKey &k = ctx->spec;
+  k.valid = true;
+  k.ws = ws;
+  k.ws_bytes = ws_bytes;
+  k.desc = *desc;
+  k.opts = opts ? *opts : jolt_spectrum_opts{JOLT_EXACT, 0, 0.0, 0, 0};
+  k.X.assign(X, X + n_cells);
+  k.seeds.assign(seeds ? seeds : (const uint64_t *)nullptr, seeds ? seeds + n_cells : (const uint64_t *)nullptr);
+  return JOLT_OK;
+}
+
+// ------------------------------------------------------------------------ compress
+extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_cells, const void *const *X,
+                             const jolt_params *params, const jolt_spectrum_opts *opts, void *ws,
+                             size_t ws_bytes, void *const *blobs, const size_t *blob_bytes,
+                             jolt_stream stream) {
+  SpecShape sh;
+  int rc = resolve_spectrum(desc, opts, &sh);
+  if (rc) return rc;
+  rc = check_common(ctx, desc, n_cells, X, ws);
+  if (rc) return rc;
+  if (!params || !blobs || !blob_bytes) return jolt_fail(JOLT_E_INVAL, "params/blobs are null");
+  for (int c = 0; c < n_cells; ++c) {
+    rc = validate_params(desc, &params[c], sh.rT_max);
+    if (rc) return rc;
+    if (params[c].group != params[0].group || params[c].factor_dtype != params[0].factor_dtype)
+      return jolt_fail(JOLT_E_INVAL, "group and factor_dtype must be equal across the cells of a call");
+    size_t need = 0;
+    jolt_compressed_size(desc, &params[c], &need);
+    if (!blobs[c] || blob_bytes[c] < need)
+      return jolt_fail(JOLT_E_WORKSPACE, "blob %d: %zu bytes < %zu", c, blob_bytes[c], need);
+    if (reinterpret_cast<uintptr_t>(blobs[c]) & 255) return jolt_fail(JOLT_E_INVAL, "blob %d not 256-byte aligned", c);
+  }
+  size_t need = 0;
+  jolt_workspace_size(desc, n_cells, opts, &need);
+  if (ws_bytes < need) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  HIP_OK(hipSetDevice(ctx->device));
+  Run R{ctx, (hipStream_t)stream, {}};
+  Carver cv(ws);
+  plan(cv, R.w, sh, n_cells);
+  const int m = sh.m, T = sh.T, d = sh.d, N = sh.N, nc = n_cells;
+  std::vector<uint64_t> seeds(nc);
+  for (int c = 0; c < nc; ++c) seeds[c] = params[c].seed;
+  // reuse the spectrum of the preceding call when it covers exactly these cells
+  const SpecKey &k = ctx->spec;
+  jolt_spectrum_opts o = opts ? *opts : jolt_spectrum_opts{JOLT_EXACT, 0, 0.0, 0, 0};
+  bool reuse = k.valid && k.ws == ws && k.ws_bytes == ws_bytes && same_desc(k.desc, *desc) &&
+               same_opts(k.opts, o) && (int)k.X.size() == nc && std::equal(k.X.begin(), k.X.end(), X);
+  if (reuse && sh.method == JOLT_FLASH) reuse = k.seeds == seeds;
+  if (!reuse) {
+    ctx->spec.valid = false;
+    rc = spectrum_device(R, sh, desc, nc, X, seeds.data(), &o);
+    if (rc) return rc;
+  }
+  rc = upload_seeds_and_signs(R, seeds.data(), nc, d);
+  if (rc) return rc;
+  std::vector<int> rT(nc), rd(nc);
+  int kmax = 0;
+  for (int c = 0; c < nc; ++c) { rT[c] = params[c].r_T; rd[c] = params[c].r_d; kmax = std::max(kmax, rT[c]); }
+  const int64_t ldu = R.w.kmaxT, u_stride = (int64_t)T * R.w.kmaxT;
+  const int64_t y_stride = (int64_t)R.w.kmaxT * N;
+  const int64_t g_stride = (int64_t)m * R.w.kmaxT * d, g_slice = (int64_t)R.w.kmaxT * d;
+  const int64_t xt_stride = (int64_t)m * T * d;
+  const bool f16 = params[0].factor_dtype == JOLT_FACTOR_F16;
+  const int fb = f16 ? 2 : 4, ft = f16 ? GT_F16 : GT_F32;
+  std::vector<BlobLayout> L(nc);
+  for (int c = 0; c < nc; ++c) L[c] = blob_layout(m, T, d, rT[c], rd[c], params[c].bits, params[0].group, fb);
+  if (kmax > 0) {
+    // token factor U_T (top r_T eigenvectors of the token Gram)
+    if (sh.method != JOLT_EXACT) return jolt_fail(JOLT_E_UNSUPPORTED, "FlashJoLT path not available in this build");
+    rc = eig_vectors(R, R.w.teig, rT, R.w.U, ldu, u_stride);
+    if (rc) return rc;
+    // Y = U_T^T X_(2)   (r_T x N per cell)
+    std::vector<GemmProblem> P;
+    for (int c = 0; c < nc; ++c) {
+      if (!rT[c]) continue;
+      GemmProblem p{};
+      p.A = plain(R.w.U + c * u_stride, ldu);        // A(m = r, k = t) = U[t][r]: m-contiguous
+      p.B = cell_operand(X[c], desc);                // B(k = t, n = col): n-contiguous
+      p.C = R.w.Y + c * y_stride; p.ldc = N;
+      p.M = rT[c]; p.N = N; p.K = T; p.alpha = 1.f;
+      P.push_back(p);
+    }
+    rc = R.gemm(P, 1, GT_F32, dtype_gt(desc->dtype), false, false);
+    if (rc) return rc;
+    // feature factor from the Gram of Y: F_Y = sum_s Y_s^T Y_s, top r_d eigenvectors
+    std::vector<FGramCell> fc(nc);
+    for (int c = 0; c < nc; ++c) fc[c] = FGramCell{R.w.Y + c * y_stride, rT[c], 0};
+    HIP_OK(hipMemcpyAsync(R.w.fcell, fc.data(), nc * sizeof(FGramCell), hipMemcpyHostToDevice, R.st));
+    FGramArgs a{};
+    a.cells = R.w.fcell; a.n_cells = nc; a.nseg = m; a.seg_heads = 1; a.seg_hi = d; a.seg_lo = 0;
+    a.row_stride = N; a.chunks_per_cell = R.w.chunks; a.partial_F = R.w.fpart; a.partial_E = R.w.epart;
+    a.nonfinite = R.w.nonfinite;
+    HIP_OK(launch_feature_gram(a, d, JOLT_F32, R.st));
+    HIP_OK(launch_feature_gram_reduce(a, d, R.w.F, R.w.E, R.st));
+    rc = eig_values(R, R.w.feig);
+    if (rc) return rc;
+    rc = eig_vectors(R, R.w.feig, rd, R.w.Ud, d, (int64_t)d * d);
+    if (rc) return rc;
+    // core G_s = Y_s U_d   (r_T x r_d per slice)
+    P.clear();
+    for (int c = 0; c < nc; ++c) {
+      if (!rT[c]) continue;
+      for (int s = 0; s < m; ++s) {
+        GemmProblem p{};
+        p.A = plain(R.w.Y + c * y_stride + (int64_t)s * d, N);     // k-contiguous
+        p.B = plain(R.w.Ud + (int64_t)c * d * d, d);               // n-contiguous
+        p.C = R.w.G + c * g_stride + s * g_slice; p.ldc = d;
+        p.M = rT[c]; p.N = rd[c]; p.K = d; p.alpha = 1.f;
+        P.push_back(p);
+      }
+    }
+    rc = R.gemm(P, 1, GT_F32, GT_F32, true, false);
+    if (rc) return rc;
+    // serialise U_T, U_d, G (fp16 with per-slice exponents, or fp32)
+    std::vector<SerFactorCell> sf(2 * nc);
+    std::vector<SerCell> sc(nc);
+    int64_t maxel = 0;
+    for (int c = 0; c < nc; ++c) {
+      uint8_t *b = static_cast<uint8_t *>(blobs[c]);
+      sf[c] = SerFactorCell{R.w.U + c * u_stride, ldu, b + L[c].UT, T, rT[c], f16 ? 1 : 0, 0};
+      sf[nc + c] = SerFactorCell{R.w.Ud + (int64_t)c * d * d, d, b + L[c].Ud, d, rd[c], f16 ? 1 : 0, 0};
+      sc[c] = SerCell{R.w.G + c * g_stride, g_slice, d, b + L[c].G, reinterpret_cast<int8_t *>(b + L[c].gexp),
+                      rT[c], rd[c], f16 ? 1 : 0, 0};
+      maxel = std::max<int64_t>(maxel, (int64_t)T * rT[c]);
+    }
+    HIP_OK(hipMemcpyAsync(R.w.sfcell, sf.data(), sf.size() * sizeof(SerFactorCell), hipMemcpyHostToDevice, R.st));
+    HIP_OK(hipMemcpyAsync(R.w.scell, sc.data(), sc.size() * sizeof(SerCell), hipMemcpyHostToDevice, R.st));
+    HIP_OK(launch_factor_pack(SerFactor{R.w.sfcell}, 2 * nc, maxel, R.st));
+    HIP_OK(launch_core_pack(SerCore{R.w.scell, m}, nc, R.st));
+  }
+  // zero exponents of cells without a backbone (the section is still present)
+  for (int c = 0; c < nc; ++c)
+    if (!rT[c]) HIP_OK(hipMemsetAsync(static_cast<uint8_t *>(blobs[c]) + L[c].gexp, 0, m, R.st));
+  // X~ from the stored factors: W_s = 2^e_s G^_s U^_d^T, X~_s = U^_T W_s
+  if (kmax > 0) {
+    std::vector<GemmProblem> P;
+    for (int c = 0; c < nc; ++c) {
+      if (!rT[c]) continue;
+      const uint8_t *b = static_cast<const uint8_t *>(blobs[c]);
+      for (int s = 0; s < m; ++s) {
+        GemmProblem p{};
+        p.A = plain(b + L[c].G + (int64_t)s * rT[c] * rd[c] * fb, rd[c]);   // k-contiguous
+        p.B = plain(b + L[c].Ud, rd[c]);                                    // B(k=j, n=f) = Ud[f][j]
+        p.C = R.w.W + c * g_stride + s * g_slice; p.ldc = d;
+        p.M = rT[c]; p.N = d; p.K = rd[c]; p.alpha = 1.f;
+        p.alpha_exp2 = reinterpret_cast<const int8_t *>(b + L[c].gexp + s);
+        P.push_back(p);
+      }
+    }
+    rc = R.gemm(P, 1, ft, ft, true, true);
+    if (rc) return rc;
+    P.clear();
+    for (int c = 0; c < nc; ++c) {
+      if (!rT[c]) continue;
+      const uint8_t *b = static_cast<const uint8_t *>(blobs[c]);
+      for (int s = 0; s < m; ++s) {
+        GemmProblem p{};
+        p.A = plain(b + L[c].UT, rT[c]);                                    // k-contiguous
+        p.B = plain(R.w.W + c * g_stride + s * g_slice, d);                 // n-contiguous
+        p.C = R.w.Xt + c * xt_stride + (int64_t)s * T * d; p.ldc = d;
+        p.M = T; p.N = d; p.K = rT[c]; p.alpha = 1.f;
+        P.push_back(p);
+      }
+    }
+    rc = R.gemm(P, 1, ft, GT_F32, true, false);
+    if (rc) return rc;
+  }
+  // residual + rotation + quantisation + packing
+  std::vector<ResidCell> rcells(nc);
+  bool any_bits = false;
+  for (int c = 0; c < nc; ++c) {
+    uint8_t *b = static_cast<uint8_t *>(blobs[c]);
+    rcells[c] = ResidCell{X[c], rT[c] ? R.w.Xt + c * xt_stride : nullptr,
+                          reinterpret_cast<uint16_t *>(b + L[c].scales), b + L[c].codes, params[c].bits, 0};
+    any_bits |= params[c].bits != 0;
+  }
+  if (any_bits) {
+    HIP_OK(hipMemcpyAsync(R.w.rcell, rcells.data(), nc * sizeof(ResidCell), hipMemcpyHostToDevice, R.st));
+    ResidArgs ra{};
+    ra.cells = R.w.rcell; ra.signs = R.w.signs; ra.n_cells = nc; ra.m = m; ra.T = T;
+    ra.heads = desc->n_heads; ra.group = params[0].group; ra.s_layer = desc->stride_layer;
+    ra.s_head = desc->stride_head; ra.s_tok = desc->stride_token; ra.inv_sqrt_d = (float)(1.0 / std::sqrt((double)d));
+    HIP_OK(launch_residual_quant(ra, d, desc->dtype, R.st));
+  }
+  // headers
+  std::vector<uint8_t> hdr((size_t)nc * kHeaderBytes);
+  for (int c = 0; c < nc; ++c) {
+    fill_header(hdr.data() + (size_t)c * kHeaderBytes, desc, &params[c], sh.method);
+    HIP_OK(hipMemcpyAsync(blobs[c], hdr.data() + (size_t)c * kHeaderBytes, kHeaderBytes, hipMemcpyHostToDevice, R.st));
+  }
+  DebugState &dbg = ctx->dbg;
+  dbg.valid = true;
+  dbg.n_cells = nc; dbg.T = T; dbg.d = d; dbg.m = m; dbg.N = N; dbg.ell = sh.ell;
+  dbg.rT = rT; dbg.rd = rd;
+  dbg.U = R.w.U; dbg.u_stride = u_stride; dbg.ldu = ldu;
+  dbg.Ud = R.w.Ud; dbg.ud_stride = (int64_t)d * d;
+  dbg.Xt = R.w.Xt; dbg.xt_stride = xt_stride;
+  dbg.Omega = R.w.Om; dbg.om_stride = (int64_t)N * sh.ell;
+  return JOLT_OK;
+}
+
+// ------------------------------------------------------------------------ decompress
+extern "C" int jolt_decompress(jolt_ctx *ctx, int n_cells, const void *const *blobs, const size_t *blob_bytes,
+                               const void *hdr_host, const jolt_cell_desc *out, void *const *Xhat, void *ws,
+                               size_t ws_bytes, jolt_stream stream) {
+  int rc = validate_desc(out);
+  if (rc) return rc;
+  if (n_cells < 1 || !blobs || !blob_bytes || !Xhat || !ws)
+    return jolt_fail(JOLT_E_INVAL, "jolt_decompress: null argument");
+  if (reinterpret_cast<uintptr_t>(ws) & 255) return jolt_fail(JOLT_E_INVAL, "workspace must be 256-byte aligned");
+  hipStream_t st = (hipStream_t)stream;
+  std::vector<uint8_t> hdr((size_t)n_cells * kHeaderBytes);
+  if (hdr_host) {
+    // host header copies are validated before the context is touched
+    std::memcpy(hdr.data(), hdr_host, hdr.size());
+    for (int c = 0; c < n_cells; ++c) {
+      BlobInfo tmp;
+      rc = parse_header(hdr.data() + (size_t)c * kHeaderBytes, blob_bytes[c], &tmp);
+      if (rc) return rc;
+    }
+    if (!ctx) return jolt_fail(JOLT_E_INVAL, "jolt_decompress: ctx is null");
+    HIP_OK(hipSetDevice(ctx->device));
+  } else {
+    if (!ctx) return jolt_fail(JOLT_E_INVAL, "jolt_decompress: ctx is null");
+    HIP_OK(hipSetDevice(ctx->device));
+    for (int c = 0; c < n_cells; ++c) {
+      if (!blobs[c] || blob_bytes[c] < (size_t)kHeaderBytes) return jolt_fail(JOLT_E_BLOB, "blob %d too small", c);
+      HIP_OK(hipMemcpyAsync(hdr.data() + (size_t)c * kHeaderBytes, blobs[c], kHeaderBytes, hipMemcpyDeviceToHost, st));
+    }
+    HIP_OK(hipStreamSynchronize(st));
+  }
+  const int m = out->n_layers * out->n_heads, T = out->T, d = out->d, N = m * d;
+  std::vector<BlobInfo> bi(n_cells);
+  int kmax = 0;
+  for (int c = 0; c < n_cells; ++c) {
+    if (!blobs[c] || !Xhat[c]) return jolt_fail(JOLT_E_INVAL, "blob/Xhat %d is null", c);
+    if (reinterpret_cast<uintptr_t>(Xhat[c]) & 15) return jolt_fail(JOLT_E_INVAL, "Xhat[%d] not 16-byte aligned", c);
+    rc = parse_header(hdr.data() + (size_t)c * kHeaderBytes, blob_bytes[c], &bi[c]);
+    if (rc) return rc;
+    const BlobInfo &b = bi[c];
+    if ((int)b.m != m || (int)b.T != T || (int)b.d != d || (int)b.heads != out->n_heads)
+      return jolt_fail(JOLT_E_BLOB, "blob %d shape (m %u, T %u, d %u) differs from the output descriptor", c, b.m, b.T, b.d);
+    if (b.group != bi[0].group || b.f16 != bi[0].f16)
+      return jolt_fail(JOLT_E_BLOB, "group and factor precision must be equal across the blobs of a call");
+    if ((int)b.rT > std::min(T, N) || (int)b.rd > d || (b.rT == 0) != (b.rd == 0) || d % b.group || b.group % 8)
+      return jolt_fail(JOLT_E_BLOB, "blob %d has invalid ranks or group", c);
+    kmax = std::max(kmax, (int)b.rT);
+  }
+  // workspace: plan with the exact-method shape (its X~ / W areas cover decoding)
+  SpecShape sh;
+  jolt_spectrum_opts eo{JOLT_EXACT, 0, 0.0, 0, 0};
+  jolt_cell_desc dd = *out;
+  rc = resolve_spectrum(&dd, &eo, &sh);
+  if (rc) {  // very long contexts: size the decode areas directly
+    sh.m = m; sh.T = T; sh.d = d; sh.N = N; sh.method = JOLT_FLASH; sh.ell = 1; sh.q = 1;
+    sh.rT_max = std::min(T, N);
+  }
+  Run R{ctx, st, {}};
+  {
+    Carver cv(nullptr);
+    Ws w;
+    plan(cv, w, sh, n_cells);
+    if (ws_bytes < cv.off) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, cv.off);
+  }
+  Carver cv(ws);
+  plan(cv, R.w, sh, n_cells);
+  std::vector<uint64_t> seeds(n_cells);
+  for (int c = 0; c < n_cells; ++c) seeds[c] = bi[c].seed;
+  rc = upload_seeds_and_signs(R, seeds.data(), n_cells, d);
+  if (rc) return rc;
+  const int64_t g_stride = (int64_t)m * R.w.kmaxT * d, g_slice = (int64_t)R.w.kmaxT * d;
+  const int64_t xt_stride = (int64_t)m * T * d;
+  const int ft = bi[0].f16 ? GT_F16 : GT_F32, fb = bi[0].f16 ? 2 : 4;
+  if (kmax > 0) {
+    std::vector<GemmProblem> P;
+    for (int c = 0; c < n_cells; ++c) {
+      const BlobInfo &b = bi[c];
+      if (!b.rT) continue;
+      const uint8_t *p8 = static_cast<const uint8_t *>(blobs[c]);
+      for (int s = 0; s < m; ++s) {
+        GemmProblem p{};
+        p.A = plain(p8 + b.L.G + (int64_t)s * b.rT * b.rd * fb, b.rd);
+        p.B = plain(p8 + b.L.Ud, b.rd);
+        p.C = R.w.W + c * g_stride + s * g_slice; p.ldc = d;
+        p.M = b.rT; p.N = d; p.K = b.rd; p.alpha = 1.f;
+        p.alpha_exp2 = reinterpret_cast<const int8_t *>(p8 + b.L.gexp + s);
+        P.push_back(p);
+      }
+    }
+    rc = R.gemm(P, 1, ft, ft, true, true);
+    if (rc) return rc;
+    P.clear();
+    for (int c = 0; c < n_cells; ++c) {
+      const BlobInfo &b = bi[c];
+      if (!b.rT) continue;
+      const uint8_t *p8 = static_cast<const uint8_t *>(blobs[c]);
+      for (int s = 0; s < m; ++s) {
+        GemmProblem p{};
+        p.A = plain(p8 + b.L.UT, b.rT);
+        p.B = plain(R.w.W + c * g_stride + s * g_slice, d);
+        p.C = R.w.Xt + c * xt_stride + (int64_t)s * T * d; p.ldc = d;
+        p.M = T; p.N = d; p.K = b.rT; p.alpha = 1.f;
+        P.push_back(p);
+      }
+    }
+    rc = R.gemm(P, 1, ft, GT_F32, true, false);
+    if (rc) return rc;
+  }
+  std::vector<DecodeCell> dc(n_cells);
+  for (int c = 0; c < n_cells; ++c) {
+    const BlobInfo &b = bi[c];
+    const uint8_t *p8 = static_cast<const uint8_t *>(blobs[c]);
+    dc[c] = DecodeCell{p8 + b.L.codes, reinterpret_cast<const uint16_t *>(p8 + b.L.scales),
+                       b.rT ? R.w.Xt + c * xt_stride : nullptr, Xhat[c], (int32_t)b.bits, 0};
+  }
+  HIP_OK(hipMemcpyAsync(R.w.dcell, dc.data(), n_cells * sizeof(DecodeCell), hipMemcpyHostToDevice, st));
+  DecodeArgs da{};
+  da.cells = R.w.dcell; da.signs = R.w.signs; da.n_cells = n_cells; da.m = m; da.T = T;
+  da.heads = out->n_heads; da.group = bi[0].group; da.s_layer = out->stride_layer; da.s_head = out->stride_head;
+  da.s_tok = out->stride_token; da.inv_sqrt_d = (float)(1.0 / std::sqrt((double)d));
+  HIP_OK(launch_decode(da, d, out->dtype, st));
+  return JOLT_OK;
+}
+
+// ------------------------------------------------------------------------ eps^2 calibration
+extern "C" int jolt_eps2_workspace_size(int d, int n_samples, size_t *bytes) {
+  if (!bytes || (d != 32 && d != 64 && d != 128) || n_samples < d || n_samples % d)
+    return jolt_fail(JOLT_E_INVAL, "jolt_eps2_workspace_size: d in {32,64,128}, n_samples a positive multiple of d");
+  *bytes = (size_t)eps2_blocks() * 4 * sizeof(double) + 256;
+  return JOLT_OK;
+}
+
+extern "C" int jolt_eps2_calibrate(jolt_ctx *ctx, int group, int d, uint64_t seed, int n_samples,
+                                   double eps2_out[4], void *ws, size_t ws_bytes, jolt_stream stream) {
+  size_t need = 0;
+  int rc = jolt_eps2_workspace_size(d, n_samples, &need);
+  if (rc) return rc;
+  if (!ctx || !eps2_out || !ws) return jolt_fail(JOLT_E_INVAL, "jolt_eps2_calibrate: null argument");
+  if (group < 8 || group > d || d % group || group % 8) return jolt_fail(JOLT_E_INVAL, "bad group %d", group);
+  if (ws_bytes < need) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  HIP_OK(hipSetDevice(ctx->device));
+  hipStream_t st = (hipStream_t)stream;
+  Eps2Args a{seed, n_samples, group, (float)(1.0 / std::sqrt((double)d)), static_cast<double *>(ws)};
+  HIP_OK(launch_eps2_partial(a, d, st));
+  std::vector<double> part((size_t)eps2_blocks() * 4);
+  HIP_OK(hipMemcpyAsync(part.data(), ws, part.size() * sizeof(double), hipMemcpyDeviceToHost, st));
+  HIP_OK(hipStreamSynchronize(st));
+  double s[4] = {0, 0, 0, 0};
+  for (int b = 0; b < eps2_blocks(); ++b)
+    for (int k = 0; k < 4; ++k) s[k] += part[(size_t)b * 4 + k];
+  eps2_out[0] = 1.0;
+  for (int k = 1; k < 4; ++k) eps2_out[k] = s[0] > 0 ? s[k] / s[0] : 0.0;
+  return JOLT_OK;
+}
+
+// ------------------------------------------------------------------------ debug export
+extern "C" int jolt_debug_export(jolt_ctx *ctx, int what, int cell, void *dst, size_t dst_bytes,
+                                 jolt_stream stream) {
+  if (!ctx || !dst) return jolt_fail(JOLT_E_INVAL, "jolt_debug_export: null argument");
+  const DebugState &g = ctx->dbg;
+  if (!g.valid) return jolt_fail(JOLT_E_STATE, "jolt_debug_export: no compress call recorded");
+  if (cell < 0 || cell >= g.n_cells) return jolt_fail(JOLT_E_INVAL, "cell out of range");
+  hipStream_t st = (hipStream_t)stream;
+  HIP_OK(hipSetDevice(ctx->device));
+  if (what == 0 || what == 1) {
+    const int rows = what == 0 ? g.T : g.d, cols = what == 0 ? g.rT[cell] : g.rd[cell];
+    const float *src = what == 0 ? g.U + cell * g.u_stride : g.Ud + cell * g.ud_stride;
+    const int64_t ld = what == 0 ? g.ldu : g.d;
+    if (dst_bytes < (size_t)rows * cols * sizeof(float)) return jolt_fail(JOLT_E_WORKSPACE, "dst too small");
+    if (cols == 0) return JOLT_OK;
+    HIP_OK(hipMemcpy2DAsync(dst, cols * sizeof(float), src, ld * sizeof(float), cols * sizeof(float), rows,
+                            hipMemcpyDeviceToDevice, st));
+    return JOLT_OK;
+  }
+  if (what == 2) {
+    const size_t n = (size_t)g.m * g.T * g.d * sizeof(float);
+    if (dst_bytes < n) return jolt_fail(JOLT_E_WORKSPACE, "dst too small");
+    if (g.rT[cell] == 0) {
+      HIP_OK(hipMemsetAsync(dst, 0, n, st));
+      return JOLT_OK;
+    }
+    HIP_OK(hipMemcpyAsync(dst, g.Xt + cell * g.xt_stride, n, hipMemcpyDeviceToDevice, st));
+    return JOLT_OK;
+  }
+  if (what == 3) {
+    if (!g.Omega) return jolt_fail(JOLT_E_STATE, "no sketch in the recorded call");
+    const size_t n = (size_t)g.N * g.ell * sizeof(uint16_t);
+    if (dst_bytes < n) return jolt_fail(JOLT_E_WORKSPACE, "dst too small");
+    HIP_OK(hipMemcpyAsync(dst, g.Omega + cell * g.om_stride, n, hipMemcpyDeviceToDevice, st));
+    return JOLT_OK;
+  }
+  return jolt_fail(JOLT_E_INVAL, "unknown export %d", what);
+}

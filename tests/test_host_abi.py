@@ -1,0 +1,136 @@
+"""Host-side checks of the C-ABI library (no GPU needed).
+
+* the shared library loads and exports every function include/jolt.h declares;
+* host-only entry points agree with the oracle: cap policy, blob size, and the
+  Lagrangian allocator, which must return the oracle's allocation bit for bit
+  when both are fed the same spectra and eps^2 values;
+* argument validation rejects bad input with the documented error codes before
+  any device work.
+"""
+import ctypes as C
+
+import numpy as np
+import pytest
+
+import paper_2607_12550_amd as J
+from conftest import lowrank_cell
+from oracle import alloc as oalloc, pipeline as opl
+
+
+def test_library_exports_every_declared_function():
+    names = J.header_functions()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(J.lib, n), n
+
+
+def test_q_cap_matches_oracle():
+    for T in list(range(1, 3000, 37)) + [4096, 8192, 16384, 32768, 131072]:
+        for R in (1.5, 2, 3, 4, 4.5, 5, 8, 10):
+            assert J.jolt_q_cap(T, R) == oalloc.q_cap(T, R)
+
+
+def _desc(dtype=J.JOLT_BF16, L=4, H=8, T=256, d=128):
+    return J.cell_desc(dtype=dtype, n_layers=L, n_heads=H, T=T, d=d, stride_layer=H * T * d,
+                       stride_head=T * d, stride_token=d)
+
+
+@pytest.mark.parametrize("rT,rd,bits,g,fdt", [(0, 0, 2, 64, 1), (64, 64, 2, 64, 0), (24, 40, 4, 32, 1),
+                                              (256, 128, 8, 128, 1), (8, 8, 0, 64, 1)])
+def test_compressed_size_matches_oracle_layout(rT, rd, bits, g, fdt):
+    desc = _desc()
+    p = J.Params(rT, rd, bits, g, fdt, 0, 0)
+    fb = 2 if fdt == 1 else 4
+    assert J.jolt_compressed_size(desc, p) == opl.blob_layout(32, 256, 128, rT, rd, bits, g, fb)["total"]
+
+
+def test_spectrum_len():
+    desc = _desc(T=4096)
+    assert J.jolt_spectrum_len(desc, None) == (4096, 4096)
+    n, r = J.jolt_spectrum_len(desc, dict(method=J.JOLT_FLASH, q=0, ratio=2.0, oversample=10, power_iters=1))
+    assert (n, r) == (129, 128)
+    n, r = J.jolt_spectrum_len(_desc(T=32768), dict(method=J.JOLT_FLASH, q=0, ratio=2.0, oversample=10,
+                                                     power_iters=1))
+    assert (n, r) == (513, 512)
+    assert J.jolt_workspace_size(desc, 2, None) > 2 * 4096 * 4096 * 4
+
+
+def _spectra(rng, n_cells, m=4, T=64, d=32, flash=False):
+    cells, X = [], []
+    for i in range(n_cells):
+        x = lowrank_cell(rng, m, T, d, 6, noise=0.05 + 0.2 * i, decay=0.6 + 0.5 * i)
+        X.append(x)
+        sp = opl.spectrum(x, method="flash" if flash else "exact", q=24, p=6, power_iters=1, seed=i)
+        cells.append(dict(m=m, T=T, d=d, c=2, g=16, E=sp["E"], lam_T=sp["lam_T"],
+                          lam_d=sp["lam_d"], rT_max=sp["rT_max"]))
+    return cells
+
+
+@pytest.mark.parametrize("flash", [False, True])
+def test_allocator_bit_identical_to_oracle(rng, flash):
+    cells = _spectra(rng, 5, flash=flash)
+    eps2 = oalloc.calibrate_eps2(group=16, d=32, n_samples=1 << 14)
+    ocells = [oalloc.CellSpectrum(m=c["m"], T=c["T"], d=c["d"], c=c["c"], g=c["g"], E=c["E"],
+                                  lam_T=c["lam_T"], lam_d=c["lam_d"], rT_max=c["rT_max"])
+              for c in cells]
+    total_in = sum(c["m"] * c["T"] * c["d"] * 2 for c in cells)
+    for ratio in (1.3, 2.0, 3.0, 5.0, 9.0, 40.0):
+        for bits in ((0, 2, 4, 8), (0, 4), (2, 4)):
+            ref = oalloc.allocate(ocells, total_in / ratio, eps2, bits=bits)
+            got = J.jolt_allocate(cells, total_in / ratio, eps2, bits=bits)
+            assert got["alloc"] == [tuple(a) for a in ref["alloc"]], (ratio, bits)
+            assert got["lam"] == ref["lam"]
+            assert got["total_bytes"] == ref["total_bytes"]
+            assert got["model_error"] == ref["model_error"]
+            assert got["infeasible"] == ref["infeasible"]
+
+
+def test_allocator_floors_and_infeasible(rng):
+    cells = _spectra(rng, 3)
+    eps2 = {0: 1.0, 2: 0.26, 4: 0.01, 8: 3.5e-5}
+    got = J.jolt_allocate(cells, 10.0, eps2, floors=(16, 8, 2))
+    ocells = [oalloc.CellSpectrum(m=c["m"], T=c["T"], d=c["d"], c=c["c"], g=c["g"], E=c["E"],
+                                  lam_T=c["lam_T"], lam_d=c["lam_d"], rT_max=c["rT_max"])
+              for c in cells]
+    ref = oalloc.allocate(ocells, 10.0, eps2, floors=(16, 8, 2))
+    assert got["infeasible"] and ref["infeasible"]
+    assert got["alloc"] == [tuple(a) for a in ref["alloc"]]
+    assert all(a[0] >= 16 and a[1] >= 8 and a[2] >= 2 for a in got["alloc"])
+
+
+def test_validation_error_codes():
+    bad = _desc(d=48)
+    with pytest.raises(J.JoltError) as e:
+        J.jolt_workspace_size(bad, 1, None)
+    assert e.value.code == -2                      # JOLT_E_UNSUPPORTED
+    desc = _desc()
+    for p in (J.Params(0, 0, 3, 64, 1, 0, 0), J.Params(8, 0, 2, 64, 1, 0, 0),
+              J.Params(300, 8, 2, 64, 1, 0, 0), J.Params(8, 8, 2, 48, 1, 0, 0),
+              J.Params(8, 200, 2, 64, 1, 0, 0), J.Params(8, 8, 2, 64, 7, 0, 0)):
+        with pytest.raises(J.JoltError) as e:
+            J.jolt_compressed_size(desc, p)
+        assert e.value.code == -1                  # JOLT_E_INVAL
+    with pytest.raises(J.JoltError):
+        J.jolt_q_cap(0, 2.0)
+    # null context and pointers are rejected before any device call
+    E = np.zeros(1); lt = np.zeros(256); ld = np.zeros(128)
+    P = C.POINTER(C.c_double)
+    rc = J.lib.jolt_spectrum(None, C.byref(desc), 1, (C.c_void_p * 1)(0), None, None, None, 0,
+                             E.ctypes.data_as(P), lt.ctypes.data_as(P), ld.ctypes.data_as(P), None)
+    assert rc == -1
+    flash_odd = J.SpectrumOpts(J.JOLT_FLASH, 0, 2.0, -1, 1)
+    with pytest.raises(J.JoltError):
+        J.jolt_spectrum_len(desc, flash_odd)
+    with pytest.raises(J.JoltError):
+        J.jolt_eps2_workspace_size(128, 100)
+
+
+def test_blob_header_rejected_when_corrupt():
+    """jolt_decompress parses host header copies first; a corrupt magic is JOLT_E_BLOB."""
+    desc = _desc()
+    hdr = np.zeros(128, np.uint8)
+    hdr[:4] = np.frombuffer(b"XOLT", np.uint8)
+    rc = J.lib.jolt_decompress(None, 1, (C.c_void_p * 1)(256), (C.c_size_t * 1)(1 << 20),
+                               hdr.ctypes.data, C.byref(desc), (C.c_void_p * 1)(256), C.c_void_p(256),
+                               1 << 30, None)
+    assert rc == -4
