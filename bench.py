@@ -1,0 +1,246 @@
+#!/usr/bin/env python3
+"""Benchmark: KV-cache compression + decompression throughput on one MI355X.
+
+Workload (default): a Mistral-7B-shaped GQA cache, bf16 keys and values,
+32 layers x 8 KV heads x T 4096 x d 128, batch 1 (536.9 MB), cut into layer
+groups of 4 -> 16 cells (8 groups x K/V, m = 32 slices each).  Exact token-mode
+spectrum, ranks and residual bits chosen by the Lagrangian dual at a 2x byte
+budget, 2/4/8-bit residual grid, group 64.  Synthetic data (seeded low-rank AR(1)
+token factors, Gaussian cores, decaying feature spectra, 2 outlier channels x10,
+N(0, 0.05^2) noise); no model weights are involved.
+
+One step = the whole path over the cache: spectrum of every cell, allocation,
+compression into blobs, decompression back to a bf16 cache.  value = cache bytes x
+steps / wall time of the timed steps (GB/s, 1 GB = 1e9 B), inputs resident in HBM.
+
+Also reported: compress-only and decompress-only rates, mean relative Frobenius
+error over layers for K and V, achieved ratio, per-stage device times from the
+library's event instrumentation, the roofline of the dominant stage, and the fp64
+oracle timed on a bounded sample on the host CPU.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_GBS = 8000.0          # MI355X HBM3E peak, GB/s
+MFMA_TF = {"fp32": 157.3, "bf16": 2500.0, "fp16": 2500.0, "fp64": 78.6}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="mistral7b_gqa_T4096")
+    ap.add_argument("--ratio", type=float, default=2.0)
+    ap.add_argument("--method", default="exact", choices=["exact", "flash"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-T", type=int, default=0,
+                    help="tokens of the oracle sample cell (0 = the workload's T)")
+    return ap.parse_args()
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def stage_work(codec, calls):
+    """Algorithmic bytes / flops of the instrumented stages over `calls` steps."""
+    L, B, H, T, d = codec.shape
+    m = codec.group_layers * H
+    N = m * d
+    nc = len(codec.cells)
+    n = T
+    in_b = 2 if codec.dtype == 1 else 4
+    rT = [p.r_T for p in codec.params]
+    rd = [p.r_d for p in codec.params]
+    bits = [p.bits for p in codec.params]
+    work = {}
+    # lower triangle of every trailing matrix, one read per column (fp32)
+    sym_bytes = nc * sum(4.0 * Lr * (Lr + 1) / 2 for Lr in range(1, n))
+    work["symv"] = ("hbm", sym_bytes * calls)
+    work["token_gram"] = ("bf16" if in_b == 2 else "fp32", nc * 2.0 * T * T * N * calls)
+    work["project"] = ("fp32", sum(2.0 * r * T * N for r in rT) * calls)
+    rec = sum(2.0 * m * r * k * d + 2.0 * m * T * r * d for r, k in zip(rT, rd))
+    work["reconstruct"] = ("fp32", 2 * rec * calls)           # compress and decompress
+    res_b = sum(m * T * d * (in_b + (4 if r else 0)) + m * T * d * b / 8 + (2 * m * T * d / codec.group if b else 0)
+                for r, b in zip(rT, bits))
+    work["residual"] = ("hbm", res_b * calls)
+    dec_b = sum(m * T * d * b / 8 + (2 * m * T * d / codec.group if b else 0) + m * T * d * ((4 if r else 0) + 2)
+                for r, b in zip(rT, bits))
+    work["decode"] = ("hbm", dec_b * calls)
+    nb = 32
+    pg = 0.0
+    for k0 in range(0, n - 1, nb):
+        jb = min(nb, n - 1 - k0)
+        rem = n - (k0 + jb)
+        pg += 2 * 2.0 * rem * rem * jb
+    work["panel_gemm"] = ("fp32", nc * pg * calls)
+    return work
+
+
+def roofline_of(stage, kind, amount, ms, launches):
+    if kind == "hbm":
+        achieved = amount / (ms * 1e-3) / 1e9
+        return {"kernel": stage, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_GBS, 4), "traffic": None,
+                "launches": launches, "avg_launch_us": round(ms * 1e3 / max(1, launches), 2)}
+    peak = MFMA_TF[kind]
+    achieved = amount / (ms * 1e-3) / 1e12
+    return {"kernel": stage, "bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
+            "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None,
+            "launches": launches, "avg_launch_us": round(ms * 1e3 / max(1, launches), 2),
+            "dtype": kind}
+
+
+def cpu_baseline(cache_np, cfg, params0, group, T_sample):
+    """fp64 oracle on one cell (keys of layer group 0) timed on the host cores."""
+    import numpy as np
+    import kvsynth
+    from oracle import pipeline as opl
+    gl, H, d = cfg["group_layers"], cfg["n_heads"], cfg["d"]
+    K = cache_np
+    x = kvsynth.bf16_bits_to_f32(K[:gl, 0, :, :T_sample, :]).astype(np.float64)
+    X = x.reshape(gl * H, T_sample, d)
+    cores = len(os.sched_getaffinity(0))
+    t0 = time.perf_counter()
+    sp = opl.spectrum(X)
+    rT = min(params0.r_T, T_sample)
+    rd = params0.r_d if rT else 0
+    out = opl.compress_cell(X, r_T=rT, r_d=rd, bits=params0.bits, group=group, seed=0,
+                            factor_bytes=2, spec=sp)
+    t1 = time.perf_counter()
+    cell_bytes = X.size * 2
+    return {"value": round(cell_bytes / (t1 - t0) / 1e9, 5), "unit": "GB/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"one cell (keys, layers 0-{gl - 1}, {H} heads, T={T_sample}, d={d}, bf16, "
+                      f"{cell_bytes / 1e6:.1f} MB): exact spectrum + compress at ranks "
+                      f"({rT},{rd}) b={params0.bits} + decode, fp64 numpy/LAPACK, "
+                      f"{t1 - t0:.1f} s", "seconds": round(t1 - t0, 2)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (cells would shard "
+              "across GPUs with an all-gather of the spectra; see the design notes).", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import kvsynth
+    import paper_2607_12550_amd as J
+    from paper_2607_12550_amd.cache import CacheCodec, layer_errors
+
+    cfg = dict(kvsynth.CONFIGS[args.workload])
+    gl = cfg.pop("group_layers")
+    log("generating", args.workload)
+    t0 = time.perf_counter()
+    Knp, Vnp = kvsynth.make_cache(**cfg)
+    log(f"generated in {time.perf_counter() - t0:.1f} s")
+    dev = torch.device("cuda", 0)
+    to_dev = (lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)) \
+        if cfg["dtype"] == "bf16" else (lambda a: torch.from_numpy(a).to(dev))
+    K, V = to_dev(Knp), to_dev(Vnp)
+    codec = CacheCodec(K, V, group_layers=gl, method=args.method, ratio=args.ratio)
+    eps2 = codec.calibrate()
+    log("eps2", eps2)
+    Kout, Vout = torch.empty_like(K), torch.empty_like(V)
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    t_comp, t_dec = [], []
+
+    def step():
+        ev[0].record(stream)
+        codec.spectrum(stream)
+        codec.allocate()
+        codec.compress(stream)
+        ev[1].record(stream)
+        codec.decompress(Kout, Vout, stream)
+        ev[2].record(stream)
+
+    for w in range(args.warmup):
+        log("warmup step", w)
+        step()
+    torch.cuda.synchronize()
+    J.jolt_profile_enable(codec.ctx, True)
+    J.jolt_profile_reset(codec.ctx)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step()
+        torch.cuda.synchronize()
+        t_comp.append(ev[0].elapsed_time(ev[1]))
+        t_dec.append(ev[1].elapsed_time(ev[2]))
+        log(f"step {s}: compress {t_comp[-1]:.1f} ms, decompress {t_dec[-1]:.1f} ms")
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    prof = J.jolt_profile_read(codec.ctx)
+    J.jolt_profile_enable(codec.ctx, False)
+
+    cache_bytes = codec.cache_bytes
+    value = cache_bytes * args.steps / elapsed / 1e9
+    eK = layer_errors(K, Kout)
+    eV = layer_errors(V, Vout)
+    comp_bytes = codec.compressed_bytes()
+    alloc = [(p.r_T, p.r_d, p.bits) for p in codec.params]
+    work = stage_work(codec, args.steps)
+    dom = max((s for s in prof if prof[s][0] > 0), key=lambda s: prof[s][0])
+    if dom in work:
+        kind, amount = work[dom]
+        roof = roofline_of(dom, kind, amount, prof[dom][0], prof[dom][1])
+    else:
+        roof = {"kernel": dom, "bound": "latency", "achieved": None, "peak": None, "unit": None,
+                "frac": None, "traffic": None}
+    stages = {s: {"ms_per_step": round(v[0] / args.steps, 3), "launches_per_step": v[1] // args.steps}
+              for s, v in prof.items() if v[1]}
+    stage_roofs = {}
+    for s, (kind, amount) in work.items():
+        if prof.get(s, (0, 0))[0] > 0:
+            r = roofline_of(s, kind, amount, prof[s][0], prof[s][1])
+            stage_roofs[s] = {k: r[k] for k in ("bound", "achieved", "unit", "frac")}
+    out = {
+        "metric": "KV GB/s compressed+decompressed per GPU; rel. Frobenius error K/V at 2x",
+        "value": round(value, 3),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "layers": cfg["n_layers"], "kv_heads": cfg["n_heads"],
+                   "T": cfg["T"], "head_dim": cfg["d"], "batch": cfg["batch"], "group_layers": gl,
+                   "cells": len(codec.cells), "method": args.method, "ratio": args.ratio,
+                   "cache_bytes": cache_bytes},
+        "compress_GBps": round(cache_bytes / (np.median(t_comp) * 1e-3) / 1e9, 3),
+        "decompress_GBps": round(cache_bytes / (np.median(t_dec) * 1e-3) / 1e9, 3),
+        "rel_frobenius_error": {"K": round(float(eK.mean()), 6), "V": round(float(eV.mean()), 6)},
+        "achieved_ratio": round(cache_bytes / comp_bytes, 4),
+        "achieved_ratio_eq1_payload": round(cache_bytes / codec.payload_bytes(), 4),
+        "allocation": alloc,
+        "stage_ms_per_step": stages,
+        "stage_roofline": stage_roofs,
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        Ts = args.cpu_sample_T or cfg["T"]
+        out["cpu_baseline"] = cpu_baseline(Knp, dict(cfg, group_layers=gl), codec.params[0],
+                                           codec.group, Ts)
+    codec.close()
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -190,6 +190,34 @@ int jolt_eps2_calibrate(jolt_ctx *ctx, int group, int d, uint64_t seed, int n_sa
 int jolt_debug_export(jolt_ctx *ctx, int what, int cell, void *dst, size_t dst_bytes,
                       jolt_stream stream);
 
+/* Benchmark instrumentation.  When enabled, the library brackets the kernels of each
+ * stage below with HIP events recorded on the call's stream; jolt_profile_read waits
+ * for the recorded events and returns the device time (ms) accumulated since the last
+ * reset and the number of bracketed launches.  Disabled by default (no events). */
+enum {
+  JOLT_STAGE_FEATURE_GRAM = 0, /* E and F = sum_s X_s^T X_s (and F_Y during ST-HOSVD) */
+  JOLT_STAGE_TOKEN_GRAM,       /* C = X_(2) X_(2)^T */
+  JOLT_STAGE_SYMV,             /* tridiagonalisation: trailing symmetric mat-vec tiles */
+  JOLT_STAGE_PANEL,            /* tridiagonalisation: per-column vector work */
+  JOLT_STAGE_PANEL_GEMM,       /* tridiagonalisation: rank-2k trailing updates */
+  JOLT_STAGE_TRIDIAG_SMALL,    /* one-workgroup tridiagonalisation (small n) */
+  JOLT_STAGE_EIGVALS,          /* fp64 bisection */
+  JOLT_STAGE_EIGVECS,          /* fp64 inverse iteration + cluster re-orthogonalisation */
+  JOLT_STAGE_BACKTRANSFORM,    /* U = Q Z */
+  JOLT_STAGE_PROJECT,          /* Y = U_T^T X_(2) */
+  JOLT_STAGE_CORE,             /* G_s = Y_s U_d */
+  JOLT_STAGE_SERIALIZE,        /* factor and core packing */
+  JOLT_STAGE_RECONSTRUCT,      /* W_s and X~_s = U_T W_s from the stored factors */
+  JOLT_STAGE_RESIDUAL,         /* residual, rotation, quantisation, packing */
+  JOLT_STAGE_DECODE,           /* dequantisation, inverse rotation, add, cast */
+  JOLT_STAGE_SKETCH,           /* FlashJoLT sketch products */
+  JOLT_STAGE_ORTH,             /* FlashJoLT orthonormalisation */
+  JOLT_STAGE_COUNT
+};
+int jolt_profile_enable(jolt_ctx *ctx, int on);
+int jolt_profile_reset(jolt_ctx *ctx);
+int jolt_profile_read(jolt_ctx *ctx, int stage, double *total_ms, int64_t *launches);
+
 #ifdef __cplusplus
 }
 #endif

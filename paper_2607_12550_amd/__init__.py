@@ -20,7 +20,8 @@ __all__ = ["JoltError", "lib", "CellDesc", "SpectrumOpts", "Params", "CellSpectr
            "JOLT_FACTOR_F16", "jolt_last_error", "jolt_create", "jolt_destroy", "jolt_q_cap",
            "jolt_spectrum_len", "jolt_workspace_size", "jolt_spectrum", "jolt_compressed_size",
            "jolt_compress", "jolt_decompress", "jolt_allocate", "jolt_eps2_workspace_size",
-           "jolt_eps2_calibrate", "jolt_debug_export", "cell_desc", "LIB_PATH", "HEADER_PATH"]
+           "jolt_eps2_calibrate", "jolt_debug_export", "jolt_profile_enable", "jolt_profile_reset",
+           "jolt_profile_read", "STAGES", "cell_desc", "LIB_PATH", "HEADER_PATH"]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libjolt.so")
@@ -95,6 +96,9 @@ _SIGS = {
     "jolt_eps2_calibrate": (C.c_int, [_vp, C.c_int, C.c_int, C.c_uint64, C.c_int, _P(_dbl),
                                       _vp, _sz, _vp]),
     "jolt_debug_export": (C.c_int, [_vp, C.c_int, C.c_int, _vp, _sz, _vp]),
+    "jolt_profile_enable": (C.c_int, [_vp, C.c_int]),
+    "jolt_profile_reset": (C.c_int, [_vp]),
+    "jolt_profile_read": (C.c_int, [_vp, C.c_int, _P(_dbl), _P(C.c_int64)]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _f = getattr(lib, _name)
@@ -258,6 +262,29 @@ def jolt_eps2_calibrate(ctx, group: int, d: int, seed: int, n_samples: int, ws,
     _check(lib.jolt_eps2_calibrate(ctx, group, d, seed, n_samples, out, _addr(ws),
                                    ws.numel() * ws.element_size(), _stream(stream)))
     return {0: out[0], 2: out[1], 4: out[2], 8: out[3]}
+
+
+STAGES = ["feature_gram", "token_gram", "symv", "panel", "panel_gemm", "tridiag_small", "eigvals",
+          "eigvecs", "backtransform", "project", "core", "serialize", "reconstruct", "residual",
+          "decode", "sketch", "orth"]
+
+
+def jolt_profile_enable(ctx, on: bool = True) -> None:
+    _check(lib.jolt_profile_enable(ctx, 1 if on else 0))
+
+
+def jolt_profile_reset(ctx) -> None:
+    _check(lib.jolt_profile_reset(ctx))
+
+
+def jolt_profile_read(ctx) -> dict:
+    """{stage name: (total ms, launches)} accumulated since the last reset."""
+    out = {}
+    for i, name in enumerate(STAGES):
+        ms, n = _dbl(), C.c_int64()
+        _check(lib.jolt_profile_read(ctx, i, C.byref(ms), C.byref(n)))
+        out[name] = (ms.value, n.value)
+    return out
 
 
 def jolt_debug_export(ctx, what: int, cell: int, dst, stream=None) -> None:

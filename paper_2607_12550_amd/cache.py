@@ -1,0 +1,202 @@
+"""Whole-cache runtime over the C-ABI: cell planning, buffers and the budgeted pipeline.
+
+A KV cache is two tensors ``[L][B][H][T][d]`` (keys, values) resident on the GPU.
+Section 4 of the paper cuts the L layers into contiguous groups and compresses
+keys and values of every group separately; here every (group, K/V, batch item)
+is one cell, read in place through a strided descriptor.  This module only
+marshals pointers, sizes buffers and sequences the library calls:
+``jolt_spectrum`` for every cell, ``jolt_allocate`` under the global byte budget
+B = cache bytes / R (eq. (3)), ``jolt_compress`` into one blob arena, and
+``jolt_decompress`` back into caller-provided tensors.  The compression method
+itself runs entirely inside libjolt.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+import torch
+
+from . import (JOLT_BF16, JOLT_EXACT, JOLT_F32, JOLT_FACTOR_F16, JOLT_FACTOR_F32, JOLT_FLASH,
+               HEADER_BYTES, Params, SpectrumOpts, cell_desc, jolt_allocate, jolt_compress,
+               jolt_compressed_size, jolt_create, jolt_decompress, jolt_destroy,
+               jolt_eps2_calibrate, jolt_eps2_workspace_size, jolt_spectrum, jolt_spectrum_len,
+               jolt_workspace_size)
+
+
+@dataclass
+class CellRef:
+    tensor: int        # 0 = keys, 1 = values
+    group: int
+    batch: int
+    ptr: int           # device address of element (layer0 of group, batch, head 0, t 0, f 0)
+
+
+@dataclass
+class Plan:
+    cells: list
+    desc: object
+    n_heads: int
+    group_layers: int
+    cache_bytes: int
+    params: list = field(default_factory=list)
+    offsets: list = field(default_factory=list)
+    sizes: list = field(default_factory=list)
+
+
+class CacheCodec:
+    """Budgeted compression of a KV cache held as two [L][B][H][T][d] tensors."""
+
+    def __init__(self, K: torch.Tensor, V: torch.Tensor, *, group_layers: int,
+                 method: str = "exact", ratio: float = 2.0, q: int = 0, oversample: int = 10,
+                 power_iters: int = 1, group: int = 64, bits=(0, 2, 4, 8), step: int = 8,
+                 count_scale_bytes: bool = True, seed: int = 0, max_cells_per_call: int = 16,
+                 device: int = 0):
+        assert K.shape == V.shape and K.dtype == V.dtype and K.is_cuda and K.is_contiguous()
+        L, B, H, T, d = K.shape
+        if L % group_layers:
+            raise ValueError("the number of layers must be a multiple of group_layers")
+        self.K, self.V = K, V
+        self.shape = (L, B, H, T, d)
+        self.dtype = JOLT_BF16 if K.dtype == torch.bfloat16 else JOLT_F32
+        esz = K.element_size()
+        self.group_layers, self.ratio, self.group, self.bits, self.step = group_layers, ratio, group, bits, step
+        self.count_scale_bytes = count_scale_bytes
+        self.method = JOLT_FLASH if method == "flash" else JOLT_EXACT
+        self.opts = SpectrumOpts(self.method, q, float(ratio), oversample, power_iters)
+        self.factor_dtype = JOLT_FACTOR_F16 if self.dtype == JOLT_BF16 else JOLT_FACTOR_F32
+        self.fbytes = 2 if self.factor_dtype == JOLT_FACTOR_F16 else 4
+        self.desc = cell_desc(dtype=self.dtype, n_layers=group_layers, n_heads=H, T=T, d=d,
+                              stride_layer=B * H * T * d, stride_head=T * d, stride_token=d)
+        self.cells = []
+        for t, X in enumerate((K, V)):
+            for g in range(L // group_layers):
+                for b in range(B):
+                    off = ((g * group_layers * B + b) * H) * T * d
+                    self.cells.append(CellRef(t, g, b, X.data_ptr() + off * esz))
+        self.seeds = [seed + i for i in range(len(self.cells))]
+        self.cache_bytes = 2 * K.numel() * esz
+        self.chunk = max(1, min(max_cells_per_call, len(self.cells)))
+        self.ctx = jolt_create(device)
+        self.ws = torch.empty(jolt_workspace_size(self.desc, self.chunk, self.opts), dtype=torch.uint8,
+                              device=K.device)
+        self.n_lam, self.rT_max = jolt_spectrum_len(self.desc, self.opts)
+        self.eps2 = None
+        # blob arena: at most the whole budget plus per-blob headers and alignment
+        arena = int(self.cache_bytes / ratio) + len(self.cells) * (HEADER_BYTES + 8 * 256) + (1 << 20)
+        self.arena = torch.zeros(arena, dtype=torch.uint8, device=K.device)
+        self.params = None
+        self.blob_ptrs = None
+        self.blob_sizes = None
+        self.hdr = None
+        self.spectra = None
+
+    def close(self):
+        if self.ctx:
+            jolt_destroy(self.ctx)
+            self.ctx = None
+
+    def _chunks(self):
+        for i in range(0, len(self.cells), self.chunk):
+            yield i, self.cells[i:i + self.chunk]
+
+    def calibrate(self, n_samples: int = 1 << 20, seed: int = 0):
+        d = self.shape[4]
+        ws = torch.empty(jolt_eps2_workspace_size(d, n_samples), dtype=torch.uint8, device=self.K.device)
+        self.eps2 = jolt_eps2_calibrate(self.ctx, self.group, d, seed, n_samples, ws)
+        return self.eps2
+
+    def spectrum(self, stream=None):
+        E, LT, LD = [], [], []
+        for i, cs in self._chunks():
+            e, lt, ld = jolt_spectrum(self.ctx, self.desc, [c.ptr for c in cs], self.seeds[i:i + len(cs)],
+                                      self.opts, self.ws, stream=stream)
+            E.append(e); LT.append(lt); LD.append(ld)
+        self.spectra = (np.concatenate(E), np.concatenate(LT), np.concatenate(LD))
+        return self.spectra
+
+    def allocate(self, budget_bytes=None):
+        E, LT, LD = self.spectra
+        L, B, H, T, d = self.shape
+        m = self.group_layers * H
+        cells = [dict(m=m, T=T, d=d, c=self.fbytes, g=self.group, E=float(E[i]), lam_T=LT[i],
+                      lam_d=LD[i], rT_max=self.rT_max) for i in range(len(self.cells))]
+        budget = self.cache_bytes / self.ratio if budget_bytes is None else budget_bytes
+        res = jolt_allocate(cells, budget, self.eps2, bits=self.bits, step=self.step,
+                            count_scale_bytes=self.count_scale_bytes)
+        self.set_params([Params(rT, rd, b, self.group, self.factor_dtype, 0, s)
+                         for (rT, rd, b), s in zip(res["alloc"], self.seeds)])
+        return res
+
+    def set_params(self, params):
+        self.params = params
+        sizes = [jolt_compressed_size(self.desc, p) for p in params]
+        offs, pos = [], 0
+        for s in sizes:
+            offs.append(pos)
+            pos += (s + 255) // 256 * 256
+        if pos > self.arena.numel():
+            self.arena = torch.zeros(pos, dtype=torch.uint8, device=self.K.device)
+        base = self.arena.data_ptr()
+        self.blob_ptrs = [base + o for o in offs]
+        self.blob_sizes = sizes
+
+    def compress(self, stream=None):
+        for i, cs in self._chunks():
+            n = len(cs)
+            jolt_compress(self.ctx, self.desc, [c.ptr for c in cs], self.params[i:i + n], self.opts,
+                          self.ws, self.blob_ptrs[i:i + n], ws_bytes=self.ws.numel(),
+                          blob_bytes=self.blob_sizes[i:i + n], stream=stream)
+
+    def headers(self):
+        """Host copy of every blob header (lets decompress skip the device->host read)."""
+        out = np.zeros((len(self.cells), HEADER_BYTES), np.uint8)
+        for i, p in enumerate(self.blob_ptrs):
+            t = torch.empty(HEADER_BYTES, dtype=torch.uint8)
+            src = self.arena[p - self.arena.data_ptr():p - self.arena.data_ptr() + HEADER_BYTES]
+            t.copy_(src)
+            out[i] = t.numpy()
+        self.hdr = out
+        return out
+
+    def decompress(self, Kout: torch.Tensor, Vout: torch.Tensor, stream=None):
+        L, B, H, T, d = self.shape
+        out_dtype = JOLT_BF16 if Kout.dtype == torch.bfloat16 else JOLT_F32
+        od = cell_desc(dtype=out_dtype, n_layers=self.group_layers, n_heads=H, T=T, d=d,
+                       stride_layer=B * H * T * d, stride_head=T * d, stride_token=d)
+        esz = Kout.element_size()
+        outs = []
+        for c in self.cells:
+            off = ((c.group * self.group_layers * B + c.batch) * H) * T * d
+            outs.append((Kout, Vout)[c.tensor].data_ptr() + off * esz)
+        for i, cs in self._chunks():
+            n = len(cs)
+            hdr = self.hdr[i:i + n] if self.hdr is not None else None
+            jolt_decompress(self.ctx, self.blob_ptrs[i:i + n], od, outs[i:i + n], self.ws, hdr_host=hdr,
+                            blob_bytes=self.blob_sizes[i:i + n], ws_bytes=self.ws.numel(), stream=stream)
+
+    def compressed_bytes(self) -> int:
+        return int(sum(self.blob_sizes))
+
+    def payload_bytes(self, with_scales: bool = True) -> int:
+        """Eq. (1) bytes of the chosen allocation (factors + codes [+ scales])."""
+        L, B, H, T, d = self.shape
+        m = self.group_layers * H
+        tot = 0
+        for p in self.params:
+            s = (m * p.r_T * p.r_d + T * p.r_T + d * p.r_d) * self.fbytes
+            if p.bits:
+                s += p.bits * m * T * d // 8 + (2 * (m * T * d // p.group) if with_scales else 0)
+            tot += s
+        return tot
+
+
+def layer_errors(X: torch.Tensor, Xh: torch.Tensor) -> np.ndarray:
+    """Relative Frobenius error per layer of a [L][B][H][T][d] cache."""
+    L = X.shape[0]
+    out = np.zeros(L)
+    for l in range(L):
+        a = X[l].float()
+        b = Xh[l].float()
+        out[l] = float(torch.linalg.vector_norm(a - b) / torch.linalg.vector_norm(a))
+    return out

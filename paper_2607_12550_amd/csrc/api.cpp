@@ -214,3 +214,77 @@ int parse_header(const uint8_t *h, size_t blob_bytes, BlobInfo *bi) {
   bi->L = L;
   return JOLT_OK;
 }
+
+// ------------------------------------------------------------------------ profiling
+static hipEvent_t pool_get(jolt_ctx *c) {
+  if (!c->prof_pool.empty()) {
+    hipEvent_t e = c->prof_pool.back();
+    c->prof_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+StageTimer::StageTimer(jolt_ctx *c, hipStream_t s, int stage_) : ctx(c), st(s), stage(stage_) {
+  if (!ctx || !ctx->prof_on) return;
+  a = pool_get(ctx);
+  if (a && hipEventRecord(a, st) != hipSuccess) {
+    ctx->prof_pool.push_back(a);
+    a = nullptr;
+  }
+}
+
+StageTimer::~StageTimer() {
+  if (!a) return;
+  hipEvent_t b = pool_get(ctx);
+  if (b && hipEventRecord(b, st) == hipSuccess) {
+    ctx->prof_pending.push_back(ProfRecord{stage, a, b});
+  } else {
+    ctx->prof_pool.push_back(a);
+    if (b) ctx->prof_pool.push_back(b);
+  }
+}
+
+jolt_ctx::~jolt_ctx() {
+  for (auto &r : prof_pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
+  for (auto e : prof_pool) (void)hipEventDestroy(e);
+}
+
+static int prof_drain(jolt_ctx *c) {
+  for (auto &r : c->prof_pending) {
+    HIP_OK(hipEventSynchronize(r.b));
+    float ms = 0.f;
+    HIP_OK(hipEventElapsedTime(&ms, r.a, r.b));
+    c->prof_ms[r.stage] += ms;
+    c->prof_n[r.stage] += 1;
+    c->prof_pool.push_back(r.a);
+    c->prof_pool.push_back(r.b);
+  }
+  c->prof_pending.clear();
+  return JOLT_OK;
+}
+
+extern "C" int jolt_profile_enable(jolt_ctx *ctx, int on) {
+  if (!ctx) return jolt_fail(JOLT_E_INVAL, "ctx is null");
+  ctx->prof_on = on != 0;
+  return JOLT_OK;
+}
+
+extern "C" int jolt_profile_reset(jolt_ctx *ctx) {
+  if (!ctx) return jolt_fail(JOLT_E_INVAL, "ctx is null");
+  int rc = prof_drain(ctx);
+  if (rc) return rc;
+  for (int i = 0; i < JOLT_STAGE_COUNT; ++i) { ctx->prof_ms[i] = 0.0; ctx->prof_n[i] = 0; }
+  return JOLT_OK;
+}
+
+extern "C" int jolt_profile_read(jolt_ctx *ctx, int stage, double *total_ms, int64_t *launches) {
+  if (!ctx || stage < 0 || stage >= JOLT_STAGE_COUNT) return jolt_fail(JOLT_E_INVAL, "bad profile query");
+  int rc = prof_drain(ctx);
+  if (rc) return rc;
+  if (total_ms) *total_ms = ctx->prof_ms[stage];
+  if (launches) *launches = ctx->prof_n[stage];
+  return JOLT_OK;
+}

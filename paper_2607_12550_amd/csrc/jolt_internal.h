@@ -45,12 +45,33 @@ struct DebugState {
   int64_t u_stride = 0, ldu = 0, ud_stride = 0, xt_stride = 0, om_stride = 0;
 };
 
+struct ProfRecord {
+  int stage;
+  hipEvent_t a, b;
+};
+
 struct jolt_ctx {
   int device = 0;
   hipDeviceProp_t prop{};
   SpecKey spec;
   DebugState dbg;
   std::vector<GemmProblem> tab_host;
+  bool prof_on = false;
+  std::vector<ProfRecord> prof_pending;
+  std::vector<hipEvent_t> prof_pool;
+  double prof_ms[JOLT_STAGE_COUNT] = {};
+  int64_t prof_n[JOLT_STAGE_COUNT] = {};
+  ~jolt_ctx();
+};
+
+// Brackets device work queued on `st` while alive (no-op unless profiling is enabled).
+struct StageTimer {
+  jolt_ctx *ctx;
+  hipStream_t st;
+  int stage;
+  hipEvent_t a = nullptr;
+  StageTimer(jolt_ctx *c, hipStream_t s, int stage_);
+  ~StageTimer();
 };
 
 int validate_desc(const jolt_cell_desc *d);

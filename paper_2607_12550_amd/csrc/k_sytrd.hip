@@ -1,0 +1,340 @@
+// Blocked Householder tridiagonalisation for large symmetric matrices (the exact
+// token Gram C = X_(2) X_(2)^T of section 4 at T in the thousands), batched over
+// matrices of one size.
+//
+// Panel of nb columns (the latrd scheme): for column i = k0 + j, o = i + 1,
+//   x  = A[:, i] - V[:, :j] W[i, :j]^T - W[:, :j] V[i, :j]^T     (column as updated so far)
+//   Householder of x[o:]: alpha = x_o, sigma = ||x[o+1:]||^2, beta, tau, scal = 1/(alpha - beta)
+//   v  = e_o + scal * x_tail           (x_tail = x with entries <= o zeroed)
+//   y  = A22 v - V (W^T v) - W (V^T v),   A22 = A[o:, o:] as at the panel start
+//   w  = tau y - (tau^2 / 2)(y^T v) v,    W[:, j] = w
+// then A22 -= V W^T + W V^T as one MFMA GEMM with K = 2 nb (full storage is kept).
+//
+// By linearity A22 v = scal * A22 x_tail + A22[:, o], so the memory-bound mat-vec
+// runs on the unnormalised x_tail while sigma and the correction dot products
+// W^T x_tail, V^T x_tail are accumulated in the same launch.  Per column:
+//   k_symv_tiles  lower-triangle 64 x 64 tiles of A22 (each read once; an off-diagonal
+//                 tile feeds two row blocks through per-slot partials, so row sums are
+//                 formed in a fixed order), plus the dot partials;
+//   k_col_finish  per 256-row block: tau, v, y, w_pre = tau y, partial w_pre^T v;
+//   k_col_next    per 256-row block: w = w_pre + alpha2 v, and the next column's x.
+// Panels are stored twice, P = [V; W] and Q = [W; V] (rows = panel columns, packed to
+// the panel's width jb), so the rank-2jb update is the single product P^T Q.  Every row
+// a kernel or the update reads (rows >= the current column's o) has been written in
+// the current panel, so the panel buffers never need clearing.
+#include <algorithm>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr int TB = 64;    // mat-vec tile
+constexpr int RB = 256;   // rows per workgroup of the column kernels
+
+JOLT_DEV void tri_decode(int t, int &I, int &J) {
+  int i = (int)((sqrtf(8.f * (float)t + 1.f) - 1.f) * 0.5f);
+  while ((i + 1) * (i + 2) / 2 <= t) ++i;
+  while (i * (i + 1) / 2 > t) --i;
+  I = i;
+  J = t - i * (i + 1) / 2;
+}
+
+struct MatView {
+  float *A, *P, *Q, *xt, *wpre, *part, *dpart, *wpart, *sc;
+  double *d, *e;
+  float *tau;
+};
+
+JOLT_DEV MatView view(const SytrdArgs &a, int mat) {
+  const int n = a.n, nb = a.nb;
+  MatView m;
+  m.A = a.A + (int64_t)mat * a.mat_stride;
+  float *base = a.work + (int64_t)mat * a.work_stride;
+  m.P = base;
+  m.Q = m.P + (int64_t)2 * nb * n;
+  m.xt = m.Q + (int64_t)2 * nb * n;
+  m.wpre = m.xt + n;
+  m.part = m.wpre + n;
+  m.dpart = m.part + (int64_t)a.slots * n;
+  m.wpart = m.dpart + (int64_t)a.slots * (2 * nb + 1);
+  m.sc = m.wpart + a.slots;          // [0] alpha, [1] diagonal
+  m.d = a.d + (int64_t)mat * n;
+  m.e = a.e + (int64_t)mat * n;
+  m.tau = a.tau + (int64_t)mat * n;
+  return m;
+}
+
+// A22 x_tail partials for tile (I, J); tiles (I, 0) also produce the dot partials
+__global__ void __launch_bounds__(256) k_symv_tiles(SytrdArgs a, int i, int j, int jbw) {
+  const int mat = blockIdx.y, n = a.n, nb = a.nb, o = i + 1, L = n - o;
+  const MatView M = view(a, mat);
+  int I, J;
+  tri_decode(blockIdx.x, I, J);
+  __shared__ float t[TB][TB + 1];
+  __shared__ float vi[TB], vj[TB];
+  const int tid = threadIdx.x;
+  const int r0 = I * TB, c0 = J * TB;
+  const float *x = M.xt + o;
+#pragma unroll 4
+  for (int q = tid; q < TB * TB; q += 256) {
+    const int rr = q / TB, cc = q % TB;
+    const int r = r0 + rr, c = c0 + cc;
+    float v = 0.f;
+    if (r < L && c < L && (I != J || cc <= rr)) v = M.A[(int64_t)(o + r) * n + (o + c)];
+    t[rr][cc] = v;
+  }
+  if (tid < TB) {
+    vi[tid] = (r0 + tid < L) ? x[r0 + tid] : 0.f;
+    vj[tid] = (c0 + tid < L) ? x[c0 + tid] : 0.f;
+  }
+  __syncthreads();
+  const int row = tid >> 2, qq = tid & 3;
+  float s = 0.f, u = 0.f;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) s = fmaf(t[row][qq * 16 + k], vj[qq * 16 + k], s);
+  if (I != J) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) u = fmaf(t[qq * 16 + k][row], vi[qq * 16 + k], u);
+  } else {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int rr = qq * 16 + k;
+      if (rr > row) u = fmaf(t[rr][row], vi[rr], u);
+    }
+  }
+  s += __shfl_xor(s, 1, 64); s += __shfl_xor(s, 2, 64);
+  u += __shfl_xor(u, 1, 64); u += __shfl_xor(u, 2, 64);
+  if (qq == 0) {
+    if (I != J) {
+      if (r0 + row < L) M.part[(int64_t)J * n + r0 + row] = s;
+      if (c0 + row < L) M.part[(int64_t)I * n + c0 + row] = u;
+    } else {
+      if (r0 + row < L) M.part[(int64_t)I * n + r0 + row] = s + u;
+    }
+  }
+  if (J != 0) return;
+  // dot partials over the rows of block I: [sigma, W_p^T x (p < j), V_p^T x (p < j)]
+  const int lane = tid & 63, wave = tid >> 6;
+  const int r = r0 + lane;
+  const float xr = (r < L) ? x[r] : 0.f;
+  const float *V = M.P, *W = M.P + (int64_t)jbw * n;
+  for (int k = wave; k < 2 * j + 1; k += 4) {
+    float pr;
+    if (k == 0) pr = xr * xr;
+    else if (k <= j) pr = (r < L) ? W[(int64_t)(k - 1) * n + o + r] * xr : 0.f;
+    else pr = (r < L) ? V[(int64_t)(k - 1 - j) * n + o + r] * xr : 0.f;
+    pr = wave_sum(pr);
+    if (lane == 0) M.dpart[(int64_t)I * (2 * nb + 1) + k] = pr;
+  }
+}
+
+JOLT_DEV void householder(float alpha, double sigma, double &beta, double &tv, double &scal) {
+  if (sigma == 0.0) { tv = 0.0; beta = alpha; scal = 0.0; return; }
+  beta = -copysign(sqrt((double)alpha * alpha + sigma), (double)alpha);
+  tv = (beta - alpha) / beta;
+  scal = 1.0 / (alpha - beta);
+}
+
+// per row block: v, y, w_pre and partial w_pre^T v for column i (panel index j)
+__global__ void __launch_bounds__(RB) k_col_finish(SytrdArgs a, int i, int j, int jbw) {
+  const int mat = blockIdx.y, n = a.n, nb = a.nb, o = i + 1, L = n - o;
+  const MatView M = view(a, mat);
+  const int nt = (L + TB - 1) / TB;
+  __shared__ float pw[64], pv[64];
+  __shared__ double red[RB / 64];
+  __shared__ double sh_sigma;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // sigma and the dots, summed over the row blocks in a fixed order
+  if (tid < 2 * j + 1) {
+    double s = 0.0;
+    for (int I = 0; I < nt; ++I) s += (double)M.dpart[(int64_t)I * (2 * nb + 1) + tid];
+    if (tid == 0) sh_sigma = s;
+    else if (tid <= j) pw[tid - 1] = (float)s;
+    else pv[tid - 1 - j] = (float)s;
+  }
+  __syncthreads();
+  const float alpha = M.sc[0];
+  double beta, tv, scal;
+  householder(alpha, sh_sigma, beta, tv, scal);
+  const float sc = (float)scal, tf = (float)tv;
+  float *V = M.P, *W = M.P + (int64_t)jbw * n;
+  float *Qv = M.Q + (int64_t)jbw * n;
+  // W^T v = scal W^T x_tail + W[o, :]  (v = e_o + scal x_tail, x_tail[o] = 0)
+  if (tid < j) {
+    pw[tid] = sc * pw[tid] + W[(int64_t)tid * n + o];
+    pv[tid] = sc * pv[tid] + V[(int64_t)tid * n + o];
+  }
+  __syncthreads();
+  const int r = o + blockIdx.x * RB + tid;
+  double dot = 0.0;
+  if (r < n) {
+    const float vr = (r == o) ? 1.f : (tv == 0.0 ? 0.f : sc * M.xt[r]);
+    float y = 0.f;
+    for (int s = 0; s < nt; ++s) y += M.part[(int64_t)s * n + (r - o)];
+    y = sc * y + M.A[(int64_t)o * n + r];        // + A22[:, 0] (row o by symmetry)
+    for (int p = 0; p < j; ++p) y -= V[(int64_t)p * n + r] * pw[p] + W[(int64_t)p * n + r] * pv[p];
+    const float wp = (tv == 0.0) ? 0.f : tf * y;
+    M.wpre[r] = wp;
+    V[(int64_t)j * n + r] = vr;
+    Qv[(int64_t)j * n + r] = vr;
+    M.A[(int64_t)r * n + i] = vr;                 // reflector kept for the back-transformation
+    dot = (double)wp * (double)vr;
+  }
+  dot = wave_sum(dot);
+  if (lane == 0) red[wave] = dot;
+  __syncthreads();
+  if (tid == 0) {
+    double s = 0.0;
+    for (int w = 0; w < RB / 64; ++w) s += red[w];
+    M.wpart[blockIdx.x] = (float)s;
+    if (blockIdx.x == 0) { M.d[i] = M.sc[1]; M.e[i] = beta; M.tau[i] = (float)tv; }
+  }
+}
+
+// per row block: final w of column i, then x for column ip (panel index jp, using the
+// panel's reflectors 0 .. jp-1); prep_only skips the w part (first column of a panel)
+__global__ void __launch_bounds__(RB) k_col_next(SytrdArgs a, int i, int j, int ip, int jp,
+                                                 int prep_only, int jbw) {
+  const int mat = blockIdx.y, n = a.n;
+  const MatView M = view(a, mat);
+  float *V = M.P, *W = M.P + (int64_t)jbw * n;
+  __shared__ float cw[64], cv[64];
+  __shared__ float alpha2_s;
+  const int tid = threadIdx.x;
+  float alpha2 = 0.f;
+  if (!prep_only) {
+    const int o = i + 1, L = n - o;
+    const int nblk = (L + RB - 1) / RB;
+    if (tid == 0) {
+      double s = 0.0;
+      for (int b = 0; b < nblk; ++b) s += (double)M.wpart[b];
+      alpha2_s = (float)(-0.5 * (double)M.tau[i] * s);
+    }
+    __syncthreads();
+    alpha2 = alpha2_s;
+    // rows o .. n-1, the same split as k_col_finish; each thread owns one row
+    const int r = o + blockIdx.x * RB + tid;
+    if (r < n) {
+      const float w = M.wpre[r] + alpha2 * V[(int64_t)j * n + r];
+      W[(int64_t)j * n + r] = w;
+      M.Q[(int64_t)j * n + r] = w;
+    }
+    if (ip >= n - 1) return;
+  }
+  // coefficients W[p][ip], V[p][ip]; reflector j's w[ip] is rebuilt here because another
+  // workgroup of this launch writes it
+  if (tid < jp) {
+    float wv = W[(int64_t)tid * n + ip];
+    if (!prep_only && tid == j) wv = M.wpre[ip] + alpha2 * V[(int64_t)j * n + ip];
+    cw[tid] = wv;
+    cv[tid] = V[(int64_t)tid * n + ip];
+  }
+  __syncthreads();
+  // x[r] = A[ip][r] - sum_p (V[p][r] W[p][ip] + W[p][r] V[p][ip]) for r >= ip (row ip = column ip);
+  // row r of W_j was written above by this same thread
+  const int r = ip + blockIdx.x * RB + tid;
+  if (r < n) {
+    float x = M.A[(int64_t)ip * n + r];
+    for (int p = 0; p < jp; ++p) x -= V[(int64_t)p * n + r] * cw[p] + W[(int64_t)p * n + r] * cv[p];
+    if (r == ip) M.sc[1] = x;
+    if (r == ip + 1) M.sc[0] = x;
+    M.xt[r] = (r > ip + 1) ? x : 0.f;
+  }
+}
+
+__global__ void __launch_bounds__(64) k_sytrd_finish(SytrdArgs a) {
+  const int mat = blockIdx.x, n = a.n;
+  float *A = a.A + (int64_t)mat * a.mat_stride;
+  if (threadIdx.x == 0) {
+    a.d[(int64_t)mat * n + n - 1] = A[(int64_t)(n - 1) * n + (n - 1)];
+    a.e[(int64_t)mat * n + n - 1] = 0.0;
+    a.tau[(int64_t)mat * n + n - 1] = 0.f;
+  }
+}
+
+// zero the upper triangle and diagonal of the reflector block (dense V for the back-transform)
+__global__ void k_reflector_clean(SytrdArgs a) {
+  const int mat = blockIdx.y, n = a.n;
+  float *A = a.A + (int64_t)mat * a.mat_stride;
+  const int64_t total = (int64_t)n * n;
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < total;
+       q += (int64_t)gridDim.x * blockDim.x) {
+    const int r = (int)(q / n), c = (int)(q % n);
+    if (c >= r || c == n - 1) A[q] = 0.f;
+  }
+}
+
+size_t per_mat_floats(int n, int nb) {
+  const size_t slots = (n + TB - 1) / TB;
+  return 4 * (size_t)nb * n + 2 * (size_t)n + slots * n + slots * (2 * nb + 1) + slots + 64;
+}
+
+}  // namespace
+
+size_t sytrd_large_work_floats(int n_mat, int n, int nb) {
+  return (size_t)n_mat * ((per_mat_floats(n, nb) + 63) / 64 * 64);
+}
+
+size_t sytrd_large_table_entries(int n_mat, int n, int nb) {
+  const int panels = (n - 1 + nb - 1) / nb;
+  return (size_t)panels * n_mat;
+}
+
+hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, GemmProblem *tab_dev,
+                              GemmProblem *tab_host, hipStream_t st, const LaunchHook &hook) {
+  const int n = b.n, nm = b.n_mat;
+  SytrdArgs a{};
+  a.A = b.A; a.mat_stride = b.mat_stride; a.n = n; a.nb = nb;
+  a.d = b.d; a.e = b.e; a.tau = b.tau;
+  a.work = work;
+  a.work_stride = (int64_t)((per_mat_floats(n, nb) + 63) / 64 * 64);
+  a.slots = (n + TB - 1) / TB;
+  const int panels = (n - 1 + nb - 1) / nb;
+  // one fused rank-2jb update per panel: A22 -= P^T Q with P = [V; W], Q = [W; V]
+  for (int p = 0; p < panels; ++p) {
+    const int k0 = p * nb, jb = std::min(nb, n - 1 - k0), s = k0 + jb, rem = n - s;
+    for (int m = 0; m < nm; ++m) {
+      float *A = b.A + (int64_t)m * b.mat_stride;
+      const float *P = work + (int64_t)m * a.work_stride;
+      const float *Q = P + (int64_t)2 * nb * n;
+      GemmProblem g{};
+      g.A = GemmOperand{P + s, n, 0, 0, 0, 1};    // A(m = r, k = p) = P[p][s + r]
+      g.B = GemmOperand{Q + s, n, 0, 0, 0, 1};    // B(k = p, n = c) = Q[p][s + c]
+      g.C = A + (int64_t)s * n + s; g.ldc = n;
+      g.M = rem; g.N = rem; g.K = 2 * jb; g.alpha = -1.f; g.beta = 1.f;
+      tab_host[(size_t)p * nm + m] = g;
+    }
+  }
+  hipError_t err = hipMemcpyAsync(tab_dev, tab_host, sizeof(GemmProblem) * panels * nm,
+                                  hipMemcpyHostToDevice, st);
+  if (err != hipSuccess) return err;
+  for (int p = 0; p < panels; ++p) {
+    const int k0 = p * nb, jb = std::min(nb, n - 1 - k0);
+    hook(JOLT_STAGE_PANEL, 1);
+    hipLaunchKernelGGL(k_col_next, dim3((n - k0 + RB - 1) / RB, nm), dim3(RB), 0, st, a, -1, 0, k0, 0, 1, jb);
+    hook(JOLT_STAGE_PANEL, 0);
+    for (int j = 0; j < jb; ++j) {
+      const int i = k0 + j, o = i + 1, L = n - o;
+      const int nt = (L + TB - 1) / TB, nblk = (L + RB - 1) / RB;
+      hook(JOLT_STAGE_SYMV, 1);
+      hipLaunchKernelGGL(k_symv_tiles, dim3(nt * (nt + 1) / 2, nm), dim3(256), 0, st, a, i, j, jb);
+      hook(JOLT_STAGE_SYMV, 0);
+      hook(JOLT_STAGE_PANEL, 1);
+      hipLaunchKernelGGL(k_col_finish, dim3(nblk, nm), dim3(RB), 0, st, a, i, j, jb);
+      const bool more = j + 1 < jb;
+      hipLaunchKernelGGL(k_col_next, dim3(nblk, nm), dim3(RB), 0, st, a, i, j, more ? i + 1 : n, j + 1, 0, jb);
+      hook(JOLT_STAGE_PANEL, 0);
+    }
+    const int s = k0 + jb;
+    if (s < n) {
+      hook(JOLT_STAGE_PANEL_GEMM, 1);
+      err = launch_gemm(tab_dev + (size_t)p * nm, nm, n - s, n - s, 1, GT_F32, GT_F32, false, false, st);
+      if (err != hipSuccess) return err;
+      hook(JOLT_STAGE_PANEL_GEMM, 0);
+    }
+  }
+  hipLaunchKernelGGL(k_sytrd_finish, dim3(nm), dim3(64), 0, st, a);
+  hipLaunchKernelGGL(k_reflector_clean, dim3(1024, nm), dim3(256), 0, st, a);
+  return hipGetLastError();
+}

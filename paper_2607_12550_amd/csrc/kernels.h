@@ -5,6 +5,16 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/jolt.h"
+
+// Optional per-launch instrumentation: fn(user, stage, 1) before and fn(user, stage, 0)
+// after a launch of the given JOLT_STAGE_* kind.
+struct LaunchHook {
+  void (*fn)(void *user, int stage, int begin) = nullptr;
+  void *user = nullptr;
+  void operator()(int stage, int begin) const { if (fn) fn(user, stage, begin); }
+};
+
 // ----------------------------------------------------------------- residual / decode
 struct ResidCell {
   const void *x;        // cell base pointer (bf16 or fp32)
@@ -123,6 +133,21 @@ struct EigBatch {
 };
 // Householder tridiagonalisation (lower): small n in one workgroup per matrix.
 hipError_t launch_sytrd_small(const EigBatch &b, hipStream_t st);
+// Blocked multi-workgroup tridiagonalisation for large n (panels of nb columns).
+// work: sytrd_large_work_floats() device floats; tables: sytrd_large_table_entries().
+struct SytrdArgs {
+  float *A;
+  int64_t mat_stride;
+  int32_t n, nb, slots, pad;
+  double *d, *e;
+  float *tau;
+  float *work;           // per-matrix panels, vectors and partial sums
+  int64_t work_stride;   // floats between matrices in work
+};
+size_t sytrd_large_work_floats(int n_mat, int n, int nb);
+size_t sytrd_large_table_entries(int n_mat, int n, int nb);
+hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, GemmProblem *tab_dev,
+                              GemmProblem *tab_host, hipStream_t st, const LaunchHook &hook);
 // all eigenvalues of the tridiagonal (fp64 bisection), descending
 hipError_t launch_tridiag_eigvals(const EigBatch &b, hipStream_t st);
 // top-k eigenvectors of the tridiagonal by fp64 inverse iteration, orthogonalised

@@ -14,6 +14,8 @@
 namespace {
 
 constexpr int KC = 256;   // inverse-iteration columns per launch (bounds its scratch)
+constexpr int SYTRD_SMALL_MAX = 768;   // larger matrices use the blocked multi-workgroup kernel
+constexpr int SYTRD_NB = 32;
 
 struct Carver {
   uint8_t *base;
@@ -33,6 +35,7 @@ struct EigWs {
   double *Z = nullptr, *lu = nullptr;
   int32_t *k = nullptr;
   float *bt = nullptr;
+  float *trd = nullptr;    // blocked tridiagonalisation work (large n only)
   int kmax = 0;
 };
 
@@ -83,6 +86,7 @@ void carve_eig(Carver &cv, EigWs &e, int nmat, int n, int kmax, float *A) {
   e.b.tau = cv.take<float>((size_t)nmat * n);
   e.kmax = kmax;
   e.k = cv.take<int32_t>(nmat);
+  if (n > SYTRD_SMALL_MAX) e.trd = cv.take<float>(sytrd_large_work_floats(nmat, n, SYTRD_NB));
   if (kmax > 0) {
     e.Z = cv.take<double>((size_t)nmat * n * kmax);
     e.lu = cv.take<double>((size_t)nmat * 3 * n * std::min(kmax, KC));
@@ -93,7 +97,8 @@ void carve_eig(Carver &cv, EigWs &e, int nmat, int n, int kmax, float *A) {
 void plan(Carver &cv, Ws &w, const SpecShape &sh, int nc) {
   const int m = sh.m, T = sh.T, d = sh.d, N = sh.N;
   const int nmax = std::max({T, d, sh.ell});
-  w.tab_n = 8192 + backtransform_table_entries(nc, nmax) + 4 * (size_t)nc * m;
+  w.tab_n = 8192 + backtransform_table_entries(nc, nmax) + 4 * (size_t)nc * m +
+            sytrd_large_table_entries(nc, nmax, SYTRD_NB);
   w.tab = cv.take<GemmProblem>(w.tab_n);
   w.rcell = cv.take<ResidCell>(nc);
   w.dcell = cv.take<DecodeCell>(nc);
@@ -153,6 +158,22 @@ GemmOperand plain(const void *p, int64_t ld) {
   return o;
 }
 
+// Launch hook that brackets individual launches with profiling events.
+struct HookState {
+  jolt_ctx *ctx;
+  hipStream_t st;
+  StageTimer *open = nullptr;
+};
+void hook_fn(void *u, int stage, int begin) {
+  HookState *h = static_cast<HookState *>(u);
+  if (begin) {
+    h->open = new StageTimer(h->ctx, h->st, stage);
+  } else {
+    delete h->open;
+    h->open = nullptr;
+  }
+}
+
 struct Run {
   jolt_ctx *ctx;
   hipStream_t st;
@@ -184,7 +205,20 @@ struct Run {
 
 // symmetric eigenvalues (all) of the n x n matrices in e.b.A
 int eig_values(Run &R, EigWs &e) {
-  HIP_OK(launch_sytrd_small(e.b, R.st));
+  if (e.b.n > SYTRD_SMALL_MAX) {
+    const size_t nt = sytrd_large_table_entries(e.b.n_mat, e.b.n, SYTRD_NB);
+    GemmProblem *tab = R.tab_slice(nt);
+    if (!tab) return jolt_fail(JOLT_E_WORKSPACE, "GEMM problem table overflow");
+    R.ctx->tab_host.resize(std::max(R.ctx->tab_host.size(), nt));
+    HookState hs{R.ctx, R.st};
+    LaunchHook hook;
+    if (R.ctx->prof_on) { hook.fn = hook_fn; hook.user = &hs; }
+    HIP_OK(launch_sytrd_large(e.b, e.trd, SYTRD_NB, tab, R.ctx->tab_host.data(), R.st, hook));
+  } else {
+    StageTimer t(R.ctx, R.st, JOLT_STAGE_TRIDIAG_SMALL);
+    HIP_OK(launch_sytrd_small(e.b, R.st));
+  }
+  StageTimer t(R.ctx, R.st, JOLT_STAGE_EIGVALS);
   HIP_OK(launch_tridiag_eigvals(e.b, R.st));
   return JOLT_OK;
 }
@@ -197,7 +231,11 @@ int eig_vectors(Run &R, EigWs &e, const std::vector<int> &k, float *U, int64_t l
   if (kmax > e.kmax) return jolt_fail(JOLT_E_WORKSPACE, "eigenvector count %d exceeds workspace %d", kmax, e.kmax);
   HIP_OK(hipMemcpyAsync(e.k, k.data(), k.size() * sizeof(int32_t), hipMemcpyHostToDevice, R.st));
   InvitWork iw{e.Z, e.lu, kmax, std::min(kmax, KC), e.k};
-  HIP_OK(launch_tridiag_eigvecs(e.b, iw, kmax, R.st));
+  {
+    StageTimer t(R.ctx, R.st, JOLT_STAGE_EIGVECS);
+    HIP_OK(launch_tridiag_eigvecs(e.b, iw, kmax, R.st));
+  }
+  StageTimer t(R.ctx, R.st, JOLT_STAGE_BACKTRANSFORM);
   const size_t nt = backtransform_table_entries(e.b.n_mat, e.b.n);
   GemmProblem *tab = R.tab_slice(nt);
   if (!tab) return jolt_fail(JOLT_E_WORKSPACE, "GEMM problem table overflow");
@@ -231,8 +269,11 @@ int feature_stage(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int n
   a.partial_F = R.w.fpart;
   a.partial_E = R.w.epart;
   a.nonfinite = R.w.nonfinite;
-  HIP_OK(launch_feature_gram(a, sh.d, desc->dtype, R.st));
-  HIP_OK(launch_feature_gram_reduce(a, sh.d, R.w.F, R.w.E, R.st));
+  {
+    StageTimer t(R.ctx, R.st, JOLT_STAGE_FEATURE_GRAM);
+    HIP_OK(launch_feature_gram(a, sh.d, desc->dtype, R.st));
+    HIP_OK(launch_feature_gram_reduce(a, sh.d, R.w.F, R.w.E, R.st));
+  }
   return eig_values(R, R.w.feig);
 }
 
@@ -250,8 +291,11 @@ int token_exact(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc,
     p.alpha = 1.f; p.beta = 0.f;
   }
   const int mode = desc->dtype == JOLT_BF16 ? 0 : 1;
-  int rc = R.gemm(P, mode, dtype_gt(desc->dtype), dtype_gt(desc->dtype), true, true);
-  if (rc) return rc;
+  {
+    StageTimer t(R.ctx, R.st, JOLT_STAGE_TOKEN_GRAM);
+    int rc = R.gemm(P, mode, dtype_gt(desc->dtype), dtype_gt(desc->dtype), true, true);
+    if (rc) return rc;
+  }
   return eig_values(R, R.w.teig);
 }
 
@@ -431,8 +475,11 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
       p.M = rT[c]; p.N = N; p.K = T; p.alpha = 1.f;
       P.push_back(p);
     }
-    rc = R.gemm(P, 1, GT_F32, dtype_gt(desc->dtype), false, false);
-    if (rc) return rc;
+    {
+      StageTimer t(R.ctx, R.st, JOLT_STAGE_PROJECT);
+      rc = R.gemm(P, 1, GT_F32, dtype_gt(desc->dtype), false, false);
+      if (rc) return rc;
+    }
     // feature factor from the Gram of Y: F_Y = sum_s Y_s^T Y_s, top r_d eigenvectors
     std::vector<FGramCell> fc(nc);
     for (int c = 0; c < nc; ++c) fc[c] = FGramCell{R.w.Y + c * y_stride, rT[c], 0};
@@ -441,8 +488,11 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
     a.cells = R.w.fcell; a.n_cells = nc; a.nseg = m; a.seg_heads = 1; a.seg_hi = d; a.seg_lo = 0;
     a.row_stride = N; a.chunks_per_cell = R.w.chunks; a.partial_F = R.w.fpart; a.partial_E = R.w.epart;
     a.nonfinite = R.w.nonfinite;
-    HIP_OK(launch_feature_gram(a, d, JOLT_F32, R.st));
-    HIP_OK(launch_feature_gram_reduce(a, d, R.w.F, R.w.E, R.st));
+    {
+      StageTimer t(R.ctx, R.st, JOLT_STAGE_FEATURE_GRAM);
+      HIP_OK(launch_feature_gram(a, d, JOLT_F32, R.st));
+      HIP_OK(launch_feature_gram_reduce(a, d, R.w.F, R.w.E, R.st));
+    }
     rc = eig_values(R, R.w.feig);
     if (rc) return rc;
     rc = eig_vectors(R, R.w.feig, rd, R.w.Ud, d, (int64_t)d * d);
@@ -460,8 +510,11 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
         P.push_back(p);
       }
     }
-    rc = R.gemm(P, 1, GT_F32, GT_F32, true, false);
-    if (rc) return rc;
+    {
+      StageTimer t(R.ctx, R.st, JOLT_STAGE_CORE);
+      rc = R.gemm(P, 1, GT_F32, GT_F32, true, false);
+      if (rc) return rc;
+    }
     // serialise U_T, U_d, G (fp16 with per-slice exponents, or fp32)
     std::vector<SerFactorCell> sf(2 * nc);
     std::vector<SerCell> sc(nc);
@@ -476,6 +529,7 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
     }
     HIP_OK(hipMemcpyAsync(R.w.sfcell, sf.data(), sf.size() * sizeof(SerFactorCell), hipMemcpyHostToDevice, R.st));
     HIP_OK(hipMemcpyAsync(R.w.scell, sc.data(), sc.size() * sizeof(SerCell), hipMemcpyHostToDevice, R.st));
+    StageTimer t(R.ctx, R.st, JOLT_STAGE_SERIALIZE);
     HIP_OK(launch_factor_pack(SerFactor{R.w.sfcell}, 2 * nc, maxel, R.st));
     HIP_OK(launch_core_pack(SerCore{R.w.scell, m}, nc, R.st));
   }
@@ -484,6 +538,7 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
     if (!rT[c]) HIP_OK(hipMemsetAsync(static_cast<uint8_t *>(blobs[c]) + L[c].gexp, 0, m, R.st));
   // X~ from the stored factors: W_s = 2^e_s G^_s U^_d^T, X~_s = U^_T W_s
   if (kmax > 0) {
+    StageTimer t(R.ctx, R.st, JOLT_STAGE_RECONSTRUCT);
     std::vector<GemmProblem> P;
     for (int c = 0; c < nc; ++c) {
       if (!rT[c]) continue;
@@ -531,6 +586,7 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
     ra.cells = R.w.rcell; ra.signs = R.w.signs; ra.n_cells = nc; ra.m = m; ra.T = T;
     ra.heads = desc->n_heads; ra.group = params[0].group; ra.s_layer = desc->stride_layer;
     ra.s_head = desc->stride_head; ra.s_tok = desc->stride_token; ra.inv_sqrt_d = (float)(1.0 / std::sqrt((double)d));
+    StageTimer t(R.ctx, R.st, JOLT_STAGE_RESIDUAL);
     HIP_OK(launch_residual_quant(ra, d, desc->dtype, R.st));
   }
   // headers
@@ -623,6 +679,7 @@ extern "C" int jolt_decompress(jolt_ctx *ctx, int n_cells, const void *const *bl
   const int64_t xt_stride = (int64_t)m * T * d;
   const int ft = bi[0].f16 ? GT_F16 : GT_F32, fb = bi[0].f16 ? 2 : 4;
   if (kmax > 0) {
+    StageTimer t(ctx, st, JOLT_STAGE_RECONSTRUCT);
     std::vector<GemmProblem> P;
     for (int c = 0; c < n_cells; ++c) {
       const BlobInfo &b = bi[c];
@@ -669,6 +726,7 @@ extern "C" int jolt_decompress(jolt_ctx *ctx, int n_cells, const void *const *bl
   da.cells = R.w.dcell; da.signs = R.w.signs; da.n_cells = n_cells; da.m = m; da.T = T;
   da.heads = out->n_heads; da.group = bi[0].group; da.s_layer = out->stride_layer; da.s_head = out->stride_head;
   da.s_tok = out->stride_token; da.inv_sqrt_d = (float)(1.0 / std::sqrt((double)d));
+  StageTimer t(ctx, st, JOLT_STAGE_DECODE);
   HIP_OK(launch_decode(da, d, out->dtype, st));
   return JOLT_OK;
 }

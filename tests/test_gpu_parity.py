@@ -150,3 +150,42 @@ def test_spectrum_then_compress_reuses_and_matches_direct():
     b_direct, _ = compress(xs, desc, params, ws=ws2)
     for a, b in zip(b_reuse, b_direct):
         assert blob_bytes(a) == blob_bytes(b)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_blocked_tridiagonalisation_spectrum_and_subspace(dtype):
+    """T = 1024 > 768 takes the blocked multi-workgroup tridiagonalisation."""
+    X = keys_cell(T=1024, H=4)
+    xs, ex, desc = device_cells([X, keys_cell(T=1024, H=4, seed=5)], dtype)
+    ws = workspace(desc, 2)
+    note("jolt_spectrum exact T=1024", dtype)
+    E, lamT, lamd = J.jolt_spectrum(ctx(), desc, xs, None, None, ws)
+    tol = 1e-5 if dtype == "f32" else 1e-3
+    for c in range(2):
+        sp = opl.spectrum(ex[c])
+        np.testing.assert_allclose(lamT[c], sp["lam_T"], rtol=0, atol=tol * sp["lam_T"][0])
+    # r_T = 32: one layer's heads share a rank-32 token factor, so the cut has a clear gap;
+    # Davis-Kahan bounds the subspace difference by ||dC|| / gap with ||dC|| ~ 1e-5 ||C||
+    sp = opl.spectrum(ex[0])
+    lam = sp["lam_T"]
+    gap = lam[31] - lam[32]
+    assert gap / lam[31] > 0.02
+    ptol = min(0.05, 1e-5 * lam[0] / gap)
+    fdt = J.JOLT_FACTOR_F32 if dtype == "f32" else J.JOLT_FACTOR_F16
+    p = [J.Params(32, 32, 4, 64, fdt, 0, 0), J.Params(48, 40, 2, 64, fdt, 0, 1)]
+    blobs, _ = compress(xs, desc, p, ws=ws)
+    U = torch.empty((1024, 32), device="cuda")
+    J.jolt_debug_export(ctx(), 0, 0, U)
+    U = U.cpu().numpy().astype(np.float64)
+    Ue = sp["U_T"][:, :32]
+    assert np.abs(U @ U.T - Ue @ Ue.T).max() < ptol
+    np.testing.assert_allclose(U.T @ U, np.eye(32), atol=1e-5)
+    ref = opl.compress_cell(ex[0], r_T=32, r_d=32, bits=4, group=64, seed=0,
+                            factor_bytes=4 if dtype == "f32" else 2, spec=sp)
+    Xt = torch.empty((4, 1024, 128), device="cuda")
+    J.jolt_debug_export(ctx(), 2, 0, Xt)
+    Xt = Xt.cpu().numpy().astype(np.float64)
+    # backbone error (first-order insensitive to the subspace) within the stated tolerance
+    eb_gpu, eb_ref = opl.rel_error(ex[0], Xt), opl.rel_error(ex[0], ref["Xtilde"])
+    assert abs(eb_gpu / eb_ref - 1) < tol, (eb_gpu, eb_ref)
+    assert np.linalg.norm(Xt - ref["Xtilde"]) <= max(tol, ptol) * np.linalg.norm(ex[0])
