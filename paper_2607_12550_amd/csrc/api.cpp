@@ -248,6 +248,8 @@ StageTimer::~StageTimer() {
 }
 
 jolt_ctx::~jolt_ctx() {
+  if (trd_exec) (void)hipGraphExecDestroy(trd_exec);
+  if (cap_stream) (void)hipStreamDestroy(cap_stream);
   for (auto &r : prof_pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
   for (auto e : prof_pool) (void)hipEventDestroy(e);
 }

@@ -61,6 +61,10 @@ struct jolt_ctx {
   std::vector<hipEvent_t> prof_pool;
   double prof_ms[JOLT_STAGE_COUNT] = {};
   int64_t prof_n[JOLT_STAGE_COUNT] = {};
+  // replay of the fixed launch sequence of the blocked tridiagonalisation
+  hipStream_t cap_stream = nullptr;
+  hipGraphExec_t trd_exec = nullptr;
+  std::vector<const void *> trd_key;
   ~jolt_ctx();
 };
 

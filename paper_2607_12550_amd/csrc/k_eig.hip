@@ -135,21 +135,72 @@ JOLT_DEV void gershgorin(const double *d, const double *e, int n, double &gl, do
   gu += 2.0 * DBL_EPSILON * tnorm + 2.0 * pivmin;
 }
 
-__global__ void k_tri_eigvals(EigBatch b) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int n = b.n;
-  if (idx >= (int64_t)b.n_mat * n) return;
-  const int mat = (int)(idx / n), k = (int)(idx % n);
+// Bisection for all eigenvalues: one workgroup per (matrix, 512 eigenvalues); d and e^2 are
+// staged in LDS and every thread advances two independent Sturm chains per sweep, which
+// doubles the work in flight of this latency-bound recurrence.
+constexpr int EV_THREADS = 256, EV_PER_THREAD = 2;
+__global__ void __launch_bounds__(EV_THREADS) k_tri_eigvals(EigBatch b) {
+  extern __shared__ double lds[];
+  const int mat = blockIdx.y, n = b.n;
+  double *dl = lds, *e2 = lds + n;
   const double *d = b.d + (int64_t)mat * n, *e = b.e + (int64_t)mat * n;
-  double lo, hi, pivmin;
-  gershgorin(d, e, n, lo, hi, pivmin);
-  for (int it = 0; it < 200; ++it) {
-    const double mid = 0.5 * (lo + hi);
-    if (hi - lo <= 2.0 * DBL_EPSILON * fmax(fabs(lo), fabs(hi)) + 4.0 * pivmin || mid == lo || mid == hi)
-      break;
-    if (sturm_count(d, e, n, mid, pivmin) > k) hi = mid; else lo = mid;
+  for (int i = threadIdx.x; i < n; i += EV_THREADS) {
+    dl[i] = d[i];
+    e2[i] = (i < n - 1) ? e[i] * e[i] : 0.0;
   }
-  b.lam[(int64_t)mat * n + (n - 1 - k)] = 0.5 * (lo + hi);
+  __syncthreads();
+  double gl, gu, pivmin;
+  gershgorin(d, e, n, gl, gu, pivmin);
+  // the tridiagonal comes from an fp32 reduction, so resolving eigenvalues beyond a
+  // 1e-11 fraction of ||T|| adds nothing; this bounds the sweeps at about 40
+  const double atol = 1e-11 * fmax(fabs(gl), fabs(gu));
+  int k[EV_PER_THREAD];
+  double lo[EV_PER_THREAD], hi[EV_PER_THREAD];
+  bool live[EV_PER_THREAD];
+#pragma unroll
+  for (int q = 0; q < EV_PER_THREAD; ++q) {
+    k[q] = blockIdx.x * EV_THREADS * EV_PER_THREAD + q * EV_THREADS + threadIdx.x;
+    lo[q] = gl; hi[q] = gu;
+    live[q] = k[q] < n;
+  }
+  for (int it = 0; it < 200; ++it) {
+    double mid[EV_PER_THREAD];
+    bool any = false;
+#pragma unroll
+    for (int q = 0; q < EV_PER_THREAD; ++q) {
+      mid[q] = 0.5 * (lo[q] + hi[q]);
+      if (live[q] && (hi[q] - lo[q] <= 2.0 * DBL_EPSILON * fmax(fabs(lo[q]), fabs(hi[q])) + 4.0 * pivmin + atol ||
+                      mid[q] == lo[q] || mid[q] == hi[q]))
+        live[q] = false;
+      any |= live[q];
+    }
+    if (!any) break;
+    // Sturm counts (number of eigenvalues below mid) for both chains in one sweep
+    double qv[EV_PER_THREAD];
+    int cnt[EV_PER_THREAD];
+#pragma unroll
+    for (int q = 0; q < EV_PER_THREAD; ++q) {
+      qv[q] = dl[0] - mid[q];
+      if (fabs(qv[q]) <= pivmin) qv[q] = -pivmin;
+      cnt[q] = qv[q] < 0.0;
+    }
+    for (int jj = 1; jj < n; ++jj) {
+      const double dj = dl[jj], ej2 = e2[jj - 1];
+#pragma unroll
+      for (int q = 0; q < EV_PER_THREAD; ++q) {
+        double t = dj - mid[q] - ej2 / qv[q];
+        if (fabs(t) <= pivmin) t = -pivmin;
+        qv[q] = t;
+        cnt[q] += t < 0.0;
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < EV_PER_THREAD; ++q)
+      if (live[q]) { if (cnt[q] > k[q]) hi[q] = mid[q]; else lo[q] = mid[q]; }
+  }
+#pragma unroll
+  for (int q = 0; q < EV_PER_THREAD; ++q)
+    if (k[q] < n) b.lam[(int64_t)mat * n + (n - 1 - k[q])] = 0.5 * (lo[q] + hi[q]);
 }
 
 // inverse iteration on (T - lam I) with partial pivoting; per-thread vectors are laid
@@ -177,7 +228,7 @@ __global__ void k_tri_eigvecs(EigBatch b, InvitWork w, int j0) {
     u32x4 r = philox4x32_10(u32x4{(uint32_t)i, (uint32_t)j, (uint32_t)mat, 4u}, 0x6a6f6c74u, 0u);
     x[(int64_t)i * ld] = ((double)r.x + 0.5) * 0x1p-31 - 1.0;
   }
-  for (int it = 0; it < 3; ++it) {
+  for (int it = 0; it < 2; ++it) {
     // forward: factor T - lam I = P L U while transforming the right-hand side in x
     double p = d[0] - lam, q = (n > 1) ? e[0] : 0.0;
     double y = x[0];
@@ -314,8 +365,15 @@ hipError_t launch_sytrd_small(const EigBatch &b, hipStream_t st) {
 }
 
 hipError_t launch_tridiag_eigvals(const EigBatch &b, hipStream_t st) {
-  int64_t total = (int64_t)b.n_mat * b.n;
-  hipLaunchKernelGGL(k_tri_eigvals, dim3((unsigned)((total + 127) / 128)), dim3(128), 0, st, b);
+  const int per_block = EV_THREADS * EV_PER_THREAD;
+  dim3 grid((b.n + per_block - 1) / per_block, b.n_mat);
+  const size_t shm = (size_t)2 * b.n * sizeof(double);
+  if (shm > 65536) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_tri_eigvals),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_tri_eigvals, grid, dim3(EV_THREADS), shm, st, b);
   return hipGetLastError();
 }
 
@@ -334,33 +392,43 @@ hipError_t launch_tridiag_eigvecs(const EigBatch &b, const InvitWork &w, int kma
 
 int backtransform_nb() { return NB; }
 
+constexpr int BT_KCHUNK = 512;   // rows per split-K chunk of W1 = V^T U
+
 size_t backtransform_scratch_floats(int n_mat, int n, int kmax) {
   const size_t panels = (n + NB - 1) / NB;
+  const size_t chunks = (n + BT_KCHUNK - 1) / BT_KCHUNK;
   return 2 * (size_t)n_mat * panels * NB * NB        // S = V^T V and T per panel
-         + 2 * (size_t)n_mat * NB * kmax;             // W1, W2
+         + (size_t)n_mat * chunks * NB * kmax         // W1 partials
+         + (size_t)n_mat * NB * kmax;                 // W2
 }
 
 size_t backtransform_table_entries(int n_mat, int n) {
   const size_t panels = (n + NB - 1) / NB;
-  return 4 * panels * (size_t)n_mat;
+  const size_t chunks = (n + BT_KCHUNK - 1) / BT_KCHUNK;
+  return panels * (size_t)n_mat * (1 + chunks + 2);
 }
 
 hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax, float *U,
                                 int64_t ldu, int64_t u_stride, float *scratch, GemmProblem *tab_dev,
                                 GemmProblem *tab_host, hipStream_t st) {
   const int n = b.n, panels = (n + NB - 1) / NB, nm = b.n_mat;
+  const int chunks_max = (n + BT_KCHUNK - 1) / BT_KCHUNK;
   {
     dim3 g((unsigned)(((int64_t)n * kmax + 255) / 256), nm);
     hipLaunchKernelGGL(k_z_to_f32, g, dim3(256), 0, st, b, w, kmax, U, ldu, u_stride);
   }
   float *Sf = scratch;
   float *Tf = Sf + (size_t)nm * panels * NB * NB;
-  float *W1 = Tf + (size_t)nm * panels * NB * NB;
-  float *W2 = W1 + (size_t)nm * NB * kmax;
-  // table layout: [S problems: panel-major x mat] then per panel [W1 | W2 | U] x mat
+  float *W1 = Tf + (size_t)nm * panels * NB * NB;            // [m][chunk * NB][kmax]
+  float *W2 = W1 + (size_t)nm * chunks_max * NB * kmax;       // [m][NB][kmax]
+  const int64_t w1_mat = (int64_t)chunks_max * NB * kmax;
+  // table: [S: panels x nm] then per panel [W1: nm x chunks | W2: nm | U: nm]
+  const size_t per_panel = (size_t)nm * (chunks_max + 2);
   GemmProblem *gS = tab_host;
   for (int p = 0; p < panels; ++p) {
     const int i0 = p * NB, pw = std::min(NB, n - 1 - i0), rows = n - (i0 + 1);
+    const int chunks = std::max(1, (rows + BT_KCHUNK - 1) / BT_KCHUNK);
+    GemmProblem *g = tab_host + (size_t)panels * nm + (size_t)p * per_panel;
     for (int m = 0; m < nm; ++m) {
       const float *A = b.A + (int64_t)m * b.mat_stride;
       GemmProblem S{};
@@ -369,31 +437,40 @@ hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax,
       S.C = Sf + ((size_t)m * panels + p) * NB * NB; S.ldc = NB;
       S.M = std::max(pw, 0); S.N = std::max(pw, 0); S.K = rows; S.alpha = 1.f; S.beta = 0.f;
       gS[(size_t)p * nm + m] = S;
-      GemmProblem *g = tab_host + (size_t)panels * nm + (size_t)p * 3 * nm;
-      GemmProblem P{};
-      P.A = GemmOperand{A + (int64_t)(i0 + 1) * n + i0, n, 0, 0, 0, 1};
-      P.B = GemmOperand{U + (int64_t)m * u_stride + (int64_t)(i0 + 1) * ldu, ldu, 0, 0, 0, 1};
-      P.C = W1 + (size_t)m * NB * kmax; P.ldc = kmax;
-      P.M = pw; P.N = kmax; P.K = rows; P.alpha = 1.f; P.beta = 0.f;
-      g[m] = P;
+      // W1 partial c = V[rows of chunk c]^T U[rows of chunk c]   (pw x kmax each)
+      for (int c = 0; c < chunks_max; ++c) {
+        GemmProblem P{};
+        const int r0 = c * BT_KCHUNK, r1 = std::min(rows, r0 + BT_KCHUNK);
+        P.A = GemmOperand{A + (int64_t)(i0 + 1 + r0) * n + i0, n, 0, 0, 0, 1};
+        P.B = GemmOperand{U + (int64_t)m * u_stride + (int64_t)(i0 + 1 + r0) * ldu, ldu, 0, 0, 0, 1};
+        P.C = W1 + m * w1_mat + (int64_t)c * NB * kmax; P.ldc = kmax;
+        P.M = (c < chunks) ? pw : 0; P.N = kmax; P.K = std::max(0, r1 - r0);
+        P.alpha = 1.f; P.beta = 0.f;
+        g[(size_t)m * chunks_max + c] = P;
+      }
+      // W2 = [T T ... T] [W1_0; W1_1; ...]: the split-K sum folded into this product
+      // (A's columns wrap onto T with a zero segment stride)
       GemmProblem Q{};
-      Q.A = GemmOperand{Tf + ((size_t)m * panels + p) * NB * NB, NB, 0, 0, 0, 1};
-      Q.B = GemmOperand{W1 + (size_t)m * NB * kmax, kmax, 0, 0, 0, 1};
+      Q.A = GemmOperand{Tf + ((size_t)m * panels + p) * NB * NB, NB, 0, 0, NB, 1};
+      Q.B = GemmOperand{W1 + m * w1_mat, kmax, 0, 0, 0, 1};
       Q.C = W2 + (size_t)m * NB * kmax; Q.ldc = kmax;
-      Q.M = pw; Q.N = kmax; Q.K = pw; Q.alpha = 1.f; Q.beta = 0.f;
-      g[nm + m] = Q;
+      Q.M = pw; Q.N = kmax; Q.K = chunks * NB; Q.alpha = 1.f; Q.beta = 0.f;
+      g[(size_t)nm * chunks_max + m] = Q;
       GemmProblem R{};
       R.A = GemmOperand{A + (int64_t)(i0 + 1) * n + i0, n, 0, 0, 0, 1};
       R.B = GemmOperand{W2 + (size_t)m * NB * kmax, kmax, 0, 0, 0, 1};
       R.C = U + (int64_t)m * u_stride + (int64_t)(i0 + 1) * ldu; R.ldc = ldu;
       R.M = rows; R.N = kmax; R.K = pw; R.alpha = -1.f; R.beta = 1.f;
-      g[2 * nm + m] = R;
+      g[(size_t)nm * (chunks_max + 1) + m] = R;
     }
   }
-  hipError_t err = hipMemcpyAsync(tab_dev, tab_host, sizeof(GemmProblem) * 4 * nm * panels,
-                                  hipMemcpyHostToDevice, st);
+  const size_t ntab = (size_t)panels * nm + (size_t)panels * per_panel;
+  hipError_t err = hipMemcpyAsync(tab_dev, tab_host, sizeof(GemmProblem) * ntab, hipMemcpyHostToDevice, st);
   if (err != hipSuccess) return err;
-  // S = V^T V for every (matrix, panel): A = V^T is m-contiguous, B = V is n-contiguous
+  // W1 rows past a short panel's width must read as zero in the folded sum: the last
+  // (shortest) panel is applied first, right after this clear
+  err = hipMemsetAsync(W1, 0, sizeof(float) * (size_t)nm * w1_mat, st);
+  if (err != hipSuccess) return err;
   err = launch_gemm(tab_dev, nm * panels, NB, NB, 1, GT_F32, GT_F32, false, false, st);
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL(k_larft, dim3(panels, nm), dim3(64), 0, st, b, Sf, Tf);
@@ -403,12 +480,12 @@ hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax,
     const int i0 = p * NB, pw = std::min(NB, n - 1 - i0);
     if (pw <= 0) continue;
     const int rows = n - (i0 + 1);
-    GemmProblem *g = tab_dev + (size_t)panels * nm + (size_t)p * 3 * nm;
-    err = launch_gemm(g, nm, pw, kmax, 1, GT_F32, GT_F32, false, false, st);
+    GemmProblem *g = tab_dev + (size_t)panels * nm + (size_t)p * per_panel;
+    err = launch_gemm(g, nm * chunks_max, pw, kmax, 1, GT_F32, GT_F32, false, false, st);
     if (err != hipSuccess) return err;
-    err = launch_gemm(g + nm, nm, pw, kmax, 1, GT_F32, GT_F32, true, false, st);
+    err = launch_gemm(g + (size_t)nm * chunks_max, nm, pw, kmax, 1, GT_F32, GT_F32, true, false, st);
     if (err != hipSuccess) return err;
-    err = launch_gemm(g + 2 * nm, nm, rows, kmax, 1, GT_F32, GT_F32, true, false, st);
+    err = launch_gemm(g + (size_t)nm * (chunks_max + 1), nm, rows, kmax, 1, GT_F32, GT_F32, true, false, st);
     if (err != hipSuccess) return err;
   }
   return hipSuccess;

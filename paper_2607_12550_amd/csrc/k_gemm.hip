@@ -226,21 +226,30 @@ __global__ void __launch_bounds__(NT) k_gemm(const GemmProblem *__restrict__ pro
 
   float alpha = P.alpha;
   if (P.alpha_exp2) alpha = ldexpf(alpha, (int)*P.alpha_exp2);
-  // epilogue: acc[i][j][q] -> C[m0 + wm*64 + i*32 + 8*(q/4) + 4*lh + q%4][n0 + wn*64 + j*32 + lr]
+  // epilogue: acc[i][j][q] -> C[m0 + wm*64 + i*32 + 8*(q/4) + 4*lh + q%4][n0 + wn*64 + j*32 + lr];
+  // the beta term's loads are all issued before any store
+  const bool use_beta = P.beta != 0.f;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int col = n0 + wn * 64 + j * 32 + lr;
-      if (col >= P.N) continue;
+      const bool cok = col < P.N;
+      float old[16];
+      if (use_beta) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int row = m0 + wm * 64 + i * 32 + 8 * (q >> 2) + 4 * lh + (q & 3);
+          old[q] = (cok && row < P.M) ? P.C[(int64_t)row * P.ldc + col] : 0.f;
+        }
+      }
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int row = m0 + wm * 64 + i * 32 + 8 * (q >> 2) + 4 * lh + (q & 3);
-        if (row < P.M) {
-          float *c = P.C + (int64_t)row * P.ldc + col;
+        if (cok && row < P.M) {
           float v = alpha * acc[i][j][q];
-          if (P.beta != 0.f) v += P.beta * *c;
-          *c = v;
+          if (use_beta) v = fmaf(P.beta, old[q], v);
+          P.C[(int64_t)row * P.ldc + col] = v;
         }
       }
     }

@@ -29,8 +29,8 @@
 
 namespace {
 
-constexpr int TB = 64;    // mat-vec tile
-constexpr int RB = 256;   // rows per workgroup of the column kernels
+constexpr int TB = 128;   // mat-vec tile
+constexpr int RB = 128;   // rows per workgroup of the column kernels
 
 JOLT_DEV void tri_decode(int t, int &I, int &J) {
   int i = (int)((sqrtf(8.f * (float)t + 1.f) - 1.f) * 0.5f);
@@ -65,65 +65,111 @@ JOLT_DEV MatView view(const SytrdArgs &a, int mat) {
   return m;
 }
 
-// A22 x_tail partials for tile (I, J); tiles (I, 0) also produce the dot partials
+// A22 x_tail partials for tile (I, J) of the trailing block.  Tiles are 128 x 128 on a grid
+// whose origin `base` is o rounded down to a multiple of 8 (so rows load as aligned float4);
+// entries with row or column < o are masked to zero.  Thread (ty, tx) of the 16 x 16 grid
+// holds an 8 x 8 sub-block in registers; row sums reduce across tx (lane shuffles), column
+// sums across ty (shuffles, then LDS across the four waves).  Tiles (I, 0) also produce the
+// dot partials [sigma, W_p^T x, V_p^T x] over their 128 rows.
 __global__ void __launch_bounds__(256) k_symv_tiles(SytrdArgs a, int i, int j, int jbw) {
-  const int mat = blockIdx.y, n = a.n, nb = a.nb, o = i + 1, L = n - o;
+  const int mat = blockIdx.y, n = a.n, nb = a.nb, o = i + 1;
+  const int base = o & ~7, Lb = n - base;
   const MatView M = view(a, mat);
   int I, J;
   tri_decode(blockIdx.x, I, J);
-  __shared__ float t[TB][TB + 1];
-  __shared__ float vi[TB], vj[TB];
-  const int tid = threadIdx.x;
-  const int r0 = I * TB, c0 = J * TB;
-  const float *x = M.xt + o;
-#pragma unroll 4
-  for (int q = tid; q < TB * TB; q += 256) {
-    const int rr = q / TB, cc = q % TB;
-    const int r = r0 + rr, c = c0 + cc;
-    float v = 0.f;
-    if (r < L && c < L && (I != J || cc <= rr)) v = M.A[(int64_t)(o + r) * n + (o + c)];
-    t[rr][cc] = v;
+  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4, lane = tid & 63, wave = tid >> 6;
+  const int r0 = I * TB + ty * 8, c0 = J * TB + tx * 8;     // relative to base
+  const float *xt = M.xt;
+  float xr[8], xc[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int gr = base + r0 + k, gc = base + c0 + k;
+    xr[k] = (gr >= o + 1 && gr < n) ? xt[gr] : 0.f;     // x_tail is zero at o and above it
+    xc[k] = (gc >= o + 1 && gc < n) ? xt[gc] : 0.f;
   }
-  if (tid < TB) {
-    vi[tid] = (r0 + tid < L) ? x[r0 + tid] : 0.f;
-    vj[tid] = (c0 + tid < L) ? x[c0 + tid] : 0.f;
-  }
-  __syncthreads();
-  const int row = tid >> 2, qq = tid & 3;
-  float s = 0.f, u = 0.f;
+  float rs[8], cs[8];
 #pragma unroll
-  for (int k = 0; k < 16; ++k) s = fmaf(t[row][qq * 16 + k], vj[qq * 16 + k], s);
-  if (I != J) {
+  for (int k = 0; k < 8; ++k) { rs[k] = 0.f; cs[k] = 0.f; }
+  const bool diag = (I == J);
 #pragma unroll
-    for (int k = 0; k < 16; ++k) u = fmaf(t[qq * 16 + k][row], vi[qq * 16 + k], u);
-  } else {
+  for (int k = 0; k < 8; ++k) {
+    const int gr = base + r0 + k;
+    float v[8];
+    const int gc0 = base + c0;
+    if (gr >= o && gr < n && gc0 + 8 <= n) {
+      const float4 *p = reinterpret_cast<const float4 *>(M.A + (int64_t)gr * n + gc0);
+      float4 u0 = p[0], u1 = p[1];
+      v[0] = u0.x; v[1] = u0.y; v[2] = u0.z; v[3] = u0.w; v[4] = u1.x; v[5] = u1.y; v[6] = u1.z; v[7] = u1.w;
+    } else {
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const int rr = qq * 16 + k;
-      if (rr > row) u = fmaf(t[rr][row], vi[rr], u);
+      for (int c = 0; c < 8; ++c)
+        v[c] = (gr >= o && gr < n && gc0 + c < n) ? M.A[(int64_t)gr * n + gc0 + c] : 0.f;
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const int gc = gc0 + c;
+      float e = (gc >= o) ? v[c] : 0.f;
+      if (diag) {
+        // lower part only: row sums take col <= row, column sums take col < row
+        const bool le = (c0 + c) <= (r0 + k), lt = (c0 + c) < (r0 + k);
+        rs[k] = fmaf(le ? e : 0.f, xc[c], rs[k]);
+        cs[c] = fmaf(lt ? e : 0.f, xr[k], cs[c]);
+      } else {
+        rs[k] = fmaf(e, xc[c], rs[k]);
+        cs[c] = fmaf(e, xr[k], cs[c]);
+      }
     }
   }
-  s += __shfl_xor(s, 1, 64); s += __shfl_xor(s, 2, 64);
-  u += __shfl_xor(u, 1, 64); u += __shfl_xor(u, 2, 64);
-  if (qq == 0) {
-    if (I != J) {
-      if (r0 + row < L) M.part[(int64_t)J * n + r0 + row] = s;
-      if (c0 + row < L) M.part[(int64_t)I * n + c0 + row] = u;
+  // row sums: reduce over tx (16 consecutive lanes)
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    float v = rs[k];
+    v += __shfl_xor(v, 1, 64); v += __shfl_xor(v, 2, 64);
+    v += __shfl_xor(v, 4, 64); v += __shfl_xor(v, 8, 64);
+    rs[k] = v;
+  }
+  // column sums: reduce over ty (lanes 16 apart in a wave, then the four waves)
+  __shared__ float csh[4][TB];
+  __shared__ float rsh[TB];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    float v = cs[c];
+    v += __shfl_xor(v, 16, 64); v += __shfl_xor(v, 32, 64);
+    cs[c] = v;
+  }
+  if (lane < 16) {
+#pragma unroll
+    for (int c = 0; c < 8; ++c) csh[wave][tx * 8 + c] = cs[c];
+  }
+  if (tx == 0) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) rsh[ty * 8 + k] = rs[k];
+  }
+  __syncthreads();
+  float *part = M.part;
+  if (tid < TB) {
+    const float colsum = csh[0][tid] + csh[1][tid] + csh[2][tid] + csh[3][tid];
+    const int rr = I * TB + tid, cc = J * TB + tid;
+    if (diag) {
+      if (rr < Lb) part[(int64_t)I * n + rr] = rsh[tid] + colsum;
     } else {
-      if (r0 + row < L) M.part[(int64_t)I * n + r0 + row] = s + u;
+      if (rr < Lb) part[(int64_t)J * n + rr] = rsh[tid];
+      if (cc < Lb) part[(int64_t)I * n + cc] = colsum;
     }
   }
   if (J != 0) return;
-  // dot partials over the rows of block I: [sigma, W_p^T x (p < j), V_p^T x (p < j)]
-  const int lane = tid & 63, wave = tid >> 6;
-  const int r = r0 + lane;
-  const float xr = (r < L) ? x[r] : 0.f;
   const float *V = M.P, *W = M.P + (int64_t)jbw * n;
+  const int g0 = base + I * TB + lane, g1 = g0 + 64;
+  const bool v0 = g0 >= o + 1 && g0 < n, v1 = g1 >= o + 1 && g1 < n;
+  const float x0 = v0 ? xt[g0] : 0.f, x1 = v1 ? xt[g1] : 0.f;
   for (int k = wave; k < 2 * j + 1; k += 4) {
     float pr;
-    if (k == 0) pr = xr * xr;
-    else if (k <= j) pr = (r < L) ? W[(int64_t)(k - 1) * n + o + r] * xr : 0.f;
-    else pr = (r < L) ? V[(int64_t)(k - 1 - j) * n + o + r] * xr : 0.f;
+    if (k == 0) {
+      pr = x0 * x0 + x1 * x1;
+    } else {
+      const float *col = (k <= j) ? W + (int64_t)(k - 1) * n : V + (int64_t)(k - 1 - j) * n;
+      pr = (v0 ? col[g0] * x0 : 0.f) + (v1 ? col[g1] * x1 : 0.f);
+    }
     pr = wave_sum(pr);
     if (lane == 0) M.dpart[(int64_t)I * (2 * nb + 1) + k] = pr;
   }
@@ -138,9 +184,9 @@ JOLT_DEV void householder(float alpha, double sigma, double &beta, double &tv, d
 
 // per row block: v, y, w_pre and partial w_pre^T v for column i (panel index j)
 __global__ void __launch_bounds__(RB) k_col_finish(SytrdArgs a, int i, int j, int jbw) {
-  const int mat = blockIdx.y, n = a.n, nb = a.nb, o = i + 1, L = n - o;
+  const int mat = blockIdx.y, n = a.n, nb = a.nb, o = i + 1;
+  const int base = o & ~7, nt = (n - base + TB - 1) / TB;
   const MatView M = view(a, mat);
-  const int nt = (L + TB - 1) / TB;
   __shared__ float pw[64], pv[64];
   __shared__ double red[RB / 64];
   __shared__ double sh_sigma;
@@ -171,7 +217,9 @@ __global__ void __launch_bounds__(RB) k_col_finish(SytrdArgs a, int i, int j, in
   if (r < n) {
     const float vr = (r == o) ? 1.f : (tv == 0.0 ? 0.f : sc * M.xt[r]);
     float y = 0.f;
-    for (int s = 0; s < nt; ++s) y += M.part[(int64_t)s * n + (r - o)];
+    const float *pp = M.part + (r - base);
+#pragma unroll 8
+    for (int s = 0; s < nt; ++s) y += pp[(int64_t)s * n];
     y = sc * y + M.A[(int64_t)o * n + r];        // + A22[:, 0] (row o by symmetry)
     for (int p = 0; p < j; ++p) y -= V[(int64_t)p * n + r] * pw[p] + W[(int64_t)p * n + r] * pv[p];
     const float wp = (tv == 0.0) ? 0.f : tf * y;
@@ -243,6 +291,29 @@ __global__ void __launch_bounds__(RB) k_col_next(SytrdArgs a, int i, int j, int 
   }
 }
 
+// After a lower-triangle trailing update, copy the lower triangle into the upper part of
+// rows s .. s+nb (the rows the next panel reads as rows): A[r][c] = A[c][r] for c > r.
+// One workgroup per 64-column chunk; the (nb+1) x 64 block is transposed through LDS.
+__global__ void __launch_bounds__(256) k_mirror_strip(SytrdArgs a, int s) {
+  const int mat = blockIdx.y, n = a.n, nb = a.nb;
+  float *A = a.A + (int64_t)mat * a.mat_stride;
+  const int rows = min(nb + 1, n - s);
+  const int c0 = s + blockIdx.x * 64;
+  __shared__ float t[64][65];
+  const int tid = threadIdx.x;
+  for (int q = tid; q < 64 * 64; q += 256) {
+    const int cc = q / 64, rr = q % 64;          // read A[c0 + cc][s + rr]: rows contiguous in rr
+    const int c = c0 + cc, r = s + rr;
+    t[cc][rr] = (rr < rows && c < n && c > r) ? A[(int64_t)c * n + r] : 0.f;
+  }
+  __syncthreads();
+  for (int q = tid; q < 64 * 64; q += 256) {
+    const int rr = q / 64, cc = q % 64;          // write A[s + rr][c0 + cc]
+    const int c = c0 + cc, r = s + rr;
+    if (rr < rows && c < n && c > r) A[(int64_t)r * n + c] = t[cc][rr];
+  }
+}
+
 __global__ void __launch_bounds__(64) k_sytrd_finish(SytrdArgs a) {
   const int mat = blockIdx.x, n = a.n;
   float *A = a.A + (int64_t)mat * a.mat_stride;
@@ -281,8 +352,30 @@ size_t sytrd_large_table_entries(int n_mat, int n, int nb) {
   return (size_t)panels * n_mat;
 }
 
-hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, GemmProblem *tab_dev,
-                              GemmProblem *tab_host, hipStream_t st, const LaunchHook &hook) {
+void sytrd_large_tables(const EigBatch &b, float *work, int nb, GemmProblem *tab_host) {
+  const int n = b.n, nm = b.n_mat;
+  const int64_t ws = (int64_t)((per_mat_floats(n, nb) + 63) / 64 * 64);
+  const int panels = (n - 1 + nb - 1) / nb;
+  // one fused rank-2jb update per panel: A22 -= P^T Q with P = [V; W], Q = [W; V]
+  for (int p = 0; p < panels; ++p) {
+    const int k0 = p * nb, jb = std::min(nb, n - 1 - k0), s = k0 + jb, rem = n - s;
+    for (int m = 0; m < nm; ++m) {
+      float *A = b.A + (int64_t)m * b.mat_stride;
+      const float *P = work + (int64_t)m * ws;
+      const float *Q = P + (int64_t)2 * nb * n;
+      GemmProblem g{};
+      g.A = GemmOperand{P + s, n, 0, 0, 0, 1};    // A(m = r, k = p) = P[p][s + r]
+      g.B = GemmOperand{Q + s, n, 0, 0, 0, 1};    // B(k = p, n = c) = Q[p][s + c]
+      g.C = A + (int64_t)s * n + s; g.ldc = n;
+      g.M = rem; g.N = rem; g.K = 2 * jb; g.alpha = -1.f; g.beta = 1.f;
+      g.lower_only = 1;   // the upper part of the next panel's rows is restored by k_mirror_strip
+      tab_host[(size_t)p * nm + m] = g;
+    }
+  }
+}
+
+hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, const GemmProblem *tab_dev,
+                              hipStream_t st, const LaunchHook &hook) {
   const int n = b.n, nm = b.n_mat;
   SytrdArgs a{};
   a.A = b.A; a.mat_stride = b.mat_stride; a.n = n; a.nb = nb;
@@ -291,24 +384,7 @@ hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, GemmProble
   a.work_stride = (int64_t)((per_mat_floats(n, nb) + 63) / 64 * 64);
   a.slots = (n + TB - 1) / TB;
   const int panels = (n - 1 + nb - 1) / nb;
-  // one fused rank-2jb update per panel: A22 -= P^T Q with P = [V; W], Q = [W; V]
-  for (int p = 0; p < panels; ++p) {
-    const int k0 = p * nb, jb = std::min(nb, n - 1 - k0), s = k0 + jb, rem = n - s;
-    for (int m = 0; m < nm; ++m) {
-      float *A = b.A + (int64_t)m * b.mat_stride;
-      const float *P = work + (int64_t)m * a.work_stride;
-      const float *Q = P + (int64_t)2 * nb * n;
-      GemmProblem g{};
-      g.A = GemmOperand{P + s, n, 0, 0, 0, 1};    // A(m = r, k = p) = P[p][s + r]
-      g.B = GemmOperand{Q + s, n, 0, 0, 0, 1};    // B(k = p, n = c) = Q[p][s + c]
-      g.C = A + (int64_t)s * n + s; g.ldc = n;
-      g.M = rem; g.N = rem; g.K = 2 * jb; g.alpha = -1.f; g.beta = 1.f;
-      tab_host[(size_t)p * nm + m] = g;
-    }
-  }
-  hipError_t err = hipMemcpyAsync(tab_dev, tab_host, sizeof(GemmProblem) * panels * nm,
-                                  hipMemcpyHostToDevice, st);
-  if (err != hipSuccess) return err;
+  hipError_t err = hipSuccess;
   for (int p = 0; p < panels; ++p) {
     const int k0 = p * nb, jb = std::min(nb, n - 1 - k0);
     hook(JOLT_STAGE_PANEL, 1);
@@ -316,7 +392,7 @@ hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, GemmProble
     hook(JOLT_STAGE_PANEL, 0);
     for (int j = 0; j < jb; ++j) {
       const int i = k0 + j, o = i + 1, L = n - o;
-      const int nt = (L + TB - 1) / TB, nblk = (L + RB - 1) / RB;
+      const int nt = (n - (o & ~7) + TB - 1) / TB, nblk = (L + RB - 1) / RB;
       hook(JOLT_STAGE_SYMV, 1);
       hipLaunchKernelGGL(k_symv_tiles, dim3(nt * (nt + 1) / 2, nm), dim3(256), 0, st, a, i, j, jb);
       hook(JOLT_STAGE_SYMV, 0);
@@ -331,6 +407,7 @@ hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, GemmProble
       hook(JOLT_STAGE_PANEL_GEMM, 1);
       err = launch_gemm(tab_dev + (size_t)p * nm, nm, n - s, n - s, 1, GT_F32, GT_F32, false, false, st);
       if (err != hipSuccess) return err;
+      hipLaunchKernelGGL(k_mirror_strip, dim3((n - s + 63) / 64, nm), dim3(256), 0, st, a, s);
       hook(JOLT_STAGE_PANEL_GEMM, 0);
     }
   }

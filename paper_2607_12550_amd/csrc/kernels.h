@@ -146,8 +146,12 @@ struct SytrdArgs {
 };
 size_t sytrd_large_work_floats(int n_mat, int n, int nb);
 size_t sytrd_large_table_entries(int n_mat, int n, int nb);
-hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, GemmProblem *tab_dev,
-                              GemmProblem *tab_host, hipStream_t st, const LaunchHook &hook);
+// host-side GEMM table of the panel updates (sytrd_large_table_entries() entries); the
+// launch sequence itself is fixed for a given shape and pointers (it may be captured once
+// into a graph and replayed).
+void sytrd_large_tables(const EigBatch &b, float *work, int nb, GemmProblem *tab_host);
+hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, const GemmProblem *tab_dev,
+                              hipStream_t st, const LaunchHook &hook);
 // all eigenvalues of the tridiagonal (fp64 bisection), descending
 hipError_t launch_tridiag_eigvals(const EigBatch &b, hipStream_t st);
 // top-k eigenvectors of the tridiagonal by fp64 inverse iteration, orthogonalised
