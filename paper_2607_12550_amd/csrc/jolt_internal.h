@@ -42,7 +42,7 @@ struct DebugState {
   std::vector<int> rT, rd;
   const float *U = nullptr, *Ud = nullptr, *Xt = nullptr;
   const uint16_t *Omega = nullptr;
-  int64_t u_stride = 0, ldu = 0, ud_stride = 0, xt_stride = 0, om_stride = 0;
+  int64_t u_stride = 0, ldu = 0, ud_stride = 0, xt_stride = 0, om_stride = 0, ldo = 0;
 };
 
 struct ProfRecord {

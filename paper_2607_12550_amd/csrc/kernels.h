@@ -200,3 +200,30 @@ struct SerFactor {
   const SerFactorCell *cells;
 };
 hipError_t launch_factor_pack(const SerFactor &a, int n_cells, int64_t max_elems, hipStream_t st);
+
+// ----------------------------------------------------------------- FlashJoLT
+struct SketchArgs {
+  const uint64_t *seeds;    // device [n_cells]
+  uint16_t *out;            // bf16 bits, [cell][N][ld]
+  int64_t cell_stride;
+  int32_t N, l, ld, pad;
+};
+hipError_t launch_sketch(const SketchArgs &a, int n_cells, hipStream_t st);
+
+struct Gram64Args {
+  const float *Y;           // [cell] rows x ld (first l columns used)
+  int64_t y_cell_stride, ld;
+  int32_t rows, l, chunks, chunk_rows;
+  double *partial;          // [cell][chunks][l][l]
+  double *G;                // [cell][l][l] (lower triangle written)
+};
+int gram64_tile();
+hipError_t launch_gram64(const Gram64Args &a, int n_cells, hipStream_t st);
+
+struct CholArgs {
+  double *G;                // [cell][l][l] in: Gram (lower); out: Cholesky factor L
+  double *M;                // [cell][l][l] out: L^-1
+  float *Rinv;              // [cell][l][ldr] out: L^-T (upper triangular)
+  int32_t l, ldr;
+};
+hipError_t launch_chol_inv(const CholArgs &a, int n_cells, hipStream_t st);

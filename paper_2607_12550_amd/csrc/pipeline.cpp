@@ -16,6 +16,7 @@ namespace {
 constexpr int KC = 256;   // inverse-iteration columns per launch (bounds its scratch)
 constexpr int SYTRD_SMALL_MAX = 768;   // larger matrices use the blocked multi-workgroup kernel
 constexpr int SYTRD_NB = 32;
+constexpr int kG64Rows = 8192;          // rows per split-K chunk of the fp64 sketch Gram
 
 struct Carver {
   uint8_t *base;
@@ -65,10 +66,14 @@ struct Ws {
   // ST-HOSVD / reconstruction
   float *Y = nullptr, *G = nullptr, *W = nullptr, *Xt = nullptr;
   // FlashJoLT
-  uint16_t *Om = nullptr;
-  float *Ysk = nullptr, *Zsk = nullptr, *Bsk = nullptr;
-  double *gram64 = nullptr;
-  float *Rinv = nullptr;
+  int ldo = 0, ldl = 0, g64_chunks = 0;
+  uint16_t *Om = nullptr;                 // sketch, N x ldo bf16 per cell
+  float *Ysk = nullptr, *Qsk = nullptr;   // T x ldl: range basis and CholeskyQR scratch
+  float *Zsk = nullptr, *Qz = nullptr;    // N x ldl: power-iteration basis and scratch
+  float *Bsk = nullptr;                   // l x N: B = Q^T X_(2)
+  float *Wsk = nullptr;                   // l x q: Ritz vectors of B B^T
+  double *g64p = nullptr, *g64 = nullptr, *chM = nullptr;
+  float *Rinv = nullptr;                  // l x ldl
   // eps2
   double *eps_part = nullptr;
 };
@@ -99,6 +104,7 @@ void plan(Carver &cv, Ws &w, const SpecShape &sh, int nc) {
   const int nmax = std::max({T, d, sh.ell});
   w.tab_n = 8192 + backtransform_table_entries(nc, nmax) + 4 * (size_t)nc * m +
             sytrd_large_table_entries(nc, nmax, SYTRD_NB);
+  if (sh.method == JOLT_FLASH) w.tab_n += (size_t)nc * 160;   // sketch, power and CholeskyQR2 products
   w.tab = cv.take<GemmProblem>(w.tab_n);
   w.rcell = cv.take<ResidCell>(nc);
   w.dcell = cv.take<DecodeCell>(nc);
@@ -121,14 +127,22 @@ void plan(Carver &cv, Ws &w, const SpecShape &sh, int nc) {
     carve_eig(cv, w.teig, nc, T, w.kmaxT, w.C);
   } else {
     const int l = sh.ell;
+    w.ldo = (l + 7) / 8 * 8;
+    w.ldl = (l + 7) / 8 * 8;
     w.C = cv.take<float>((size_t)nc * l * l);
     carve_eig(cv, w.teig, nc, l, sh.q, w.C);
-    w.Om = cv.take<uint16_t>((size_t)nc * N * l);
-    w.Ysk = cv.take<float>((size_t)nc * T * l);
-    w.Zsk = cv.take<float>((size_t)nc * N * l);
+    w.Om = cv.take<uint16_t>((size_t)nc * N * w.ldo);
+    w.Ysk = cv.take<float>((size_t)nc * T * w.ldl);
+    w.Qsk = cv.take<float>((size_t)nc * T * w.ldl);
+    w.Zsk = cv.take<float>((size_t)nc * N * w.ldl);
+    w.Qz = cv.take<float>((size_t)nc * N * w.ldl);
     w.Bsk = cv.take<float>((size_t)nc * l * N);
-    w.gram64 = cv.take<double>((size_t)nc * l * l);
-    w.Rinv = cv.take<float>((size_t)nc * l * l);
+    w.Wsk = cv.take<float>((size_t)nc * l * std::max(sh.q, 1));
+    w.g64_chunks = (std::max(T, N) + kG64Rows - 1) / kG64Rows;
+    w.g64p = cv.take<double>((size_t)nc * w.g64_chunks * l * l);
+    w.g64 = cv.take<double>((size_t)nc * l * l);
+    w.chM = cv.take<double>((size_t)nc * l * l);
+    w.Rinv = cv.take<float>((size_t)nc * l * w.ldl);
   }
   w.U = cv.take<float>((size_t)nc * T * std::max(w.kmaxT, 1));
   w.Y = cv.take<float>((size_t)nc * std::max(w.kmaxT, 1) * N);
@@ -372,13 +386,135 @@ static bool same_opts(const jolt_spectrum_opts &a, const jolt_spectrum_opts &b) 
 
 namespace {
 
+// CholeskyQR2 of the rows x l matrices in buf (ld ldl): result back in buf, tmp is scratch
+int orth(Run &R, const SpecShape &sh, int nc, float *buf, float *tmp, int rows) {
+  const int l = sh.ell, ldl = R.w.ldl;
+  float *src = buf, *dst = tmp;
+  for (int pass = 0; pass < 2; ++pass) {
+    Gram64Args g{};
+    g.Y = src; g.y_cell_stride = (int64_t)rows * ldl; g.ld = ldl;
+    g.rows = rows; g.l = l; g.chunk_rows = kG64Rows; g.chunks = (rows + kG64Rows - 1) / kG64Rows;
+    g.partial = R.w.g64p; g.G = R.w.g64;
+    HIP_OK(launch_gram64(g, nc, R.st));
+    CholArgs ca{R.w.g64, R.w.chM, R.w.Rinv, l, ldl};
+    HIP_OK(launch_chol_inv(ca, nc, R.st));
+    std::vector<GemmProblem> P(nc);
+    for (int c = 0; c < nc; ++c) {
+      GemmProblem &p = P[c];
+      p = GemmProblem{};
+      p.A = plain(src + (int64_t)c * rows * ldl, ldl);             // k-contiguous
+      p.B = plain(R.w.Rinv + (int64_t)c * l * ldl, ldl);           // n-contiguous
+      p.C = dst + (int64_t)c * rows * ldl; p.ldc = ldl;
+      p.M = rows; p.N = l; p.K = l; p.alpha = 1.f;
+    }
+    int rc = R.gemm(P, 1, GT_F32, GT_F32, true, false);
+    if (rc) return rc;
+    std::swap(src, dst);
+  }
+  return JOLT_OK;
+}
+
+// FlashJoLT token spectrum: range finder with power iterations, B = Q^T X_(2), eig(B B^T)
+int token_flash(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc, const void *const *X,
+                const uint64_t *seeds, const jolt_spectrum_opts *o) {
+  const int T = sh.T, N = sh.N, l = sh.ell, ldl = R.w.ldl, ldo = R.w.ldo;
+  const int dt = dtype_gt(desc->dtype);
+  HIP_OK(hipMemcpyAsync(R.w.seeds, seeds, nc * sizeof(uint64_t), hipMemcpyHostToDevice, R.st));
+  {
+    StageTimer t(R.ctx, R.st, JOLT_STAGE_SKETCH);
+    SketchArgs sa{R.w.seeds, R.w.Om, (int64_t)N * ldo, N, l, ldo, 0};
+    HIP_OK(launch_sketch(sa, nc, R.st));
+    std::vector<GemmProblem> P(nc);
+    for (int c = 0; c < nc; ++c) {
+      GemmProblem &p = P[c];
+      p = GemmProblem{};
+      p.A = cell_operand(X[c], desc);                               // X_(2): k-contiguous
+      p.B = plain(R.w.Om + (int64_t)c * N * ldo, ldo);               // Omega: n-contiguous
+      p.C = R.w.Ysk + (int64_t)c * T * ldl; p.ldc = ldl;
+      p.M = T; p.N = l; p.K = N; p.alpha = 1.f;
+    }
+    int rc = desc->dtype == JOLT_BF16 ? R.gemm(P, 0, GT_BF16, GT_BF16, true, false)
+                                      : R.gemm(P, 1, GT_F32, GT_BF16, true, false);
+    if (rc) return rc;
+  }
+  int rc;
+  {
+    StageTimer t(R.ctx, R.st, JOLT_STAGE_ORTH);
+    rc = orth(R, sh, nc, R.w.Ysk, R.w.Qsk, T);
+    if (rc) return rc;
+  }
+  for (int it = 0; it < o->power_iters; ++it) {
+    std::vector<GemmProblem> P(nc);
+    {
+      StageTimer t(R.ctx, R.st, JOLT_STAGE_SKETCH);
+      for (int c = 0; c < nc; ++c) {                                 // Z = X_(2)^T Q   (N x l)
+        GemmProblem &p = P[c];
+        p = GemmProblem{};
+        p.A = cell_operand(X[c], desc);                             // m-contiguous view of X_(2)^T
+        p.B = plain(R.w.Ysk + (int64_t)c * T * ldl, ldl);
+        p.C = R.w.Zsk + (int64_t)c * N * ldl; p.ldc = ldl;
+        p.M = N; p.N = l; p.K = T; p.alpha = 1.f;
+      }
+      rc = R.gemm(P, 1, dt, GT_F32, false, false);
+      if (rc) return rc;
+    }
+    {
+      StageTimer t(R.ctx, R.st, JOLT_STAGE_ORTH);
+      rc = orth(R, sh, nc, R.w.Zsk, R.w.Qz, N);
+      if (rc) return rc;
+    }
+    {
+      StageTimer t(R.ctx, R.st, JOLT_STAGE_SKETCH);
+      for (int c = 0; c < nc; ++c) {                                 // Y = X_(2) Q'   (T x l)
+        GemmProblem &p = P[c];
+        p = GemmProblem{};
+        p.A = cell_operand(X[c], desc);
+        p.B = plain(R.w.Zsk + (int64_t)c * N * ldl, ldl);
+        p.C = R.w.Ysk + (int64_t)c * T * ldl; p.ldc = ldl;
+        p.M = T; p.N = l; p.K = N; p.alpha = 1.f;
+      }
+      rc = R.gemm(P, 1, dt, GT_F32, true, false);
+      if (rc) return rc;
+    }
+    {
+      StageTimer t(R.ctx, R.st, JOLT_STAGE_ORTH);
+      rc = orth(R, sh, nc, R.w.Ysk, R.w.Qsk, T);
+      if (rc) return rc;
+    }
+  }
+  {
+    StageTimer t(R.ctx, R.st, JOLT_STAGE_SKETCH);
+    std::vector<GemmProblem> P(nc);
+    for (int c = 0; c < nc; ++c) {                                   // B = Q^T X_(2)   (l x N)
+      GemmProblem &p = P[c];
+      p = GemmProblem{};
+      p.A = plain(R.w.Ysk + (int64_t)c * T * ldl, ldl);              // m-contiguous view of Q^T
+      p.B = cell_operand(X[c], desc);                               // n-contiguous
+      p.C = R.w.Bsk + (int64_t)c * l * N; p.ldc = N;
+      p.M = l; p.N = N; p.K = T; p.alpha = 1.f;
+    }
+    rc = R.gemm(P, 1, GT_F32, dt, false, false);
+    if (rc) return rc;
+    for (int c = 0; c < nc; ++c) {                                   // B B^T   (l x l)
+      GemmProblem &p = P[c];
+      p = GemmProblem{};
+      p.A = plain(R.w.Bsk + (int64_t)c * l * N, N);
+      p.B = plain(R.w.Bsk + (int64_t)c * l * N, N);
+      p.C = R.w.C + (int64_t)c * l * l; p.ldc = l;
+      p.M = l; p.N = l; p.K = N; p.alpha = 1.f;
+    }
+    rc = R.gemm(P, 1, GT_F32, GT_F32, true, true);
+    if (rc) return rc;
+  }
+  return eig_values(R, R.w.teig);
+}
+
 int spectrum_device(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc,
                     const void *const *X, const uint64_t *seeds, const jolt_spectrum_opts *o) {
   int rc = feature_stage(R, sh, desc, nc, X);
   if (rc) return rc;
   if (sh.method == JOLT_EXACT) return token_exact(R, sh, desc, nc, X);
-  (void)seeds; (void)o;
-  return jolt_fail(JOLT_E_UNSUPPORTED, "FlashJoLT path not available in this build");
+  return token_flash(R, sh, desc, nc, X, seeds, o);
 }
 
 }  // namespace
@@ -407,8 +543,11 @@ extern "C" int jolt_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
   std::vector<double> lt((size_t)n_cells * sh.T), ld((size_t)n_cells * sh.d);
   HIP_OK(hipMemcpyAsync(E, R.w.E, n_cells * sizeof(double), hipMemcpyDeviceToHost, R.st));
   HIP_OK(hipMemcpyAsync(ld.data(), R.w.feig.b.lam, ld.size() * sizeof(double), hipMemcpyDeviceToHost, R.st));
+  std::vector<double> lf((size_t)n_cells * std::max(sh.ell, 1));
   if (sh.method == JOLT_EXACT)
     HIP_OK(hipMemcpyAsync(lt.data(), R.w.teig.b.lam, lt.size() * sizeof(double), hipMemcpyDeviceToHost, R.st));
+  else
+    HIP_OK(hipMemcpyAsync(lf.data(), R.w.teig.b.lam, lf.size() * sizeof(double), hipMemcpyDeviceToHost, R.st));
   std::vector<int32_t> bad(n_cells);
   HIP_OK(hipMemcpyAsync(bad.data(), R.w.nonfinite, n_cells * sizeof(int32_t), hipMemcpyDeviceToHost, R.st));
   HIP_OK(hipStreamSynchronize(R.st));
@@ -417,8 +556,18 @@ extern "C" int jolt_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
   // eigenvalues are clipped at 0 (the Grams are positive semi-definite)
   for (int c = 0; c < n_cells; ++c) {
     for (int i = 0; i < sh.d; ++i) lam_d[(size_t)c * sh.d + i] = std::max(0.0, ld[(size_t)c * sh.d + i]);
-    if (sh.method == JOLT_EXACT)
+    if (sh.method == JOLT_EXACT) {
       for (int i = 0; i < sh.T; ++i) lam_T[(size_t)c * sh.T + i] = std::max(0.0, lt[(size_t)c * sh.T + i]);
+    } else {
+      // the q captured Ritz values, then the omitted energy as one synthetic value
+      double captured = 0.0;
+      for (int i = 0; i < sh.q; ++i) {
+        const double v = std::max(0.0, lf[(size_t)c * sh.ell + i]);
+        lam_T[(size_t)c * (sh.q + 1) + i] = v;
+        captured += v;
+      }
+      lam_T[(size_t)c * (sh.q + 1) + sh.q] = std::max(0.0, E[c] - captured);
+    }
   }
   SpecKey &k = ctx->spec;
   k.valid = true;
@@ -488,24 +637,52 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
   std::vector<BlobLayout> L(nc);
   for (int c = 0; c < nc; ++c) L[c] = blob_layout(m, T, d, rT[c], rd[c], params[c].bits, params[0].group, fb);
   if (kmax > 0) {
-    // token factor U_T (top r_T eigenvectors of the token Gram)
-    if (sh.method != JOLT_EXACT) return jolt_fail(JOLT_E_UNSUPPORTED, "FlashJoLT path not available in this build");
-    rc = eig_vectors(R, R.w.teig, rT, R.w.U, ldu, u_stride);
-    if (rc) return rc;
-    // Y = U_T^T X_(2)   (r_T x N per cell)
     std::vector<GemmProblem> P;
-    for (int c = 0; c < nc; ++c) {
-      if (!rT[c]) continue;
-      GemmProblem p{};
-      p.A = plain(R.w.U + c * u_stride, ldu);        // A(m = r, k = t) = U[t][r]: m-contiguous
-      p.B = cell_operand(X[c], desc);                // B(k = t, n = col): n-contiguous
-      p.C = R.w.Y + c * y_stride; p.ldc = N;
-      p.M = rT[c]; p.N = N; p.K = T; p.alpha = 1.f;
-      P.push_back(p);
-    }
-    {
+    if (sh.method == JOLT_EXACT) {
+      // token factor U_T: top r_T eigenvectors of the token Gram
+      rc = eig_vectors(R, R.w.teig, rT, R.w.U, ldu, u_stride);
+      if (rc) return rc;
+      // Y = U_T^T X_(2)   (r_T x N per cell)
+      for (int c = 0; c < nc; ++c) {
+        if (!rT[c]) continue;
+        GemmProblem p{};
+        p.A = plain(R.w.U + c * u_stride, ldu);        // A(m = r, k = t) = U[t][r]: m-contiguous
+        p.B = cell_operand(X[c], desc);                // B(k = t, n = col): n-contiguous
+        p.C = R.w.Y + c * y_stride; p.ldc = N;
+        p.M = rT[c]; p.N = N; p.K = T; p.alpha = 1.f;
+        P.push_back(p);
+      }
       StageTimer t(R.ctx, R.st, JOLT_STAGE_PROJECT);
       rc = R.gemm(P, 1, GT_F32, dtype_gt(desc->dtype), false, false);
+      if (rc) return rc;
+    } else {
+      // FlashJoLT: Ritz vectors W of B B^T, U_T = Q W, and Y = W_r^T B (no pass over X)
+      const int l = sh.ell, q = sh.q, ldl = R.w.ldl;
+      rc = eig_vectors(R, R.w.teig, rT, R.w.Wsk, q, (int64_t)l * q);
+      if (rc) return rc;
+      StageTimer t(R.ctx, R.st, JOLT_STAGE_PROJECT);
+      for (int c = 0; c < nc; ++c) {
+        if (!rT[c]) continue;
+        GemmProblem p{};
+        p.A = plain(R.w.Ysk + (int64_t)c * T * ldl, ldl);             // Q: k-contiguous
+        p.B = plain(R.w.Wsk + (int64_t)c * l * q, q);                 // W: n-contiguous
+        p.C = R.w.U + c * u_stride; p.ldc = ldu;
+        p.M = T; p.N = rT[c]; p.K = l; p.alpha = 1.f;
+        P.push_back(p);
+      }
+      rc = R.gemm(P, 1, GT_F32, GT_F32, true, false);
+      if (rc) return rc;
+      P.clear();
+      for (int c = 0; c < nc; ++c) {
+        if (!rT[c]) continue;
+        GemmProblem p{};
+        p.A = plain(R.w.Wsk + (int64_t)c * l * q, q);                 // W^T: m-contiguous
+        p.B = plain(R.w.Bsk + (int64_t)c * l * N, N);                 // B: n-contiguous
+        p.C = R.w.Y + c * y_stride; p.ldc = N;
+        p.M = rT[c]; p.N = N; p.K = l; p.alpha = 1.f;
+        P.push_back(p);
+      }
+      rc = R.gemm(P, 1, GT_F32, GT_F32, false, false);
       if (rc) return rc;
     }
     // feature factor from the Gram of Y: F_Y = sum_s Y_s^T Y_s, top r_d eigenvectors
@@ -630,7 +807,7 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
   dbg.U = R.w.U; dbg.u_stride = u_stride; dbg.ldu = ldu;
   dbg.Ud = R.w.Ud; dbg.ud_stride = (int64_t)d * d;
   dbg.Xt = R.w.Xt; dbg.xt_stride = xt_stride;
-  dbg.Omega = R.w.Om; dbg.om_stride = (int64_t)N * sh.ell;
+  dbg.Omega = R.w.Om; dbg.om_stride = (int64_t)N * R.w.ldo; dbg.ldo = R.w.ldo;
   return JOLT_OK;
 }
 
@@ -823,7 +1000,9 @@ extern "C" int jolt_debug_export(jolt_ctx *ctx, int what, int cell, void *dst, s
     if (!g.Omega) return jolt_fail(JOLT_E_STATE, "no sketch in the recorded call");
     const size_t n = (size_t)g.N * g.ell * sizeof(uint16_t);
     if (dst_bytes < n) return jolt_fail(JOLT_E_WORKSPACE, "dst too small");
-    HIP_OK(hipMemcpyAsync(dst, g.Omega + cell * g.om_stride, n, hipMemcpyDeviceToDevice, st));
+    HIP_OK(hipMemcpy2DAsync(dst, g.ell * sizeof(uint16_t), g.Omega + cell * g.om_stride,
+                            g.ldo * sizeof(uint16_t), g.ell * sizeof(uint16_t), g.N,
+                            hipMemcpyDeviceToDevice, st));
     return JOLT_OK;
   }
   return jolt_fail(JOLT_E_INVAL, "unknown export %d", what);
