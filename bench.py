@@ -30,6 +30,14 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_GBS = 8000.0          # MI355X HBM3E peak, GB/s
+# method and byte budget each synthetic workload is run at (section 6 set-ups)
+WORKLOAD_RUN = {
+    "keys_fp32_8h_T256": ("exact", 2.0),
+    "mistral7b_gqa_T4096": ("exact", 2.0),
+    "mistral7b_gqa_T32768": ("flash", 2.0),
+    "llama2_13b_mha_T4096_b4": ("exact", 2.0),
+    "longctx_4L8h_T131072": ("flash", 3.0),
+}
 MFMA_TF = {"fp32": 157.3, "bf16": 2500.0, "fp16": 2500.0, "fp64": 78.6}
 
 
@@ -39,8 +47,11 @@ def parse():
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="mistral7b_gqa_T4096")
-    ap.add_argument("--ratio", type=float, default=2.0)
-    ap.add_argument("--method", default="exact", choices=["exact", "flash"])
+    ap.add_argument("--ratio", type=float, default=0.0, help="0 = the workload's budget")
+    ap.add_argument("--method", default="", choices=["", "exact", "flash"],
+                    help="empty = the workload's method")
+    ap.add_argument("--power-iters", type=int, default=1)
+    ap.add_argument("--oversample", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-T", type=int, default=0,
                     help="tokens of the oracle sample cell (0 = the workload's T)")
@@ -59,15 +70,24 @@ def stage_work(codec, calls):
     nc = len(codec.cells)
     n = T
     in_b = 2 if codec.dtype == 1 else 4
+    flash = codec.method == 1
     rT = [p.r_T for p in codec.params]
     rd = [p.r_d for p in codec.params]
     bits = [p.bits for p in codec.params]
     work = {}
-    # lower triangle of every trailing matrix, one read per column (fp32)
-    sym_bytes = nc * sum(4.0 * Lr * (Lr + 1) / 2 for Lr in range(1, n))
-    work["symv"] = ("hbm", sym_bytes * calls)
-    work["token_gram"] = ("bf16" if in_b == 2 else "fp32", nc * 2.0 * T * T * N * calls)
-    work["project"] = ("fp32", sum(2.0 * r * T * N for r in rT) * calls)
+    if flash:
+        ell = codec.ell
+        # Y = X Omega on bf16 MFMA; per power iteration X^T Q and X Q' (fp32 MFMA), then B = Q^T X
+        # and B B^T (fp32 MFMA): charged at the fp32 peak, the lower of the two
+        sk = nc * (2.0 * T * N * ell * (1 + 2 * codec.opts.power_iters + 1) + 2.0 * ell * ell * N)
+        work["sketch"] = ("fp32", sk * calls)
+        work["project"] = ("fp32", sum(2.0 * r * T * ell + 2.0 * r * ell * N for r in rT) * calls)
+    else:
+        # lower triangle of every trailing matrix, one read per column (fp32)
+        sym_bytes = nc * sum(4.0 * Lr * (Lr + 1) / 2 for Lr in range(1, n))
+        work["symv"] = ("hbm", sym_bytes * calls)
+        work["token_gram"] = ("bf16" if in_b == 2 else "fp32", nc * 2.0 * T * T * N * calls)
+        work["project"] = ("fp32", sum(2.0 * r * T * N for r in rT) * calls)
     rec = sum(2.0 * m * r * k * d + 2.0 * m * T * r * d for r, k in zip(rT, rd))
     work["reconstruct"] = ("fp32", 2 * rec * calls)           # compress and decompress
     res_b = sum(m * T * d * (in_b + (4 if r else 0)) + m * T * d * b / 8 + (2 * m * T * d / codec.group if b else 0)
@@ -76,13 +96,14 @@ def stage_work(codec, calls):
     dec_b = sum(m * T * d * b / 8 + (2 * m * T * d / codec.group if b else 0) + m * T * d * ((4 if r else 0) + 2)
                 for r, b in zip(rT, bits))
     work["decode"] = ("hbm", dec_b * calls)
-    nb = 32
-    pg = 0.0
-    for k0 in range(0, n - 1, nb):
-        jb = min(nb, n - 1 - k0)
-        rem = n - (k0 + jb)
-        pg += 2 * 2.0 * rem * rem * jb
-    work["panel_gemm"] = ("fp32", nc * pg * calls)
+    if not flash:
+        nb = 32
+        pg = 0.0
+        for k0 in range(0, n - 1, nb):
+            jb = min(nb, n - 1 - k0)
+            rem = n - (k0 + jb)
+            pg += 2 * 2.0 * rem * rem * jb
+        work["panel_gemm"] = ("fp32", nc * pg * calls)
     return work
 
 
@@ -100,7 +121,7 @@ def roofline_of(stage, kind, amount, ms, launches):
             "dtype": kind}
 
 
-def cpu_baseline(cache_np, cfg, params0, group, T_sample):
+def cpu_baseline(cache_np, cfg, params0, group, T_sample, method, q, p, iters):
     """fp64 oracle on one cell (keys of layer group 0) timed on the host cores."""
     import numpy as np
     import kvsynth
@@ -111,8 +132,8 @@ def cpu_baseline(cache_np, cfg, params0, group, T_sample):
     X = x.reshape(gl * H, T_sample, d)
     cores = len(os.sched_getaffinity(0))
     t0 = time.perf_counter()
-    sp = opl.spectrum(X)
-    rT = min(params0.r_T, T_sample)
+    sp = opl.spectrum(X, method=method, q=q, p=p, power_iters=iters, seed=0)
+    rT = min(params0.r_T, sp["rT_max"])
     rd = params0.r_d if rT else 0
     out = opl.compress_cell(X, r_T=rT, r_d=rd, bits=params0.bits, group=group, seed=0,
                             factor_bytes=2, spec=sp)
@@ -121,7 +142,7 @@ def cpu_baseline(cache_np, cfg, params0, group, T_sample):
     return {"value": round(cell_bytes / (t1 - t0) / 1e9, 5), "unit": "GB/s", "cores": cores,
             "kind": "oracle",
             "sample": f"one cell (keys, layers 0-{gl - 1}, {H} heads, T={T_sample}, d={d}, bf16, "
-                      f"{cell_bytes / 1e6:.1f} MB): exact spectrum + compress at ranks "
+                      f"{cell_bytes / 1e6:.1f} MB): {method} spectrum + compress at ranks "
                       f"({rT},{rd}) b={params0.bits} + decode, fp64 numpy/LAPACK, "
                       f"{t1 - t0:.1f} s", "seconds": round(t1 - t0, 2)}
 
@@ -129,8 +150,8 @@ def cpu_baseline(cache_np, cfg, params0, group, T_sample):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (cells would shard "
-              "across GPUs with an all-gather of the spectra; see the design notes).", file=sys.stderr)
+        print("bench.py measures one GPU: there is no multi-GPU path (cells would shard "
+              "across GPUs, with an all-gather of the spectra before the allocation).", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
@@ -141,6 +162,9 @@ def main():
 
     cfg = dict(kvsynth.CONFIGS[args.workload])
     gl = cfg.pop("group_layers")
+    method, ratio = WORKLOAD_RUN.get(args.workload, ("exact", 2.0))
+    method = args.method or method
+    ratio = args.ratio or ratio
     log("generating", args.workload)
     t0 = time.perf_counter()
     Knp, Vnp = kvsynth.make_cache(**cfg)
@@ -149,7 +173,8 @@ def main():
     to_dev = (lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)) \
         if cfg["dtype"] == "bf16" else (lambda a: torch.from_numpy(a).to(dev))
     K, V = to_dev(Knp), to_dev(Vnp)
-    codec = CacheCodec(K, V, group_layers=gl, method=args.method, ratio=args.ratio)
+    codec = CacheCodec(K, V, group_layers=gl, method=method, ratio=ratio,
+                       oversample=args.oversample, power_iters=args.power_iters)
     eps2 = codec.calibrate()
     log("eps2", eps2)
     Kout, Vout = torch.empty_like(K), torch.empty_like(V)
@@ -224,7 +249,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "layers": cfg["n_layers"], "kv_heads": cfg["n_heads"],
                    "T": cfg["T"], "head_dim": cfg["d"], "batch": cfg["batch"], "group_layers": gl,
-                   "cells": len(codec.cells), "method": args.method, "ratio": args.ratio,
+                   "cells": len(codec.cells), "method": method, "ratio": ratio,
                    "cache_bytes": cache_bytes},
         "compress_GBps": round(cache_bytes / (np.median(t_comp) * 1e-3) / 1e9, 3),
         "decompress_GBps": round(cache_bytes / (np.median(t_dec) * 1e-3) / 1e9, 3),
@@ -240,7 +265,8 @@ def main():
         log("cpu baseline (oracle) ...")
         Ts = args.cpu_sample_T or cfg["T"]
         out["cpu_baseline"] = cpu_baseline(Knp, dict(cfg, group_layers=gl), codec.params[0],
-                                           codec.group, Ts)
+                                           codec.group, Ts, method, codec.opts.q or codec.rT_max,
+                                           args.oversample, args.power_iters)
     codec.close()
     print(json.dumps(out))
 

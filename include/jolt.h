@@ -45,7 +45,8 @@ typedef void *jolt_stream; /* hipStream_t */
 enum {
   JOLT_OK = 0,
   JOLT_E_INVAL = -1,       /* bad argument (null pointer, out-of-range value) */
-  JOLT_E_UNSUPPORTED = -2, /* valid but not supported (e.g. d not a power of two) */
+  JOLT_E_UNSUPPORTED = -2, /* valid but not supported (d outside {32, 64, 128}, exact
+                              spectrum beyond T = 8192, sketch wider than 1024, not gfx950) */
   JOLT_E_WORKSPACE = -3,   /* workspace or blob buffer too small */
   JOLT_E_BLOB = -4,        /* corrupt or mismatched blob header */
   JOLT_E_HIP = -5,         /* HIP runtime error (message has the HIP error string) */
@@ -66,7 +67,7 @@ typedef struct {
   int32_t n_layers;     /* layers in the group (>= 1) */
   int32_t n_heads;      /* heads per layer (>= 1); m = n_layers * n_heads */
   int32_t T;            /* tokens (>= 1) */
-  int32_t d;            /* features: power of two, 32 <= d <= 256 */
+  int32_t d;            /* features (head dimension): 32, 64 or 128 */
   int32_t reserved;
   int64_t stride_layer;
   int64_t stride_head;
@@ -131,51 +132,81 @@ int jolt_q_cap(int T, double ratio);
 int jolt_spectrum_len(const jolt_cell_desc *desc, const jolt_spectrum_opts *opts,
                       int32_t *n_lam_T, int32_t *rT_max);
 
-/* Device workspace needed by jolt_spectrum / jolt_compress / jolt_decompress
- * for n_cells cells of this shape (opts NULL = exact method). */
+/* Device workspace (bytes) needed by jolt_spectrum and jolt_compress for n_cells
+ * cells of this shape and method (opts NULL = exact method).  The same workspace
+ * also serves jolt_decompress of the blobs those calls write.  Errors: as
+ * jolt_spectrum's validation of desc/opts. */
 int jolt_workspace_size(const jolt_cell_desc *desc, int n_cells, const jolt_spectrum_opts *opts,
                         size_t *bytes);
 
-/* a2-a4: E[n_cells], lam_T[n_cells * n_lam_T], lam_d[n_cells * d] (host arrays).
- * seeds[n_cells] seed the FlashJoLT sketch (may be NULL for JOLT_EXACT).
- * The workspace keeps the factors; a following jolt_compress on the same cells,
- * workspace and options reuses them. */
+/* Device workspace (bytes) jolt_decompress needs for n_cells blobs of shape out_desc
+ * whose largest token rank is max_rT (callers that only decode need no more). */
+int jolt_decompress_workspace_size(const jolt_cell_desc *out_desc, int n_cells, int max_rT,
+                                   size_t *bytes);
+
+/* Token- and feature-mode spectra of every cell (section 4, "Partial Tucker
+ * backbone"; section 5 for JOLT_FLASH).
+ *   X[i]    device pointer to cell i, laid out by desc; read only.
+ *   seeds   host array of n_cells sketch seeds (Philox key of the FlashJoLT Gaussian
+ *           test matrix); required for JOLT_FLASH, ignored (may be NULL) otherwise.
+ *   E       host, n_cells: ||X||_F^2 (fp64 sums).
+ *   lam_T   host, n_cells x n_lam_T (jolt_spectrum_len), descending, clipped at 0:
+ *           exact - all T eigenvalues of X_(2) X_(2)^T;  FlashJoLT - the q_eff Ritz
+ *           values of the sketch followed by the synthetic tail E - sum(captured).
+ *   lam_d   host, n_cells x d: eigenvalues of sum_s X_s^T X_s, descending.
+ *   ws      device workspace of jolt_workspace_size bytes, 256-byte aligned; it keeps
+ *           the token factors, so a following jolt_compress of the same cells with the
+ *           same workspace, options and seeds skips the spectrum.
+ * Synchronises the stream (the outputs are host arrays).  Errors: JOLT_E_INVAL
+ * (null/misaligned pointers), JOLT_E_WORKSPACE, JOLT_E_NONFINITE (a cell holds NaN or
+ * Inf; outputs then undefined), JOLT_E_UNSUPPORTED, JOLT_E_HIP. */
 int jolt_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_cells, const void *const *X,
                   const uint64_t *seeds, const jolt_spectrum_opts *opts, void *ws, size_t ws_bytes,
                   double *E, double *lam_T, double *lam_d, jolt_stream stream);
 
-/* Blob size for one cell: 128-byte header + sections (see the blob format in the
- * oracle / design notes): U_T (T x r_T), U_d (d x r_d), G (m x r_T x r_d) at c bytes,
- * m int8 core exponents, fp16 scales (m*T*d/g), packed codes (m*T*d*b/8). */
+/* Bytes of one cell's blob: a 128-byte header, then 256-byte aligned sections
+ * U_T (T x r_T), U_d (d x r_d), G (m x r_T x r_d) at c bytes per scalar (fp16 or fp32,
+ * row-major), m int8 core exponents (fp16 cores are stored as G_s / 2^e_s), fp16
+ * group scales (m*T*d/g) and the b-bit codes (m*T*d*b/8 bytes, packed LSB first). */
 int jolt_compressed_size(const jolt_cell_desc *desc, const jolt_params *params, size_t *bytes);
 
-/* a6-a9 for every cell: writes blob i (device memory of blob_bytes[i] bytes).
- * opts gives the token-mode method; when the workspace holds the spectrum of the
- * same cells from the preceding jolt_spectrum call it is reused, otherwise the
- * spectrum is recomputed on the device. */
+/* Compresses every cell into its blob (section 4): ST-HOSVD truncation to (r_T, r_d)
+ * with the token mode first, factors rounded to the stored precision, residual
+ * R = X - X~ against the stored factors, randomized Hadamard rotation of every
+ * feature row and b-bit symmetric group quantisation.
+ *   params  host, n_cells; group and factor_dtype must be equal across the call.
+ *   blobs   device pointers (256-byte aligned) to blob_bytes[i] >= jolt_compressed_size
+ *           bytes each; written completely (header included), owned by the caller.
+ * Asynchronous on the stream.  Errors: as jolt_spectrum, plus JOLT_E_WORKSPACE for a
+ * short blob and JOLT_E_INVAL for ranks above jolt_spectrum_len's rT_max. */
 int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_cells, const void *const *X,
                   const jolt_params *params, const jolt_spectrum_opts *opts, void *ws,
                   size_t ws_bytes, void *const *blobs, const size_t *blob_bytes,
                   jolt_stream stream);
 
-/* a10: reconstructs every blob into Xhat[i] laid out by out_desc (its dtype is the
- * output type: JOLT_BF16 rounds to nearest even, JOLT_F32 keeps fp32).  The blobs'
- * shapes must equal out_desc's.  hdr_host (optional, may be NULL) is a host copy of
- * the n_cells 128-byte headers; without it the headers are copied device->host,
- * which synchronises the stream. */
+/* Reconstructs every blob (section 4, decoding): X^ = U_T G_s U_d^T + rotation^-1 of the
+ * dequantised residual, written to Xhat[i] (device, 16-byte aligned) laid out by
+ * out_desc, whose dtype is the output type (JOLT_BF16 rounds to nearest even,
+ * JOLT_F32 keeps fp32).  The blobs' shapes must equal out_desc's.  hdr_host (optional,
+ * may be NULL) is a host copy of the n_cells 128-byte headers; without it the headers
+ * are copied device->host, which synchronises the stream.  ws: at least
+ * jolt_decompress_workspace_size bytes.  Errors: JOLT_E_BLOB for a corrupt or
+ * mismatched header (checked before any device work), JOLT_E_WORKSPACE, JOLT_E_INVAL. */
 int jolt_decompress(jolt_ctx *ctx, int n_cells, const void *const *blobs, const size_t *blob_bytes,
                     const void *hdr_host, const jolt_cell_desc *out_desc, void *const *Xhat,
                     void *ws, size_t ws_bytes, jolt_stream stream);
 
-/* a5 (host only, no device work): eq. (3) through eq. (4).  Outputs per cell
- * r_T, r_d, bits; lambda_star, total bytes and summed model error; *infeasible is
- * 1 when even the cheapest grid point of every cell exceeds the budget (the
- * cheapest allocation is then returned). */
+/* Budgeted allocation (section 4, eq. (1)-(4); host only, no device work): for every
+ * cell the grid point (r_T, r_d, b) minimising eq. (2)'s model error plus lambda times
+ * eq. (1)'s bytes, with lambda found by bisection so that the summed bytes meet the
+ * budget.  Outputs (host, n_cells each) r_T, r_d, bits; lambda_star, total bytes and
+ * summed model error.  *infeasible is 1 when even the cheapest grid point of every cell
+ * exceeds the budget (the cheapest allocation is then returned). */
 int jolt_allocate(const jolt_cell_spectrum *cells, int n_cells, const jolt_alloc_opts *opts,
                   int32_t *r_T, int32_t *r_d, int32_t *bits, double *lambda_star,
                   double *total_bytes, double *model_error, int32_t *infeasible);
 
-/* eq. (2) calibration: eps^2(b) for b = 0, 2, 4, 8 from a round trip of n_samples
+/* Eq. (2) calibration: eps^2(b) for b = 0, 2, 4, 8 from a round trip of n_samples
  * Gaussian samples (rows of d, group g, Philox seed).  n_samples must be a
  * multiple of d.  ws: at least jolt_eps2_workspace_size bytes. */
 int jolt_eps2_workspace_size(int d, int n_samples, size_t *bytes);

@@ -18,7 +18,7 @@ import numpy as np
 __all__ = ["JoltError", "lib", "CellDesc", "SpectrumOpts", "Params", "CellSpectrum", "AllocOpts",
            "JOLT_F32", "JOLT_BF16", "JOLT_EXACT", "JOLT_FLASH", "JOLT_FACTOR_F32",
            "JOLT_FACTOR_F16", "jolt_last_error", "jolt_create", "jolt_destroy", "jolt_q_cap",
-           "jolt_spectrum_len", "jolt_workspace_size", "jolt_spectrum", "jolt_compressed_size",
+           "jolt_spectrum_len", "jolt_workspace_size", "jolt_decompress_workspace_size", "jolt_spectrum", "jolt_compressed_size",
            "jolt_compress", "jolt_decompress", "jolt_allocate", "jolt_eps2_workspace_size",
            "jolt_eps2_calibrate", "jolt_debug_export", "jolt_profile_enable", "jolt_profile_reset",
            "jolt_profile_read", "STAGES", "cell_desc", "LIB_PATH", "HEADER_PATH"]
@@ -83,6 +83,7 @@ _SIGS = {
     "jolt_q_cap": (C.c_int, [C.c_int, _dbl]),
     "jolt_spectrum_len": (C.c_int, [_P(CellDesc), _P(SpectrumOpts), _P(_i32), _P(_i32)]),
     "jolt_workspace_size": (C.c_int, [_P(CellDesc), C.c_int, _P(SpectrumOpts), _P(_sz)]),
+    "jolt_decompress_workspace_size": (C.c_int, [_P(CellDesc), C.c_int, C.c_int, _P(_sz)]),
     "jolt_spectrum": (C.c_int, [_vp, _P(CellDesc), C.c_int, _P(_vp), _P(C.c_uint64),
                                 _P(SpectrumOpts), _vp, _sz, _P(_dbl), _P(_dbl), _P(_dbl), _vp]),
     "jolt_compressed_size": (C.c_int, [_P(CellDesc), _P(Params), _P(_sz)]),
@@ -178,6 +179,12 @@ def jolt_spectrum_len(desc: CellDesc, opts=None):
 def jolt_workspace_size(desc: CellDesc, n_cells: int, opts=None) -> int:
     b = _sz()
     _check(lib.jolt_workspace_size(C.byref(desc), n_cells, _opts(opts), C.byref(b)))
+    return b.value
+
+
+def jolt_decompress_workspace_size(out_desc: CellDesc, n_cells: int, max_rT: int) -> int:
+    b = _sz()
+    _check(lib.jolt_decompress_workspace_size(C.byref(out_desc), n_cells, max_rT, C.byref(b)))
     return b.value
 
 

@@ -20,7 +20,7 @@ import torch
 from . import (JOLT_BF16, JOLT_EXACT, JOLT_F32, JOLT_FACTOR_F16, JOLT_FACTOR_F32, JOLT_FLASH,
                HEADER_BYTES, Params, SpectrumOpts, cell_desc, jolt_allocate, jolt_compress,
                jolt_compressed_size, jolt_create, jolt_decompress, jolt_destroy,
-               jolt_eps2_calibrate, jolt_eps2_workspace_size, jolt_spectrum, jolt_spectrum_len,
+               jolt_eps2_calibrate, jolt_eps2_workspace_size, jolt_q_cap, jolt_spectrum, jolt_spectrum_len,
                jolt_workspace_size)
 
 
@@ -81,6 +81,9 @@ class CacheCodec:
         self.ws = torch.empty(jolt_workspace_size(self.desc, self.chunk, self.opts), dtype=torch.uint8,
                               device=K.device)
         self.n_lam, self.rT_max = jolt_spectrum_len(self.desc, self.opts)
+        # FlashJoLT sketch width l = min(q + p, T, m d) (section 5); 0 for the exact path
+        qq = q or (jolt_q_cap(T, ratio) if self.method == JOLT_FLASH else 0)
+        self.ell = min(qq + oversample, T, group_layers * H * d) if self.method == JOLT_FLASH else 0
         self.eps2 = None
         # blob arena: at most the whole budget plus per-blob headers and alignment
         arena = int(self.cache_bytes / ratio) + len(self.cells) * (HEADER_BYTES + 8 * 256) + (1 << 20)

@@ -5,9 +5,9 @@
 // counter (c, j, 0, 2) and key = seed; Box-Muller runs in fp64 and is rounded once to bf16.
 // CholeskyQR2: G = Y^T Y accumulated in fp64 (split over row chunks, partials summed in a
 // fixed order), G = L L^T, Q = Y L^-T, applied twice.  fp64 keeps the Gram usable for
-// condition numbers up to ~1e7, which a power-iterated sketch of a decaying spectrum
-// reaches.  Directions whose Cholesky pivot falls below 1e-14 of the largest diagonal
-// are treated as numerically absent (pivot clamped), so rank-deficient sketches stay finite.
+// condition numbers up to ~1e7.  Directions whose Cholesky pivot falls below 1e-14 of
+// the largest diagonal are treated as numerically absent (pivot clamped), so
+// rank-deficient sketches stay finite.
 #include "common.h"
 #include "kernels.h"
 
@@ -93,57 +93,197 @@ __global__ void k_gram64_reduce(Gram64Args a) {
   }
 }
 
-// one workgroup per cell: G = L L^T (lower, in place), M = L^-1, Rinv = M^T (fp32, l x ldr)
-constexpr int CT = 1024;
-__global__ void __launch_bounds__(CT) k_chol_inv(CholArgs a) {
+// Blocked Cholesky G = L L^T and triangular inverse M = L^-1 in fp64, 64 x 64 tiles.
+// Per block column kb: k_chol_diag factors the diagonal tile in LDS and inverts it
+// (D_kb = L_kb,kb^-1), k_chol_panel forms L_I,kb = G_I,kb D_kb^T below it and
+// k_chol_update subtracts L_I,kb L_J,kb^T from the trailing lower tiles.  The inverse
+// is then built one block row at a time: M_IJ = -D_I sum_{J<=K<I} L_IK M_KJ.
+// Pivots below 1e-14 of the largest diagonal entry of G are raised to that floor.
+constexpr int CB = 64, CLD = CB + 1;
+
+JOLT_DEV void tile_load(double (*t)[CLD], const double *A, int l, int r0, int c0) {
+  for (int q = threadIdx.x; q < CB * CB; q += 256) {
+    const int i = q / CB, j = q % CB, r = r0 + i, c = c0 + j;
+    t[i][j] = (r < l && c < l) ? A[(int64_t)r * l + c] : 0.0;
+  }
+}
+
+__global__ void __launch_bounds__(256) k_chol_diag(CholArgs a, int kb) {
   const int cell = blockIdx.x, l = a.l, tid = threadIdx.x;
-  const int64_t ll = (int64_t)l * l;
-  double *G = a.G + (int64_t)cell * ll;
-  double *M = a.M + (int64_t)cell * ll;
+  double *G = a.G + (int64_t)cell * l * l;
+  double *D = a.Dinv + ((int64_t)cell * a.nbk + kb) * CB * CB;
+  double *M = a.M + (int64_t)cell * l * l;
+  __shared__ double t[CB][CLD], inv[CB][CLD];
+  __shared__ double part[4][CB];
+  __shared__ double red[4], sdmax;
+  if (kb == 0) {                       // largest diagonal entry of the untouched Gram
+    double mx = 0.0;
+    for (int i = tid; i < l; i += 256) mx = fmax(mx, G[(int64_t)i * l + i]);
+    for (int o = 32; o >= 1; o >>= 1) mx = fmax(mx, __shfl_xor(mx, o, 64));
+    if ((tid & 63) == 0) red[tid >> 6] = mx;
+    __syncthreads();
+    if (tid == 0) {
+      sdmax = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
+      a.dmax[cell] = sdmax;
+    }
+  } else if (tid == 0) {
+    sdmax = a.dmax[cell];                // written by the kb = 0 launch
+  }
+  const int o = kb * CB, nb = min(CB, l - o);
+  tile_load(t, G, l, o, o);
+  __syncthreads();
+  if (tid < CB && tid >= nb) t[tid][tid] = 1.0;   // identity on the padding
+  const double floor_piv = fmax(1e-14 * sdmax, 1e-300);
+  __syncthreads();
+  for (int j = 0; j < CB; ++j) {
+    const double piv = sqrt(fmax(t[j][j], j < nb ? floor_piv : 1.0));
+    __syncthreads();
+    if (tid < CB) {
+      if (tid > j) t[tid][j] /= piv;
+      else if (tid == j) t[j][j] = piv;
+    }
+    __syncthreads();
+    {
+      const int i = tid >> 2, k0 = (tid & 3) * 16;
+      if (i > j) {
+        const double lij = t[i][j];
+#pragma unroll 4
+        for (int k = k0; k < k0 + 16; ++k)
+          if (k > j && k <= i) t[i][k] = fma(-lij, t[k][j], t[i][k]);
+      }
+    }
+    __syncthreads();
+  }
+  // inverse of the lower-triangular tile, one row at a time: column j < i of row i is
+  // -(sum_{j<=k<i} t[i][k] inv[k][j]) / t[i][i], the k sum split four ways
+  if (tid < CB)
+    for (int i = 0; i < CB; ++i) inv[i][tid] = (i == tid) ? 1.0 / t[i][i] : 0.0;
+  __syncthreads();
+  const int j = tid & 63, w = tid >> 6;
+  for (int i = 1; i < CB; ++i) {
+    double s = 0.0;
+    if (j < i) {
+      const int len = i - j, k0 = j + (len * w) / 4, k1 = j + (len * (w + 1)) / 4;
+      for (int k = k0; k < k1; ++k) s = fma(t[i][k], inv[k][j], s);
+    }
+    part[w][j] = s;
+    __syncthreads();
+    if (w == 0 && j < i) inv[i][j] = -(part[0][j] + part[1][j] + part[2][j] + part[3][j]) / t[i][i];
+    __syncthreads();
+  }
+  for (int q = tid; q < CB * CB; q += 256) {
+    const int r = q / CB, c = q % CB;
+    D[q] = inv[r][c];
+    if (r < nb && c < nb) {
+      if (c <= r) G[(int64_t)(o + r) * l + o + c] = t[r][c];
+      M[(int64_t)(o + r) * l + o + c] = inv[r][c];
+    }
+  }
+}
+
+// 4 x 4 outputs per thread of a 64 x 64 tile: acc[r][c] += sum_k A[r][k] B[c][k]
+JOLT_DEV void tile_mma_nt(double (&acc)[4][4], const double (*A)[CLD], const double (*B)[CLD], int k0, int k1) {
+  const int r0 = (threadIdx.x >> 4) * 4, c0 = (threadIdx.x & 15) * 4;
+  for (int k = k0; k < k1; ++k) {
+    double av[4], bv[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { av[i] = A[r0 + i][k]; bv[i] = B[c0 + i][k]; }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[i][c] = fma(av[i], bv[c], acc[i][c]);
+  }
+}
+
+__global__ void __launch_bounds__(256) k_chol_panel(CholArgs a, int kb) {
+  const int cell = blockIdx.y, I = kb + 1 + blockIdx.x, l = a.l;
+  double *G = a.G + (int64_t)cell * l * l;
+  const double *D = a.Dinv + ((int64_t)cell * a.nbk + kb) * CB * CB;
+  __shared__ double ta[CB][CLD], td[CB][CLD];
+  tile_load(ta, G, l, I * CB, kb * CB);
+  for (int q = threadIdx.x; q < CB * CB; q += 256) td[q / CB][q % CB] = D[q];
+  __syncthreads();
+  double acc[4][4] = {};
+  tile_mma_nt(acc, ta, td, 0, CB);             // L_I,kb = G_I,kb D^T
+  const int r0 = (threadIdx.x >> 4) * 4, c0 = (threadIdx.x & 15) * 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int r = I * CB + r0 + i, cc = kb * CB + c0 + c;
+      if (r < l && cc < l) G[(int64_t)r * l + cc] = acc[i][c];
+    }
+}
+
+__global__ void __launch_bounds__(256) k_chol_update(CholArgs a, int kb) {
+  const int cell = blockIdx.y, l = a.l;
+  int t = blockIdx.x, ti = 0;
+  while ((ti + 1) * (ti + 2) / 2 <= t) ++ti;
+  const int I = kb + 1 + ti, J = kb + 1 + (t - ti * (ti + 1) / 2);
+  double *G = a.G + (int64_t)cell * l * l;
+  __shared__ double ta[CB][CLD], tb[CB][CLD];
+  tile_load(ta, G, l, I * CB, kb * CB);
+  tile_load(tb, G, l, J * CB, kb * CB);
+  __syncthreads();
+  double acc[4][4] = {};
+  tile_mma_nt(acc, ta, tb, 0, CB);
+  const int r0 = (threadIdx.x >> 4) * 4, c0 = (threadIdx.x & 15) * 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int r = I * CB + r0 + i, cc = J * CB + c0 + c;
+      if (r < l && cc < l) G[(int64_t)r * l + cc] -= acc[i][c];
+    }
+}
+
+// block row I of M = L^-1: M_IJ = -D_I sum_{K=J}^{I-1} L_IK M_KJ for every J < I
+__global__ void __launch_bounds__(256) k_chol_inv_row(CholArgs a, int I) {
+  const int cell = blockIdx.y, J = blockIdx.x, l = a.l;
+  const double *G = a.G + (int64_t)cell * l * l;
+  double *M = a.M + (int64_t)cell * l * l;
+  const double *D = a.Dinv + ((int64_t)cell * a.nbk + I) * CB * CB;
+  __shared__ double ta[CB][CLD], tb[CB][CLD];
+  const int r0 = (threadIdx.x >> 4) * 4, c0 = (threadIdx.x & 15) * 4;
+  double acc[4][4] = {};
+  for (int K = J; K < I; ++K) {
+    __syncthreads();
+    tile_load(ta, G, l, I * CB, K * CB);                  // L_IK
+    for (int q = threadIdx.x; q < CB * CB; q += 256) {    // M_KJ, transposed: tb[c][k] = M[k][c]
+      const int k = q / CB, c = q % CB, r = K * CB + k, cc = J * CB + c;
+      tb[c][k] = (r < l && cc < l) ? M[(int64_t)r * l + cc] : 0.0;
+    }
+    __syncthreads();
+    tile_mma_nt(acc, ta, tb, 0, CB);
+  }
+  __syncthreads();
+  // S = acc -> tb (transposed, tb[c][k] = S[k][c]); D_I -> ta
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) tb[c0 + c][r0 + i] = acc[i][c];
+  for (int q = threadIdx.x; q < CB * CB; q += 256) ta[q / CB][q % CB] = D[q];
+  __syncthreads();
+  double out[4][4] = {};
+  tile_mma_nt(out, ta, tb, 0, CB);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int r = I * CB + r0 + i, cc = J * CB + c0 + c;
+      if (r < l && cc < l) M[(int64_t)r * l + cc] = -out[i][c];
+    }
+}
+
+// Rinv = M^T in fp32 (l x ldr), zero above the diagonal of M and in the padding columns
+__global__ void k_chol_rinv(CholArgs a) {
+  const int cell = blockIdx.y, l = a.l;
+  const double *M = a.M + (int64_t)cell * l * l;
   float *R = a.Rinv + (int64_t)cell * l * a.ldr;
-  __shared__ double smax;
-  __shared__ double red[CT / 64];
-  double mx = 0.0;
-  for (int i = tid; i < l; i += CT) mx = fmax(mx, G[(int64_t)i * l + i]);
-  for (int o = 32; o >= 1; o >>= 1) mx = fmax(mx, __shfl_xor(mx, o, 64));
-  if ((tid & 63) == 0) red[tid >> 6] = mx;
-  __syncthreads();
-  if (tid == 0) {
-    double m = 0.0;
-    for (int w = 0; w < CT / 64; ++w) m = fmax(m, red[w]);
-    smax = m;
-  }
-  __syncthreads();
-  const double floor_piv = fmax(1e-14 * smax, 1e-300);
-  for (int k = 0; k < l; ++k) {
-    double piv = G[(int64_t)k * l + k];
-    piv = sqrt(fmax(piv, floor_piv));
-    __syncthreads();
-    for (int i = k + 1 + tid; i < l; i += CT) G[(int64_t)i * l + k] /= piv;
-    if (tid == 0) G[(int64_t)k * l + k] = piv;
-    __syncthreads();
-    // trailing update of the lower triangle, one row per thread: G[i][j] -= L[i][k] L[j][k]
-    for (int gi = k + 1 + tid; gi < l; gi += CT) {
-      const double lik = G[(int64_t)gi * l + k];
-      double *row = G + (int64_t)gi * l;
-      for (int gj = k + 1; gj <= gi; ++gj) row[gj] = fma(-lik, G[(int64_t)gj * l + k], row[gj]);
-    }
-    __syncthreads();
-  }
-  // M = L^-1 column by column (thread per column, forward substitution down the column)
-  for (int j = tid; j < l; j += CT) {
-    for (int i = 0; i < j; ++i) M[(int64_t)i * l + j] = 0.0;
-    M[(int64_t)j * l + j] = 1.0 / G[(int64_t)j * l + j];
-    for (int i = j + 1; i < l; ++i) {
-      double s = 0.0;
-      for (int k = j; k < i; ++k) s = fma(G[(int64_t)i * l + k], M[(int64_t)k * l + j], s);
-      M[(int64_t)i * l + j] = -s / G[(int64_t)i * l + i];
-    }
-  }
-  __syncthreads();
-  for (int64_t q = tid; q < (int64_t)l * a.ldr; q += CT) {
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < (int64_t)l * a.ldr;
+       q += (int64_t)gridDim.x * blockDim.x) {
     const int r = (int)(q / a.ldr), c = (int)(q % a.ldr);
-    R[q] = (c < l) ? (float)M[(int64_t)c * l + r] : 0.f;   // Rinv[r][c] = M[c][r]
+    R[q] = (c < l && c >= r) ? (float)M[(int64_t)c * l + r] : 0.f;
   }
 }
 
@@ -169,7 +309,23 @@ hipError_t launch_gram64(const Gram64Args &a, int n_cells, hipStream_t st) {
   return hipGetLastError();
 }
 
+int chol_blocks(int l) { return (l + CB - 1) / CB; }
+
 hipError_t launch_chol_inv(const CholArgs &a, int n_cells, hipStream_t st) {
-  hipLaunchKernelGGL(k_chol_inv, dim3(n_cells), dim3(CT), 0, st, a);
+  const int nbk = a.nbk;
+  if (nbk != chol_blocks(a.l)) return hipErrorInvalidValue;
+  for (int kb = 0; kb < nbk; ++kb) {
+    hipLaunchKernelGGL(k_chol_diag, dim3(n_cells), dim3(256), 0, st, a, kb);
+    const int below = nbk - kb - 1;
+    if (below > 0) {
+      hipLaunchKernelGGL(k_chol_panel, dim3(below, n_cells), dim3(256), 0, st, a, kb);
+      hipLaunchKernelGGL(k_chol_update, dim3(below * (below + 1) / 2, n_cells), dim3(256), 0, st, a, kb);
+    }
+  }
+  for (int I = 1; I < nbk; ++I)
+    hipLaunchKernelGGL(k_chol_inv_row, dim3(I, n_cells), dim3(256), 0, st, a, I);
+  const int64_t tot = (int64_t)a.l * a.ldr;
+  hipLaunchKernelGGL(k_chol_rinv, dim3((unsigned)std::min<int64_t>((tot + 255) / 256, 1024), n_cells),
+                     dim3(256), 0, st, a);
   return hipGetLastError();
 }

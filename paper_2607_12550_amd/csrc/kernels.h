@@ -221,9 +221,12 @@ int gram64_tile();
 hipError_t launch_gram64(const Gram64Args &a, int n_cells, hipStream_t st);
 
 struct CholArgs {
-  double *G;                // [cell][l][l] in: Gram (lower); out: Cholesky factor L
-  double *M;                // [cell][l][l] out: L^-1
-  float *Rinv;              // [cell][l][ldr] out: L^-T (upper triangular)
-  int32_t l, ldr;
+  double *G;                // [cell][l][l] in: Gram (lower); out: Cholesky factor L (lower)
+  double *M;                // [cell][l][l] out: L^-1 (lower)
+  float *Rinv;              // [cell][l][ldr] out: L^-T (upper triangular), zero padding
+  double *Dinv;             // [cell][nbk][64][64] scratch: inverses of the diagonal tiles
+  double *dmax;             // [cell] scratch: largest diagonal entry of G
+  int32_t l, ldr, nbk, pad; // nbk = chol_blocks(l)
 };
+int chol_blocks(int l);
 hipError_t launch_chol_inv(const CholArgs &a, int n_cells, hipStream_t st);

@@ -72,7 +72,7 @@ struct Ws {
   float *Zsk = nullptr, *Qz = nullptr;    // N x ldl: power-iteration basis and scratch
   float *Bsk = nullptr;                   // l x N: B = Q^T X_(2)
   float *Wsk = nullptr;                   // l x q: Ritz vectors of B B^T
-  double *g64p = nullptr, *g64 = nullptr, *chM = nullptr;
+  double *g64p = nullptr, *g64 = nullptr, *chM = nullptr, *chD = nullptr, *chMax = nullptr;
   float *Rinv = nullptr;                  // l x ldl
   // eps2
   double *eps_part = nullptr;
@@ -142,6 +142,8 @@ void plan(Carver &cv, Ws &w, const SpecShape &sh, int nc) {
     w.g64p = cv.take<double>((size_t)nc * w.g64_chunks * l * l);
     w.g64 = cv.take<double>((size_t)nc * l * l);
     w.chM = cv.take<double>((size_t)nc * l * l);
+    w.chD = cv.take<double>((size_t)nc * chol_blocks(l) * 64 * 64);
+    w.chMax = cv.take<double>(nc);
     w.Rinv = cv.take<float>((size_t)nc * l * w.ldl);
   }
   w.U = cv.take<float>((size_t)nc * T * std::max(w.kmaxT, 1));
@@ -149,6 +151,18 @@ void plan(Carver &cv, Ws &w, const SpecShape &sh, int nc) {
   w.G = cv.take<float>((size_t)nc * m * std::max(w.kmaxT, 1) * d);
   w.W = cv.take<float>((size_t)nc * m * std::max(w.kmaxT, 1) * d);
   w.Xt = cv.take<float>((size_t)nc * m * T * d);
+}
+
+// decode-only areas: problem table, per-cell records, rotation signs, W_s = G_s U_d^T and X~
+void plan_decode(Carver &cv, Ws &w, int m, int T, int d, int nc, int kmax) {
+  w.tab_n = 64 + 2 * (size_t)nc * m;
+  w.tab = cv.take<GemmProblem>(w.tab_n);
+  w.dcell = cv.take<DecodeCell>(nc);
+  w.seeds = cv.take<uint64_t>(nc);
+  w.signs = cv.take<float>((size_t)nc * d);
+  w.kmaxT = std::max(kmax, 1);
+  w.W = cv.take<float>((size_t)nc * m * w.kmaxT * d);
+  w.Xt = kmax ? cv.take<float>((size_t)nc * m * T * d) : nullptr;
 }
 
 int dtype_gt(int dt) { return dt == JOLT_BF16 ? GT_BF16 : GT_F32; }
@@ -360,6 +374,19 @@ extern "C" int jolt_workspace_size(const jolt_cell_desc *desc, int n_cells,
   return JOLT_OK;
 }
 
+extern "C" int jolt_decompress_workspace_size(const jolt_cell_desc *out_desc, int n_cells, int max_rT,
+                                              size_t *bytes) {
+  int rc = validate_desc(out_desc);
+  if (rc) return rc;
+  if (n_cells < 1 || max_rT < 0 || !bytes)
+    return jolt_fail(JOLT_E_INVAL, "jolt_decompress_workspace_size: n_cells >= 1, max_rT >= 0 and bytes required");
+  Carver cv(nullptr);
+  Ws w;
+  plan_decode(cv, w, out_desc->n_layers * out_desc->n_heads, out_desc->T, out_desc->d, n_cells, max_rT);
+  *bytes = cv.off + 256;
+  return JOLT_OK;
+}
+
 static int check_common(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_cells, const void *const *X,
                         void *ws) {
   if (!ctx) return jolt_fail(JOLT_E_INVAL, "ctx is null");
@@ -396,7 +423,7 @@ int orth(Run &R, const SpecShape &sh, int nc, float *buf, float *tmp, int rows) 
     g.rows = rows; g.l = l; g.chunk_rows = kG64Rows; g.chunks = (rows + kG64Rows - 1) / kG64Rows;
     g.partial = R.w.g64p; g.G = R.w.g64;
     HIP_OK(launch_gram64(g, nc, R.st));
-    CholArgs ca{R.w.g64, R.w.chM, R.w.Rinv, l, ldl};
+    CholArgs ca{R.w.g64, R.w.chM, R.w.Rinv, R.w.chD, R.w.chMax, l, ldl, chol_blocks(l), 0};
     HIP_OK(launch_chol_inv(ca, nc, R.st));
     std::vector<GemmProblem> P(nc);
     for (int c = 0; c < nc; ++c) {
@@ -858,24 +885,15 @@ extern "C" int jolt_decompress(jolt_ctx *ctx, int n_cells, const void *const *bl
       return jolt_fail(JOLT_E_BLOB, "blob %d has invalid ranks or group", c);
     kmax = std::max(kmax, (int)b.rT);
   }
-  // workspace: plan with the exact-method shape (its X~ / W areas cover decoding)
-  SpecShape sh;
-  jolt_spectrum_opts eo{JOLT_EXACT, 0, 0.0, 0, 0};
-  jolt_cell_desc dd = *out;
-  rc = resolve_spectrum(&dd, &eo, &sh);
-  if (rc) {  // very long contexts: size the decode areas directly
-    sh.m = m; sh.T = T; sh.d = d; sh.N = N; sh.method = JOLT_FLASH; sh.ell = 1; sh.q = 1;
-    sh.rT_max = std::min(T, N);
-  }
   Run R{ctx, st, {}};
   {
     Carver cv(nullptr);
     Ws w;
-    plan(cv, w, sh, n_cells);
+    plan_decode(cv, w, m, T, d, n_cells, kmax);
     if (ws_bytes < cv.off) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, cv.off);
   }
   Carver cv(ws);
-  plan(cv, R.w, sh, n_cells);
+  plan_decode(cv, R.w, m, T, d, n_cells, kmax);
   std::vector<uint64_t> seeds(n_cells);
   for (int c = 0; c < n_cells; ++c) seeds[c] = bi[c].seed;
   rc = upload_seeds_and_signs(R, seeds.data(), n_cells, d);

@@ -78,6 +78,33 @@ def test_flash_spectrum_matches_oracle(dtype, iters):
         np.testing.assert_allclose(lamT[c].sum(), Er, rtol=1e-9)  # captured + tail = E
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_flash_wide_sketch_matches_oracle(dtype):
+    """l = 200 spans four 64-wide Cholesky blocks (the last one ragged)."""
+    cells = [kv_cell(700, 4, 64, seed=7), kv_cell(700, 4, 64, seed=8, alpha=0.7, tensor=1)]
+    xs, ex, desc = device_cells(cells, dtype)
+    o = flash_opts(190, 10, 1)
+    ws = workspace(desc, 2, o)
+    note("jolt_spectrum flash l=200", dtype)
+    E, lamT, _ = J.jolt_spectrum(ctx(), desc, xs, [11, 12], o, ws)
+    tol = 1e-5 if dtype == "f32" else 1e-3
+    for c in range(2):
+        lam, _, _ = otk.token_spectrum_flash(ex[c], q=190, p=10, power_iters=1, seed=11 + c)
+        np.testing.assert_allclose(lamT[c, :190], lam[:190], rtol=0, atol=tol * lam[0])
+        assert abs(lamT[c, 190] - lam[190]) <= tol * E[c]
+    p = [J.Params(160, 48, 2, 64, J.JOLT_FACTOR_F32, 0, 11), J.Params(96, 64, 4, 64, J.JOLT_FACTOR_F32, 0, 12)]
+    blobs, _ = compress(xs, desc, p, o, ws=ws)
+    for c in range(2):
+        U = export(0, c, (700, p[c].r_T)).cpu().numpy().astype(np.float64)
+        np.testing.assert_allclose(U.T @ U, np.eye(p[c].r_T), atol=1e-5)
+        ref = opl.compress_cell(ex[c], r_T=p[c].r_T, r_d=p[c].r_d, bits=p[c].bits, group=64,
+                                seed=11 + c, factor_bytes=4, method="flash", q=190, p=10,
+                                power_iters=1)
+        Xt = export(2, c, (4, 700, 64)).cpu().numpy().astype(np.float64)
+        eb_gpu, eb_ref = opl.rel_error(ex[c], Xt), opl.rel_error(ex[c], ref["Xtilde"])
+        assert abs(eb_gpu / eb_ref - 1) < tol, (c, eb_gpu, eb_ref)
+
+
 @pytest.mark.parametrize("dtype,fdt", [("f32", J.JOLT_FACTOR_F32), ("bf16", J.JOLT_FACTOR_F16)])
 def test_flash_compress_matches_oracle(dtype, fdt):
     """Fixed ranks (24, 32), 4-bit residual, group 64, one power iteration."""

@@ -134,3 +134,19 @@ def test_blob_header_rejected_when_corrupt():
                                hdr.ctypes.data, C.byref(desc), (C.c_void_p * 1)(256), C.c_void_p(256),
                                1 << 30, None)
     assert rc == -4
+
+
+def test_decode_workspace_fits_inside_the_compress_workspace():
+    """A decode-only caller needs less than the compress workspace of the same cells."""
+    for T, opts in [(4096, None), (32768, J.SpectrumOpts(J.JOLT_FLASH, 0, 2.0, 10, 1))]:
+        desc = J.cell_desc(dtype=J.JOLT_BF16, n_layers=4, n_heads=8, T=T, d=128,
+                           stride_layer=8 * T * 128, stride_head=T * 128, stride_token=128)
+        _, rT_max = J.jolt_spectrum_len(desc, opts)
+        for n in (1, 16):
+            dec = J.jolt_decompress_workspace_size(desc, n, rT_max)
+            assert 0 < dec <= J.jolt_workspace_size(desc, n, opts)
+            # the reconstruction buffer dominates: m*T*d fp32 per cell
+            assert dec >= n * 32 * T * 128 * 4
+        assert J.jolt_decompress_workspace_size(desc, 2, 0) < 1 << 20   # residual-only blobs
+    with pytest.raises(J.JoltError):
+        J.jolt_decompress_workspace_size(desc, 0, 8)
