@@ -55,6 +55,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-T", type=int, default=0,
                     help="tokens of the oracle sample cell (0 = the workload's T)")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="before the run, one device-to-device copy of this many MiB: the "
+                         "reference dispatch for scaling HBM traffic counters")
     return ap.parse_args()
 
 
@@ -121,30 +124,42 @@ def roofline_of(stage, kind, amount, ms, launches):
             "dtype": kind}
 
 
-def cpu_baseline(cache_np, cfg, params0, group, T_sample, method, q, p, iters):
-    """fp64 oracle on one cell (keys of layer group 0) timed on the host cores."""
+def cpu_baseline(K_np, V_np, cfg, params, group, T_sample, method, q, p, iters,
+                 min_seconds=10.0, max_cells=4):
+    """fp64 oracle on whole cells (keys, then values, of layer groups 0, 1, ...) timed on
+    the host cores until at least min_seconds of work (at most max_cells cells)."""
     import numpy as np
     import kvsynth
     from oracle import pipeline as opl
     gl, H, d = cfg["group_layers"], cfg["n_heads"], cfg["d"]
-    K = cache_np
-    x = kvsynth.bf16_bits_to_f32(K[:gl, 0, :, :T_sample, :]).astype(np.float64)
-    X = x.reshape(gl * H, T_sample, d)
+    n_groups = cfg["n_layers"] // gl
     cores = len(os.sched_getaffinity(0))
-    t0 = time.perf_counter()
-    sp = opl.spectrum(X, method=method, q=q, p=p, power_iters=iters, seed=0)
-    rT = min(params0.r_T, sp["rT_max"])
-    rd = params0.r_d if rT else 0
-    out = opl.compress_cell(X, r_T=rT, r_d=rd, bits=params0.bits, group=group, seed=0,
-                            factor_bytes=2, spec=sp)
-    t1 = time.perf_counter()
-    cell_bytes = X.size * 2
-    return {"value": round(cell_bytes / (t1 - t0) / 1e9, 5), "unit": "GB/s", "cores": cores,
+    done, nbytes, t_all = [], 0, 0.0
+    for i in range(max_cells):
+        g, tensor = i // 2, i % 2
+        if g >= n_groups:
+            break
+        src = (K_np, V_np)[tensor]
+        x = kvsynth.bf16_bits_to_f32(src[g * gl:(g + 1) * gl, 0, :, :T_sample, :]).astype(np.float64)
+        X = x.reshape(gl * H, T_sample, d)
+        pc = params[(tensor * n_groups + g) * cfg["batch"]]   # codec cell order: tensor, group, batch
+        t0 = time.perf_counter()
+        sp = opl.spectrum(X, method=method, q=q, p=p, power_iters=iters, seed=0)
+        rT = min(pc.r_T, sp["rT_max"])
+        rd = pc.r_d if rT else 0
+        opl.compress_cell(X, r_T=rT, r_d=rd, bits=pc.bits, group=group, seed=0,
+                          factor_bytes=2, spec=sp)
+        t_all += time.perf_counter() - t0
+        nbytes += X.size * 2
+        done.append(f"{'KV'[tensor]}{g}:({rT},{rd},{pc.bits})")
+        if t_all >= min_seconds:
+            break
+    return {"value": round(nbytes / t_all / 1e9, 5), "unit": "GB/s", "cores": cores,
             "kind": "oracle",
-            "sample": f"one cell (keys, layers 0-{gl - 1}, {H} heads, T={T_sample}, d={d}, bf16, "
-                      f"{cell_bytes / 1e6:.1f} MB): {method} spectrum + compress at ranks "
-                      f"({rT},{rd}) b={params0.bits} + decode, fp64 numpy/LAPACK, "
-                      f"{t1 - t0:.1f} s", "seconds": round(t1 - t0, 2)}
+            "sample": f"{len(done)} whole cells ({gl} layers x {H} heads, T={T_sample}, d={d}, bf16, "
+                      f"{nbytes / 1e6:.1f} MB) {' '.join(done)}: {method} spectrum + compress at the "
+                      f"allocated ranks/bits + decode, fp64 numpy/LAPACK, {t_all:.1f} s",
+            "seconds": round(t_all, 2)}
 
 
 def main():
@@ -173,6 +188,14 @@ def main():
     to_dev = (lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)) \
         if cfg["dtype"] == "bf16" else (lambda a: torch.from_numpy(a).to(dev))
     K, V = to_dev(Knp), to_dev(Vnp)
+    if args.calib_copy_mib:
+        src = torch.ones(args.calib_copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy: {args.calib_copy_mib} MiB read + written")
+        del src, dst
     codec = CacheCodec(K, V, group_layers=gl, method=method, ratio=ratio,
                        oversample=args.oversample, power_iters=args.power_iters)
     eps2 = codec.calibrate()
@@ -264,7 +287,7 @@ def main():
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         Ts = args.cpu_sample_T or cfg["T"]
-        out["cpu_baseline"] = cpu_baseline(Knp, dict(cfg, group_layers=gl), codec.params[0],
+        out["cpu_baseline"] = cpu_baseline(Knp, Vnp, dict(cfg, group_layers=gl), codec.params,
                                            codec.group, Ts, method, codec.opts.q or codec.rT_max,
                                            args.oversample, args.power_iters)
     codec.close()
