@@ -226,33 +226,49 @@ __global__ void __launch_bounds__(NT) k_gemm(const GemmProblem *__restrict__ pro
 
   float alpha = P.alpha;
   if (P.alpha_exp2) alpha = ldexpf(alpha, (int)*P.alpha_exp2);
-  // epilogue: acc[i][j][q] -> C[m0 + wm*64 + i*32 + 8*(q/4) + 4*lh + q%4][n0 + wn*64 + j*32 + lr];
-  // the beta term's loads are all issued before any store
+  // Epilogue through LDS, 32 rows at a time (one MFMA row block of one wave row per round),
+  // so that C is read (beta != 0) and written as float4 rows: acc[i][j][q] is the output at
+  // row wm*64 + i*32 + 8*(q/4) + 4*lh + q%4, column wn*64 + j*32 + lr of the tile.
+  float *cs = reinterpret_cast<float *>(&sm);
+  constexpr int CLD = BN + 4;
+  static_assert(32 * CLD * sizeof(float) <= sizeof(Smem<MODE>), "epilogue tile exceeds LDS");
   const bool use_beta = P.beta != 0.f;
+  const bool vec = ((reinterpret_cast<uintptr_t>(P.C) & 15) == 0) && (P.ldc % 4 == 0);
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int h = 0; h < 4; ++h) {
+    __syncthreads();
+    if (wm == (h >> 1)) {
+      const int i = h & 1;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int col = n0 + wn * 64 + j * 32 + lr;
-      const bool cok = col < P.N;
-      float old[16];
-      if (use_beta) {
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
-        for (int q = 0; q < 16; ++q) {
-          const int row = m0 + wm * 64 + i * 32 + 8 * (q >> 2) + 4 * lh + (q & 3);
-          old[q] = (cok && row < P.M) ? P.C[(int64_t)row * P.ldc + col] : 0.f;
+        for (int q = 0; q < 16; ++q)
+          cs[(8 * (q >> 2) + 4 * lh + (q & 3)) * CLD + wn * 64 + j * 32 + lr] = acc[i][j][q];
+    }
+    __syncthreads();
+    // 32 rows x 32 float4 chunks, 4 per thread
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = tid + u * NT, rr = idx >> 5, cc = (idx & 31) * 4;
+      const int row = m0 + h * 32 + rr, col = n0 + cc;
+      if (row >= P.M || col >= P.N) continue;
+      const float4 a4 = *reinterpret_cast<const float4 *>(&cs[rr * CLD + cc]);
+      float v[4] = {alpha * a4.x, alpha * a4.y, alpha * a4.z, alpha * a4.w};
+      float *dst = P.C + (int64_t)row * P.ldc + col;
+      if (vec && col + 4 <= P.N) {
+        if (use_beta) {
+          const float4 o4 = *reinterpret_cast<const float4 *>(dst);
+          v[0] = fmaf(P.beta, o4.x, v[0]); v[1] = fmaf(P.beta, o4.y, v[1]);
+          v[2] = fmaf(P.beta, o4.z, v[2]); v[3] = fmaf(P.beta, o4.w, v[3]);
         }
-      }
+        *reinterpret_cast<float4 *>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+      } else {
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int row = m0 + wm * 64 + i * 32 + 8 * (q >> 2) + 4 * lh + (q & 3);
-        if (cok && row < P.M) {
-          float v = alpha * acc[i][j][q];
-          if (use_beta) v = fmaf(P.beta, old[q], v);
-          P.C[(int64_t)row * P.ldc + col] = v;
-        }
+        for (int e = 0; e < 4; ++e)
+          if (col + e < P.N) dst[e] = use_beta ? fmaf(P.beta, dst[e], v[e]) : v[e];
       }
     }
+  }
 }
 
 template <int MODE, int TA, int TB>

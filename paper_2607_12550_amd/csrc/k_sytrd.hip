@@ -11,13 +11,14 @@
 // then A22 -= V W^T + W V^T as one MFMA GEMM with K = 2 nb (full storage is kept).
 //
 // By linearity A22 v = scal * A22 x_tail + A22[:, o], so the memory-bound mat-vec
-// runs on the unnormalised x_tail while sigma and the correction dot products
-// W^T x_tail, V^T x_tail are accumulated in the same launch.  Per column:
-//   k_symv_tiles  lower-triangle 64 x 64 tiles of A22 (each read once; an off-diagonal
+// runs on the unnormalised x_tail; sigma and the correction dot products W^T x_tail,
+// V^T x_tail are formed where x_tail is produced.  Per column:
+//   k_symv_tiles  lower-triangle 128 x 128 tiles of A22 (each read once; an off-diagonal
 //                 tile feeds two row blocks through per-slot partials, so row sums are
-//                 formed in a fixed order), plus the dot partials;
-//   k_col_finish  per 256-row block: tau, v, y, w_pre = tau y, partial w_pre^T v;
-//   k_col_next    per 256-row block: w = w_pre + alpha2 v, and the next column's x.
+//                 formed in a fixed order);
+//   k_col_finish  per 128-row block: tau, v, y, w_pre = tau y, partial w_pre^T v;
+//   k_col_next    per 128-row block: w = w_pre + alpha2 v, the next column's x and the
+//                 block partials of its sigma and dot products.
 // Panels are stored twice, P = [V; W] and Q = [W; V] (rows = panel columns, packed to
 // the panel's width jb), so the rank-2jb update is the single product P^T Q.  Every row
 // a kernel or the update reads (rows >= the current column's o) has been written in
@@ -71,12 +72,82 @@ JOLT_DEV MatView view(const SytrdArgs &a, int mat) {
 // holds an 8 x 8 sub-block in registers; row sums reduce across tx (lane shuffles), column
 // sums across ty (shuffles, then LDS across the four waves).  Tiles (I, 0) also produce the
 // dot partials [sigma, W_p^T x, V_p^T x] over their 128 rows.
-__global__ void __launch_bounds__(256) k_symv_tiles(SytrdArgs a, int i, int j, int jbw) {
+JOLT_DEV void householder(float alpha, double sigma, double &beta, double &tv, double &scal) {
+  if (sigma == 0.0) { tv = 0.0; beta = alpha; scal = 0.0; return; }
+  beta = -copysign(sqrt((double)alpha * alpha + sigma), (double)alpha);
+  tv = (beta - alpha) / beta;
+  scal = 1.0 / (alpha - beta);
+}
+
+// per 128-row block from o: v, y, w_pre and partial w_pre^T v for column i (panel index j)
+__global__ void __launch_bounds__(RB) k_col_finish(SytrdArgs a, int i, int j, int jbw) {
   const int mat = blockIdx.y, n = a.n, nb = a.nb, o = i + 1;
+  const int base = o & ~7, nt = (n - base + TB - 1) / TB;
+  const int nprev = (n - i + RB - 1) / RB;     // row blocks of the k_col_next launch that made x
+  const MatView M = view(a, mat);
+  __shared__ float pw[64], pv[64];
+  __shared__ double red[RB / 64];
+  __shared__ double sh_sigma;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // sigma and the dots, summed over the row blocks in a fixed order
+  if (tid < 2 * j + 1) {
+    double s = 0.0;
+    for (int b = 0; b < nprev; ++b) s += (double)M.dpart[(int64_t)b * (2 * nb + 1) + tid];
+    if (tid == 0) sh_sigma = s;
+    else if (tid <= j) pw[tid - 1] = (float)s;
+    else pv[tid - 1 - j] = (float)s;
+  }
+  __syncthreads();
+  const float alpha = M.sc[0];
+  double beta, tv, scal;
+  householder(alpha, sh_sigma, beta, tv, scal);
+  const float sc = (float)scal, tf = (float)tv;
+  float *V = M.P, *W = M.P + (int64_t)jbw * n;
+  float *Qv = M.Q + (int64_t)jbw * n;
+  // W^T v = scal W^T x_tail + W[o, :]  (v = e_o + scal x_tail, x_tail[o] = 0)
+  if (tid < j) {
+    pw[tid] = sc * pw[tid] + W[(int64_t)tid * n + o];
+    pv[tid] = sc * pv[tid] + V[(int64_t)tid * n + o];
+  }
+  __syncthreads();
+  const int r = o + blockIdx.x * RB + tid;
+  double dot = 0.0;
+  if (r < n) {
+    const float vr = (r == o) ? 1.f : (tv == 0.0 ? 0.f : sc * M.xt[r]);
+    float y = 0.f;
+    const float *pp = M.part + (r - base);
+#pragma unroll 8
+    for (int s = 0; s < nt; ++s) y += pp[(int64_t)s * n];
+    y = sc * y + M.A[(int64_t)o * n + r];        // + A22[:, 0] (row o by symmetry)
+    for (int p = 0; p < j; ++p) y -= V[(int64_t)p * n + r] * pw[p] + W[(int64_t)p * n + r] * pv[p];
+    const float wp = (tv == 0.0) ? 0.f : tf * y;
+    M.wpre[r] = wp;
+    V[(int64_t)j * n + r] = vr;
+    Qv[(int64_t)j * n + r] = vr;
+    M.A[(int64_t)r * n + i] = vr;                 // reflector kept for the back-transformation
+    dot = (double)wp * (double)vr;
+  }
+  dot = wave_sum(dot);
+  if (lane == 0) red[wave] = dot;
+  __syncthreads();
+  if (tid == 0) {
+    double s = 0.0;
+    for (int w = 0; w < RB / 64; ++w) s += red[w];
+    M.wpart[blockIdx.x] = (float)s;
+    if (blockIdx.x == 0) { M.d[i] = M.sc[1]; M.e[i] = beta; M.tau[i] = (float)tv; }
+  }
+}
+
+__global__ void __launch_bounds__(256) k_symv_tiles(SytrdArgs a, int i) {
+  // odd columns walk the matrices and tiles in reverse, so a pass starts on the data the
+  // previous pass touched last (still cache-resident when the matrices exceed the caches)
+  const bool rev = i & 1;
+  const int mat = rev ? gridDim.y - 1 - blockIdx.y : blockIdx.y;
+  const int n = a.n, o = i + 1;
   const int base = o & ~7, Lb = n - base;
   const MatView M = view(a, mat);
   int I, J;
-  tri_decode(blockIdx.x, I, J);
+  tri_decode(rev ? gridDim.x - 1 - blockIdx.x : blockIdx.x, I, J);
   const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4, lane = tid & 63, wave = tid >> 6;
   const int r0 = I * TB + ty * 8, c0 = J * TB + tx * 8;     // relative to base
   const float *xt = M.xt;
@@ -91,24 +162,41 @@ __global__ void __launch_bounds__(256) k_symv_tiles(SytrdArgs a, int i, int j, i
 #pragma unroll
   for (int k = 0; k < 8; ++k) { rs[k] = 0.f; cs[k] = 0.f; }
   const bool diag = (I == J);
+  // All 16 row loads are issued before any is consumed: rows outside [o, n) read a clamped
+  // in-range row and are zeroed afterwards, so no load sits behind a branch.
+  const int gc0 = base + c0;
+  float v[8][8];
+  if (gc0 + 8 <= n) {
+    float4 u[8][2];
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const int gr = base + r0 + k;
-    float v[8];
-    const int gc0 = base + c0;
-    if (gr >= o && gr < n && gc0 + 8 <= n) {
+    for (int k = 0; k < 8; ++k) {
+      const int gr = min(max(base + r0 + k, o), n - 1);
       const float4 *p = reinterpret_cast<const float4 *>(M.A + (int64_t)gr * n + gc0);
-      float4 u0 = p[0], u1 = p[1];
-      v[0] = u0.x; v[1] = u0.y; v[2] = u0.z; v[3] = u0.w; v[4] = u1.x; v[5] = u1.y; v[6] = u1.z; v[7] = u1.w;
-    } else {
+      u[k][0] = p[0];
+      u[k][1] = p[1];
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int gr = base + r0 + k;
+      const float rm = (gr >= o && gr < n) ? 1.f : 0.f;
+      v[k][0] = u[k][0].x * rm; v[k][1] = u[k][0].y * rm; v[k][2] = u[k][0].z * rm; v[k][3] = u[k][0].w * rm;
+      v[k][4] = u[k][1].x * rm; v[k][5] = u[k][1].y * rm; v[k][6] = u[k][1].z * rm; v[k][7] = u[k][1].w * rm;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int gr = base + r0 + k;
 #pragma unroll
       for (int c = 0; c < 8; ++c)
-        v[c] = (gr >= o && gr < n && gc0 + c < n) ? M.A[(int64_t)gr * n + gc0 + c] : 0.f;
+        v[k][c] = (gr >= o && gr < n && gc0 + c < n) ? M.A[(int64_t)gr * n + gc0 + c] : 0.f;
     }
+  }
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
 #pragma unroll
     for (int c = 0; c < 8; ++c) {
       const int gc = gc0 + c;
-      float e = (gc >= o) ? v[c] : 0.f;
+      const float e = (gc >= o) ? v[k][c] : 0.f;
       if (diag) {
         // lower part only: row sums take col <= row, column sums take col < row
         const bool le = (c0 + c) <= (r0 + k), lt = (c0 + c) < (r0 + k);
@@ -157,91 +245,8 @@ __global__ void __launch_bounds__(256) k_symv_tiles(SytrdArgs a, int i, int j, i
       if (cc < Lb) part[(int64_t)I * n + cc] = colsum;
     }
   }
-  if (J != 0) return;
-  const float *V = M.P, *W = M.P + (int64_t)jbw * n;
-  const int g0 = base + I * TB + lane, g1 = g0 + 64;
-  const bool v0 = g0 >= o + 1 && g0 < n, v1 = g1 >= o + 1 && g1 < n;
-  const float x0 = v0 ? xt[g0] : 0.f, x1 = v1 ? xt[g1] : 0.f;
-  for (int k = wave; k < 2 * j + 1; k += 4) {
-    float pr;
-    if (k == 0) {
-      pr = x0 * x0 + x1 * x1;
-    } else {
-      const float *col = (k <= j) ? W + (int64_t)(k - 1) * n : V + (int64_t)(k - 1 - j) * n;
-      pr = (v0 ? col[g0] * x0 : 0.f) + (v1 ? col[g1] * x1 : 0.f);
-    }
-    pr = wave_sum(pr);
-    if (lane == 0) M.dpart[(int64_t)I * (2 * nb + 1) + k] = pr;
-  }
 }
 
-JOLT_DEV void householder(float alpha, double sigma, double &beta, double &tv, double &scal) {
-  if (sigma == 0.0) { tv = 0.0; beta = alpha; scal = 0.0; return; }
-  beta = -copysign(sqrt((double)alpha * alpha + sigma), (double)alpha);
-  tv = (beta - alpha) / beta;
-  scal = 1.0 / (alpha - beta);
-}
-
-// per row block: v, y, w_pre and partial w_pre^T v for column i (panel index j)
-__global__ void __launch_bounds__(RB) k_col_finish(SytrdArgs a, int i, int j, int jbw) {
-  const int mat = blockIdx.y, n = a.n, nb = a.nb, o = i + 1;
-  const int base = o & ~7, nt = (n - base + TB - 1) / TB;
-  const MatView M = view(a, mat);
-  __shared__ float pw[64], pv[64];
-  __shared__ double red[RB / 64];
-  __shared__ double sh_sigma;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // sigma and the dots, summed over the row blocks in a fixed order
-  if (tid < 2 * j + 1) {
-    double s = 0.0;
-    for (int I = 0; I < nt; ++I) s += (double)M.dpart[(int64_t)I * (2 * nb + 1) + tid];
-    if (tid == 0) sh_sigma = s;
-    else if (tid <= j) pw[tid - 1] = (float)s;
-    else pv[tid - 1 - j] = (float)s;
-  }
-  __syncthreads();
-  const float alpha = M.sc[0];
-  double beta, tv, scal;
-  householder(alpha, sh_sigma, beta, tv, scal);
-  const float sc = (float)scal, tf = (float)tv;
-  float *V = M.P, *W = M.P + (int64_t)jbw * n;
-  float *Qv = M.Q + (int64_t)jbw * n;
-  // W^T v = scal W^T x_tail + W[o, :]  (v = e_o + scal x_tail, x_tail[o] = 0)
-  if (tid < j) {
-    pw[tid] = sc * pw[tid] + W[(int64_t)tid * n + o];
-    pv[tid] = sc * pv[tid] + V[(int64_t)tid * n + o];
-  }
-  __syncthreads();
-  const int r = o + blockIdx.x * RB + tid;
-  double dot = 0.0;
-  if (r < n) {
-    const float vr = (r == o) ? 1.f : (tv == 0.0 ? 0.f : sc * M.xt[r]);
-    float y = 0.f;
-    const float *pp = M.part + (r - base);
-#pragma unroll 8
-    for (int s = 0; s < nt; ++s) y += pp[(int64_t)s * n];
-    y = sc * y + M.A[(int64_t)o * n + r];        // + A22[:, 0] (row o by symmetry)
-    for (int p = 0; p < j; ++p) y -= V[(int64_t)p * n + r] * pw[p] + W[(int64_t)p * n + r] * pv[p];
-    const float wp = (tv == 0.0) ? 0.f : tf * y;
-    M.wpre[r] = wp;
-    V[(int64_t)j * n + r] = vr;
-    Qv[(int64_t)j * n + r] = vr;
-    M.A[(int64_t)r * n + i] = vr;                 // reflector kept for the back-transformation
-    dot = (double)wp * (double)vr;
-  }
-  dot = wave_sum(dot);
-  if (lane == 0) red[wave] = dot;
-  __syncthreads();
-  if (tid == 0) {
-    double s = 0.0;
-    for (int w = 0; w < RB / 64; ++w) s += red[w];
-    M.wpart[blockIdx.x] = (float)s;
-    if (blockIdx.x == 0) { M.d[i] = M.sc[1]; M.e[i] = beta; M.tau[i] = (float)tv; }
-  }
-}
-
-// per row block: final w of column i, then x for column ip (panel index jp, using the
-// panel's reflectors 0 .. jp-1); prep_only skips the w part (first column of a panel)
 __global__ void __launch_bounds__(RB) k_col_next(SytrdArgs a, int i, int j, int ip, int jp,
                                                  int prep_only, int jbw) {
   const int mat = blockIdx.y, n = a.n;
@@ -252,8 +257,8 @@ __global__ void __launch_bounds__(RB) k_col_next(SytrdArgs a, int i, int j, int 
   const int tid = threadIdx.x;
   float alpha2 = 0.f;
   if (!prep_only) {
-    const int o = i + 1, L = n - o;
-    const int nblk = (L + RB - 1) / RB;
+    const int o = i + 1;
+    const int nblk = (n - o + RB - 1) / RB;          // row blocks of column i's k_col_finish
     if (tid == 0) {
       double s = 0.0;
       for (int b = 0; b < nblk; ++b) s += (double)M.wpart[b];
@@ -261,7 +266,7 @@ __global__ void __launch_bounds__(RB) k_col_next(SytrdArgs a, int i, int j, int 
     }
     __syncthreads();
     alpha2 = alpha2_s;
-    // rows o .. n-1, the same split as k_col_finish; each thread owns one row
+    // rows o .. n-1 in blocks of 128; each thread owns one row
     const int r = o + blockIdx.x * RB + tid;
     if (r < n) {
       const float w = M.wpre[r] + alpha2 * V[(int64_t)j * n + r];
@@ -282,12 +287,30 @@ __global__ void __launch_bounds__(RB) k_col_next(SytrdArgs a, int i, int j, int 
   // x[r] = A[ip][r] - sum_p (V[p][r] W[p][ip] + W[p][r] V[p][ip]) for r >= ip (row ip = column ip);
   // row r of W_j was written above by this same thread
   const int r = ip + blockIdx.x * RB + tid;
+  float xtail = 0.f;
   if (r < n) {
     float x = M.A[(int64_t)ip * n + r];
     for (int p = 0; p < jp; ++p) x -= V[(int64_t)p * n + r] * cw[p] + W[(int64_t)p * n + r] * cv[p];
     if (r == ip) M.sc[1] = x;
     if (r == ip + 1) M.sc[0] = x;
-    M.xt[r] = (r > ip + 1) ? x : 0.f;
+    xtail = (r > ip + 1) ? x : 0.f;
+    M.xt[r] = xtail;
+  }
+  // partials over this block's rows of the next column's sigma = x_tail^T x_tail and of
+  // W_p^T x_tail, V_p^T x_tail (p < jp), in that order; summed over blocks by k_col_finish
+  __shared__ float prod[2 * 32 + 1][RB];
+  const int nk = 2 * jp + 1;
+  prod[0][tid] = xtail * xtail;
+  for (int p = 0; p < jp; ++p) {
+    const bool ok = r < n;
+    prod[1 + p][tid] = ok ? W[(int64_t)p * n + r] * xtail : 0.f;
+    prod[1 + jp + p][tid] = ok ? V[(int64_t)p * n + r] * xtail : 0.f;
+  }
+  __syncthreads();
+  if (tid < nk) {
+    float sum = 0.f;
+    for (int t = 0; t < RB; ++t) sum += prod[tid][t];
+    M.dpart[(int64_t)blockIdx.x * (2 * a.nb + 1) + tid] = sum;
   }
 }
 
@@ -377,6 +400,7 @@ void sytrd_large_tables(const EigBatch &b, float *work, int nb, GemmProblem *tab
 hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, const GemmProblem *tab_dev,
                               hipStream_t st, const LaunchHook &hook) {
   const int n = b.n, nm = b.n_mat;
+  if (nb > 32) return hipErrorInvalidValue;     // k_col_next's partial buffer holds 2 nb + 1 dots
   SytrdArgs a{};
   a.A = b.A; a.mat_stride = b.mat_stride; a.n = n; a.nb = nb;
   a.d = b.d; a.e = b.e; a.tau = b.tau;
@@ -394,7 +418,7 @@ hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, const Gemm
       const int i = k0 + j, o = i + 1, L = n - o;
       const int nt = (n - (o & ~7) + TB - 1) / TB, nblk = (L + RB - 1) / RB;
       hook(JOLT_STAGE_SYMV, 1);
-      hipLaunchKernelGGL(k_symv_tiles, dim3(nt * (nt + 1) / 2, nm), dim3(256), 0, st, a, i, j, jb);
+      hipLaunchKernelGGL(k_symv_tiles, dim3(nt * (nt + 1) / 2, nm), dim3(256), 0, st, a, i);
       hook(JOLT_STAGE_SYMV, 0);
       hook(JOLT_STAGE_PANEL, 1);
       hipLaunchKernelGGL(k_col_finish, dim3(nblk, nm), dim3(RB), 0, st, a, i, j, jb);
