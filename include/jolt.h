@@ -81,6 +81,12 @@ typedef struct {
   double ratio;        /* target compression ratio R read by the cap policy */
   int32_t oversample;  /* p: sketch width l = min(q + p, T, m*d) */
   int32_t power_iters; /* power (subspace) iterations of the range finder */
+  int32_t reuse;       /* jolt_compress only.  1: take the token spectrum that the last
+                          jolt_spectrum or jolt_compress call on this workspace left there
+                          for these same cells, options and seeds (JOLT_E_STATE if the
+                          context recorded none); the caller guarantees that the workspace
+                          was neither written nor freed since.  0: compute it. */
+  int32_t reserved;
 } jolt_spectrum_opts;
 
 /* Per-cell compression parameters. */
@@ -155,8 +161,11 @@ int jolt_decompress_workspace_size(const jolt_cell_desc *out_desc, int n_cells, 
  *           values of the sketch followed by the synthetic tail E - sum(captured).
  *   lam_d   host, n_cells x d: eigenvalues of sum_s X_s^T X_s, descending.
  *   ws      device workspace of jolt_workspace_size bytes, 256-byte aligned; it keeps
- *           the token factors, so a following jolt_compress of the same cells with the
- *           same workspace, options and seeds skips the spectrum.
+ *           the token factors, so a later jolt_compress of the same cells with the same
+ *           workspace, options and seeds can skip the spectrum (opts->reuse = 1).  The
+ *           context records one spectrum per workspace; any call that writes an
+ *           overlapping workspace (jolt_spectrum, jolt_compress, jolt_decompress,
+ *           jolt_eps2_calibrate) first drops the record.
  * Synchronises the stream (the outputs are host arrays).  Errors: JOLT_E_INVAL
  * (null/misaligned pointers), JOLT_E_WORKSPACE, JOLT_E_NONFINITE (a cell holds NaN or
  * Inf; outputs then undefined), JOLT_E_UNSUPPORTED, JOLT_E_HIP. */

@@ -40,7 +40,8 @@ class JoltError(RuntimeError):
 
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_12550_amd.build`")
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2607_12550_amd/build.py` "
+                      "(or __graft_entry__.build())")
 lib = C.CDLL(LIB_PATH)
 
 
@@ -53,7 +54,8 @@ class CellDesc(C.Structure):
 
 class SpectrumOpts(C.Structure):
     _fields_ = [("method", C.c_int32), ("q", C.c_int32), ("ratio", C.c_double),
-                ("oversample", C.c_int32), ("power_iters", C.c_int32)]
+                ("oversample", C.c_int32), ("power_iters", C.c_int32), ("reuse", C.c_int32),
+                ("reserved", C.c_int32)]
 
 
 class Params(C.Structure):

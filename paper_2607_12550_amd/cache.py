@@ -20,8 +20,8 @@ import torch
 from . import (JOLT_BF16, JOLT_EXACT, JOLT_F32, JOLT_FACTOR_F16, JOLT_FACTOR_F32, JOLT_FLASH,
                HEADER_BYTES, Params, SpectrumOpts, cell_desc, jolt_allocate, jolt_compress,
                jolt_compressed_size, jolt_create, jolt_decompress, jolt_destroy,
-               jolt_eps2_calibrate, jolt_eps2_workspace_size, jolt_q_cap, jolt_spectrum, jolt_spectrum_len,
-               jolt_workspace_size)
+               jolt_decompress_workspace_size, jolt_eps2_calibrate, jolt_eps2_workspace_size, jolt_q_cap,
+               jolt_spectrum, jolt_spectrum_len, jolt_workspace_size)
 
 
 @dataclass
@@ -51,7 +51,7 @@ class CacheCodec:
                  method: str = "exact", ratio: float = 2.0, q: int = 0, oversample: int = 10,
                  power_iters: int = 1, group: int = 64, bits=(0, 2, 4, 8), step: int = 8,
                  count_scale_bytes: bool = True, seed: int = 0, max_cells_per_call: int = 16,
-                 device: int = 0):
+                 workspace_cap_bytes: int = 0, device: int = 0):
         assert K.shape == V.shape and K.dtype == V.dtype and K.is_cuda and K.is_contiguous()
         L, B, H, T, d = K.shape
         if L % group_layers:
@@ -63,7 +63,9 @@ class CacheCodec:
         self.group_layers, self.ratio, self.group, self.bits, self.step = group_layers, ratio, group, bits, step
         self.count_scale_bytes = count_scale_bytes
         self.method = JOLT_FLASH if method == "flash" else JOLT_EXACT
-        self.opts = SpectrumOpts(self.method, q, float(ratio), oversample, power_iters)
+        self.opts = SpectrumOpts(self.method, q, float(ratio), oversample, power_iters, 0, 0)
+        # compress takes each chunk's spectrum from the workspace its spectrum call filled
+        self.reuse_opts = SpectrumOpts(self.method, q, float(ratio), oversample, power_iters, 1, 0)
         self.factor_dtype = JOLT_FACTOR_F16 if self.dtype == JOLT_BF16 else JOLT_FACTOR_F32
         self.fbytes = 2 if self.factor_dtype == JOLT_FACTOR_F16 else 4
         self.desc = cell_desc(dtype=self.dtype, n_layers=group_layers, n_heads=H, T=T, d=d,
@@ -78,9 +80,18 @@ class CacheCodec:
         self.cache_bytes = 2 * K.numel() * esz
         self.chunk = max(1, min(max_cells_per_call, len(self.cells)))
         self.ctx = jolt_create(device)
-        self.ws = torch.empty(jolt_workspace_size(self.desc, self.chunk, self.opts), dtype=torch.uint8,
-                              device=K.device)
         self.n_lam, self.rT_max = jolt_spectrum_len(self.desc, self.opts)
+        # one workspace per chunk of cells when they fit under the cap, so that compress
+        # reuses every chunk's spectrum; otherwise one shared workspace (spectra recomputed)
+        n_chunks = (len(self.cells) + self.chunk - 1) // self.chunk
+        ws_bytes = jolt_workspace_size(self.desc, self.chunk, self.opts)
+        if not workspace_cap_bytes:      # default: half of the device's memory
+            workspace_cap_bytes = torch.cuda.get_device_properties(K.device).total_memory // 2
+        n_ws = n_chunks if n_chunks * ws_bytes <= workspace_cap_bytes else 1
+        self.ws_list = [torch.empty(ws_bytes, dtype=torch.uint8, device=K.device) for _ in range(n_ws)]
+        self.ws = self.ws_list[0]
+        self.dec_ws = torch.empty(jolt_decompress_workspace_size(self.desc, self.chunk, self.rT_max),
+                                  dtype=torch.uint8, device=K.device)
         # FlashJoLT sketch width l = min(q + p, T, m d) (section 5); 0 for the exact path
         qq = q or (jolt_q_cap(T, ratio) if self.method == JOLT_FLASH else 0)
         self.ell = min(qq + oversample, T, group_layers * H * d) if self.method == JOLT_FLASH else 0
@@ -89,6 +100,7 @@ class CacheCodec:
         arena = int(self.cache_bytes / ratio) + len(self.cells) * (HEADER_BYTES + 8 * 256) + (1 << 20)
         self.arena = torch.zeros(arena, dtype=torch.uint8, device=K.device)
         self.params = None
+        self.spectra_fresh = False
         self.blob_ptrs = None
         self.blob_sizes = None
         self.hdr = None
@@ -103,6 +115,9 @@ class CacheCodec:
         for i in range(0, len(self.cells), self.chunk):
             yield i, self.cells[i:i + self.chunk]
 
+    def _ws(self, i):
+        return self.ws_list[(i // self.chunk) % len(self.ws_list)]
+
     def calibrate(self, n_samples: int = 1 << 20, seed: int = 0):
         d = self.shape[4]
         ws = torch.empty(jolt_eps2_workspace_size(d, n_samples), dtype=torch.uint8, device=self.K.device)
@@ -113,9 +128,10 @@ class CacheCodec:
         E, LT, LD = [], [], []
         for i, cs in self._chunks():
             e, lt, ld = jolt_spectrum(self.ctx, self.desc, [c.ptr for c in cs], self.seeds[i:i + len(cs)],
-                                      self.opts, self.ws, stream=stream)
+                                      self.opts, self._ws(i), stream=stream)
             E.append(e); LT.append(lt); LD.append(ld)
         self.spectra = (np.concatenate(E), np.concatenate(LT), np.concatenate(LD))
+        self.spectra_fresh = True
         return self.spectra
 
     def allocate(self, budget_bytes=None):
@@ -147,8 +163,11 @@ class CacheCodec:
     def compress(self, stream=None):
         for i, cs in self._chunks():
             n = len(cs)
-            jolt_compress(self.ctx, self.desc, [c.ptr for c in cs], self.params[i:i + n], self.opts,
-                          self.ws, self.blob_ptrs[i:i + n], ws_bytes=self.ws.numel(),
+            ws = self._ws(i)
+            reuse = len(self.ws_list) * self.chunk >= len(self.cells) and self.spectra_fresh
+            jolt_compress(self.ctx, self.desc, [c.ptr for c in cs], self.params[i:i + n],
+                          self.reuse_opts if reuse else self.opts,
+                          ws, self.blob_ptrs[i:i + n], ws_bytes=ws.numel(),
                           blob_bytes=self.blob_sizes[i:i + n], stream=stream)
 
     def headers(self):
@@ -175,8 +194,8 @@ class CacheCodec:
         for i, cs in self._chunks():
             n = len(cs)
             hdr = self.hdr[i:i + n] if self.hdr is not None else None
-            jolt_decompress(self.ctx, self.blob_ptrs[i:i + n], od, outs[i:i + n], self.ws, hdr_host=hdr,
-                            blob_bytes=self.blob_sizes[i:i + n], ws_bytes=self.ws.numel(), stream=stream)
+            jolt_decompress(self.ctx, self.blob_ptrs[i:i + n], od, outs[i:i + n], self.dec_ws, hdr_host=hdr,
+                            blob_bytes=self.blob_sizes[i:i + n], ws_bytes=self.dec_ws.numel(), stream=stream)
 
     def compressed_bytes(self) -> int:
         return int(sum(self.blob_sizes))

@@ -36,6 +36,9 @@ struct SpecKey {
   std::vector<uint64_t> seeds;
 };
 
+// Forget every recorded spectrum whose workspace overlaps [ws, ws + bytes), except `keep`.
+void forget_spectra(jolt_ctx *ctx, const void *ws, size_t bytes, const SpecKey *keep = nullptr);
+
 struct DebugState {
   bool valid = false;
   int n_cells = 0, T = 0, d = 0, m = 0, N = 0, ell = 0;
@@ -53,7 +56,8 @@ struct ProfRecord {
 struct jolt_ctx {
   int device = 0;
   hipDeviceProp_t prop{};
-  SpecKey spec;
+  // spectra left in caller workspaces by jolt_spectrum / jolt_compress, one per workspace
+  std::vector<SpecKey> specs;
   DebugState dbg;
   std::vector<GemmProblem> tab_host;
   bool prof_on = false;

@@ -398,14 +398,19 @@ void sytrd_large_tables(const EigBatch &b, float *work, int nb, GemmProblem *tab
 }
 
 hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, const GemmProblem *tab_dev,
-                              hipStream_t st, const LaunchHook &hook) {
-  const int n = b.n, nm = b.n_mat;
+                              hipStream_t st, const LaunchHook &hook, int m0, int m1) {
+  // matrices m0 .. m1-1 of the batch (all by default)
+  const int n = b.n;
+  if (m1 < 0) m1 = b.n_mat;
+  const int nm = m1 - m0;
+  if (nm <= 0 || m0 < 0 || m1 > b.n_mat) return hipErrorInvalidValue;
   if (nb > 32) return hipErrorInvalidValue;     // k_col_next's partial buffer holds 2 nb + 1 dots
+  const int64_t wstride = (int64_t)((per_mat_floats(n, nb) + 63) / 64 * 64);
   SytrdArgs a{};
-  a.A = b.A; a.mat_stride = b.mat_stride; a.n = n; a.nb = nb;
-  a.d = b.d; a.e = b.e; a.tau = b.tau;
-  a.work = work;
-  a.work_stride = (int64_t)((per_mat_floats(n, nb) + 63) / 64 * 64);
+  a.A = b.A + (int64_t)m0 * b.mat_stride; a.mat_stride = b.mat_stride; a.n = n; a.nb = nb;
+  a.d = b.d + (int64_t)m0 * n; a.e = b.e + (int64_t)m0 * n; a.tau = b.tau + (int64_t)m0 * n;
+  a.work = work + m0 * wstride;
+  a.work_stride = wstride;
   a.slots = (n + TB - 1) / TB;
   const int panels = (n - 1 + nb - 1) / nb;
   hipError_t err = hipSuccess;
@@ -429,7 +434,7 @@ hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, const Gemm
     const int s = k0 + jb;
     if (s < n) {
       hook(JOLT_STAGE_PANEL_GEMM, 1);
-      err = launch_gemm(tab_dev + (size_t)p * nm, nm, n - s, n - s, 1, GT_F32, GT_F32, false, false, st);
+      err = launch_gemm(tab_dev + (size_t)p * b.n_mat + m0, nm, n - s, n - s, 1, GT_F32, GT_F32, false, false, st);
       if (err != hipSuccess) return err;
       hipLaunchKernelGGL(k_mirror_strip, dim3((n - s + 63) / 64, nm), dim3(256), 0, st, a, s);
       hook(JOLT_STAGE_PANEL_GEMM, 0);

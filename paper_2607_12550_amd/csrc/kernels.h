@@ -151,7 +151,8 @@ size_t sytrd_large_table_entries(int n_mat, int n, int nb);
 // into a graph and replayed).
 void sytrd_large_tables(const EigBatch &b, float *work, int nb, GemmProblem *tab_host);
 hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, const GemmProblem *tab_dev,
-                              hipStream_t st, const LaunchHook &hook);
+                              hipStream_t st, const LaunchHook &hook,
+                              int m0 = 0, int m1 = -1);
 // all eigenvalues of the tridiagonal (fp64 bisection), descending
 hipError_t launch_tridiag_eigvals(const EigBatch &b, hipStream_t st);
 // top-k eigenvectors of the tridiagonal by fp64 inverse iteration, orthogonalised

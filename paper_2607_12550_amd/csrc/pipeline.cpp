@@ -361,6 +361,16 @@ int spectrum_device(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int
 }  // namespace
 
 // ------------------------------------------------------------------------ sizes
+void forget_spectra(jolt_ctx *ctx, const void *ws, size_t bytes, const SpecKey *keep) {
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(ws), a1 = a0 + bytes;
+  std::vector<SpecKey> kept;
+  for (SpecKey &k : ctx->specs) {
+    const uintptr_t b0 = reinterpret_cast<uintptr_t>(k.ws), b1 = b0 + k.ws_bytes;
+    if (&k == keep || b1 <= a0 || a1 <= b0) kept.push_back(std::move(k));
+  }
+  ctx->specs.swap(kept);
+}
+
 extern "C" int jolt_workspace_size(const jolt_cell_desc *desc, int n_cells,
                                    const jolt_spectrum_opts *opts, size_t *bytes) {
   SpecShape sh;
@@ -564,7 +574,7 @@ extern "C" int jolt_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
   Run R{ctx, (hipStream_t)stream, {}};
   Carver cv(ws);
   plan(cv, R.w, sh, n_cells);
-  ctx->spec.valid = false;
+  forget_spectra(ctx, ws, ws_bytes);
   rc = spectrum_device(R, sh, desc, n_cells, X, seeds, opts);
   if (rc) return rc;
   std::vector<double> lt((size_t)n_cells * sh.T), ld((size_t)n_cells * sh.d);
@@ -596,12 +606,13 @@ extern "C" int jolt_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
       lam_T[(size_t)c * (sh.q + 1) + sh.q] = std::max(0.0, E[c] - captured);
     }
   }
-  SpecKey &k = ctx->spec;
+  ctx->specs.emplace_back();
+  SpecKey &k = ctx->specs.back();
   k.valid = true;
   k.ws = ws;
   k.ws_bytes = ws_bytes;
   k.desc = *desc;
-  k.opts = opts ? *opts : jolt_spectrum_opts{JOLT_EXACT, 0, 0.0, 0, 0};
+  k.opts = opts ? *opts : jolt_spectrum_opts{JOLT_EXACT, 0, 0.0, 0, 0, 0, 0};
   k.X.assign(X, X + n_cells);
   k.seeds.assign(seeds ? seeds : (const uint64_t *)nullptr, seeds ? seeds + n_cells : (const uint64_t *)nullptr);
   return JOLT_OK;
@@ -639,16 +650,33 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
   const int m = sh.m, T = sh.T, d = sh.d, N = sh.N, nc = n_cells;
   std::vector<uint64_t> seeds(nc);
   for (int c = 0; c < nc; ++c) seeds[c] = params[c].seed;
-  // reuse the spectrum of the preceding call when it covers exactly these cells
-  const SpecKey &k = ctx->spec;
-  jolt_spectrum_opts o = opts ? *opts : jolt_spectrum_opts{JOLT_EXACT, 0, 0.0, 0, 0};
-  bool reuse = k.valid && k.ws == ws && k.ws_bytes == ws_bytes && same_desc(k.desc, *desc) &&
-               same_opts(k.opts, o) && (int)k.X.size() == nc && std::equal(k.X.begin(), k.X.end(), X);
-  if (reuse && sh.method == JOLT_FLASH) reuse = k.seeds == seeds;
-  if (!reuse) {
-    ctx->spec.valid = false;
+  // the spectrum: taken from the workspace on request (it must hold these cells' spectrum),
+  // computed otherwise
+  jolt_spectrum_opts o = opts ? *opts : jolt_spectrum_opts{JOLT_EXACT, 0, 0.0, 0, 0, 0, 0};
+  if (o.reuse) {
+    const SpecKey *found = nullptr;
+    for (const SpecKey &k : ctx->specs) {
+      bool ok = k.valid && k.ws == ws && k.ws_bytes == ws_bytes && same_desc(k.desc, *desc) &&
+                same_opts(k.opts, o) && (int)k.X.size() == nc && std::equal(k.X.begin(), k.X.end(), X);
+      if (ok && sh.method == JOLT_FLASH) ok = k.seeds == seeds;
+      if (ok) { found = &k; break; }
+    }
+    if (!found)
+      return jolt_fail(JOLT_E_STATE, "reuse requested but the workspace holds no spectrum of these cells");
+    forget_spectra(ctx, ws, ws_bytes, found);
+  } else {
+    forget_spectra(ctx, ws, ws_bytes);
     rc = spectrum_device(R, sh, desc, nc, X, seeds.data(), &o);
     if (rc) return rc;
+    ctx->specs.emplace_back();
+    SpecKey &k = ctx->specs.back();
+    k.valid = true;
+    k.ws = ws;
+    k.ws_bytes = ws_bytes;
+    k.desc = *desc;
+    k.opts = o;
+    k.X.assign(X, X + nc);
+    k.seeds = seeds;
   }
   rc = upload_seeds_and_signs(R, seeds.data(), nc, d);
   if (rc) return rc;
@@ -892,6 +920,7 @@ extern "C" int jolt_decompress(jolt_ctx *ctx, int n_cells, const void *const *bl
     plan_decode(cv, w, m, T, d, n_cells, kmax);
     if (ws_bytes < cv.off) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, cv.off);
   }
+  forget_spectra(ctx, ws, ws_bytes);
   Carver cv(ws);
   plan_decode(cv, R.w, m, T, d, n_cells, kmax);
   std::vector<uint64_t> seeds(n_cells);
@@ -970,6 +999,7 @@ extern "C" int jolt_eps2_calibrate(jolt_ctx *ctx, int group, int d, uint64_t see
   if (!ctx || !eps2_out || !ws) return jolt_fail(JOLT_E_INVAL, "jolt_eps2_calibrate: null argument");
   if (group < 8 || group > d || d % group || group % 8) return jolt_fail(JOLT_E_INVAL, "bad group %d", group);
   if (ws_bytes < need) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  forget_spectra(ctx, ws, ws_bytes);
   HIP_OK(hipSetDevice(ctx->device));
   hipStream_t st = (hipStream_t)stream;
   Eps2Args a{seed, n_samples, group, (float)(1.0 / std::sqrt((double)d)), static_cast<double *>(ws)};

@@ -145,11 +145,13 @@ def test_spectrum_then_compress_reuses_and_matches_direct():
     ws = workspace(desc, 2)
     E, lamT, lamd = J.jolt_spectrum(ctx(), desc, xs, None, None, ws)
     params = [J.Params(16, 24, 4, 64, J.JOLT_FACTOR_F16, 0, 1), J.Params(24, 16, 2, 64, J.JOLT_FACTOR_F16, 0, 2)]
-    b_reuse, _ = compress(xs, desc, params, ws=ws)
+    reuse = J.SpectrumOpts(J.JOLT_EXACT, 0, 0.0, 0, 0, 1, 0)
+    b_reuse, _ = compress(xs, desc, params, reuse, ws=ws)
+    b_again, _ = compress(xs, desc, params, reuse, ws=ws)     # compress keeps the spectrum
     ws2 = workspace(desc, 2)
     b_direct, _ = compress(xs, desc, params, ws=ws2)
-    for a, b in zip(b_reuse, b_direct):
-        assert blob_bytes(a) == blob_bytes(b)
+    for a, b, c in zip(b_reuse, b_again, b_direct):
+        assert blob_bytes(a) == blob_bytes(b) == blob_bytes(c)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -189,3 +191,29 @@ def test_blocked_tridiagonalisation_spectrum_and_subspace(dtype):
     eb_gpu, eb_ref = opl.rel_error(ex[0], Xt), opl.rel_error(ex[0], ref["Xtilde"])
     assert abs(eb_gpu / eb_ref - 1) < tol, (eb_gpu, eb_ref)
     assert np.linalg.norm(Xt - ref["Xtilde"]) <= max(tol, ptol) * np.linalg.norm(ex[0])
+
+
+def test_workspace_overwrite_forgets_the_spectrum():
+    """Reuse is explicit: after a decompress into the workspace that held the spectrum, a
+    compress asking for reuse is refused, and one that recomputes equals a fresh one."""
+    xs, ex, desc = device_cells([keys_cell(T=128, H=4, seed=9), keys_cell(T=128, H=4, seed=10)], "bf16")
+    ws = workspace(desc, 2)
+    params = [J.Params(16, 24, 4, 64, J.JOLT_FACTOR_F16, 0, 3), J.Params(24, 16, 2, 64, J.JOLT_FACTOR_F16, 0, 4)]
+    reuse = J.SpectrumOpts(J.JOLT_EXACT, 0, 0.0, 0, 0, 1, 0)
+    J.jolt_spectrum(ctx(), desc, xs, None, None, ws)
+    blobs, _ = compress(xs, desc, params, ws=workspace(desc, 2))
+    decompress(blobs, desc, "f32", ws=ws)          # overwrites ws
+    with pytest.raises(J.JoltError) as ei:
+        compress(xs, desc, params, reuse, ws=ws)
+    assert ei.value.code == -7                    # JOLT_E_STATE
+    b_after, _ = compress(xs, desc, params, ws=ws)
+    for a, b in zip(blobs, b_after):
+        assert blob_bytes(a) == blob_bytes(b)
+    # two workspaces keep their own spectra
+    ws2 = workspace(desc, 2)
+    J.jolt_spectrum(ctx(), desc, xs, None, None, ws)
+    J.jolt_spectrum(ctx(), desc, xs, None, None, ws2)
+    b1, _ = compress(xs, desc, params, reuse, ws=ws)
+    b2, _ = compress(xs, desc, params, reuse, ws=ws2)
+    for a, b, c in zip(blobs, b1, b2):
+        assert blob_bytes(a) == blob_bytes(b) == blob_bytes(c)
