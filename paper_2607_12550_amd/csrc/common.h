@@ -9,6 +9,20 @@
 
 typedef uint16_t bf16_t;  // bf16 bit pattern
 
+// Global-memory views of generic pointers: loads and stores through them compile to
+// global_* instructions (waited on by vmcnt alone) instead of flat_* ones, which also
+// hold lgkmcnt and so serialise against LDS traffic.
+#define JOLT_GLOBAL __attribute__((address_space(1)))
+template <class T>
+JOLT_DEV const JOLT_GLOBAL T *gptr(const T *p) { return (const JOLT_GLOBAL T *)p; }
+template <class T>
+JOLT_DEV JOLT_GLOBAL T *gptr(T *p) { return (JOLT_GLOBAL T *)p; }
+typedef float jf4 __attribute__((ext_vector_type(4)));
+typedef uint32_t ju4 __attribute__((ext_vector_type(4)));
+JOLT_DEV jf4 gload_f4(const void *p) { return *(const JOLT_GLOBAL jf4 *)p; }
+JOLT_DEV ju4 gload_u4(const void *p) { return *(const JOLT_GLOBAL ju4 *)p; }
+JOLT_DEV void gstore_f4(void *p, jf4 v) { *(JOLT_GLOBAL jf4 *)p = v; }
+
 // ---------------------------------------------------------------- number formats
 JOLT_HD float bf16_to_f32(bf16_t b) {
   uint32_t u = (uint32_t)b << 16;

@@ -451,7 +451,7 @@ hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax,
       // W2 = [T T ... T] [W1_0; W1_1; ...]: the split-K sum folded into this product
       // (A's columns wrap onto T with a zero segment stride)
       GemmProblem Q{};
-      Q.A = GemmOperand{Tf + ((size_t)m * panels + p) * NB * NB, NB, 0, 0, NB, 1};
+      Q.A = seg_operand(Tf + ((size_t)m * panels + p) * NB * NB, NB, 0, 0, NB, 1);
       Q.B = GemmOperand{W1 + m * w1_mat, kmax, 0, 0, 0, 1};
       Q.C = W2 + (size_t)m * NB * kmax; Q.ldc = kmax;
       Q.M = pw; Q.N = kmax; Q.K = chunks * NB; Q.alpha = 1.f; Q.beta = 0.f;

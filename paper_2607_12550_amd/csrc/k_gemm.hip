@@ -26,17 +26,14 @@ namespace {
 constexpr int BM = 128, BN = 128, BK = 32, NT = 256;
 
 JOLT_DEV int64_t op_offset(const GemmOperand &op, int row, int col) {
-  if (op.seg_len == 0) return (int64_t)row * op.ld + col;
-  const int s = col / op.seg_len, w = col - s * op.seg_len;
-  return (int64_t)(s / op.seg_heads) * op.seg_hi + (int64_t)(s % op.seg_heads) * op.seg_lo +
-         (int64_t)row * op.ld + w;
+  return (int64_t)row * op.ld + operand_col(op, col);
 }
 
 template <int TY>
 JOLT_DEV float load_elem(const void *p, int64_t off) {
-  if constexpr (TY == GT_BF16) return bf16_to_f32(reinterpret_cast<const uint16_t *>(p)[off]);
-  else if constexpr (TY == GT_F16) return (float)reinterpret_cast<const _Float16 *>(p)[off];
-  else return reinterpret_cast<const float *>(p)[off];
+  if constexpr (TY == GT_BF16) return bf16_to_f32(gptr(reinterpret_cast<const uint16_t *>(p))[off]);
+  else if constexpr (TY == GT_F16) return (float)gptr(reinterpret_cast<const _Float16 *>(p))[off];
+  else return gptr(reinterpret_cast<const float *>(p))[off];
 }
 
 // 8 consecutive elements along the operand's contiguous dimension, widened to fp32
@@ -49,11 +46,11 @@ JOLT_DEV void load8_f32(const GemmOperand &op, int row, int col, int nrows, int 
       ((reinterpret_cast<uintptr_t>(op.ptr) + (uintptr_t)off0 * esz) & 15) == 0) {
     const int64_t off = off0;
     if constexpr (TY == GT_F32) {
-      const float4 *q = reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(op.ptr) + off);
-      float4 a = q[0], b = q[1];
+      const float *q = reinterpret_cast<const float *>(op.ptr) + off;
+      const jf4 a = gload_f4(q), b = gload_f4(q + 4);
       v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
     } else {
-      uint4 u = *reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(op.ptr) + off);
+      const ju4 u = gload_u4(reinterpret_cast<const uint16_t *>(op.ptr) + off);
       uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -76,10 +73,10 @@ JOLT_DEV void load8_f32(const GemmOperand &op, int row, int col, int nrows, int 
 
 JOLT_DEV void load8_raw16(const GemmOperand &op, int row, int col, int nrows, int ncols,
                           uint16_t (&v)[8]) {
-  const uint16_t *p = reinterpret_cast<const uint16_t *>(op.ptr);
+  const JOLT_GLOBAL uint16_t *p = gptr(reinterpret_cast<const uint16_t *>(op.ptr));
   const int64_t off0 = (row < nrows && col + 8 <= ncols) ? op_offset(op, row, col) : 0;
   if (row < nrows && col + 8 <= ncols && ((reinterpret_cast<uintptr_t>(p + off0)) & 15) == 0) {
-    uint4 u = *reinterpret_cast<const uint4 *>(p + off0);
+    const ju4 u = gload_u4((const void *)(reinterpret_cast<const uint16_t *>(op.ptr) + off0));
     uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) { v[2 * i] = (uint16_t)(w[i] & 0xffff); v[2 * i + 1] = (uint16_t)(w[i] >> 16); }
@@ -225,7 +222,7 @@ __global__ void __launch_bounds__(NT) k_gemm(const GemmProblem *__restrict__ pro
   }
 
   float alpha = P.alpha;
-  if (P.alpha_exp2) alpha = ldexpf(alpha, (int)*P.alpha_exp2);
+  if (P.alpha_exp2) alpha = ldexpf(alpha, (int)*gptr(P.alpha_exp2));
   // Epilogue through LDS, 32 rows at a time (one MFMA row block of one wave row per round),
   // so that C is read (beta != 0) and written as float4 rows: acc[i][j][q] is the output at
   // row wm*64 + i*32 + 8*(q/4) + 4*lh + q%4, column wn*64 + j*32 + lr of the tile.
@@ -254,14 +251,14 @@ __global__ void __launch_bounds__(NT) k_gemm(const GemmProblem *__restrict__ pro
       if (row >= P.M || col >= P.N) continue;
       const float4 a4 = *reinterpret_cast<const float4 *>(&cs[rr * CLD + cc]);
       float v[4] = {alpha * a4.x, alpha * a4.y, alpha * a4.z, alpha * a4.w};
-      float *dst = P.C + (int64_t)row * P.ldc + col;
+      JOLT_GLOBAL float *dst = gptr(P.C + (int64_t)row * P.ldc + col);
       if (vec && col + 4 <= P.N) {
         if (use_beta) {
-          const float4 o4 = *reinterpret_cast<const float4 *>(dst);
+          const jf4 o4 = *reinterpret_cast<const JOLT_GLOBAL jf4 *>(dst);
           v[0] = fmaf(P.beta, o4.x, v[0]); v[1] = fmaf(P.beta, o4.y, v[1]);
           v[2] = fmaf(P.beta, o4.z, v[2]); v[3] = fmaf(P.beta, o4.w, v[3]);
         }
-        *reinterpret_cast<float4 *>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+        *reinterpret_cast<JOLT_GLOBAL jf4 *>(dst) = jf4{v[0], v[1], v[2], v[3]};
       } else {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
@@ -288,8 +285,9 @@ hipError_t launch_gemm(const GemmProblem *probs_dev, int n_probs, int max_M, int
   dim3 grid((max_N + BN - 1) / BN, (max_M + BM - 1) / BM, n_probs);
   if (mode == 0) {
     if (ta != GT_BF16 || tb != GT_BF16) return hipErrorInvalidValue;
-    return launch_t<0, GT_BF16, GT_BF16>(probs_dev, n_probs, grid, a_kcontig, b_kcontig, st);
+    return launch_gemm16(probs_dev, n_probs, max_M, max_N, ta, tb, a_kcontig, b_kcontig, st);
   }
+  if (mode == 2) return launch_gemm16(probs_dev, n_probs, max_M, max_N, ta, tb, a_kcontig, b_kcontig, st);
 #define TT(A_, B_) if (ta == A_ && tb == B_) return launch_t<1, A_, B_>(probs_dev, n_probs, grid, a_kcontig, b_kcontig, st)
   TT(GT_F32, GT_F32);
   TT(GT_BF16, GT_F32);

@@ -75,12 +75,37 @@ hipError_t launch_eps2_partial(const Eps2Args &a, int d, hipStream_t st);
 // or "n-contiguous" (row = k, col = n).
 enum GemmType { GT_BF16 = 0, GT_F16 = 1, GT_F32 = 2, GT_F64 = 3 };
 
+// Element (row, col) of an operand sits at row * ld + col, or, when seg_len > 0, the
+// contiguous index col runs over segments of seg_len elements (seg_len a power of two):
+// segment s = col / seg_len starts at (s / seg_heads) * seg_hi + (s % seg_heads) * seg_lo.
+// seg_shift = log2(seg_len) and heads_magic = ceil(2^32 / seg_heads) make both divisions
+// a shift and a multiply (exact for s < 2^20, seg_heads < 2^12); build with seg_operand().
 struct GemmOperand {
   const void *ptr;
   int64_t ld;
   int64_t seg_hi, seg_lo;
   int32_t seg_len, seg_heads;
+  int32_t seg_shift, pad_;
+  uint64_t heads_magic;
 };
+
+inline GemmOperand seg_operand(const void *ptr, int64_t ld, int64_t seg_hi, int64_t seg_lo,
+                               int32_t seg_len, int32_t seg_heads) {
+  GemmOperand o{ptr, ld, seg_hi, seg_lo, seg_len, seg_heads, 0, 0, 0};
+  if (seg_len > 0) {
+    while ((1 << o.seg_shift) < seg_len) ++o.seg_shift;
+    o.heads_magic = ((uint64_t(1) << 32) + (uint64_t)seg_heads - 1) / (uint64_t)seg_heads;
+  }
+  return o;
+}
+
+__device__ __forceinline__ int64_t operand_col(const GemmOperand &op, int col) {
+  if (op.seg_len == 0) return col;
+  const uint32_t s = (uint32_t)col >> op.seg_shift;
+  const uint32_t hq = (uint32_t)(((uint64_t)s * op.heads_magic) >> 32);
+  const uint32_t hr = s - hq * (uint32_t)op.seg_heads;
+  return (int64_t)hq * op.seg_hi + (int64_t)hr * op.seg_lo + (col & (op.seg_len - 1));
+}
 
 struct GemmProblem {
   GemmOperand A, B;
@@ -93,10 +118,15 @@ struct GemmProblem {
   const int8_t *alpha_exp2;  // optional: alpha is multiplied by 2^(*alpha_exp2)
 };
 
-// mode: 0 = bf16 x bf16 inputs on bf16 MFMA; 1 = fp32 MFMA with A/B of types ta/tb
+// mode: 0 = bf16 x bf16 inputs on bf16 MFMA; 1 = fp32 MFMA with A/B of types ta/tb;
+//       2 = bf16 MFMA with one fp32 operand split into bf16 hi + lo
 // converted exactly to fp32 (bf16, fp16 or fp32 inputs).
 hipError_t launch_gemm(const GemmProblem *probs_dev, int n_probs, int max_M, int max_N,
                        int mode, int ta, int tb, bool a_kcontig, bool b_kcontig, hipStream_t st);
+// bf16 matrix-core GEMM; ta/tb GT_BF16 (used as is) or GT_F32 (split into bf16 hi + lo,
+// at most one operand)
+hipError_t launch_gemm16(const GemmProblem *probs_dev, int n_probs, int max_M, int max_N, int ta,
+                         int tb, bool a_kcontig, bool b_kcontig, hipStream_t st);
 
 // ----------------------------------------------------------------- feature Gram / energy
 // F[cell] = sum over rows of x^T x for the row set {(s, r) : s < nseg, r < rows_per_seg}

@@ -168,14 +168,7 @@ void plan_decode(Carver &cv, Ws &w, int m, int T, int d, int nc, int kmax) {
 int dtype_gt(int dt) { return dt == JOLT_BF16 ? GT_BF16 : GT_F32; }
 
 GemmOperand cell_operand(const void *x, const jolt_cell_desc *d) {
-  GemmOperand o{};
-  o.ptr = x;
-  o.ld = d->stride_token;
-  o.seg_len = d->d;
-  o.seg_heads = d->n_heads;
-  o.seg_hi = d->stride_layer;
-  o.seg_lo = d->stride_head;
-  return o;
+  return seg_operand(x, d->stride_token, d->stride_layer, d->stride_head, d->d, d->n_heads);
 }
 
 GemmOperand plain(const void *p, int64_t ld) {
@@ -492,7 +485,7 @@ int token_flash(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc,
         p.C = R.w.Zsk + (int64_t)c * N * ldl; p.ldc = ldl;
         p.M = N; p.N = l; p.K = T; p.alpha = 1.f;
       }
-      rc = R.gemm(P, 1, dt, GT_F32, false, false);
+      rc = R.gemm(P, dt == GT_BF16 ? 2 : 1, dt, GT_F32, false, false);
       if (rc) return rc;
     }
     {
@@ -510,7 +503,7 @@ int token_flash(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc,
         p.C = R.w.Ysk + (int64_t)c * T * ldl; p.ldc = ldl;
         p.M = T; p.N = l; p.K = N; p.alpha = 1.f;
       }
-      rc = R.gemm(P, 1, dt, GT_F32, true, false);
+      rc = R.gemm(P, dt == GT_BF16 ? 2 : 1, dt, GT_F32, true, false);
       if (rc) return rc;
     }
     {
@@ -530,7 +523,7 @@ int token_flash(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc,
       p.C = R.w.Bsk + (int64_t)c * l * N; p.ldc = N;
       p.M = l; p.N = N; p.K = T; p.alpha = 1.f;
     }
-    rc = R.gemm(P, 1, GT_F32, dt, false, false);
+    rc = R.gemm(P, dt == GT_BF16 ? 2 : 1, GT_F32, dt, false, false);
     if (rc) return rc;
     for (int c = 0; c < nc; ++c) {                                   // B B^T   (l x l)
       GemmProblem &p = P[c];
@@ -708,7 +701,7 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
         P.push_back(p);
       }
       StageTimer t(R.ctx, R.st, JOLT_STAGE_PROJECT);
-      rc = R.gemm(P, 1, GT_F32, dtype_gt(desc->dtype), false, false);
+      rc = R.gemm(P, desc->dtype == JOLT_BF16 ? 2 : 1, GT_F32, dtype_gt(desc->dtype), false, false);
       if (rc) return rc;
     } else {
       // FlashJoLT: Ritz vectors W of B B^T, U_T = Q W, and Y = W_r^T B (no pass over X)
