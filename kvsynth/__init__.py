@@ -38,10 +38,16 @@ def _rng(*key: int) -> np.random.Generator:
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round fp32 values to bf16 (nearest, ties to even); return uint16 bits."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    rounding = ((u >> 16) & 1) + 0x7FFF
-    out = ((u + rounding) >> 16).astype(np.uint16)
-    nan = np.isnan(np.asarray(x, dtype=np.float32))
+    x32 = np.ascontiguousarray(x, dtype=np.float32)
+    u = x32.view(np.uint32)
+    # u + 0x7FFF + lsb stays below 2^32 for every non-NaN pattern; NaNs are replaced below
+    with np.errstate(over="ignore"):
+        r = (u >> 16) & np.uint32(1)
+        r += np.uint32(0x7FFF)
+        r += u
+        r >>= 16
+    out = r.astype(np.uint16)
+    nan = np.isnan(x32)
     if nan.any():
         out[nan] = 0x7FC0
     return out
@@ -92,26 +98,46 @@ def layer_alpha(layer: int, tensor: int, lo: float, hi: float, data_seed: int = 
 def make_cache(*, n_layers: int, n_heads: int, T: int, d: int, batch: int = 1,
                alpha_K=1.5, alpha_V=0.7, n_out: int = 2, out_scale: float = 10.0,
                noise: float = 0.05, dtype: str = "bf16", data_seed: int = 0,
-               layers=None):
+               layers=None, workers: int = 1):
     """Whole cache as two arrays [L][batch][n_heads][T][d].
 
     ``alpha_K`` / ``alpha_V`` are floats or (lo, hi) ranges for a per-layer
     draw.  ``dtype='bf16'`` returns uint16 bf16 bit patterns, ``'f32'`` returns
     float32.  ``layers`` restricts generation to a subset of layer indices.
+    ``workers > 1`` generates the (layer, K/V) slabs in that many processes; the
+    values do not depend on it.
     """
     layers = list(range(n_layers)) if layers is None else list(layers)
     shape = (len(layers), batch, n_heads, T, d)
     np_dt = np.uint16 if dtype == "bf16" else np.float32
     K = np.empty(shape, dtype=np_dt)
     V = np.empty(shape, dtype=np_dt)
+    jobs = []
     for i, l in enumerate(layers):
-        for t, (arr, a) in enumerate(((K, alpha_K), (V, alpha_V))):
+        for t, a in enumerate((alpha_K, alpha_V)):
             alpha = layer_alpha(l, t, *a, data_seed=data_seed) if isinstance(a, tuple) else a
-            x = layer_kv(layer=l, tensor=t, n_heads=n_heads, T=T, d=d, batch=batch,
-                         alpha=alpha, n_out=n_out, out_scale=out_scale, noise=noise,
-                         data_seed=data_seed)
-            arr[i] = f32_to_bf16_bits(x) if dtype == "bf16" else x
+            jobs.append((i, t, dict(layer=l, tensor=t, n_heads=n_heads, T=T, d=d, batch=batch,
+                                    alpha=alpha, n_out=n_out, out_scale=out_scale, noise=noise,
+                                    data_seed=data_seed, bf16=dtype == "bf16")))
+    if workers > 1 and len(jobs) > 1:
+        import concurrent.futures as cf
+        import multiprocessing as mp
+        with cf.ProcessPoolExecutor(max_workers=min(workers, len(jobs)),
+                                    mp_context=mp.get_context("spawn")) as ex:
+            results = ex.map(_layer_job, [j[2] for j in jobs])
+            for (i, t, _), x in zip(jobs, results):
+                (K, V)[t][i] = x
+    else:
+        for i, t, kw in jobs:
+            (K, V)[t][i] = _layer_job(kw)
     return K, V
+
+
+def _layer_job(kw):
+    kw = dict(kw)
+    bf16 = kw.pop("bf16")
+    x = layer_kv(**kw)
+    return f32_to_bf16_bits(x) if bf16 else x
 
 
 # Workload shapes (synthetic stand-ins for the paper's Mistral-7B / LLaMA-2-13B caches).

@@ -125,11 +125,11 @@ def st_hosvd(X: np.ndarray, U_T: np.ndarray, r_T: int, r_d: int):
     if r_T == 0:
         return np.zeros((T, 0)), np.zeros((d, 0)), np.zeros((m, 0, 0)), np.zeros(d)
     U = U_T[:, :r_T]
-    Y = np.einsum("std,tr->srd", X, U)          # Y_s = U^T X_s  (r_T x d)
+    Y = np.stack([U.T @ X[s] for s in range(m)])         # Y_s = U^T X_s  (r_T x d)
     Yf = Y.reshape(m * r_T, d)
     mu_Y, V = _eigh_desc(Yf.T @ Yf)             # feature spectrum of Y
     U_d = V[:, :r_d]
-    G = np.einsum("srd,dk->srk", Y, U_d)        # G_s = Y_s U_d  (r_T x r_d)
+    G = np.stack([Y[s] @ U_d for s in range(m)])         # G_s = Y_s U_d  (r_T x r_d)
     return U, U_d, G, mu_Y
 
 
@@ -160,5 +160,5 @@ def reconstruct(U_hat: np.ndarray, Ud_hat: np.ndarray, G_hat: np.ndarray,
     if U_hat.shape[1] == 0:
         return np.zeros((m, T, d))
     G = np.ldexp(G_hat, gexp[:, None, None])
-    W = np.einsum("srk,dk->srd", G, Ud_hat)     # W_s = G_s U_d^T  (r_T x d)
-    return np.einsum("tr,srd->std", U_hat, W)
+    W = [G[s] @ Ud_hat.T for s in range(m)]              # W_s = G_s U_d^T  (r_T x d)
+    return np.stack([U_hat @ W[s] for s in range(m)])    # X~_s = U_T W_s  (T x d)
