@@ -78,19 +78,22 @@ def stage_work(codec, calls):
     rd = [p.r_d for p in codec.params]
     bits = [p.bits for p in codec.params]
     work = {}
+    # products that read a bf16 cache run on the bf16 matrix cores (an fp32 partner operand is
+    # split into two bf16 terms, i.e. two MFMA passes); useful flops are charged at the bf16 peak
+    cache_mfma = "bf16" if in_b == 2 else "fp32"
     if flash:
         ell = codec.ell
-        # Y = X Omega on bf16 MFMA; per power iteration X^T Q and X Q' (fp32 MFMA), then B = Q^T X
-        # and B B^T (fp32 MFMA): charged at the fp32 peak, the lower of the two
+        # Y = X Omega, per power iteration X^T Q and X Q', then B = Q^T X (all over the cache),
+        # and B B^T (fp32 MFMA, < 1% of the flops)
         sk = nc * (2.0 * T * N * ell * (1 + 2 * codec.opts.power_iters + 1) + 2.0 * ell * ell * N)
-        work["sketch"] = ("fp32", sk * calls)
+        work["sketch"] = (cache_mfma, sk * calls)
         work["project"] = ("fp32", sum(2.0 * r * T * ell + 2.0 * r * ell * N for r in rT) * calls)
     else:
         # lower triangle of every trailing matrix, one read per column (fp32)
         sym_bytes = nc * sum(4.0 * Lr * (Lr + 1) / 2 for Lr in range(1, n))
         work["symv"] = ("hbm", sym_bytes * calls)
-        work["token_gram"] = ("bf16" if in_b == 2 else "fp32", nc * 2.0 * T * T * N * calls)
-        work["project"] = ("fp32", sum(2.0 * r * T * N for r in rT) * calls)
+        work["token_gram"] = (cache_mfma, nc * 2.0 * T * T * N * calls)
+        work["project"] = (cache_mfma, sum(2.0 * r * T * N for r in rT) * calls)
     rec = sum(2.0 * m * r * k * d + 2.0 * m * T * r * d for r, k in zip(rT, rd))
     work["reconstruct"] = ("fp32", 2 * rec * calls)           # compress and decompress
     res_b = sum(m * T * d * (in_b + (4 if r else 0)) + m * T * d * b / 8 + (2 * m * T * d / codec.group if b else 0)
@@ -125,7 +128,7 @@ def roofline_of(stage, kind, amount, ms, launches):
 
 
 def cpu_baseline(K_np, V_np, cfg, params, group, T_sample, method, q, p, iters,
-                 min_seconds=10.0, max_cells=4):
+                 min_seconds=10.0, max_cells=16):
     """fp64 oracle on whole cells (keys, then values, of layer groups 0, 1, ...) timed on
     the host cores until at least min_seconds of work (at most max_cells cells)."""
     import numpy as np

@@ -193,6 +193,34 @@ def test_blocked_tridiagonalisation_spectrum_and_subspace(dtype):
     assert np.linalg.norm(Xt - ref["Xtilde"]) <= max(tol, ptol) * np.linalg.norm(ex[0])
 
 
+@pytest.mark.parametrize("T,H", [(1001, 4), (900, 1)])
+def test_blocked_tridiagonalisation_ragged_and_rank_deficient(T, H):
+    """T = 1001: the last panel is ragged and rows are not 16-byte aligned; H = 1 with
+    T = 900 > N = 128: the token Gram has rank 128, so the trailing columns of the
+    reduction are numerically zero.  Spectrum within 1e-5 of lambda_1 (fp32 cell) and the
+    backbone error at a gapped rank within 1e-5 relative."""
+    X = keys_cell(T=T, H=H, seed=3)
+    xs, ex, desc = device_cells([X], "f32")
+    ws = workspace(desc, 1)
+    note("jolt_spectrum exact blocked", T, H)
+    E, lamT, lamd = J.jolt_spectrum(ctx(), desc, xs, None, None, ws)
+    sp = opl.spectrum(ex[0])
+    np.testing.assert_allclose(lamT[0], sp["lam_T"], rtol=0, atol=1e-5 * sp["lam_T"][0])
+    assert np.all(np.isfinite(lamT))
+    p = [J.Params(32, 32, 4, 64, J.JOLT_FACTOR_F32, 0, 0)]
+    blobs, _ = compress(xs, desc, p, ws=ws)
+    U = torch.empty((T, 32), device="cuda")
+    J.jolt_debug_export(ctx(), 0, 0, U)
+    U = U.cpu().numpy().astype(np.float64)
+    np.testing.assert_allclose(U.T @ U, np.eye(32), atol=1e-5)
+    ref = opl.compress_cell(ex[0], r_T=32, r_d=32, bits=4, group=64, seed=0, factor_bytes=4, spec=sp)
+    Xt = torch.empty((H, T, 128), device="cuda")
+    J.jolt_debug_export(ctx(), 2, 0, Xt)
+    Xt = Xt.cpu().numpy().astype(np.float64)
+    eb_gpu, eb_ref = opl.rel_error(ex[0], Xt), opl.rel_error(ex[0], ref["Xtilde"])
+    assert abs(eb_gpu / eb_ref - 1) < 1e-5, (eb_gpu, eb_ref)
+
+
 def test_workspace_overwrite_forgets_the_spectrum():
     """Reuse is explicit: after a decompress into the workspace that held the spectrum, a
     compress asking for reuse is refused, and one that recomputes equals a fresh one."""
