@@ -56,8 +56,12 @@ def parse():
     ap.add_argument("--cpu-sample-T", type=int, default=0,
                     help="tokens of the oracle sample cell (0 = the workload's T)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
-                    help="before the run, one device-to-device copy of this many MiB: the "
-                         "reference dispatch for scaling HBM traffic counters")
+                    help="before the run, one streaming pass (out = -in, fp32) that reads and "
+                         "writes this many MiB: the reference dispatch for scaling HBM "
+                         "traffic counters")
+    ap.add_argument("--no-stage-profile", action="store_true",
+                    help="skip the event-instrumented pass (for hardware-counter runs); the "
+                         "stage and roofline fields are then omitted")
     return ap.parse_args()
 
 
@@ -111,6 +115,32 @@ def stage_work(codec, calls):
             pg += 2 * 2.0 * rem * rem * jb
         work["panel_gemm"] = ("fp32", nc * pg * calls)
     return work
+
+
+# kernel source of each instrumented stage whose HBM traffic was taken with hardware counters
+STAGE_SOURCE = {"symv": "paper_2607_12550_amd/csrc/k_sytrd.hip"}
+
+
+def measured_traffic(stage, workload):
+    """HBM bytes per launch of a stage from the committed counter summary
+    profiles/traffic_<stage>_<workload>.md (lines 'traffic_bytes_per_launch: X' and
+    'source_sha256: H'); None when there is none or the kernel source changed since."""
+    import hashlib
+    src = STAGE_SOURCE.get(stage)
+    path = os.path.join(ROOT, "profiles", f"traffic_{stage}_{workload}.md")
+    if not src or not os.path.exists(path):
+        return None
+    with open(os.path.join(ROOT, src), "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and line.split(":", 1)[0].strip() in ("traffic_bytes_per_launch", "source_sha256"):
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip().strip("`")
+    if fields.get("source_sha256") != sha or "traffic_bytes_per_launch" not in fields:
+        return None
+    return float(fields["traffic_bytes_per_launch"])
 
 
 def roofline_of(stage, kind, amount, ms, launches):
@@ -192,12 +222,12 @@ def main():
         if cfg["dtype"] == "bf16" else (lambda a: torch.from_numpy(a).to(dev))
     K, V = to_dev(Knp), to_dev(Vnp)
     if args.calib_copy_mib:
-        src = torch.ones(args.calib_copy_mib << 20, dtype=torch.uint8, device=dev)
+        src = torch.ones((args.calib_copy_mib << 20) // 4, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
-        dst.copy_(src)
+        torch.neg(src, out=dst)
         torch.cuda.synchronize()
-        log(f"calibration copy: {args.calib_copy_mib} MiB read + written")
+        log(f"calibration pass: {args.calib_copy_mib} MiB read + written")
         del src, dst
     codec = CacheCodec(K, V, group_layers=gl, method=method, ratio=ratio,
                        oversample=args.oversample, power_iters=args.power_iters)
@@ -232,12 +262,14 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     # one extra instrumented step: HIP events around every stage / kernel launch
-    J.jolt_profile_enable(codec.ctx, True)
-    J.jolt_profile_reset(codec.ctx)
-    step()
-    torch.cuda.synchronize()
-    prof = J.jolt_profile_read(codec.ctx)
-    J.jolt_profile_enable(codec.ctx, False)
+    prof = {}
+    if not args.no_stage_profile:
+        J.jolt_profile_enable(codec.ctx, True)
+        J.jolt_profile_reset(codec.ctx)
+        step()
+        torch.cuda.synchronize()
+        prof = J.jolt_profile_read(codec.ctx)
+        J.jolt_profile_enable(codec.ctx, False)
 
     cache_bytes = codec.cache_bytes
     value = cache_bytes * args.steps / elapsed / 1e9
@@ -246,13 +278,16 @@ def main():
     comp_bytes = codec.compressed_bytes()
     alloc = [(p.r_T, p.r_d, p.bits) for p in codec.params]
     work = stage_work(codec, 1)
-    dom = max((s for s in prof if prof[s][0] > 0), key=lambda s: prof[s][0])
-    if dom in work:
-        kind, amount = work[dom]
-        roof = roofline_of(dom, kind, amount, prof[dom][0], prof[dom][1])
-    else:
-        roof = {"kernel": dom, "bound": "latency", "achieved": None, "peak": None, "unit": None,
-                "frac": None, "traffic": None}
+    roof = None
+    if prof:
+        dom = max((s for s in prof if prof[s][0] > 0), key=lambda s: prof[s][0])
+        if dom in work:
+            kind, amount = work[dom]
+            roof = roofline_of(dom, kind, amount, prof[dom][0], prof[dom][1])
+            roof["traffic"] = measured_traffic(dom, args.workload)
+        else:
+            roof = {"kernel": dom, "bound": "latency", "achieved": None, "peak": None, "unit": None,
+                    "frac": None, "traffic": None}
     stages = {s: {"ms_per_step": round(v[0], 3), "launches_per_step": v[1]}
               for s, v in prof.items() if v[1]}
     stage_roofs = {}

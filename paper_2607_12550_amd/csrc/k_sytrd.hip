@@ -67,7 +67,8 @@ JOLT_DEV MatView view(const SytrdArgs &a, int mat) {
 }
 
 // A22 x_tail partials for tile (I, J) of the trailing block.  Tiles are 128 x 128 on a grid
-// whose origin `base` is o rounded down to a multiple of 8 (so rows load as aligned float4);
+// whose origin `base` is o rounded down to a multiple of 32 (so the 128-float row segment a
+// tile reads covers exactly four 128-byte cache lines);
 // entries with row or column < o are masked to zero.  Thread (ty, tx) of the 16 x 16 grid
 // holds an 8 x 8 sub-block in registers; row sums reduce across tx (lane shuffles), column
 // sums across ty (shuffles, then LDS across the four waves).  Tiles (I, 0) also produce the
@@ -82,7 +83,7 @@ JOLT_DEV void householder(float alpha, double sigma, double &beta, double &tv, d
 // per 128-row block from o: v, y, w_pre and partial w_pre^T v for column i (panel index j)
 __global__ void __launch_bounds__(RB) k_col_finish(SytrdArgs a, int i, int j, int jbw) {
   const int mat = blockIdx.y, n = a.n, nb = a.nb, o = i + 1;
-  const int base = o & ~7, nt = (n - base + TB - 1) / TB;
+  const int base = o & ~31, nt = (n - base + TB - 1) / TB;
   const int nprev = (n - i + RB - 1) / RB;     // row blocks of the k_col_next launch that made x
   const MatView M = view(a, mat);
   __shared__ float pw[64], pv[64];
@@ -144,7 +145,7 @@ __global__ void __launch_bounds__(256) k_symv_tiles(SytrdArgs a, int i) {
   const bool rev = i & 1;
   const int mat = rev ? gridDim.y - 1 - blockIdx.y : blockIdx.y;
   const int n = a.n, o = i + 1;
-  const int base = o & ~7, Lb = n - base;
+  const int base = o & ~31, Lb = n - base;
   const MatView M = view(a, mat);
   int I, J;
   tri_decode(rev ? gridDim.x - 1 - blockIdx.x : blockIdx.x, I, J);
@@ -421,7 +422,7 @@ hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, const Gemm
     hook(JOLT_STAGE_PANEL, 0);
     for (int j = 0; j < jb; ++j) {
       const int i = k0 + j, o = i + 1, L = n - o;
-      const int nt = (n - (o & ~7) + TB - 1) / TB, nblk = (L + RB - 1) / RB;
+      const int nt = (n - (o & ~31) + TB - 1) / TB, nblk = (L + RB - 1) / RB;
       hook(JOLT_STAGE_SYMV, 1);
       hipLaunchKernelGGL(k_symv_tiles, dim3(nt * (nt + 1) / 2, nm), dim3(256), 0, st, a, i);
       hook(JOLT_STAGE_SYMV, 0);
