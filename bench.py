@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--ratio", type=float, default=0.0, help="0 = the workload's budget")
     ap.add_argument("--method", default="", choices=["", "exact", "flash"],
                     help="empty = the workload's method")
+    ap.add_argument("--allocator", default="joint", choices=["joint", "greedy", "rank_only", "uniform"],
+                    help="allocation strategy (the joint dual, or an ablation allocator)")
     ap.add_argument("--power-iters", type=int, default=1)
     ap.add_argument("--oversample", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -238,10 +240,12 @@ def main():
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
     t_comp, t_dec = [], []
 
+    alloc_res = {}
+
     def step():
         ev[0].record(stream)
         codec.spectrum(stream)
-        codec.allocate()
+        alloc_res.update(codec.allocate(strategy=args.allocator))
         codec.compress(stream)
         ev[1].record(stream)
         codec.decompress(Kout, Vout, stream)
@@ -311,13 +315,14 @@ def main():
         "config": {"workload": args.workload, "layers": cfg["n_layers"], "kv_heads": cfg["n_heads"],
                    "T": cfg["T"], "head_dim": cfg["d"], "batch": cfg["batch"], "group_layers": gl,
                    "cells": len(codec.cells), "method": method, "ratio": ratio,
-                   "cache_bytes": cache_bytes},
+                   "allocator": args.allocator, "cache_bytes": cache_bytes},
         "compress_GBps": round(cache_bytes / (np.median(t_comp) * 1e-3) / 1e9, 3),
         "decompress_GBps": round(cache_bytes / (np.median(t_dec) * 1e-3) / 1e9, 3),
         "rel_frobenius_error": {"K": round(float(eK.mean()), 6), "V": round(float(eV.mean()), 6)},
         "achieved_ratio": round(cache_bytes / comp_bytes, 4),
         "achieved_ratio_eq1_payload": round(cache_bytes / codec.payload_bytes(), 4),
         "allocation": alloc,
+        "allocation_model_error": alloc_res.get("model_error"),
         "stage_ms_per_step": stages,
         "stage_roofline": stage_roofs,
         "roofline": roof,

@@ -107,7 +107,7 @@ typedef struct {
   int32_t g;             /* quantiser group size */
   int32_t n_lam_T;       /* entries of lam_T */
   int32_t rT_max;        /* largest admissible r_T */
-  int32_t reserved;
+  int32_t pool;          /* budget pool (e.g. 0 = keys, 1 = values) for JOLT_ALLOC_GREEDY */
   double E;              /* ||X||_F^2 */
   const double *lam_T;   /* token-mode eigenvalues, descending (FlashJoLT: q_eff values
                             followed by the synthetic tail) */
@@ -121,7 +121,23 @@ typedef struct {
   int32_t step;          /* rank grid step (ranks are multiples of step) */
   int32_t floor_rT, floor_rd, floor_bits; /* per-cell floors (0 = none) */
   int32_t count_scale_bytes;              /* 1: add 2 bytes per quantiser group to s */
+  int32_t strategy;      /* JOLT_ALLOC_JOINT (0, the default) or an ablation allocator */
 } jolt_alloc_opts;
+
+/* Allocation strategies.  JOINT is the Lagrangian dual of eq. (3)-(4).  The others are
+ * the simpler schemes of the section 7 ablations (A1, A5), on the same grid, costs and
+ * model errors:
+ *   RANK_ONLY: the joint dual without residual (only b = 0 is allowed);
+ *   GREEDY:    every cell starts at its cheapest grid point and the upgrade with the
+ *              largest model-error reduction per extra byte is taken repeatedly (a cell's
+ *              upgrades walk its Pareto frontier one point at a time; upgrades that do not
+ *              fit are skipped; equal efficiencies go to the lower cell index).  No global
+ *              multiplier: each pool (jolt_cell_spectrum.pool) spends its own share of the
+ *              budget, proportional to its cells' m T d;
+ *   UNIFORM:   one (r_T, r_d, b) for every cell, the one of least summed model error whose
+ *              summed cost fits (ties to the smaller cost, then b, r_T, r_d).
+ * lambda_star is 0 for GREEDY and UNIFORM. */
+enum { JOLT_ALLOC_JOINT = 0, JOLT_ALLOC_GREEDY = 1, JOLT_ALLOC_RANK_ONLY = 2, JOLT_ALLOC_UNIFORM = 3 };
 
 const char *jolt_last_error(void);
 
@@ -208,9 +224,10 @@ int jolt_decompress(jolt_ctx *ctx, int n_cells, const void *const *blobs, const 
 /* Budgeted allocation (section 4, eq. (1)-(4); host only, no device work): for every
  * cell the grid point (r_T, r_d, b) minimising eq. (2)'s model error plus lambda times
  * eq. (1)'s bytes, with lambda found by bisection so that the summed bytes meet the
- * budget.  Outputs (host, n_cells each) r_T, r_d, bits; lambda_star, total bytes and
- * summed model error.  *infeasible is 1 when even the cheapest grid point of every cell
- * exceeds the budget (the cheapest allocation is then returned). */
+ * budget (opts->strategy selects an ablation allocator instead, see JOLT_ALLOC_*).
+ * Outputs (host, n_cells each) r_T, r_d, bits; lambda_star, total bytes and summed
+ * model error.  *infeasible is 1 when even the cheapest grid point of every cell (of a
+ * pool, for GREEDY) exceeds the budget (the cheapest allocation is then returned). */
 int jolt_allocate(const jolt_cell_spectrum *cells, int n_cells, const jolt_alloc_opts *opts,
                   int32_t *r_T, int32_t *r_d, int32_t *bits, double *lambda_star,
                   double *total_bytes, double *model_error, int32_t *infeasible);

@@ -79,56 +79,62 @@ class CellSpectrum:
     extra: dict = field(default_factory=dict)
 
 
+def cell_grid(cell, eps2: dict, *, bits=BIT_GRID, step: int = 8, floors=(0, 0, 0),
+              count_scales: bool = True):
+    """Grid points of one cell ordered by (cost, b, r_T, r_d): arrays s, e and P = [s, b, r_T, r_d]."""
+    tau_T = tail_fractions(cell.lam_T, cell.E)
+    tau_d = tail_fractions(cell.lam_d, cell.E)
+    fT, fd, fb = floors
+    rTs = [0] + list(range(step, cell.rT_max + 1, step))
+    rds = list(range(step, cell.d + 1, step))
+    pts = []
+    for b in bits:
+        if b < fb:
+            continue
+        for rT in rTs:
+            if rT < fT:
+                continue
+            for rd in ([0] if rT == 0 else rds):
+                if rT > 0 and rd < fd:
+                    continue
+                pts.append((byte_cost(cell.m, cell.T, cell.d, rT, rd, b, cell.c,
+                                      cell.g, count_scales), b, rT, rd))
+    if not pts:
+        raise ValueError("empty allocation grid (floors exclude every point)")
+    pts.sort()
+    P = np.array(pts, dtype=np.int64)
+    s = P[:, 0].astype(np.float64)
+    eb = np.array([float(eps2[int(x)]) for x in P[:, 1]])
+    e = eb * np.minimum(1.0, tau_T[P[:, 2]] + tau_d[P[:, 3]])
+    return s, e, P
+
+
+def _result(grids, idx, lam, infeasible):
+    alloc = [tuple(int(v) for v in g[2][i][[2, 3, 1]]) for g, i in zip(grids, idx)]
+    total = float(sum(g[0][i] for g, i in zip(grids, idx)))
+    err = float(sum(g[1][i] for g, i in zip(grids, idx)))
+    return dict(alloc=alloc, lam=lam, total_bytes=total, model_error=err,
+                infeasible=infeasible)
+
+
 def allocate(cells, budget: float, eps2: dict, *, bits=BIT_GRID, step: int = 8,
              floors=(0, 0, 0), count_scales: bool = True):
     """Solve eq. (3) through eq. (4); returns dict(alloc=[(r_T, r_d, b)], ...)."""
-    grids = []
-    for cell in cells:
-        tau_T = tail_fractions(cell.lam_T, cell.E)
-        tau_d = tail_fractions(cell.lam_d, cell.E)
-        fT, fd, fb = floors
-        rTs = [0] + list(range(step, cell.rT_max + 1, step))
-        rds = list(range(step, cell.d + 1, step))
-        pts = []
-        for b in bits:
-            if b < fb:
-                continue
-            for rT in rTs:
-                if rT < fT:
-                    continue
-                for rd in ([0] if rT == 0 else rds):
-                    if rT > 0 and rd < fd:
-                        continue
-                    pts.append((byte_cost(cell.m, cell.T, cell.d, rT, rd, b, cell.c,
-                                          cell.g, count_scales), b, rT, rd))
-        if not pts:
-            raise ValueError("empty allocation grid (floors exclude every point)")
-        pts.sort()
-        P = np.array(pts, dtype=np.int64)
-        s = P[:, 0].astype(np.float64)
-        eb = np.array([float(eps2[int(x)]) for x in P[:, 1]])
-        e = eb * np.minimum(1.0, tau_T[P[:, 2]] + tau_d[P[:, 3]])
-        grids.append((s, e, P))
+    grids = [cell_grid(c, eps2, bits=bits, step=step, floors=floors, count_scales=count_scales)
+             for c in cells]
 
     def choose(lam):
         idx = [int(np.argmin(e + lam * s)) for (s, e, _) in grids]
         total = float(sum(g[0][i] for g, i in zip(grids, idx)))
         return idx, total
 
-    def result(idx, lam, infeasible):
-        alloc = [tuple(int(v) for v in g[2][i][[2, 3, 1]]) for g, i in zip(grids, idx)]
-        total = float(sum(g[0][i] for g, i in zip(grids, idx)))
-        err = float(sum(g[1][i] for g, i in zip(grids, idx)))
-        return dict(alloc=alloc, lam=lam, total_bytes=total, model_error=err,
-                    infeasible=infeasible)
-
     idx0, S0 = choose(0.0)
     if S0 <= budget:
-        return result(idx0, 0.0, False)
+        return _result(grids, idx0, 0.0, False)
     lo, hi = 0.0, LAMBDA_HI
     idx_hi, S_hi = choose(hi)
     if S_hi > budget:
-        return result(idx_hi, hi, True)
+        return _result(grids, idx_hi, hi, True)
     for _ in range(MAX_HALVINGS):
         if hi - lo <= 1e-15 * hi:
             break
@@ -138,7 +144,105 @@ def allocate(cells, budget: float, eps2: dict, *, bits=BIT_GRID, step: int = 8,
             hi, idx_hi = mid, idx_mid
         else:
             lo = mid
-    return result(idx_hi, hi, False)
+    return _result(grids, idx_hi, hi, False)
+
+
+# --------------------------------------------------------------------- ablation allocators
+# Section 7 ablations (A1, A5) compare the joint dual with three simpler schemes.  The
+# paper describes them in words; the readings written out here (identically in the
+# library) are:
+#
+# * rank-only: the joint dual with no residual, i.e. the bit grid {0};
+# * greedy: every cell starts at its cheapest grid point and repeatedly takes the upgrade,
+#   among all cells, with the largest error reduction per extra byte.  A cell's upgrades
+#   walk its Pareto frontier (the points, in grid order, whose error is below that of
+#   every cheaper point), one frontier point at a time; an upgrade that would exceed the
+#   remaining budget is skipped.  There is no global multiplier: the cells are split into
+#   pools (keys and values) and each pool spends its own share of the budget, in
+#   proportion to its cells' m T d.  Equal efficiencies go to the lower cell index; an
+#   upgrade of zero extra bytes is taken first;
+# * uniform: one (r_T, r_d, b) shared by every cell, the one of least summed error whose
+#   summed cost fits the budget (ties to the smaller cost, then b, r_T, r_d).
+def _pareto(s, e):
+    keep, best = [], math.inf
+    for k in range(len(s)):
+        if e[k] < best:
+            keep.append(k)
+            best = e[k]
+    return keep
+
+
+def allocate_greedy(cells, budget: float, eps2: dict, pools, *, bits=BIT_GRID, step: int = 8,
+                    floors=(0, 0, 0), count_scales: bool = True):
+    grids = [cell_grid(c, eps2, bits=bits, step=step, floors=floors, count_scales=count_scales)
+             for c in cells]
+    fronts = [_pareto(g[0], g[1]) for g in grids]
+    cur = [0] * len(cells)
+    size = [c.m * c.T * c.d for c in cells]
+    total_size = sum(size)
+    infeasible = False
+    for pool in sorted(set(pools)):
+        members = [i for i, p in enumerate(pools) if p == pool]
+        share = budget * sum(size[i] for i in members) / total_size
+        spent = sum(grids[i][0][fronts[i][0]] for i in members)
+        if spent > share:
+            infeasible = True
+            continue
+        while True:
+            best, best_eff = -1, -math.inf
+            for i in members:
+                f = fronts[i]
+                if cur[i] + 1 >= len(f):
+                    continue
+                k0, k1 = f[cur[i]], f[cur[i] + 1]
+                ds = grids[i][0][k1] - grids[i][0][k0]
+                if spent + ds > share:
+                    continue
+                de = grids[i][1][k0] - grids[i][1][k1]
+                eff = math.inf if ds == 0 else de / ds
+                if eff > best_eff:
+                    best, best_eff = i, eff
+            if best < 0:
+                break
+            f = fronts[best]
+            spent += grids[best][0][f[cur[best] + 1]] - grids[best][0][f[cur[best]]]
+            cur[best] += 1
+    idx = [fronts[i][cur[i]] for i in range(len(cells))]
+    return _result(grids, idx, 0.0, infeasible)
+
+
+def allocate_uniform(cells, budget: float, eps2: dict, *, bits=BIT_GRID, step: int = 8,
+                     floors=(0, 0, 0), count_scales: bool = True):
+    grids = [cell_grid(c, eps2, bits=bits, step=step, floors=floors, count_scales=count_scales)
+             for c in cells]
+    where = []
+    for s, e, P in grids:
+        where.append({(int(b), int(rT), int(rd)): k for k, (_, b, rT, rd) in enumerate(P)})
+    common = set(where[0])
+    for w in where[1:]:
+        common &= set(w)
+    cands = []
+    for t in common:
+        S = 0.0
+        Err = 0.0
+        for g, w in zip(grids, where):
+            S += g[0][w[t]]
+            Err += g[1][w[t]]
+        cands.append((S, t[0], t[1], t[2], Err))
+    if not cands:
+        raise ValueError("no grid point common to every cell")
+    cands.sort()
+    fit = [c for c in cands if c[0] <= budget]
+    infeasible = not fit
+    if fit:
+        pick, best = None, math.inf
+        for c in fit:
+            if c[4] < best:
+                pick, best = c, c[4]
+    else:
+        pick = cands[0]
+    t = (pick[1], pick[2], pick[3])
+    return _result(grids, [w[t] for w in where], 0.0, infeasible)
 
 
 def allocation_cost(cells, alloc, *, count_scales=True) -> float:

@@ -66,14 +66,14 @@ class Params(C.Structure):
 class CellSpectrum(C.Structure):
     _fields_ = [("m", C.c_int32), ("T", C.c_int32), ("d", C.c_int32), ("c", C.c_int32),
                 ("g", C.c_int32), ("n_lam_T", C.c_int32), ("rT_max", C.c_int32),
-                ("reserved", C.c_int32), ("E", C.c_double),
+                ("pool", C.c_int32), ("E", C.c_double),
                 ("lam_T", C.POINTER(C.c_double)), ("lam_d", C.POINTER(C.c_double))]
 
 
 class AllocOpts(C.Structure):
     _fields_ = [("budget_bytes", C.c_double), ("eps2", C.c_double * 4), ("bit_mask", C.c_int32),
                 ("step", C.c_int32), ("floor_rT", C.c_int32), ("floor_rd", C.c_int32),
-                ("floor_bits", C.c_int32), ("count_scale_bytes", C.c_int32)]
+                ("floor_bits", C.c_int32), ("count_scale_bytes", C.c_int32), ("strategy", C.c_int32)]
 
 
 _vp, _sz, _i32, _dbl = C.c_void_p, C.c_size_t, C.c_int32, C.c_double
@@ -235,9 +235,13 @@ def jolt_decompress(ctx, blobs, out_desc: CellDesc, Xhat, ws=None, hdr_host=None
                                _ptrs(Xhat), _addr(ws), wsb, _stream(stream)))
 
 
+ALLOC_STRATEGIES = {"joint": 0, "greedy": 1, "rank_only": 2, "uniform": 3}
+
+
 def jolt_allocate(cells, budget_bytes: float, eps2, *, bits=(0, 2, 4, 8), step: int = 8,
-                  floors=(0, 0, 0), count_scale_bytes: bool = True) -> dict:
-    """cells: dicts with m, T, d, c, g, E, lam_T, lam_d, rT_max (numpy arrays for lam_*)."""
+                  floors=(0, 0, 0), count_scale_bytes: bool = True, strategy: str = "joint") -> dict:
+    """cells: dicts with m, T, d, c, g, E, lam_T, lam_d, rT_max (numpy arrays for lam_*) and
+    optionally pool (budget pool of the greedy allocator, default 0)."""
     n = len(cells)
     keep = []
     arr = (CellSpectrum * n)()
@@ -245,12 +249,13 @@ def jolt_allocate(cells, budget_bytes: float, eps2, *, bits=(0, 2, 4, 8), step: 
         lt = np.ascontiguousarray(c["lam_T"], dtype=np.float64)
         ld = np.ascontiguousarray(c["lam_d"], dtype=np.float64)
         keep += [lt, ld]
-        arr[i] = CellSpectrum(c["m"], c["T"], c["d"], c["c"], c["g"], len(lt), c["rT_max"], 0,
-                              c["E"], lt.ctypes.data_as(_P(_dbl)), ld.ctypes.data_as(_P(_dbl)))
+        arr[i] = CellSpectrum(c["m"], c["T"], c["d"], c["c"], c["g"], len(lt), c["rT_max"],
+                              int(c.get("pool", 0)), c["E"], lt.ctypes.data_as(_P(_dbl)),
+                              ld.ctypes.data_as(_P(_dbl)))
     mask = sum(1 << i for i, b in enumerate((0, 2, 4, 8)) if b in bits)
     e4 = (C.c_double * 4)(*[float(eps2[b]) for b in (0, 2, 4, 8)])
     o = AllocOpts(budget_bytes, e4, mask, step, floors[0], floors[1], floors[2],
-                  1 if count_scale_bytes else 0)
+                  1 if count_scale_bytes else 0, ALLOC_STRATEGIES[strategy])
     rT, rd, bb = (_i32 * n)(), (_i32 * n)(), (_i32 * n)()
     lam, tot, err, inf = _dbl(), _dbl(), _dbl(), _i32()
     _check(lib.jolt_allocate(arr, n, C.byref(o), rT, rd, bb, C.byref(lam), C.byref(tot),

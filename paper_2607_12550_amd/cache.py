@@ -134,15 +134,19 @@ class CacheCodec:
         self.spectra_fresh = True
         return self.spectra
 
-    def allocate(self, budget_bytes=None):
+    def allocate(self, budget_bytes=None, strategy: str = "joint"):
+        """Ranks and bits of every cell under the byte budget: the joint Lagrangian dual, or
+        one of the ablation allocators ("greedy", "rank_only", "uniform"; the greedy one
+        spends the keys' and the values' shares separately)."""
         E, LT, LD = self.spectra
         L, B, H, T, d = self.shape
         m = self.group_layers * H
         cells = [dict(m=m, T=T, d=d, c=self.fbytes, g=self.group, E=float(E[i]), lam_T=LT[i],
-                      lam_d=LD[i], rT_max=self.rT_max) for i in range(len(self.cells))]
+                      lam_d=LD[i], rT_max=self.rT_max, pool=self.cells[i].tensor)
+                 for i in range(len(self.cells))]
         budget = self.cache_bytes / self.ratio if budget_bytes is None else budget_bytes
         res = jolt_allocate(cells, budget, self.eps2, bits=self.bits, step=self.step,
-                            count_scale_bytes=self.count_scale_bytes)
+                            count_scale_bytes=self.count_scale_bytes, strategy=strategy)
         self.set_params([Params(rT, rd, b, self.group, self.factor_dtype, 0, s)
                          for (rT, rd, b), s in zip(res["alloc"], self.seeds)])
         return res

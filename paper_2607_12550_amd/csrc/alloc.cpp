@@ -14,9 +14,16 @@
 // eigenvalue upward; the bisection halves [0, 1e3] until hi - lo <= 1e-15 hi (at
 // most 200 halvings) and returns the allocation at hi.  This file is compiled
 // without floating-point contraction so the arithmetic is plain IEEE double.
+//
+// The ablation allocators of section 7 (rank-only, greedy, uniform rank) use the same
+// grid, costs and model errors; their definitions are stated with JOLT_ALLOC_* in the
+// public header.
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <limits>
+#include <map>
+#include <set>
 #include <tuple>
 #include <vector>
 
@@ -53,6 +60,16 @@ int64_t byte_cost(int64_t m, int64_t T, int64_t d, int64_t rT, int64_t rd, int64
   return s;
 }
 
+// Pareto frontier of a grid in grid order: the points whose error is below that of every
+// earlier (cheaper or equal-cost, earlier-ordered) point
+std::vector<int> pareto(const std::vector<Point> &pts) {
+  std::vector<int> keep;
+  double best = std::numeric_limits<double>::infinity();
+  for (int k = 0; k < (int)pts.size(); ++k)
+    if (pts[k].e < best) { keep.push_back(k); best = pts[k].e; }
+  return keep;
+}
+
 }  // namespace
 
 extern "C" int jolt_allocate(const jolt_cell_spectrum *cells, int n_cells, const jolt_alloc_opts *o,
@@ -62,7 +79,10 @@ extern "C" int jolt_allocate(const jolt_cell_spectrum *cells, int n_cells, const
     return jolt_fail(JOLT_E_INVAL, "jolt_allocate: null argument or negative cell count");
   if (o->step < 1) return jolt_fail(JOLT_E_INVAL, "jolt_allocate: step must be >= 1");
   if (!(o->budget_bytes >= 0.0)) return jolt_fail(JOLT_E_INVAL, "jolt_allocate: budget must be >= 0");
+  if (o->strategy < JOLT_ALLOC_JOINT || o->strategy > JOLT_ALLOC_UNIFORM)
+    return jolt_fail(JOLT_E_INVAL, "jolt_allocate: unknown strategy %d", o->strategy);
   const int bit_values[4] = {0, 2, 4, 8};
+  const int mask = o->strategy == JOLT_ALLOC_RANK_ONLY ? (o->bit_mask & 1) : o->bit_mask;
   std::vector<std::vector<Point>> grids(n_cells);
   for (int ci = 0; ci < n_cells; ++ci) {
     const jolt_cell_spectrum &c = cells[ci];
@@ -73,7 +93,7 @@ extern "C" int jolt_allocate(const jolt_cell_spectrum *cells, int n_cells, const
     const std::vector<double> td = tail_fractions(c.lam_d, c.d, c.E);
     std::vector<Point> &pts = grids[ci];
     for (int bi = 0; bi < 4; ++bi) {
-      if (!(o->bit_mask & (1 << bi))) continue;
+      if (!(mask & (1 << bi))) continue;
       const int b = bit_values[bi];
       if (b < o->floor_bits) continue;
       std::vector<int> rTs{0};
@@ -102,6 +122,98 @@ extern "C" int jolt_allocate(const jolt_cell_spectrum *cells, int n_cells, const
     });
   }
   std::vector<int> idx(n_cells), idx_hi(n_cells);
+  auto emit = [&](const std::vector<int> &sel, double lam, int infeas) {
+    double tb = 0.0, te = 0.0;
+    for (int ci = 0; ci < n_cells; ++ci) {
+      const Point &p = grids[ci][sel[ci]];
+      r_T[ci] = p.rT; r_d[ci] = p.rd; bits[ci] = p.b;
+      tb += (double)p.s; te += p.e;
+    }
+    if (lambda_star) *lambda_star = lam;
+    if (total_bytes) *total_bytes = tb;
+    if (model_error) *model_error = te;
+    if (infeasible) *infeasible = infeas;
+    return JOLT_OK;
+  };
+  const double B = o->budget_bytes;
+  if (o->strategy == JOLT_ALLOC_GREEDY) {
+    std::vector<std::vector<int>> front(n_cells);
+    for (int ci = 0; ci < n_cells; ++ci) front[ci] = pareto(grids[ci]);
+    std::vector<int> cur(n_cells, 0);
+    double total_size = 0.0;
+    for (int ci = 0; ci < n_cells; ++ci) total_size += (double)cells[ci].m * cells[ci].T * cells[ci].d;
+    std::set<int> pools;
+    for (int ci = 0; ci < n_cells; ++ci) pools.insert(cells[ci].pool);
+    int infeas = 0;
+    for (int pool : pools) {
+      std::vector<int> mem;
+      double size = 0.0, spent = 0.0;
+      for (int ci = 0; ci < n_cells; ++ci)
+        if (cells[ci].pool == pool) {
+          mem.push_back(ci);
+          size += (double)cells[ci].m * cells[ci].T * cells[ci].d;
+        }
+      const double share = B * size / total_size;
+      for (int ci : mem) spent += (double)grids[ci][front[ci][0]].s;
+      if (spent > share) { infeas = 1; continue; }
+      for (;;) {
+        int best = -1;
+        double best_eff = -std::numeric_limits<double>::infinity();
+        for (int ci : mem) {
+          const std::vector<int> &f = front[ci];
+          if (cur[ci] + 1 >= (int)f.size()) continue;
+          const Point &p0 = grids[ci][f[cur[ci]]], &p1 = grids[ci][f[cur[ci] + 1]];
+          const double ds = (double)p1.s - (double)p0.s;
+          if (spent + ds > share) continue;
+          const double de = p0.e - p1.e;
+          const double eff = ds == 0.0 ? std::numeric_limits<double>::infinity() : de / ds;
+          if (eff > best_eff) { best = ci; best_eff = eff; }
+        }
+        if (best < 0) break;
+        const std::vector<int> &f = front[best];
+        spent += (double)grids[best][f[cur[best] + 1]].s - (double)grids[best][f[cur[best]]].s;
+        ++cur[best];
+      }
+    }
+    for (int ci = 0; ci < n_cells; ++ci) idx[ci] = front[ci][cur[ci]];
+    return emit(idx, 0.0, infeas);
+  }
+  if (o->strategy == JOLT_ALLOC_UNIFORM) {
+    // points shared by every cell, keyed by (b, r_T, r_d)
+    std::vector<std::map<std::tuple<int, int, int>, int>> where(n_cells);
+    for (int ci = 0; ci < n_cells; ++ci)
+      for (int k = 0; k < (int)grids[ci].size(); ++k)
+        where[ci][std::make_tuple(grids[ci][k].b, grids[ci][k].rT, grids[ci][k].rd)] = k;
+    struct Cand { double S; int b, rT, rd; double err; };
+    std::vector<Cand> cands;
+    if (n_cells > 0) {
+      for (const auto &kv : where[0]) {
+        bool shared = true;
+        for (int ci = 1; ci < n_cells && shared; ++ci) shared = where[ci].count(kv.first) > 0;
+        if (!shared) continue;
+        double S = 0.0, err = 0.0;
+        for (int ci = 0; ci < n_cells; ++ci) {
+          const Point &p = grids[ci][where[ci].at(kv.first)];
+          S += (double)p.s;
+          err += p.e;
+        }
+        cands.push_back(Cand{S, std::get<0>(kv.first), std::get<1>(kv.first), std::get<2>(kv.first), err});
+      }
+      if (cands.empty()) return jolt_fail(JOLT_E_INVAL, "jolt_allocate: no grid point common to every cell");
+    }
+    std::sort(cands.begin(), cands.end(), [](const Cand &a, const Cand &b) {
+      return std::make_tuple(a.S, a.b, a.rT, a.rd) < std::make_tuple(b.S, b.b, b.rT, b.rd);
+    });
+    int pick = -1;
+    double best = std::numeric_limits<double>::infinity();
+    for (int k = 0; k < (int)cands.size(); ++k)
+      if (cands[k].S <= B && cands[k].err < best) { pick = k; best = cands[k].err; }
+    const int infeas = (pick < 0 && !cands.empty()) ? 1 : 0;
+    if (pick < 0) pick = 0;
+    for (int ci = 0; ci < n_cells; ++ci)
+      idx[ci] = where[ci].at(std::make_tuple(cands[pick].b, cands[pick].rT, cands[pick].rd));
+    return emit(idx, 0.0, infeas);
+  }
   auto choose = [&](double lam, std::vector<int> &out) {
     double total = 0.0;
     for (int ci = 0; ci < n_cells; ++ci) {
@@ -117,20 +229,6 @@ extern "C" int jolt_allocate(const jolt_cell_spectrum *cells, int n_cells, const
     }
     return total;
   };
-  auto emit = [&](const std::vector<int> &sel, double lam, int infeas) {
-    double tb = 0.0, te = 0.0;
-    for (int ci = 0; ci < n_cells; ++ci) {
-      const Point &p = grids[ci][sel[ci]];
-      r_T[ci] = p.rT; r_d[ci] = p.rd; bits[ci] = p.b;
-      tb += (double)p.s; te += p.e;
-    }
-    if (lambda_star) *lambda_star = lam;
-    if (total_bytes) *total_bytes = tb;
-    if (model_error) *model_error = te;
-    if (infeasible) *infeasible = infeas;
-    return JOLT_OK;
-  };
-  const double B = o->budget_bytes;
   if (choose(0.0, idx) <= B) return emit(idx, 0.0, 0);
   double lo = 0.0, hi = 1e3;
   if (choose(hi, idx_hi) > B) return emit(idx_hi, hi, 1);

@@ -85,6 +85,33 @@ def test_allocator_bit_identical_to_oracle(rng, flash):
             assert got["infeasible"] == ref["infeasible"]
 
 
+@pytest.mark.parametrize("strategy", ["greedy", "uniform", "rank_only"])
+def test_ablation_allocators_bit_identical_to_oracle(rng, strategy):
+    """Section 7 ablation allocators: the library and the oracle agree bit for bit on
+    allocation, bytes, model error and the infeasible flag (keys / values pools)."""
+    cells = _spectra(rng, 6)
+    for i, c in enumerate(cells):
+        c["pool"] = i % 2
+    eps2 = oalloc.calibrate_eps2(group=16, d=32, n_samples=1 << 14)
+    ocells = [oalloc.CellSpectrum(m=c["m"], T=c["T"], d=c["d"], c=c["c"], g=c["g"], E=c["E"],
+                                  lam_T=c["lam_T"], lam_d=c["lam_d"], rT_max=c["rT_max"])
+              for c in cells]
+    total_in = sum(c["m"] * c["T"] * c["d"] * 2 for c in cells)
+    for ratio in (1.3, 2.0, 3.0, 5.0, 9.0, 40.0):
+        B = total_in / ratio
+        got = J.jolt_allocate(cells, B, eps2, strategy=strategy)
+        if strategy == "greedy":
+            ref = oalloc.allocate_greedy(ocells, B, eps2, [c["pool"] for c in cells])
+        elif strategy == "uniform":
+            ref = oalloc.allocate_uniform(ocells, B, eps2)
+        else:
+            ref = oalloc.allocate(ocells, B, eps2, bits=(0,))
+        assert got["alloc"] == [tuple(a) for a in ref["alloc"]], (ratio, strategy)
+        assert got["total_bytes"] == ref["total_bytes"]
+        assert got["model_error"] == ref["model_error"]
+        assert got["infeasible"] == ref["infeasible"]
+
+
 def test_allocator_floors_and_infeasible(rng):
     cells = _spectra(rng, 3)
     eps2 = {0: 1.0, 2: 0.26, 4: 0.01, 8: 3.5e-5}

@@ -102,3 +102,73 @@ def test_generous_budget_gives_min_error_and_tiny_budget_flags(rng):
     assert tiny["infeasible"] and all(a[0] >= 8 for a in tiny["alloc"])
     zero = alloc.allocate(cells, 0.0, eps2)
     assert not zero["infeasible"] and zero["alloc"] == [(0, 0, 0)] * 2
+
+
+# ------------------------------------------------------------------ ablation allocators (section 7)
+EPS2 = {0: 1.0, 2: 0.26, 4: 0.0101, 8: 3.5e-5}
+
+
+def test_rank_only_is_the_optimum_without_residual(rng):
+    """Rank-only spends nothing on residual bits and, at the bytes it spends, no
+    residual-free allocation has a smaller summed model error (brute force)."""
+    cells = _cells(rng, 3)
+    per = [[p for p in grid if p[2][2] == 0] for grid in _enumerate(cells, EPS2, 8)]
+    total_in = sum(c.m * c.T * c.d * 2 for c in cells)
+    for ratio in (2.0, 4.0, 8.0):
+        res = alloc.allocate(cells, total_in / ratio, EPS2, bits=(0,))
+        assert all(b == 0 for _, _, b in res["alloc"])
+        best = min(sum(p[1] for p in combo) for combo in itertools.product(*per)
+                   if sum(p[0] for p in combo) <= res["total_bytes"])
+        assert res["model_error"] <= best + 1e-15
+
+
+def test_greedy_single_cell_takes_the_best_point_within_budget(rng):
+    """With one cell the frontier walk stops at the least-error point that fits: the
+    brute-force optimum of a single cell."""
+    cell = _cells(rng, 1)
+    per = _enumerate(cell, EPS2, 8)[0]
+    full = cell[0].m * cell[0].T * cell[0].d * 2
+    for ratio in (1.3, 2.0, 3.0, 5.0, 12.0):
+        B = full / ratio
+        res = alloc.allocate_greedy(cell, B, EPS2, [0])
+        best = min(p[1] for p in per if p[0] <= B)
+        assert res["total_bytes"] <= B
+        assert res["model_error"] == best
+
+
+def test_greedy_pools_spend_their_own_share(rng):
+    """Keys and values are separate pools: each spends at most its share of the budget,
+    and changing one pool's cells leaves the other pool's allocation unchanged."""
+    cells = _cells(rng, 4)
+    pools = [0, 0, 1, 1]
+    total_in = sum(c.m * c.T * c.d * 2 for c in cells)
+    for ratio in (2.0, 4.0):
+        B = total_in / ratio
+        res = alloc.allocate_greedy(cells, B, EPS2, pools)
+        spend = [alloc.byte_cost(c.m, c.T, c.d, rT, rd, b, c.c, c.g)
+                 for c, (rT, rd, b) in zip(cells, res["alloc"])]
+        assert spend[0] + spend[1] <= B / 2 and spend[2] + spend[3] <= B / 2
+        other = _cells(np.random.default_rng(99), 4)
+        res2 = alloc.allocate_greedy(cells[:2] + other[2:], B, EPS2, pools)
+        assert res2["alloc"][:2] == res["alloc"][:2]
+    # the joint dual may move bytes between the pools and is never worse on the model
+    # error at the bytes it spends than any allocation within those bytes (Everett)
+    j = alloc.allocate(cells, total_in / 4.0, EPS2)
+    g = alloc.allocate_greedy(cells, total_in / 4.0, EPS2, pools)
+    if g["total_bytes"] <= j["total_bytes"]:
+        assert j["model_error"] <= g["model_error"] + 1e-15
+
+
+def test_uniform_is_the_best_shared_point(rng):
+    """Uniform rank: every cell gets the same (r_T, r_d, b), the shared point of least
+    summed model error that fits the budget (brute force over the shared points)."""
+    cells = _cells(rng, 3)
+    per = _enumerate(cells, EPS2, 8)
+    total_in = sum(c.m * c.T * c.d * 2 for c in cells)
+    for ratio in (1.5, 3.0, 6.0):
+        B = total_in / ratio
+        res = alloc.allocate_uniform(cells, B, EPS2)
+        assert len(set(res["alloc"])) == 1
+        shared = [(sum(g[k][0] for g in per), sum(g[k][1] for g in per)) for k in range(len(per[0]))]
+        best = min(e for s, e in shared if s <= B)
+        assert res["total_bytes"] <= B and res["model_error"] == pytest.approx(best, rel=0, abs=1e-15)
