@@ -52,6 +52,9 @@ def parse():
                     help="empty = the workload's method")
     ap.add_argument("--allocator", default="joint", choices=["joint", "greedy", "rank_only", "uniform"],
                     help="allocation strategy (the joint dual, or an ablation allocator)")
+    ap.add_argument("--rope-post", type=float, default=0.0,
+                    help="> 1: compress post-RoPE keys (rotary base given) instead of pre-RoPE "
+                         "ones, for the appendix-B comparison")
     ap.add_argument("--power-iters", type=int, default=1)
     ap.add_argument("--oversample", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -218,6 +221,12 @@ def main():
     log("generating", args.workload)
     t0 = time.perf_counter()
     Knp, Vnp = kvsynth.make_cache(**cfg)
+    if args.rope_post > 1.0:
+        for l in range(Knp.shape[0]):
+            xr = kvsynth.apply_rope(kvsynth.bf16_bits_to_f32(Knp[l]) if cfg["dtype"] == "bf16" else Knp[l],
+                                    args.rope_post)
+            Knp[l] = kvsynth.f32_to_bf16_bits(xr) if cfg["dtype"] == "bf16" else xr
+        log(f"keys rotated (RoPE base {args.rope_post:g}) before compression")
     log(f"generated in {time.perf_counter() - t0:.1f} s")
     dev = torch.device("cuda", 0)
     to_dev = (lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)) \
@@ -315,7 +324,8 @@ def main():
         "config": {"workload": args.workload, "layers": cfg["n_layers"], "kv_heads": cfg["n_heads"],
                    "T": cfg["T"], "head_dim": cfg["d"], "batch": cfg["batch"], "group_layers": gl,
                    "cells": len(codec.cells), "method": method, "ratio": ratio,
-                   "allocator": args.allocator, "cache_bytes": cache_bytes},
+                   "allocator": args.allocator, "keys": "post-rope" if args.rope_post > 1.0 else "pre-rope",
+                   "cache_bytes": cache_bytes},
         "compress_GBps": round(cache_bytes / (np.median(t_comp) * 1e-3) / 1e9, 3),
         "decompress_GBps": round(cache_bytes / (np.median(t_dec) * 1e-3) / 1e9, 3),
         "rel_frobenius_error": {"K": round(float(eK.mean()), 6), "V": round(float(eV.mean()), 6)},

@@ -221,6 +221,26 @@ int jolt_decompress(jolt_ctx *ctx, int n_cells, const void *const *blobs, const 
                     const void *hdr_host, const jolt_cell_desc *out_desc, void *const *Xhat,
                     void *ws, size_t ws_bytes, jolt_stream stream);
 
+/* Rotary position embedding applied while decoding (appendix B: keys are compressed
+ * before RoPE and the rotation is re-applied at decode time).  Feature pairs (j, j + d/2)
+ * of token t rotate by the angle (t + position_offset) * base^(-2 j / d), j < d/2
+ * (the half-split pairing of the Mistral / LLaMA checkpoints):
+ *   x'_j = x_j cos - x_{j+d/2} sin,   x'_{j+d/2} = x_{j+d/2} cos + x_j sin.
+ * Angles are formed and reduced in fp64; the rotation is applied in fp32 to the decoded
+ * values before the output cast. */
+typedef struct {
+  double base;             /* e.g. 1e4 (LLaMA-2) or 1e6 (Mistral-7B-v0.3); must be > 1 */
+  int32_t position_offset; /* position of token 0 of every cell (>= 0) */
+  int32_t reserved;
+} jolt_rope;
+
+/* jolt_decompress with the rotary embedding above applied to every decoded row (rope
+ * NULL: identical to jolt_decompress).  Errors: as jolt_decompress, plus JOLT_E_INVAL
+ * for base <= 1 or a negative offset. */
+int jolt_decompress_rope(jolt_ctx *ctx, int n_cells, const void *const *blobs, const size_t *blob_bytes,
+                         const void *hdr_host, const jolt_cell_desc *out_desc, void *const *Xhat,
+                         const jolt_rope *rope, void *ws, size_t ws_bytes, jolt_stream stream);
+
 /* Budgeted allocation (section 4, eq. (1)-(4); host only, no device work): for every
  * cell the grid point (r_T, r_d, b) minimising eq. (2)'s model error plus lambda times
  * eq. (1)'s bytes, with lambda found by bisection so that the summed bytes meet the

@@ -27,7 +27,7 @@ from __future__ import annotations
 import numpy as np
 
 __all__ = ["layer_kv", "make_cache", "f32_to_bf16_bits", "bf16_bits_to_f32",
-           "CONFIGS"]
+           "apply_rope", "CONFIGS"]
 
 _ROLE_A, _ROLE_C, _ROLE_F, _ROLE_N, _ROLE_O, _ROLE_ALPHA = 1, 2, 3, 4, 5, 6
 
@@ -138,6 +138,28 @@ def _layer_job(kw):
     bf16 = kw.pop("bf16")
     x = layer_kv(**kw)
     return f32_to_bf16_bits(x) if bf16 else x
+
+
+def apply_rope(x: np.ndarray, base: float) -> np.ndarray:
+    """Post-RoPE variant of a key tensor [..., T, d] (fp32): the rotary position
+    embedding of the Mistral / LLaMA checkpoints (feature pairs (j, j + d/2) of token t
+    turned by t * base^(-2 j / d)), computed in fp64 and returned as fp32.  Used to build
+    the post-RoPE inputs of appendix B's comparison; it is part of the model, not of the
+    compression method."""
+    T, d = x.shape[-2], x.shape[-1]
+    h = d // 2
+    w = base ** (-2.0 * np.arange(h) / d)
+    ang = np.arange(T, dtype=np.float64)[:, None] * w[None, :]
+    c, s = np.cos(ang), np.sin(ang)
+    out = np.empty(x.shape, dtype=np.float32)
+    flat_in = x.reshape(-1, T, d)
+    flat_out = out.reshape(-1, T, d)
+    for i in range(flat_in.shape[0]):
+        a = flat_in[i].astype(np.float64)
+        x1, x2 = a[:, :h], a[:, h:]
+        flat_out[i, :, :h] = x1 * c - x2 * s
+        flat_out[i, :, h:] = x2 * c + x1 * s
+    return out
 
 
 # Workload shapes (synthetic stand-ins for the paper's Mistral-7B / LLaMA-2-13B caches).

@@ -22,9 +22,11 @@ Module map (paper passages in brackets):
   policy (section 5, "Cap selection"), epsilon^2(b) calibration.
 * :mod:`oracle.pipeline`  - one cell end to end, budgeted whole-cache
   compression, the blob byte format, metrics.
+* :mod:`oracle.rope`      - rotary position embedding re-applied to decoded
+  keys (appendix B: keys are compressed before RoPE).
 
 Parity-unpinned items (no value in the paper can be reproduced on synthetic
 data): the absolute reconstruction errors, the epsilon^2(b) values, the chosen
 ranks and the speedups.
 """
-from . import rounding, philox, residual, tucker, alloc, pipeline  # noqa: F401,E402
+from . import rounding, philox, residual, tucker, alloc, pipeline, rope  # noqa: F401,E402

@@ -17,7 +17,7 @@ import numpy as np
 
 __all__ = ["JoltError", "lib", "CellDesc", "SpectrumOpts", "Params", "CellSpectrum", "AllocOpts",
            "JOLT_F32", "JOLT_BF16", "JOLT_EXACT", "JOLT_FLASH", "JOLT_FACTOR_F32",
-           "JOLT_FACTOR_F16", "jolt_last_error", "jolt_create", "jolt_destroy", "jolt_q_cap",
+           "JOLT_FACTOR_F16", "Rope", "jolt_last_error", "jolt_create", "jolt_destroy", "jolt_q_cap",
            "jolt_spectrum_len", "jolt_workspace_size", "jolt_decompress_workspace_size", "jolt_spectrum", "jolt_compressed_size",
            "jolt_compress", "jolt_decompress", "jolt_allocate", "jolt_eps2_workspace_size",
            "jolt_eps2_calibrate", "jolt_debug_export", "jolt_profile_enable", "jolt_profile_reset",
@@ -70,6 +70,10 @@ class CellSpectrum(C.Structure):
                 ("lam_T", C.POINTER(C.c_double)), ("lam_d", C.POINTER(C.c_double))]
 
 
+class Rope(C.Structure):
+    _fields_ = [("base", C.c_double), ("position_offset", C.c_int32), ("reserved", C.c_int32)]
+
+
 class AllocOpts(C.Structure):
     _fields_ = [("budget_bytes", C.c_double), ("eps2", C.c_double * 4), ("bit_mask", C.c_int32),
                 ("step", C.c_int32), ("floor_rT", C.c_int32), ("floor_rd", C.c_int32),
@@ -93,6 +97,8 @@ _SIGS = {
                                 _P(SpectrumOpts), _vp, _sz, _P(_vp), _P(_sz), _vp]),
     "jolt_decompress": (C.c_int, [_vp, C.c_int, _P(_vp), _P(_sz), _vp, _P(CellDesc), _P(_vp),
                                   _vp, _sz, _vp]),
+    "jolt_decompress_rope": (C.c_int, [_vp, C.c_int, _P(_vp), _P(_sz), _vp, _P(CellDesc), _P(_vp),
+                                       _P(Rope), _vp, _sz, _vp]),
     "jolt_allocate": (C.c_int, [_P(CellSpectrum), C.c_int, _P(AllocOpts), _P(_i32), _P(_i32),
                                 _P(_i32), _P(_dbl), _P(_dbl), _P(_dbl), _P(_i32)]),
     "jolt_eps2_workspace_size": (C.c_int, [C.c_int, C.c_int, _P(_sz)]),
@@ -223,7 +229,8 @@ def jolt_compress(ctx, desc: CellDesc, X, params, opts=None, ws=None, blobs=None
 
 
 def jolt_decompress(ctx, blobs, out_desc: CellDesc, Xhat, ws=None, hdr_host=None,
-                    blob_bytes=None, ws_bytes=None, stream=None) -> None:
+                    blob_bytes=None, ws_bytes=None, stream=None, rope=None) -> None:
+    """rope: None, or (base, position_offset) to re-apply the rotary embedding while decoding."""
     n = len(blobs)
     bb = blob_bytes if blob_bytes is not None else [b.numel() * b.element_size() for b in blobs]
     wsb = ws_bytes if ws_bytes is not None else (ws.numel() * ws.element_size())
@@ -231,8 +238,13 @@ def jolt_decompress(ctx, blobs, out_desc: CellDesc, Xhat, ws=None, hdr_host=None
     if hdr_host is not None:
         hdr_host = np.ascontiguousarray(hdr_host, dtype=np.uint8)
         hdr = hdr_host.ctypes.data
-    _check(lib.jolt_decompress(ctx, n, _ptrs(blobs), (_sz * n)(*bb), hdr, C.byref(out_desc),
-                               _ptrs(Xhat), _addr(ws), wsb, _stream(stream)))
+    if rope is None:
+        _check(lib.jolt_decompress(ctx, n, _ptrs(blobs), (_sz * n)(*bb), hdr, C.byref(out_desc),
+                                   _ptrs(Xhat), _addr(ws), wsb, _stream(stream)))
+    else:
+        r = Rope(float(rope[0]), int(rope[1]), 0)
+        _check(lib.jolt_decompress_rope(ctx, n, _ptrs(blobs), (_sz * n)(*bb), hdr, C.byref(out_desc),
+                                        _ptrs(Xhat), C.byref(r), _addr(ws), wsb, _stream(stream)))
 
 
 ALLOC_STRATEGIES = {"joint": 0, "greedy": 1, "rank_only": 2, "uniform": 3}

@@ -23,6 +23,23 @@ struct RowLayout {
   static constexpr int R = 64 / L;       // rows per wave
 };
 
+// Rotary embedding of one decoded row spread over L lanes (8 features each): features j and
+// j + D/2 sit in lanes l and l + L/2 and rotate together by the angle pos * theta_j, formed
+// and reduced in fp64.
+template <int D>
+JOLT_DEV void rope_row(float (&v)[8], int lane_in_row, double pos, const double (&theta)[8]) {
+  constexpr int L = RowLayout<D>::L;
+  const bool upper = lane_in_row >= L / 2;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float partner = shfl_xor(v[i], L / 2);
+    double sn, cs;
+    sincos(pos * theta[i], &sn, &cs);
+    const float c = (float)cs, s = (float)sn;
+    v[i] = upper ? fmaf(partner, s, v[i] * c) : fmaf(-partner, s, v[i] * c);
+  }
+}
+
 // in-place Walsh-Hadamard transform of the D-entry row spread over L lanes
 template <int D>
 JOLT_DEV void fwht_row(float (&v)[8], int lane_in_row) {
@@ -195,11 +212,18 @@ __global__ void __launch_bounds__(256) k_residual_quant(ResidArgs a) {
   }
 }
 
-template <int D, typename TO>
+template <int D, typename TO, bool ROPE>
 __global__ void __launch_bounds__(256) k_decode(DecodeArgs a) {
   constexpr int L = RowLayout<D>::L, R = RowLayout<D>::R;
   const int lane = threadIdx.x & 63;
   const int row_in_wave = lane / L, lane_in_row = lane % L;
+  // rotary frequencies of this lane's 8 features: base^(-2 j / D), j = feature mod D/2
+  double theta[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int j = (lane_in_row * 8 + i) % (D / 2);
+    theta[i] = ROPE ? exp2(-(2.0 * j / D) * a.rope_log2_base) : 0.0;
+  }
   const int64_t rows_per_cell = (int64_t)a.m * a.T;
   const int64_t blocks_per_cell = (rows_per_cell + R - 1) / R;
   const int64_t total = blocks_per_cell * a.n_cells;
@@ -234,6 +258,7 @@ __global__ void __launch_bounds__(256) k_decode(DecodeArgs a) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) v[i] = xt[i] + v[i];
     }
+    if constexpr (ROPE) rope_row<D>(v, lane_in_row, (double)(t + a.rope_offset), theta);
     TO *o = reinterpret_cast<TO *>(c.out) +
             ((int64_t)(s / a.heads) * a.s_layer + (int64_t)(s % a.heads) * a.s_head +
              (int64_t)t * a.s_tok) + lane_in_row * 8;
@@ -357,10 +382,14 @@ hipError_t launch_decode(const DecodeArgs &a, int d, int out_dtype, hipStream_t 
   int64_t waves = ((int64_t)a.m * a.T + R - 1) / R * a.n_cells;
   int grid = grid_for(waves);
   DISPATCH_D(d, {
-    if (out_dtype == 1)
-      hipLaunchKernelGGL((k_decode<DD, bf16_t>), dim3(grid), dim3(256), 0, st, a);
+    if (out_dtype == 1 && a.rope)
+      hipLaunchKernelGGL((k_decode<DD, bf16_t, true>), dim3(grid), dim3(256), 0, st, a);
+    else if (out_dtype == 1)
+      hipLaunchKernelGGL((k_decode<DD, bf16_t, false>), dim3(grid), dim3(256), 0, st, a);
+    else if (a.rope)
+      hipLaunchKernelGGL((k_decode<DD, float, true>), dim3(grid), dim3(256), 0, st, a);
     else
-      hipLaunchKernelGGL((k_decode<DD, float>), dim3(grid), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((k_decode<DD, float, false>), dim3(grid), dim3(256), 0, st, a);
   });
   return hipGetLastError();
 }

@@ -48,6 +48,9 @@ struct DecodeArgs {
   int32_t n_cells, m, T, heads, group;
   int64_t s_layer, s_head, s_tok;
   float inv_sqrt_d;
+  int32_t rope;             // 1: rotate feature pairs (j, j + d/2) by position t + rope_offset
+  int32_t rope_offset;
+  double rope_log2_base;    // log2 of the rotary base
 };
 
 struct Eps2Args {

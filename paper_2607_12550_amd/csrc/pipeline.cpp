@@ -863,8 +863,18 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
 extern "C" int jolt_decompress(jolt_ctx *ctx, int n_cells, const void *const *blobs, const size_t *blob_bytes,
                                const void *hdr_host, const jolt_cell_desc *out, void *const *Xhat, void *ws,
                                size_t ws_bytes, jolt_stream stream) {
+  return jolt_decompress_rope(ctx, n_cells, blobs, blob_bytes, hdr_host, out, Xhat, nullptr, ws, ws_bytes,
+                              stream);
+}
+
+extern "C" int jolt_decompress_rope(jolt_ctx *ctx, int n_cells, const void *const *blobs,
+                                    const size_t *blob_bytes, const void *hdr_host, const jolt_cell_desc *out,
+                                    void *const *Xhat, const jolt_rope *rope, void *ws, size_t ws_bytes,
+                                    jolt_stream stream) {
   int rc = validate_desc(out);
   if (rc) return rc;
+  if (rope && (!(rope->base > 1.0) || rope->position_offset < 0))
+    return jolt_fail(JOLT_E_INVAL, "jolt_decompress_rope: base must be > 1 and position_offset >= 0");
   if (n_cells < 1 || !blobs || !blob_bytes || !Xhat || !ws)
     return jolt_fail(JOLT_E_INVAL, "jolt_decompress: null argument");
   if (reinterpret_cast<uintptr_t>(ws) & 255) return jolt_fail(JOLT_E_INVAL, "workspace must be 256-byte aligned");
@@ -971,6 +981,11 @@ extern "C" int jolt_decompress(jolt_ctx *ctx, int n_cells, const void *const *bl
   da.cells = R.w.dcell; da.signs = R.w.signs; da.n_cells = n_cells; da.m = m; da.T = T;
   da.heads = out->n_heads; da.group = bi[0].group; da.s_layer = out->stride_layer; da.s_head = out->stride_head;
   da.s_tok = out->stride_token; da.inv_sqrt_d = (float)(1.0 / std::sqrt((double)d));
+  if (rope) {
+    da.rope = 1;
+    da.rope_offset = rope->position_offset;
+    da.rope_log2_base = std::log2(rope->base);
+  }
   StageTimer t(ctx, st, JOLT_STAGE_DECODE);
   HIP_OK(launch_decode(da, d, out->dtype, st));
   return JOLT_OK;

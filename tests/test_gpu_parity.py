@@ -245,3 +245,36 @@ def test_workspace_overwrite_forgets_the_spectrum():
     b2, _ = compress(xs, desc, params, reuse, ws=ws2)
     for a, b, c in zip(blobs, b1, b2):
         assert blob_bytes(a) == blob_bytes(b) == blob_bytes(c)
+
+
+@pytest.mark.parametrize("out_dtype", ["f32", "bf16"])
+def test_decompress_reapplies_rope(out_dtype):
+    """Appendix B: keys compressed before RoPE, rotation re-applied while decoding.  The
+    decoder with RoPE equals the oracle's decode of the same blob followed by the oracle's
+    rotation (base 1e6, positions 1000 + t)."""
+    from oracle.rope import rope
+    X = keys_cell(T=256, H=8, seed=2)
+    xs, ex, desc = device_cells([X], "bf16")
+    blobs, ws = compress(xs, desc, [J.Params(48, 64, 4, 64, J.JOLT_FACTOR_F16, 0, 5)])
+    got_blob = opl.read_blob(blob_bytes(blobs[0]))
+    dec = opl.decode_parts_from_factors(got_blob["U_hat"], got_blob["Ud_hat"], got_blob["G_hat"],
+                                        got_blob["gexp"], got_blob["codes"], got_blob["scales"],
+                                        T=256, d=128, bits=4, group=64, seed=5)
+    want = rope(dec, 1e6, np.arange(256) + 1000.0)
+    od = J.cell_desc(dtype=J.JOLT_BF16 if out_dtype == "bf16" else J.JOLT_F32, n_layers=1, n_heads=8,
+                     T=256, d=128, stride_layer=8 * 256 * 128, stride_head=256 * 128, stride_token=128)
+    out = torch.empty((8, 256, 128), dtype=torch.bfloat16 if out_dtype == "bf16" else torch.float32,
+                      device="cuda")
+    note("jolt_decompress_rope", out_dtype)
+    J.jolt_decompress(ctx(), blobs, od, [out], ws, rope=(1e6, 1000))
+    torch.cuda.synchronize()
+    Xh = out.float().cpu().numpy().astype(np.float64)
+    if out_dtype == "f32":
+        assert np.linalg.norm(Xh - want) <= 1e-5 * np.linalg.norm(want)
+    else:
+        w16 = opl.cast_output(want, "bf16")
+        diff = np.abs(Xh - w16)
+        assert np.mean(diff != 0) < 1e-3
+        assert (diff - np.abs(w16) * 2 ** -7).max() <= 1e-5 * float(np.sqrt(np.mean(X * X)))
+    with pytest.raises(J.JoltError):
+        J.jolt_decompress(ctx(), blobs, od, [out], ws, rope=(1.0, 0))

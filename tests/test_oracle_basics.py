@@ -164,3 +164,38 @@ def test_eps2_monotone_and_rotation_invariant():
         codes, sc = residual.quantize(z, b, 64)
         ref = np.sum((residual.dequantize(codes, sc, b, 64) - z) ** 2) / np.sum(z * z)
         assert abs(e[b] / ref - 1.0) < 0.03, (b, e[b], ref)
+
+
+# ------------------------------------------------------------------ rotary embedding (appendix B)
+def test_rope_two_features_is_a_plane_rotation():
+    """d = 2: one pair with frequency base^0 = 1, so position p turns the row by p radians."""
+    from oracle.rope import rope
+    x = np.array([[0.3, -1.7], [2.0, 0.5], [-0.4, 0.9]])
+    p = np.array([0.0, 1.0, 7.5])
+    got = rope(x, 1e4, p)
+    for r in range(3):
+        c, s = np.cos(p[r]), np.sin(p[r])
+        want = np.array([[c, -s], [s, c]]) @ x[r]
+        np.testing.assert_allclose(got[r], want, rtol=0, atol=1e-15)
+
+
+def test_rope_keeps_norms_and_inverts():
+    from oracle.rope import rope
+    rng = np.random.default_rng(4)
+    X = rng.standard_normal((3, 50, 128))
+    pos = np.arange(50) + 1000.0
+    Y = rope(X, 1e6, pos)
+    np.testing.assert_allclose(np.linalg.norm(Y, axis=-1), np.linalg.norm(X, axis=-1), rtol=1e-13)
+    np.testing.assert_allclose(rope(Y, 1e6, -pos), X, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(rope(X, 1e6, np.zeros(50)), X, rtol=0, atol=0)
+
+
+def test_rope_scores_depend_only_on_relative_position():
+    """The defining property: <rope(q, p1), rope(k, p2)> depends on p2 - p1 alone."""
+    from oracle.rope import rope
+    rng = np.random.default_rng(5)
+    q, k = rng.standard_normal((1, 64)), rng.standard_normal((1, 64))
+    for p1, p2, shift in ((3, 10, 500), (0, 4000, 77), (123, 45, 9999)):
+        a = float((rope(q, 1e4, [p1]) @ rope(k, 1e4, [p2]).T)[0, 0])
+        b = float((rope(q, 1e4, [p1 + shift]) @ rope(k, 1e4, [p2 + shift]).T)[0, 0])
+        assert abs(a - b) <= 1e-9 * (abs(a) + 1)
