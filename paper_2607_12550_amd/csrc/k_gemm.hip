@@ -1,24 +1,20 @@
-// Batched MFMA GEMM for gfx950 used by every dense contraction of the path: the token
-// Gram X_(2) X_(2)^T, the ST-HOSVD projections and core products, the
-// reconstruction U_T W_s, the FlashJoLT sketch products and the eigensolver's
-// blocked updates.
+// Batched fp32 MFMA GEMM for gfx950 (v_mfma_f32_32x32x2_f32): the products that need
+// fp32 operands in full, i.e. the reconstruction U_T W_s from the stored factors, the
+// ST-HOSVD core products, the eigensolver's blocked updates and back-transforms, the
+// FlashJoLT B B^T and fp32 cells, and the fallback for any table the bf16 kernel's layout
+// conditions reject.  Inputs (bf16 / fp16 / fp32) are widened exactly to fp32.
 //
 // Tile: 128 x 128 outputs per 256-thread workgroup, 4 wavefronts in a 2 x 2 grid,
 // each wave owning 64 x 64 = 2 x 2 MFMA 32x32 blocks.  K advances in steps of 32;
 // the next K tile is fetched into registers while the current one is multiplied
-// out of LDS.  Two arithmetic modes:
-//   mode 0: bf16 x bf16 on v_mfma_f32_32x32x16_bf16 (products exact, fp32 sums);
-//   mode 1: inputs (bf16 / fp16 / fp32) widened exactly to fp32 on
-//           v_mfma_f32_32x32x2_f32.
-// LDS keeps both operands k-contiguous; within a K tile the k index is permuted
-// identically for A and B (a sum over k does not depend on its order) so that each
-// lane reads its fragment with 16-byte LDS loads.
+// out of LDS.  LDS keeps both operands k-contiguous; within a K tile the k index is
+// permuted identically for A and B (a sum over k does not depend on its order) so
+// that each lane reads its fragment with 16-byte LDS loads.
 // Operands are addressed through GemmOperand so the cache cell (slices at two-level
 // strides) is read in place, never repacked.
 #include "common.h"
 #include "kernels.h"
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 namespace {
@@ -71,22 +67,6 @@ JOLT_DEV void load8_f32(const GemmOperand &op, int row, int col, int nrows, int 
   }
 }
 
-JOLT_DEV void load8_raw16(const GemmOperand &op, int row, int col, int nrows, int ncols,
-                          uint16_t (&v)[8]) {
-  const JOLT_GLOBAL uint16_t *p = gptr(reinterpret_cast<const uint16_t *>(op.ptr));
-  const int64_t off0 = (row < nrows && col + 8 <= ncols) ? op_offset(op, row, col) : 0;
-  if (row < nrows && col + 8 <= ncols && ((reinterpret_cast<uintptr_t>(p + off0)) & 15) == 0) {
-    const ju4 u = gload_u4((const void *)(reinterpret_cast<const uint16_t *>(op.ptr) + off0));
-    uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) { v[2 * i] = (uint16_t)(w[i] & 0xffff); v[2 * i + 1] = (uint16_t)(w[i] >> 16); }
-  } else {
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      v[i] = (row < nrows && col + i < ncols) ? p[op_offset(op, row, col + i)] : (uint16_t)0;
-  }
-}
-
 // Each thread moves two 8-element chunks of a 128 x 32 (k-contiguous) or
 // 32 x 128 (mn-contiguous) operand tile per K step.
 template <bool KCONTIG>
@@ -95,27 +75,19 @@ JOLT_DEV void chunk_coords(int chunk, int &r, int &c) {
   else { r = chunk >> 4; c = (chunk & 15) * 8; }          // 32 rows x 16 chunks
 }
 
-template <int MODE>
-struct Smem;
-template <>
-struct Smem<0> {
-  static constexpr int LD = BK + 8;                       // bf16 elements
-  uint16_t a[BM * LD], b[BN * LD];
-};
-template <>
-struct Smem<1> {
+struct Smem {
   static constexpr int LD = BK + 4;                       // fp32 elements
   float a[BM * LD], b[BN * LD];
 };
 
-template <int MODE, int TA, int TB, bool AK, bool BK_>
+template <int TA, int TB, bool AK, bool BK_>
 __global__ void __launch_bounds__(NT) k_gemm(const GemmProblem *__restrict__ probs) {
   const GemmProblem &P = probs[blockIdx.z];
   const int tm = blockIdx.y, tn = blockIdx.x;
   if (tm * BM >= P.M || tn * BN >= P.N) return;
   if (P.lower_only && tm < tn) return;
-  __shared__ Smem<MODE> sm;
-  constexpr int LD = Smem<MODE>::LD;
+  __shared__ Smem sm;
+  constexpr int LD = Smem::LD;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int m0 = tm * BM, n0 = tn * BN;
@@ -134,7 +106,6 @@ __global__ void __launch_bounds__(NT) k_gemm(const GemmProblem *__restrict__ pro
 
   // register staging of the next tile
   float ra[2][8], rb[2][8];
-  uint16_t ha[2][8], hb[2][8];
 
   auto fetch = [&](int k0) {
 #pragma unroll
@@ -145,13 +116,8 @@ __global__ void __launch_bounds__(NT) k_gemm(const GemmProblem *__restrict__ pro
       const int ar = AK ? m0 + r : k0 + r, ac = AK ? k0 + c : m0 + c;
       chunk_coords<BK_>(chunk, r, c);
       const int br = BK_ ? n0 + r : k0 + r, bc = BK_ ? k0 + c : n0 + c;
-      if constexpr (MODE == 0) {
-        load8_raw16(P.A, ar, ac, a_rows, a_cols, ha[h]);
-        load8_raw16(P.B, br, bc, b_rows, b_cols, hb[h]);
-      } else {
-        load8_f32<TA>(P.A, ar, ac, a_rows, a_cols, ra[h]);
-        load8_f32<TB>(P.B, br, bc, b_rows, b_cols, rb[h]);
-      }
+      load8_f32<TA>(P.A, ar, ac, a_rows, a_cols, ra[h]);
+      load8_f32<TB>(P.B, br, bc, b_rows, b_cols, rb[h]);
     }
   };
   auto stash = [&]() {
@@ -163,13 +129,13 @@ __global__ void __launch_bounds__(NT) k_gemm(const GemmProblem *__restrict__ pro
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const int idx = AK ? r * LD + c + i : (c + i) * LD + r;
-        if constexpr (MODE == 0) sm.a[idx] = ha[h][i]; else sm.a[idx] = ra[h][i];
+        sm.a[idx] = ra[h][i];
       }
       chunk_coords<BK_>(chunk, r, c);
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const int idx = BK_ ? r * LD + c + i : (c + i) * LD + r;
-        if constexpr (MODE == 0) sm.b[idx] = hb[h][i]; else sm.b[idx] = rb[h][i];
+        sm.b[idx] = rb[h][i];
       }
     }
   };
@@ -181,43 +147,22 @@ __global__ void __launch_bounds__(NT) k_gemm(const GemmProblem *__restrict__ pro
     stash();
     __syncthreads();
     if (k0 + BK < P.K) fetch(k0 + BK);
-    if constexpr (MODE == 0) {
-      // lane group lh covers k in [16 lh, 16 lh + 16): two MFMA steps of 8
-      bf16x8_t fa[2][2], fb[2][2];
+    // lane group lh covers k in [16 lh, 16 lh + 16): sixteen MFMA steps of 2
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float4 fa[2], fb[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        const uint16_t *pa = &sm.a[(wm * 64 + i * 32 + lr) * LD + lh * 16];
-        const uint16_t *pb = &sm.b[(wn * 64 + i * 32 + lr) * LD + lh * 16];
-        fa[i][0] = *reinterpret_cast<const bf16x8_t *>(pa);
-        fa[i][1] = *reinterpret_cast<const bf16x8_t *>(pa + 8);
-        fb[i][0] = *reinterpret_cast<const bf16x8_t *>(pb);
-        fb[i][1] = *reinterpret_cast<const bf16x8_t *>(pb + 8);
+        fa[i] = *reinterpret_cast<const float4 *>(&sm.a[(wm * 64 + i * 32 + lr) * LD + lh * 16 + q * 4]);
+        fb[i] = *reinterpret_cast<const float4 *>(&sm.b[(wn * 64 + i * 32 + lr) * LD + lh * 16 + q * 4]);
       }
 #pragma unroll
-      for (int s = 0; s < 2; ++s)
+      for (int s = 0; s < 4; ++s)
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
           for (int j = 0; j < 2; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i][s], fb[j][s], acc[i][j], 0, 0, 0);
-    } else {
-      // lane group lh covers k in [16 lh, 16 lh + 16): sixteen MFMA steps of 2
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float4 fa[2], fb[2];
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          fa[i] = *reinterpret_cast<const float4 *>(&sm.a[(wm * 64 + i * 32 + lr) * LD + lh * 16 + q * 4]);
-          fb[i] = *reinterpret_cast<const float4 *>(&sm.b[(wn * 64 + i * 32 + lr) * LD + lh * 16 + q * 4]);
-        }
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-#pragma unroll
-          for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int j = 0; j < 2; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i][s], fb[j][s], acc[i][j], 0, 0, 0);
-      }
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i][s], fb[j][s], acc[i][j], 0, 0, 0);
     }
   }
 
@@ -228,7 +173,7 @@ __global__ void __launch_bounds__(NT) k_gemm(const GemmProblem *__restrict__ pro
   // row wm*64 + i*32 + 8*(q/4) + 4*lh + q%4, column wn*64 + j*32 + lr of the tile.
   float *cs = reinterpret_cast<float *>(&sm);
   constexpr int CLD = BN + 4;
-  static_assert(32 * CLD * sizeof(float) <= sizeof(Smem<MODE>), "epilogue tile exceeds LDS");
+  static_assert(32 * CLD * sizeof(float) <= sizeof(Smem), "epilogue tile exceeds LDS");
   const bool use_beta = P.beta != 0.f;
   const bool vec = ((reinterpret_cast<uintptr_t>(P.C) & 15) == 0) && (P.ldc % 4 == 0);
 #pragma unroll
@@ -268,12 +213,12 @@ __global__ void __launch_bounds__(NT) k_gemm(const GemmProblem *__restrict__ pro
   }
 }
 
-template <int MODE, int TA, int TB>
+template <int TA, int TB>
 hipError_t launch_t(const GemmProblem *probs, int n, dim3 grid, bool ak, bool bk, hipStream_t st) {
-  if (ak && bk) hipLaunchKernelGGL((k_gemm<MODE, TA, TB, true, true>), grid, dim3(NT), 0, st, probs);
-  else if (ak) hipLaunchKernelGGL((k_gemm<MODE, TA, TB, true, false>), grid, dim3(NT), 0, st, probs);
-  else if (bk) hipLaunchKernelGGL((k_gemm<MODE, TA, TB, false, true>), grid, dim3(NT), 0, st, probs);
-  else hipLaunchKernelGGL((k_gemm<MODE, TA, TB, false, false>), grid, dim3(NT), 0, st, probs);
+  if (ak && bk) hipLaunchKernelGGL((k_gemm<TA, TB, true, true>), grid, dim3(NT), 0, st, probs);
+  else if (ak) hipLaunchKernelGGL((k_gemm<TA, TB, true, false>), grid, dim3(NT), 0, st, probs);
+  else if (bk) hipLaunchKernelGGL((k_gemm<TA, TB, false, true>), grid, dim3(NT), 0, st, probs);
+  else hipLaunchKernelGGL((k_gemm<TA, TB, false, false>), grid, dim3(NT), 0, st, probs);
   return hipGetLastError();
 }
 
@@ -283,12 +228,8 @@ hipError_t launch_gemm(const GemmProblem *probs_dev, int n_probs, int max_M, int
                        int ta, int tb, bool a_kcontig, bool b_kcontig, hipStream_t st) {
   if (n_probs <= 0 || max_M <= 0 || max_N <= 0) return hipSuccess;
   dim3 grid((max_N + BN - 1) / BN, (max_M + BM - 1) / BM, n_probs);
-  if (mode == 0) {
-    if (ta != GT_BF16 || tb != GT_BF16) return hipErrorInvalidValue;
-    return launch_gemm16(probs_dev, n_probs, max_M, max_N, ta, tb, a_kcontig, b_kcontig, st);
-  }
-  if (mode == 2) return launch_gemm16(probs_dev, n_probs, max_M, max_N, ta, tb, a_kcontig, b_kcontig, st);
-#define TT(A_, B_) if (ta == A_ && tb == B_) return launch_t<1, A_, B_>(probs_dev, n_probs, grid, a_kcontig, b_kcontig, st)
+  if (mode != 1) return hipErrorInvalidValue;
+#define TT(A_, B_) if (ta == A_ && tb == B_) return launch_t<A_, B_>(probs_dev, n_probs, grid, a_kcontig, b_kcontig, st)
   TT(GT_F32, GT_F32);
   TT(GT_BF16, GT_F32);
   TT(GT_F32, GT_BF16);

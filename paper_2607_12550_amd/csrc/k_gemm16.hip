@@ -1,27 +1,50 @@
 // Batched GEMM on the bf16 matrix cores (v_mfma_f32_32x32x16_bf16, fp32 accumulate) for
 // the contractions that read the cache: the token Gram, the FlashJoLT sketch products
-// X Omega, X^T Q, X Q' and Q^T X, and the ST-HOSVD projection U_T^T X.
+// X Omega, X^T Q, X Q' and Q^T X, the ST-HOSVD projection U_T^T X, and the products of
+// the FlashJoLT orthonormaliser.
 //
 // Operands are bf16 (used as they are) or fp32, in which case each element is split on
 // the fly into x = hi + lo with hi = bf16(x), lo = bf16(x - hi) (both round to nearest
-// even) and the product takes two MFMA passes (A hi * B + A lo * B, or the same for B):
-// |x - hi - lo| <= 2^-17 |x|, so the products carry about 16 significant bits where the
-// other operand is exact bf16 data.
+// even): |x - hi - lo| <= 2^-17 |x|.  One fp32 operand takes two MFMA passes
+// (A hi * B + A lo * B, or the same for B); two fp32 operands take three
+// (hi*hi + lo*hi + hi*lo, dropping lo*lo, which is below 2^-16 of the product).
 //
-// Tile 128 x 128 per 256-thread workgroup (4 waves, each 64 x 64 = 2 x 2 MFMA blocks),
-// K tiles of 64 staged through LDS with the next tile held in registers while the current
-// one is multiplied.  LDS keeps both operands k-contiguous (rows of 64 + 8 bf16); an
+// Tile BM x 128 (BM = 128 or 256) per 256-thread workgroup, 4 waves in a 2 x 2 grid, each
+// (BM/2) x 64 = (BM/64) x 2 MFMA blocks; K tiles of 64.  Operands go global -> registers ->
+// LDS; the next K tile's loads are issued before the current tile is multiplied and their
+// registers are only read when they are stored to LDS, so the loads stay in flight during
+// the MFMAs.  When two LDS tiles fit (160 KB per CU) the next tile is stored into the
+// second buffer while the first is multiplied, with one barrier per step.  LDS keeps both
+// operands k-contiguous (rows of 64 + 8 bf16: conflict-free 16-byte fragment reads); an
 // operand whose memory layout is contiguous along M/N is transposed in registers (each
-// thread moves a 4 (k) x 8 (m) block and writes 8-byte k-runs), never element by element.
+// thread moves a 4 (k) x 8 (m) block; 16 lanes write one LDS row as 8-byte runs).
+//
+// Work decomposition: a 1-D grid over all tiles of all problems.  The hardware deals
+// workgroups to the 8 XCDs round-robin; the kernel remaps its block index so that each XCD
+// takes a contiguous run of tiles (ordered in groups of 8 tile rows), so tiles that share
+// operand panels run on the same XCD and share its L2.
+//
+// Full K tiles load through per-thread 32-bit offsets fixed at the start, without bounds
+// checks: rows (or column runs) beyond the operand's extent read a clamped in-range address
+// and only feed outputs the epilogue does not store.  A ragged last K tile is loaded with
+// every element checked (zeros beyond K).  gemm16_prepare() checks on the host that a
+// table meets the layout conditions this needs; otherwise the caller uses the fp32 kernel.
 #include "common.h"
 #include "kernels.h"
+#include <algorithm>
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 namespace {
 
-constexpr int BM = 128, BN = 128, BK = 64, NT = 256, LDK = BK + 8;
+constexpr int BN = 128, BK = 64, NT = 256, LDK = BK + 8;
+constexpr int LDS_BYTES = 160 * 1024;
+
+struct Grid {
+  int tiles_m, tiles_n, per_prob, lower_only;
+  int total, per_xcd;
+};
 
 JOLT_DEV int64_t opoff(const GemmOperand &op, int row, int col) {
   return (int64_t)row * op.ld + operand_col(op, col);
@@ -32,16 +55,9 @@ JOLT_DEV void split_bf16(float x, uint16_t &h, uint16_t &l) {
   l = f32_to_bf16(x - bf16_to_f32(h));
 }
 
-// 8 consecutive elements along the operand's contiguous axis at (row, col): raw bf16 bits,
-// or fp32 values; out-of-range elements read as zero
-template <bool F32>
-struct Vec8 {
-  uint16_t h[8];
-};
-template <>
-struct Vec8<true> {
-  float f[8];
-};
+// 8 elements as loaded: bf16 bits in four 32-bit words, or two float4
+template <bool F32> struct Vec8 { ju4 w; };
+template <> struct Vec8<true> { jf4 a, b; };
 
 template <bool F32>
 JOLT_DEV void load8(const GemmOperand &op, int row, int col, int nrows, int ncols, Vec8<F32> &v) {
@@ -50,56 +66,107 @@ JOLT_DEV void load8(const GemmOperand &op, int row, int col, int nrows, int ncol
   if constexpr (F32) {
     const float *p = reinterpret_cast<const float *>(op.ptr) + o;
     if (in && (reinterpret_cast<uintptr_t>(p) & 15) == 0) {
-      const jf4 a = gload_f4(p), b = gload_f4(p + 4);
-      v.f[0] = a.x; v.f[1] = a.y; v.f[2] = a.z; v.f[3] = a.w;
-      v.f[4] = b.x; v.f[5] = b.y; v.f[6] = b.z; v.f[7] = b.w;
+      v.a = gload_f4(p); v.b = gload_f4(p + 4);
     } else {
+      float f[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i)
-        v.f[i] = (row < nrows && col + i < ncols)
-                     ? gptr(reinterpret_cast<const float *>(op.ptr))[opoff(op, row, col + i)] : 0.f;
+        f[i] = (row < nrows && col + i < ncols)
+                   ? gptr(reinterpret_cast<const float *>(op.ptr))[opoff(op, row, col + i)] : 0.f;
+      v.a = jf4{f[0], f[1], f[2], f[3]}; v.b = jf4{f[4], f[5], f[6], f[7]};
     }
   } else {
     const uint16_t *p = reinterpret_cast<const uint16_t *>(op.ptr) + o;
     if (in && (reinterpret_cast<uintptr_t>(p) & 15) == 0) {
-      const ju4 u = gload_u4(p);
-      const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) { v.h[2 * i] = (uint16_t)(w[i] & 0xffff); v.h[2 * i + 1] = (uint16_t)(w[i] >> 16); }
+      v.w = gload_u4(p);
     } else {
+      uint32_t h[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i)
-        v.h[i] = (row < nrows && col + i < ncols)
-                     ? gptr(reinterpret_cast<const uint16_t *>(op.ptr))[opoff(op, row, col + i)] : (uint16_t)0;
+        h[i] = (row < nrows && col + i < ncols)
+                   ? gptr(reinterpret_cast<const uint16_t *>(op.ptr))[opoff(op, row, col + i)] : 0u;
+      v.w = ju4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
     }
   }
 }
 
 JOLT_DEV uint32_t pk(uint16_t a, uint16_t b) { return (uint32_t)a | ((uint32_t)b << 16); }
 
-// Staging of one 128 (m or n) x 64 (k) operand tile.
-//   k-contiguous: thread t moves units u = t + 256 q (q < 4): row u / 8, k run (u % 8) * 8;
-//   mn-contiguous: thread t moves the 4 (k) x 8 (mn) block at k (t / 16) * 4, mn (t % 16) * 8.
-template <bool KC, bool F32>
-struct Stager {
-  static constexpr int NV = KC ? 4 : 4;   // vectors held per thread
+// Staging of one R (m or n) x 64 (k) operand tile through registers.
+//   k-contiguous: unit u = tid + 256 q: row u / 8, k run (u % 8) * 8 (8 lanes per 128-byte row);
+//   mn-contiguous: 4 (k) x 8 (mn) blocks b = tid + 256 p: k block b % 16, mn block b / 16, so
+//   16 lanes write one LDS row's 64 k values as consecutive 8-byte runs.
+// Full K tiles use precomputed per-thread offsets and branch-free loads (rows or columns
+// beyond the operand's extent are read at a clamped in-range address and zeroed); a ragged
+// last K tile goes through the bounds-checked load8.
+template <int R, bool KC, bool F32>
+struct Stage {
+  static constexpr int NV = R * BK / 8 / NT;   // 8-element vectors per thread
   Vec8<F32> v[NV];
+};
 
-  JOLT_DEV void fetch(const GemmOperand &op, int mn0, int k0, int MN, int K, int tid) {
+template <int R, bool KC, bool F32>
+struct Addr {
+  static constexpr int NV = R * BK / 8 / NT;
+  uint32_t off[NV];     // element offset at k0 = 0 (KC: without the k column part)
+
+  // Rows (KC) or column runs (mn-contiguous) beyond the operand's extent are read at a
+  // clamped in-range address and not zeroed: they only feed output rows / columns that the
+  // epilogue does not store.
+  JOLT_DEV void init(const GemmOperand &op, int mn0, int MN, int tid) {
 #pragma unroll
     for (int q = 0; q < NV; ++q) {
       if constexpr (KC) {
-        const int u = tid + NT * q, r = u >> 3, kc = (u & 7) * 8;
-        load8<F32>(op, mn0 + r, k0 + kc, MN, K, v[q]);
+        const int u = tid + NT * q, r = mn0 + (u >> 3), kc = (u & 7) * 8;
+        off[q] = (uint32_t)((r < MN ? r : 0) * op.ld + kc);
       } else {
-        const int kb = (tid >> 4) * 4, mb = (tid & 15) * 8;
-        load8<F32>(op, k0 + kb + q, mn0 + mb, K, MN, v[q]);
+        const int b = tid + NT * (q >> 2), kb = (b & 15) * 4 + (q & 3), mb = mn0 + (b >> 4) * 8;
+        off[q] = (uint32_t)(kb * op.ld + operand_col(op, mb < MN ? mb : 0));
       }
     }
   }
 
-  // hi (and lo for fp32) tiles: [128][LDK] bf16 each
-  JOLT_DEV void stash(uint16_t *hi, uint16_t *lo, int tid) const {
+  // full K tile at k0 (k0 + 64 <= K); the raw registers are only read by stash, so the
+  // loads stay in flight while earlier tiles are multiplied
+  JOLT_DEV void fetch_full(const GemmOperand &op, int k0, Stage<R, KC, F32> &s) const {
+    int64_t step;
+    if constexpr (KC) step = operand_col(op, k0);      // a 64-wide k run stays in one segment
+    else step = (int64_t)k0 * op.ld;
+#pragma unroll
+    for (int q = 0; q < NV; ++q) {
+      const int64_t o = (int64_t)off[q] + step;
+      if constexpr (F32) {
+        const float *p = reinterpret_cast<const float *>(op.ptr) + o;
+        s.v[q].a = gload_f4(p); s.v[q].b = gload_f4(p + 4);
+      } else {
+        s.v[q].w = gload_u4(reinterpret_cast<const uint16_t *>(op.ptr) + o);
+      }
+    }
+  }
+
+  // ragged K tile: every element bounds-checked
+  JOLT_DEV void fetch_tail(const GemmOperand &op, int mn0, int k0, int MN, int K, int tid,
+                           Stage<R, KC, F32> &s) const {
+#pragma unroll
+    for (int q = 0; q < NV; ++q) {
+      if constexpr (KC) {
+        const int u = tid + NT * q, r = u >> 3, kc = (u & 7) * 8;
+        load8<F32>(op, mn0 + r, k0 + kc, MN, K, s.v[q]);
+      } else {
+        const int b = tid + NT * (q >> 2), kb = (b & 15) * 4 + (q & 3), mb = (b >> 4) * 8;
+        load8<F32>(op, k0 + kb, mn0 + mb, K, MN, s.v[q]);
+      }
+    }
+  }
+
+  JOLT_DEV float elem_f(const Stage<R, KC, F32> &s, int q, int e) const {
+    return e < 4 ? s.v[q].a[e] : s.v[q].b[e - 4];
+  }
+  JOLT_DEV uint16_t elem_h(const Stage<R, KC, F32> &s, int q, int e) const {
+    return (uint16_t)(s.v[q].w[e >> 1] >> (16 * (e & 1)));
+  }
+
+  JOLT_DEV void stash(const Stage<R, KC, F32> &s, uint16_t *hi, uint16_t *lo, int tid) const {
     if constexpr (KC) {
 #pragma unroll
       for (int q = 0; q < NV; ++q) {
@@ -107,158 +174,351 @@ struct Stager {
         uint16_t h[8], l[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          if constexpr (F32) split_bf16(v[q].f[i], h[i], l[i]);
-          else h[i] = v[q].h[i];
+          if constexpr (F32) split_bf16(elem_f(s, q, i), h[i], l[i]);
+          else h[i] = elem_h(s, q, i);
         }
         *reinterpret_cast<uint4 *>(hi + r * LDK + kc) = make_uint4(pk(h[0], h[1]), pk(h[2], h[3]), pk(h[4], h[5]), pk(h[6], h[7]));
         if constexpr (F32)
           *reinterpret_cast<uint4 *>(lo + r * LDK + kc) = make_uint4(pk(l[0], l[1]), pk(l[2], l[3]), pk(l[4], l[5]), pk(l[6], l[7]));
       }
     } else {
-      const int kb = (tid >> 4) * 4, mb = (tid & 15) * 8;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        uint16_t h[4], l[4];
+      for (int p = 0; p < NV / 4; ++p) {
+        const int b = tid + NT * p, kb = (b & 15) * 4, mb = (b >> 4) * 8;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          if constexpr (F32) split_bf16(v[q].f[e], h[q], l[q]);
-          else h[q] = v[q].h[e];
+        for (int e = 0; e < 8; ++e) {
+          uint16_t h[4], l[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            if constexpr (F32) split_bf16(elem_f(s, 4 * p + q, e), h[q], l[q]);
+            else h[q] = elem_h(s, 4 * p + q, e);
+          }
+          *reinterpret_cast<uint2 *>(hi + (mb + e) * LDK + kb) = make_uint2(pk(h[0], h[1]), pk(h[2], h[3]));
+          if constexpr (F32)
+            *reinterpret_cast<uint2 *>(lo + (mb + e) * LDK + kb) = make_uint2(pk(l[0], l[1]), pk(l[2], l[3]));
         }
-        *reinterpret_cast<uint2 *>(hi + (mb + e) * LDK + kb) = make_uint2(pk(h[0], h[1]), pk(h[2], h[3]));
-        if constexpr (F32)
-          *reinterpret_cast<uint2 *>(lo + (mb + e) * LDK + kb) = make_uint2(pk(l[0], l[1]), pk(l[2], l[3]));
       }
     }
   }
 };
 
-template <bool AS, bool BS>
-struct Lds16 {
-  static constexpr int TILE = 128 * LDK;
-  uint16_t a[TILE * (AS ? 2 : 1)];
-  uint16_t b[TILE * (BS ? 2 : 1)];
+template <int BM, bool AS, bool BS>
+struct Lds {
+  static constexpr int LA = BM * LDK * (AS ? 2 : 1), LB = BN * LDK * (BS ? 2 : 1);
+  static constexpr bool DB = 2 * 2 * (LA + LB) <= LDS_BYTES;   // two buffers fit
+  uint16_t a[LA * (DB ? 2 : 1)];
+  uint16_t b[LB * (DB ? 2 : 1)];
 };
 
-// AK/BK_: operand k-contiguous in memory; AS/BS: operand is fp32 (split into hi + lo)
-template <bool AK, bool BK_, bool AS, bool BS>
-__global__ void __launch_bounds__(NT) k_gemm16(const GemmProblem *__restrict__ probs) {
-  const GemmProblem &P = probs[blockIdx.z];
-  const int tm = blockIdx.y, tn = blockIdx.x;
+// tile of work item j (after the XCD remap): problem, tile row, tile column
+JOLT_DEV bool decode(const Grid &g, int j, int &z, int &tm, int &tn) {
+  if (j >= g.total) return false;
+  z = j / g.per_prob;
+  int r = j - z * g.per_prob;
+  if (g.lower_only) {
+    // r-th lower tile in row-major order: tm (tm + 1) / 2 <= r
+    int t = (int)((sqrtf(8.f * (float)r + 1.f) - 1.f) * 0.5f);
+    while ((t + 1) * (t + 2) / 2 <= r) ++t;
+    while (t * (t + 1) / 2 > r) --t;
+    tm = t; tn = r - t * (t + 1) / 2;
+  } else {
+    // groups of 8 tile rows, column-major inside a group
+    constexpr int GR = 8;
+    const int gsz = GR * g.tiles_n, grp = r / gsz, in = r - grp * gsz;
+    const int rows = min(GR, g.tiles_m - grp * GR);
+    tm = grp * GR + in % rows; tn = in / rows;
+  }
+  return true;
+}
+
+// BM x 128 tile per 256-thread workgroup; waves in a 2 x 2 grid, each (BM/2) x 64.
+template <int BM, bool AK, bool BK_, bool AS, bool BS>
+__global__ void __launch_bounds__(NT) k_gemm16(const GemmProblem *__restrict__ probs, Grid g) {
+  // blocks are dealt to the 8 XCDs round-robin; give each XCD a contiguous run of tiles
+  const int i = blockIdx.x, j = (i & 7) * g.per_xcd + (i >> 3);
+  int z, tm, tn;
+  if (!decode(g, j, z, tm, tn)) return;
+  const GemmProblem P = probs[z];
   if (tm * BM >= P.M || tn * BN >= P.N) return;
-  if (P.lower_only && tm < tn) return;
-  __shared__ __attribute__((aligned(16))) Lds16<AS, BS> sm;
-  constexpr int TILE = Lds16<AS, BS>::TILE;
+  constexpr int MI = BM / 64;      // 32-row MFMA blocks per wave
+  __shared__ __attribute__((aligned(16))) Lds<BM, AS, BS> sm;
+  constexpr int TA = BM * LDK, TB = BN * LDK;
+  constexpr int LA = Lds<BM, AS, BS>::LA, LB = Lds<BM, AS, BS>::LB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1, lr = lane & 31, lh = lane >> 5;
   const int m0 = tm * BM, n0 = tn * BN;
 
-  f32x16_t acc[2][2];
+  f32x16_t acc[MI][2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int a = 0; a < MI; ++a)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int b = 0; b < 2; ++b)
 #pragma unroll
-      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
+      for (int q = 0; q < 16; ++q) acc[a][b][q] = 0.f;
 
-  Stager<AK, AS> sa;
-  Stager<BK_, BS> sb;
-  sa.fetch(P.A, m0, 0, P.M, P.K, tid);
-  sb.fetch(P.B, n0, 0, P.N, P.K, tid);
-  for (int k0 = 0; k0 < P.K; k0 += BK) {
-    __syncthreads();
-    sa.stash(sm.a, sm.a + TILE, tid);
-    sb.stash(sm.b, sm.b + TILE, tid);
-    __syncthreads();
-    if (k0 + BK < P.K) {
-      sa.fetch(P.A, m0, k0 + BK, P.M, P.K, tid);
-      sb.fetch(P.B, n0, k0 + BK, P.N, P.K, tid);
-    }
+  constexpr int NS = 1;   // register stages (a deeper prefetch measured no faster)
+  Addr<BM, AK, AS> ad_a;
+  Addr<BN, BK_, BS> ad_b;
+  Stage<BM, AK, AS> sa[NS];
+  Stage<BN, BK_, BS> sb[NS];
+  ad_a.init(P.A, m0, P.M, tid);
+  ad_b.init(P.B, n0, P.N, tid);
+  const int kfull = P.K & ~(BK - 1);
+#define MM_FETCH(s, k) do { const int k_ = (k); \
+    if (k_ < kfull) { ad_a.fetch_full(P.A, k_, sa[s]); ad_b.fetch_full(P.B, k_, sb[s]); } } while (0)
+  auto compute_at = [&](int buf) {
+    const uint16_t *la_ = sm.a + buf * LA, *lb_ = sm.b + buf * LB;
 #pragma unroll
     for (int s = 0; s < BK / 16; ++s) {
       const int ko = s * 16 + 8 * lh;
-      bf16x8_t fa[2], fb[2], la[2], lb[2];
+      bf16x8_t fa[MI], fb[2], la[MI], lb[2];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int ra = (wm * 64 + i * 32 + lr) * LDK + ko, rb = (wn * 64 + i * 32 + lr) * LDK + ko;
-        fa[i] = *reinterpret_cast<const bf16x8_t *>(sm.a + ra);
-        fb[i] = *reinterpret_cast<const bf16x8_t *>(sm.b + rb);
-        if constexpr (AS) la[i] = *reinterpret_cast<const bf16x8_t *>(sm.a + TILE + ra);
-        if constexpr (BS) lb[i] = *reinterpret_cast<const bf16x8_t *>(sm.b + TILE + rb);
+      for (int a = 0; a < MI; ++a) {
+        const int ra = (wm * (BM / 2) + a * 32 + lr) * LDK + ko;
+        fa[a] = *reinterpret_cast<const bf16x8_t *>(la_ + ra);
+        if constexpr (AS) la[a] = *reinterpret_cast<const bf16x8_t *>(la_ + TA + ra);
       }
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int b = 0; b < 2; ++b) {
+        const int rb = (wn * 64 + b * 32 + lr) * LDK + ko;
+        fb[b] = *reinterpret_cast<const bf16x8_t *>(lb_ + rb);
+        if constexpr (BS) lb[b] = *reinterpret_cast<const bf16x8_t *>(lb_ + TB + rb);
+      }
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-          if constexpr (AS) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(la[i], fb[j], acc[i][j], 0, 0, 0);
-          if constexpr (BS) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], lb[j], acc[i][j], 0, 0, 0);
+      for (int a = 0; a < MI; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], acc[a][b], 0, 0, 0);
+          if constexpr (AS) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(la[a], fb[b], acc[a][b], 0, 0, 0);
+          if constexpr (BS) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], lb[b], acc[a][b], 0, 0, 0);
         }
     }
+  };
+  if constexpr (Lds<BM, AS, BS>::DB) {
+  // two LDS buffers: tile k+1 is stored into one while tile k is multiplied out of the
+  // other; one barrier per step
+  
+  int cur = 0;
+  if (kfull > 0) {
+    MM_FETCH(0, 0);
+    ad_a.stash(sa[0], sm.a, sm.a + TA, tid);
+    ad_b.stash(sb[0], sm.b, sm.b + TB, tid);
+    MM_FETCH(0, BK);
+    __syncthreads();
+  }
+  for (int k0 = 0; k0 < kfull; k0 += BK) {
+    compute_at(cur);
+    if (k0 + BK < kfull) {
+      ad_a.stash(sa[0], sm.a + (cur ^ 1) * LA, sm.a + (cur ^ 1) * LA + TA, tid);
+      ad_b.stash(sb[0], sm.b + (cur ^ 1) * LB, sm.b + (cur ^ 1) * LB + TB, tid);
+      MM_FETCH(0, k0 + 2 * BK);
+    }
+    __syncthreads();
+    cur ^= 1;
+  }
+  } else {
+#pragma unroll
+  for (int s = 0; s < NS; ++s) MM_FETCH(s, s * BK);
+  for (int k0 = 0; k0 < kfull; k0 += NS * BK) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      if (k0 + s * BK >= kfull) break;
+      __syncthreads();
+      ad_a.stash(sa[s], sm.a, sm.a + TA, tid);
+      ad_b.stash(sb[s], sm.b, sm.b + TB, tid);
+      __syncthreads();
+      MM_FETCH(s, k0 + (s + NS) * BK);
+      compute_at(0);
+    }
+  }
+  }
+#undef MM_FETCH
+  if (kfull < P.K) {            // ragged last K tile, every element bounds-checked
+    ad_a.fetch_tail(P.A, m0, kfull, P.M, P.K, tid, sa[0]);
+    ad_b.fetch_tail(P.B, n0, kfull, P.N, P.K, tid, sb[0]);
+    __syncthreads();
+    ad_a.stash(sa[0], sm.a, sm.a + TA, tid);
+    ad_b.stash(sb[0], sm.b, sm.b + TB, tid);
+    __syncthreads();
+    compute_at(0);
   }
 
   float alpha = P.alpha;
   if (P.alpha_exp2) alpha = ldexpf(alpha, (int)*gptr(P.alpha_exp2));
-  // epilogue through LDS, 32 rows per round: acc[i][j][q] is the output at row
-  // wm*64 + i*32 + 8*(q/4) + 4*lh + q%4, column wn*64 + j*32 + lr of the tile
+  // epilogue through LDS, 32 rows per round: acc[a][b][q] is the output at row
+  // wm*(BM/2) + a*32 + 8*(q/4) + 4*lh + q%4, column wn*64 + b*32 + lr of the tile
   float *cs = reinterpret_cast<float *>(&sm);
   constexpr int CLD = BN + 4;
-  static_assert(32 * CLD * sizeof(float) <= sizeof(Lds16<AS, BS>), "epilogue tile exceeds LDS");
+  static_assert(32 * CLD * sizeof(float) <= sizeof(Lds<BM, AS, BS>), "epilogue tile exceeds LDS");
   const bool use_beta = P.beta != 0.f;
+  const bool ct = P.c_trans != 0;   // store the transpose: C[col * ldc + row]
   const bool vec = ((reinterpret_cast<uintptr_t>(P.C) & 15) == 0) && (P.ldc % 4 == 0);
 #pragma unroll
-  for (int h = 0; h < 4; ++h) {
+  for (int h = 0; h < BM / 32; ++h) {
     __syncthreads();
-    if (wm == (h >> 1)) {
-      const int i = h & 1;
+    if (wm == h / MI) {
+      const int a = h % MI;
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int b = 0; b < 2; ++b)
 #pragma unroll
         for (int q = 0; q < 16; ++q)
-          cs[(8 * (q >> 2) + 4 * lh + (q & 3)) * CLD + wn * 64 + j * 32 + lr] = acc[i][j][q];
+          cs[(8 * (q >> 2) + 4 * lh + (q & 3)) * CLD + wn * 64 + b * 32 + lr] = acc[a][b][q];
     }
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const int idx = tid + u * NT, rr = idx >> 5, cc = (idx & 31) * 4;
+      const int idx = tid + u * NT;
+      int rr, cc;
+      if (ct) { cc = idx >> 3; rr = (idx & 7) * 4; }
+      else { rr = idx >> 5; cc = (idx & 31) * 4; }
       const int row = m0 + h * 32 + rr, col = n0 + cc;
-      if (row >= P.M || col >= P.N) continue;
-      const float4 a4 = *reinterpret_cast<const float4 *>(&cs[rr * CLD + cc]);
-      float v[4] = {alpha * a4.x, alpha * a4.y, alpha * a4.z, alpha * a4.w};
-      JOLT_GLOBAL float *dst = gptr(P.C + (int64_t)row * P.ldc + col);
-      if (vec && col + 4 <= P.N) {
-        if (use_beta) {
-          const jf4 o4 = *reinterpret_cast<const JOLT_GLOBAL jf4 *>(dst);
-          v[0] = fmaf(P.beta, o4.x, v[0]); v[1] = fmaf(P.beta, o4.y, v[1]);
-          v[2] = fmaf(P.beta, o4.z, v[2]); v[3] = fmaf(P.beta, o4.w, v[3]);
-        }
-        *reinterpret_cast<JOLT_GLOBAL jf4 *>(dst) = jf4{v[0], v[1], v[2], v[3]};
-      } else {
+      if (ct) {
+        if (col >= P.N || row >= P.M) continue;
+        float v[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (col + e < P.N) dst[e] = use_beta ? fmaf(P.beta, dst[e], v[e]) : v[e];
+        for (int e = 0; e < 4; ++e) v[e] = alpha * cs[(rr + e) * CLD + cc];
+        JOLT_GLOBAL float *dst = gptr(P.C + (int64_t)col * P.ldc + row);
+        if (vec && row + 4 <= P.M) {
+          if (use_beta) {
+            const jf4 o4 = *reinterpret_cast<const JOLT_GLOBAL jf4 *>(dst);
+            v[0] = fmaf(P.beta, o4.x, v[0]); v[1] = fmaf(P.beta, o4.y, v[1]);
+            v[2] = fmaf(P.beta, o4.z, v[2]); v[3] = fmaf(P.beta, o4.w, v[3]);
+          }
+          *reinterpret_cast<JOLT_GLOBAL jf4 *>(dst) = jf4{v[0], v[1], v[2], v[3]};
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (row + e < P.M) dst[e] = use_beta ? fmaf(P.beta, dst[e], v[e]) : v[e];
+        }
+      } else {
+        if (row >= P.M || col >= P.N) continue;
+        const float4 a4 = *reinterpret_cast<const float4 *>(&cs[rr * CLD + cc]);
+        float v[4] = {alpha * a4.x, alpha * a4.y, alpha * a4.z, alpha * a4.w};
+        JOLT_GLOBAL float *dst = gptr(P.C + (int64_t)row * P.ldc + col);
+        if (vec && col + 4 <= P.N) {
+          if (use_beta) {
+            const jf4 o4 = *reinterpret_cast<const JOLT_GLOBAL jf4 *>(dst);
+            v[0] = fmaf(P.beta, o4.x, v[0]); v[1] = fmaf(P.beta, o4.y, v[1]);
+            v[2] = fmaf(P.beta, o4.z, v[2]); v[3] = fmaf(P.beta, o4.w, v[3]);
+          }
+          *reinterpret_cast<JOLT_GLOBAL jf4 *>(dst) = jf4{v[0], v[1], v[2], v[3]};
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (col + e < P.N) dst[e] = use_beta ? fmaf(P.beta, dst[e], v[e]) : v[e];
+        }
       }
     }
   }
 }
 
-template <bool AS, bool BS>
-hipError_t launch16(const GemmProblem *probs, dim3 grid, bool ak, bool bk, hipStream_t st) {
-  if (ak && bk) hipLaunchKernelGGL((k_gemm16<true, true, AS, BS>), grid, dim3(NT), 0, st, probs);
-  else if (ak) hipLaunchKernelGGL((k_gemm16<true, false, AS, BS>), grid, dim3(NT), 0, st, probs);
-  else if (bk) hipLaunchKernelGGL((k_gemm16<false, true, AS, BS>), grid, dim3(NT), 0, st, probs);
-  else hipLaunchKernelGGL((k_gemm16<false, false, AS, BS>), grid, dim3(NT), 0, st, probs);
+template <int BM, bool AS, bool BS>
+hipError_t launch_bm(const GemmProblem *probs, const Grid &g, bool ak, bool bk, hipStream_t st) {
+  const dim3 grid(g.per_xcd * 8);
+  if (ak && bk) hipLaunchKernelGGL((k_gemm16<BM, true, true, AS, BS>), grid, dim3(NT), 0, st, probs, g);
+  else if (ak) hipLaunchKernelGGL((k_gemm16<BM, true, false, AS, BS>), grid, dim3(NT), 0, st, probs, g);
+  else if (bk) hipLaunchKernelGGL((k_gemm16<BM, false, true, AS, BS>), grid, dim3(NT), 0, st, probs, g);
+  else hipLaunchKernelGGL((k_gemm16<BM, false, false, AS, BS>), grid, dim3(NT), 0, st, probs, g);
   return hipGetLastError();
+}
+
+// largest element offset of an operand view of rows x cols (row-major over ld with segments)
+int64_t max_offset(const GemmOperand &o, int64_t rows, int64_t cols) {
+  if (rows <= 0 || cols <= 0) return 0;
+  int64_t colmax = cols - 1;
+  if (o.seg_len > 0) {
+    const int64_t segs = (cols + o.seg_len - 1) / o.seg_len;
+    int64_t best = 0;
+    // the segment offset grows with both its quotient and remainder by seg_heads
+    const int64_t hq = (segs - 1) / o.seg_heads, hr = std::min<int64_t>(segs - 1, o.seg_heads - 1);
+    best = hq * o.seg_hi + hr * o.seg_lo + (o.seg_len - 1);
+    colmax = best;
+  }
+  return (rows - 1) * o.ld + colmax;
+}
+
+// Layout conditions of the fast loads for one operand: 16-byte aligned vectors at every
+// (row, 8-aligned column), 64-wide k runs inside one segment (k-contiguous), 8-wide
+// column runs inside one segment and inside the row (mn-contiguous), 32-bit offsets.
+bool operand_ok(const GemmOperand &o, bool kc, bool f32, int MN, int K) {
+  const int esz = f32 ? 4 : 2, vec = 16 / esz;
+  if (reinterpret_cast<uintptr_t>(o.ptr) % 16) return false;
+  if (o.ld % vec) return false;
+  if (o.seg_len > 0) {
+    if (o.seg_hi % vec || o.seg_lo % vec) return false;
+    if (kc ? (o.seg_len % BK) : (o.seg_len % 8)) return false;
+  }
+  const int64_t lim = (int64_t)1 << 31;
+  if (kc) {
+    // per-thread part: row * ld + (k run within the tile); the k column part is added
+    // in 64 bits per step
+    if ((int64_t)(MN - 1) * o.ld + BK >= lim) return false;
+    if (o.seg_len == 0 && o.ld < K) return false;
+  } else {
+    // column runs may overhang MN by up to 7 elements inside the row's ld
+    if (MN % 8 && o.seg_len == 0 && o.ld < ((MN + 7) / 8) * 8) return false;
+    if ((int64_t)BK * o.ld + max_offset(o, 1, MN) >= lim) return false;
+  }
+  return true;
 }
 
 }  // namespace
 
+bool gemm16_prepare(GemmProblem *probs, int n, int &ta, int &tb, bool &ak, bool &bk, int &bm) {
+  if (n <= 0) return false;
+  if ((ta != GT_BF16 && ta != GT_F32) || (tb != GT_BF16 && tb != GT_F32)) return false;
+  // one fp32 operand is taken on the B side (its 128-wide tile keeps the split registers
+  // small): swap the roles of A and B and store C^T
+  const bool swap = ta == GT_F32 && tb == GT_BF16;
+  for (int i = 0; i < n; ++i) {
+    GemmProblem p = probs[i];
+    if (p.c_trans) return false;
+    if (swap) { std::swap(p.A, p.B); std::swap(p.M, p.N); p.c_trans = 1; }
+    const bool a32 = (swap ? tb : ta) == GT_F32, b32 = (swap ? ta : tb) == GT_F32;
+    const bool akc = swap ? bk : ak, bkc = swap ? ak : bk;
+    if (!operand_ok(p.A, akc, a32, p.M, p.K) || !operand_ok(p.B, bkc, b32, p.N, p.K)) return false;
+    if (p.c_trans && p.lower_only) return false;
+  }
+  for (int i = 1; i < n; ++i)
+    if ((probs[i].lower_only != 0) != (probs[0].lower_only != 0)) return false;
+  int maxM = 0;
+  bool lower = false;
+  for (int i = 0; i < n; ++i) {
+    GemmProblem &p = probs[i];
+    if (swap) { std::swap(p.A, p.B); std::swap(p.M, p.N); p.c_trans = 1; }
+    maxM = std::max(maxM, p.M);
+    lower = lower || p.lower_only;
+  }
+  if (swap) { std::swap(ta, tb); std::swap(ak, bk); }
+  // 256-row tiles for split-operand products over long M (two LDS buffers still fit);
+  // 128 otherwise, and always for lower-triangle tables
+  bm = (tb == GT_F32 && ta == GT_BF16 && maxM >= 2048 && !lower) ? 256 : 128;
+  return true;
+}
+
 hipError_t launch_gemm16(const GemmProblem *probs_dev, int n_probs, int max_M, int max_N, int ta,
-                         int tb, bool a_kcontig, bool b_kcontig, hipStream_t st) {
+                         int tb, bool a_kcontig, bool b_kcontig, int bm, bool lower_only,
+                         hipStream_t st) {
   if (n_probs <= 0 || max_M <= 0 || max_N <= 0) return hipSuccess;
-  const dim3 grid((max_N + BN - 1) / BN, (max_M + BM - 1) / BM, n_probs);
   const bool as = ta == GT_F32, bs = tb == GT_F32;
-  if ((ta != GT_BF16 && !as) || (tb != GT_BF16 && !bs) || (as && bs)) return hipErrorInvalidValue;
-  if (as) return launch16<true, false>(probs_dev, grid, a_kcontig, b_kcontig, st);
-  if (bs) return launch16<false, true>(probs_dev, grid, a_kcontig, b_kcontig, st);
-  return launch16<false, false>(probs_dev, grid, a_kcontig, b_kcontig, st);
+  if ((ta != GT_BF16 && !as) || (tb != GT_BF16 && !bs)) return hipErrorInvalidValue;
+  if (bm != 128 && bm != 256) return hipErrorInvalidValue;
+  if (lower_only && bm != BN) return hipErrorInvalidValue;
+  Grid g;
+  g.tiles_m = (max_M + bm - 1) / bm;
+  g.tiles_n = (max_N + BN - 1) / BN;
+  g.lower_only = lower_only ? 1 : 0;
+  g.per_prob = lower_only ? g.tiles_m * (g.tiles_m + 1) / 2 : g.tiles_m * g.tiles_n;
+  g.total = g.per_prob * n_probs;
+  g.per_xcd = (g.total + 7) / 8;
+  if (bm == 256) {
+    if (as && bs) return hipErrorInvalidValue;
+    if (as) return launch_bm<256, true, false>(probs_dev, g, a_kcontig, b_kcontig, st);
+    if (bs) return launch_bm<256, false, true>(probs_dev, g, a_kcontig, b_kcontig, st);
+    return launch_bm<256, false, false>(probs_dev, g, a_kcontig, b_kcontig, st);
+  }
+  if (as && bs) return launch_bm<128, true, true>(probs_dev, g, a_kcontig, b_kcontig, st);
+  if (as) return launch_bm<128, true, false>(probs_dev, g, a_kcontig, b_kcontig, st);
+  if (bs) return launch_bm<128, false, true>(probs_dev, g, a_kcontig, b_kcontig, st);
+  return launch_bm<128, false, false>(probs_dev, g, a_kcontig, b_kcontig, st);
 }

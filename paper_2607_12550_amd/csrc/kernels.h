@@ -117,19 +117,24 @@ struct GemmProblem {
   int32_t M, N, K;
   float alpha, beta;
   int32_t lower_only;    // compute only tiles with tile_m >= tile_n (symmetric outputs)
-  int32_t pad;
+  int32_t c_trans;       // bf16 kernel only: store element (m, n) at C[n * ldc + m]
   const int8_t *alpha_exp2;  // optional: alpha is multiplied by 2^(*alpha_exp2)
 };
 
-// mode: 0 = bf16 x bf16 inputs on bf16 MFMA; 1 = fp32 MFMA with A/B of types ta/tb;
-//       2 = bf16 MFMA with one fp32 operand split into bf16 hi + lo
-// converted exactly to fp32 (bf16, fp16 or fp32 inputs).
+// fp32 MFMA GEMM (mode 1): A/B of types ta/tb (bf16, fp16 or fp32) converted exactly to
+// fp32; every table accepted.
 hipError_t launch_gemm(const GemmProblem *probs_dev, int n_probs, int max_M, int max_N,
                        int mode, int ta, int tb, bool a_kcontig, bool b_kcontig, hipStream_t st);
-// bf16 matrix-core GEMM; ta/tb GT_BF16 (used as is) or GT_F32 (split into bf16 hi + lo,
-// at most one operand)
+// bf16 matrix-core GEMM; ta/tb GT_BF16 (used as is) or GT_F32 (split into bf16 hi + lo).
+// gemm16_prepare() runs on the host copy of the table before it is uploaded: it returns
+// false when a layout condition of the kernel is not met (use launch_gemm then), and may
+// rewrite the table and the type / layout arguments (an fp32 A is moved to the B side by
+// computing C^T) and picks the tile height bm for launch_gemm16.
+bool gemm16_prepare(GemmProblem *probs_host, int n_probs, int &ta, int &tb, bool &a_kcontig,
+                    bool &b_kcontig, int &bm);
 hipError_t launch_gemm16(const GemmProblem *probs_dev, int n_probs, int max_M, int max_N, int ta,
-                         int tb, bool a_kcontig, bool b_kcontig, hipStream_t st);
+                         int tb, bool a_kcontig, bool b_kcontig, int bm, bool lower_only,
+                         hipStream_t st);
 
 // ----------------------------------------------------------------- feature Gram / energy
 // F[cell] = sum over rows of x^T x for the row set {(s, r) : s < nseg, r < rows_per_seg}

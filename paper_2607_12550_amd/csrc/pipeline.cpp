@@ -201,18 +201,30 @@ struct Run {
   Ws w;
   size_t tab_used = 0;
 
-  // upload a problem table into the next slice of the device table area, then launch
-  int gemm(const std::vector<GemmProblem> &probs, int mode, int ta, int tb, bool ak, bool bk) {
-    if (probs.empty()) return JOLT_OK;
-    if (tab_used + probs.size() > w.tab_n)
+  // upload a problem table into the next slice of the device table area, then launch.
+  // mode 0: bf16 x bf16 on the bf16 matrix cores; mode 2: the same kernel with fp32
+  // operands split into bf16 hi + lo; mode 1: fp32 MFMA.  A table the bf16 kernel's layout
+  // conditions reject runs on the fp32 kernel.
+  int gemm(const std::vector<GemmProblem> &probs_in, int mode, int ta, int tb, bool ak, bool bk) {
+    if (probs_in.empty()) return JOLT_OK;
+    if (tab_used + probs_in.size() > w.tab_n)
       return jolt_fail(JOLT_E_WORKSPACE, "GEMM problem table overflow");
+    std::vector<GemmProblem> probs(probs_in);
+    int bm = 128;
+    bool fast = false;
+    if (mode == 0 || mode == 2) {
+      fast = gemm16_prepare(probs.data(), (int)probs.size(), ta, tb, ak, bk, bm);
+      if (!fast) probs = probs_in;
+    }
     GemmProblem *dst = w.tab + tab_used;
     tab_used += probs.size();
     HIP_OK(hipMemcpyAsync(dst, probs.data(), probs.size() * sizeof(GemmProblem),
                           hipMemcpyHostToDevice, st));
     int maxM = 0, maxN = 0;
-    for (auto &p : probs) { maxM = std::max(maxM, p.M); maxN = std::max(maxN, p.N); }
-    HIP_OK(launch_gemm(dst, (int)probs.size(), maxM, maxN, mode, ta, tb, ak, bk, st));
+    bool lower = false;
+    for (auto &p : probs) { maxM = std::max(maxM, p.M); maxN = std::max(maxN, p.N); lower = lower || p.lower_only; }
+    if (fast) HIP_OK(launch_gemm16(dst, (int)probs.size(), maxM, maxN, ta, tb, ak, bk, bm, lower, st));
+    else HIP_OK(launch_gemm(dst, (int)probs.size(), maxM, maxN, 1, ta, tb, ak, bk, st));
     return JOLT_OK;
   }
 
@@ -416,8 +428,11 @@ static bool same_opts(const jolt_spectrum_opts &a, const jolt_spectrum_opts &b) 
 
 namespace {
 
-// CholeskyQR2 of the rows x l matrices in buf (ld ldl): result back in buf, tmp is scratch
-int orth(Run &R, const SpecShape &sh, int nc, float *buf, float *tmp, int rows) {
+// CholeskyQR2 of the rows x l matrices in buf (ld ldl): result back in buf, tmp is scratch.
+// split_first: the first pass's product Y R^-1 runs on the bf16 matrix cores with both
+// operands split into hi + lo (relative error ~2^-16: the basis it yields is orthonormal
+// to that order, which the second pass, in fp32, restores to fp32 accuracy).
+int orth(Run &R, const SpecShape &sh, int nc, float *buf, float *tmp, int rows, bool split_first) {
   const int l = sh.ell, ldl = R.w.ldl;
   float *src = buf, *dst = tmp;
   for (int pass = 0; pass < 2; ++pass) {
@@ -437,7 +452,7 @@ int orth(Run &R, const SpecShape &sh, int nc, float *buf, float *tmp, int rows) 
       p.C = dst + (int64_t)c * rows * ldl; p.ldc = ldl;
       p.M = rows; p.N = l; p.K = l; p.alpha = 1.f;
     }
-    int rc = R.gemm(P, 1, GT_F32, GT_F32, true, false);
+    int rc = R.gemm(P, split_first && pass == 0 ? 2 : 1, GT_F32, GT_F32, true, false);
     if (rc) return rc;
     std::swap(src, dst);
   }
@@ -470,7 +485,7 @@ int token_flash(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc,
   int rc;
   {
     StageTimer t(R.ctx, R.st, JOLT_STAGE_ORTH);
-    rc = orth(R, sh, nc, R.w.Ysk, R.w.Qsk, T);
+    rc = orth(R, sh, nc, R.w.Ysk, R.w.Qsk, T, dt == GT_BF16);
     if (rc) return rc;
   }
   for (int it = 0; it < o->power_iters; ++it) {
@@ -490,7 +505,7 @@ int token_flash(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc,
     }
     {
       StageTimer t(R.ctx, R.st, JOLT_STAGE_ORTH);
-      rc = orth(R, sh, nc, R.w.Zsk, R.w.Qz, N);
+      rc = orth(R, sh, nc, R.w.Zsk, R.w.Qz, N, dt == GT_BF16);
       if (rc) return rc;
     }
     {
@@ -508,7 +523,7 @@ int token_flash(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc,
     }
     {
       StageTimer t(R.ctx, R.st, JOLT_STAGE_ORTH);
-      rc = orth(R, sh, nc, R.w.Ysk, R.w.Qsk, T);
+      rc = orth(R, sh, nc, R.w.Ysk, R.w.Qsk, T, dt == GT_BF16);
       if (rc) return rc;
     }
   }
