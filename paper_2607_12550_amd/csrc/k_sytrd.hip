@@ -80,7 +80,34 @@ JOLT_DEV void householder(float alpha, double sigma, double &beta, double &tv, d
   scal = 1.0 / (alpha - beta);
 }
 
-// per 128-row block from o: v, y, w_pre and partial w_pre^T v for column i (panel index j)
+// sum_{b < nb_} x[b * stride] in the order b = 0, 1, ... (fp64), loads issued eight at a time
+JOLT_DEV double strided_sum(const float *x, int64_t stride, int nb_) {
+  double s = 0.0;
+  int b = 0;
+  for (; b + 8 <= nb_; b += 8) {
+    float t[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) t[q] = x[(int64_t)(b + q) * stride];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) s += (double)t[q];
+  }
+  for (; b < nb_; ++b) s += (double)x[(int64_t)b * stride];
+  return s;
+}
+
+// sum of the nt partial-slot entries of one row (slot s at s * n), in slot order; the
+// first 32 loads are issued together
+JOLT_DEV float slot_sum(const float *pp, int64_t n, int nt) {
+  float t[32];
+#pragma unroll
+  for (int s = 0; s < 32; ++s) t[s] = s < nt ? pp[(int64_t)s * n] : 0.f;
+  float y = 0.f;
+#pragma unroll
+  for (int s = 0; s < 32; ++s) y += t[s];
+  for (int s = 32; s < nt; ++s) y += pp[(int64_t)s * n];
+  return y;
+}
+
 __global__ void __launch_bounds__(RB) k_col_finish(SytrdArgs a, int i, int j, int jbw) {
   const int mat = blockIdx.y, n = a.n, nb = a.nb, o = i + 1;
   const int base = o & ~31, nt = (n - base + TB - 1) / TB;
@@ -90,10 +117,26 @@ __global__ void __launch_bounds__(RB) k_col_finish(SytrdArgs a, int i, int j, in
   __shared__ double red[RB / 64];
   __shared__ double sh_sigma;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  float *V = M.P, *W = M.P + (int64_t)jbw * n;
+  float *Qv = M.Q + (int64_t)jbw * n;
+  const int r = o + blockIdx.x * RB + tid;
+  const int rr = r < n ? r : o;                 // in-range row for the loads
+  // Loads that do not depend on this column's Householder scalars go first, so their
+  // latency overlaps the reduction of sigma and the dots below.
+  const float ysl = slot_sum(M.part + (rr - base), n, nt);
+  const float a_o = M.A[(int64_t)o * n + rr];   // A22[:, 0] (row o by symmetry)
+  const float x_r = M.xt[rr];
+  float vrow[32], wrow[32];
+#pragma unroll
+  for (int p = 0; p < 32; ++p) {
+    vrow[p] = p < j ? V[(int64_t)p * n + rr] : 0.f;
+    wrow[p] = p < j ? W[(int64_t)p * n + rr] : 0.f;
+  }
+  float w_o = 0.f, v_o = 0.f;
+  if (tid < j) { w_o = W[(int64_t)tid * n + o]; v_o = V[(int64_t)tid * n + o]; }
   // sigma and the dots, summed over the row blocks in a fixed order
   if (tid < 2 * j + 1) {
-    double s = 0.0;
-    for (int b = 0; b < nprev; ++b) s += (double)M.dpart[(int64_t)b * (2 * nb + 1) + tid];
+    const double s = strided_sum(M.dpart + tid, 2 * nb + 1, nprev);
     if (tid == 0) sh_sigma = s;
     else if (tid <= j) pw[tid - 1] = (float)s;
     else pv[tid - 1 - j] = (float)s;
@@ -103,24 +146,19 @@ __global__ void __launch_bounds__(RB) k_col_finish(SytrdArgs a, int i, int j, in
   double beta, tv, scal;
   householder(alpha, sh_sigma, beta, tv, scal);
   const float sc = (float)scal, tf = (float)tv;
-  float *V = M.P, *W = M.P + (int64_t)jbw * n;
-  float *Qv = M.Q + (int64_t)jbw * n;
   // W^T v = scal W^T x_tail + W[o, :]  (v = e_o + scal x_tail, x_tail[o] = 0)
   if (tid < j) {
-    pw[tid] = sc * pw[tid] + W[(int64_t)tid * n + o];
-    pv[tid] = sc * pv[tid] + V[(int64_t)tid * n + o];
+    pw[tid] = sc * pw[tid] + w_o;
+    pv[tid] = sc * pv[tid] + v_o;
   }
   __syncthreads();
-  const int r = o + blockIdx.x * RB + tid;
   double dot = 0.0;
   if (r < n) {
-    const float vr = (r == o) ? 1.f : (tv == 0.0 ? 0.f : sc * M.xt[r]);
-    float y = 0.f;
-    const float *pp = M.part + (r - base);
-#pragma unroll 8
-    for (int s = 0; s < nt; ++s) y += pp[(int64_t)s * n];
-    y = sc * y + M.A[(int64_t)o * n + r];        // + A22[:, 0] (row o by symmetry)
-    for (int p = 0; p < j; ++p) y -= V[(int64_t)p * n + r] * pw[p] + W[(int64_t)p * n + r] * pv[p];
+    const float vr = (r == o) ? 1.f : (tv == 0.0 ? 0.f : sc * x_r);
+    float y = sc * ysl + a_o;
+#pragma unroll
+    for (int p = 0; p < 32; ++p)
+      if (p < j) y -= vrow[p] * pw[p] + wrow[p] * pv[p];
     const float wp = (tv == 0.0) ? 0.f : tf * y;
     M.wpre[r] = wp;
     V[(int64_t)j * n + r] = vr;
@@ -256,42 +294,53 @@ __global__ void __launch_bounds__(RB) k_col_next(SytrdArgs a, int i, int j, int 
   __shared__ float cw[64], cv[64];
   __shared__ float alpha2_s;
   const int tid = threadIdx.x;
-  float alpha2 = 0.f;
+  // rows from ip (= i + 1 = o of column i unless prep_only) in blocks of 128, one per thread
+  const int r = (prep_only ? ip : i + 1) + blockIdx.x * RB + tid;
+  const int rr = r < n ? r : n - 1;             // in-range row for the loads
+  const bool next = ip < n - 1;
+  // Loads that do not need alpha2 go first: panel rows p < j of V and W at this row and at
+  // row ip, the row ip of A, and what rebuilds w_j
+  float vrow[32], wrow[32];
+#pragma unroll
+  for (int p = 0; p < 32; ++p) {
+    const bool ld = next && p < jp && (prep_only || p < j);
+    vrow[p] = ld ? V[(int64_t)p * n + rr] : 0.f;
+    wrow[p] = ld ? W[(int64_t)p * n + rr] : 0.f;
+  }
+  const float a_ip = next ? M.A[(int64_t)ip * n + rr] : 0.f;
+  float cw_t = 0.f, cv_t = 0.f;
+  if (next && tid < jp) {
+    cv_t = V[(int64_t)tid * n + ip];
+    if (prep_only || tid < j) cw_t = W[(int64_t)tid * n + ip];
+  }
+  float alpha2 = 0.f, w = 0.f;
   if (!prep_only) {
     const int o = i + 1;
+    const float wpre_r = M.wpre[rr], vj_r = V[(int64_t)j * n + rr];
+    vrow[j] = vj_r;
     const int nblk = (n - o + RB - 1) / RB;          // row blocks of column i's k_col_finish
-    if (tid == 0) {
-      double s = 0.0;
-      for (int b = 0; b < nblk; ++b) s += (double)M.wpart[b];
-      alpha2_s = (float)(-0.5 * (double)M.tau[i] * s);
-    }
+    if (tid == 0) alpha2_s = (float)(-0.5 * (double)M.tau[i] * strided_sum(M.wpart, 1, nblk));
     __syncthreads();
     alpha2 = alpha2_s;
-    // rows o .. n-1 in blocks of 128; each thread owns one row
-    const int r = o + blockIdx.x * RB + tid;
+    w = wpre_r + alpha2 * vj_r;
+    wrow[j] = w;
     if (r < n) {
-      const float w = M.wpre[r] + alpha2 * V[(int64_t)j * n + r];
       W[(int64_t)j * n + r] = w;
       M.Q[(int64_t)j * n + r] = w;
     }
-    if (ip >= n - 1) return;
+    if (!next) return;
+    // reflector j's w[ip] is rebuilt here because another workgroup of this launch writes it
+    if (tid == j) cw_t = M.wpre[ip] + alpha2 * V[(int64_t)j * n + ip];
   }
-  // coefficients W[p][ip], V[p][ip]; reflector j's w[ip] is rebuilt here because another
-  // workgroup of this launch writes it
-  if (tid < jp) {
-    float wv = W[(int64_t)tid * n + ip];
-    if (!prep_only && tid == j) wv = M.wpre[ip] + alpha2 * V[(int64_t)j * n + ip];
-    cw[tid] = wv;
-    cv[tid] = V[(int64_t)tid * n + ip];
-  }
+  if (tid < jp) { cw[tid] = cw_t; cv[tid] = cv_t; }
   __syncthreads();
-  // x[r] = A[ip][r] - sum_p (V[p][r] W[p][ip] + W[p][r] V[p][ip]) for r >= ip (row ip = column ip);
-  // row r of W_j was written above by this same thread
-  const int r = ip + blockIdx.x * RB + tid;
+  // x[r] = A[ip][r] - sum_p (V[p][r] W[p][ip] + W[p][r] V[p][ip]) for r >= ip (row ip = column ip)
   float xtail = 0.f;
   if (r < n) {
-    float x = M.A[(int64_t)ip * n + r];
-    for (int p = 0; p < jp; ++p) x -= V[(int64_t)p * n + r] * cw[p] + W[(int64_t)p * n + r] * cv[p];
+    float x = a_ip;
+#pragma unroll
+    for (int p = 0; p < 32; ++p)
+      if (p < jp) x -= vrow[p] * cw[p] + wrow[p] * cv[p];
     if (r == ip) M.sc[1] = x;
     if (r == ip + 1) M.sc[0] = x;
     xtail = (r > ip + 1) ? x : 0.f;
@@ -302,14 +351,13 @@ __global__ void __launch_bounds__(RB) k_col_next(SytrdArgs a, int i, int j, int 
   __shared__ float prod[2 * 32 + 1][RB];
   const int nk = 2 * jp + 1;
   prod[0][tid] = xtail * xtail;
-  for (int p = 0; p < jp; ++p) {
-    const bool ok = r < n;
-    prod[1 + p][tid] = ok ? W[(int64_t)p * n + r] * xtail : 0.f;
-    prod[1 + jp + p][tid] = ok ? V[(int64_t)p * n + r] * xtail : 0.f;
-  }
+#pragma unroll
+  for (int p = 0; p < 32; ++p)
+    if (p < jp) { prod[1 + p][tid] = wrow[p] * xtail; prod[1 + jp + p][tid] = vrow[p] * xtail; }
   __syncthreads();
   if (tid < nk) {
     float sum = 0.f;
+#pragma unroll 16
     for (int t = 0; t < RB; ++t) sum += prod[tid][t];
     M.dpart[(int64_t)blockIdx.x * (2 * a.nb + 1) + tid] = sum;
   }
