@@ -24,9 +24,11 @@ Module map (paper passages in brackets):
   compression, the blob byte format, metrics.
 * :mod:`oracle.rope`      - rotary position embedding re-applied to decoded
   keys (appendix B: keys are compressed before RoPE).
+* :mod:`oracle.diagnostics` - singular values of the three mode unfoldings and
+  their appendix-A summary (section 3, appendix A).
 
 Parity-unpinned items (no value in the paper can be reproduced on synthetic
 data): the absolute reconstruction errors, the epsilon^2(b) values, the chosen
 ranks and the speedups.
 """
-from . import rounding, philox, residual, tucker, alloc, pipeline, rope  # noqa: F401,E402
+from . import rounding, philox, residual, tucker, alloc, pipeline, rope, diagnostics  # noqa: F401,E402
