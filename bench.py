@@ -67,6 +67,10 @@ def parse():
     ap.add_argument("--no-stage-profile", action="store_true",
                     help="skip the event-instrumented pass (for hardware-counter runs); the "
                          "stage and roofline fields are then omitted")
+    ap.add_argument("--diagnostics", action="store_true",
+                    help="instead of the benchmark step: the appendix-A three-mode table of one "
+                         "synthetic Mistral-shaped layer (layer 15, T = 1024, K and V), and the "
+                         "slice-mode spectrum timed over every cell of --workload")
     return ap.parse_args()
 
 
@@ -200,8 +204,76 @@ def cpu_baseline(K_np, V_np, cfg, params, group, T_sample, method, q, p, iters,
             "seconds": round(t_all, 2)}
 
 
+def diagnostics(args):
+    """Appendix A's table (sigma_1 / sigma_min and ranks at 10% / 20% relative Frobenius
+    error per mode) for one synthetic layer, from the library's three mode spectra; then
+    the slice-mode Gram of every cell of the workload, timed with the stage events."""
+    import numpy as np
+    import torch
+
+    import kvsynth
+    import paper_2607_12550_amd as J
+    from paper_2607_12550_amd.cache import CacheCodec
+
+    ctx = J.jolt_create(0)
+    H, T, d = 8, 1024, 128
+    desc = J.cell_desc(dtype=J.JOLT_BF16, n_layers=1, n_heads=H, T=T, d=d,
+                       stride_layer=H * T * d, stride_head=T * d, stride_token=d)
+    ws_s = torch.empty(J.jolt_slice_spectrum_workspace_size(desc, 1), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(J.jolt_workspace_size(desc, 1, None), dtype=torch.uint8, device="cuda")
+    rows = []
+    for tensor, name in ((0, "K"), (1, "V")):
+        x = kvsynth.layer_kv(layer=15, tensor=tensor, n_heads=H, T=T, d=d, alpha=(1.5, 0.7)[tensor],
+                             n_out=2, out_scale=10.0, data_seed=0)[0]
+        t = torch.from_numpy(kvsynth.f32_to_bf16_bits(x).view(np.int16)).view(torch.bfloat16).cuda()
+        lam_s = J.jolt_slice_spectrum(ctx, desc, [t], ws_s)[0]
+        _, lam_t, lam_f = J.jolt_spectrum(ctx, desc, [t], None, None, ws)
+        for mode, lam, n in (("heads", lam_s, H), ("tokens", lam_t[0], T), ("features", lam_f[0], d)):
+            rng, r10, r20 = J.jolt_mode_summary(lam, 0.10, 0.20)
+            # an infinite range: the smallest eigenvalue is below the fp32 Gram's resolution
+            rows.append({"tensor": name, "mode": f"{mode} ({n})",
+                         "sigma_range": round(rng, 2) if np.isfinite(rng) else "inf",
+                         "r_10pct": f"{r10}/{n}", "r_20pct": f"{r20}/{n}"})
+            log(f"{name} {mode:9s} ({n:5d})  sigma1/sigmamin {rng:12.2f}  r10 {r10:5d}/{n}  r20 {r20:5d}/{n}")
+    # slice-mode Gram over every cell of the workload
+    cfg = dict(kvsynth.CONFIGS[args.workload])
+    gl = cfg.pop("group_layers")
+    cfg["workers"] = 8
+    Knp, Vnp = kvsynth.make_cache(**cfg)
+    to_dev = (lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()) \
+        if cfg["dtype"] == "bf16" else (lambda a: torch.from_numpy(a).cuda())
+    K, V = to_dev(Knp), to_dev(Vnp)
+    codec = CacheCodec(K, V, group_layers=gl, method="exact", ratio=2.0)
+    cd, ptrs = codec.desc, [c.ptr for c in codec.cells]
+    wsc = torch.empty(J.jolt_slice_spectrum_workspace_size(cd, len(ptrs)), dtype=torch.uint8, device="cuda")
+    J.jolt_slice_spectrum(ctx, cd, ptrs, wsc)                       # warm-up
+    J.jolt_profile_enable(ctx, True)
+    J.jolt_profile_reset(ctx)
+    reps = 5
+    for _ in range(reps):
+        J.jolt_slice_spectrum(ctx, cd, ptrs, wsc)
+    prof = J.jolt_profile_read(ctx)
+    J.jolt_profile_enable(ctx, False)
+    ms = prof["slice_gram"][0] / reps
+    m = cd.n_layers * cd.n_heads
+    elems = float(m) * cd.T * cd.d * len(ptrs)
+    flops = float(m) * (m + 16) * cd.T * cd.d * len(ptrs)       # the tile pairs I >= J
+    esz = 2 if cfg["dtype"] == "bf16" else 4
+    out = {"diagnostics": "appendix A, synthetic Mistral-shaped layer 15, T = 1024", "rows": rows,
+           "slice_gram": {"workload": args.workload, "cells": len(ptrs), "m": m, "ms": round(ms, 4),
+                          "GBps_cache_read": round(elems * esz / ms / 1e6, 1),
+                          "TFLOPs_fp32": round(flops / ms / 1e9, 2), "peak_fp32_TFLOPs": 157.3,
+                          "eig_ms": round((prof["tridiag_small"][0] + prof["eigvals"][0]) / reps, 4)}}
+    print(json.dumps(out))
+    codec.close()
+    J.jolt_destroy(ctx)
+
+
 def main():
     args = parse()
+    if args.diagnostics:
+        diagnostics(args)
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: there is no multi-GPU path (cells would shard "
               "across GPUs, with an all-gather of the spectra before the allocation).", file=sys.stderr)

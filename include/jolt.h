@@ -259,6 +259,32 @@ int jolt_eps2_workspace_size(int d, int n_samples, size_t *bytes);
 int jolt_eps2_calibrate(jolt_ctx *ctx, int group, int d, uint64_t seed, int n_samples,
                         double eps2_out[4], void *ws, size_t ws_bytes, jolt_stream stream);
 
+/* Three-mode spectral diagnostics (section 3 and appendix A).  The token- and
+ * feature-mode spectra of a cell are jolt_spectrum's (exact method: all T eigenvalues
+ * of X_(2) X_(2)^T, all d of F); the slice mode completes the three unfoldings.
+ *
+ * jolt_slice_spectrum: for each cell, all m = n_layers * n_heads eigenvalues, descending
+ * and clipped at 0, of the slice Gram S[s][s'] = sum_{t,f} X[s][t][f] X[s'][t][f] (the
+ * squared singular values of the slice unfolding; for one layer, the head mode).  The
+ * Gram is accumulated per token in fp32 and across tokens in fp64, reduced over token
+ * chunks in a fixed order, and diagonalised by the one-workgroup tridiagonalisation and
+ * fp64 bisection.  Cells, strides and X as for jolt_spectrum; m <= 768
+ * (JOLT_E_UNSUPPORTED otherwise).  lam_s: host, n_cells x m doubles.  ws: device,
+ * 256-byte aligned, at least jolt_slice_spectrum_workspace_size bytes, owned by the
+ * caller.  Synchronises the stream. */
+int jolt_slice_spectrum_workspace_size(const jolt_cell_desc *desc, int n_cells, size_t *bytes);
+int jolt_slice_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_cells, const void *const *X,
+                        void *ws, size_t ws_bytes, double *lam_s, jolt_stream stream);
+
+/* Appendix-A summary of one mode spectrum (host only): lam holds the n squared singular
+ * values of an n-row unfolding, descending, >= 0.  sigma_range = sqrt(lam[0] / lam[n-1])
+ * (+inf when lam[n-1] is 0); rank_a / rank_b = the smallest r in 0..n with
+ * sqrt(sum_{i >= r} lam[i] / sum_i lam[i]) <= err_a / err_b (the relative Frobenius error
+ * of keeping the top r; 0 when the spectrum is all zero).  JOLT_E_INVAL for n < 1, null
+ * pointers, a negative or increasing spectrum, or a threshold outside [0, 1]. */
+int jolt_mode_summary(const double *lam, int n, double err_a, double err_b, double *sigma_range,
+                      int32_t *rank_a, int32_t *rank_b);
+
 /* Test hook: copies an intermediate of the most recent jolt_compress on this
  * context for cell `cell` into dst (device memory, dst_bytes): 0 = U_T (T x r_T fp32),
  * 1 = U_d (d x r_d fp32), 2 = X~ (m x T x d fp32 from the stored factors),
@@ -289,6 +315,7 @@ enum {
   JOLT_STAGE_DECODE,           /* dequantisation, inverse rotation, add, cast */
   JOLT_STAGE_SKETCH,           /* FlashJoLT sketch products */
   JOLT_STAGE_ORTH,             /* FlashJoLT orthonormalisation */
+  JOLT_STAGE_SLICE_GRAM,       /* slice-mode Gram of the three-mode diagnostics */
   JOLT_STAGE_COUNT
 };
 int jolt_profile_enable(jolt_ctx *ctx, int on);

@@ -20,7 +20,8 @@ __all__ = ["JoltError", "lib", "CellDesc", "SpectrumOpts", "Params", "CellSpectr
            "JOLT_FACTOR_F16", "Rope", "jolt_last_error", "jolt_create", "jolt_destroy", "jolt_q_cap",
            "jolt_spectrum_len", "jolt_workspace_size", "jolt_decompress_workspace_size", "jolt_spectrum", "jolt_compressed_size",
            "jolt_compress", "jolt_decompress", "jolt_allocate", "jolt_eps2_workspace_size",
-           "jolt_eps2_calibrate", "jolt_debug_export", "jolt_profile_enable", "jolt_profile_reset",
+           "jolt_eps2_calibrate", "jolt_slice_spectrum_workspace_size", "jolt_slice_spectrum",
+           "jolt_mode_summary", "jolt_debug_export", "jolt_profile_enable", "jolt_profile_reset",
            "jolt_profile_read", "STAGES", "cell_desc", "LIB_PATH", "HEADER_PATH"]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -104,6 +105,9 @@ _SIGS = {
     "jolt_eps2_workspace_size": (C.c_int, [C.c_int, C.c_int, _P(_sz)]),
     "jolt_eps2_calibrate": (C.c_int, [_vp, C.c_int, C.c_int, C.c_uint64, C.c_int, _P(_dbl),
                                       _vp, _sz, _vp]),
+    "jolt_slice_spectrum_workspace_size": (C.c_int, [_P(CellDesc), C.c_int, _P(_sz)]),
+    "jolt_slice_spectrum": (C.c_int, [_vp, _P(CellDesc), C.c_int, _P(_vp), _vp, _sz, _P(_dbl), _vp]),
+    "jolt_mode_summary": (C.c_int, [_P(_dbl), C.c_int, _dbl, _dbl, _P(_dbl), _P(_i32), _P(_i32)]),
     "jolt_debug_export": (C.c_int, [_vp, C.c_int, C.c_int, _vp, _sz, _vp]),
     "jolt_profile_enable": (C.c_int, [_vp, C.c_int]),
     "jolt_profile_reset": (C.c_int, [_vp]),
@@ -292,7 +296,7 @@ def jolt_eps2_calibrate(ctx, group: int, d: int, seed: int, n_samples: int, ws,
 
 STAGES = ["feature_gram", "token_gram", "symv", "panel", "panel_gemm", "tridiag_small", "eigvals",
           "eigvecs", "backtransform", "project", "core", "serialize", "reconstruct", "residual",
-          "decode", "sketch", "orth"]
+          "decode", "sketch", "orth", "slice_gram"]
 
 
 def jolt_profile_enable(ctx, on: bool = True) -> None:
@@ -311,6 +315,32 @@ def jolt_profile_read(ctx) -> dict:
         _check(lib.jolt_profile_read(ctx, i, C.byref(ms), C.byref(n)))
         out[name] = (ms.value, n.value)
     return out
+
+
+def jolt_slice_spectrum_workspace_size(desc: CellDesc, n_cells: int) -> int:
+    n = _sz(0)
+    _check(lib.jolt_slice_spectrum_workspace_size(C.byref(desc), n_cells, C.byref(n)))
+    return n.value
+
+
+def jolt_slice_spectrum(ctx, desc: CellDesc, X, ws, ws_bytes=None, stream=None) -> np.ndarray:
+    """Slice-mode eigenvalues [n_cells, m] (descending) of each cell, as float64."""
+    n = len(X)
+    m = desc.n_layers * desc.n_heads
+    lam = np.zeros((n, m))
+    wsb = ws_bytes if ws_bytes is not None else (ws.numel() * ws.element_size())
+    _check(lib.jolt_slice_spectrum(ctx, C.byref(desc), n, _ptrs(X), _addr(ws), wsb,
+                                   lam.ctypes.data_as(_P(_dbl)), _stream(stream)))
+    return lam
+
+
+def jolt_mode_summary(lam, err_a: float = 0.10, err_b: float = 0.20):
+    """(sigma_1 / sigma_min, rank at err_a, rank at err_b) of one mode spectrum."""
+    lam = np.ascontiguousarray(lam, dtype=np.float64)
+    rng, ra, rb = _dbl(0), _i32(0), _i32(0)
+    _check(lib.jolt_mode_summary(lam.ctypes.data_as(_P(_dbl)), len(lam), err_a, err_b,
+                                 C.byref(rng), C.byref(ra), C.byref(rb)))
+    return rng.value, ra.value, rb.value
 
 
 def jolt_debug_export(ctx, what: int, cell: int, dst, stream=None) -> None:

@@ -1,5 +1,6 @@
 // Feature-mode Gram matrix F = sum_s X_s^T X_s (d x d) and energy E = ||X||_F^2
-// (section 4: the feature-mode spectrum is kept exact in both variants, section 5).
+// (section 4: the feature-mode spectrum is kept exact in both variants, section 5), and
+// the slice-mode Gram of the three-mode diagnostics (section 3, appendix A).
 //
 // The row set {(s, r)} of a cell is cut into `chunks_per_cell` contiguous runs;
 // one 256-thread workgroup reduces a run into a d x d fp32 partial (16 x 16 thread
@@ -103,7 +104,104 @@ __global__ void k_fgram_reduce(FGramArgs a, int D, float *F_out, double *E_out) 
   }
 }
 
+// Slice-mode Gram: thread (a, b) of the 16 x 16 grid owns entry (I*16 + a, J*16 + b) of the
+// tile pair (I >= J).  TOK tokens of the 32 slices' feature rows are staged in LDS as fp32
+// per step; each token's d-term dot product is summed in fp32 and added to an fp64
+// accumulator.
+template <int D, typename TX>
+__global__ void __launch_bounds__(256) k_slice_gram(SliceGramArgs a) {
+  constexpr int TOK = 2, LD = D + 4;
+  __shared__ __attribute__((aligned(16))) float xs[2][TOK][16][LD];
+  const int cell = blockIdx.z, chunk = blockIdx.y;
+  int I = 0, J = 0;
+  {
+    int t = blockIdx.x, i = (int)((sqrtf(8.f * (float)t + 1.f) - 1.f) * 0.5f);
+    while ((i + 1) * (i + 2) / 2 <= t) ++i;
+    while (i * (i + 1) / 2 > t) --i;
+    I = i; J = t - i * (i + 1) / 2;
+  }
+  const int tid = threadIdx.x, ta = tid / 16, tb = tid % 16;
+  const int t0 = (int)((int64_t)a.T * chunk / a.chunks), t1 = (int)((int64_t)a.T * (chunk + 1) / a.chunks);
+  const TX *base = reinterpret_cast<const TX *>(a.cells[cell].base);
+  double acc = 0.0;
+  constexpr int LPR = D / 8;                       // threads per feature row when loading
+  for (int tt = t0; tt < t1; tt += TOK) {
+    __syncthreads();
+    // 2 tiles x TOK tokens x 16 slices rows of D features, 8 features per thread and pass
+    for (int q = tid; q < 2 * TOK * 16 * LPR; q += 256) {
+      const int c8 = (q % LPR) * 8, row = q / LPR;
+      const int sl = row % 16, k = (row / 16) % TOK, which = row / (16 * TOK);
+      const int s = (which ? J : I) * 16 + sl, t = tt + k;
+      float v[8];
+      if (s < a.m && t < t1) {
+        const TX *p = base + (int64_t)(s / a.heads) * a.s_layer + (int64_t)(s % a.heads) * a.s_head +
+                      (int64_t)t * a.s_tok + c8;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          if constexpr (sizeof(TX) == 2) v[i] = bf16_to_f32(reinterpret_cast<const uint16_t *>(p)[i]);
+          else v[i] = reinterpret_cast<const float *>(p)[i];
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = 0.f;
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) xs[which][k][sl][c8 + i] = v[i];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < TOK; ++k) {
+      float sum = 0.f;
+#pragma unroll 8
+      for (int f = 0; f < D; f += 4) {
+        const float4 x = *reinterpret_cast<const float4 *>(&xs[0][k][ta][f]);
+        const float4 y = *reinterpret_cast<const float4 *>(&xs[1][k][tb][f]);
+        sum = fmaf(x.x, y.x, sum); sum = fmaf(x.y, y.y, sum);
+        sum = fmaf(x.z, y.z, sum); sum = fmaf(x.w, y.w, sum);
+      }
+      acc += (double)sum;
+    }
+  }
+  const int si = I * 16 + ta, sj = J * 16 + tb;
+  if (si < a.m && sj < a.m)
+    a.partial[(((int64_t)cell * a.chunks + chunk) * a.m + si) * a.m + sj] = acc;
+}
+
+// S[cell][i][j] = sum over chunks of the partial at (max(i, j), min(i, j)) (tile-pair
+// blocks cover rows in the higher tile; both orders are written inside a diagonal tile)
+__global__ void k_slice_gram_reduce(SliceGramArgs a, float *S_out) {
+  const int cell = blockIdx.y;
+  const int64_t mm = (int64_t)a.m * a.m;
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= mm) return;
+  const int i = (int)(q / a.m), j = (int)(q % a.m);
+  const int hi = (i / 16 > j / 16) || (i / 16 == j / 16) ? i : j, lo = hi == i ? j : i;
+  double s = 0.0;
+  const double *p = a.partial + (int64_t)cell * a.chunks * mm + (int64_t)hi * a.m + lo;
+  for (int c = 0; c < a.chunks; ++c) s += p[c * mm];
+  S_out[cell * mm + q] = (float)s;
+}
+
 }  // namespace
+
+hipError_t launch_slice_gram(const SliceGramArgs &a, int d, int dtype, hipStream_t st) {
+  dim3 grid(a.tiles * (a.tiles + 1) / 2, a.chunks, a.n_cells);
+#define L_(D_) \
+  if (d == D_) { \
+    if (dtype == 1) hipLaunchKernelGGL((k_slice_gram<D_, uint16_t>), grid, dim3(256), 0, st, a); \
+    else hipLaunchKernelGGL((k_slice_gram<D_, float>), grid, dim3(256), 0, st, a); \
+    return hipGetLastError(); }
+  L_(32) L_(64) L_(128)
+#undef L_
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_slice_gram_reduce(const SliceGramArgs &a, float *S_out, hipStream_t st) {
+  const int64_t mm = (int64_t)a.m * a.m;
+  dim3 grid((unsigned)((mm + 255) / 256), a.n_cells);
+  hipLaunchKernelGGL(k_slice_gram_reduce, grid, dim3(256), 0, st, a, S_out);
+  return hipGetLastError();
+}
 
 hipError_t launch_feature_gram(const FGramArgs &a, int d, int dtype, hipStream_t st) {
   dim3 grid(a.chunks_per_cell, a.n_cells);

@@ -159,6 +159,21 @@ hipError_t launch_feature_gram(const FGramArgs &a, int d, int dtype, hipStream_t
 hipError_t launch_feature_gram_reduce(const FGramArgs &a, int d, float *F_out, double *E_out,
                                       hipStream_t st);
 
+// ----------------------------------------------------------------- slice-mode Gram
+// S[cell][s][s'] = sum over tokens t and features f of X[s][t][f] X[s'][t][f] (the Gram of
+// the slice unfolding: appendix A's head mode).  Workgroup (pair of 16-slice tiles, token
+// chunk, cell) writes an fp64 partial for its tile pair; the reduce adds the chunks in a
+// fixed order and writes the full symmetric fp32 matrix.
+struct SliceGramArgs {
+  const FGramCell *cells;   // base per cell
+  int32_t n_cells, m, T, heads;
+  int64_t s_layer, s_head, s_tok;
+  int32_t tiles, chunks;    // ceil(m / 16) slice tiles; token chunks per cell
+  double *partial;          // [n_cells][chunks][m][m]
+};
+hipError_t launch_slice_gram(const SliceGramArgs &a, int d, int dtype, hipStream_t st);
+hipError_t launch_slice_gram_reduce(const SliceGramArgs &a, float *S_out, hipStream_t st);
+
 // ----------------------------------------------------------------- eigensolver
 struct EigBatch {
   float *A;              // [n_mat][n][n] row-major; lower triangle read, overwritten with

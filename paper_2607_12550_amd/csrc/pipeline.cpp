@@ -1038,6 +1038,85 @@ extern "C" int jolt_eps2_calibrate(jolt_ctx *ctx, int group, int d, uint64_t see
   return JOLT_OK;
 }
 
+// ------------------------------------------------------------------------ slice-mode spectrum
+namespace {
+constexpr int kSliceTileRows = 16;
+
+int slice_chunks(int T) { return std::max(1, std::min(256, (T + 63) / 64)); }
+
+// workspace: cell table, fp64 partials, the fp32 Gram and the eigensolver arrays
+void plan_slice(Carver &cv, int m, int T, int nc, FGramCell **cells, double **partial, EigWs &e) {
+  *cells = cv.take<FGramCell>(nc);
+  *partial = cv.take<double>((size_t)nc * slice_chunks(T) * m * m);
+  float *S = cv.take<float>((size_t)nc * m * m);
+  carve_eig(cv, e, nc, m, 0, S);
+}
+}  // namespace
+
+extern "C" int jolt_slice_spectrum_workspace_size(const jolt_cell_desc *desc, int n_cells, size_t *bytes) {
+  if (!bytes || n_cells < 1) return jolt_fail(JOLT_E_INVAL, "jolt_slice_spectrum_workspace_size: bad argument");
+  int rc = validate_desc(desc);
+  if (rc) return rc;
+  const int m = desc->n_layers * desc->n_heads;
+  if (m > SYTRD_SMALL_MAX) return jolt_fail(JOLT_E_UNSUPPORTED, "slice spectrum limited to m <= %d", SYTRD_SMALL_MAX);
+  Carver cv(nullptr);
+  FGramCell *fc;
+  double *part;
+  EigWs e;
+  plan_slice(cv, m, desc->T, n_cells, &fc, &part, e);
+  *bytes = cv.off + 256;
+  return JOLT_OK;
+}
+
+extern "C" int jolt_slice_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_cells, const void *const *X,
+                                   void *ws, size_t ws_bytes, double *lam_s, jolt_stream stream) {
+  size_t need = 0;
+  int rc = jolt_slice_spectrum_workspace_size(desc, n_cells, &need);
+  if (rc) return rc;
+  rc = check_common(ctx, desc, n_cells, X, ws);
+  if (rc) return rc;
+  if (!lam_s) return jolt_fail(JOLT_E_INVAL, "lam_s is null");
+  if (ws_bytes < need) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  HIP_OK(hipSetDevice(ctx->device));
+  forget_spectra(ctx, ws, ws_bytes);
+  hipStream_t st = (hipStream_t)stream;
+  const int m = desc->n_layers * desc->n_heads;
+  Carver cv(ws);
+  FGramCell *fc;
+  double *part;
+  EigWs e;
+  plan_slice(cv, m, desc->T, n_cells, &fc, &part, e);
+  std::vector<FGramCell> cells(n_cells);
+  for (int c = 0; c < n_cells; ++c) cells[c] = FGramCell{X[c], desc->T, 0};
+  HIP_OK(hipMemcpyAsync(fc, cells.data(), n_cells * sizeof(FGramCell), hipMemcpyHostToDevice, st));
+  SliceGramArgs a{};
+  a.cells = fc;
+  a.n_cells = n_cells; a.m = m; a.T = desc->T; a.heads = desc->n_heads;
+  a.s_layer = desc->stride_layer; a.s_head = desc->stride_head; a.s_tok = desc->stride_token;
+  a.tiles = (m + kSliceTileRows - 1) / kSliceTileRows;
+  a.chunks = slice_chunks(desc->T);
+  a.partial = part;
+  {
+    StageTimer t(ctx, st, JOLT_STAGE_SLICE_GRAM);
+    HIP_OK(launch_slice_gram(a, desc->d, desc->dtype, st));
+    HIP_OK(launch_slice_gram_reduce(a, e.b.A, st));
+  }
+  {
+    StageTimer t(ctx, st, JOLT_STAGE_TRIDIAG_SMALL);
+    HIP_OK(launch_sytrd_small(e.b, st));
+  }
+  {
+    StageTimer t(ctx, st, JOLT_STAGE_EIGVALS);
+    HIP_OK(launch_tridiag_eigvals(e.b, st));
+  }
+  std::vector<double> lam((size_t)n_cells * m);
+  HIP_OK(hipMemcpyAsync(lam.data(), e.b.lam, lam.size() * sizeof(double), hipMemcpyDeviceToHost, st));
+  HIP_OK(hipStreamSynchronize(st));
+  // eigenvalues are clipped at 0 (the Gram is positive semi-definite)
+  for (size_t i = 0; i < lam.size(); ++i) lam_s[i] = std::max(0.0, lam[i]);
+  return JOLT_OK;
+}
+
 // ------------------------------------------------------------------------ debug export
 extern "C" int jolt_debug_export(jolt_ctx *ctx, int what, int cell, void *dst, size_t dst_bytes,
                                  jolt_stream stream) {

@@ -177,3 +177,39 @@ def test_decode_workspace_fits_inside_the_compress_workspace():
         assert J.jolt_decompress_workspace_size(desc, 2, 0) < 1 << 20   # residual-only blobs
     with pytest.raises(J.JoltError):
         J.jolt_decompress_workspace_size(desc, 0, 8)
+
+
+# ----------------------------------------------------------------- three-mode diagnostics
+def test_mode_summary_matches_oracle(rng):
+    from oracle import diagnostics as dg
+    spectra = [np.full(8, 2.0), np.array([0.5, 0.3, 0.15, 0.05]), np.array([3.0, 0.0, 0.0]),
+               np.sort(rng.exponential(1.0, 128))[::-1],
+               np.sort(rng.exponential(1.0, 1024) ** 4)[::-1], np.zeros(5)]
+    for lam in spectra:
+        for ea, eb in ((0.1, 0.2), (0.0, 1.0), (0.05, 0.5)):
+            rng_, ra, rb = J.jolt_mode_summary(lam, ea, eb)
+            want = dg.mode_summary(lam, errs=(ea, eb))
+            assert [ra, rb] == want["ranks"], (lam[:4], ea, eb)
+            if np.isinf(want["sigma_range"]):
+                assert np.isinf(rng_)
+            else:
+                assert rng_ == pytest.approx(want["sigma_range"], rel=1e-14)
+
+
+def test_mode_summary_and_slice_spectrum_validation():
+    for lam, ea in ((np.array([1.0, 2.0]), 0.1), (np.array([1.0, -1.0]), 0.1),
+                    (np.array([1.0, 0.5]), 1.5), (np.array([np.nan]), 0.1)):
+        with pytest.raises(J.JoltError) as e:
+            J.jolt_mode_summary(lam, ea, 0.2)
+        assert e.value.code == -1
+    big = J.cell_desc(dtype=J.JOLT_BF16, n_layers=20, n_heads=40, T=64, d=128,
+                      stride_layer=40 * 64 * 128, stride_head=64 * 128, stride_token=128)
+    with pytest.raises(J.JoltError) as e:
+        J.jolt_slice_spectrum_workspace_size(big, 1)       # m = 800 > 768
+    assert e.value.code == -2
+    ok = J.cell_desc(dtype=J.JOLT_BF16, n_layers=1, n_heads=8, T=1024, d=128,
+                     stride_layer=8 * 1024 * 128, stride_head=1024 * 128, stride_token=128)
+    assert J.jolt_slice_spectrum_workspace_size(ok, 2) > 2 * 8 * 8 * 8
+    rc = J.lib.jolt_slice_spectrum(None, C.byref(ok), 1, (C.c_void_p * 1)(0), None, 0,
+                                   np.zeros(8).ctypes.data_as(C.POINTER(C.c_double)), None)
+    assert rc == -1
