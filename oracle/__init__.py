@@ -26,9 +26,11 @@ Module map (paper passages in brackets):
   keys (appendix B: keys are compressed before RoPE).
 * :mod:`oracle.diagnostics` - singular values of the three mode unfoldings and
   their appendix-A summary (section 3, appendix A).
+* :mod:`oracle.attention` - decode-time softmax attention over the decompressed
+  cache (the result a fused attention-on-factors kernel must reproduce; section 8).
 
 Parity-unpinned items (no value in the paper can be reproduced on synthetic
 data): the absolute reconstruction errors, the epsilon^2(b) values, the chosen
 ranks and the speedups.
 """
-from . import rounding, philox, residual, tucker, alloc, pipeline, rope, diagnostics  # noqa: F401,E402
+from . import rounding, philox, residual, tucker, alloc, pipeline, rope, diagnostics, attention  # noqa: F401,E402
