@@ -67,6 +67,11 @@ def parse():
     ap.add_argument("--no-stage-profile", action="store_true",
                     help="skip the event-instrumented pass (for hardware-counter runs); the "
                          "stage and roofline fields are then omitted")
+    ap.add_argument("--attend", action="store_true",
+                    help="instead of the benchmark step: decode-time attention of one new token "
+                         "(4 query heads per key-value head for GQA caches, 1 for MHA) over every "
+                         "layer of the compressed --workload cache, on the factors vs the "
+                         "materialising path (decompress, then attention)")
     ap.add_argument("--diagnostics", action="store_true",
                     help="instead of the benchmark step: the appendix-A three-mode table of one "
                          "synthetic Mistral-shaped layer (layer 15, T = 1024, K and V), and the "
@@ -269,8 +274,116 @@ def diagnostics(args):
     J.jolt_destroy(ctx)
 
 
+def attend_bench(args):
+    """Decode-time attention on the compressed cache.  The cache is compressed once (the
+    workload's method and budget); then one query token per sequence attends over every
+    layer: with the fused kernels reading only the blobs, and, for reference, with the
+    materialising path (jolt_decompress of every cell to bf16, then fp32 attention in torch).
+    Algorithmic bytes of the fused path: per item (layer) the key and value token factors
+    U_T (T r_T c), the codes of the layer's H slices (H T d b / 8) and their scales
+    (2 H T d / g); the core and feature factors are negligible."""
+    import numpy as np
+    import torch
+
+    import kvsynth
+    import paper_2607_12550_amd as J
+    from paper_2607_12550_amd.cache import CacheCodec
+
+    cfg = dict(kvsynth.CONFIGS[args.workload])
+    gl = cfg.pop("group_layers")
+    method, ratio = WORKLOAD_RUN.get(args.workload, ("exact", 2.0))
+    method, ratio = args.method or method, args.ratio or ratio
+    cfg["workers"] = 8
+    log("generating", args.workload)
+    Knp, Vnp = kvsynth.make_cache(**cfg)
+    dev = torch.device("cuda", 0)
+    to_dev = (lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)) \
+        if cfg["dtype"] == "bf16" else (lambda a: torch.from_numpy(a).to(dev))
+    K, V = to_dev(Knp), to_dev(Vnp)
+    del Knp, Vnp
+    codec = CacheCodec(K, V, group_layers=gl, method=method, ratio=ratio)
+    codec.calibrate()
+    codec.spectrum()
+    codec.allocate()
+    codec.compress()
+    hdr = codec.headers()
+    L, B, H, T, d = codec.shape
+    rep = 4 if H == 8 else 1
+    n_q = rep * H
+    # items: every (group, batch item, layer of the group)
+    pair = {}
+    for i, c in enumerate(codec.cells):
+        pair.setdefault((c.group, c.batch), [None, None])[c.tensor] = i
+    items = [(pair[(g, b)][0], pair[(g, b)][1], li, g * gl + li, b)
+             for (g, b) in sorted(pair) for li in range(gl)]
+    kb = [codec.blob_ptrs[k] for k, _, _, _, _ in items]
+    vb = [codec.blob_ptrs[v] for _, v, _, _, _ in items]
+    ks = [codec.blob_sizes[k] for k, _, _, _, _ in items]
+    vs = [codec.blob_sizes[v] for _, v, _, _, _ in items]
+    kh = np.stack([hdr[k] for k, _, _, _, _ in items])
+    vh = np.stack([hdr[v] for _, v, _, _, _ in items])
+    layers = [li for _, _, li, _, _ in items]
+    params = codec.params
+    rk = max(params[k].r_T for k, _, _, _, _ in items)
+    rv = max(params[v].r_T for _, v, _, _, _ in items)
+    n = len(items)
+    ws = torch.empty(J.jolt_attend_workspace_size(n, n_q, T, d, rk, rv), dtype=torch.uint8, device=dev)
+    g = torch.Generator(device="cpu").manual_seed(0)
+    Q = torch.randn((n, n_q, d), generator=g).to(dev)
+    O = torch.empty_like(Q)
+    scale = 1.0 / float(np.sqrt(d))
+    call = lambda: J.jolt_attend(codec.ctx, kb, vb, kh, vh, layers, Q, O, scale, ws, k_bytes=ks, v_bytes=vs)
+    call()
+    torch.cuda.synchronize()
+    reps = 20
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    fused_ms = e0.elapsed_time(e1) / reps
+    # materialising path: decompress every cell to bf16, then attention of the same queries
+    Kout, Vout = torch.empty_like(K), torch.empty_like(V)
+
+    def materialise():
+        codec.decompress(Kout, Vout)
+        Kl = torch.stack([Kout[l, b] for _, _, _, l, b in items]).float()        # [n, H, T, d]
+        Vl = torch.stack([Vout[l, b] for _, _, _, l, b in items]).float()
+        q = Q.view(n, H, rep, d)
+        p_ = torch.softmax(scale * torch.matmul(q, Kl.transpose(-1, -2).contiguous()), dim=-1)
+        return torch.matmul(p_, Vl).view(n, n_q, d)
+
+    ref = materialise()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        materialise()
+    e1.record()
+    torch.cuda.synchronize()
+    mat_ms = e0.elapsed_time(e1) / reps
+    rel = float(torch.linalg.norm(O - ref) / torch.linalg.norm(ref))
+    c = 2 if params[0].factor_dtype == J.JOLT_FACTOR_F16 else 4
+    nbytes = 0
+    for k, v, _, _, _ in items:
+        for p_ in (params[k], params[v]):
+            nbytes += T * p_.r_T * c + H * T * d * p_.bits // 8 + (2 * H * T * d // p_.group if p_.bits else 0)
+    cache_layer_bytes = n * 2 * H * T * d * (2 if cfg["dtype"] == "bf16" else 4)
+    out = {"attend": {"workload": args.workload, "method": method, "ratio": ratio, "items": n, "n_q": n_q,
+                      "kv_heads": H, "T": T, "d": d, "fused_ms": round(fused_ms, 4),
+                      "materialise_ms": round(mat_ms, 4), "speedup": round(mat_ms / fused_ms, 2),
+                      "bytes_read": nbytes, "uncompressed_kv_bytes": cache_layer_bytes,
+                      "GBps": round(nbytes / fused_ms / 1e6, 1), "frac_hbm": round(nbytes / fused_ms / 1e6 / HBM_GBS, 4),
+                      "rel_diff_vs_materialising": rel}}
+    print(json.dumps(out))
+    codec.close()
+
+
 def main():
     args = parse()
+    if args.attend:
+        attend_bench(args)
+        return
     if args.diagnostics:
         diagnostics(args)
         return

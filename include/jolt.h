@@ -285,6 +285,34 @@ int jolt_slice_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_cells, 
 int jolt_mode_summary(const double *lam, int n, double err_a, double err_b, double *sigma_range,
                       int32_t *rank_a, int32_t *rank_b);
 
+/* Decode-time attention evaluated on the compressed factors (section 8 and the
+ * conclusion: attention run directly on the factors, without materialising the cache).
+ * Item i pairs a key blob and a value blob of the same cell shape (as written by
+ * jolt_compress, any ranks and bits) with a layer index layers[i] of that cell's group and
+ * n_q query heads; with H key-value heads per layer (n_q a multiple of H), query head j
+ * reads slice s = layers[i] * H + j / (n_q / H).  The result is
+ *   O[i][j] = sum_t softmax_t(scale * Q[i][j] . K^[s][t]) V^[s][t],
+ * with K^ and V^ the cells jolt_decompress would return in fp32, computed without forming
+ * them: the key scores are U_T (2^e G_s U_d^T q) plus the dequantised codes dotted with
+ * the query rotated once (H (signs . q) / sqrt(d)), and the value side sums U_T rows and
+ * dequantised codes under the softmax weights before the value factors and the inverse
+ * rotation are applied once per head.  fp32 arithmetic; chunks of 64 tokens are merged
+ * with the max / rescale rule in a fixed order (deterministic).  Keys are used as stored
+ * (no position rotation is applied).
+ * k_hdr_host / v_hdr_host: host copies of the n_items 128-byte blob headers (validated
+ * before any device work); blobs, Q ([n_items][n_q][d] fp32) and O (same shape) are device
+ * memory owned by the caller; all items share m, T, d, H and the quantiser group; ranks at
+ * most 1024, n_q at most 64 and at most 8 query heads per key-value head
+ * (JOLT_E_UNSUPPORTED).  ws: device, 256-byte aligned, at least
+ * jolt_attend_workspace_size bytes (max_rT_k / max_rT_v: largest key / value r_T of the
+ * call).  Asynchronous on the stream. */
+int jolt_attend_workspace_size(int n_items, int n_q, int T, int d, int max_rT_k, int max_rT_v,
+                               size_t *bytes);
+int jolt_attend(jolt_ctx *ctx, int n_items, const void *const *k_blobs, const size_t *k_bytes,
+                const void *const *v_blobs, const size_t *v_bytes, const void *k_hdr_host,
+                const void *v_hdr_host, const int32_t *layers, int n_q, const float *Q, float scale,
+                float *O, void *ws, size_t ws_bytes, jolt_stream stream);
+
 /* Test hook: copies an intermediate of the most recent jolt_compress on this
  * context for cell `cell` into dst (device memory, dst_bytes): 0 = U_T (T x r_T fp32),
  * 1 = U_d (d x r_d fp32), 2 = X~ (m x T x d fp32 from the stored factors),
@@ -316,6 +344,7 @@ enum {
   JOLT_STAGE_SKETCH,           /* FlashJoLT sketch products */
   JOLT_STAGE_ORTH,             /* FlashJoLT orthonormalisation */
   JOLT_STAGE_SLICE_GRAM,       /* slice-mode Gram of the three-mode diagnostics */
+  JOLT_STAGE_ATTEND,           /* decode attention on the factors */
   JOLT_STAGE_COUNT
 };
 int jolt_profile_enable(jolt_ctx *ctx, int on);

@@ -21,7 +21,7 @@ __all__ = ["JoltError", "lib", "CellDesc", "SpectrumOpts", "Params", "CellSpectr
            "jolt_spectrum_len", "jolt_workspace_size", "jolt_decompress_workspace_size", "jolt_spectrum", "jolt_compressed_size",
            "jolt_compress", "jolt_decompress", "jolt_allocate", "jolt_eps2_workspace_size",
            "jolt_eps2_calibrate", "jolt_slice_spectrum_workspace_size", "jolt_slice_spectrum",
-           "jolt_mode_summary", "jolt_debug_export", "jolt_profile_enable", "jolt_profile_reset",
+           "jolt_mode_summary", "jolt_attend_workspace_size", "jolt_attend", "jolt_debug_export", "jolt_profile_enable", "jolt_profile_reset",
            "jolt_profile_read", "STAGES", "cell_desc", "LIB_PATH", "HEADER_PATH"]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -108,6 +108,9 @@ _SIGS = {
     "jolt_slice_spectrum_workspace_size": (C.c_int, [_P(CellDesc), C.c_int, _P(_sz)]),
     "jolt_slice_spectrum": (C.c_int, [_vp, _P(CellDesc), C.c_int, _P(_vp), _vp, _sz, _P(_dbl), _vp]),
     "jolt_mode_summary": (C.c_int, [_P(_dbl), C.c_int, _dbl, _dbl, _P(_dbl), _P(_i32), _P(_i32)]),
+    "jolt_attend_workspace_size": (C.c_int, [C.c_int, C.c_int, C.c_int, C.c_int, C.c_int, C.c_int, _P(_sz)]),
+    "jolt_attend": (C.c_int, [_vp, C.c_int, _P(_vp), _P(_sz), _P(_vp), _P(_sz), _vp, _vp, _P(_i32),
+                              C.c_int, _vp, C.c_float, _vp, _vp, _sz, _vp]),
     "jolt_debug_export": (C.c_int, [_vp, C.c_int, C.c_int, _vp, _sz, _vp]),
     "jolt_profile_enable": (C.c_int, [_vp, C.c_int]),
     "jolt_profile_reset": (C.c_int, [_vp]),
@@ -296,7 +299,7 @@ def jolt_eps2_calibrate(ctx, group: int, d: int, seed: int, n_samples: int, ws,
 
 STAGES = ["feature_gram", "token_gram", "symv", "panel", "panel_gemm", "tridiag_small", "eigvals",
           "eigvecs", "backtransform", "project", "core", "serialize", "reconstruct", "residual",
-          "decode", "sketch", "orth", "slice_gram"]
+          "decode", "sketch", "orth", "slice_gram", "attend"]
 
 
 def jolt_profile_enable(ctx, on: bool = True) -> None:
@@ -341,6 +344,29 @@ def jolt_mode_summary(lam, err_a: float = 0.10, err_b: float = 0.20):
     _check(lib.jolt_mode_summary(lam.ctypes.data_as(_P(_dbl)), len(lam), err_a, err_b,
                                  C.byref(rng), C.byref(ra), C.byref(rb)))
     return rng.value, ra.value, rb.value
+
+
+def jolt_attend_workspace_size(n_items: int, n_q: int, T: int, d: int, max_rT_k: int, max_rT_v: int) -> int:
+    n = _sz(0)
+    _check(lib.jolt_attend_workspace_size(n_items, n_q, T, d, max_rT_k, max_rT_v, C.byref(n)))
+    return n.value
+
+
+def jolt_attend(ctx, k_blobs, v_blobs, k_hdr, v_hdr, layers, Q, O, scale: float, ws, ws_bytes=None,
+                stream=None, k_bytes=None, v_bytes=None) -> None:
+    """Attention of Q [n_items, n_q, d] (device fp32) over the compressed cells; writes O.
+
+    k_hdr / v_hdr: host uint8 arrays [n_items, 128] of the blob headers."""
+    n = len(k_blobs)
+    kb = k_bytes if k_bytes is not None else [b.numel() for b in k_blobs]
+    vb = v_bytes if v_bytes is not None else [b.numel() for b in v_blobs]
+    kh = np.ascontiguousarray(k_hdr, dtype=np.uint8)
+    vh = np.ascontiguousarray(v_hdr, dtype=np.uint8)
+    lay = (_i32 * n)(*layers)
+    wsb = ws_bytes if ws_bytes is not None else (ws.numel() * ws.element_size())
+    _check(lib.jolt_attend(ctx, n, _ptrs(k_blobs), (_sz * n)(*kb), _ptrs(v_blobs), (_sz * n)(*vb),
+                           kh.ctypes.data, vh.ctypes.data, lay, Q.shape[1], _addr(Q), float(scale),
+                           _addr(O), _addr(ws), wsb, _stream(stream)))
 
 
 def jolt_debug_export(ctx, what: int, cell: int, dst, stream=None) -> None:

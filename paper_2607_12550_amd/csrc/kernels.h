@@ -174,6 +174,38 @@ struct SliceGramArgs {
 hipError_t launch_slice_gram(const SliceGramArgs &a, int d, int dtype, hipStream_t st);
 hipError_t launch_slice_gram_reduce(const SliceGramArgs &a, float *S_out, hipStream_t st);
 
+// ----------------------------------------------------------------- attention on the factors
+// One item = a layer of a compressed key cell and of the matching value cell, and n_q
+// query heads; key-value head h of the layer is slice s = layer * heads + h, query head j
+// reads head j / (n_q / heads).
+struct AttnBlob {
+  const void *UT, *Ud, *G;     // fp16 (f16 = 1) or fp32 factors: T x rT, d x rd, m x rT x rd
+  const int8_t *gexp;          // per-slice core exponents
+  const uint8_t *codes;        // packed residual codes (s, t, f) order, LSB first
+  const uint16_t *scales;      // fp16 group scales
+  int32_t rT, rd, bits, f16;
+};
+struct AttnItem {
+  AttnBlob k, v;
+  int32_t layer, pad;
+};
+struct AttnArgs {
+  const AttnItem *items;
+  const float *signs;          // [n_items][2][d]: key, value rotation signs
+  const float *Q;              // [n_items][n_q][d]
+  float *O;                    // [n_items][n_q][d]
+  float *gk;                   // [n_items][n_q][rk_max]: 2^e G_s U_d^T q (key side)
+  float *qr;                   // [n_items][n_q][d]: H (signs . q) / sqrt(d)
+  float *part;                 // [n_items][chunks][n_q][2 + rv_max + d] chunk partials
+  int32_t n_items, n_q, heads, T, group, chunks, rk_max, rv_max;
+  float scale, inv_sqrt_d;
+};
+constexpr int ATTN_CHUNK = 64;      // tokens per workgroup of the chunk pass
+constexpr int ATTN_QMAX = 64;       // query heads per item
+constexpr int ATTN_REP_MAX = 8;     // query heads per key-value head
+constexpr int ATTN_RT_MAX = 1024;   // largest value rank the combine kernel stages in LDS
+hipError_t launch_attend(const AttnArgs &a, int d, hipStream_t st);
+
 // ----------------------------------------------------------------- eigensolver
 struct EigBatch {
   float *A;              // [n_mat][n][n] row-major; lower triangle read, overwritten with

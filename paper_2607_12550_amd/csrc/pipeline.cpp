@@ -1117,6 +1117,102 @@ extern "C" int jolt_slice_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, in
   return JOLT_OK;
 }
 
+// ------------------------------------------------------------------------ attention on the factors
+namespace {
+void plan_attend(Carver &cv, int n, int n_q, int T, int d, int rk, int rv, AttnItem **items, uint64_t **seeds,
+                 float **signs, float **gk, float **qr, float **part) {
+  const int chunks = (T + ATTN_CHUNK - 1) / ATTN_CHUNK;
+  *items = cv.take<AttnItem>(n);
+  *seeds = cv.take<uint64_t>(2 * (size_t)n);
+  *signs = cv.take<float>(2 * (size_t)n * d);
+  *gk = cv.take<float>((size_t)n * n_q * std::max(rk, 1));
+  *qr = cv.take<float>((size_t)n * n_q * d);
+  *part = cv.take<float>((size_t)n * chunks * n_q * (2 + rv + d));
+}
+}  // namespace
+
+extern "C" int jolt_attend_workspace_size(int n_items, int n_q, int T, int d, int max_rT_k, int max_rT_v,
+                                          size_t *bytes) {
+  if (!bytes || n_items < 1 || n_q < 1 || T < 1 || (d != 32 && d != 64 && d != 128) || max_rT_k < 0 ||
+      max_rT_v < 0 || max_rT_k > ATTN_RT_MAX || max_rT_v > ATTN_RT_MAX)
+    return jolt_fail(JOLT_E_INVAL, "jolt_attend_workspace_size: bad argument (ranks <= %d)", ATTN_RT_MAX);
+  Carver cv(nullptr);
+  AttnItem *it; uint64_t *sd; float *sg, *gk, *qr, *part;
+  plan_attend(cv, n_items, n_q, T, d, max_rT_k, max_rT_v, &it, &sd, &sg, &gk, &qr, &part);
+  *bytes = cv.off + 256;
+  return JOLT_OK;
+}
+
+extern "C" int jolt_attend(jolt_ctx *ctx, int n_items, const void *const *k_blobs, const size_t *k_bytes,
+                           const void *const *v_blobs, const size_t *v_bytes, const void *k_hdr_host,
+                           const void *v_hdr_host, const int32_t *layers, int n_q, const float *Q,
+                           float scale, float *O, void *ws, size_t ws_bytes, jolt_stream stream) {
+  if (!ctx || n_items < 1 || !k_blobs || !k_bytes || !v_blobs || !v_bytes || !k_hdr_host || !v_hdr_host ||
+      !layers || n_q < 1 || !Q || !O || !ws)
+    return jolt_fail(JOLT_E_INVAL, "jolt_attend: null argument or empty call");
+  if (reinterpret_cast<uintptr_t>(ws) & 255) return jolt_fail(JOLT_E_INVAL, "workspace must be 256-byte aligned");
+  if (!(scale > 0.f) || !std::isfinite(scale)) return jolt_fail(JOLT_E_INVAL, "jolt_attend: scale must be > 0");
+  const uint8_t *kh = static_cast<const uint8_t *>(k_hdr_host), *vh = static_cast<const uint8_t *>(v_hdr_host);
+  std::vector<BlobInfo> kb(n_items), vb(n_items);
+  int rk = 0, rv = 0;
+  for (int i = 0; i < n_items; ++i) {
+    int rc = parse_header(kh + (size_t)i * kHeaderBytes, k_bytes[i], &kb[i]);
+    if (rc) return rc;
+    rc = parse_header(vh + (size_t)i * kHeaderBytes, v_bytes[i], &vb[i]);
+    if (rc) return rc;
+    const BlobInfo &a = kb[i], &b = vb[i], &z = kb[0];
+    if (a.m != b.m || a.T != b.T || a.d != b.d || a.heads != b.heads || a.group != b.group)
+      return jolt_fail(JOLT_E_BLOB, "item %d: key and value blobs differ in shape or group", i);
+    if (a.T != z.T || a.d != z.d || a.heads != z.heads || a.group != z.group || a.m != z.m)
+      return jolt_fail(JOLT_E_BLOB, "item %d: all items of a call must share m, T, d, heads and group", i);
+    if (!k_blobs[i] || !v_blobs[i]) return jolt_fail(JOLT_E_INVAL, "item %d: null blob", i);
+    if (layers[i] < 0 || (int64_t)layers[i] * a.heads >= a.m)
+      return jolt_fail(JOLT_E_INVAL, "item %d: layer %d outside the cell's %u layers", i, layers[i], a.m / a.heads);
+    if ((int)a.rT > ATTN_RT_MAX || (int)b.rT > ATTN_RT_MAX)
+      return jolt_fail(JOLT_E_UNSUPPORTED, "jolt_attend: ranks above %d", ATTN_RT_MAX);
+    rk = std::max(rk, (int)a.rT);
+    rv = std::max(rv, (int)b.rT);
+  }
+  const int T = kb[0].T, d = kb[0].d, H = kb[0].heads;
+  if (n_q % H) return jolt_fail(JOLT_E_INVAL, "jolt_attend: n_q = %d is not a multiple of the %d key-value heads", n_q, H);
+  if (n_q > ATTN_QMAX || n_q / H > ATTN_REP_MAX)
+    return jolt_fail(JOLT_E_UNSUPPORTED, "jolt_attend: at most %d query heads, %d per key-value head", ATTN_QMAX, ATTN_REP_MAX);
+  size_t need = 0;
+  int rc = jolt_attend_workspace_size(n_items, n_q, T, d, rk, rv, &need);
+  if (rc) return rc;
+  if (ws_bytes < need) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  HIP_OK(hipSetDevice(ctx->device));
+  forget_spectra(ctx, ws, ws_bytes);
+  hipStream_t st = (hipStream_t)stream;
+  Carver cv(ws);
+  AttnItem *items; uint64_t *seeds; float *signs, *gk, *qr, *part;
+  plan_attend(cv, n_items, n_q, T, d, rk, rv, &items, &seeds, &signs, &gk, &qr, &part);
+  std::vector<AttnItem> hi(n_items);
+  std::vector<uint64_t> hs(2 * (size_t)n_items);
+  auto blob = [](const void *base, const BlobInfo &b) {
+    const uint8_t *p8 = static_cast<const uint8_t *>(base);
+    return AttnBlob{p8 + b.L.UT, p8 + b.L.Ud, p8 + b.L.G, reinterpret_cast<const int8_t *>(p8 + b.L.gexp),
+                    p8 + b.L.codes, reinterpret_cast<const uint16_t *>(p8 + b.L.scales),
+                    (int32_t)b.rT, (int32_t)b.rd, (int32_t)b.bits, (int32_t)b.f16};
+  };
+  for (int i = 0; i < n_items; ++i) {
+    hi[i] = AttnItem{blob(k_blobs[i], kb[i]), blob(v_blobs[i], vb[i]), layers[i], 0};
+    hs[2 * i] = kb[i].seed;
+    hs[2 * i + 1] = vb[i].seed;
+  }
+  HIP_OK(hipMemcpyAsync(items, hi.data(), hi.size() * sizeof(AttnItem), hipMemcpyHostToDevice, st));
+  HIP_OK(hipMemcpyAsync(seeds, hs.data(), hs.size() * sizeof(uint64_t), hipMemcpyHostToDevice, st));
+  HIP_OK(launch_rotation_signs(seeds, 2 * n_items, d, signs, st));
+  AttnArgs a{};
+  a.items = items; a.signs = signs; a.Q = Q; a.O = O; a.gk = gk; a.qr = qr; a.part = part;
+  a.n_items = n_items; a.n_q = n_q; a.heads = H; a.T = T; a.group = kb[0].group;
+  a.chunks = (T + ATTN_CHUNK - 1) / ATTN_CHUNK; a.rk_max = std::max(rk, 1); a.rv_max = rv;
+  a.scale = scale; a.inv_sqrt_d = (float)(1.0 / std::sqrt((double)d));
+  StageTimer t(ctx, st, JOLT_STAGE_ATTEND);
+  HIP_OK(launch_attend(a, d, st));
+  return JOLT_OK;
+}
+
 // ------------------------------------------------------------------------ debug export
 extern "C" int jolt_debug_export(jolt_ctx *ctx, int what, int cell, void *dst, size_t dst_bytes,
                                  jolt_stream stream) {
