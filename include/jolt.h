@@ -302,7 +302,7 @@ int jolt_mode_summary(const double *lam, int n, double err_a, double err_b, doub
  * k_hdr_host / v_hdr_host: host copies of the n_items 128-byte blob headers (validated
  * before any device work); blobs, Q ([n_items][n_q][d] fp32) and O (same shape) are device
  * memory owned by the caller; all items share m, T, d, H and the quantiser group; ranks at
- * most 1024, n_q at most 64 and at most 8 query heads per key-value head
+ * most 1024, n_q at most 64, at most 8 query heads per key-value head and T at most 524288
  * (JOLT_E_UNSUPPORTED).  ws: device, 256-byte aligned, at least
  * jolt_attend_workspace_size bytes (max_rT_k / max_rT_v: largest key / value r_T of the
  * call).  Asynchronous on the stream. */

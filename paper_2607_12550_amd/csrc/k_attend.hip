@@ -287,22 +287,23 @@ __global__ void __launch_bounds__(128) k_attend_combine(AttnArgs a) {
   const float *part = a.part + ((int64_t)item * a.chunks * a.n_q + j) * stride;
   const int64_t cstride = (int64_t)a.n_q * stride;
   __shared__ float av[ATTN_RT_MAX], w[D], bv[D];
-  __shared__ float M_s, L_s;
+  __shared__ float L_s;
+  extern __shared__ float cw[];                 // per-chunk weights exp(max_c - M)
   if (tid == 0) {
     float M = -INFINITY;
     for (int c = 0; c < a.chunks; ++c) M = fmaxf(M, part[c * cstride]);
     float L = 0.f;
-    for (int c = 0; c < a.chunks; ++c) L += part[c * cstride + 1] * expf(part[c * cstride] - M);
-    M_s = M; L_s = L;
+    for (int c = 0; c < a.chunks; ++c) {
+      cw[c] = expf(part[c * cstride] - M);
+      L += part[c * cstride + 1] * cw[c];
+    }
+    L_s = L;
   }
   __syncthreads();
-  const float M = M_s;
   for (int i = tid; i < vb.rT + D; i += 128) {
     float acc = 0.f;
-    for (int c = 0; c < a.chunks; ++c) {
-      const float wgt = expf(part[c * cstride] - M);
-      acc = fmaf(wgt, part[c * cstride + 2 + (i < vb.rT ? i : a.rv_max + (i - vb.rT))], acc);
-    }
+    const float *pc = part + 2 + (i < vb.rT ? i : a.rv_max + (i - vb.rT));
+    for (int c = 0; c < a.chunks; ++c) acc = fmaf(cw[c], pc[c * cstride], acc);
     if (i < vb.rT) av[i] = acc;
     else bv[i - vb.rT] = acc;
   }
@@ -338,7 +339,7 @@ hipError_t launch_attend(const AttnArgs &a, int d, hipStream_t st) {
   if (d == D_) { \
     hipLaunchKernelGGL((k_attend_prep<D_>), dim3(a.n_items, a.n_q), dim3(128), 0, st, a); \
     hipLaunchKernelGGL((k_attend_chunk<D_>), dim3(a.chunks, a.n_items), dim3(256), 0, st, a); \
-    hipLaunchKernelGGL((k_attend_combine<D_>), dim3(a.n_items, a.n_q), dim3(128), 0, st, a); \
+    hipLaunchKernelGGL((k_attend_combine<D_>), dim3(a.n_items, a.n_q), dim3(128), a.chunks * sizeof(float), st, a); \
     return hipGetLastError(); }
   L_(32) L_(64) L_(128)
 #undef L_

@@ -429,10 +429,10 @@ static bool same_opts(const jolt_spectrum_opts &a, const jolt_spectrum_opts &b) 
 namespace {
 
 // CholeskyQR2 of the rows x l matrices in buf (ld ldl): result back in buf, tmp is scratch.
-// split_first: the first pass's product Y R^-1 runs on the bf16 matrix cores with both
-// operands split into hi + lo (relative error ~2^-16: the basis it yields is orthonormal
-// to that order, which the second pass, in fp32, restores to fp32 accuracy).
-int orth(Run &R, const SpecShape &sh, int nc, float *buf, float *tmp, int rows, bool split_first) {
+// split: the products Y R^-1 run on the bf16 matrix cores with both operands split into
+// hi + lo (relative error ~2^-16, so the basis is orthonormal to ~1e-5 instead of fp32
+// accuracy; used for bf16 cells, whose spectra are compared at 1e-3); the Grams stay fp64.
+int orth(Run &R, const SpecShape &sh, int nc, float *buf, float *tmp, int rows, bool split) {
   const int l = sh.ell, ldl = R.w.ldl;
   float *src = buf, *dst = tmp;
   for (int pass = 0; pass < 2; ++pass) {
@@ -452,7 +452,7 @@ int orth(Run &R, const SpecShape &sh, int nc, float *buf, float *tmp, int rows, 
       p.C = dst + (int64_t)c * rows * ldl; p.ldc = ldl;
       p.M = rows; p.N = l; p.K = l; p.alpha = 1.f;
     }
-    int rc = R.gemm(P, split_first && pass == 0 ? 2 : 1, GT_F32, GT_F32, true, false);
+    int rc = R.gemm(P, split ? 2 : 1, GT_F32, GT_F32, true, false);
     if (rc) return rc;
     std::swap(src, dst);
   }
@@ -1174,6 +1174,7 @@ extern "C" int jolt_attend(jolt_ctx *ctx, int n_items, const void *const *k_blob
     rv = std::max(rv, (int)b.rT);
   }
   const int T = kb[0].T, d = kb[0].d, H = kb[0].heads;
+  if (T > 8192 * ATTN_CHUNK) return jolt_fail(JOLT_E_UNSUPPORTED, "jolt_attend: T above %d", 8192 * ATTN_CHUNK);
   if (n_q % H) return jolt_fail(JOLT_E_INVAL, "jolt_attend: n_q = %d is not a multiple of the %d key-value heads", n_q, H);
   if (n_q > ATTN_QMAX || n_q / H > ATTN_REP_MAX)
     return jolt_fail(JOLT_E_UNSUPPORTED, "jolt_attend: at most %d query heads, %d per key-value head", ATTN_QMAX, ATTN_REP_MAX);
