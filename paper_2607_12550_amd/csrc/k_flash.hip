@@ -93,6 +93,13 @@ __global__ void k_gram64_reduce(Gram64Args a) {
   }
 }
 
+// fp32 Gram (from the matrix-core GEMM) widened to the fp64 layout the Cholesky reads
+__global__ void k_widen_gram(const float *C, double *G, int l, int n_cells) {
+  const int64_t ll = (int64_t)l * l, total = ll * n_cells;
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < total; q += (int64_t)gridDim.x * blockDim.x)
+    G[q] = (double)C[q];
+}
+
 // Blocked Cholesky G = L L^T and triangular inverse M = L^-1 in fp64, 64 x 64 tiles.
 // Per block column kb: k_chol_diag factors the diagonal tile in LDS and inverts it
 // (D_kb = L_kb,kb^-1), k_chol_panel forms L_I,kb = G_I,kb D_kb^T below it and
@@ -297,6 +304,13 @@ hipError_t launch_sketch(const SketchArgs &a, int n_cells, hipStream_t st) {
 }
 
 int gram64_tile() { return GT; }
+
+hipError_t launch_widen_gram(const float *C, double *G, int l, int n_cells, hipStream_t st) {
+  const int64_t total = (int64_t)l * l * n_cells;
+  hipLaunchKernelGGL(k_widen_gram, dim3((unsigned)std::min<int64_t>((total + 255) / 256, 4096)), dim3(256), 0, st,
+                     C, G, l, n_cells);
+  return hipGetLastError();
+}
 
 hipError_t launch_gram64(const Gram64Args &a, int n_cells, hipStream_t st) {
   const int nt = (a.l + GT - 1) / GT;

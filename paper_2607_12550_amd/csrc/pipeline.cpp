@@ -429,18 +429,35 @@ static bool same_opts(const jolt_spectrum_opts &a, const jolt_spectrum_opts &b) 
 namespace {
 
 // CholeskyQR2 of the rows x l matrices in buf (ld ldl): result back in buf, tmp is scratch.
-// split: the products Y R^-1 run on the bf16 matrix cores with both operands split into
-// hi + lo (relative error ~2^-16, so the basis is orthonormal to ~1e-5 instead of fp32
-// accuracy; used for bf16 cells, whose spectra are compared at 1e-3); the Grams stay fp64.
+// split (bf16 cells, whose spectra are compared at 1e-3): the products Y R^-1 and the
+// second pass's Gram run on the bf16 matrix cores with both operands split into hi + lo
+// (relative error ~2^-16, so the basis is orthonormal to ~1e-5 instead of fp32 accuracy).
+// The first pass's Gram is always fp64: the raw range basis can be ill-conditioned, the
+// first pass's output is not (its Gram has a condition number near 1).
 int orth(Run &R, const SpecShape &sh, int nc, float *buf, float *tmp, int rows, bool split) {
   const int l = sh.ell, ldl = R.w.ldl;
   float *src = buf, *dst = tmp;
   for (int pass = 0; pass < 2; ++pass) {
-    Gram64Args g{};
-    g.Y = src; g.y_cell_stride = (int64_t)rows * ldl; g.ld = ldl;
-    g.rows = rows; g.l = l; g.chunk_rows = kG64Rows; g.chunks = (rows + kG64Rows - 1) / kG64Rows;
-    g.partial = R.w.g64p; g.G = R.w.g64;
-    HIP_OK(launch_gram64(g, nc, R.st));
+    if (split && pass == 1) {
+      std::vector<GemmProblem> G(nc);
+      for (int c = 0; c < nc; ++c) {
+        GemmProblem &p = G[c];
+        p = GemmProblem{};
+        p.A = plain(src + (int64_t)c * rows * ldl, ldl);             // Y^T: m-contiguous
+        p.B = plain(src + (int64_t)c * rows * ldl, ldl);             // Y: n-contiguous
+        p.C = R.w.C + (int64_t)c * l * l; p.ldc = l;
+        p.M = l; p.N = l; p.K = rows; p.alpha = 1.f;
+      }
+      int rc = R.gemm(G, 2, GT_F32, GT_F32, false, false);
+      if (rc) return rc;
+      HIP_OK(launch_widen_gram(R.w.C, R.w.g64, l, nc, R.st));
+    } else {
+      Gram64Args g{};
+      g.Y = src; g.y_cell_stride = (int64_t)rows * ldl; g.ld = ldl;
+      g.rows = rows; g.l = l; g.chunk_rows = kG64Rows; g.chunks = (rows + kG64Rows - 1) / kG64Rows;
+      g.partial = R.w.g64p; g.G = R.w.g64;
+      HIP_OK(launch_gram64(g, nc, R.st));
+    }
     CholArgs ca{R.w.g64, R.w.chM, R.w.Rinv, R.w.chD, R.w.chMax, l, ldl, chol_blocks(l), 0};
     HIP_OK(launch_chol_inv(ca, nc, R.st));
     std::vector<GemmProblem> P(nc);
