@@ -8,9 +8,12 @@ Section 4, "Joint Lagrangian allocation":
   negligible per-row term (switchable);
 * eq. (2) error model e = eps^2(b) * tau(r_T, r_d), with eps^2(0) = 1 and
   eps^2(b) calibrated once on a Gaussian round trip; tau is the relative
-  Frobenius mass the truncation discards, read here as
+  Frobenius mass the truncation discards, read by default as
   min(1, tau_T(r_T) + tau_d(r_d)) from the mode spectra of the original cell
-  (the ST-HOSVD upper bound; (0, 0) discards everything, tau = 1);
+  (the ST-HOSVD upper bound; (0, 0) discards everything, tau = 1).  When the
+  cell carries the truncated feature spectra mu (row k: r_T = (k + 1) step,
+  see tucker.truncated_feature_spectra) tau is the exact ST-HOSVD value
+  (E - sum_{i < r_d} mu_k[i]) / E and the r_T grid stops at the table's end;
 * eq. (3) minimise the summed error subject to the summed cost <= B;
 * eq. (4) Lagrangian relaxation: for fixed lambda each cell minimises
   e + lambda s over its finite grid independently, and one bisection on
@@ -77,6 +80,25 @@ class CellSpectrum:
     lam_d: np.ndarray      # feature-mode eigenvalues (d values)
     rT_max: int            # largest admissible token rank
     extra: dict = field(default_factory=dict)
+    mu: np.ndarray | None = None   # K x d truncated feature spectra (exact tau) or None
+
+
+def st_tau_table(E: float, mu: np.ndarray) -> np.ndarray:
+    """Exact ST-HOSVD tau: tab[k][r_d] = (E - sum_{i < r_d} mu[k][i]) / E in [0, 1].
+
+    The head sums run from i = 0 upward, one term at a time; E = 0 gives 0.
+    """
+    K, d = mu.shape
+    tab = np.zeros((K, d + 1))
+    if not E > 0.0:
+        return tab
+    for k in range(K):
+        acc = 0.0
+        tab[k][0] = 1.0
+        for i in range(d):
+            acc += float(mu[k][i])
+            tab[k][i + 1] = min(1.0, max(0.0, (E - acc) / E))
+    return tab
 
 
 def cell_grid(cell, eps2: dict, *, bits=BIT_GRID, step: int = 8, floors=(0, 0, 0),
@@ -85,7 +107,11 @@ def cell_grid(cell, eps2: dict, *, bits=BIT_GRID, step: int = 8, floors=(0, 0, 0
     tau_T = tail_fractions(cell.lam_T, cell.E)
     tau_d = tail_fractions(cell.lam_d, cell.E)
     fT, fd, fb = floors
-    rTs = [0] + list(range(step, cell.rT_max + 1, step))
+    rT_hi = cell.rT_max
+    if cell.mu is not None:
+        tab = st_tau_table(cell.E, np.asarray(cell.mu, dtype=np.float64))
+        rT_hi = min(rT_hi, step * tab.shape[0])
+    rTs = [0] + list(range(step, rT_hi + 1, step))
     rds = list(range(step, cell.d + 1, step))
     pts = []
     for b in bits:
@@ -105,7 +131,12 @@ def cell_grid(cell, eps2: dict, *, bits=BIT_GRID, step: int = 8, floors=(0, 0, 0
     P = np.array(pts, dtype=np.int64)
     s = P[:, 0].astype(np.float64)
     eb = np.array([float(eps2[int(x)]) for x in P[:, 1]])
-    e = eb * np.minimum(1.0, tau_T[P[:, 2]] + tau_d[P[:, 3]])
+    if cell.mu is None:
+        tau = np.minimum(1.0, tau_T[P[:, 2]] + tau_d[P[:, 3]])
+    else:
+        tau = np.array([(1.0 if cell.E > 0.0 else 0.0) if rT == 0 else tab[rT // step - 1][rd]
+                        for rT, rd in zip(P[:, 2], P[:, 3])])
+    e = eb * tau
     return s, e, P
 
 

@@ -219,10 +219,13 @@ def cast_output(Xhat: np.ndarray, out_dtype: str) -> np.ndarray:
 def compress_cells(cells, *, ratio: float, eps2: dict, method: str = "exact",
                    in_bytes: int = 2, group: int = 64, seeds=None, bits=(0, 2, 4, 8),
                    q: int = 0, p: int = 10, power_iters: int = 1, step: int = 8,
-                   count_scales: bool = True, factor_bytes: int | None = None):
+                   count_scales: bool = True, factor_bytes: int | None = None,
+                   tau: str = "bound"):
     """Budgeted compression of a list of cells X (each m x T x d) at ``ratio``.
 
     Budget B = (cache bytes) / ratio with cache bytes = sum of m T d * in_bytes.
+    tau = "bound" models the truncation error by the additive mode-tail bound,
+    "exact" by the truncated feature spectra at every grid r_T (exact ST-HOSVD).
     Returns dict(specs, allocation, parts per cell).
     """
     fb = factor_bytes if factor_bytes is not None else (2 if in_bytes == 2 else 4)
@@ -232,8 +235,13 @@ def compress_cells(cells, *, ratio: float, eps2: dict, method: str = "exact",
         sp = spectrum(X, method=method, R=ratio, q=q, p=p, power_iters=power_iters, seed=sd)
         specs.append(sp)
         m, T, d = X.shape
+        mu = None
+        if tau == "exact":
+            mu = tk.truncated_feature_spectra(X, sp["U_T"], list(range(step, sp["rT_max"] + 1, step)))
+        elif tau != "bound":
+            raise ValueError(tau)
         cs.append(CellSpectrum(m=m, T=T, d=d, c=fb, g=group, E=sp["E"], lam_T=sp["lam_T"],
-                               lam_d=sp["lam_d"], rT_max=sp["rT_max"]))
+                               lam_d=sp["lam_d"], rT_max=sp["rT_max"], mu=mu))
     total_in = float(sum(X.size for X in cells) * in_bytes)
     res = allocate(cs, total_in / ratio, eps2, bits=bits, step=step,
                    count_scales=count_scales)

@@ -17,6 +17,8 @@ size T x d and only the token mode (T) and feature mode (d) are truncated.
 * ST-HOSVD (Vannieuwenhoven et al. 2012, cited in section 4): truncate the
   token mode first with U_T, then take the feature factor from the projected
   tensor Y = X x_2 U_T^T, core G = Y x_3 U_d^T;
+* truncated feature spectra: the eigenvalues of Y's feature Gram at every grid
+  token rank, from which the exact discarded mass of every (r_T, r_d) follows;
 * serialisation: fp16 factors (c = 2 bytes per scalar, section 9) with one
   power-of-two exponent per core slice, or fp32 factors (c = 4);
 * reconstruction X~_s = U^_T G^_s U^_d^T from the *stored* factors.
@@ -115,6 +117,29 @@ def tail_fractions(lam: np.ndarray, E: float) -> np.ndarray:
     if E <= 0.0:
         return np.zeros(n + 1)
     return suf / E
+
+
+def truncated_feature_spectra(X: np.ndarray, U_T: np.ndarray, r_list) -> np.ndarray:
+    """Feature spectra of the token-truncated cell, one row per token rank.
+
+    The token-first ST-HOSVD (section 4) takes its feature factor from the
+    projected cell Y = X x_2 U_r^T, U_r = the first r columns of U_T, i.e. from
+    F_Y(r) = sum_s Y_s^T Y_s = sum_s X_s^T U_r U_r^T X_s.  Row k of the result
+    holds the d eigenvalues of F_Y(r_list[k]), descending, clipped at 0.  With
+    orthonormal U_r and U_d the truncation keeps ||G||^2 = the sum of the top
+    r_d of them, so these rows give the exact discarded mass at every (r, r_d).
+    """
+    m, T, d = X.shape
+    out = np.zeros((len(r_list), d))
+    for k, r in enumerate(r_list):
+        U = U_T[:, :r]
+        F = np.zeros((d, d))
+        for s in range(m):
+            Ys = U.T @ X[s]                     # r x d
+            F += Ys.T @ Ys
+        mu, _ = _eigh_desc(F)
+        out[k] = np.maximum(mu, 0.0)
+    return out
 
 
 def st_hosvd(X: np.ndarray, U_T: np.ndarray, r_T: int, r_d: int):
