@@ -52,6 +52,9 @@ def parse():
                     help="empty = the workload's method")
     ap.add_argument("--allocator", default="joint", choices=["joint", "greedy", "rank_only", "uniform"],
                     help="allocation strategy (the joint dual, or an ablation allocator)")
+    ap.add_argument("--tau", default="bound", choices=["bound", "exact"],
+                    help="eq. (2)'s truncation error: the additive mode-tail bound, or the exact "
+                         "ST-HOSVD value from the truncated feature spectra (one extra pass per step)")
     ap.add_argument("--rope-post", type=float, default=0.0,
                     help="> 1: compress post-RoPE keys (rotary base given) instead of pre-RoPE "
                          "ones, for the appendix-B comparison")
@@ -112,6 +115,14 @@ def stage_work(codec, calls):
         work["symv"] = ("hbm", sym_bytes * calls)
         work["token_gram"] = (cache_mfma, nc * 2.0 * T * T * N * calls)
         work["project"] = (cache_mfma, sum(2.0 * r * T * N for r in rT) * calls)
+    if codec.tau == "exact":
+        # the truncated spectra: Y at the grid's largest r_T (a second projection), then the
+        # Grams of its row blocks (fp32 vector arithmetic)
+        r_hi = codec.step * codec.tau_nr
+        extra = nc * 2.0 * r_hi * (codec.ell if flash else T) * N
+        kind, amount = work["project"]
+        work["project"] = (kind, amount + extra * calls)
+        work["trunc_gram"] = ("fp32", nc * codec.tau_nr * 2.0 * d * d * m * codec.step * calls)
     rec = sum(2.0 * m * r * k * d + 2.0 * m * T * r * d for r, k in zip(rT, rd))
     work["reconstruct"] = ("fp32", 2 * rec * calls)           # compress and decompress
     res_b = sum(m * T * d * (in_b + (4 if r else 0)) + m * T * d * b / 8 + (2 * m * T * d / codec.group if b else 0)
@@ -426,7 +437,7 @@ def main():
         log(f"calibration pass: {args.calib_copy_mib} MiB read + written")
         del src, dst
     codec = CacheCodec(K, V, group_layers=gl, method=method, ratio=ratio,
-                       oversample=args.oversample, power_iters=args.power_iters)
+                       oversample=args.oversample, power_iters=args.power_iters, tau=args.tau)
     eps2 = codec.calibrate()
     log("eps2", eps2)
     Kout, Vout = torch.empty_like(K), torch.empty_like(V)
@@ -509,7 +520,8 @@ def main():
         "config": {"workload": args.workload, "layers": cfg["n_layers"], "kv_heads": cfg["n_heads"],
                    "T": cfg["T"], "head_dim": cfg["d"], "batch": cfg["batch"], "group_layers": gl,
                    "cells": len(codec.cells), "method": method, "ratio": ratio,
-                   "allocator": args.allocator, "keys": "post-rope" if args.rope_post > 1.0 else "pre-rope",
+                   "allocator": args.allocator, "tau": args.tau,
+                   "keys": "post-rope" if args.rope_post > 1.0 else "pre-rope",
                    "cache_bytes": cache_bytes},
         "compress_GBps": round(cache_bytes / (np.median(t_comp) * 1e-3) / 1e9, 3),
         "decompress_GBps": round(cache_bytes / (np.median(t_dec) * 1e-3) / 1e9, 3),

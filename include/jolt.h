@@ -112,6 +112,14 @@ typedef struct {
   const double *lam_T;   /* token-mode eigenvalues, descending (FlashJoLT: q_eff values
                             followed by the synthetic tail) */
   const double *lam_d;   /* d feature-mode eigenvalues, descending */
+  int32_t n_mu;          /* 0: eq. (2)'s tau is the additive mode-tail bound
+                            min(1, tau_T(r_T) + tau_d(r_d)).  > 0: mu holds n_mu rows of d
+                            truncated feature spectra (jolt_truncated_spectra, row k at
+                            r_T = (k + 1) * step of the allocation's grid step) and tau is
+                            the exact ST-HOSVD value (E - sum_{i < r_d} mu_k[i]) / E,
+                            clipped to [0, 1]; the r_T grid then ends at n_mu * step */
+  int32_t reserved;
+  const double *mu;      /* host, n_mu x d, rows descending; NULL when n_mu = 0 */
 } jolt_cell_spectrum;
 
 typedef struct {
@@ -259,6 +267,34 @@ int jolt_eps2_workspace_size(int d, int n_samples, size_t *bytes);
 int jolt_eps2_calibrate(jolt_ctx *ctx, int group, int d, uint64_t seed, int n_samples,
                         double eps2_out[4], void *ws, size_t ws_bytes, jolt_stream stream);
 
+/* Truncated feature spectra: the exact ST-HOSVD truncation error of every grid point
+ * (section 4, eq. (2)'s tau; the token mode is truncated first).  For every cell and
+ * every r_T = step, 2 step, ..., n_r * step, the d eigenvalues (descending, clipped at 0)
+ * of F_Y(r_T) = sum_s Y_s^T Y_s with Y_s = U_r^T X_s and U_r the first r_T columns of the
+ * token factor (exact method: top eigenvectors of the token Gram; FlashJoLT: Q W).  With
+ * orthonormal factors the truncation at (r_T, r_d) keeps exactly the top r_d of them, so
+ * jolt_allocate takes tau = (E - their sum) / E from these rows (jolt_cell_spectrum.mu).
+ * Y is formed once at r_T = n_r * step; F_Y(k step) is the running sum over k of the
+ * Grams of its row blocks k (fp32 per block, fp64 running sums, fp32 matrices), then
+ * diagonalised by the one-workgroup tridiagonalisation and fp64 bisection.
+ *   X, seeds, opts, stream: as jolt_spectrum.  opts->reuse = 1 takes the token spectrum a
+ *         jolt_spectrum or jolt_compress call left in this same workspace for these cells
+ *         (JOLT_E_STATE if there is none); 0 computes it (and records it, as jolt_spectrum).
+ *   step, n_r   step >= 1, n_r >= 1, n_r * step <= rT_max of jolt_spectrum_len.
+ *   mu    host, n_cells x n_r x d doubles.
+ *   ws    device, 256-byte aligned, at least jolt_truncated_spectra_workspace_size bytes,
+ *         owned by the caller; its first jolt_workspace_size bytes are laid out as the
+ *         spectrum workspace of the same cells, so a spectrum reused from it must have
+ *         been computed with this same ws and ws_bytes.
+ * Synchronises the stream.  Errors: as jolt_spectrum, plus JOLT_E_INVAL for step or n_r
+ * out of range. */
+int jolt_truncated_spectra_workspace_size(const jolt_cell_desc *desc, int n_cells,
+                                          const jolt_spectrum_opts *opts, int step, int n_r,
+                                          size_t *bytes);
+int jolt_truncated_spectra(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_cells, const void *const *X,
+                           const uint64_t *seeds, const jolt_spectrum_opts *opts, int step, int n_r,
+                           void *ws, size_t ws_bytes, double *mu, jolt_stream stream);
+
 /* Three-mode spectral diagnostics (section 3 and appendix A).  The token- and
  * feature-mode spectra of a cell are jolt_spectrum's (exact method: all T eigenvalues
  * of X_(2) X_(2)^T, all d of F); the slice mode completes the three unfoldings.
@@ -345,6 +381,7 @@ enum {
   JOLT_STAGE_ORTH,             /* FlashJoLT orthonormalisation */
   JOLT_STAGE_SLICE_GRAM,       /* slice-mode Gram of the three-mode diagnostics */
   JOLT_STAGE_ATTEND,           /* decode attention on the factors */
+  JOLT_STAGE_TRUNC_GRAM,       /* prefix feature Grams of the token-truncated cell */
   JOLT_STAGE_COUNT
 };
 int jolt_profile_enable(jolt_ctx *ctx, int on);

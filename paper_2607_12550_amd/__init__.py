@@ -21,7 +21,8 @@ __all__ = ["JoltError", "lib", "CellDesc", "SpectrumOpts", "Params", "CellSpectr
            "jolt_spectrum_len", "jolt_workspace_size", "jolt_decompress_workspace_size", "jolt_spectrum", "jolt_compressed_size",
            "jolt_compress", "jolt_decompress", "jolt_allocate", "jolt_eps2_workspace_size",
            "jolt_eps2_calibrate", "jolt_slice_spectrum_workspace_size", "jolt_slice_spectrum",
-           "jolt_mode_summary", "jolt_attend_workspace_size", "jolt_attend", "jolt_debug_export", "jolt_profile_enable", "jolt_profile_reset",
+           "jolt_mode_summary", "jolt_truncated_spectra_workspace_size", "jolt_truncated_spectra",
+           "jolt_attend_workspace_size", "jolt_attend", "jolt_debug_export", "jolt_profile_enable", "jolt_profile_reset",
            "jolt_profile_read", "STAGES", "cell_desc", "LIB_PATH", "HEADER_PATH"]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -68,7 +69,8 @@ class CellSpectrum(C.Structure):
     _fields_ = [("m", C.c_int32), ("T", C.c_int32), ("d", C.c_int32), ("c", C.c_int32),
                 ("g", C.c_int32), ("n_lam_T", C.c_int32), ("rT_max", C.c_int32),
                 ("pool", C.c_int32), ("E", C.c_double),
-                ("lam_T", C.POINTER(C.c_double)), ("lam_d", C.POINTER(C.c_double))]
+                ("lam_T", C.POINTER(C.c_double)), ("lam_d", C.POINTER(C.c_double)),
+                ("n_mu", C.c_int32), ("reserved", C.c_int32), ("mu", C.POINTER(C.c_double))]
 
 
 class Rope(C.Structure):
@@ -111,6 +113,10 @@ _SIGS = {
     "jolt_attend_workspace_size": (C.c_int, [C.c_int, C.c_int, C.c_int, C.c_int, C.c_int, C.c_int, _P(_sz)]),
     "jolt_attend": (C.c_int, [_vp, C.c_int, _P(_vp), _P(_sz), _P(_vp), _P(_sz), _vp, _vp, _P(_i32),
                               C.c_int, _vp, C.c_float, _vp, _vp, _sz, _vp]),
+    "jolt_truncated_spectra_workspace_size": (C.c_int, [_P(CellDesc), C.c_int, _P(SpectrumOpts),
+                                                         C.c_int, C.c_int, _P(_sz)]),
+    "jolt_truncated_spectra": (C.c_int, [_vp, _P(CellDesc), C.c_int, _P(_vp), _P(C.c_uint64),
+                                         _P(SpectrumOpts), C.c_int, C.c_int, _vp, _sz, _P(_dbl), _vp]),
     "jolt_debug_export": (C.c_int, [_vp, C.c_int, C.c_int, _vp, _sz, _vp]),
     "jolt_profile_enable": (C.c_int, [_vp, C.c_int]),
     "jolt_profile_reset": (C.c_int, [_vp]),
@@ -219,6 +225,27 @@ def jolt_spectrum(ctx, desc: CellDesc, X, seeds=None, opts=None, ws=None, ws_byt
     return E, lam_T, lam_d
 
 
+def jolt_truncated_spectra_workspace_size(desc: CellDesc, n_cells: int, step: int, n_r: int,
+                                          opts=None) -> int:
+    b = _sz()
+    _check(lib.jolt_truncated_spectra_workspace_size(C.byref(desc), n_cells, _opts(opts), step, n_r,
+                                                     C.byref(b)))
+    return b.value
+
+
+def jolt_truncated_spectra(ctx, desc: CellDesc, X, step: int, n_r: int, seeds=None, opts=None,
+                           ws=None, ws_bytes=None, stream=None) -> np.ndarray:
+    """mu[n_cells, n_r, d] (float64): eigenvalues of the feature Gram of the cell truncated
+    to r_T = (k + 1) step in the token mode, row k, descending."""
+    n = len(X)
+    mu = np.zeros((n, n_r, desc.d))
+    sd = (C.c_uint64 * n)(*seeds) if seeds is not None else None
+    wsb = ws_bytes if ws_bytes is not None else (ws.numel() * ws.element_size())
+    _check(lib.jolt_truncated_spectra(ctx, C.byref(desc), n, _ptrs(X), sd, _opts(opts), step, n_r,
+                                      _addr(ws), wsb, mu.ctypes.data_as(_P(_dbl)), _stream(stream)))
+    return mu
+
+
 def jolt_compressed_size(desc: CellDesc, params: Params) -> int:
     b = _sz()
     _check(lib.jolt_compressed_size(C.byref(desc), C.byref(params), C.byref(b)))
@@ -259,8 +286,9 @@ ALLOC_STRATEGIES = {"joint": 0, "greedy": 1, "rank_only": 2, "uniform": 3}
 
 def jolt_allocate(cells, budget_bytes: float, eps2, *, bits=(0, 2, 4, 8), step: int = 8,
                   floors=(0, 0, 0), count_scale_bytes: bool = True, strategy: str = "joint") -> dict:
-    """cells: dicts with m, T, d, c, g, E, lam_T, lam_d, rT_max (numpy arrays for lam_*) and
-    optionally pool (budget pool of the greedy allocator, default 0)."""
+    """cells: dicts with m, T, d, c, g, E, lam_T, lam_d, rT_max (numpy arrays for lam_*),
+    optionally pool (budget pool of the greedy allocator, default 0) and mu (n_mu x d
+    truncated feature spectra at r_T = step, 2 step, ...: exact ST-HOSVD tau)."""
     n = len(cells)
     keep = []
     arr = (CellSpectrum * n)()
@@ -268,9 +296,17 @@ def jolt_allocate(cells, budget_bytes: float, eps2, *, bits=(0, 2, 4, 8), step: 
         lt = np.ascontiguousarray(c["lam_T"], dtype=np.float64)
         ld = np.ascontiguousarray(c["lam_d"], dtype=np.float64)
         keep += [lt, ld]
+        mu = c.get("mu")
+        n_mu, mu_p = 0, None
+        if mu is not None:
+            mu = np.ascontiguousarray(mu, dtype=np.float64)
+            if mu.ndim != 2 or mu.shape[1] != c["d"]:
+                raise ValueError("mu must be n_mu x d")
+            keep.append(mu)
+            n_mu, mu_p = mu.shape[0], mu.ctypes.data_as(_P(_dbl))
         arr[i] = CellSpectrum(c["m"], c["T"], c["d"], c["c"], c["g"], len(lt), c["rT_max"],
                               int(c.get("pool", 0)), c["E"], lt.ctypes.data_as(_P(_dbl)),
-                              ld.ctypes.data_as(_P(_dbl)))
+                              ld.ctypes.data_as(_P(_dbl)), n_mu, 0, mu_p)
     mask = sum(1 << i for i, b in enumerate((0, 2, 4, 8)) if b in bits)
     e4 = (C.c_double * 4)(*[float(eps2[b]) for b in (0, 2, 4, 8)])
     o = AllocOpts(budget_bytes, e4, mask, step, floors[0], floors[1], floors[2],
@@ -299,7 +335,7 @@ def jolt_eps2_calibrate(ctx, group: int, d: int, seed: int, n_samples: int, ws,
 
 STAGES = ["feature_gram", "token_gram", "symv", "panel", "panel_gemm", "tridiag_small", "eigvals",
           "eigvecs", "backtransform", "project", "core", "serialize", "reconstruct", "residual",
-          "decode", "sketch", "orth", "slice_gram", "attend"]
+          "decode", "sketch", "orth", "slice_gram", "attend", "trunc_gram"]
 
 
 def jolt_profile_enable(ctx, on: bool = True) -> None:

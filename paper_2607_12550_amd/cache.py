@@ -5,7 +5,8 @@ Section 4 of the paper cuts the L layers into contiguous groups and compresses
 keys and values of every group separately; here every (group, K/V, batch item)
 is one cell, read in place through a strided descriptor.  This module only
 marshals pointers, sizes buffers and sequences the library calls:
-``jolt_spectrum`` for every cell, ``jolt_allocate`` under the global byte budget
+``jolt_spectrum`` for every cell (and ``jolt_truncated_spectra`` when eq. (2)'s tau is
+taken exactly), ``jolt_allocate`` under the global byte budget
 B = cache bytes / R (eq. (3)), ``jolt_compress`` into one blob arena, and
 ``jolt_decompress`` back into caller-provided tensors.  The compression method
 itself runs entirely inside libjolt.
@@ -21,7 +22,8 @@ from . import (JOLT_BF16, JOLT_EXACT, JOLT_F32, JOLT_FACTOR_F16, JOLT_FACTOR_F32
                HEADER_BYTES, Params, SpectrumOpts, cell_desc, jolt_allocate, jolt_compress,
                jolt_compressed_size, jolt_create, jolt_decompress, jolt_destroy,
                jolt_decompress_workspace_size, jolt_eps2_calibrate, jolt_eps2_workspace_size, jolt_q_cap,
-               jolt_spectrum, jolt_spectrum_len, jolt_workspace_size)
+               jolt_spectrum, jolt_spectrum_len, jolt_truncated_spectra,
+               jolt_truncated_spectra_workspace_size, jolt_workspace_size)
 
 
 @dataclass
@@ -51,7 +53,8 @@ class CacheCodec:
                  method: str = "exact", ratio: float = 2.0, q: int = 0, oversample: int = 10,
                  power_iters: int = 1, group: int = 64, bits=(0, 2, 4, 8), step: int = 8,
                  count_scale_bytes: bool = True, seed: int = 0, max_cells_per_call: int = 16,
-                 workspace_cap_bytes: int = 0, device: int = 0):
+                 workspace_cap_bytes: int = 0, device: int = 0, tau: str = "bound",
+                 tau_rT_cap: int = 0):
         assert K.shape == V.shape and K.dtype == V.dtype and K.is_cuda and K.is_contiguous()
         L, B, H, T, d = K.shape
         if L % group_layers:
@@ -84,7 +87,17 @@ class CacheCodec:
         # one workspace per chunk of cells when they fit under the cap, so that compress
         # reuses every chunk's spectrum; otherwise one shared workspace (spectra recomputed)
         n_chunks = (len(self.cells) + self.chunk - 1) // self.chunk
-        ws_bytes = jolt_workspace_size(self.desc, self.chunk, self.opts)
+        # eq. (2)'s tau: the additive mode-tail bound, or the exact ST-HOSVD value from the
+        # truncated feature spectra on the r_T grid (up to tau_rT_cap, default rT_max)
+        if tau not in ("bound", "exact"):
+            raise ValueError("tau must be 'bound' or 'exact'")
+        self.tau = tau
+        self.tau_nr = (min(self.rT_max, tau_rT_cap or self.rT_max)) // step if tau == "exact" else 0
+        if tau == "exact" and self.tau_nr < 1:
+            raise ValueError("the r_T grid holds no point below the cap")
+        self.mu = None
+        ws_bytes = jolt_workspace_size(self.desc, self.chunk, self.opts) if tau == "bound" else \
+            jolt_truncated_spectra_workspace_size(self.desc, self.chunk, step, self.tau_nr, self.opts)
         if not workspace_cap_bytes:      # default: half of the device's memory
             workspace_cap_bytes = torch.cuda.get_device_properties(K.device).total_memory // 2
         n_ws = n_chunks if n_chunks * ws_bytes <= workspace_cap_bytes else 1
@@ -125,12 +138,16 @@ class CacheCodec:
         return self.eps2
 
     def spectrum(self, stream=None):
-        E, LT, LD = [], [], []
+        E, LT, LD, MU = [], [], [], []
         for i, cs in self._chunks():
-            e, lt, ld = jolt_spectrum(self.ctx, self.desc, [c.ptr for c in cs], self.seeds[i:i + len(cs)],
-                                      self.opts, self._ws(i), stream=stream)
+            ptrs, seeds = [c.ptr for c in cs], self.seeds[i:i + len(cs)]
+            e, lt, ld = jolt_spectrum(self.ctx, self.desc, ptrs, seeds, self.opts, self._ws(i), stream=stream)
             E.append(e); LT.append(lt); LD.append(ld)
+            if self.tau == "exact":
+                MU.append(jolt_truncated_spectra(self.ctx, self.desc, ptrs, self.step, self.tau_nr, seeds=seeds,
+                                                 opts=self.reuse_opts, ws=self._ws(i), stream=stream))
         self.spectra = (np.concatenate(E), np.concatenate(LT), np.concatenate(LD))
+        self.mu = np.concatenate(MU) if MU else None
         self.spectra_fresh = True
         return self.spectra
 
@@ -144,6 +161,9 @@ class CacheCodec:
         cells = [dict(m=m, T=T, d=d, c=self.fbytes, g=self.group, E=float(E[i]), lam_T=LT[i],
                       lam_d=LD[i], rT_max=self.rT_max, pool=self.cells[i].tensor)
                  for i in range(len(self.cells))]
+        if self.mu is not None:
+            for i, c in enumerate(cells):
+                c["mu"] = self.mu[i]
         budget = self.cache_bytes / self.ratio if budget_bytes is None else budget_bytes
         res = jolt_allocate(cells, budget, self.eps2, bits=self.bits, step=self.step,
                             count_scale_bytes=self.count_scale_bytes, strategy=strategy)

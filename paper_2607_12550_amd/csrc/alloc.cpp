@@ -3,8 +3,12 @@
 //
 // Cost (eq. (1)):  s = (m r_T r_d + T r_T + d r_d) c + [b > 0] (b m T d / 8 + 2 m T d / g)
 //                  (the scale term is optional: the paper treats it as negligible).
-// Error (eq. (2)): e = eps2(b) * min(1, tau_T(r_T) + tau_d(r_d)), tau from the mode
-//                  spectra of the cell, tau(r) = (sum of eigenvalues past r) / E.
+// Error (eq. (2)): e = eps2(b) * tau(r_T, r_d).  By default tau = min(1, tau_T(r_T) +
+//                  tau_d(r_d)) from the mode spectra of the cell, tau(r) = (sum of
+//                  eigenvalues past r) / E (the ST-HOSVD bound).  With the truncated
+//                  feature spectra mu_k of the cell (row k at r_T = (k + 1) step) tau is
+//                  the exact discarded mass (E - sum_{i < r_d} mu_k[i]) / E, head sums
+//                  accumulated from i = 0 upward, clipped to [0, 1].
 // Problem (eq. (3)) is solved through the relaxation of eq. (4): for a fixed lambda
 // every cell independently takes the grid point minimising e + lambda s, and one
 // bisection on lambda drives the total cost to the budget.
@@ -50,6 +54,22 @@ std::vector<double> tail_fractions(const double *lam, int n, double E) {
   return suf;
 }
 
+// exact ST-HOSVD tau, n_mu rows of d + 1: tab[k][r_d] = (E - sum_{i < r_d} mu_k[i]) / E
+std::vector<double> exact_tau_table(const double *mu, int n_mu, int d, double E) {
+  std::vector<double> tab((size_t)std::max(n_mu, 0) * (d + 1), 0.0);
+  if (!(E > 0.0)) return tab;
+  for (int k = 0; k < n_mu; ++k) {
+    double acc = 0.0;
+    double *row = tab.data() + (size_t)k * (d + 1);
+    row[0] = 1.0;
+    for (int i = 0; i < d; ++i) {
+      acc += mu[(size_t)k * d + i];
+      row[i + 1] = std::min(1.0, std::max(0.0, (E - acc) / E));
+    }
+  }
+  return tab;
+}
+
 int64_t byte_cost(int64_t m, int64_t T, int64_t d, int64_t rT, int64_t rd, int64_t b, int64_t c,
                   int64_t g, bool scales) {
   int64_t s = (m * rT * rd + T * rT + d * rd) * c;
@@ -89,20 +109,24 @@ extern "C" int jolt_allocate(const jolt_cell_spectrum *cells, int n_cells, const
     if (c.m < 1 || c.T < 1 || c.d < 1 || (c.c != 2 && c.c != 4) || c.g < 1 || c.n_lam_T < 1 ||
         c.rT_max < 0 || c.rT_max > c.n_lam_T || !c.lam_T || !c.lam_d)
       return jolt_fail(JOLT_E_INVAL, "jolt_allocate: malformed cell spectrum %d", ci);
+    if (c.n_mu < 0 || (c.n_mu > 0 && !c.mu))
+      return jolt_fail(JOLT_E_INVAL, "jolt_allocate: malformed truncated spectra of cell %d", ci);
     const std::vector<double> tT = tail_fractions(c.lam_T, c.n_lam_T, c.E);
     const std::vector<double> td = tail_fractions(c.lam_d, c.d, c.E);
+    const std::vector<double> tx = exact_tau_table(c.mu, c.n_mu, c.d, c.E);
+    const int rT_hi = c.n_mu > 0 ? std::min<int64_t>(c.rT_max, (int64_t)c.n_mu * o->step) : c.rT_max;
     std::vector<Point> &pts = grids[ci];
     for (int bi = 0; bi < 4; ++bi) {
       if (!(mask & (1 << bi))) continue;
       const int b = bit_values[bi];
       if (b < o->floor_bits) continue;
       std::vector<int> rTs{0};
-      for (int r = o->step; r <= c.rT_max; r += o->step) rTs.push_back(r);
+      for (int r = o->step; r <= rT_hi; r += o->step) rTs.push_back(r);
       for (int rT : rTs) {
         if (rT < o->floor_rT) continue;
         if (rT == 0) {
           Point p{byte_cost(c.m, c.T, c.d, 0, 0, b, c.c, c.g, o->count_scale_bytes != 0), b, 0, 0, 0.0};
-          const double tau = std::min(1.0, tT[0] + td[0]);
+          const double tau = c.n_mu > 0 ? (c.E > 0.0 ? 1.0 : 0.0) : std::min(1.0, tT[0] + td[0]);
           p.e = o->eps2[bi] * tau;
           pts.push_back(p);
           continue;
@@ -110,7 +134,8 @@ extern "C" int jolt_allocate(const jolt_cell_spectrum *cells, int n_cells, const
         for (int rd = o->step; rd <= c.d; rd += o->step) {
           if (rd < o->floor_rd) continue;
           Point p{byte_cost(c.m, c.T, c.d, rT, rd, b, c.c, c.g, o->count_scale_bytes != 0), b, rT, rd, 0.0};
-          const double tau = std::min(1.0, tT[rT] + td[rd]);
+          const double tau = c.n_mu > 0 ? tx[(size_t)(rT / o->step - 1) * (c.d + 1) + rd]
+                                        : std::min(1.0, tT[rT] + td[rd]);
           p.e = o->eps2[bi] * tau;
           pts.push_back(p);
         }

@@ -182,7 +182,38 @@ __global__ void k_slice_gram_reduce(SliceGramArgs a, float *S_out) {
   S_out[cell * mm + q] = (float)s;
 }
 
+// One thread per matrix element of a cell; the n_k loads of a run are independent of
+// the running sum, so eight are issued ahead of their adds.
+__global__ void __launch_bounds__(256) k_prefix_sum_mats(float *M, int n_k, int64_t elems) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= elems) return;
+  float *p = M + (int64_t)blockIdx.y * n_k * elems + e;
+  double acc = 0.0;
+  int k = 0;
+  for (; k + 8 <= n_k; k += 8) {
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = p[(int64_t)(k + j) * elems];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      acc += (double)v[j];
+      p[(int64_t)(k + j) * elems] = (float)acc;
+    }
+  }
+  for (; k < n_k; ++k) {
+    acc += (double)p[(int64_t)k * elems];
+    p[(int64_t)k * elems] = (float)acc;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_prefix_sum_mats(float *M, int n_cells, int n_k, int64_t elems, hipStream_t st) {
+  if (n_cells < 1 || n_k < 1 || elems < 1) return hipErrorInvalidValue;
+  dim3 grid((unsigned)((elems + 255) / 256), n_cells);
+  hipLaunchKernelGGL(k_prefix_sum_mats, grid, dim3(256), 0, st, M, n_k, elems);
+  return hipGetLastError();
+}
 
 hipError_t launch_slice_gram(const SliceGramArgs &a, int d, int dtype, hipStream_t st) {
   dim3 grid(a.tiles * (a.tiles + 1) / 2, a.chunks, a.n_cells);

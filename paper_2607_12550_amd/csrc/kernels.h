@@ -159,6 +159,10 @@ hipError_t launch_feature_gram(const FGramArgs &a, int d, int dtype, hipStream_t
 hipError_t launch_feature_gram_reduce(const FGramArgs &a, int d, float *F_out, double *E_out,
                                       hipStream_t st);
 
+// Running sums over the n_k matrices of each cell, in place: M[c][k] <- sum_{j <= k} M[c][j]
+// (elems floats per matrix, fp64 accumulation, fp32 stores).
+hipError_t launch_prefix_sum_mats(float *M, int n_cells, int n_k, int64_t elems, hipStream_t st);
+
 // ----------------------------------------------------------------- slice-mode Gram
 // S[cell][s][s'] = sum over tokens t and features f of X[s][t][f] X[s'][t][f] (the Gram of
 // the slice unfolding: appendix A's head mode).  Workgroup (pair of 16-slice tiles, token

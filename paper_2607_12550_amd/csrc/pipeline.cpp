@@ -644,6 +644,45 @@ extern "C" int jolt_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
 }
 
 // ------------------------------------------------------------------------ compress
+namespace {
+
+// The token spectrum of these cells in the workspace: taken from it on request (the context
+// must have recorded one for the same cells, options, seeds and workspace), computed and
+// recorded otherwise.
+int acquire_spectrum(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc,
+                     const void *const *X, const std::vector<uint64_t> &seeds,
+                     const jolt_spectrum_opts &o, void *ws, size_t ws_bytes) {
+  jolt_ctx *ctx = R.ctx;
+  if (o.reuse) {
+    const SpecKey *found = nullptr;
+    for (const SpecKey &k : ctx->specs) {
+      bool ok = k.valid && k.ws == ws && k.ws_bytes == ws_bytes && same_desc(k.desc, *desc) &&
+                same_opts(k.opts, o) && (int)k.X.size() == nc && std::equal(k.X.begin(), k.X.end(), X);
+      if (ok && sh.method == JOLT_FLASH) ok = k.seeds == seeds;
+      if (ok) { found = &k; break; }
+    }
+    if (!found)
+      return jolt_fail(JOLT_E_STATE, "reuse requested but the workspace holds no spectrum of these cells");
+    forget_spectra(ctx, ws, ws_bytes, found);
+    return JOLT_OK;
+  }
+  forget_spectra(ctx, ws, ws_bytes);
+  int rc = spectrum_device(R, sh, desc, nc, X, seeds.data(), &o);
+  if (rc) return rc;
+  ctx->specs.emplace_back();
+  SpecKey &k = ctx->specs.back();
+  k.valid = true;
+  k.ws = ws;
+  k.ws_bytes = ws_bytes;
+  k.desc = *desc;
+  k.opts = o;
+  k.X.assign(X, X + nc);
+  k.seeds = seeds;
+  return JOLT_OK;
+}
+
+}  // namespace
+
 extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_cells, const void *const *X,
                              const jolt_params *params, const jolt_spectrum_opts *opts, void *ws,
                              size_t ws_bytes, void *const *blobs, const size_t *blob_bytes,
@@ -675,34 +714,9 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
   const int m = sh.m, T = sh.T, d = sh.d, N = sh.N, nc = n_cells;
   std::vector<uint64_t> seeds(nc);
   for (int c = 0; c < nc; ++c) seeds[c] = params[c].seed;
-  // the spectrum: taken from the workspace on request (it must hold these cells' spectrum),
-  // computed otherwise
   jolt_spectrum_opts o = opts ? *opts : jolt_spectrum_opts{JOLT_EXACT, 0, 0.0, 0, 0, 0, 0};
-  if (o.reuse) {
-    const SpecKey *found = nullptr;
-    for (const SpecKey &k : ctx->specs) {
-      bool ok = k.valid && k.ws == ws && k.ws_bytes == ws_bytes && same_desc(k.desc, *desc) &&
-                same_opts(k.opts, o) && (int)k.X.size() == nc && std::equal(k.X.begin(), k.X.end(), X);
-      if (ok && sh.method == JOLT_FLASH) ok = k.seeds == seeds;
-      if (ok) { found = &k; break; }
-    }
-    if (!found)
-      return jolt_fail(JOLT_E_STATE, "reuse requested but the workspace holds no spectrum of these cells");
-    forget_spectra(ctx, ws, ws_bytes, found);
-  } else {
-    forget_spectra(ctx, ws, ws_bytes);
-    rc = spectrum_device(R, sh, desc, nc, X, seeds.data(), &o);
-    if (rc) return rc;
-    ctx->specs.emplace_back();
-    SpecKey &k = ctx->specs.back();
-    k.valid = true;
-    k.ws = ws;
-    k.ws_bytes = ws_bytes;
-    k.desc = *desc;
-    k.opts = o;
-    k.X.assign(X, X + nc);
-    k.seeds = seeds;
-  }
+  rc = acquire_spectrum(R, sh, desc, nc, X, seeds, o, ws, ws_bytes);
+  if (rc) return rc;
   rc = upload_seeds_and_signs(R, seeds.data(), nc, d);
   if (rc) return rc;
   std::vector<int> rT(nc), rd(nc);
@@ -888,6 +902,145 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
   dbg.Ud = R.w.Ud; dbg.ud_stride = (int64_t)d * d;
   dbg.Xt = R.w.Xt; dbg.xt_stride = xt_stride;
   dbg.Omega = R.w.Om; dbg.om_stride = (int64_t)N * R.w.ldo; dbg.ldo = R.w.ldo;
+  return JOLT_OK;
+}
+
+// ------------------------------------------------------------------------ truncated feature spectra
+namespace {
+
+struct TruncWs {
+  GemmProblem *tab = nullptr;   // replaces the spectrum plan's table for this call
+  size_t tab_n = 0;
+  FGramCell *fcell = nullptr;   // one per (cell, row block)
+  double *epart = nullptr;
+  int32_t *nonfinite = nullptr;
+  float *F = nullptr;           // [cell][block][d][d]: block Grams, then running sums
+  EigWs eig;
+};
+
+void plan_trunc(Carver &cv, TruncWs &t, const Ws &w, int nc, int n_r, int d) {
+  const size_t nm = (size_t)nc * n_r;
+  t.tab_n = w.tab_n + 2 * (size_t)nc;
+  t.tab = cv.take<GemmProblem>(t.tab_n);
+  t.fcell = cv.take<FGramCell>(nm);
+  t.epart = cv.take<double>(nm);
+  t.nonfinite = cv.take<int32_t>(nm);
+  t.F = cv.take<float>(nm * d * d);
+  carve_eig(cv, t.eig, (int)nm, d, 0, t.F);
+}
+
+int check_trunc(const SpecShape &sh, int step, int n_r) {
+  if (step < 1 || n_r < 1 || (int64_t)step * n_r > sh.rT_max)
+    return jolt_fail(JOLT_E_INVAL, "step %d x n_r %d must be >= 1 and <= rT_max %d", step, n_r, sh.rT_max);
+  return JOLT_OK;
+}
+
+}  // namespace
+
+extern "C" int jolt_truncated_spectra_workspace_size(const jolt_cell_desc *desc, int n_cells,
+                                                     const jolt_spectrum_opts *opts, int step, int n_r,
+                                                     size_t *bytes) {
+  SpecShape sh;
+  int rc = resolve_spectrum(desc, opts, &sh);
+  if (rc) return rc;
+  rc = check_trunc(sh, step, n_r);
+  if (rc) return rc;
+  if (n_cells < 1 || !bytes) return jolt_fail(JOLT_E_INVAL, "n_cells >= 1 and bytes required");
+  Carver cv(nullptr);
+  Ws w;
+  plan(cv, w, sh, n_cells);
+  TruncWs t;
+  plan_trunc(cv, t, w, n_cells, n_r, sh.d);
+  *bytes = cv.off;
+  return JOLT_OK;
+}
+
+extern "C" int jolt_truncated_spectra(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_cells,
+                                      const void *const *X, const uint64_t *seeds,
+                                      const jolt_spectrum_opts *opts, int step, int n_r, void *ws,
+                                      size_t ws_bytes, double *mu, jolt_stream stream) {
+  SpecShape sh;
+  int rc = resolve_spectrum(desc, opts, &sh);
+  if (rc) return rc;
+  rc = check_trunc(sh, step, n_r);
+  if (rc) return rc;
+  rc = check_common(ctx, desc, n_cells, X, ws);
+  if (rc) return rc;
+  if (sh.method == JOLT_FLASH && !seeds) return jolt_fail(JOLT_E_INVAL, "FlashJoLT needs seeds");
+  if (!mu) return jolt_fail(JOLT_E_INVAL, "mu is null");
+  size_t need = 0;
+  jolt_truncated_spectra_workspace_size(desc, n_cells, opts, step, n_r, &need);
+  if (ws_bytes < need) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  HIP_OK(hipSetDevice(ctx->device));
+  Run R{ctx, (hipStream_t)stream, {}};
+  Carver cv(ws);
+  plan(cv, R.w, sh, n_cells);
+  TruncWs t;
+  plan_trunc(cv, t, R.w, n_cells, n_r, sh.d);
+  R.w.tab = t.tab;
+  R.w.tab_n = t.tab_n;
+  const int m = sh.m, T = sh.T, d = sh.d, N = sh.N, nc = n_cells, rmax = step * n_r;
+  std::vector<uint64_t> sd(nc, 0);
+  if (seeds) std::copy(seeds, seeds + nc, sd.begin());
+  jolt_spectrum_opts o = opts ? *opts : jolt_spectrum_opts{JOLT_EXACT, 0, 0.0, 0, 0, 0, 0};
+  rc = acquire_spectrum(R, sh, desc, nc, X, sd, o, ws, ws_bytes);
+  if (rc) return rc;
+  // Y = U_r^T X_(2) at r = n_r * step (rows r, columns s * d + f), as the compression's
+  // projection forms it
+  const std::vector<int> kr(nc, rmax);
+  const int64_t ldu = R.w.kmaxT, u_stride = (int64_t)T * R.w.kmaxT, y_stride = (int64_t)R.w.kmaxT * N;
+  std::vector<GemmProblem> P;
+  if (sh.method == JOLT_EXACT) {
+    rc = eig_vectors(R, R.w.teig, kr, R.w.U, ldu, u_stride);
+    if (rc) return rc;
+    for (int c = 0; c < nc; ++c) {
+      GemmProblem p{};
+      p.A = plain(R.w.U + c * u_stride, ldu);
+      p.B = cell_operand(X[c], desc);
+      p.C = R.w.Y + c * y_stride; p.ldc = N;
+      p.M = rmax; p.N = N; p.K = T; p.alpha = 1.f;
+      P.push_back(p);
+    }
+    StageTimer tm(R.ctx, R.st, JOLT_STAGE_PROJECT);
+    rc = R.gemm(P, desc->dtype == JOLT_BF16 ? 2 : 1, GT_F32, dtype_gt(desc->dtype), false, false);
+    if (rc) return rc;
+  } else {
+    const int l = sh.ell, q = sh.q;
+    rc = eig_vectors(R, R.w.teig, kr, R.w.Wsk, q, (int64_t)l * q);
+    if (rc) return rc;
+    for (int c = 0; c < nc; ++c) {
+      GemmProblem p{};
+      p.A = plain(R.w.Wsk + (int64_t)c * l * q, q);
+      p.B = plain(R.w.Bsk + (int64_t)c * l * N, N);
+      p.C = R.w.Y + c * y_stride; p.ldc = N;
+      p.M = rmax; p.N = N; p.K = l; p.alpha = 1.f;
+      P.push_back(p);
+    }
+    StageTimer tm(R.ctx, R.st, JOLT_STAGE_PROJECT);
+    rc = R.gemm(P, 1, GT_F32, GT_F32, false, false);
+    if (rc) return rc;
+  }
+  // Gram of every row block k of Y (rows k step .. (k+1) step - 1 of all m slices), then
+  // running sums over k: F_Y((k+1) step)
+  const int nm = nc * n_r;
+  std::vector<FGramCell> fc(nm);
+  for (int c = 0; c < nc; ++c)
+    for (int k = 0; k < n_r; ++k) fc[(size_t)c * n_r + k] = FGramCell{R.w.Y + c * y_stride + (int64_t)k * step * N, step, 0};
+  HIP_OK(hipMemcpyAsync(t.fcell, fc.data(), nm * sizeof(FGramCell), hipMemcpyHostToDevice, R.st));
+  FGramArgs a{};
+  a.cells = t.fcell; a.n_cells = nm; a.nseg = m; a.seg_heads = 1; a.seg_hi = d; a.seg_lo = 0;
+  a.row_stride = N; a.chunks_per_cell = 1; a.partial_F = t.F; a.partial_E = t.epart;
+  a.nonfinite = t.nonfinite;
+  {
+    StageTimer tm(R.ctx, R.st, JOLT_STAGE_TRUNC_GRAM);
+    HIP_OK(launch_feature_gram(a, d, JOLT_F32, R.st));
+    HIP_OK(launch_prefix_sum_mats(t.F, nc, n_r, (int64_t)d * d, R.st));
+  }
+  rc = eig_values(R, t.eig);
+  if (rc) return rc;
+  HIP_OK(hipMemcpyAsync(mu, t.eig.b.lam, (size_t)nm * d * sizeof(double), hipMemcpyDeviceToHost, R.st));
+  HIP_OK(hipStreamSynchronize(R.st));
+  for (size_t i = 0; i < (size_t)nm * d; ++i) mu[i] = std::max(0.0, mu[i]);
   return JOLT_OK;
 }
 

@@ -112,6 +112,61 @@ def test_ablation_allocators_bit_identical_to_oracle(rng, strategy):
         assert got["infeasible"] == ref["infeasible"]
 
 
+@pytest.mark.parametrize("flash,cap", [(False, None), (False, 3), (True, None)])
+@pytest.mark.parametrize("strategy", ["joint", "greedy", "uniform"])
+def test_exact_tau_allocators_bit_identical_to_oracle(rng, flash, cap, strategy):
+    """With the truncated feature spectra (exact ST-HOSVD tau) the library and the oracle
+    agree bit for bit, also when the table stops short of rT_max (the grid ends there)."""
+    step = 8
+    cells = _spectra(rng, 4, flash=flash)
+    for i, c in enumerate(cells):
+        x = lowrank_cell(np.random.default_rng(7 + i), 4, 64, 32, 6, noise=0.1 + 0.1 * i)
+        sp = opl.spectrum(x, method="flash" if flash else "exact", q=24, p=6, power_iters=1, seed=i)
+        c.update(E=sp["E"], lam_T=sp["lam_T"], lam_d=sp["lam_d"], rT_max=sp["rT_max"], pool=i % 2)
+        rs = list(range(step, sp["rT_max"] + 1, step))[:cap]
+        c["mu"] = opl.tk.truncated_feature_spectra(x, sp["U_T"], rs)
+    eps2 = oalloc.calibrate_eps2(group=16, d=32, n_samples=1 << 14)
+    ocells = [oalloc.CellSpectrum(m=c["m"], T=c["T"], d=c["d"], c=c["c"], g=c["g"], E=c["E"],
+                                  lam_T=c["lam_T"], lam_d=c["lam_d"], rT_max=c["rT_max"], mu=c["mu"])
+              for c in cells]
+    total_in = sum(c["m"] * c["T"] * c["d"] * 2 for c in cells)
+    for ratio in (1.3, 2.0, 3.0, 5.0, 9.0):
+        B = total_in / ratio
+        got = J.jolt_allocate(cells, B, eps2, step=step, strategy=strategy)
+        if strategy == "greedy":
+            ref = oalloc.allocate_greedy(ocells, B, eps2, [c["pool"] for c in cells], step=step)
+        elif strategy == "uniform":
+            ref = oalloc.allocate_uniform(ocells, B, eps2, step=step)
+        else:
+            ref = oalloc.allocate(ocells, B, eps2, step=step)
+        assert got["alloc"] == [tuple(a) for a in ref["alloc"]], (ratio, strategy)
+        assert got["total_bytes"] == ref["total_bytes"]
+        assert got["model_error"] == ref["model_error"]
+        assert got["infeasible"] == ref["infeasible"]
+        if cap:
+            assert all(a[0] <= cap * step for a in got["alloc"])
+
+
+def test_truncated_spectra_workspace_validation():
+    desc = _desc(T=256)
+    n = J.jolt_truncated_spectra_workspace_size(desc, 2, 8, 32)
+    assert n > J.jolt_workspace_size(desc, 2, None) + 2 * 32 * 128 * 128 * 4
+    for step, n_r in ((0, 4), (8, 0), (8, 33), (257, 1)):
+        with pytest.raises(J.JoltError) as e:
+            J.jolt_truncated_spectra_workspace_size(desc, 2, step, n_r)
+        assert e.value.code == -1                  # JOLT_E_INVAL
+    fl = dict(method=J.JOLT_FLASH, q=24, ratio=2.0, oversample=6, power_iters=1)
+    assert J.jolt_truncated_spectra_workspace_size(desc, 1, 8, 3, fl) > 0
+    with pytest.raises(J.JoltError):
+        J.jolt_truncated_spectra_workspace_size(desc, 1, 8, 4, fl)     # 32 > q = 24
+    # a malformed table is refused by the allocator
+    cells = [dict(m=4, T=16, d=8, c=2, g=8, E=1.0, lam_T=np.ones(16), lam_d=np.ones(8), rT_max=16,
+                  mu=np.ones((2, 8)))]
+    cells[0]["mu"] = np.ones((2, 4))
+    with pytest.raises(ValueError):
+        J.jolt_allocate(cells, 100.0, {0: 1.0, 2: 0.3, 4: 0.01, 8: 1e-4})
+
+
 def test_allocator_floors_and_infeasible(rng):
     cells = _spectra(rng, 3)
     eps2 = {0: 1.0, 2: 0.26, 4: 0.01, 8: 3.5e-5}
