@@ -118,11 +118,11 @@ def stage_work(codec, calls):
     if codec.tau == "exact":
         # the truncated spectra: Y at the grid's largest r_T (a second projection), then the
         # Grams of its row blocks (fp32 vector arithmetic)
-        r_hi = codec.step * codec.tau_nr
+        r_hi = codec.tau_cap_used
         extra = nc * 2.0 * r_hi * (codec.ell if flash else T) * N
         kind, amount = work["project"]
         work["project"] = (kind, amount + extra * calls)
-        work["trunc_gram"] = ("fp32", nc * codec.tau_nr * 2.0 * d * d * m * codec.step * calls)
+        work["trunc_gram"] = ("fp32", nc * 2.0 * d * d * m * r_hi * calls)
     rec = sum(2.0 * m * r * k * d + 2.0 * m * T * r * d for r, k in zip(rT, rd))
     work["reconstruct"] = ("fp32", 2 * rec * calls)           # compress and decompress
     res_b = sum(m * T * d * (in_b + (4 if r else 0)) + m * T * d * b / 8 + (2 * m * T * d / codec.group if b else 0)
@@ -521,6 +521,7 @@ def main():
                    "T": cfg["T"], "head_dim": cfg["d"], "batch": cfg["batch"], "group_layers": gl,
                    "cells": len(codec.cells), "method": method, "ratio": ratio,
                    "allocator": args.allocator, "tau": args.tau,
+                   **({"tau_rT_cap": codec.tau_cap_used} if args.tau == "exact" else {}),
                    "keys": "post-rope" if args.rope_post > 1.0 else "pre-rope",
                    "cache_bytes": cache_bytes},
         "compress_GBps": round(cache_bytes / (np.median(t_comp) * 1e-3) / 1e9, 3),

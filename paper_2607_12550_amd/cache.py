@@ -54,7 +54,7 @@ class CacheCodec:
                  power_iters: int = 1, group: int = 64, bits=(0, 2, 4, 8), step: int = 8,
                  count_scale_bytes: bool = True, seed: int = 0, max_cells_per_call: int = 16,
                  workspace_cap_bytes: int = 0, device: int = 0, tau: str = "bound",
-                 tau_rT_cap: int = 0):
+                 tau_rT_cap: int | None = None):
         assert K.shape == V.shape and K.dtype == V.dtype and K.is_cuda and K.is_contiguous()
         L, B, H, T, d = K.shape
         if L % group_layers:
@@ -88,14 +88,19 @@ class CacheCodec:
         # reuses every chunk's spectrum; otherwise one shared workspace (spectra recomputed)
         n_chunks = (len(self.cells) + self.chunk - 1) // self.chunk
         # eq. (2)'s tau: the additive mode-tail bound, or the exact ST-HOSVD value from the
-        # truncated feature spectra on the r_T grid (up to tau_rT_cap, default rT_max)
+        # truncated feature spectra on the r_T grid up to a cap: tau_rT_cap tokens, or (None)
+        # one chosen per allocation -- 4x the largest r_T the bound's allocation takes (at
+        # least 256), doubled while the exact allocation reaches it
         if tau not in ("bound", "exact"):
             raise ValueError("tau must be 'bound' or 'exact'")
         self.tau = tau
-        self.tau_nr = (min(self.rT_max, tau_rT_cap or self.rT_max)) // step if tau == "exact" else 0
+        self.tau_auto = tau == "exact" and tau_rT_cap is None
+        nr_max = self.rT_max // step
+        self.tau_nr = (nr_max if self.tau_auto else min(self.rT_max, tau_rT_cap) // step) if tau == "exact" else 0
         if tau == "exact" and self.tau_nr < 1:
             raise ValueError("the r_T grid holds no point below the cap")
         self.mu = None
+        self.tau_cap_used = 0
         ws_bytes = jolt_workspace_size(self.desc, self.chunk, self.opts) if tau == "bound" else \
             jolt_truncated_spectra_workspace_size(self.desc, self.chunk, step, self.tau_nr, self.opts)
         if not workspace_cap_bytes:      # default: half of the device's memory
@@ -138,18 +143,31 @@ class CacheCodec:
         return self.eps2
 
     def spectrum(self, stream=None):
-        E, LT, LD, MU = [], [], [], []
+        E, LT, LD = [], [], []
         for i, cs in self._chunks():
-            ptrs, seeds = [c.ptr for c in cs], self.seeds[i:i + len(cs)]
-            e, lt, ld = jolt_spectrum(self.ctx, self.desc, ptrs, seeds, self.opts, self._ws(i), stream=stream)
+            e, lt, ld = jolt_spectrum(self.ctx, self.desc, [c.ptr for c in cs], self.seeds[i:i + len(cs)],
+                                      self.opts, self._ws(i), stream=stream)
             E.append(e); LT.append(lt); LD.append(ld)
-            if self.tau == "exact":
-                MU.append(jolt_truncated_spectra(self.ctx, self.desc, ptrs, self.step, self.tau_nr, seeds=seeds,
-                                                 opts=self.reuse_opts, ws=self._ws(i), stream=stream))
         self.spectra = (np.concatenate(E), np.concatenate(LT), np.concatenate(LD))
-        self.mu = np.concatenate(MU) if MU else None
+        self.mu = None
+        if self.tau == "exact" and not self.tau_auto:
+            self.truncated_spectra(self.tau_nr, stream)
         self.spectra_fresh = True
         return self.spectra
+
+    def truncated_spectra(self, n_r: int, stream=None):
+        """mu of every cell on the r_T grid step .. n_r step; each chunk's token spectrum is
+        taken from its workspace when every chunk has its own (recomputed otherwise)."""
+        own = len(self.ws_list) * self.chunk >= len(self.cells) and self.spectra_fresh
+        MU = []
+        for i, cs in self._chunks():
+            MU.append(jolt_truncated_spectra(self.ctx, self.desc, [c.ptr for c in cs], self.step, n_r,
+                                             seeds=self.seeds[i:i + len(cs)],
+                                             opts=self.reuse_opts if own else self.opts, ws=self._ws(i),
+                                             stream=stream))
+        self.mu = np.concatenate(MU)
+        self.tau_cap_used = n_r * self.step
+        return self.mu
 
     def allocate(self, budget_bytes=None, strategy: str = "joint"):
         """Ranks and bits of every cell under the byte budget: the joint Lagrangian dual, or
@@ -165,8 +183,24 @@ class CacheCodec:
             for i, c in enumerate(cells):
                 c["mu"] = self.mu[i]
         budget = self.cache_bytes / self.ratio if budget_bytes is None else budget_bytes
-        res = jolt_allocate(cells, budget, self.eps2, bits=self.bits, step=self.step,
-                            count_scale_bytes=self.count_scale_bytes, strategy=strategy)
+
+        def run(cs):
+            return jolt_allocate(cs, budget, self.eps2, bits=self.bits, step=self.step,
+                                 count_scale_bytes=self.count_scale_bytes, strategy=strategy)
+
+        if self.tau_auto:
+            top = max(r for r, _, _ in run([{k: v for k, v in c.items() if k != "mu"} for c in cells])["alloc"])
+            n_r = min(self.tau_nr, max(256, 4 * top) // self.step)
+            while True:
+                self.truncated_spectra(n_r)
+                for i, c in enumerate(cells):
+                    c["mu"] = self.mu[i]
+                res = run(cells)
+                if n_r >= self.tau_nr or max(r for r, _, _ in res["alloc"]) < n_r * self.step:
+                    break
+                n_r = min(self.tau_nr, 2 * n_r)
+        else:
+            res = run(cells)
         self.set_params([Params(rT, rd, b, self.group, self.factor_dtype, 0, s)
                          for (rT, rd, b), s in zip(res["alloc"], self.seeds)])
         return res
