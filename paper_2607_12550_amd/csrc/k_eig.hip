@@ -139,6 +139,18 @@ JOLT_DEV void gershgorin(const double *d, const double *e, int n, double &gl, do
 // staged in LDS and every thread advances two independent Sturm chains per sweep, which
 // doubles the work in flight of this latency-bound recurrence.
 constexpr int EV_THREADS = 256, EV_PER_THREAD = 2;
+// 1/x from the hardware estimate refined by two Newton steps (each squares the relative
+// error, so the result is within a few units in the last place).  The Sturm count only
+// needs each step's quotient to that accuracy: it is then the exact count of a tridiagonal
+// within a few ulps of the given one (|x| >= pivmin > 0 here).
+JOLT_DEV double recip(double x) {
+  double r = __builtin_amdgcn_rcp(x);
+  double e = fma(-x, r, 1.0);
+  r = fma(r, e, r);
+  e = fma(-x, r, 1.0);
+  return fma(r, e, r);
+}
+
 __global__ void __launch_bounds__(EV_THREADS) k_tri_eigvals(EigBatch b) {
   extern __shared__ double lds[];
   const int mat = blockIdx.y, n = b.n;
@@ -188,7 +200,7 @@ __global__ void __launch_bounds__(EV_THREADS) k_tri_eigvals(EigBatch b) {
       const double dj = dl[jj], ej2 = e2[jj - 1];
 #pragma unroll
       for (int q = 0; q < EV_PER_THREAD; ++q) {
-        double t = dj - mid[q] - ej2 / qv[q];
+        double t = dj - mid[q] - ej2 * recip(qv[q]);
         if (fabs(t) <= pivmin) t = -pivmin;
         qv[q] = t;
         cnt[q] += t < 0.0;
