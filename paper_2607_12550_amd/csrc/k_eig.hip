@@ -135,10 +135,15 @@ JOLT_DEV void gershgorin(const double *d, const double *e, int n, double &gl, do
   gu += 2.0 * DBL_EPSILON * tnorm + 2.0 * pivmin;
 }
 
-// Bisection for all eigenvalues: one workgroup per (matrix, 512 eigenvalues); d and e^2 are
-// staged in LDS and every thread advances two independent Sturm chains per sweep, which
-// doubles the work in flight of this latency-bound recurrence.
-constexpr int EV_THREADS = 256, EV_PER_THREAD = 2;
+// Bisection for all eigenvalues: one workgroup per (matrix, 256 eigenvalues), one
+// eigenvalue per thread; d and e^2 are staged in LDS.  Each sweep evaluates the Sturm count
+// at three points that split the interval in four (multisection), so a thread advances
+// three independent recurrences per step -- work in flight for this latency-bound chain --
+// and gains two bits per sweep.  The interval is narrowed to the first quarter whose upper
+// point counts more than k eigenvalues, as three successive bisections on the same counts
+// would.  The Gershgorin interval and pivmin are reduced over the workgroup (min / max,
+// independent of order).
+constexpr int EV_THREADS = 256;
 // 1/x from the hardware estimate refined by two Newton steps (each squares the relative
 // error, so the result is within a few units in the last place).  The Sturm count only
 // needs each step's quotient to that accuracy: it is then the exact count of a tridiagonal
@@ -153,66 +158,80 @@ JOLT_DEV double recip(double x) {
 
 __global__ void __launch_bounds__(EV_THREADS) k_tri_eigvals(EigBatch b) {
   extern __shared__ double lds[];
-  const int mat = blockIdx.y, n = b.n;
+  __shared__ double red[3][EV_THREADS / 64];
+  const int mat = blockIdx.y, n = b.n, tid = threadIdx.x;
   double *dl = lds, *e2 = lds + n;
   const double *d = b.d + (int64_t)mat * n, *e = b.e + (int64_t)mat * n;
-  for (int i = threadIdx.x; i < n; i += EV_THREADS) {
-    dl[i] = d[i];
-    e2[i] = (i < n - 1) ? e[i] * e[i] : 0.0;
+  // Gershgorin bounds and pivmin (as the serial gershgorin(): min / max over rows)
+  double g_lo = DBL_MAX, g_hi = -DBL_MAX, emax2 = 0.0;
+  for (int i = tid; i < n; i += EV_THREADS) {
+    const double di = d[i], ei = i < n - 1 ? e[i] : 0.0, ep = i > 0 ? e[i - 1] : 0.0;
+    dl[i] = di;
+    e2[i] = ei * ei;
+    const double r = fabs(ep) + fabs(ei);
+    g_lo = fmin(g_lo, di - r);
+    g_hi = fmax(g_hi, di + r);
+    emax2 = fmax(emax2, ei * ei);
   }
+  for (int o = 32; o >= 1; o >>= 1) {
+    g_lo = fmin(g_lo, __shfl_xor(g_lo, o, 64));
+    g_hi = fmax(g_hi, __shfl_xor(g_hi, o, 64));
+    emax2 = fmax(emax2, __shfl_xor(emax2, o, 64));
+  }
+  if ((tid & 63) == 0) { red[0][tid >> 6] = g_lo; red[1][tid >> 6] = g_hi; red[2][tid >> 6] = emax2; }
   __syncthreads();
-  double gl, gu, pivmin;
-  gershgorin(d, e, n, gl, gu, pivmin);
-  // the tridiagonal comes from an fp32 reduction, so resolving eigenvalues beyond a
-  // 1e-11 fraction of ||T|| adds nothing; this bounds the sweeps at about 40
-  const double atol = 1e-11 * fmax(fabs(gl), fabs(gu));
-  int k[EV_PER_THREAD];
-  double lo[EV_PER_THREAD], hi[EV_PER_THREAD];
-  bool live[EV_PER_THREAD];
-#pragma unroll
-  for (int q = 0; q < EV_PER_THREAD; ++q) {
-    k[q] = blockIdx.x * EV_THREADS * EV_PER_THREAD + q * EV_THREADS + threadIdx.x;
-    lo[q] = gl; hi[q] = gu;
-    live[q] = k[q] < n;
+  double gl = red[0][0], gu = red[1][0];
+  emax2 = red[2][0];
+  for (int w = 1; w < EV_THREADS / 64; ++w) {
+    gl = fmin(gl, red[0][w]); gu = fmax(gu, red[1][w]); emax2 = fmax(emax2, red[2][w]);
   }
+  const double pivmin = DBL_MIN * fmax(1.0, emax2);
+  {
+    const double tnorm = fmax(fabs(gl), fabs(gu));
+    gl -= 2.0 * DBL_EPSILON * tnorm + 2.0 * pivmin;
+    gu += 2.0 * DBL_EPSILON * tnorm + 2.0 * pivmin;
+  }
+  // the tridiagonal comes from an fp32 reduction, so resolving eigenvalues beyond a
+  // 1e-11 fraction of ||T|| adds nothing; this bounds the sweeps at about 20
+  const double atol = 1e-11 * fmax(fabs(gl), fabs(gu));
+  const int k = blockIdx.x * EV_THREADS + tid;
+  double lo = gl, hi = gu;
+  bool live = k < n;
   for (int it = 0; it < 200; ++it) {
-    double mid[EV_PER_THREAD];
-    bool any = false;
+    const double mid = 0.5 * (lo + hi);
+    if (live && (hi - lo <= 2.0 * DBL_EPSILON * fmax(fabs(lo), fabs(hi)) + 4.0 * pivmin + atol ||
+                 mid == lo || mid == hi))
+      live = false;
+    if (!__any(live)) break;
+    // Sturm counts (eigenvalues below x) at the quarter points x[0] < x[1] < x[2]
+    const double h4 = 0.25 * (hi - lo);
+    const double x[3] = {lo + h4, mid, hi - h4};
+    double qv[3];
+    int cnt[3];
 #pragma unroll
-    for (int q = 0; q < EV_PER_THREAD; ++q) {
-      mid[q] = 0.5 * (lo[q] + hi[q]);
-      if (live[q] && (hi[q] - lo[q] <= 2.0 * DBL_EPSILON * fmax(fabs(lo[q]), fabs(hi[q])) + 4.0 * pivmin + atol ||
-                      mid[q] == lo[q] || mid[q] == hi[q]))
-        live[q] = false;
-      any |= live[q];
-    }
-    if (!any) break;
-    // Sturm counts (number of eigenvalues below mid) for both chains in one sweep
-    double qv[EV_PER_THREAD];
-    int cnt[EV_PER_THREAD];
-#pragma unroll
-    for (int q = 0; q < EV_PER_THREAD; ++q) {
-      qv[q] = dl[0] - mid[q];
+    for (int q = 0; q < 3; ++q) {
+      qv[q] = dl[0] - x[q];
       if (fabs(qv[q]) <= pivmin) qv[q] = -pivmin;
       cnt[q] = qv[q] < 0.0;
     }
     for (int jj = 1; jj < n; ++jj) {
       const double dj = dl[jj], ej2 = e2[jj - 1];
 #pragma unroll
-      for (int q = 0; q < EV_PER_THREAD; ++q) {
-        double t = dj - mid[q] - ej2 * recip(qv[q]);
+      for (int q = 0; q < 3; ++q) {
+        double t = dj - x[q] - ej2 * recip(qv[q]);
         if (fabs(t) <= pivmin) t = -pivmin;
         qv[q] = t;
         cnt[q] += t < 0.0;
       }
     }
-#pragma unroll
-    for (int q = 0; q < EV_PER_THREAD; ++q)
-      if (live[q]) { if (cnt[q] > k[q]) hi[q] = mid[q]; else lo[q] = mid[q]; }
+    if (live) {
+      if (cnt[0] > k) hi = x[0];
+      else if (cnt[1] > k) { lo = x[0]; hi = x[1]; }
+      else if (cnt[2] > k) { lo = x[1]; hi = x[2]; }
+      else lo = x[2];
+    }
   }
-#pragma unroll
-  for (int q = 0; q < EV_PER_THREAD; ++q)
-    if (k[q] < n) b.lam[(int64_t)mat * n + (n - 1 - k[q])] = 0.5 * (lo[q] + hi[q]);
+  if (k < n) b.lam[(int64_t)mat * n + (n - 1 - k)] = 0.5 * (lo + hi);
 }
 
 // inverse iteration on (T - lam I) with partial pivoting; per-thread vectors are laid
@@ -377,7 +396,7 @@ hipError_t launch_sytrd_small(const EigBatch &b, hipStream_t st) {
 }
 
 hipError_t launch_tridiag_eigvals(const EigBatch &b, hipStream_t st) {
-  const int per_block = EV_THREADS * EV_PER_THREAD;
+  const int per_block = EV_THREADS;
   dim3 grid((b.n + per_block - 1) / per_block, b.n_mat);
   const size_t shm = (size_t)2 * b.n * sizeof(double);
   if (shm > 65536) {
