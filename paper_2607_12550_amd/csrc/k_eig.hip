@@ -214,6 +214,7 @@ __global__ void __launch_bounds__(EV_THREADS) k_tri_eigvals(EigBatch b) {
       if (fabs(qv[q]) <= pivmin) qv[q] = -pivmin;
       cnt[q] = qv[q] < 0.0;
     }
+#pragma unroll 4
     for (int jj = 1; jj < n; ++jj) {
       const double dj = dl[jj], ej2 = e2[jj - 1];
 #pragma unroll
