@@ -237,7 +237,7 @@ __global__ void __launch_bounds__(EV_THREADS) k_tri_eigvals(EigBatch b) {
 
 // inverse iteration on (T - lam I) with partial pivoting; per-thread vectors are laid
 // out [array][i][column] so neighbouring threads touch neighbouring addresses.
-__global__ void k_tri_eigvecs(EigBatch b, InvitWork w, int j0) {
+__global__ void __launch_bounds__(64) k_tri_eigvecs(EigBatch b, InvitWork w, int j0) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int n = b.n;
   if (idx >= (int64_t)b.n_mat * w.ldlu) return;
@@ -260,55 +260,119 @@ __global__ void k_tri_eigvecs(EigBatch b, InvitWork w, int j0) {
     u32x4 r = philox4x32_10(u32x4{(uint32_t)i, (uint32_t)j, (uint32_t)mat, 4u}, 0x6a6f6c74u, 0u);
     x[(int64_t)i * ld] = ((double)r.x + 0.5) * 0x1p-31 - 1.0;
   }
+  // Each sweep below walks the column serially; its steps are taken in blocks of IB whose
+  // loads are issued one block ahead (they never touch an element the current block
+  // stores), so the memory latency is paid once per block instead of once per step.  The
+  // arithmetic of every step is unchanged.
+  constexpr int IB = 8;
   for (int it = 0; it < 2; ++it) {
     // forward: factor T - lam I = P L U while transforming the right-hand side in x
     double p = d[0] - lam, q = (n > 1) ? e[0] : 0.0;
     double y = x[0];
-    for (int i = 0; i < n - 1; ++i) {
-      const double c = e[i];                       // sub-diagonal entry of row i+1
-      const double a1 = d[i + 1] - lam;
-      const double b1 = (i + 1 < n - 1) ? e[i + 1] : 0.0;
-      double y1 = x[(int64_t)(i + 1) * ld];
-      if (fabs(p) >= fabs(c)) {
-        if (fabs(p) < tiny) p = copysign(tiny, p == 0.0 ? 1.0 : p);
-        const double l = c / p;
-        u0[(int64_t)(i) * ll] = p; u1[(int64_t)(i) * ll] = q; u2[(int64_t)(i) * ll] = 0.0;
-        x[(int64_t)i * ld] = y;
-        y = y1 - l * y;
-        p = a1 - l * q;
-        q = b1;
-      } else {
-        const double l = p / c;
-        u0[(int64_t)(i) * ll] = c; u1[(int64_t)(i) * ll] = a1; u2[(int64_t)(i) * ll] = b1;
-        x[(int64_t)i * ld] = y1;
-        const double ynew = y - l * y1;
-        const double pnew = q - l * a1;
-        q = -l * b1;
-        p = pnew;
-        y = ynew;
+    double nc[IB], na1[IB], nb1[IB], ny1[IB];
+    auto load_fwd = [&](int i0) {
+#pragma unroll
+      for (int s = 0; s < IB; ++s) {
+        const int i = i0 + s;
+        const bool in = i < n - 1;
+        nc[s] = in ? e[i] : 0.0;
+        na1[s] = in ? d[i + 1] - lam : 0.0;
+        nb1[s] = (in && i + 1 < n - 1) ? e[i + 1] : 0.0;
+        ny1[s] = in ? x[(int64_t)(i + 1) * ld] : 0.0;
+      }
+    };
+    load_fwd(0);
+    for (int i0 = 0; i0 < n - 1; i0 += IB) {
+      double cc[IB], ca1[IB], cb1[IB], cy1[IB];
+#pragma unroll
+      for (int s = 0; s < IB; ++s) { cc[s] = nc[s]; ca1[s] = na1[s]; cb1[s] = nb1[s]; cy1[s] = ny1[s]; }
+      if (i0 + IB < n - 1) load_fwd(i0 + IB);
+#pragma unroll
+      for (int s = 0; s < IB; ++s) {
+        const int i = i0 + s;
+        if (i >= n - 1) break;
+        const double c = cc[s];                      // sub-diagonal entry of row i+1
+        const double a1 = ca1[s], b1 = cb1[s], y1 = cy1[s];
+        if (fabs(p) >= fabs(c)) {
+          if (fabs(p) < tiny) p = copysign(tiny, p == 0.0 ? 1.0 : p);
+          const double l = c / p;
+          u0[(int64_t)(i) * ll] = p; u1[(int64_t)(i) * ll] = q; u2[(int64_t)(i) * ll] = 0.0;
+          x[(int64_t)i * ld] = y;
+          y = y1 - l * y;
+          p = a1 - l * q;
+          q = b1;
+        } else {
+          const double l = p / c;
+          u0[(int64_t)(i) * ll] = c; u1[(int64_t)(i) * ll] = a1; u2[(int64_t)(i) * ll] = b1;
+          x[(int64_t)i * ld] = y1;
+          const double ynew = y - l * y1;
+          const double pnew = q - l * a1;
+          q = -l * b1;
+          p = pnew;
+          y = ynew;
+        }
       }
     }
     if (fabs(p) < tiny) p = copysign(tiny, p == 0.0 ? 1.0 : p);
     u0[(int64_t)(n - 1) * ll] = p;
     x[(int64_t)(n - 1) * ld] = y;
-    // back substitution
-    double xn1 = x[(int64_t)(n - 1) * ld] / p, xn2 = 0.0;
+    // back substitution, blocks of rows n-2, n-3, ... loaded one block ahead
+    double xn1 = y / p, xn2 = 0.0;
     x[(int64_t)(n - 1) * ld] = xn1;
     double amax = fabs(xn1);
-    for (int i = n - 2; i >= 0; --i) {
-      const double xi = (x[(int64_t)i * ld] - u1[(int64_t)(i) * ll] * xn1 - u2[(int64_t)(i) * ll] * xn2) /
-                        u0[(int64_t)(i) * ll];
-      x[(int64_t)i * ld] = xi;
-      xn2 = xn1; xn1 = xi;
-      amax = fmax(amax, fabs(xi));
+    double bx[IB], b0[IB], b1v[IB], b2[IB];
+    auto load_back = [&](int i0) {                 // rows i0, i0 - 1, ..., i0 - IB + 1
+#pragma unroll
+      for (int s = 0; s < IB; ++s) {
+        const int i = i0 - s;
+        const bool in = i >= 0;
+        bx[s] = in ? x[(int64_t)i * ld] : 0.0;
+        b0[s] = in ? u0[(int64_t)i * ll] : 1.0;
+        b1v[s] = in ? u1[(int64_t)i * ll] : 0.0;
+        b2[s] = in ? u2[(int64_t)i * ll] : 0.0;
+      }
+    };
+    load_back(n - 2);
+    for (int i0 = n - 2; i0 >= 0; i0 -= IB) {
+      double cx[IB], c0[IB], c1[IB], c2[IB];
+#pragma unroll
+      for (int s = 0; s < IB; ++s) { cx[s] = bx[s]; c0[s] = b0[s]; c1[s] = b1v[s]; c2[s] = b2[s]; }
+      if (i0 - IB >= 0) load_back(i0 - IB);
+#pragma unroll
+      for (int s = 0; s < IB; ++s) {
+        const int i = i0 - s;
+        if (i < 0) break;
+        const double xi = (cx[s] - c1[s] * xn1 - c2[s] * xn2) / c0[s];
+        x[(int64_t)i * ld] = xi;
+        xn2 = xn1; xn1 = xi;
+        amax = fmax(amax, fabs(xi));
+      }
     }
-    const double s = amax > 0.0 ? 1.0 / amax : 1.0;
-    for (int i = 0; i < n; ++i) x[(int64_t)i * ld] *= s;
+    const double sc = amax > 0.0 ? 1.0 / amax : 1.0;
+    for (int i0 = 0; i0 < n; i0 += IB) {
+      double v[IB];
+#pragma unroll
+      for (int s = 0; s < IB; ++s) v[s] = i0 + s < n ? x[(int64_t)(i0 + s) * ld] : 0.0;
+#pragma unroll
+      for (int s = 0; s < IB; ++s) if (i0 + s < n) x[(int64_t)(i0 + s) * ld] = v[s] * sc;
+    }
   }
   double nrm = 0.0;
-  for (int i = 0; i < n; ++i) nrm += x[(int64_t)i * ld] * x[(int64_t)i * ld];
+  for (int i0 = 0; i0 < n; i0 += IB) {
+    double v[IB];
+#pragma unroll
+    for (int s = 0; s < IB; ++s) v[s] = i0 + s < n ? x[(int64_t)(i0 + s) * ld] : 0.0;
+#pragma unroll
+    for (int s = 0; s < IB; ++s) nrm += v[s] * v[s];
+  }
   nrm = nrm > 0.0 ? 1.0 / sqrt(nrm) : 0.0;
-  for (int i = 0; i < n; ++i) x[(int64_t)i * ld] *= nrm;
+  for (int i0 = 0; i0 < n; i0 += IB) {
+    double v[IB];
+#pragma unroll
+    for (int s = 0; s < IB; ++s) v[s] = i0 + s < n ? x[(int64_t)(i0 + s) * ld] : 0.0;
+#pragma unroll
+    for (int s = 0; s < IB; ++s) if (i0 + s < n) x[(int64_t)(i0 + s) * ld] = v[s] * nrm;
+  }
 }
 
 // Modified Gram-Schmidt (two passes) over each cluster of eigenvalues whose
