@@ -426,8 +426,8 @@ __global__ void k_z_to_f32(EigBatch b, InvitWork w, int kmax, float *U, int64_t 
 // T factor of the block reflector of panel p (columns i0 .. i0+pw-1 of A):
 // H_i0 ... H_{i0+pw-1} = I - V T V^T with T upper triangular, built by the forward
 // recurrence T[0:j, j] = -tau_j T[0:j, 0:j] (V^T V)[0:j, j] from the precomputed Gram S.
-constexpr int NB = 64;
-__global__ void __launch_bounds__(64) k_larft(EigBatch b, const float *S_all, float *Tout) {
+constexpr int NB = 128;
+__global__ void __launch_bounds__(NB) k_larft(EigBatch b, const float *S_all, float *Tout) {
   const int mat = blockIdx.y, p = blockIdx.x, n = b.n;
   const int panels = (n + NB - 1) / NB;
   const int i0 = p * NB;
@@ -569,7 +569,7 @@ hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax,
   if (err != hipSuccess) return err;
   err = launch_gemm(tab_dev, nm * panels, NB, NB, 1, GT_F32, GT_F32, false, false, st);
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(k_larft, dim3(panels, nm), dim3(64), 0, st, b, Sf, Tf);
+  hipLaunchKernelGGL(k_larft, dim3(panels, nm), dim3(NB), 0, st, b, Sf, Tf);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   for (int p = panels - 1; p >= 0; --p) {
