@@ -115,75 +115,70 @@ JOLT_DEV void tile_load(double (*t)[CLD], const double *A, int l, int r0, int c0
   }
 }
 
-__global__ void __launch_bounds__(256) k_chol_diag(CholArgs a, int kb) {
-  const int cell = blockIdx.x, l = a.l, tid = threadIdx.x;
+// Diagonal tile of block column kb, one wavefront: lane i keeps row i of the tile in
+// registers.  Column j is factored by broadcasting its pivot and its entries l_kj across the
+// lanes (shuffles, no barriers), with the same operations in the same order as a
+// right-looking factorisation: l_ij = t_ij / sqrt(t_jj), t_ik -= l_ij l_kj (j < k <= i).  The
+// factor is then staged in LDS and lane j forms column j of its inverse by forward
+// substitution: inv_jj = 1 / l_jj, inv_ij = -(sum_{j<=k<i} l_ik inv_kj) / l_ii.
+__global__ void __launch_bounds__(CB) k_chol_diag(CholArgs a, int kb) {
+  static_assert(CB == 64, "one lane per tile row");
+  const int cell = blockIdx.x, l = a.l, lane = threadIdx.x;
   double *G = a.G + (int64_t)cell * l * l;
   double *D = a.Dinv + ((int64_t)cell * a.nbk + kb) * CB * CB;
   double *M = a.M + (int64_t)cell * l * l;
-  __shared__ double t[CB][CLD], inv[CB][CLD];
-  __shared__ double part[4][CB];
-  __shared__ double red[4], sdmax;
+  __shared__ double ts[CB][CLD];
+  double sdmax;
   if (kb == 0) {                       // largest diagonal entry of the untouched Gram
     double mx = 0.0;
-    for (int i = tid; i < l; i += 256) mx = fmax(mx, G[(int64_t)i * l + i]);
+    for (int i = lane; i < l; i += CB) mx = fmax(mx, G[(int64_t)i * l + i]);
     for (int o = 32; o >= 1; o >>= 1) mx = fmax(mx, __shfl_xor(mx, o, 64));
-    if ((tid & 63) == 0) red[tid >> 6] = mx;
-    __syncthreads();
-    if (tid == 0) {
-      sdmax = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
-      a.dmax[cell] = sdmax;
-    }
-  } else if (tid == 0) {
-    sdmax = a.dmax[cell];                // written by the kb = 0 launch
+    if (lane == 0) a.dmax[cell] = mx;
+    sdmax = mx;
+  } else {
+    sdmax = a.dmax[cell];              // written by the kb = 0 launch
   }
   const int o = kb * CB, nb = min(CB, l - o);
-  tile_load(t, G, l, o, o);
-  __syncthreads();
-  if (tid < CB && tid >= nb) t[tid][tid] = 1.0;   // identity on the padding
+  double t[CB];
+#pragma unroll
+  for (int c = 0; c < CB; ++c)        // zeros outside the matrix, identity on the padding
+    t[c] = (lane < nb && c < nb) ? G[(int64_t)(o + lane) * l + o + c] : (c == lane && lane >= nb ? 1.0 : 0.0);
   const double floor_piv = fmax(1e-14 * sdmax, 1e-300);
-  __syncthreads();
+#pragma unroll
   for (int j = 0; j < CB; ++j) {
-    const double piv = sqrt(fmax(t[j][j], j < nb ? floor_piv : 1.0));
-    __syncthreads();
-    if (tid < CB) {
-      if (tid > j) t[tid][j] /= piv;
-      else if (tid == j) t[j][j] = piv;
+    const double piv = sqrt(fmax(__shfl(t[j], j, 64), j < nb ? floor_piv : 1.0));
+    if (lane > j) t[j] /= piv;
+    else if (lane == j) t[j] = piv;
+    const double lij = t[j];
+#pragma unroll
+    for (int k = j + 1; k < CB; ++k) {
+      const double lkj = __shfl(lij, k, 64);
+      if (lane >= k) t[k] = fma(-lij, lkj, t[k]);
     }
-    __syncthreads();
-    {
-      const int i = tid >> 2, k0 = (tid & 3) * 16;
-      if (i > j) {
-        const double lij = t[i][j];
-#pragma unroll 4
-        for (int k = k0; k < k0 + 16; ++k)
-          if (k > j && k <= i) t[i][k] = fma(-lij, t[k][j], t[i][k]);
-      }
-    }
-    __syncthreads();
   }
-  // inverse of the lower-triangular tile, one row at a time: column j < i of row i is
-  // -(sum_{j<=k<i} t[i][k] inv[k][j]) / t[i][i], the k sum split four ways
-  if (tid < CB)
-    for (int i = 0; i < CB; ++i) inv[i][tid] = (i == tid) ? 1.0 / t[i][i] : 0.0;
+#pragma unroll
+  for (int c = 0; c < CB; ++c) ts[lane][c] = t[c];
   __syncthreads();
-  const int j = tid & 63, w = tid >> 6;
+  // column `lane` of the inverse of the lower-triangular factor
+  double inv[CB];
+#pragma unroll
+  for (int i = 0; i < CB; ++i) inv[i] = 0.0;
+  const double djj = 1.0 / ts[lane][lane];
+#pragma unroll
+  for (int i = 0; i < CB; ++i) if (i == lane) inv[i] = djj;
+#pragma unroll
   for (int i = 1; i < CB; ++i) {
-    double s = 0.0;
-    if (j < i) {
-      const int len = i - j, k0 = j + (len * w) / 4, k1 = j + (len * (w + 1)) / 4;
-      for (int k = k0; k < k1; ++k) s = fma(t[i][k], inv[k][j], s);
-    }
-    part[w][j] = s;
-    __syncthreads();
-    if (w == 0 && j < i) inv[i][j] = -(part[0][j] + part[1][j] + part[2][j] + part[3][j]) / t[i][i];
-    __syncthreads();
+    double sum = 0.0;
+#pragma unroll
+    for (int k = 0; k < i; ++k) sum = fma(ts[i][k], inv[k], sum);   // inv[k] = 0 for k < lane
+    if (lane < i) inv[i] = -sum / ts[i][i];
   }
-  for (int q = tid; q < CB * CB; q += 256) {
-    const int r = q / CB, c = q % CB;
-    D[q] = inv[r][c];
-    if (r < nb && c < nb) {
-      if (c <= r) G[(int64_t)(o + r) * l + o + c] = t[r][c];
-      M[(int64_t)(o + r) * l + o + c] = inv[r][c];
+#pragma unroll
+  for (int r = 0; r < CB; ++r) {
+    D[r * CB + lane] = inv[r];
+    if (r < nb && lane < nb) {
+      if (lane <= r) G[(int64_t)(o + r) * l + o + lane] = ts[r][lane];
+      M[(int64_t)(o + r) * l + o + lane] = inv[r];
     }
   }
 }
@@ -329,7 +324,7 @@ hipError_t launch_chol_inv(const CholArgs &a, int n_cells, hipStream_t st) {
   const int nbk = a.nbk;
   if (nbk != chol_blocks(a.l)) return hipErrorInvalidValue;
   for (int kb = 0; kb < nbk; ++kb) {
-    hipLaunchKernelGGL(k_chol_diag, dim3(n_cells), dim3(256), 0, st, a, kb);
+    hipLaunchKernelGGL(k_chol_diag, dim3(n_cells), dim3(CB), 0, st, a, kb);
     const int below = nbk - kb - 1;
     if (below > 0) {
       hipLaunchKernelGGL(k_chol_panel, dim3(below, n_cells), dim3(256), 0, st, a, kb);
