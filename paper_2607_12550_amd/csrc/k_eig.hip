@@ -36,6 +36,19 @@ JOLT_DEV double block_sum(double v, double *red) {
 // the sizes this kernel serves).  Writes d, e, tau and leaves v_i in column i of A
 // (rows i+1..n-1, v_i(i+1) = 1) with zeros above, the dense form the blocked
 // back-transformation multiplies by.
+//
+// Blocked in panels of SB columns (the LAPACK latrd scheme inside one workgroup): the
+// panel's reflectors V and the vectors W (A_i v_i corrected for the panel's earlier
+// reflectors, then w += K v) are kept in LDS by absolute row.  Column i is brought up to
+// date with the panel's earlier reflectors only when it becomes current; the mat-vec reads
+// the trailing matrix as it was at the panel start and subtracts V (W^T v) + W (V^T v); the
+// trailing matrix past the panel takes the rank-2 SB update once, at the panel end.  Each
+// column then reads the trailing matrix once instead of three times (mat-vec, and the
+// read and write of an immediate rank-2 update).
+constexpr int SB = 16, SBL = SB + 1;     // panel width, LDS row stride of V and W
+
+size_t sytd2_lds_bytes(int n) { return ((size_t)2 * n + (size_t)2 * n * SBL + 2 * SB) * sizeof(float); }
+
 __global__ void __launch_bounds__(SYTD2_THREADS) k_sytd2(EigBatch b) {
   const int mat = blockIdx.x, n = b.n;
   float *A = b.A + (int64_t)mat * b.mat_stride;
@@ -43,54 +56,97 @@ __global__ void __launch_bounds__(SYTD2_THREADS) k_sytd2(EigBatch b) {
   float *tau = b.tau + (int64_t)mat * n;
   extern __shared__ float sh[];
   float *v = sh, *w = sh + n;
+  float *Vp = w + n, *Wp = Vp + (size_t)n * SBL, *yv = Wp + (size_t)n * SBL;
   __shared__ double red[SYTD2_THREADS / 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = SYTD2_THREADS / 64;
-  for (int i = 0; i < n - 1; ++i) {
-    const int L = n - 1 - i;
-    for (int t = tid; t < L; t += SYTD2_THREADS) v[t] = A[(int64_t)(i + 1 + t) * n + i];
-    __syncthreads();
-    double part = 0.0;
-    for (int t = 1 + tid; t < L; t += SYTD2_THREADS) part += (double)v[t] * (double)v[t];
-    const double sigma = block_sum(part, red);
-    const double alpha = v[0];
-    double beta, tv, scal;
-    if (sigma == 0.0) {
-      tv = 0.0; beta = alpha; scal = 0.0;
-    } else {
-      beta = -copysign(sqrt(alpha * alpha + sigma), alpha);
-      tv = (beta - alpha) / beta;
-      scal = 1.0 / (alpha - beta);
+  for (int k0 = 0; k0 < n - 1; k0 += SB) {
+    const int jb = min(SB, n - 1 - k0);
+    for (int q = tid; q < (n - k0) * SBL; q += SYTD2_THREADS) {
+      Vp[(size_t)k0 * SBL + q] = 0.f;
+      Wp[(size_t)k0 * SBL + q] = 0.f;
     }
     __syncthreads();
-    for (int t = tid; t < L; t += SYTD2_THREADS) {
-      float vt = (t == 0) ? 1.f : (float)((double)v[t] * scal);
-      if (tv == 0.0) vt = (t == 0) ? 1.f : 0.f;
-      v[t] = vt;
-      A[(int64_t)(i + 1 + t) * n + i] = vt;
+    for (int j = 0; j < jb; ++j) {
+      const int i = k0 + j, L = n - 1 - i;
+      // column i (rows i..n-1) brought up to date with reflectors k0 .. i-1
+      for (int r = i + tid; r < n; r += SYTD2_THREADS) {
+        float a = A[(int64_t)r * n + i];
+        for (int p = 0; p < j; ++p)
+          a -= Vp[(size_t)r * SBL + p] * Wp[(size_t)i * SBL + p] + Wp[(size_t)r * SBL + p] * Vp[(size_t)i * SBL + p];
+        if (r == i) A[(int64_t)i * n + i] = a;
+        else v[r - i - 1] = a;
+      }
+      __syncthreads();
+      double part = 0.0;
+      for (int t = 1 + tid; t < L; t += SYTD2_THREADS) part += (double)v[t] * (double)v[t];
+      const double sigma = block_sum(part, red);
+      const double alpha = v[0];
+      double beta, tv, scal;
+      if (sigma == 0.0) {
+        tv = 0.0; beta = alpha; scal = 0.0;
+      } else {
+        beta = -copysign(sqrt(alpha * alpha + sigma), alpha);
+        tv = (beta - alpha) / beta;
+        scal = 1.0 / (alpha - beta);
+      }
+      __syncthreads();
+      for (int t = tid; t < L; t += SYTD2_THREADS) {
+        float vt = (t == 0) ? 1.f : (float)((double)v[t] * scal);
+        if (tv == 0.0) vt = (t == 0) ? 1.f : 0.f;
+        v[t] = vt;
+        A[(int64_t)(i + 1 + t) * n + i] = vt;
+        Vp[(size_t)(i + 1 + t) * SBL + j] = vt;
+      }
+      if (tid == 0) { ee[i] = beta; tau[i] = (float)tv; }
+      __syncthreads();
+      if (tv == 0.0) continue;                     // W column stays zero
+      const float tf = (float)tv;
+      // w' = A22 v over the trailing matrix as of the panel start (one wavefront per row)
+      for (int r = wave; r < L; r += nw) {
+        const float *row = A + (int64_t)(i + 1 + r) * n + (i + 1);
+        float sacc = 0.f;
+        for (int c = lane; c < L; c += 64) sacc = fmaf(row[c], v[c], sacc);
+        sacc = wave_sum(sacc);
+        if (lane == 0) w[r] = sacc;
+      }
+      // yv = [W^T v ; V^T v] over rows i+1.. for the panel's earlier reflectors
+      for (int q = wave; q < 2 * j; q += nw) {
+        const float *col = (q < j ? Wp : Vp) + (q < j ? q : q - j);
+        float sacc = 0.f;
+        for (int t = lane; t < L; t += 64) sacc = fmaf(col[(size_t)(i + 1 + t) * SBL], v[t], sacc);
+        sacc = wave_sum(sacc);
+        if (lane == 0) yv[q < j ? q : SB + q - j] = sacc;
+      }
+      __syncthreads();
+      for (int t = tid; t < L; t += SYTD2_THREADS) {
+        float c = w[t];
+        const size_t rr = (size_t)(i + 1 + t) * SBL;
+        for (int p = 0; p < j; ++p) c -= Vp[rr + p] * yv[p] + Wp[rr + p] * yv[SB + p];
+        w[t] = tf * c;
+      }
+      __syncthreads();
+      part = 0.0;
+      for (int t = tid; t < L; t += SYTD2_THREADS) part += (double)w[t] * (double)v[t];
+      const float K = (float)(-0.5 * tv * block_sum(part, red));
+      for (int t = tid; t < L; t += SYTD2_THREADS) {
+        const float wt = fmaf(K, v[t], w[t]);
+        Wp[(size_t)(i + 1 + t) * SBL + j] = wt;
+      }
+      __syncthreads();
     }
-    if (tid == 0) { ee[i] = beta; tau[i] = (float)tv; }
-    __syncthreads();
-    if (tv == 0.0) continue;
-    const float tf = (float)tv;
-    // w = tau * A22 v  (one wavefront per row, lanes along the row)
-    for (int r = wave; r < L; r += nw) {
-      const float *row = A + (int64_t)(i + 1 + r) * n + (i + 1);
-      float s = 0.f;
-      for (int c = lane; c < L; c += 64) s = fmaf(row[c], v[c], s);
-      s = wave_sum(s);
-      if (lane == 0) w[r] = tf * s;
-    }
-    __syncthreads();
-    part = 0.0;
-    for (int t = tid; t < L; t += SYTD2_THREADS) part += (double)w[t] * (double)v[t];
-    const float K = (float)(-0.5 * tv * block_sum(part, red));
-    for (int t = tid; t < L; t += SYTD2_THREADS) w[t] = fmaf(K, v[t], w[t]);
-    __syncthreads();
-    // A22 -= v w^T + w v^T
-    for (int r = wave; r < L; r += nw) {
-      float *row = A + (int64_t)(i + 1 + r) * n + (i + 1);
-      const float vr = v[r], wr = w[r];
-      for (int c = lane; c < L; c += 64) row[c] -= vr * w[c] + wr * v[c];
+    // trailing matrix past the panel: A -= V W^T + W V^T (both triangles)
+    const int s0 = k0 + jb;
+    for (int r = s0 + wave; r < n; r += nw) {
+      float vr[SB], wr[SB];
+#pragma unroll
+      for (int p = 0; p < SB; ++p) { vr[p] = Vp[(size_t)r * SBL + p]; wr[p] = Wp[(size_t)r * SBL + p]; }
+      float *row = A + (int64_t)r * n;
+      for (int c = s0 + lane; c < n; c += 64) {
+        float acc = 0.f;
+#pragma unroll
+        for (int p = 0; p < SB; ++p) acc = fmaf(vr[p], Wp[(size_t)c * SBL + p], fmaf(wr[p], Vp[(size_t)c * SBL + p], acc));
+        row[c] -= acc;
+      }
     }
     __syncthreads();
   }
@@ -455,7 +511,12 @@ __global__ void __launch_bounds__(NB) k_larft(EigBatch b, const float *S_all, fl
 }  // namespace
 
 hipError_t launch_sytrd_small(const EigBatch &b, hipStream_t st) {
-  size_t shm = (size_t)2 * b.n * sizeof(float);
+  const size_t shm = sytd2_lds_bytes(b.n);
+  if (shm > 65536) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_sytd2),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+    if (e != hipSuccess) return e;
+  }
   hipLaunchKernelGGL(k_sytd2, dim3(b.n_mat), dim3(SYTD2_THREADS), shm, st, b);
   return hipGetLastError();
 }
