@@ -32,6 +32,20 @@ JOLT_DEV double block_sum(double v, double *red) {
   return s;
 }
 
+// Workgroup sum with one barrier: successive calls alternate between two halves of red
+// (2 x waves entries), so a call never overwrites values an earlier call is still reading.
+JOLT_DEV double block_sum1(double v, double *red, int &flip) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  v = wave_sum(v);
+  double *r = red + flip * nw;
+  flip ^= 1;
+  if (lane == 0) r[wave] = v;
+  __syncthreads();
+  double s = 0.0;
+  for (int w = 0; w < nw; ++w) s += r[w];
+  return s;
+}
+
 // One workgroup per matrix; full symmetric storage in global memory (L2-resident for
 // the sizes this kernel serves).  Writes d, e, tau and leaves v_i in column i of A
 // (rows i+1..n-1, v_i(i+1) = 1) with zeros above, the dense form the blocked
@@ -57,8 +71,10 @@ __global__ void __launch_bounds__(SYTD2_THREADS) k_sytd2(EigBatch b) {
   extern __shared__ float sh[];
   float *v = sh, *w = sh + n;
   float *Vp = w + n, *Wp = Vp + (size_t)n * SBL, *yv = Wp + (size_t)n * SBL;
-  __shared__ double red[SYTD2_THREADS / 64];
+  __shared__ double red[2 * (SYTD2_THREADS / 64)];
+  __shared__ double s_alpha;                        // x[0] of the current column
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = SYTD2_THREADS / 64;
+  int flip = 0;
   for (int k0 = 0; k0 < n - 1; k0 += SB) {
     const int jb = min(SB, n - 1 - k0);
     for (int q = tid; q < (n - k0) * SBL; q += SYTD2_THREADS) {
@@ -68,19 +84,22 @@ __global__ void __launch_bounds__(SYTD2_THREADS) k_sytd2(EigBatch b) {
     __syncthreads();
     for (int j = 0; j < jb; ++j) {
       const int i = k0 + j, L = n - 1 - i;
-      // column i (rows i..n-1) brought up to date with reflectors k0 .. i-1
+      // column i (rows i..n-1) brought up to date with reflectors k0 .. i-1; the squared
+      // norm of x[1..] is accumulated on the way
+      double part = 0.0;
       for (int r = i + tid; r < n; r += SYTD2_THREADS) {
         float a = A[(int64_t)r * n + i];
         for (int p = 0; p < j; ++p)
           a -= Vp[(size_t)r * SBL + p] * Wp[(size_t)i * SBL + p] + Wp[(size_t)r * SBL + p] * Vp[(size_t)i * SBL + p];
         if (r == i) A[(int64_t)i * n + i] = a;
         else v[r - i - 1] = a;
+        if (r == i + 1) s_alpha = a;
+        if (r > i + 1) part += (double)a * (double)a;
       }
-      __syncthreads();
-      double part = 0.0;
-      for (int t = 1 + tid; t < L; t += SYTD2_THREADS) part += (double)v[t] * (double)v[t];
-      const double sigma = block_sum(part, red);
-      const double alpha = v[0];
+      // its barrier also publishes v and x[0]; v[0] is overwritten below, so x[0] is read
+      // from its own copy (rewritten only after two more barriers)
+      const double sigma = block_sum1(part, red, flip);
+      const double alpha = s_alpha;
       double beta, tv, scal;
       if (sigma == 0.0) {
         tv = 0.0; beta = alpha; scal = 0.0;
@@ -89,25 +108,40 @@ __global__ void __launch_bounds__(SYTD2_THREADS) k_sytd2(EigBatch b) {
         tv = (beta - alpha) / beta;
         scal = 1.0 / (alpha - beta);
       }
-      __syncthreads();
-      for (int t = tid; t < L; t += SYTD2_THREADS) {
+      // v = x scaled (v[0] = 1); every entry has one owner in this loop
+      for (int r = i + 1 + tid; r < n; r += SYTD2_THREADS) {
+        const int t = r - i - 1;
         float vt = (t == 0) ? 1.f : (float)((double)v[t] * scal);
         if (tv == 0.0) vt = (t == 0) ? 1.f : 0.f;
         v[t] = vt;
-        A[(int64_t)(i + 1 + t) * n + i] = vt;
-        Vp[(size_t)(i + 1 + t) * SBL + j] = vt;
+        A[(int64_t)r * n + i] = vt;
+        Vp[(size_t)r * SBL + j] = vt;
       }
       if (tid == 0) { ee[i] = beta; tau[i] = (float)tv; }
       __syncthreads();
       if (tv == 0.0) continue;                     // W column stays zero
       const float tf = (float)tv;
-      // w' = A22 v over the trailing matrix as of the panel start (one wavefront per row)
-      for (int r = wave; r < L; r += nw) {
-        const float *row = A + (int64_t)(i + 1 + r) * n + (i + 1);
-        float sacc = 0.f;
-        for (int c = lane; c < L; c += 64) sacc = fmaf(row[c], v[c], sacc);
-        sacc = wave_sum(sacc);
-        if (lane == 0) w[r] = sacc;
+      // w' = A22 v over the trailing matrix as of the panel start: a wavefront takes four
+      // rows at a time (rows r, r + nw, r + 2 nw, r + 3 nw) so that their loads are in
+      // flight together; rows past L read row L - 1 and are not stored
+      for (int r0 = wave; r0 < L; r0 += 4 * nw) {
+        const float *row[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) row[u] = A + (int64_t)(i + 1 + min(r0 + u * nw, L - 1)) * n + (i + 1);
+        float sacc[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int c = lane; c < L; c += 64) {
+          float x[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) x[u] = row[u][c];
+          const float vc = v[c];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) sacc[u] = fmaf(x[u], vc, sacc[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float su = wave_sum(sacc[u]);
+          if (lane == 0 && r0 + u * nw < L) w[r0 + u * nw] = su;
+        }
       }
       // yv = [W^T v ; V^T v] over rows i+1.. for the panel's earlier reflectors
       for (int q = wave; q < 2 * j; q += nw) {
@@ -118,19 +152,27 @@ __global__ void __launch_bounds__(SYTD2_THREADS) k_sytd2(EigBatch b) {
         if (lane == 0) yv[q < j ? q : SB + q - j] = sacc;
       }
       __syncthreads();
-      for (int t = tid; t < L; t += SYTD2_THREADS) {
-        float c = w[t];
-        const size_t rr = (size_t)(i + 1 + t) * SBL;
-        for (int p = 0; p < j; ++p) c -= Vp[rr + p] * yv[p] + Wp[rr + p] * yv[SB + p];
-        w[t] = tf * c;
-      }
-      __syncthreads();
+      // corrected w = tau (w' - V yv_W - W yv_V), kept in a register by the thread that owns
+      // row t, and its dot with v for K
       part = 0.0;
-      for (int t = tid; t < L; t += SYTD2_THREADS) part += (double)w[t] * (double)v[t];
-      const float K = (float)(-0.5 * tv * block_sum(part, red));
-      for (int t = tid; t < L; t += SYTD2_THREADS) {
-        const float wt = fmaf(K, v[t], w[t]);
-        Wp[(size_t)(i + 1 + t) * SBL + j] = wt;
+      float wt[(1024 + SYTD2_THREADS - 1) / SYTD2_THREADS];
+#pragma unroll
+      for (int u = 0; u < (int)(sizeof(wt) / sizeof(float)); ++u) {
+        const int t = tid + u * SYTD2_THREADS;
+        wt[u] = 0.f;
+        if (t < L) {
+          float c = w[t];
+          const size_t rr = (size_t)(i + 1 + t) * SBL;
+          for (int p = 0; p < j; ++p) c -= Vp[rr + p] * yv[p] + Wp[rr + p] * yv[SB + p];
+          wt[u] = tf * c;
+          part += (double)wt[u] * (double)v[t];
+        }
+      }
+      const float K = (float)(-0.5 * tv * block_sum1(part, red, flip));
+#pragma unroll
+      for (int u = 0; u < (int)(sizeof(wt) / sizeof(float)); ++u) {
+        const int t = tid + u * SYTD2_THREADS;
+        if (t < L) Wp[(size_t)(i + 1 + t) * SBL + j] = fmaf(K, v[t], wt[u]);
       }
       __syncthreads();
     }
@@ -511,6 +553,7 @@ __global__ void __launch_bounds__(NB) k_larft(EigBatch b, const float *S_all, fl
 }  // namespace
 
 hipError_t launch_sytrd_small(const EigBatch &b, hipStream_t st) {
+  if (b.n > SYTD2_THREADS) return hipErrorInvalidValue;   // one corrected w entry per thread
   const size_t shm = sytd2_lds_bytes(b.n);
   if (shm > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_sytd2),
