@@ -533,14 +533,22 @@ __global__ void __launch_bounds__(NB) k_larft(EigBatch b, const float *S_all, fl
   const float *tau = b.tau + (int64_t)mat * n;
   const float *S = S_all + ((int64_t)mat * panels + p) * NB * NB;
   __shared__ float T[NB][NB + 1];
+  __shared__ float Ss[NB][NB + 1];              // the panel's Gram, staged once
   const int a = threadIdx.x;
   for (int c = 0; c < NB; ++c) T[a][c] = 0.f;
+  for (int r0 = 0; r0 < NB; r0 += 16) {         // sixteen loads in flight per thread
+    float x[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) x[k] = S[(r0 + k) * NB + a];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) Ss[r0 + k][a] = x[k];
+  }
   __syncthreads();
   for (int j = 0; j < pw; ++j) {
     const float tj = tau[i0 + j];
     float s = 0.f;
     if (a < j)
-      for (int c = a; c < j; ++c) s = fmaf(T[a][c], S[c * NB + j], s);
+      for (int c = a; c < j; ++c) s = fmaf(T[a][c], Ss[c][j], s);
     __syncthreads();
     if (a < j) T[a][j] = -tj * s;
     if (a == j) T[j][j] = tj;
