@@ -255,7 +255,8 @@ def diagnostics(args):
     cfg = dict(kvsynth.CONFIGS[args.workload])
     gl = cfg.pop("group_layers")
     cfg["workers"] = 8
-    Knp, Vnp = kvsynth.make_cache(**cfg)
+    # generation runs in worker processes (the values do not depend on their number)
+    Knp, Vnp = kvsynth.make_cache(**cfg, workers=min(16, os.cpu_count() or 1))
     to_dev = (lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()) \
         if cfg["dtype"] == "bf16" else (lambda a: torch.from_numpy(a).cuda())
     K, V = to_dev(Knp), to_dev(Vnp)
@@ -306,7 +307,8 @@ def attend_bench(args):
     method, ratio = args.method or method, args.ratio or ratio
     cfg["workers"] = 8
     log("generating", args.workload)
-    Knp, Vnp = kvsynth.make_cache(**cfg)
+    # generation runs in worker processes (the values do not depend on their number)
+    Knp, Vnp = kvsynth.make_cache(**cfg, workers=min(16, os.cpu_count() or 1))
     dev = torch.device("cuda", 0)
     to_dev = (lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)) \
         if cfg["dtype"] == "bf16" else (lambda a: torch.from_numpy(a).to(dev))
@@ -416,7 +418,8 @@ def main():
     ratio = args.ratio or ratio
     log("generating", args.workload)
     t0 = time.perf_counter()
-    Knp, Vnp = kvsynth.make_cache(**cfg)
+    # generation runs in worker processes (the values do not depend on their number)
+    Knp, Vnp = kvsynth.make_cache(**cfg, workers=min(16, os.cpu_count() or 1))
     if args.rope_post > 1.0:
         for l in range(Knp.shape[0]):
             xr = kvsynth.apply_rope(kvsynth.bf16_bits_to_f32(Knp[l]) if cfg["dtype"] == "bf16" else Knp[l],
