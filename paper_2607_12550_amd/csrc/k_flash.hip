@@ -300,6 +300,28 @@ hipError_t launch_sketch(const SketchArgs &a, int n_cells, hipStream_t st) {
 
 int gram64_tile() { return GT; }
 
+// Split-K partial Grams (lower-triangle tiles of each row chunk's product, chunk t of cell c
+// at part[(c * n_split + t) * l * l]) summed in chunk order in fp64 into the full symmetric
+// fp64 Gram the Cholesky reads
+__global__ void k_sum_gram_parts(const float *part, double *G, int l, int n_split, int n_cells) {
+  const int64_t ll = (int64_t)l * l, total = ll * n_cells;
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < total; q += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t c = q / ll, e = q - c * ll;
+    const int i = (int)(e / l), j = (int)(e - (int64_t)i * l);
+    const float *p = part + c * n_split * ll + (int64_t)max(i, j) * l + min(i, j);
+    double s = 0.0;
+    for (int t = 0; t < n_split; ++t) s += (double)p[(int64_t)t * ll];
+    G[q] = s;
+  }
+}
+
+hipError_t launch_sum_gram_parts(const float *part, double *G, int l, int n_split, int n_cells, hipStream_t st) {
+  const int64_t total = (int64_t)l * l * n_cells;
+  hipLaunchKernelGGL(k_sum_gram_parts, dim3((unsigned)std::min<int64_t>((total + 255) / 256, 4096)), dim3(256), 0,
+                     st, part, G, l, n_split, n_cells);
+  return hipGetLastError();
+}
+
 hipError_t launch_widen_gram(const float *C, double *G, int l, int n_cells, hipStream_t st) {
   const int64_t total = (int64_t)l * l * n_cells;
   hipLaunchKernelGGL(k_widen_gram, dim3((unsigned)std::min<int64_t>((total + 255) / 256, 4096)), dim3(256), 0, st,

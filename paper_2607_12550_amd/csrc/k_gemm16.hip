@@ -13,7 +13,7 @@
 // (BM/2) x 64 = (BM/64) x 2 MFMA blocks; K tiles of 64.  Operands go global -> registers ->
 // LDS; the next K tile's loads are issued before the current tile is multiplied and their
 // registers are only read when they are stored to LDS, so the loads stay in flight during
-// the MFMAs.  When two LDS tiles fit (160 KB per CU) the next tile is stored into the
+// the MFMAs.  With two LDS buffers (see Lds for when) the next tile is stored into the
 // second buffer while the first is multiplied, with one barrier per step.  LDS keeps both
 // operands k-contiguous (rows of 64 + 8 bf16: conflict-free 16-byte fragment reads); an
 // operand whose memory layout is contiguous along M/N is transposed in registers (each
@@ -202,10 +202,13 @@ struct Addr {
   }
 };
 
+// Two LDS buffers are used when they fit in half the LDS (two workgroups per CU), or, for
+// the 256-row tiles, in all of it: one workgroup per CU with double buffering measured
+// faster than two single-buffered ones there, slower for the 128-row split-operand tiles.
 template <int BM, bool AS, bool BS>
 struct Lds {
   static constexpr int LA = BM * LDK * (AS ? 2 : 1), LB = BN * LDK * (BS ? 2 : 1);
-  static constexpr bool DB = 2 * 2 * (LA + LB) <= LDS_BYTES;   // two buffers fit
+  static constexpr bool DB = 2 * 2 * (LA + LB) <= (BM == 256 ? LDS_BYTES : LDS_BYTES / 2);
   uint16_t a[LA * (DB ? 2 : 1)];
   uint16_t b[LB * (DB ? 2 : 1)];
 };
@@ -490,9 +493,11 @@ bool gemm16_prepare(GemmProblem *probs, int n, int &ta, int &tb, bool &ak, bool 
     lower = lower || p.lower_only;
   }
   if (swap) { std::swap(ta, tb); std::swap(ak, bk); }
-  // 256-row tiles for split-operand products over long M (two LDS buffers still fit);
-  // 128 otherwise, and always for lower-triangle tables
-  bm = (tb == GT_F32 && ta == GT_BF16 && maxM >= 2048 && !lower) ? 256 : 128;
+  // 256-row tiles for split-operand products over long M whose bf16 operand is k-contiguous
+  // (two LDS buffers still fit); 128 otherwise (an m-contiguous bf16 operand is transposed
+  // on its way to LDS, and the 128-row tile then runs two workgroups per CU), and always for
+  // lower-triangle tables
+  bm = (tb == GT_F32 && ta == GT_BF16 && maxM >= 2048 && !lower && ak) ? 256 : 128;
   return true;
 }
 

@@ -311,6 +311,8 @@ int gram64_tile();
 hipError_t launch_gram64(const Gram64Args &a, int n_cells, hipStream_t st);
 // G[cell] = (double) C[cell], both [cell][l][l]
 hipError_t launch_widen_gram(const float *C, double *G, int l, int n_cells, hipStream_t st);
+// sum of n_split partial lower-triangle Grams per cell into the full symmetric fp64 Gram
+hipError_t launch_sum_gram_parts(const float *part, double *G, int l, int n_split, int n_cells, hipStream_t st);
 
 struct CholArgs {
   double *G;                // [cell][l][l] in: Gram (lower); out: Cholesky factor L (lower)

@@ -17,6 +17,7 @@ constexpr int KC = 256;   // inverse-iteration columns per launch (bounds its sc
 constexpr int SYTRD_SMALL_MAX = 768;   // larger matrices use the blocked multi-workgroup kernel
 constexpr int SYTRD_NB = 32;
 constexpr int kG64Rows = 8192;          // rows per split-K chunk of the fp64 sketch Gram
+constexpr int kGramSplitMax = 16;       // row chunks of the second CholeskyQR pass's Gram
 
 struct Carver {
   uint8_t *base;
@@ -104,7 +105,9 @@ void plan(Carver &cv, Ws &w, const SpecShape &sh, int nc) {
   const int nmax = std::max({T, d, sh.ell});
   w.tab_n = 8192 + backtransform_table_entries(nc, nmax) + 4 * (size_t)nc * m +
             sytrd_large_table_entries(nc, nmax, SYTRD_NB);
-  if (sh.method == JOLT_FLASH) w.tab_n += (size_t)nc * 160;   // sketch, power and CholeskyQR2 products
+  // sketch, power and CholeskyQR2 products (up to 33 orthonormalisations, each with a
+  // split-K Gram of up to kGramSplitMax chunks per cell)
+  if (sh.method == JOLT_FLASH) w.tab_n += (size_t)nc * (160 + 33 * kGramSplitMax);
   w.tab = cv.take<GemmProblem>(w.tab_n);
   w.rcell = cv.take<ResidCell>(nc);
   w.dcell = cv.take<DecodeCell>(nc);
@@ -439,18 +442,28 @@ int orth(Run &R, const SpecShape &sh, int nc, float *buf, float *tmp, int rows, 
   float *src = buf, *dst = tmp;
   for (int pass = 0; pass < 2; ++pass) {
     if (split && pass == 1) {
-      std::vector<GemmProblem> G(nc);
-      for (int c = 0; c < nc; ++c) {
-        GemmProblem &p = G[c];
-        p = GemmProblem{};
-        p.A = plain(src + (int64_t)c * rows * ldl, ldl);             // Y^T: m-contiguous
-        p.B = plain(src + (int64_t)c * rows * ldl, ldl);             // Y: n-contiguous
-        p.C = R.w.C + (int64_t)c * l * l; p.ldc = l;
-        p.M = l; p.N = l; p.K = rows; p.alpha = 1.f;
-      }
+      // Y^T Y split over row chunks (only l x l outputs per cell: without the split too few
+      // workgroups would each run the whole row loop), lower-triangle tiles, into partial
+      // Grams kept in the fp64 Gram's partial area; summed in chunk order in fp64
+      const int S = std::max(1, std::min({kGramSplitMax, rows / 1024, 2 * R.w.g64_chunks}));
+      const int Kc = ((rows + S - 1) / S + 63) / 64 * 64;
+      float *part = reinterpret_cast<float *>(R.w.g64p);
+      std::vector<GemmProblem> G;
+      G.reserve((size_t)nc * S);
+      for (int c = 0; c < nc; ++c)
+        for (int t = 0; t < S; ++t) {
+          const int k0 = t * Kc, kn = std::max(0, std::min(Kc, rows - k0));
+          GemmProblem p{};
+          const float *y = src + (int64_t)c * rows * ldl + (int64_t)std::min(k0, rows - 1) * ldl;
+          p.A = plain(y, ldl);                                       // Y^T rows chunk: m-contiguous
+          p.B = plain(y, ldl);                                       // Y: n-contiguous
+          p.C = part + ((int64_t)c * S + t) * l * l; p.ldc = l;
+          p.M = l; p.N = l; p.K = kn; p.alpha = 1.f; p.lower_only = 1;
+          G.push_back(p);
+        }
       int rc = R.gemm(G, 2, GT_F32, GT_F32, false, false);
       if (rc) return rc;
-      HIP_OK(launch_widen_gram(R.w.C, R.w.g64, l, nc, R.st));
+      HIP_OK(launch_sum_gram_parts(part, R.w.g64, l, S, nc, R.st));
     } else {
       Gram64Args g{};
       g.Y = src; g.y_cell_stride = (int64_t)rows * ldl; g.ld = ldl;
