@@ -87,6 +87,109 @@ __global__ void __launch_bounds__(256) k_fgram(FGramArgs a) {
   }
 }
 
+// bf16 cells with d = 128: the same partials on the bf16 matrix cores.  Each stage takes 64
+// rows; thread (row group g = tid / 16, feature block f = tid % 16) loads rows 4g .. 4g+3,
+// features 8f .. 8f+7 (16-byte loads), adds their squares to the fp64 energy, and stores them
+// transposed into LDS as xt[feature][row] (four rows of one feature per 8-byte store; the
+// features are visited in a lane-dependent order so the stores spread over the banks).
+// Wave (wm, wn) then accumulates the 64 x 64 block (wm, wn) of F with 2 x 2
+// v_mfma_f32_32x32x16_bf16 per 16 rows.  The products of bf16 values are exact in fp32, so
+// only the fp32 accumulation order differs from the vector kernel.
+constexpr int FR = 64, FLD = FR + 8;
+
+__global__ void __launch_bounds__(256) k_fgram_mfma128(FGramArgs a) {
+  typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+  typedef float f32x16_t __attribute__((ext_vector_type(16)));
+  constexpr int D = 128;
+  __shared__ __attribute__((aligned(16))) uint16_t xt[D * FLD];
+  const int cell = blockIdx.y, chunk = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1, lr = lane & 31, lh = lane >> 5;
+  const int fb = tid & 15, rg = tid >> 4;
+  const int rps = a.cells[cell].rows_per_seg;
+  const int64_t total = (int64_t)a.nseg * rps;
+  const int64_t r0 = total * chunk / a.chunks_per_cell, r1 = total * (chunk + 1) / a.chunks_per_cell;
+  const uint16_t *base = reinterpret_cast<const uint16_t *>(a.cells[cell].base);
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
+  double e = 0.0;
+  int bad = 0;
+  for (int64_t rb = r0; rb < r1; rb += FR) {
+    const int64_t row0 = rb + rg * 4;
+    int s = 0, r = 0;
+    if (row0 < r1) { s = (int)(row0 / rps); r = (int)(row0 - (int64_t)s * rps); }
+    ju4 u[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (row0 + k < r1) {
+        const uint16_t *p = base + (int64_t)(s / a.seg_heads) * a.seg_hi + (int64_t)(s % a.seg_heads) * a.seg_lo +
+                            (int64_t)r * a.row_stride + fb * 8;
+        u[k] = gload_u4(p);
+      } else {
+        u[k] = ju4{0u, 0u, 0u, 0u};
+      }
+      if (++r == rps) { r = 0; ++s; }
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float lo = bf16_to_f32((bf16_t)(u[k][w] & 0xffffu)), hi = bf16_to_f32((bf16_t)(u[k][w] >> 16));
+        e += (double)lo * (double)lo;
+        e += (double)hi * (double)hi;
+        bad |= (int)!isfinite(lo) | (int)!isfinite(hi);
+      }
+    __syncthreads();                      // the previous stage's fragments have been read
+#pragma unroll
+    for (int ii = 0; ii < 8; ++ii) {
+      const int i = (ii + fb) & 7, w = i >> 1, sh = 16 * (i & 1);
+      const uint32_t h0 = (u[0][w] >> sh) & 0xffffu, h1 = (u[1][w] >> sh) & 0xffffu;
+      const uint32_t h2 = (u[2][w] >> sh) & 0xffffu, h3 = (u[3][w] >> sh) & 0xffffu;
+      *reinterpret_cast<uint2 *>(xt + (fb * 8 + i) * FLD + rg * 4) = make_uint2(h0 | (h1 << 16), h2 | (h3 << 16));
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < FR / 16; ++ks) {
+      const int ko = ks * 16 + 8 * lh;
+      bf16x8_t fa[2], fbv[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        fa[t] = *reinterpret_cast<const bf16x8_t *>(xt + (wm * 64 + t * 32 + lr) * FLD + ko);
+        fbv[t] = *reinterpret_cast<const bf16x8_t *>(xt + (wn * 64 + t * 32 + lr) * FLD + ko);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fbv[j], acc[i][j], 0, 0, 0);
+    }
+  }
+  // acc[i][j][q] is F at row wm*64 + i*32 + 8*(q/4) + 4*lh + q%4, column wn*64 + j*32 + lr
+  float *pf = a.partial_F + ((int64_t)cell * a.chunks_per_cell + chunk) * D * D;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q)
+        pf[(wm * 64 + i * 32 + 8 * (q >> 2) + 4 * lh + (q & 3)) * D + wn * 64 + j * 32 + lr] = acc[i][j][q];
+  __shared__ double es[4];
+  __shared__ int bs[4];
+  double ew = wave_sum(e);
+  int bw = __any(bad) ? 1 : 0;
+  if (lane == 0) { es[wave] = ew; bs[wave] = bw; }
+  __syncthreads();
+  if (tid == 0) {
+    a.partial_E[(int64_t)cell * a.chunks_per_cell + chunk] = es[0] + es[1] + es[2] + es[3];
+    if (bs[0] | bs[1] | bs[2] | bs[3]) atomicOr(&a.nonfinite[cell], 1);
+  }
+}
+
 __global__ void k_fgram_reduce(FGramArgs a, int D, float *F_out, double *E_out) {
   const int cell = blockIdx.y;
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -236,6 +339,10 @@ hipError_t launch_slice_gram_reduce(const SliceGramArgs &a, float *S_out, hipStr
 
 hipError_t launch_feature_gram(const FGramArgs &a, int d, int dtype, hipStream_t st) {
   dim3 grid(a.chunks_per_cell, a.n_cells);
+  if (d == 128 && dtype == 1 && a.vec16) {
+    hipLaunchKernelGGL(k_fgram_mfma128, grid, dim3(256), 0, st, a);
+    return hipGetLastError();
+  }
 #define L_(D_) \
   if (d == D_) { \
     if (dtype == 1) hipLaunchKernelGGL((k_fgram<D_, uint16_t>), grid, dim3(256), 0, st, a); \

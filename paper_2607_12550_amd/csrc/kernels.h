@@ -150,6 +150,7 @@ struct FGramArgs {
   int32_t n_cells, nseg, seg_heads;
   int64_t seg_hi, seg_lo, row_stride;
   int32_t chunks_per_cell;  // work items per cell (each a contiguous run of rows)
+  int32_t vec16;            // set by the caller: every row start is 16-byte aligned
   float *partial_F;         // [n_cells][chunks][d][d]
   double *partial_E;        // [n_cells][chunks]
   int32_t *nonfinite;       // [n_cells]

@@ -333,6 +333,9 @@ int feature_stage(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int n
   a.partial_F = R.w.fpart;
   a.partial_E = R.w.epart;
   a.nonfinite = R.w.nonfinite;
+  // 16-byte row loads: 8-element aligned strides and 16-byte aligned cell bases
+  a.vec16 = desc->stride_layer % 8 == 0 && desc->stride_head % 8 == 0 && desc->stride_token % 8 == 0;
+  for (int c = 0; c < nc; ++c) a.vec16 = a.vec16 && (reinterpret_cast<uintptr_t>(X[c]) % 16 == 0);
   {
     StageTimer t(R.ctx, R.st, JOLT_STAGE_FEATURE_GRAM);
     HIP_OK(launch_feature_gram(a, sh.d, desc->dtype, R.st));
