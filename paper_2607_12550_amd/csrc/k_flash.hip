@@ -32,8 +32,23 @@ __global__ void k_sketch(SketchArgs a) {
 }
 
 // partial fp64 Gram of a row chunk: Gp[cell][chunk] += Y[rows]^T Y[rows] for the 64 x 64
-// output tile (ti, tj), ti >= tj (lower tiles only; the Cholesky reads the lower triangle)
+// output tile (ti, tj), ti >= tj (lower tiles only; the Cholesky reads the lower triangle).
+// Each thread loads two 4-column runs of both 32 x 64 operand blocks; the next block's loads
+// are issued before the current block is multiplied, so their latency overlaps the fp64
+// multiply-adds.
 constexpr int GT = 64, GR = 32;
+
+// four consecutive entries of row r from column c (zero at and beyond column l)
+JOLT_DEV jf4 gram64_load4(const float *Y, int64_t ld, int64_t r, bool row_ok, int c, int l) {
+  if (!row_ok || c >= l) return jf4{0.f, 0.f, 0.f, 0.f};
+  const float *p = Y + r * ld + c;
+  if (c + 4 <= l && ((reinterpret_cast<uintptr_t>(p) & 15) == 0)) return gload_f4(p);
+  float v[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) v[e] = c + e < l ? p[e] : 0.f;
+  return jf4{v[0], v[1], v[2], v[3]};
+}
+
 __global__ void __launch_bounds__(256) k_gram64(Gram64Args a) {
   const int cell = blockIdx.z, chunk = blockIdx.y;
   int t = blockIdx.x, ti = 0;
@@ -49,16 +64,28 @@ __global__ void __launch_bounds__(256) k_gram64(Gram64Args a) {
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+  // staging: thread (ty, tx) moves rows ty and ty + 16, columns 4 tx .. 4 tx + 3 of each block
+  jf4 pa[2], pb[2];
+  auto fetch = [&](int64_t rb) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int64_t r = rb + ty + 16 * h;
+      pa[h] = gram64_load4(Y, a.ld, r, r < r1, ti * GT + 4 * tx, l);
+      pb[h] = gram64_load4(Y, a.ld, r, r < r1, tj * GT + 4 * tx, l);
+    }
+  };
+  if (r0 < r1) fetch(r0);
   for (int64_t rb = r0; rb < r1; rb += GR) {
     __syncthreads();
-    for (int q = tid; q < GR * GT; q += 256) {
-      const int rr = q / GT, cc = q % GT;
-      const int64_t r = rb + rr;
-      const int ca = ti * GT + cc, cb = tj * GT + cc;
-      ya[rr][cc] = (r < r1 && ca < l) ? Y[r * a.ld + ca] : 0.f;
-      yb[rr][cc] = (r < r1 && cb < l) ? Y[r * a.ld + cb] : 0.f;
-    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        ya[ty + 16 * h][4 * tx + e] = pa[h][e];
+        yb[ty + 16 * h][4 * tx + e] = pb[h][e];
+      }
     __syncthreads();
+    if (rb + GR < r1) fetch(rb + GR);
 #pragma unroll 4
     for (int rr = 0; rr < GR; ++rr) {
       double va[4], vb[4];
