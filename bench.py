@@ -113,7 +113,8 @@ def stage_work(codec, calls):
         # lower triangle of every trailing matrix, one read per column (fp32)
         sym_bytes = nc * sum(4.0 * Lr * (Lr + 1) / 2 for Lr in range(1, n))
         work["symv"] = ("hbm", sym_bytes * calls)
-        work["token_gram"] = (cache_mfma, nc * 2.0 * T * T * N * calls)
+        # symmetric rank-N update: T (T + 1) N flops (the syrk count; only lower tiles are formed)
+        work["token_gram"] = (cache_mfma, nc * 1.0 * T * (T + 1) * N * calls)
         work["project"] = (cache_mfma, sum(2.0 * r * T * N for r in rT) * calls)
     if codec.tau == "exact":
         # the truncated spectra: Y at the grid's largest r_T (a second projection), then the

@@ -463,6 +463,9 @@ hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, const Gemm
   a.slots = (n + TB - 1) / TB;
   const int panels = (n - 1 + nb - 1) / nb;
   hipError_t err = hipSuccess;
+  // only the lower triangle (and the diagonal tiles) of the input is read: the upper part of
+  // the first panel's rows is restored from it here, that of later panels after each update
+  hipLaunchKernelGGL(k_mirror_strip, dim3((n + 63) / 64, nm), dim3(256), 0, st, a, 0);
   for (int p = 0; p < panels; ++p) {
     const int k0 = p * nb, jb = std::min(nb, n - 1 - k0);
     hook(JOLT_STAGE_PANEL, 1);

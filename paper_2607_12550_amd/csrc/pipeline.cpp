@@ -356,6 +356,9 @@ int token_exact(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc,
     p.ldc = sh.T;
     p.M = sh.T; p.N = sh.T; p.K = sh.N;
     p.alpha = 1.f; p.beta = 0.f;
+    // the blocked tridiagonalisation reads the lower triangle (it restores the upper part of
+    // each panel's rows itself), so only the lower tiles of the symmetric Gram are formed
+    p.lower_only = sh.T > SYTRD_SMALL_MAX ? 1 : 0;
   }
   const int mode = desc->dtype == JOLT_BF16 ? 0 : 1;
   {
