@@ -44,6 +44,11 @@ class JoltError(RuntimeError):
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2607_12550_amd/build.py` "
                       "(or __graft_entry__.build())")
+# torch ships its own HIP runtime; loading it first makes the library bind to that same
+# runtime instance (loaded the other way round, the library's first HIP call can find no
+# device in a process where torch already uses the GPU)
+import torch  # noqa: E402,F401
+
 lib = C.CDLL(LIB_PATH)
 
 
