@@ -171,15 +171,21 @@ __global__ void __launch_bounds__(CB) k_chol_diag(CholArgs a, int kb) {
   for (int c = 0; c < CB; ++c)        // zeros outside the matrix, identity on the padding
     t[c] = (lane < nb && c < nb) ? G[(int64_t)(o + lane) * l + o + c] : (c == lane && lane >= nb ? 1.0 : 0.0);
   const double floor_piv = fmax(1e-14 * sdmax, 1e-300);
+  // column j of the factor is broadcast through LDS (two alternating buffers, so one
+  // barrier per column): every lane reads the entries l_kj it needs with independent
+  // broadcast loads instead of one cross-lane shuffle pair per entry
+  __shared__ double colb[2][CB];
 #pragma unroll
   for (int j = 0; j < CB; ++j) {
     const double piv = sqrt(fmax(__shfl(t[j], j, 64), j < nb ? floor_piv : 1.0));
     if (lane > j) t[j] /= piv;
     else if (lane == j) t[j] = piv;
     const double lij = t[j];
+    colb[j & 1][lane] = lij;
+    __syncthreads();
 #pragma unroll
     for (int k = j + 1; k < CB; ++k) {
-      const double lkj = __shfl(lij, k, 64);
+      const double lkj = colb[j & 1][k];
       if (lane >= k) t[k] = fma(-lij, lkj, t[k]);
     }
   }
