@@ -281,14 +281,30 @@ __global__ void __launch_bounds__(256) k_chol_inv_row(CholArgs a, int I) {
   __shared__ double ta[CB][CLD], tb[CB][CLD];
   const int r0 = (threadIdx.x >> 4) * 4, c0 = (threadIdx.x & 15) * 4;
   double acc[4][4] = {};
+  // the tiles of step K + 1 (L_I,K+1 and M_K+1,J) are loaded into registers while step K
+  // is multiplied; thread element h is entry (q / CB, q % CB), q = tid + 256 h, of each tile
+  constexpr int PE = CB * CB / 256;
+  double pa[PE], pb[PE];
+  auto fetch = [&](int K) {
+#pragma unroll
+    for (int h = 0; h < PE; ++h) {
+      const int q = threadIdx.x + 256 * h, i = q / CB, j = q % CB;
+      const int ra = I * CB + i, ca = K * CB + j, rb = K * CB + i, cb = J * CB + j;
+      pa[h] = (ra < l && ca < l) ? G[(int64_t)ra * l + ca] : 0.0;          // L_IK[i][j]
+      pb[h] = (rb < l && cb < l) ? M[(int64_t)rb * l + cb] : 0.0;          // M_KJ[i][j]
+    }
+  };
+  if (J < I) fetch(J);
   for (int K = J; K < I; ++K) {
     __syncthreads();
-    tile_load(ta, G, l, I * CB, K * CB);                  // L_IK
-    for (int q = threadIdx.x; q < CB * CB; q += 256) {    // M_KJ, transposed: tb[c][k] = M[k][c]
-      const int k = q / CB, c = q % CB, r = K * CB + k, cc = J * CB + c;
-      tb[c][k] = (r < l && cc < l) ? M[(int64_t)r * l + cc] : 0.0;
+#pragma unroll
+    for (int h = 0; h < PE; ++h) {
+      const int q = threadIdx.x + 256 * h, i = q / CB, j = q % CB;
+      ta[i][j] = pa[h];
+      tb[j][i] = pb[h];                                   // transposed: tb[c][k] = M_KJ[k][c]
     }
     __syncthreads();
+    if (K + 1 < I) fetch(K + 1);
     tile_mma_nt(acc, ta, tb, 0, CB);
   }
   __syncthreads();
