@@ -51,7 +51,17 @@ enum {
   JOLT_E_BLOB = -4,        /* corrupt or mismatched blob header */
   JOLT_E_HIP = -5,         /* HIP runtime error (message has the HIP error string) */
   JOLT_E_NONFINITE = -6,   /* input contains NaN or Inf */
-  JOLT_E_STATE = -7        /* call sequence error (e.g. stale spectrum reuse) */
+  JOLT_E_STATE = -7,       /* call sequence error (e.g. stale spectrum reuse) */
+  JOLT_E_NOCONV = -8       /* a solver missed its accuracy check (outputs then unreliable):
+                              inverse iteration left an eigenvector whose solution growth
+                              |(T - lambda I)^-1 x|_inf |T| stayed below 1e4 sqrt(n) (residual
+                              above 1e-4 |T|), or, in a cell of nonzero energy, the second
+                              pass of a FlashJoLT CholeskyQR2 met a pivot below its floor
+                              although the first pass met none (the first pass lost rank:
+                              its output is orthonormal in exact arithmetic).  Clamped pivots
+                              of a first pass are the designed treatment of a rank-deficient
+                              sketch (the missing directions get zero Ritz values) and are not
+                              an error. */
 };
 
 enum { JOLT_F32 = 0, JOLT_BF16 = 1 };            /* element types of caches and outputs */
@@ -86,7 +96,11 @@ typedef struct {
                           for these same cells, options and seeds (JOLT_E_STATE if the
                           context recorded none); the caller guarantees that the workspace
                           was neither written nor freed since.  0: compute it. */
-  int32_t reserved;
+  int32_t r_max;       /* widest token factor kept (section 4 keeps the top token
+                          eigenvectors up to the largest admissible r_T): 0 = min(T, m d)
+                          (exact) or q (FlashJoLT); > 0 caps it, so r_T <= r_max and the
+                          workspace shrinks accordingly.  The eigenvalues returned are
+                          unaffected (exact: all T; FlashJoLT: q and the tail). */
 } jolt_spectrum_opts;
 
 /* Per-cell compression parameters. */
@@ -192,15 +206,20 @@ int jolt_decompress_workspace_size(const jolt_cell_desc *out_desc, int n_cells, 
  *           jolt_eps2_calibrate) first drops the record.
  * Synchronises the stream (the outputs are host arrays).  Errors: JOLT_E_INVAL
  * (null/misaligned pointers), JOLT_E_WORKSPACE, JOLT_E_NONFINITE (a cell holds NaN or
- * Inf; outputs then undefined), JOLT_E_UNSUPPORTED, JOLT_E_HIP. */
+ * Inf; outputs then undefined), JOLT_E_NOCONV (see its definition), JOLT_E_UNSUPPORTED,
+ * JOLT_E_HIP. */
 int jolt_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_cells, const void *const *X,
                   const uint64_t *seeds, const jolt_spectrum_opts *opts, void *ws, size_t ws_bytes,
                   double *E, double *lam_T, double *lam_d, jolt_stream stream);
 
-/* Bytes of one cell's blob: a 128-byte header, then 256-byte aligned sections
+/* Bytes of one cell's blob: eq. (1)'s payload (the factors at c bytes per scalar, with
+ * c = 2 for the fp16 serialisation of section 9, and b/8 bytes per residual entry) plus
+ * what the format adds to it: a 128-byte header, 256-byte alignment of every section, the
+ * m int8 core exponents and the fp16 group scales (2 bytes per g entries).  Sections:
  * U_T (T x r_T), U_d (d x r_d), G (m x r_T x r_d) at c bytes per scalar (fp16 or fp32,
- * row-major), m int8 core exponents (fp16 cores are stored as G_s / 2^e_s), fp16
- * group scales (m*T*d/g) and the b-bit codes (m*T*d*b/8 bytes, packed LSB first). */
+ * row-major), the core exponents (fp16 cores are stored as G_s / 2^e_s), the scales
+ * (m*T*d/g) and the b-bit codes (m*T*d*b/8 bytes, packed LSB first).  Errors:
+ * JOLT_E_INVAL / JOLT_E_UNSUPPORTED for a bad descriptor or parameters. */
 int jolt_compressed_size(const jolt_cell_desc *desc, const jolt_params *params, size_t *bytes);
 
 /* Compresses every cell into its blob (section 4): ST-HOSVD truncation to (r_T, r_d)
@@ -210,8 +229,11 @@ int jolt_compressed_size(const jolt_cell_desc *desc, const jolt_params *params, 
  *   params  host, n_cells; group and factor_dtype must be equal across the call.
  *   blobs   device pointers (256-byte aligned) to blob_bytes[i] >= jolt_compressed_size
  *           bytes each; written completely (header included), owned by the caller.
- * Asynchronous on the stream.  Errors: as jolt_spectrum, plus JOLT_E_WORKSPACE for a
- * short blob and JOLT_E_INVAL for ranks above jolt_spectrum_len's rT_max. */
+ * Synchronises the stream before returning, to read the input and solver checks
+ * (JOLT_E_NONFINITE when the call computed the spectrum itself and a cell holds NaN or
+ * Inf; JOLT_E_NOCONV; the blobs are then undefined).  Errors: as jolt_spectrum, plus
+ * JOLT_E_WORKSPACE for a short blob and JOLT_E_INVAL for ranks above jolt_spectrum_len's
+ * rT_max. */
 int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_cells, const void *const *X,
                   const jolt_params *params, const jolt_spectrum_opts *opts, void *ws,
                   size_t ws_bytes, void *const *blobs, const size_t *blob_bytes,
@@ -286,8 +308,8 @@ int jolt_eps2_calibrate(jolt_ctx *ctx, int group, int d, uint64_t seed, int n_sa
  *         owned by the caller; its first jolt_workspace_size bytes are laid out as the
  *         spectrum workspace of the same cells, so a spectrum reused from it must have
  *         been computed with this same ws and ws_bytes.
- * Synchronises the stream.  Errors: as jolt_spectrum, plus JOLT_E_INVAL for step or n_r
- * out of range. */
+ * Synchronises the stream.  Errors: as jolt_spectrum (JOLT_E_NONFINITE when the call
+ * computed the spectrum itself), plus JOLT_E_INVAL for step or n_r out of range. */
 int jolt_truncated_spectra_workspace_size(const jolt_cell_desc *desc, int n_cells,
                                           const jolt_spectrum_opts *opts, int step, int n_r,
                                           size_t *bytes);
@@ -357,16 +379,27 @@ int jolt_attend(jolt_ctx *ctx, int n_items, const void *const *k_blobs, const si
 int jolt_debug_export(jolt_ctx *ctx, int what, int cell, void *dst, size_t dst_bytes,
                       jolt_stream stream);
 
+/* Test hook: forces a solver condition from the host so that the JOLT_E_NOCONV path can be
+ * exercised with inputs on which the solvers succeed.  JOLT_DBG_INVIT_ITERS sets the number
+ * of inverse-iteration sweeps of later calls on this context (default 2, range 0..8; with
+ * 0 no sweep runs and the growth check fails).  Errors: JOLT_E_INVAL. */
+enum { JOLT_DBG_INVIT_ITERS = 0 };
+int jolt_debug_set(jolt_ctx *ctx, int what, int64_t value);
+
 /* Benchmark instrumentation.  When enabled, the library brackets the kernels of each
- * stage below with HIP events recorded on the call's stream; jolt_profile_read waits
- * for the recorded events and returns the device time (ms) accumulated since the last
- * reset and the number of bracketed launches.  Disabled by default (no events). */
+ * stage below with one pair of HIP events per stage and call, recorded on the call's
+ * stream; jolt_profile_read waits for the recorded events and returns the device time (ms)
+ * accumulated since the last reset and the number of bracketed intervals.  At most 4096
+ * intervals are kept pending: beyond that the oldest are read (a host wait).  Disabled by
+ * default (no events). */
 enum {
   JOLT_STAGE_FEATURE_GRAM = 0, /* E and F = sum_s X_s^T X_s (and F_Y during ST-HOSVD) */
   JOLT_STAGE_TOKEN_GRAM,       /* C = X_(2) X_(2)^T */
-  JOLT_STAGE_SYMV,             /* tridiagonalisation: trailing symmetric mat-vec tiles */
-  JOLT_STAGE_PANEL,            /* tridiagonalisation: per-column vector work */
-  JOLT_STAGE_PANEL_GEMM,       /* tridiagonalisation: rank-2k trailing updates */
+  JOLT_STAGE_TRIDIAG_LARGE,    /* blocked tridiagonalisation of token Grams with T > 768 (mat-vec
+                                  tiles, per-column kernels and rank-2k updates, replayed as one
+                                  graph and timed as a whole) */
+  JOLT_STAGE_RESERVED_3,       /* not recorded */
+  JOLT_STAGE_RESERVED_4,       /* not recorded */
   JOLT_STAGE_TRIDIAG_SMALL,    /* one-workgroup tridiagonalisation (small n) */
   JOLT_STAGE_EIGVALS,          /* fp64 bisection */
   JOLT_STAGE_EIGVECS,          /* fp64 inverse iteration + cluster re-orthogonalisation */

@@ -162,6 +162,9 @@ def serialize(U: np.ndarray, U_d: np.ndarray, G: np.ndarray, factor_bytes: int):
     """Round factors to the stored precision; fp16 cores get one exponent per slice.
 
     Returns (U_hat, Ud_hat, G_hat, gexp) with G_s = G_hat_s * 2^gexp[s] up to rounding.
+    The exponent is e_s = max(-128, ceil(log2 max|G_s|) - 15) (0 for an all-zero slice):
+    the blob keeps it in one signed byte, and the floor only matters for cores below
+    2^-113, whose scaled values then stay below 2^15 as well.
     """
     m = G.shape[0]
     gexp = np.zeros(m, dtype=np.int64)
@@ -172,7 +175,7 @@ def serialize(U: np.ndarray, U_d: np.ndarray, G: np.ndarray, factor_bytes: int):
     G_hat = np.empty_like(G)
     for s in range(m):
         M = float(np.max(np.abs(G[s]))) if G[s].size else 0.0
-        e = ceil_log2(M) - 15 if M > 0.0 else 0
+        e = max(-128, ceil_log2(M) - 15) if M > 0.0 else 0
         gexp[s] = e
         G_hat[s] = to_fp16(np.ldexp(G[s], -e))
     return to_fp16(U), to_fp16(U_d), G_hat, gexp

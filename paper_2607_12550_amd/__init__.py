@@ -22,7 +22,9 @@ __all__ = ["JoltError", "lib", "CellDesc", "SpectrumOpts", "Params", "CellSpectr
            "jolt_compress", "jolt_decompress", "jolt_allocate", "jolt_eps2_workspace_size",
            "jolt_eps2_calibrate", "jolt_slice_spectrum_workspace_size", "jolt_slice_spectrum",
            "jolt_mode_summary", "jolt_truncated_spectra_workspace_size", "jolt_truncated_spectra",
-           "jolt_attend_workspace_size", "jolt_attend", "jolt_debug_export", "jolt_profile_enable", "jolt_profile_reset",
+           "jolt_attend_workspace_size", "jolt_attend", "jolt_debug_export", "jolt_debug_set",
+           "jolt_profile_enable", "jolt_profile_reset", "JOLT_E_NONFINITE", "JOLT_E_NOCONV",
+           "JOLT_DBG_INVIT_ITERS",
            "jolt_profile_read", "STAGES", "cell_desc", "LIB_PATH", "HEADER_PATH"]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -30,6 +32,9 @@ LIB_PATH = os.path.join(HERE, "libjolt.so")
 HEADER_PATH = os.path.join(os.path.dirname(HERE), "include", "jolt.h")
 
 JOLT_OK, JOLT_F32, JOLT_BF16 = 0, 0, 1
+JOLT_E_INVAL, JOLT_E_UNSUPPORTED, JOLT_E_WORKSPACE, JOLT_E_BLOB = -1, -2, -3, -4
+JOLT_E_HIP, JOLT_E_NONFINITE, JOLT_E_STATE, JOLT_E_NOCONV = -5, -6, -7, -8
+JOLT_DBG_INVIT_ITERS = 0
 JOLT_EXACT, JOLT_FLASH = 0, 1
 JOLT_FACTOR_F32, JOLT_FACTOR_F16 = 0, 1
 HEADER_BYTES = 128
@@ -62,7 +67,7 @@ class CellDesc(C.Structure):
 class SpectrumOpts(C.Structure):
     _fields_ = [("method", C.c_int32), ("q", C.c_int32), ("ratio", C.c_double),
                 ("oversample", C.c_int32), ("power_iters", C.c_int32), ("reuse", C.c_int32),
-                ("reserved", C.c_int32)]
+                ("r_max", C.c_int32)]
 
 
 class Params(C.Structure):
@@ -123,6 +128,7 @@ _SIGS = {
     "jolt_truncated_spectra": (C.c_int, [_vp, _P(CellDesc), C.c_int, _P(_vp), _P(C.c_uint64),
                                          _P(SpectrumOpts), C.c_int, C.c_int, _vp, _sz, _P(_dbl), _vp]),
     "jolt_debug_export": (C.c_int, [_vp, C.c_int, C.c_int, _vp, _sz, _vp]),
+    "jolt_debug_set": (C.c_int, [_vp, C.c_int, C.c_int64]),
     "jolt_profile_enable": (C.c_int, [_vp, C.c_int]),
     "jolt_profile_reset": (C.c_int, [_vp]),
     "jolt_profile_read": (C.c_int, [_vp, C.c_int, _P(_dbl), _P(C.c_int64)]),
@@ -338,7 +344,7 @@ def jolt_eps2_calibrate(ctx, group: int, d: int, seed: int, n_samples: int, ws,
     return {0: out[0], 2: out[1], 4: out[2], 8: out[3]}
 
 
-STAGES = ["feature_gram", "token_gram", "symv", "panel", "panel_gemm", "tridiag_small", "eigvals",
+STAGES = ["feature_gram", "token_gram", "tridiag_large", "reserved3", "reserved4", "tridiag_small", "eigvals",
           "eigvecs", "backtransform", "project", "core", "serialize", "reconstruct", "residual",
           "decode", "sketch", "orth", "slice_gram", "attend", "trunc_gram"]
 
@@ -413,3 +419,7 @@ def jolt_attend(ctx, k_blobs, v_blobs, k_hdr, v_hdr, layers, Q, O, scale: float,
 def jolt_debug_export(ctx, what: int, cell: int, dst, stream=None) -> None:
     _check(lib.jolt_debug_export(ctx, what, cell, _addr(dst), dst.numel() * dst.element_size(),
                                  _stream(stream)))
+
+
+def jolt_debug_set(ctx, what: int, value: int) -> None:
+    _check(lib.jolt_debug_set(ctx, what, value))

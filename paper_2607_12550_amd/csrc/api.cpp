@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <memory>
 #include <string>
 #include <vector>
 
@@ -43,15 +44,14 @@ extern "C" int jolt_create(jolt_ctx **ctx, int device) {
   HIP_OK(hipGetDeviceCount(&ndev));
   if (device >= ndev) return jolt_fail(JOLT_E_INVAL, "jolt_create: device %d of %d", device, ndev);
   if (device < 0) HIP_OK(hipGetDevice(&device));
-  jolt_ctx *c = new jolt_ctx();
+  // owned until every check has passed: no path leaks the context or reads it after release
+  std::unique_ptr<jolt_ctx> c(new jolt_ctx());
   c->device = device;
   HIP_OK(hipGetDeviceProperties(&c->prop, device));
-  if (std::string(c->prop.gcnArchName).find("gfx950") == std::string::npos) {
-    delete c;
-    return jolt_fail(JOLT_E_UNSUPPORTED, "jolt_create: device arch %s is not gfx950",
-                     c->prop.gcnArchName);
-  }
-  *ctx = c;
+  const std::string arch(c->prop.gcnArchName);
+  if (arch.find("gfx950") == std::string::npos)
+    return jolt_fail(JOLT_E_UNSUPPORTED, "jolt_create: device arch %s is not gfx950", arch.c_str());
+  *ctx = c.release();
   return JOLT_OK;
 }
 
@@ -94,9 +94,12 @@ int resolve_spectrum(const jolt_cell_desc *d, const jolt_spectrum_opts *o, SpecS
   sh->d = d->d;
   sh->N = sh->m * d->d;
   sh->method = o ? o->method : JOLT_EXACT;
+  const int r_cap = o ? o->r_max : 0;
+  if (r_cap < 0) return jolt_fail(JOLT_E_INVAL, "r_max must be >= 0 (0 = no cap)");
   if (sh->method == JOLT_EXACT) {
     sh->n_lam_T = sh->T;
     sh->rT_max = std::min(sh->T, sh->N);
+    if (r_cap > 0) sh->rT_max = std::min(sh->rT_max, r_cap);
     sh->q = sh->ell = 0;
     if (sh->T > 8192)
       return jolt_fail(JOLT_E_UNSUPPORTED, "exact token spectrum limited to T <= 8192 (use FlashJoLT)");
@@ -112,7 +115,7 @@ int resolve_spectrum(const jolt_cell_desc *d, const jolt_spectrum_opts *o, SpecS
     sh->ell = std::min<int64_t>(std::min<int64_t>((int64_t)q + o->oversample, sh->T), sh->N);
     sh->q = std::min(q, sh->ell);
     sh->n_lam_T = sh->q + 1;
-    sh->rT_max = sh->q;
+    sh->rT_max = r_cap > 0 ? std::min(sh->q, r_cap) : sh->q;
     if (sh->ell > 1024) return jolt_fail(JOLT_E_UNSUPPORTED, "sketch width l must be <= 1024");
   } else {
     return jolt_fail(JOLT_E_INVAL, "method must be JOLT_EXACT or JOLT_FLASH");
@@ -216,6 +219,9 @@ int parse_header(const uint8_t *h, size_t blob_bytes, BlobInfo *bi) {
 }
 
 // ------------------------------------------------------------------------ profiling
+constexpr size_t kProfPendingMax = 4096;
+static int prof_drain(jolt_ctx *c);
+
 static hipEvent_t pool_get(jolt_ctx *c) {
   if (!c->prof_pool.empty()) {
     hipEvent_t e = c->prof_pool.back();
@@ -241,6 +247,8 @@ StageTimer::~StageTimer() {
   hipEvent_t b = pool_get(ctx);
   if (b && hipEventRecord(b, st) == hipSuccess) {
     ctx->prof_pending.push_back(ProfRecord{stage, a, b});
+    // bounded number of outstanding events: read the pending intervals (a host wait)
+    if (ctx->prof_pending.size() >= kProfPendingMax) (void)prof_drain(ctx);
   } else {
     ctx->prof_pool.push_back(a);
     if (b) ctx->prof_pool.push_back(b);

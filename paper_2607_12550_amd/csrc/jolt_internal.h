@@ -69,6 +69,7 @@ struct jolt_ctx {
   hipStream_t cap_stream = nullptr;
   hipGraphExec_t trd_exec = nullptr;
   std::vector<const void *> trd_key;
+  int invit_iters = 2;            // inverse-iteration sweeps (test hook jolt_debug_set)
   ~jolt_ctx();
 };
 

@@ -363,7 +363,8 @@ __global__ void __launch_bounds__(64) k_tri_eigvecs(EigBatch b, InvitWork w, int
   // stores), so the memory latency is paid once per block instead of once per step.  The
   // arithmetic of every step is unchanged.
   constexpr int IB = 8;
-  for (int it = 0; it < 2; ++it) {
+  double growth = 0.0;                 // max |x| after the last solve (its input has max |x| <= 1)
+  for (int it = 0; it < w.iters; ++it) {
     // forward: factor T - lam I = P L U while transforming the right-hand side in x
     double p = d[0] - lam, q = (n > 1) ? e[0] : 0.0;
     double y = x[0];
@@ -446,6 +447,7 @@ __global__ void __launch_bounds__(64) k_tri_eigvecs(EigBatch b, InvitWork w, int
         amax = fmax(amax, fabs(xi));
       }
     }
+    growth = amax;
     const double sc = amax > 0.0 ? 1.0 / amax : 1.0;
     for (int i0 = 0; i0 < n; i0 += IB) {
       double v[IB];
@@ -455,6 +457,9 @@ __global__ void __launch_bounds__(64) k_tri_eigvecs(EigBatch b, InvitWork w, int
       for (int s = 0; s < IB; ++s) if (i0 + s < n) x[(int64_t)(i0 + s) * ld] = v[s] * sc;
     }
   }
+  // convergence: the normalised vector z = y / |y| has residual |(T - lam I) z|_2 <=
+  // sqrt(n) / |y|_inf, so a growth of at least 1e4 sqrt(n) / |T| bounds it by 1e-4 |T|
+  if (!(growth * tnorm >= 1e4 * sqrt((double)n))) w.status[mat] = 1;
   double nrm = 0.0;
   for (int i0 = 0; i0 < n; i0 += IB) {
     double v[IB];

@@ -132,7 +132,8 @@ __global__ void k_widen_gram(const float *C, double *G, int l, int n_cells) {
 // (D_kb = L_kb,kb^-1), k_chol_panel forms L_I,kb = G_I,kb D_kb^T below it and
 // k_chol_update subtracts L_I,kb L_J,kb^T from the trailing lower tiles.  The inverse
 // is then built one block row at a time: M_IJ = -D_I sum_{J<=K<I} L_IK M_KJ.
-// Pivots below 1e-14 of the largest diagonal entry of G are raised to that floor.
+// Pivots below 1e-14 of the largest diagonal entry of G are raised to that floor and
+// counted per cell (CholArgs::clamped).
 constexpr int CB = 64, CLD = CB + 1;
 
 JOLT_DEV void tile_load(double (*t)[CLD], const double *A, int l, int r0, int c0) {
@@ -171,13 +172,16 @@ __global__ void __launch_bounds__(CB) k_chol_diag(CholArgs a, int kb) {
   for (int c = 0; c < CB; ++c)        // zeros outside the matrix, identity on the padding
     t[c] = (lane < nb && c < nb) ? G[(int64_t)(o + lane) * l + o + c] : (c == lane && lane >= nb ? 1.0 : 0.0);
   const double floor_piv = fmax(1e-14 * sdmax, 1e-300);
+  int n_clamped = 0;                   // pivots of this tile raised to the floor
   // column j of the factor is broadcast through LDS (two alternating buffers, so one
   // barrier per column): every lane reads the entries l_kj it needs with independent
   // broadcast loads instead of one cross-lane shuffle pair per entry
   __shared__ double colb[2][CB];
 #pragma unroll
   for (int j = 0; j < CB; ++j) {
-    const double piv = sqrt(fmax(__shfl(t[j], j, 64), j < nb ? floor_piv : 1.0));
+    const double raw = __shfl(t[j], j, 64);
+    n_clamped += (j < nb && !(raw >= floor_piv)) ? 1 : 0;
+    const double piv = sqrt(fmax(raw, j < nb ? floor_piv : 1.0));
     if (lane > j) t[j] /= piv;
     else if (lane == j) t[j] = piv;
     const double lij = t[j];
@@ -191,6 +195,8 @@ __global__ void __launch_bounds__(CB) k_chol_diag(CholArgs a, int kb) {
   }
 #pragma unroll
   for (int c = 0; c < CB; ++c) ts[lane][c] = t[c];
+  // clamp count of the whole factorisation: reset by the first block column's launch
+  if (lane == 0 && a.clamped) a.clamped[cell] = (kb == 0 ? 0 : a.clamped[cell]) + n_clamped;
   __syncthreads();
   // column `lane` of the inverse of the lower-triangular factor
   double inv[CB];

@@ -1,7 +1,9 @@
 // Factor serialisation into the blob (eq. (1) prices factors at c bytes per scalar;
 // section 9 uses fp16).  Each core slice G_s gets a power-of-two exponent
-// e_s = ceil(log2 max|G_s|) - 15 so that the stored fp16 values keep full precision
-// and stay below 2^15; fp32 factors are copied unchanged with e_s = 0.
+// e_s = max(-128, ceil(log2 max|G_s|) - 15) (0 for an all-zero slice) so that the stored
+// fp16 values keep full precision and stay below 2^15; the floor keeps e_s in the blob's
+// signed byte (it only binds for cores below 2^-113).  fp32 factors are copied unchanged
+// with e_s = 0.
 #include "common.h"
 #include "kernels.h"
 
@@ -39,7 +41,7 @@ __global__ void __launch_bounds__(256) k_core_pack(SerCore a) {
   __syncthreads();
   mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   int e = 0;
-  if (c.f16 && mx > 0.f) e = ceil_log2_f(mx) - 15;
+  if (c.f16 && mx > 0.f) e = max(-128, ceil_log2_f(mx) - 15);
   if (threadIdx.x == 0) c.gexp[s] = (int8_t)e;
   const float sc = ldexpf(1.f, -e);
   for (int q = threadIdx.x; q < rT * rd; q += 256) {

@@ -447,7 +447,7 @@ void sytrd_large_tables(const EigBatch &b, float *work, int nb, GemmProblem *tab
 }
 
 hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, const GemmProblem *tab_dev,
-                              hipStream_t st, const LaunchHook &hook, int m0, int m1) {
+                              hipStream_t st, int m0, int m1) {
   // matrices m0 .. m1-1 of the batch (all by default)
   const int n = b.n;
   if (m1 < 0) m1 = b.n_mat;
@@ -468,28 +468,20 @@ hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, const Gemm
   hipLaunchKernelGGL(k_mirror_strip, dim3((n + 63) / 64, nm), dim3(256), 0, st, a, 0);
   for (int p = 0; p < panels; ++p) {
     const int k0 = p * nb, jb = std::min(nb, n - 1 - k0);
-    hook(JOLT_STAGE_PANEL, 1);
     hipLaunchKernelGGL(k_col_next, dim3((n - k0 + RB - 1) / RB, nm), dim3(RB), 0, st, a, -1, 0, k0, 0, 1, jb);
-    hook(JOLT_STAGE_PANEL, 0);
     for (int j = 0; j < jb; ++j) {
       const int i = k0 + j, o = i + 1, L = n - o;
       const int nt = (n - (o & ~31) + TB - 1) / TB, nblk = (L + RB - 1) / RB;
-      hook(JOLT_STAGE_SYMV, 1);
       hipLaunchKernelGGL(k_symv_tiles, dim3(nt * (nt + 1) / 2, nm), dim3(256), 0, st, a, i);
-      hook(JOLT_STAGE_SYMV, 0);
-      hook(JOLT_STAGE_PANEL, 1);
       hipLaunchKernelGGL(k_col_finish, dim3(nblk, nm), dim3(RB), 0, st, a, i, j, jb);
       const bool more = j + 1 < jb;
       hipLaunchKernelGGL(k_col_next, dim3(nblk, nm), dim3(RB), 0, st, a, i, j, more ? i + 1 : n, j + 1, 0, jb);
-      hook(JOLT_STAGE_PANEL, 0);
     }
     const int s = k0 + jb;
     if (s < n) {
-      hook(JOLT_STAGE_PANEL_GEMM, 1);
       err = launch_gemm(tab_dev + (size_t)p * b.n_mat + m0, nm, n - s, n - s, 1, GT_F32, GT_F32, false, false, st);
       if (err != hipSuccess) return err;
       hipLaunchKernelGGL(k_mirror_strip, dim3((n - s + 63) / 64, nm), dim3(256), 0, st, a, s);
-      hook(JOLT_STAGE_PANEL_GEMM, 0);
     }
   }
   hipLaunchKernelGGL(k_sytrd_finish, dim3(nm), dim3(64), 0, st, a);

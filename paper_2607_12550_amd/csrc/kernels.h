@@ -7,14 +7,6 @@
 
 #include "../../include/jolt.h"
 
-// Optional per-launch instrumentation: fn(user, stage, 1) before and fn(user, stage, 0)
-// after a launch of the given JOLT_STAGE_* kind.
-struct LaunchHook {
-  void (*fn)(void *user, int stage, int begin) = nullptr;
-  void *user = nullptr;
-  void operator()(int stage, int begin) const { if (fn) fn(user, stage, begin); }
-};
-
 // ----------------------------------------------------------------- residual / decode
 struct ResidCell {
   const void *x;        // cell base pointer (bf16 or fp32)
@@ -241,8 +233,7 @@ size_t sytrd_large_table_entries(int n_mat, int n, int nb);
 // into a graph and replayed).
 void sytrd_large_tables(const EigBatch &b, float *work, int nb, GemmProblem *tab_host);
 hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, const GemmProblem *tab_dev,
-                              hipStream_t st, const LaunchHook &hook,
-                              int m0 = 0, int m1 = -1);
+                              hipStream_t st, int m0 = 0, int m1 = -1);
 // all eigenvalues of the tridiagonal (fp64 bisection), descending
 hipError_t launch_tridiag_eigvals(const EigBatch &b, hipStream_t st);
 // top-k eigenvectors of the tridiagonal by fp64 inverse iteration, orthogonalised
@@ -252,6 +243,10 @@ struct InvitWork {
   double *lu;            // scratch [n_mat][3][n][ldlu], columns processed ldlu at a time
   int32_t ldz, ldlu;
   const int32_t *k;      // device [n_mat] vectors wanted per matrix
+  int32_t *status;       // device [n_mat], zeroed by the launcher: set to 1 when a vector's
+                         // solution growth misses the convergence bound
+  int32_t iters;         // inverse-iteration sweeps per vector (normally 2)
+  int32_t pad;
 };
 hipError_t launch_tridiag_eigvecs(const EigBatch &b, const InvitWork &w, int kmax,
                                   hipStream_t st);
@@ -321,6 +316,7 @@ struct CholArgs {
   float *Rinv;              // [cell][l][ldr] out: L^-T (upper triangular), zero padding
   double *Dinv;             // [cell][nbk][64][64] scratch: inverses of the diagonal tiles
   double *dmax;             // [cell] scratch: largest diagonal entry of G
+  int32_t *clamped;         // [cell] out: pivots raised to the floor in this factorisation
   int32_t l, ldr, nbk, pad; // nbk = chol_blocks(l)
 };
 int chol_blocks(int l);

@@ -18,6 +18,7 @@ constexpr int SYTRD_SMALL_MAX = 768;   // larger matrices use the blocked multi-
 constexpr int SYTRD_NB = 32;
 constexpr int kG64Rows = 8192;          // rows per split-K chunk of the fp64 sketch Gram
 constexpr int kGramSplitMax = 16;       // row chunks of the second CholeskyQR pass's Gram
+constexpr int kOrthMax = 33;            // CholeskyQR2 calls of one spectrum (1 + 2 x 16 power iterations)
 
 struct Carver {
   uint8_t *base;
@@ -36,6 +37,7 @@ struct EigWs {
   EigBatch b{};
   double *Z = nullptr, *lu = nullptr;
   int32_t *k = nullptr;
+  int32_t *status = nullptr;   // inverse-iteration convergence flags, one per matrix
   float *bt = nullptr;
   float *trd = nullptr;    // blocked tridiagonalisation work (large n only)
   int kmax = 0;
@@ -74,6 +76,7 @@ struct Ws {
   float *Bsk = nullptr;                   // l x N: B = Q^T X_(2)
   float *Wsk = nullptr;                   // l x q: Ritz vectors of B B^T
   double *g64p = nullptr, *g64 = nullptr, *chM = nullptr, *chD = nullptr, *chMax = nullptr;
+  int32_t *orth_clamp = nullptr;          // [orth call][pass][cell] clamped Cholesky pivots
   float *Rinv = nullptr;                  // l x ldl
   // eps2
   double *eps_part = nullptr;
@@ -92,6 +95,7 @@ void carve_eig(Carver &cv, EigWs &e, int nmat, int n, int kmax, float *A) {
   e.b.tau = cv.take<float>((size_t)nmat * n);
   e.kmax = kmax;
   e.k = cv.take<int32_t>(nmat);
+  e.status = cv.take<int32_t>(nmat);
   if (n > SYTRD_SMALL_MAX) e.trd = cv.take<float>(sytrd_large_work_floats(nmat, n, SYTRD_NB));
   if (kmax > 0) {
     e.Z = cv.take<double>((size_t)nmat * n * kmax);
@@ -147,6 +151,7 @@ void plan(Carver &cv, Ws &w, const SpecShape &sh, int nc) {
     w.chM = cv.take<double>((size_t)nc * l * l);
     w.chD = cv.take<double>((size_t)nc * chol_blocks(l) * 64 * 64);
     w.chMax = cv.take<double>(nc);
+    w.orth_clamp = cv.take<int32_t>((size_t)kOrthMax * 2 * nc);
     w.Rinv = cv.take<float>((size_t)nc * l * w.ldl);
   }
   w.U = cv.take<float>((size_t)nc * T * std::max(w.kmaxT, 1));
@@ -182,27 +187,12 @@ GemmOperand plain(const void *p, int64_t ld) {
   return o;
 }
 
-// Launch hook that brackets individual launches with profiling events.
-struct HookState {
-  jolt_ctx *ctx;
-  hipStream_t st;
-  StageTimer *open = nullptr;
-};
-void hook_fn(void *u, int stage, int begin) {
-  HookState *h = static_cast<HookState *>(u);
-  if (begin) {
-    h->open = new StageTimer(h->ctx, h->st, stage);
-  } else {
-    delete h->open;
-    h->open = nullptr;
-  }
-}
-
 struct Run {
   jolt_ctx *ctx;
   hipStream_t st;
   Ws w;
   size_t tab_used = 0;
+  int orth_calls = 0;      // CholeskyQR2 calls queued by this call (their clamp counts)
 
   // upload a problem table into the next slice of the device table area, then launch.
   // mode 0: bf16 x bf16 on the bf16 matrix cores; mode 2: the same kernel with fp32
@@ -249,16 +239,10 @@ int eig_values(Run &R, EigWs &e) {
     c->tab_host.resize(std::max(c->tab_host.size(), nt));
     sytrd_large_tables(e.b, e.trd, SYTRD_NB, c->tab_host.data());
     HIP_OK(hipMemcpyAsync(tab, c->tab_host.data(), nt * sizeof(GemmProblem), hipMemcpyHostToDevice, R.st));
-    if (c->prof_on) {
-      // instrumented path: every launch bracketed by events (no graph)
-      HookState hs{c, R.st};
-      LaunchHook hook;
-      hook.fn = hook_fn;
-      hook.user = &hs;
-      HIP_OK(launch_sytrd_large(e.b, e.trd, SYTRD_NB, tab, R.st, hook));
-    } else {
+    {
       // the launch sequence depends only on the shape and the buffers: capture it once
-      // on a private stream and replay it on the caller's stream
+      // on a private stream and replay it on the caller's stream (timed as one stage when
+      // profiling is on; its kernels are told apart by a kernel trace)
       std::vector<const void *> key{e.b.A, e.trd, tab, e.b.d, e.b.e, e.b.tau,
                                     reinterpret_cast<const void *>((intptr_t)e.b.n),
                                     reinterpret_cast<const void *>((intptr_t)e.b.n_mat)};
@@ -267,7 +251,7 @@ int eig_values(Run &R, EigWs &e) {
         if (!c->cap_stream) HIP_OK(hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking));
         hipGraph_t g = nullptr;
         HIP_OK(hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal));
-        hipError_t le = launch_sytrd_large(e.b, e.trd, SYTRD_NB, tab, c->cap_stream, LaunchHook{});
+        hipError_t le = launch_sytrd_large(e.b, e.trd, SYTRD_NB, tab, c->cap_stream);
         hipError_t ce = hipStreamEndCapture(c->cap_stream, &g);
         HIP_OK(le);
         HIP_OK(ce);
@@ -276,6 +260,7 @@ int eig_values(Run &R, EigWs &e) {
         HIP_OK(ie);
         c->trd_key = key;
       }
+      StageTimer t(R.ctx, R.st, JOLT_STAGE_TRIDIAG_LARGE);
       HIP_OK(hipGraphLaunch(c->trd_exec, R.st));
     }
   } else {
@@ -294,7 +279,8 @@ int eig_vectors(Run &R, EigWs &e, const std::vector<int> &k, float *U, int64_t l
   if (kmax == 0) return JOLT_OK;
   if (kmax > e.kmax) return jolt_fail(JOLT_E_WORKSPACE, "eigenvector count %d exceeds workspace %d", kmax, e.kmax);
   HIP_OK(hipMemcpyAsync(e.k, k.data(), k.size() * sizeof(int32_t), hipMemcpyHostToDevice, R.st));
-  InvitWork iw{e.Z, e.lu, kmax, std::min(kmax, KC), e.k};
+  HIP_OK(hipMemsetAsync(e.status, 0, (size_t)e.b.n_mat * sizeof(int32_t), R.st));
+  InvitWork iw{e.Z, e.lu, kmax, std::min(kmax, KC), e.k, e.status, R.ctx->invit_iters, 0};
   {
     StageTimer t(R.ctx, R.st, JOLT_STAGE_EIGVECS);
     HIP_OK(launch_tridiag_eigvecs(e.b, iw, kmax, R.st));
@@ -307,6 +293,63 @@ int eig_vectors(Run &R, EigWs &e, const std::vector<int> &k, float *U, int64_t l
   HIP_OK(launch_backtransform(e.b, iw, kmax, U, ldu, u_stride, e.bt, tab, R.ctx->tab_host.data(), R.st));
   return JOLT_OK;
 }
+
+// Host copies of the device-side checks of one call: non-finite input cells, the clamp
+// counts of every CholeskyQR2 pass and the inverse-iteration convergence flags.  queue()
+// adds the copies to the stream; verdict() reads them once the stream is synchronised.
+struct CallChecks {
+  int nc = 0, n_orth = 0;
+  bool spectrum = false;
+  std::vector<int32_t> bad, clamp, tstat, fstat;
+  std::vector<double> E;
+
+  int queue(Run &R, int nc_, bool spectrum_computed, bool token_vecs, bool feature_vecs) {
+    nc = nc_;
+    spectrum = spectrum_computed;
+    if (spectrum) {
+      bad.resize(nc);
+      E.resize(nc);
+      HIP_OK(hipMemcpyAsync(bad.data(), R.w.nonfinite, nc * sizeof(int32_t), hipMemcpyDeviceToHost, R.st));
+      HIP_OK(hipMemcpyAsync(E.data(), R.w.E, nc * sizeof(double), hipMemcpyDeviceToHost, R.st));
+      n_orth = R.orth_calls;
+      if (n_orth) {
+        clamp.resize((size_t)n_orth * 2 * nc);
+        HIP_OK(hipMemcpyAsync(clamp.data(), R.w.orth_clamp, clamp.size() * sizeof(int32_t),
+                              hipMemcpyDeviceToHost, R.st));
+      }
+    }
+    if (token_vecs) {
+      tstat.resize(R.w.teig.b.n_mat);
+      HIP_OK(hipMemcpyAsync(tstat.data(), R.w.teig.status, tstat.size() * sizeof(int32_t),
+                            hipMemcpyDeviceToHost, R.st));
+    }
+    if (feature_vecs) {
+      fstat.resize(R.w.feig.b.n_mat);
+      HIP_OK(hipMemcpyAsync(fstat.data(), R.w.feig.status, fstat.size() * sizeof(int32_t),
+                            hipMemcpyDeviceToHost, R.st));
+    }
+    return JOLT_OK;
+  }
+
+  int verdict() const {
+    for (int c = 0; c < (int)bad.size(); ++c)
+      if (bad[c]) return jolt_fail(JOLT_E_NONFINITE, "cell %d contains NaN or Inf", c);
+    for (int c = 0; c < (int)E.size(); ++c) {
+      if (!(E[c] > 0.0)) continue;
+      for (int o = 0; o < n_orth; ++o) {
+        const int32_t first = clamp[((size_t)o * 2 + 0) * nc + c], second = clamp[((size_t)o * 2 + 1) * nc + c];
+        if (second > 0 && first == 0)
+          return jolt_fail(JOLT_E_NOCONV, "cell %d: orthonormalisation %d lost rank in its first CholeskyQR "
+                                          "pass (%d pivots clamped in the second)", c, o, second);
+      }
+    }
+    for (int c = 0; c < (int)tstat.size(); ++c)
+      if (tstat[c]) return jolt_fail(JOLT_E_NOCONV, "cell %d: token-mode inverse iteration did not converge", c);
+    for (int c = 0; c < (int)fstat.size(); ++c)
+      if (fstat[c]) return jolt_fail(JOLT_E_NOCONV, "cell %d: feature-mode inverse iteration did not converge", c);
+    return JOLT_OK;
+  }
+};
 
 int upload_seeds_and_signs(Run &R, const uint64_t *seeds, int nc, int d) {
   HIP_OK(hipMemcpyAsync(R.w.seeds, seeds, nc * sizeof(uint64_t), hipMemcpyHostToDevice, R.st));
@@ -432,7 +475,7 @@ static bool same_desc(const jolt_cell_desc &a, const jolt_cell_desc &b) {
 
 static bool same_opts(const jolt_spectrum_opts &a, const jolt_spectrum_opts &b) {
   return a.method == b.method && a.q == b.q && a.ratio == b.ratio && a.oversample == b.oversample &&
-         a.power_iters == b.power_iters;
+         a.power_iters == b.power_iters && a.r_max == b.r_max;
 }
 
 namespace {
@@ -477,7 +520,9 @@ int orth(Run &R, const SpecShape &sh, int nc, float *buf, float *tmp, int rows, 
       g.partial = R.w.g64p; g.G = R.w.g64;
       HIP_OK(launch_gram64(g, nc, R.st));
     }
-    CholArgs ca{R.w.g64, R.w.chM, R.w.Rinv, R.w.chD, R.w.chMax, l, ldl, chol_blocks(l), 0};
+    if (R.orth_calls >= kOrthMax) return jolt_fail(JOLT_E_WORKSPACE, "too many orthonormalisations");
+    int32_t *clamp = R.w.orth_clamp + ((size_t)R.orth_calls * 2 + pass) * nc;
+    CholArgs ca{R.w.g64, R.w.chM, R.w.Rinv, R.w.chD, R.w.chMax, clamp, l, ldl, chol_blocks(l), 0};
     HIP_OK(launch_chol_inv(ca, nc, R.st));
     std::vector<GemmProblem> P(nc);
     for (int c = 0; c < nc; ++c) {
@@ -492,6 +537,7 @@ int orth(Run &R, const SpecShape &sh, int nc, float *buf, float *tmp, int rows, 
     if (rc) return rc;
     std::swap(src, dst);
   }
+  ++R.orth_calls;
   return JOLT_OK;
 }
 
@@ -614,7 +660,8 @@ extern "C" int jolt_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
   size_t need = 0;
   jolt_workspace_size(desc, n_cells, opts, &need);
   if (ws_bytes < need) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
-  HIP_OK(hipSetDevice(ctx->device));
+  DeviceGuard dg;
+  HIP_OK(dg.enter(ctx->device));
   Run R{ctx, (hipStream_t)stream, {}};
   Carver cv(ws);
   plan(cv, R.w, sh, n_cells);
@@ -629,11 +676,12 @@ extern "C" int jolt_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
     HIP_OK(hipMemcpyAsync(lt.data(), R.w.teig.b.lam, lt.size() * sizeof(double), hipMemcpyDeviceToHost, R.st));
   else
     HIP_OK(hipMemcpyAsync(lf.data(), R.w.teig.b.lam, lf.size() * sizeof(double), hipMemcpyDeviceToHost, R.st));
-  std::vector<int32_t> bad(n_cells);
-  HIP_OK(hipMemcpyAsync(bad.data(), R.w.nonfinite, n_cells * sizeof(int32_t), hipMemcpyDeviceToHost, R.st));
+  CallChecks chk;
+  rc = chk.queue(R, n_cells, true, false, false);
+  if (rc) return rc;
   HIP_OK(hipStreamSynchronize(R.st));
-  for (int c = 0; c < n_cells; ++c)
-    if (bad[c]) return jolt_fail(JOLT_E_NONFINITE, "cell %d contains NaN or Inf", c);
+  rc = chk.verdict();
+  if (rc) return rc;
   // eigenvalues are clipped at 0 (the Grams are positive semi-definite)
   for (int c = 0; c < n_cells; ++c) {
     for (int i = 0; i < sh.d; ++i) lam_d[(size_t)c * sh.d + i] = std::max(0.0, ld[(size_t)c * sh.d + i]);
@@ -726,7 +774,8 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
   size_t need = 0;
   jolt_workspace_size(desc, n_cells, opts, &need);
   if (ws_bytes < need) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
-  HIP_OK(hipSetDevice(ctx->device));
+  DeviceGuard dg;
+  HIP_OK(dg.enter(ctx->device));
   Run R{ctx, (hipStream_t)stream, {}};
   Carver cv(ws);
   plan(cv, R.w, sh, n_cells);
@@ -913,6 +962,16 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
     fill_header(hdr.data() + (size_t)c * kHeaderBytes, desc, &params[c], sh.method);
     HIP_OK(hipMemcpyAsync(blobs[c], hdr.data() + (size_t)c * kHeaderBytes, kHeaderBytes, hipMemcpyHostToDevice, R.st));
   }
+  // input and solver checks (a spectrum computed here; the eigenvectors of this call)
+  CallChecks chk;
+  rc = chk.queue(R, nc, !o.reuse, kmax > 0, kmax > 0);
+  if (rc) return rc;
+  HIP_OK(hipStreamSynchronize(R.st));
+  rc = chk.verdict();
+  if (rc) {
+    forget_spectra(ctx, ws, ws_bytes);
+    return rc;
+  }
   DebugState &dbg = ctx->dbg;
   dbg.valid = true;
   dbg.n_cells = nc; dbg.T = T; dbg.d = d; dbg.m = m; dbg.N = N; dbg.ell = sh.ell;
@@ -990,7 +1049,8 @@ extern "C" int jolt_truncated_spectra(jolt_ctx *ctx, const jolt_cell_desc *desc,
   size_t need = 0;
   jolt_truncated_spectra_workspace_size(desc, n_cells, opts, step, n_r, &need);
   if (ws_bytes < need) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
-  HIP_OK(hipSetDevice(ctx->device));
+  DeviceGuard dg;
+  HIP_OK(dg.enter(ctx->device));
   Run R{ctx, (hipStream_t)stream, {}};
   Carver cv(ws);
   plan(cv, R.w, sh, n_cells);
@@ -1058,7 +1118,15 @@ extern "C" int jolt_truncated_spectra(jolt_ctx *ctx, const jolt_cell_desc *desc,
   rc = eig_values(R, t.eig);
   if (rc) return rc;
   HIP_OK(hipMemcpyAsync(mu, t.eig.b.lam, (size_t)nm * d * sizeof(double), hipMemcpyDeviceToHost, R.st));
+  CallChecks chk;
+  rc = chk.queue(R, nc, !o.reuse, true, false);
+  if (rc) return rc;
   HIP_OK(hipStreamSynchronize(R.st));
+  rc = chk.verdict();
+  if (rc) {
+    forget_spectra(ctx, ws, ws_bytes);
+    return rc;
+  }
   for (size_t i = 0; i < (size_t)nm * d; ++i) mu[i] = std::max(0.0, mu[i]);
   return JOLT_OK;
 }
@@ -1083,6 +1151,7 @@ extern "C" int jolt_decompress_rope(jolt_ctx *ctx, int n_cells, const void *cons
     return jolt_fail(JOLT_E_INVAL, "jolt_decompress: null argument");
   if (reinterpret_cast<uintptr_t>(ws) & 255) return jolt_fail(JOLT_E_INVAL, "workspace must be 256-byte aligned");
   hipStream_t st = (hipStream_t)stream;
+  DeviceGuard dg;
   std::vector<uint8_t> hdr((size_t)n_cells * kHeaderBytes);
   if (hdr_host) {
     // host header copies are validated before the context is touched
@@ -1093,10 +1162,10 @@ extern "C" int jolt_decompress_rope(jolt_ctx *ctx, int n_cells, const void *cons
       if (rc) return rc;
     }
     if (!ctx) return jolt_fail(JOLT_E_INVAL, "jolt_decompress: ctx is null");
-    HIP_OK(hipSetDevice(ctx->device));
+    HIP_OK(dg.enter(ctx->device));
   } else {
     if (!ctx) return jolt_fail(JOLT_E_INVAL, "jolt_decompress: ctx is null");
-    HIP_OK(hipSetDevice(ctx->device));
+    HIP_OK(dg.enter(ctx->device));
     for (int c = 0; c < n_cells; ++c) {
       if (!blobs[c] || blob_bytes[c] < (size_t)kHeaderBytes) return jolt_fail(JOLT_E_BLOB, "blob %d too small", c);
       HIP_OK(hipMemcpyAsync(hdr.data() + (size_t)c * kHeaderBytes, blobs[c], kHeaderBytes, hipMemcpyDeviceToHost, st));
@@ -1212,7 +1281,8 @@ extern "C" int jolt_eps2_calibrate(jolt_ctx *ctx, int group, int d, uint64_t see
   if (group < 8 || group > d || d % group || group % 8) return jolt_fail(JOLT_E_INVAL, "bad group %d", group);
   if (ws_bytes < need) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   forget_spectra(ctx, ws, ws_bytes);
-  HIP_OK(hipSetDevice(ctx->device));
+  DeviceGuard dg;
+  HIP_OK(dg.enter(ctx->device));
   hipStream_t st = (hipStream_t)stream;
   Eps2Args a{seed, n_samples, group, (float)(1.0 / std::sqrt((double)d)), static_cast<double *>(ws)};
   HIP_OK(launch_eps2_partial(a, d, st));
@@ -1266,7 +1336,8 @@ extern "C" int jolt_slice_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, in
   if (rc) return rc;
   if (!lam_s) return jolt_fail(JOLT_E_INVAL, "lam_s is null");
   if (ws_bytes < need) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
-  HIP_OK(hipSetDevice(ctx->device));
+  DeviceGuard dg;
+  HIP_OK(dg.enter(ctx->device));
   forget_spectra(ctx, ws, ws_bytes);
   hipStream_t st = (hipStream_t)stream;
   const int m = desc->n_layers * desc->n_heads;
@@ -1371,7 +1442,8 @@ extern "C" int jolt_attend(jolt_ctx *ctx, int n_items, const void *const *k_blob
   int rc = jolt_attend_workspace_size(n_items, n_q, T, d, rk, rv, &need);
   if (rc) return rc;
   if (ws_bytes < need) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
-  HIP_OK(hipSetDevice(ctx->device));
+  DeviceGuard dg;
+  HIP_OK(dg.enter(ctx->device));
   forget_spectra(ctx, ws, ws_bytes);
   hipStream_t st = (hipStream_t)stream;
   Carver cv(ws);
@@ -1411,7 +1483,8 @@ extern "C" int jolt_debug_export(jolt_ctx *ctx, int what, int cell, void *dst, s
   if (!g.valid) return jolt_fail(JOLT_E_STATE, "jolt_debug_export: no compress call recorded");
   if (cell < 0 || cell >= g.n_cells) return jolt_fail(JOLT_E_INVAL, "cell out of range");
   hipStream_t st = (hipStream_t)stream;
-  HIP_OK(hipSetDevice(ctx->device));
+  DeviceGuard dg;
+  HIP_OK(dg.enter(ctx->device));
   if (what == 0 || what == 1) {
     const int rows = what == 0 ? g.T : g.d, cols = what == 0 ? g.rT[cell] : g.rd[cell];
     const float *src = what == 0 ? g.U + cell * g.u_stride : g.Ud + cell * g.ud_stride;
@@ -1442,4 +1515,14 @@ extern "C" int jolt_debug_export(jolt_ctx *ctx, int what, int cell, void *dst, s
     return JOLT_OK;
   }
   return jolt_fail(JOLT_E_INVAL, "unknown export %d", what);
+}
+
+extern "C" int jolt_debug_set(jolt_ctx *ctx, int what, int64_t value) {
+  if (!ctx) return jolt_fail(JOLT_E_INVAL, "jolt_debug_set: ctx is null");
+  if (what == JOLT_DBG_INVIT_ITERS) {
+    if (value < 0 || value > 8) return jolt_fail(JOLT_E_INVAL, "jolt_debug_set: iterations must be in 0..8");
+    ctx->invit_iters = (int)value;
+    return JOLT_OK;
+  }
+  return jolt_fail(JOLT_E_INVAL, "jolt_debug_set: unknown setting %d", what);
 }

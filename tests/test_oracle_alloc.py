@@ -9,17 +9,47 @@ from oracle import alloc, pipeline, tucker as tk
 
 
 def test_byte_model_matches_paper_footprint():
-    """Section 8: Mistral-7B at ctx-2048 occupies 268.4 MB uncompressed, and the
-    compressed footprints at 2/3/4/8x land at the printed sizes (1.99-7.98x)."""
+    """Section 8: Mistral-7B at ctx-2048 occupies 268.4 MB uncompressed, and the compressed
+    footprints at 2/3/4/8x land at the printed sizes (1.99-7.98x).  The oracle's own byte
+    model prices the uncompressed cache (every entry at b = 16 bits, no factors) and its
+    allocator, fed the cells of that cache (16 cells: 8 layer groups x K/V, 32 slices of
+    2048 x 128) under budget = cache / R, never exceeds the budget and spends it to within
+    2% (the Lagrangian dual only reaches points of each cell's lower convex hull, so with 16
+    cells it can stop short of the budget: 2.008x, 3.000x, 4.074x and 8.044x here), while the
+    paper's printed footprints sit within 0.5% of cache / R."""
     g = golden("paper_memory_footprint.json")
     mdl = g["model"]
-    total = 2 * mdl["layers"] * mdl["kv_heads"] * mdl["ctx"] * mdl["head_dim"] * mdl["bytes_per_scalar"]
+    group_layers = 4
+    m = group_layers * mdl["kv_heads"]
+    n_cells = 2 * mdl["layers"] // group_layers
+    T, d, c = mdl["ctx"], mdl["head_dim"], mdl["bytes_per_scalar"]
+    # uncompressed: eq. (1) with no factors and 8 c bits per entry, no scale term
+    per_cell = alloc.byte_cost(m, T, d, 0, 0, 8 * c, c, 64, count_scales=False)
+    total = n_cells * per_cell
     assert round(total / 1e6, 1) == g["uncompressed_MB"]
+    # spectra of that shape (power laws, a different decay per cell), the paper's group 64
+    rng = np.random.default_rng(0)
+    cells = []
+    for i in range(n_cells):
+        aT, ad = rng.uniform(0.8, 1.6), rng.uniform(0.5, 1.5)
+        lam_T = np.arange(1, T + 1, dtype=np.float64) ** -aT
+        lam_d = np.arange(1, d + 1, dtype=np.float64) ** -ad
+        lam_d *= lam_T.sum() / lam_d.sum()
+        cells.append(alloc.CellSpectrum(m=m, T=T, d=d, c=c, g=64, E=float(lam_T.sum()),
+                                        lam_T=lam_T, lam_d=lam_d, rT_max=T))
+    eps2 = {0: 1.0, 2: 0.26, 4: 0.010, 8: 3.5e-5}
     lo, hi = g["achieved_ratio_range"]
+    assert lo <= min(map(float, g["compressed_MB"])) and max(map(float, g["compressed_MB"])) <= hi + 0.05
     for R, mb in g["compressed_MB"].items():
-        achieved = total / (mb * 1e6)
-        assert lo - 0.005 <= achieved <= hi + 0.005
-        assert abs(achieved / float(R) - 1) < 0.005     # meets each target to 0.5%
+        res = alloc.allocate(cells, total / float(R), eps2)
+        assert not res["infeasible"]
+        spent = alloc.allocation_cost(cells, res["alloc"])
+        assert spent == res["total_bytes"] <= total / float(R)
+        achieved = total / spent
+        assert achieved >= float(R) and achieved / float(R) - 1 < 0.02, (R, achieved)
+        # the paper's printed footprint, priced against the same uncompressed bytes
+        assert abs(total / (mb * 1e6) / float(R) - 1) < 0.005
+        assert lo - 0.005 <= total / (mb * 1e6) <= hi + 0.005
 
 
 def test_byte_cost_eq1_terms():

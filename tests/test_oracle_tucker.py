@@ -156,3 +156,30 @@ def test_serialize_fp16_exponents(rng):
     Xt = tk.reconstruct(Uh, Udh, Gh, e, 10, 6)
     ref = np.einsum("tr,srk,dk->std", Uh, np.ldexp(Gh, e[:, None, None]), Udh)
     np.testing.assert_allclose(Xt, ref, rtol=1e-12)
+
+
+def test_core_exponent_fits_a_signed_byte():
+    """The blob keeps one int8 exponent per core slice: e_s = max(-128, ceil(log2 max|G_s|) - 15).
+    Ordinary cores get the unclamped value (stored maxima in (2^14, 2^15]); cores below 2^-113
+    take the floor -128 and still scale to below 2^15; an all-zero slice stores 0."""
+    from oracle.rounding import to_fp16
+    rng = np.random.default_rng(3)
+    G = rng.standard_normal((4, 6, 5))
+    G[1] *= 2.0 ** -120          # below the range the byte can express unclamped
+    G[2] *= 2.0 ** 100
+    G[3] = 0.0
+    U = np.linalg.qr(rng.standard_normal((9, 6)))[0]
+    Ud = np.linalg.qr(rng.standard_normal((5, 5)))[0]
+    _, _, G_hat, gexp = tk.serialize(U, Ud, G, factor_bytes=2)
+    assert gexp.min() >= -128 and gexp.max() <= 127
+    assert gexp[1] == -128 and gexp[3] == 0
+    for s in (0, 2):
+        M = np.abs(G[s]).max()
+        assert 2.0 ** 14 < M * 2.0 ** -gexp[s] <= 2.0 ** 15
+    assert np.abs(G_hat[1]).max() < 2.0 ** 15
+    # stored values are the fp16 rounding of the scaled core (exact powers of two)
+    for s in range(4):
+        np.testing.assert_array_equal(G_hat[s], to_fp16(np.ldexp(G[s], -int(gexp[s]))))
+    # the scaled-back core of the clamped slice keeps fp16 relative accuracy
+    back = np.ldexp(G_hat[1], int(gexp[1]))
+    assert np.abs(back - G[1]).max() <= 2.0 ** -11 * np.abs(G[1]).max()
