@@ -1,22 +1,24 @@
 #!/usr/bin/env python3
 """Benchmark: KV-cache compression + decompression throughput on one MI355X.
 
-Workload (default): a Mistral-7B-shaped GQA cache, bf16 keys and values,
-32 layers x 8 KV heads x T 4096 x d 128, batch 1 (536.9 MB), cut into layer
-groups of 4 -> 16 cells (8 groups x K/V, m = 32 slices each).  Exact token-mode
-spectrum, ranks and residual bits chosen by the Lagrangian dual at a 2x byte
-budget, 2/4/8-bit residual grid, group 64.  Synthetic data (seeded low-rank AR(1)
-token factors, Gaussian cores, decaying feature spectra, 2 outlier channels x10,
-N(0, 0.05^2) noise); no model weights are involved.
+Workload (default): a LLaMA-2-13B-shaped MHA cache, bf16 keys and values, 40 layers x
+40 heads x T 4096 x d 128, batch 4 (13.4 GB), cut into layer groups of 5 -> 64 cells
+(8 groups x K/V x 4 batch items, m = 200 slices each), all cells in one library call.
+Exact token-mode spectrum, ranks and residual bits chosen by the Lagrangian dual at a
+2x byte budget, 2/4/8-bit residual grid, group 64.  Synthetic data (seeded low-rank
+AR(1) token factors, Gaussian cores, per-layer feature-spectrum decays, 2 outlier
+channels x10, N(0, 0.05^2) noise); no model weights are involved.
 
 One step = the whole path over the cache: spectrum of every cell, allocation,
 compression into blobs, decompression back to a bf16 cache.  value = cache bytes x
 steps / wall time of the timed steps (GB/s, 1 GB = 1e9 B), inputs resident in HBM.
 
-Also reported: compress-only and decompress-only rates, mean relative Frobenius
-error over layers for K and V, achieved ratio, per-stage device times from the
-library's event instrumentation, the roofline of the dominant stage, and the fp64
-oracle timed on a bounded sample on the host CPU.
+Also reported: compress-only and decompress-only rates, mean relative Frobenius error
+over layers for K and V, achieved ratio, per-stage device times from the library's
+event instrumentation (one extra step), per-pass and whole-path roofline fractions on
+the algorithmic bytes and flops of the design, FlashJoLT on the same cache and budget
+(exact / FlashJoLT compression-time ratio), and the fp64 oracle timed on a bounded
+sample of cells on the host CPU.
 """
 from __future__ import annotations
 
@@ -44,9 +46,14 @@ MFMA_TF = {"fp32": 157.3, "bf16": 2500.0, "fp16": 2500.0, "fp64": 78.6}
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="mistral7b_gqa_T4096")
+    ap.add_argument("--workload", default="llama2_13b_mha_T4096_b4")
+    ap.add_argument("--cells-per-call", type=int, default=64,
+                    help="cells batched into one library call (each call has its own workspace)")
+    ap.add_argument("--compare-steps", type=int, default=3,
+                    help="timed compress passes of FlashJoLT on the same cache after an exact run "
+                         "(0 = skip the comparison)")
     ap.add_argument("--ratio", type=float, default=0.0, help="0 = the workload's budget")
     ap.add_argument("--method", default="", choices=["", "exact", "flash"],
                     help="empty = the workload's method")
@@ -68,8 +75,8 @@ def parse():
                          "writes this many MiB: the reference dispatch for scaling HBM "
                          "traffic counters")
     ap.add_argument("--no-stage-profile", action="store_true",
-                    help="skip the event-instrumented pass (for hardware-counter runs); the "
-                         "stage and roofline fields are then omitted")
+                    help="skip the event-instrumented step; the stage and roofline fields are "
+                         "then omitted")
     ap.add_argument("--attend", action="store_true",
                     help="instead of the benchmark step: decode-time attention of one new token "
                          "(4 query heads per key-value head for GQA caches, 1 for MHA) over every "
@@ -86,74 +93,84 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def stage_work(codec, calls):
-    """Algorithmic bytes / flops of the instrumented stages over `calls` steps."""
+def pass_model(codec):
+    """Algorithmic bytes and flops of the roofline passes of one step (the section-4/5 path
+    over every cell, then its decompression), as the design counts them: bytes are the
+    minimum each pass must move (an fp32 X~ round trip is not algorithmic), flops the
+    useful ones.  Eigensolvers, QR and the allocator are timed but on neither roofline.
+    Returns {pass: dict(bytes, flops, peak_tf, stages, direction)}; `stages` are the
+    instrumented library stages whose time the pass takes."""
     L, B, H, T, d = codec.shape
     m = codec.group_layers * H
     N = m * d
     nc = len(codec.cells)
-    n = T
-    in_b = 2 if codec.dtype == 1 else 4
+    esz = 2 if codec.dtype == 1 else 4
+    elt = float(m) * T * d                        # entries per cell
     flash = codec.method == 1
+    mfma = 2500.0 if esz == 2 else 157.3          # products reading the cache: bf16 cores
     rT = [p.r_T for p in codec.params]
-    rd = [p.r_d for p in codec.params]
     bits = [p.bits for p in codec.params]
-    work = {}
-    # products that read a bf16 cache run on the bf16 matrix cores (an fp32 partner operand is
-    # split into two bf16 terms, i.e. two MFMA passes); useful flops are charged at the bf16 peak
-    cache_mfma = "bf16" if in_b == 2 else "fp32"
+    g = codec.group
+    out = {}
+    fg_peak = 2500.0 if (esz == 2 and d == 128) else 157.3
+    out["feature_gram"] = dict(bytes=nc * elt * esz, flops=nc * elt * 2.0 * d, peak_tf=fg_peak,
+                               stages=["feature_gram"], direction="compress")
     if flash:
-        ell = codec.ell
-        # Y = X Omega, per power iteration X^T Q and X Q', then B = Q^T X (all over the cache),
-        # and B B^T (fp32 MFMA, < 1% of the flops)
-        sk = nc * (2.0 * T * N * ell * (1 + 2 * codec.opts.power_iters + 1) + 2.0 * ell * ell * N)
-        work["sketch"] = (cache_mfma, sk * calls)
-        work["project"] = ("fp32", sum(2.0 * r * T * ell + 2.0 * r * ell * N for r in rT) * calls)
+        reads = 2 + 2 * codec.opts.power_iters      # X Omega, (X^T Q, X Q') per iteration, Q^T X
+        out["sketch"] = dict(bytes=nc * elt * esz * reads, flops=nc * elt * 2.0 * codec.ell * reads,
+                             peak_tf=mfma, stages=["sketch"], direction="compress")
     else:
-        # lower triangle of every trailing matrix, one read per column (fp32)
-        sym_bytes = nc * sum(4.0 * Lr * (Lr + 1) / 2 for Lr in range(1, n))
-        work["symv"] = ("hbm", sym_bytes * calls)
-        # symmetric rank-N update: T (T + 1) N flops (the syrk count; only lower tiles are formed)
-        work["token_gram"] = (cache_mfma, nc * 1.0 * T * (T + 1) * N * calls)
-        work["project"] = (cache_mfma, sum(2.0 * r * T * N for r in rT) * calls)
-    if codec.tau == "exact":
-        # the truncated spectra: Y at the grid's largest r_T (a second projection), then the
-        # Grams of its row blocks (fp32 vector arithmetic)
-        r_hi = codec.tau_cap_used
-        extra = nc * 2.0 * r_hi * (codec.ell if flash else T) * N
-        kind, amount = work["project"]
-        work["project"] = (kind, amount + extra * calls)
-        work["trunc_gram"] = ("fp32", nc * 2.0 * d * d * m * r_hi * calls)
-    rec = sum(2.0 * m * r * k * d + 2.0 * m * T * r * d for r, k in zip(rT, rd))
-    work["reconstruct"] = ("fp32", 2 * rec * calls)           # compress and decompress
-    res_b = sum(m * T * d * (in_b + (4 if r else 0)) + m * T * d * b / 8 + (2 * m * T * d / codec.group if b else 0)
-                for r, b in zip(rT, bits))
-    work["residual"] = ("hbm", res_b * calls)
-    dec_b = sum(m * T * d * b / 8 + (2 * m * T * d / codec.group if b else 0) + m * T * d * ((4 if r else 0) + 2)
-                for r, b in zip(rT, bits))
-    work["decode"] = ("hbm", dec_b * calls)
-    if not flash:
-        nb = 32
-        pg = 0.0
-        for k0 in range(0, n - 1, nb):
-            jb = min(nb, n - 1 - k0)
-            rem = n - (k0 + jb)
-            pg += 2 * 2.0 * rem * rem * jb
-        work["panel_gemm"] = ("fp32", nc * pg * calls)
-    return work
+        out["token_gram"] = dict(bytes=nc * elt * esz, flops=nc * elt * float(T + 1), peak_tf=mfma,
+                                 stages=["token_gram"], direction="compress")
+        out["project"] = dict(bytes=nc * elt * esz, flops=sum(elt * 2.0 * r for r in rT), peak_tf=mfma,
+                              stages=["project"], direction="compress")
+    code_b = sum(elt * (b / 8.0 + (2.0 / g if b else 0.0)) for b in bits)
+    recon_f = sum(elt * 2.0 * r for r in rT)
+    out["residual"] = dict(bytes=nc * elt * esz + code_b, flops=recon_f, peak_tf=2500.0,
+                           stages=["reconstruct", "residual"], direction="compress")
+    out["decode"] = dict(bytes=code_b + nc * elt * esz, flops=recon_f, peak_tf=2500.0,
+                         stages=["reconstruct", "decode"], direction="decompress")
+    return out
 
 
-# kernel source of each instrumented stage whose HBM traffic was taken with hardware counters
-STAGE_SOURCE = {"symv": "paper_2607_12550_amd/csrc/k_sytrd.hip"}
+def roofline_report(model, prof_c, prof_d, step_ms):
+    """Per-pass fractions and the whole-path fraction t_roof / t from the instrumented
+    compress (prof_c) and decompress (prof_d) stage times of one step."""
+    passes = {}
+    t_roof = 0.0
+    for name, p in model.items():
+        prof = prof_c if p["direction"] == "compress" else prof_d
+        ms = sum(prof.get(s, (0.0, 0))[0] for s in p["stages"])
+        launches = sum(prof.get(s, (0.0, 0))[1] for s in p["stages"])
+        t_b = p["bytes"] / (HBM_GBS * 1e9) * 1e3           # ms at the HBM peak
+        t_f = p["flops"] / (p["peak_tf"] * 1e12) * 1e3      # ms at the matrix-core peak
+        t_roof += max(t_b, t_f)
+        if ms <= 0:
+            continue
+        passes[name] = {"ms": round(ms, 3), "launches": launches,
+                        "bound": "hbm" if t_b >= t_f else "mfma",
+                        "GBps": round(p["bytes"] / ms / 1e6, 1), "hbm_frac": round(t_b / ms, 4),
+                        "TFLOPs": round(p["flops"] / ms / 1e9, 2), "mfma_peak_TFLOPs": p["peak_tf"],
+                        "mfma_frac": round(t_f / ms, 4), "frac": round(max(t_b, t_f) / ms, 4),
+                        "alg_bytes": p["bytes"], "alg_flops": p["flops"]}
+    whole = {"t_roof_ms": round(t_roof, 3), "t_ms": round(step_ms, 3),
+             "frac": round(t_roof / step_ms, 5) if step_ms > 0 else None}
+    return passes, whole
 
 
-def measured_traffic(stage, workload):
-    """HBM bytes per launch of a stage from the committed counter summary
-    profiles/traffic_<stage>_<workload>.md (lines 'traffic_bytes_per_launch: X' and
+# kernel source of each pass whose HBM traffic was taken with hardware counters
+PASS_SOURCE = {"token_gram": "paper_2607_12550_amd/csrc/k_gemm16.hip",
+               "residual": "paper_2607_12550_amd/csrc/k_residual.hip",
+               "decode": "paper_2607_12550_amd/csrc/k_residual.hip"}
+
+
+def measured_traffic(name, workload):
+    """HBM bytes per launch of a pass from the committed counter summary
+    profiles/traffic_<pass>_<workload>.md (lines 'traffic_bytes_per_launch: X' and
     'source_sha256: H'); None when there is none or the kernel source changed since."""
     import hashlib
-    src = STAGE_SOURCE.get(stage)
-    path = os.path.join(ROOT, "profiles", f"traffic_{stage}_{workload}.md")
+    src = PASS_SOURCE.get(name)
+    path = os.path.join(ROOT, "profiles", f"traffic_{name}_{workload}.md")
     if not src or not os.path.exists(path):
         return None
     with open(os.path.join(ROOT, src), "rb") as f:
@@ -169,24 +186,11 @@ def measured_traffic(stage, workload):
     return float(fields["traffic_bytes_per_launch"])
 
 
-def roofline_of(stage, kind, amount, ms, launches):
-    if kind == "hbm":
-        achieved = amount / (ms * 1e-3) / 1e9
-        return {"kernel": stage, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_GBS, 4), "traffic": None,
-                "launches": launches, "avg_launch_us": round(ms * 1e3 / max(1, launches), 2)}
-    peak = MFMA_TF[kind]
-    achieved = amount / (ms * 1e-3) / 1e12
-    return {"kernel": stage, "bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
-            "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None,
-            "launches": launches, "avg_launch_us": round(ms * 1e3 / max(1, launches), 2),
-            "dtype": kind}
-
-
-def cpu_baseline(K_np, V_np, cfg, params, group, T_sample, method, q, p, iters,
+def cpu_baseline(K_np, V_np, cfg, params, group, T_sample, method, q, p, iters, n_cells,
                  min_seconds=10.0, max_cells=16):
-    """fp64 oracle on whole cells (keys, then values, of layer groups 0, 1, ...) timed on
-    the host cores until at least min_seconds of work (at most max_cells cells)."""
+    """fp64 oracle on whole cells (keys, then values, of layer groups 0, 1, ... of batch item
+    0) timed on the host cores until at least min_seconds of work (at most max_cells cells);
+    the whole cache's oracle time is that sample's time scaled by n_cells / k."""
     import numpy as np
     import kvsynth
     from oracle import pipeline as opl
@@ -213,12 +217,15 @@ def cpu_baseline(K_np, V_np, cfg, params, group, T_sample, method, q, p, iters,
         done.append(f"{'KV'[tensor]}{g}:({rT},{rd},{pc.bits})")
         if t_all >= min_seconds:
             break
+    k = len(done)
     return {"value": round(nbytes / t_all / 1e9, 5), "unit": "GB/s", "cores": cores,
             "kind": "oracle",
-            "sample": f"{len(done)} whole cells ({gl} layers x {H} heads, T={T_sample}, d={d}, bf16, "
-                      f"{nbytes / 1e6:.1f} MB) {' '.join(done)}: {method} spectrum + compress at the "
-                      f"allocated ranks/bits + decode, fp64 numpy/LAPACK, {t_all:.1f} s",
-            "seconds": round(t_all, 2)}
+            "sample": f"{k} of {n_cells} cells, whole ({gl} layers x {H} heads, T={T_sample}, d={d}, "
+                      f"bf16, {nbytes / 1e6:.1f} MB) {' '.join(done)}: {method} spectrum + compress at "
+                      f"the allocated ranks/bits + decode, fp64 numpy/LAPACK, {t_all:.1f} s; the whole "
+                      f"cache extrapolated x{n_cells / k:.0f}",
+            "seconds": round(t_all, 2),
+            "extrapolated_full_cache_s": round(t_all * n_cells / k, 1)}
 
 
 def diagnostics(args):
@@ -393,6 +400,63 @@ def attend_bench(args):
     codec.close()
 
 
+def _profiled_step(J, codec, Kout, Vout, allocator):
+    """One extra step with the library's stage events on: stage times of the compress part
+    (spectrum, allocation, compress) and of the decompression, separately."""
+    import torch
+    J.jolt_profile_enable(codec.ctx, True)
+    J.jolt_profile_reset(codec.ctx)
+    codec.spectrum()
+    codec.allocate(strategy=allocator)
+    codec.compress()
+    torch.cuda.synchronize()
+    prof_c = J.jolt_profile_read(codec.ctx)
+    J.jolt_profile_reset(codec.ctx)
+    codec.decompress(Kout, Vout)
+    torch.cuda.synchronize()
+    prof_d = J.jolt_profile_read(codec.ctx)
+    J.jolt_profile_enable(codec.ctx, False)
+    return prof_c, prof_d
+
+
+def method_comparison(K, V, gl, ratio, args, exact_compress_ms):
+    """FlashJoLT against the exact path on the same cache and budget (section 5 reports
+    5.25-13.57x on real caches at T = 1024): the compress part of a step (spectrum,
+    allocation, compress) timed for the randomized method, with its error."""
+    import numpy as np
+    import torch
+    from paper_2607_12550_amd.cache import CacheCodec, layer_errors
+    codec = CacheCodec(K, V, group_layers=gl, method="flash", ratio=ratio,
+                       oversample=args.oversample, power_iters=args.power_iters, max_cells_per_call=64)
+    codec.calibrate()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    times = []
+    for s in range(1 + args.compare_steps):
+        e0.record()
+        codec.spectrum()
+        codec.allocate()
+        codec.compress()
+        e1.record()
+        torch.cuda.synchronize()
+        if s:
+            times.append(e0.elapsed_time(e1))
+    Kout, Vout = torch.empty_like(K), torch.empty_like(V)
+    codec.decompress(Kout, Vout)
+    torch.cuda.synchronize()
+    eK, eV = layer_errors(K, Kout), layer_errors(V, Vout)
+    flash_ms = float(np.median(times))
+    out = {"flash_compress_ms": round(flash_ms, 2), "exact_compress_ms": round(exact_compress_ms, 2),
+           "exact_over_flash": round(exact_compress_ms / flash_ms, 2), "flash_q": codec.opts.q or codec.rT_max,
+           "flash_ell": codec.ell, "flash_rel_frobenius_error": {"K": round(float(eK.mean()), 6),
+                                                                  "V": round(float(eV.mean()), 6)},
+           "paper_context": "5.25-13.57x FlashJoLT over exact compression time (Mistral-7B-v0.3, "
+                            "T = 1024, real caches, one A100-40GB; section 5, appendix C)"}
+    codec.close()
+    del codec, Kout, Vout
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.attend:
@@ -441,9 +505,10 @@ def main():
         log(f"calibration pass: {args.calib_copy_mib} MiB read + written")
         del src, dst
     codec = CacheCodec(K, V, group_layers=gl, method=method, ratio=ratio,
-                       oversample=args.oversample, power_iters=args.power_iters, tau=args.tau)
+                       oversample=args.oversample, power_iters=args.power_iters, tau=args.tau,
+                       max_cells_per_call=args.cells_per_call)
     eps2 = codec.calibrate()
-    log("eps2", eps2)
+    log("eps2", eps2, "cells", len(codec.cells), "per call", codec.chunk)
     Kout, Vout = torch.empty_like(K), torch.empty_like(V)
     stream = torch.cuda.current_stream()
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
@@ -474,15 +539,9 @@ def main():
         log(f"step {s}: compress {t_comp[-1]:.1f} ms, decompress {t_dec[-1]:.1f} ms")
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    # one extra instrumented step: HIP events around every stage / kernel launch
-    prof = {}
-    if not args.no_stage_profile:
-        J.jolt_profile_enable(codec.ctx, True)
-        J.jolt_profile_reset(codec.ctx)
-        step()
-        torch.cuda.synchronize()
-        prof = J.jolt_profile_read(codec.ctx)
-        J.jolt_profile_enable(codec.ctx, False)
+    step_ms = elapsed / args.steps * 1e3
+    # one extra instrumented step: HIP events around every stage, compress and decompress apart
+    prof_c, prof_d = ({}, {}) if args.no_stage_profile else _profiled_step(J, codec, Kout, Vout, args.allocator)
 
     cache_bytes = codec.cache_bytes
     value = cache_bytes * args.steps / elapsed / 1e9
@@ -490,32 +549,26 @@ def main():
     eV = layer_errors(V, Vout)
     comp_bytes = codec.compressed_bytes()
     alloc = [(p.r_T, p.r_d, p.bits) for p in codec.params]
-    work = stage_work(codec, 1)
-    roof = None
-    if prof:
-        # the slowest stage with an algorithmic work model; a slower stage without one (the
-        # latency-bound CholeskyQR chain of FlashJoLT) is named beside it
-        timed = [s for s in prof if prof[s][0] > 0]
-        slowest = max(timed, key=lambda s: prof[s][0])
-        modelled = [s for s in timed if s in work]
-        if modelled:
-            dom = max(modelled, key=lambda s: prof[s][0])
-            kind, amount = work[dom]
-            roof = roofline_of(dom, kind, amount, prof[dom][0], prof[dom][1])
-            roof["traffic"] = measured_traffic(dom, args.workload)
-            if slowest != dom:
-                roof["slowest_stage"] = {"stage": slowest, "ms_per_step": round(prof[slowest][0], 3),
-                                         "bound": "latency"}
+    roof, passes, whole = None, {}, None
+    if prof_c:
+        passes, whole = roofline_report(pass_model(codec), prof_c, prof_d, step_ms)
+        dom = max(passes, key=lambda k: passes[k]["ms"])
+        P = passes[dom]
+        if P["bound"] == "hbm":
+            roof = {"kernel": dom, "bound": "hbm", "achieved": P["GBps"], "peak": HBM_GBS, "unit": "GB/s",
+                    "frac": P["hbm_frac"]}
         else:
-            roof = {"kernel": slowest, "bound": "latency", "achieved": None, "peak": None, "unit": None,
-                    "frac": None, "traffic": None}
-    stages = {s: {"ms_per_step": round(v[0], 3), "launches_per_step": v[1]}
-              for s, v in prof.items() if v[1]}
-    stage_roofs = {}
-    for s, (kind, amount) in work.items():
-        if prof.get(s, (0, 0))[0] > 0:
-            r = roofline_of(s, kind, amount, prof[s][0], prof[s][1])
-            stage_roofs[s] = {k: r[k] for k in ("bound", "achieved", "unit", "frac")}
+            roof = {"kernel": dom, "bound": "mfma", "achieved": P["TFLOPs"], "peak": P["mfma_peak_TFLOPs"],
+                    "unit": "TFLOP/s", "frac": P["mfma_frac"]}
+        roof["traffic"] = measured_traffic(dom, args.workload)
+        roof["launches"] = P["launches"]
+        roof["avg_launch_us"] = round(P["ms"] * 1e3 / max(1, P["launches"]), 2)
+        roof["whole_path"] = whole
+    stages = {}
+    for tag, prof in (("compress", prof_c), ("decompress", prof_d)):
+        for s_, v in prof.items():
+            if v[1]:
+                stages[f"{tag}:{s_}"] = {"ms_per_step": round(v[0], 3), "launches_per_step": v[1]}
     out = {
         "metric": "KV GB/s compressed+decompressed per GPU; rel. Frobenius error K/V at 2x",
         "value": round(value, 3),
@@ -523,16 +576,16 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(elapsed / args.steps * 1e3, 2),
+        "ms_per_step": round(step_ms, 2),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": cfg["dtype"],
         "data": "synthetic",
         "config": {"workload": args.workload, "layers": cfg["n_layers"], "kv_heads": cfg["n_heads"],
                    "T": cfg["T"], "head_dim": cfg["d"], "batch": cfg["batch"], "group_layers": gl,
-                   "cells": len(codec.cells), "method": method, "ratio": ratio,
-                   "allocator": args.allocator, "tau": args.tau,
+                   "cells": len(codec.cells), "cells_per_call": codec.chunk, "method": method,
+                   "ratio": ratio, "allocator": args.allocator, "tau": args.tau,
                    **({"tau_rT_cap": codec.tau_cap_used} if args.tau == "exact" else {}),
                    "keys": "post-rope" if args.rope_post > 1.0 else "pre-rope",
                    "cache_bytes": cache_bytes},
@@ -541,10 +594,10 @@ def main():
         "rel_frobenius_error": {"K": round(float(eK.mean()), 6), "V": round(float(eV.mean()), 6)},
         "achieved_ratio": round(cache_bytes / comp_bytes, 4),
         "achieved_ratio_eq1_payload": round(cache_bytes / codec.payload_bytes(), 4),
-        "allocation": alloc,
+        "allocation_rT_max": max(a[0] for a in alloc),
         "allocation_model_error": alloc_res.get("model_error"),
         "stage_ms_per_step": stages,
-        "stage_roofline": stage_roofs,
+        "passes": passes,
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
@@ -552,8 +605,14 @@ def main():
         Ts = args.cpu_sample_T or cfg["T"]
         out["cpu_baseline"] = cpu_baseline(Knp, Vnp, dict(cfg, group_layers=gl), codec.params,
                                            codec.group, Ts, method, codec.opts.q or codec.rT_max,
-                                           args.oversample, args.power_iters)
+                                           args.oversample, args.power_iters, len(codec.cells))
+    exact_compress_ms = float(np.median(t_comp))
     codec.close()
+    del codec, Kout, Vout
+    torch.cuda.empty_cache()
+    if method == "exact" and args.compare_steps > 0:
+        log("FlashJoLT on the same cache ...")
+        out["method_comparison"] = method_comparison(K, V, gl, ratio, args, exact_compress_ms)
     print(json.dumps(out))
 
 

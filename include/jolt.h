@@ -373,9 +373,10 @@ int jolt_attend(jolt_ctx *ctx, int n_items, const void *const *k_blobs, const si
 
 /* Test hook: copies an intermediate of the most recent jolt_compress on this
  * context for cell `cell` into dst (device memory, dst_bytes): 0 = U_T (T x r_T fp32),
- * 1 = U_d (d x r_d fp32), 2 = X~ (m x T x d fp32 from the stored factors),
- * 3 = FlashJoLT sketch Omega (m*d x l, bf16 bits).  Requires the workspace of that
- * call to be untouched since. */
+ * 1 = U_d (d x r_d fp32), 2 = X~ (m x T x d fp32 from the stored factors, recomputed by
+ * the call's own fused reconstruction in an export mode: the residual pass never stores
+ * it; dst 16-byte aligned), 3 = FlashJoLT sketch Omega (m*d x l, bf16 bits).  Requires the
+ * workspace and the blobs of that call to be untouched since. */
 int jolt_debug_export(jolt_ctx *ctx, int what, int cell, void *dst, size_t dst_bytes,
                       jolt_stream stream);
 

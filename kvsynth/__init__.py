@@ -30,6 +30,7 @@ __all__ = ["layer_kv", "make_cache", "f32_to_bf16_bits", "bf16_bits_to_f32",
            "apply_rope", "CONFIGS"]
 
 _ROLE_A, _ROLE_C, _ROLE_F, _ROLE_N, _ROLE_O, _ROLE_ALPHA = 1, 2, 3, 4, 5, 6
+_THREAD_VARS = ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS")
 
 
 def _rng(*key: int) -> np.random.Generator:
@@ -122,11 +123,23 @@ def make_cache(*, n_layers: int, n_heads: int, T: int, d: int, batch: int = 1,
     if workers > 1 and len(jobs) > 1:
         import concurrent.futures as cf
         import multiprocessing as mp
-        with cf.ProcessPoolExecutor(max_workers=min(workers, len(jobs)),
-                                    mp_context=mp.get_context("spawn")) as ex:
-            results = ex.map(_layer_job, [j[2] for j in jobs])
-            for (i, t, _), x in zip(jobs, results):
-                (K, V)[t][i] = x
+        import os
+        # one BLAS thread per worker process: the workers already occupy the cores, and
+        # nested BLAS threads only oversubscribe them (the values do not depend on it)
+        saved = {k: os.environ.get(k) for k in _THREAD_VARS}
+        os.environ.update({k: "1" for k in _THREAD_VARS})
+        try:
+            with cf.ProcessPoolExecutor(max_workers=min(workers, len(jobs)),
+                                        mp_context=mp.get_context("spawn")) as ex:
+                results = ex.map(_layer_job, [j[2] for j in jobs])
+                for (i, t, _), x in zip(jobs, results):
+                    (K, V)[t][i] = x
+        finally:
+            for k, v in saved.items():
+                if v is None:
+                    os.environ.pop(k, None)
+                else:
+                    os.environ[k] = v
     else:
         for i, t, kw in jobs:
             (K, V)[t][i] = _layer_job(kw)

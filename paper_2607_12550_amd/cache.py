@@ -52,7 +52,7 @@ class CacheCodec:
     def __init__(self, K: torch.Tensor, V: torch.Tensor, *, group_layers: int,
                  method: str = "exact", ratio: float = 2.0, q: int = 0, oversample: int = 10,
                  power_iters: int = 1, group: int = 64, bits=(0, 2, 4, 8), step: int = 8,
-                 count_scale_bytes: bool = True, seed: int = 0, max_cells_per_call: int = 16,
+                 count_scale_bytes: bool = True, seed: int = 0, max_cells_per_call: int = 16, r_max: int = 0,
                  workspace_cap_bytes: int = 0, device: int = 0, tau: str = "bound",
                  tau_rT_cap: int | None = None):
         assert K.shape == V.shape and K.dtype == V.dtype and K.is_cuda and K.is_contiguous()
@@ -66,9 +66,9 @@ class CacheCodec:
         self.group_layers, self.ratio, self.group, self.bits, self.step = group_layers, ratio, group, bits, step
         self.count_scale_bytes = count_scale_bytes
         self.method = JOLT_FLASH if method == "flash" else JOLT_EXACT
-        self.opts = SpectrumOpts(self.method, q, float(ratio), oversample, power_iters, 0, 0)
+        self.opts = SpectrumOpts(self.method, q, float(ratio), oversample, power_iters, 0, r_max)
         # compress takes each chunk's spectrum from the workspace its spectrum call filled
-        self.reuse_opts = SpectrumOpts(self.method, q, float(ratio), oversample, power_iters, 1, 0)
+        self.reuse_opts = SpectrumOpts(self.method, q, float(ratio), oversample, power_iters, 1, r_max)
         self.factor_dtype = JOLT_FACTOR_F16 if self.dtype == JOLT_BF16 else JOLT_FACTOR_F32
         self.fbytes = 2 if self.factor_dtype == JOLT_FACTOR_F16 else 4
         self.desc = cell_desc(dtype=self.dtype, n_layers=group_layers, n_heads=H, T=T, d=d,
@@ -108,7 +108,8 @@ class CacheCodec:
         n_ws = n_chunks if n_chunks * ws_bytes <= workspace_cap_bytes else 1
         self.ws_list = [torch.empty(ws_bytes, dtype=torch.uint8, device=K.device) for _ in range(n_ws)]
         self.ws = self.ws_list[0]
-        self.dec_ws = torch.empty(jolt_decompress_workspace_size(self.desc, self.chunk, self.rT_max),
+        # decode workspace: sized for the largest r_T of each allocation (set_params)
+        self.dec_ws = torch.empty(jolt_decompress_workspace_size(self.desc, self.chunk, 0),
                                   dtype=torch.uint8, device=K.device)
         # FlashJoLT sketch width l = min(q + p, T, m d) (section 5); 0 for the exact path
         qq = q or (jolt_q_cap(T, ratio) if self.method == JOLT_FLASH else 0)
@@ -207,6 +208,10 @@ class CacheCodec:
 
     def set_params(self, params):
         self.params = params
+        need = jolt_decompress_workspace_size(self.desc, self.chunk, max(p.r_T for p in params))
+        if need > self.dec_ws.numel():
+            self.dec_ws = None
+            self.dec_ws = torch.empty(need, dtype=torch.uint8, device=self.K.device)
         sizes = [jolt_compressed_size(self.desc, p) for p in params]
         offs, pos = [], 0
         for s in sizes:

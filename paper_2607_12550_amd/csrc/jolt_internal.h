@@ -43,9 +43,14 @@ struct DebugState {
   bool valid = false;
   int n_cells = 0, T = 0, d = 0, m = 0, N = 0, ell = 0;
   std::vector<int> rT, rd;
-  const float *U = nullptr, *Ud = nullptr, *Xt = nullptr;
+  const float *U = nullptr, *Ud = nullptr;
   const uint16_t *Omega = nullptr;
-  int64_t u_stride = 0, ldu = 0, ud_stride = 0, xt_stride = 0, om_stride = 0, ldo = 0;
+  int64_t u_stride = 0, ldu = 0, ud_stride = 0, om_stride = 0, ldo = 0;
+  // the fused reconstruction of the call (its records, device table and arguments)
+  std::vector<FusedCell> fused;
+  FusedCell *fcell_dev = nullptr;
+  FusedArgs fargs{};
+  bool split = false;
 };
 
 struct ProfRecord {

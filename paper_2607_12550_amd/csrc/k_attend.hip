@@ -151,7 +151,7 @@ __global__ void __launch_bounds__(128) k_attend_prep(AttnArgs a) {
   }
   if (tid < kb.rd) qt[tid] = qk;
   float *gk = a.gk + ((int64_t)item * a.n_q + j) * a.rk_max;
-  const float e = kb.rT ? ldexpf(1.f, (int)gptr(kb.gexp)[s]) : 0.f;
+  const int ge = kb.rT ? (int)gptr(kb.gexp)[s] : 0;       // applied per value: 2^ge may not be an fp32
   const int64_t g0 = (int64_t)s * kb.rT * kb.rd;
   for (int i0 = 0; i0 < kb.rT; i0 += ROWS) {
     const int ni = min(ROWS, kb.rT - i0);
@@ -161,7 +161,7 @@ __global__ void __launch_bounds__(128) k_attend_prep(AttnArgs a) {
     for (int i = tid; i < ni; i += 128) {
       float acc = 0.f;
       for (int k = 0; k < kb.rd; ++k) acc = fmaf(fs[i * kb.rd + k], qt[k], acc);
-      gk[i0 + i] = e * acc;
+      gk[i0 + i] = kb.rT ? ldexpf(acc, ge) : 0.f;
     }
   }
 }
@@ -450,7 +450,7 @@ __global__ void __launch_bounds__(256) k_attend_combine(AttnArgs a) {
   }
   __syncthreads();
   // w = 2^e_s (a^T G_s): r_d values, G_s staged by row blocks
-  const float e = vb.rT ? ldexpf(1.f, (int)gptr(vb.gexp)[s]) : 0.f;
+  const int ge = vb.rT ? (int)gptr(vb.gexp)[s] : 0;       // applied per value: 2^ge may not be an fp32
   const int64_t g0 = (int64_t)s * vb.rT * vb.rd;
   const int gcap = max(1, (CG * ncol) / max(vb.rd, 1));          // rows of G_s per staging pass
   float wk = 0.f;
@@ -462,7 +462,7 @@ __global__ void __launch_bounds__(256) k_attend_combine(AttnArgs a) {
     if (tid < vb.rd)
       for (int i = 0; i < ni; ++i) wk = fmaf(av[i0 + i], stage[i * vb.rd + tid], wk);
   }
-  if (tid < vb.rd) w[tid] = e * wk;
+  if (tid < vb.rd) w[tid] = ldexpf(wk, ge);
   // U_d staged whole when it fits the staging area, else read directly
   const bool ud_lds = D * vb.rd <= CG * ncol;
   __syncthreads();

@@ -353,6 +353,14 @@ __global__ void __launch_bounds__(64) k_tri_eigvecs(EigBatch b, InvitWork w, int
   gershgorin(d, e, n, gl, gu, pivmin);
   const double tnorm = fmax(fmax(fabs(gl), fabs(gu)), DBL_MIN);
   const double tiny = DBL_EPSILON * tnorm;
+  bool zero = true;
+  for (int i = 0; i < n && zero; ++i) zero = d[i] == 0.0 && (i == n - 1 || e[i] == 0.0);
+  if (zero) {
+    // the zero matrix (an all-zero cell): every unit vector is an eigenvector; e_j keeps the
+    // k vectors orthonormal without a solve that would divide by the zero pivots
+    for (int i = 0; i < n; ++i) x[(int64_t)i * ld] = i == j ? 1.0 : 0.0;
+    return;
+  }
   // deterministic start vector in [-1, 1]
   for (int i = 0; i < n; ++i) {
     u32x4 r = philox4x32_10(u32x4{(uint32_t)i, (uint32_t)j, (uint32_t)mat, 4u}, 0x6a6f6c74u, 0u);

@@ -171,7 +171,8 @@ __global__ void __launch_bounds__(CB) k_chol_diag(CholArgs a, int kb) {
 #pragma unroll
   for (int c = 0; c < CB; ++c)        // zeros outside the matrix, identity on the padding
     t[c] = (lane < nb && c < nb) ? G[(int64_t)(o + lane) * l + o + c] : (c == lane && lane >= nb ? 1.0 : 0.0);
-  const double floor_piv = fmax(1e-14 * sdmax, 1e-300);
+  // an all-zero Gram (a zero cell) factors as the identity: Q = Y L^-T stays zero and finite
+  const double floor_piv = sdmax > 0.0 ? fmax(1e-14 * sdmax, 1e-300) : 1.0;
   int n_clamped = 0;                   // pivots of this tile raised to the floor
   // column j of the factor is broadcast through LDS (two alternating buffers, so one
   // barrier per column): every lane reads the entries l_kj it needs with independent

@@ -1,0 +1,371 @@
+// Reconstruction fused into the residual and decode passes (section 4: R = X - X~ with X~
+// rebuilt from the stored factors; decoding adds the dequantised, unrotated residual back).
+//
+// For slice s of a cell, X~_s = U^_T W_s with W_s = 2^e_s G^_s U^_d^T (r_T x d).  A small
+// GEMM forms W_s^T (d x r_T, fp32) in the workspace and k_w_exponent picks a power of two
+// 2^k_s with max |W_s| 2^-k_s <= 2^14.  The fused kernel then multiplies, per tile of 128
+// tokens x d features of one slice, on the fp16 matrix cores (v_mfma_f32_32x32x16_f16,
+// fp32 accumulation):
+//   * U^_T is an exact fp16 operand when the factors are stored in fp16; fp32 factors are
+//     scaled by 2^6 and split into hi + lo fp16 terms;
+//   * W_s 2^-k_s is split into hi + lo fp16 terms (hi = fp16(w), lo = fp16(w - hi)), so
+//     |w - hi - lo| <= 2^-22 |w| for entries in the fp16 normal range;
+//   * X~ = 2^(k_s - u) (U_hi (W_hi + W_lo) [+ U_lo W_hi]), u = 6 for split factors, else 0:
+//     two MFMA passes per K step (three for fp32 factors), products exact in fp32.
+// The accumulator tile goes through LDS to the row layout of the residual kernels (a
+// feature row over d/8 lanes) and the epilogue finishes the row in registers:
+//   residual: r = X - X~, rotate (FWHT), group max, fp16 scale, codes, pack;
+//   decode:   dequantise, inverse rotation, + X~, optional RoPE, cast, store;
+//   export:   X~ itself (fp32; the test hook of the closed loop).
+// X~ never reaches HBM: per cache entry the residual pass reads the cache once and writes
+// the codes and scales, the decode pass reads codes and scales and writes the output.
+//
+// Tiles: 128 tokens x d features of one slice per 256-thread workgroup, 4 waves in a
+// WM x WN grid (2 x 2 for d >= 64), K = r_T in steps of 32 (zero-padded).  The 1-D grid
+// is remapped so that each XCD takes a contiguous run of tiles, ordered cell, slice, token
+// block: the token blocks of a slice share W_s, the slices of a cell share U^_T.
+#include "common.h"
+#include "kernels.h"
+#include "rowops.h"
+
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+namespace {
+using namespace rowops;
+
+constexpr int BT = 128, BK = 32, LDK = BK + 8, NT = 256;
+
+template <int D, bool USPLIT>
+struct FusedLds {
+  static constexpr int A = BT * LDK, B = D * LDK;              // halves per operand term
+  static constexpr int OPER = (USPLIT ? 2 : 1) * A + 2 * B;     // A hi [A lo] B hi B lo
+  static constexpr int EPI = BT * (D + 4) * 2;                  // fp32 epilogue tile, in halves
+  static constexpr int HALVES = OPER > EPI ? OPER : EPI;
+};
+
+JOLT_DEV uint16_t h_bits(float x) {
+  _Float16 h = (_Float16)x;
+  uint16_t b;
+  __builtin_memcpy(&b, &h, 2);
+  return b;
+}
+JOLT_DEV float h_val(uint16_t b) {
+  _Float16 h;
+  __builtin_memcpy(&h, &b, 2);
+  return (float)h;
+}
+// x = hi + lo, hi = fp16(x), lo = fp16(x - hi)
+JOLT_DEV void split_f16(float x, uint16_t &hi, uint16_t &lo) {
+  hi = h_bits(x);
+  lo = h_bits(x - h_val(hi));
+}
+JOLT_DEV uint32_t pk2(uint16_t a, uint16_t b) { return (uint32_t)a | ((uint32_t)b << 16); }
+
+// 8 consecutive operand values along k (k0 .. k0 + 7 of row `row`), fp32; zeros beyond
+// the row count or beyond K.  Aligned full runs use 16-byte loads.
+template <bool F32>
+JOLT_DEV void load_run(const void *base, int64_t ld, int row, int rows, int k0, int K, float (&v)[8]) {
+  if (row >= rows || k0 >= K) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = 0.f;
+    return;
+  }
+  if constexpr (F32) {
+    const float *p = reinterpret_cast<const float *>(base) + (int64_t)row * ld + k0;
+    if (k0 + 8 <= K && (reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+      const jf4 a = gload_f4(p), b = gload_f4(p + 4);
+      v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = k0 + i < K ? gptr(p)[i] : 0.f;
+    }
+  } else {
+    const uint16_t *p = reinterpret_cast<const uint16_t *>(base) + (int64_t)row * ld + k0;
+    if (k0 + 8 <= K && (reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+      const ju4 u = gload_u4(p);
+      const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        v[2 * i] = h_val((uint16_t)(w[i] & 0xffffu));
+        v[2 * i + 1] = h_val((uint16_t)(w[i] >> 16));
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = k0 + i < K ? h_val(gptr(p)[i]) : 0.f;
+    }
+  }
+}
+
+template <int D, int MODE, typename TIO, bool USPLIT, bool ROPE>
+__global__ void __launch_bounds__(NT, 2) k_fused(FusedArgs a) {
+  constexpr int WN = D >= 64 ? 2 : 1, WM = 4 / WN;
+  constexpr int WR = BT / WM, WC = D / WN;          // wave tile
+  constexpr int MI = WR / 32, NI = WC / 32;         // 32 x 32 MFMA blocks per wave
+  constexpr int L = RowLayout<D>::L, R = RowLayout<D>::R;
+  using Lds = FusedLds<D, USPLIT>;
+  __shared__ __attribute__((aligned(16))) uint16_t lds[Lds::HALVES];
+  uint16_t *sa = lds, *sa_lo = lds + Lds::A, *sb = lds + (USPLIT ? 2 : 1) * Lds::A, *sb_lo = sb + Lds::B;
+
+  // tile: XCD-contiguous order (cell, slice, token block)
+  const int i = blockIdx.x, j = (i & 7) * a.per_xcd + (i >> 3);
+  if (j >= a.total) return;
+  const int per_cell = a.m * a.tiles_t;
+  const int cell = j / per_cell, rem = j - cell * per_cell;
+  const int s = rem / a.tiles_t, t0 = (rem - s * a.tiles_t) * BT;
+  const FusedCell c = a.cells[cell];
+  if (MODE == FUSED_RESIDUAL && c.bits == 0) return;
+  const int rT = c.rT, T = a.T;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN, lr = lane & 31, lh = lane >> 5;
+
+  f32x16_t acc[MI][NI];
+#pragma unroll
+  for (int x = 0; x < MI; ++x)
+#pragma unroll
+    for (int y = 0; y < NI; ++y)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[x][y][q] = 0.f;
+
+  int ks = 0;                              // X~ = 2^(ks - u) acc, applied per value
+  if (rT > 0) {
+    ks = c.wexp[s];
+    const float *W = c.Wt + (int64_t)s * D * c.ldw;
+    // operand units of 8 k values: A has BT rows x 4 units, B has D rows x 4 units
+    constexpr int AU = BT * (BK / 8) / NT, BU = D * (BK / 8) / NT > 0 ? D * (BK / 8) / NT : 1;
+    float ra[AU][8], rb[BU][8];
+    auto fetch = [&](int k0) {
+#pragma unroll
+      for (int q = 0; q < AU; ++q) {
+        const int u = tid + NT * q, r = u >> 2, kc = (u & 3) * 8;
+        load_run<USPLIT>(c.UT, rT, t0 + r, T, k0 + kc, rT, ra[q]);
+      }
+#pragma unroll
+      for (int q = 0; q < BU; ++q) {
+        const int u = tid + NT * q, r = u >> 2, kc = (u & 3) * 8;
+        if (u < D * (BK / 8)) load_run<true>(W, c.ldw, r, D, k0 + kc, rT, rb[q]);
+      }
+    };
+    auto stash = [&]() {
+#pragma unroll
+      for (int q = 0; q < AU; ++q) {
+        const int u = tid + NT * q, r = u >> 2, kc = (u & 3) * 8;
+        uint16_t h[8], l[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          if constexpr (USPLIT) split_f16(ra[q][e] * 64.f, h[e], l[e]);
+          else h[e] = h_bits(ra[q][e]);        // exact: the value came from fp16
+        }
+        *reinterpret_cast<uint4 *>(sa + r * LDK + kc) = make_uint4(pk2(h[0], h[1]), pk2(h[2], h[3]), pk2(h[4], h[5]), pk2(h[6], h[7]));
+        if constexpr (USPLIT)
+          *reinterpret_cast<uint4 *>(sa_lo + r * LDK + kc) = make_uint4(pk2(l[0], l[1]), pk2(l[2], l[3]), pk2(l[4], l[5]), pk2(l[6], l[7]));
+      }
+#pragma unroll
+      for (int q = 0; q < BU; ++q) {
+        const int u = tid + NT * q, r = u >> 2, kc = (u & 3) * 8;
+        if (u >= D * (BK / 8)) continue;
+        uint16_t h[8], l[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) split_f16(ldexpf(rb[q][e], -ks), h[e], l[e]);
+        *reinterpret_cast<uint4 *>(sb + r * LDK + kc) = make_uint4(pk2(h[0], h[1]), pk2(h[2], h[3]), pk2(h[4], h[5]), pk2(h[6], h[7]));
+        *reinterpret_cast<uint4 *>(sb_lo + r * LDK + kc) = make_uint4(pk2(l[0], l[1]), pk2(l[2], l[3]), pk2(l[4], l[5]), pk2(l[6], l[7]));
+      }
+    };
+    fetch(0);
+    for (int k0 = 0; k0 < rT; k0 += BK) {
+      __syncthreads();                     // the previous step's fragments have been read
+      stash();
+      __syncthreads();
+      if (k0 + BK < rT) fetch(k0 + BK);    // in flight during the MFMAs below
+#pragma unroll
+      for (int ks = 0; ks < BK / 16; ++ks) {
+        const int ko = ks * 16 + 8 * lh;
+        f16x8_t fa[MI], fl[MI], fb[NI], fbl[NI];
+#pragma unroll
+        for (int x = 0; x < MI; ++x) {
+          const int ra_ = (wm * WR + x * 32 + lr) * LDK + ko;
+          fa[x] = *reinterpret_cast<const f16x8_t *>(sa + ra_);
+          if constexpr (USPLIT) fl[x] = *reinterpret_cast<const f16x8_t *>(sa_lo + ra_);
+        }
+#pragma unroll
+        for (int y = 0; y < NI; ++y) {
+          const int rb_ = (wn * WC + y * 32 + lr) * LDK + ko;
+          fb[y] = *reinterpret_cast<const f16x8_t *>(sb + rb_);
+          fbl[y] = *reinterpret_cast<const f16x8_t *>(sb_lo + rb_);
+        }
+#pragma unroll
+        for (int x = 0; x < MI; ++x)
+#pragma unroll
+          for (int y = 0; y < NI; ++y) {
+            acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[x], fb[y], acc[x][y], 0, 0, 0);
+            acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[x], fbl[y], acc[x][y], 0, 0, 0);
+            if constexpr (USPLIT)
+              acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fl[x], fb[y], acc[x][y], 0, 0, 0);
+          }
+      }
+    }
+  }
+  // accumulators -> LDS tile [BT][D + 4] (fp32): acc[x][y][q] is row
+  // wm WR + x 32 + 8 (q / 4) + 4 lh + q % 4, column wn WC + y 32 + lr
+  constexpr int ELD = D + 4;
+  float *E = reinterpret_cast<float *>(lds);
+  __syncthreads();
+#pragma unroll
+  for (int x = 0; x < MI; ++x)
+#pragma unroll
+    for (int y = 0; y < NI; ++y)
+#pragma unroll
+      for (int q = 0; q < 16; ++q)
+        E[(wm * WR + x * 32 + 8 * (q >> 2) + 4 * lh + (q & 3)) * ELD + wn * WC + y * 32 + lr] = acc[x][y][q];
+  __syncthreads();
+
+  // epilogue: wave w finishes rows 32 w .. 32 w + 31 of the tile, R rows at a time
+  const int row_in_wave = lane / L, lane_in_row = lane % L;
+  const float *sg = a.signs + (int64_t)cell * D + lane_in_row * 8;
+  float sgv[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) sgv[e] = sg[e];
+  double theta[8];
+  if constexpr (ROPE) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int jj = (lane_in_row * 8 + e) % (D / 2);
+      theta[e] = exp2(-(2.0 * jj / D) * a.rope_log2_base);
+    }
+  }
+  const int gl = a.group / 8;
+  const int64_t srow = (int64_t)(s / a.heads) * a.s_layer + (int64_t)(s % a.heads) * a.s_head;
+#pragma unroll 2
+  for (int p = 0; p < 32 / R; ++p) {
+    const int r = wave * 32 + p * R + row_in_wave, t = t0 + r;
+    if (t >= T) continue;                  // whole rows (L lanes) drop out together
+    float xt[8];
+    {
+      const jf4 u0 = *reinterpret_cast<const jf4 *>(E + r * ELD + lane_in_row * 8);
+      const jf4 u1 = *reinterpret_cast<const jf4 *>(E + r * ELD + lane_in_row * 8 + 4);
+      xt[0] = u0.x; xt[1] = u0.y; xt[2] = u0.z; xt[3] = u0.w; xt[4] = u1.x; xt[5] = u1.y; xt[6] = u1.z; xt[7] = u1.w;
+      const int xe = ks - (USPLIT ? 6 : 0);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xt[e] = rT > 0 ? ldexpf(xt[e], xe) : 0.f;   // exact
+    }
+    const int64_t elem = ((int64_t)s * T + t) * D + lane_in_row * 8;
+    if constexpr (MODE == FUSED_XTILDE) {
+      store8(c.xt_out + elem, xt);
+    } else if constexpr (MODE == FUSED_RESIDUAL) {
+      float v[8];
+      load8<TIO>(reinterpret_cast<const TIO *>(c.x) + srow + (int64_t)t * a.s_tok + lane_in_row * 8, v);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = (v[e] - xt[e]) * sgv[e];
+      fwht_row<D>(v, lane_in_row);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] *= a.inv_sqrt_d;
+      uint32_t code[8];
+      float delta;
+      quantize8(v, c.bits, gl, code, delta);
+      store_codes(c.codes, elem, c.bits, code);
+      if ((lane_in_row % gl) == 0) c.scales[elem / a.group] = h_bits(delta);
+    } else {
+      float v[8];
+      if (c.bits) {
+        uint32_t code[8];
+        load_codes(c.codes, elem, c.bits, code);
+        const float delta = h_val(c.scales[elem / a.group]);
+        const float mid = 0.5f * (float)((1 << c.bits) - 1);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = ((float)code[e] - mid) * delta;
+        fwht_row<D>(v, lane_in_row);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = xt[e] + sgv[e] * (v[e] * a.inv_sqrt_d);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = xt[e];
+      }
+      if constexpr (ROPE) rope_row<D>(v, lane_in_row, (double)(t + a.rope_offset), theta);
+      store8(reinterpret_cast<TIO *>(c.out) + srow + (int64_t)t * a.s_tok + lane_in_row * 8, v);
+    }
+  }
+}
+
+// k_s of every (cell, slice): the smallest power of two with max |W_s| 2^-k_s <= 2^14
+// (0 for an all-zero slice or a cell without backbone); one workgroup per (slice, cell).
+__global__ void __launch_bounds__(256) k_w_exponent(const FusedCell *cells, int m, int d) {
+  const int s = blockIdx.x, cell = blockIdx.y;
+  const FusedCell &c = cells[cell];
+  if (s >= m) return;
+  float mx = 0.f;
+  if (c.rT > 0) {
+    const float *W = c.Wt + (int64_t)s * d * c.ldw;
+    for (int q = threadIdx.x; q < d * c.rT; q += 256) {
+      const int f = q / c.rT, k = q - f * c.rT;
+      mx = fmaxf(mx, fabsf(W[(int64_t)f * c.ldw + k]));
+    }
+  }
+  for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  __shared__ float red[4];
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    int e = 0;
+    if (mx > 0.f) {
+      int ex;
+      const float f = frexpf(mx, &ex);            // mx = f 2^ex, 0.5 <= f < 1
+      e = (f == 0.5f ? ex - 1 : ex) - 14;          // ceil(log2 mx) - 14
+    }
+    c.wexp[s] = e;
+  }
+}
+
+template <int D, int MODE, typename TIO, bool USPLIT>
+hipError_t launch_mode(const FusedArgs &a, bool rope, hipStream_t st) {
+  const dim3 grid((unsigned)(a.per_xcd * 8)), block(NT);
+  if constexpr (MODE == FUSED_DECODE) {
+    if (rope) {
+      hipLaunchKernelGGL((k_fused<D, MODE, TIO, USPLIT, true>), grid, block, 0, st, a);
+      return hipGetLastError();
+    }
+  }
+  hipLaunchKernelGGL((k_fused<D, MODE, TIO, USPLIT, false>), grid, block, 0, st, a);
+  return hipGetLastError();
+}
+
+template <int D, int MODE>
+hipError_t launch_d(const FusedArgs &a, int io_dtype, bool split, bool rope, hipStream_t st) {
+  if (MODE == FUSED_XTILDE || io_dtype == JOLT_F32)
+    return split ? launch_mode<D, MODE, float, true>(a, rope, st) : launch_mode<D, MODE, float, false>(a, rope, st);
+  return split ? launch_mode<D, MODE, bf16_t, true>(a, rope, st) : launch_mode<D, MODE, bf16_t, false>(a, rope, st);
+}
+
+template <int MODE>
+hipError_t launch_m(const FusedArgs &a, int d, int io_dtype, bool split, bool rope, hipStream_t st) {
+  switch (d) {
+    case 32: return launch_d<32, MODE>(a, io_dtype, split, rope, st);
+    case 64: return launch_d<64, MODE>(a, io_dtype, split, rope, st);
+    case 128: return launch_d<128, MODE>(a, io_dtype, split, rope, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+int fused_tile_tokens() { return BT; }
+
+hipError_t launch_w_exponent(const FusedCell *cells_dev, int n_cells, int m, int d, hipStream_t st) {
+  if (n_cells <= 0 || m <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_w_exponent, dim3(m, n_cells), dim3(256), 0, st, cells_dev, m, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_fused(FusedArgs a, int mode, int d, int io_dtype, bool split_factors, hipStream_t st) {
+  a.tiles_t = (a.T + BT - 1) / BT;
+  const int64_t total = (int64_t)a.n_cells * a.m * a.tiles_t;
+  if (total <= 0) return hipSuccess;
+  if (total > (int64_t)1 << 30) return hipErrorInvalidValue;
+  a.total = (int32_t)total;
+  a.per_xcd = (int32_t)((total + 7) / 8);
+  const bool rope = a.rope != 0 && mode == FUSED_DECODE;
+  if (mode == FUSED_RESIDUAL) return launch_m<FUSED_RESIDUAL>(a, d, io_dtype, split_factors, false, st);
+  if (mode == FUSED_DECODE) return launch_m<FUSED_DECODE>(a, d, io_dtype, split_factors, rope, st);
+  if (mode == FUSED_XTILDE) return launch_m<FUSED_XTILDE>(a, d, JOLT_F32, split_factors, false, st);
+  return hipErrorInvalidValue;
+}

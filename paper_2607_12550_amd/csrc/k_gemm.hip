@@ -166,8 +166,9 @@ __global__ void __launch_bounds__(NT) k_gemm(const GemmProblem *__restrict__ pro
     }
   }
 
-  float alpha = P.alpha;
-  if (P.alpha_exp2) alpha = ldexpf(alpha, (int)*gptr(P.alpha_exp2));
+  // alpha 2^e is applied as ldexp(alpha * acc, e): 2^e alone may lie outside fp32's range
+  const float alpha = P.alpha;
+  const int aexp = P.alpha_exp2 ? (int)*gptr(P.alpha_exp2) : 0;
   // Epilogue through LDS, 32 rows at a time (one MFMA row block of one wave row per round),
   // so that C is read (beta != 0) and written as float4 rows: acc[i][j][q] is the output at
   // row wm*64 + i*32 + 8*(q/4) + 4*lh + q%4, column wn*64 + j*32 + lr of the tile.
@@ -195,7 +196,8 @@ __global__ void __launch_bounds__(NT) k_gemm(const GemmProblem *__restrict__ pro
       const int row = m0 + h * 32 + rr, col = n0 + cc;
       if (row >= P.M || col >= P.N) continue;
       const float4 a4 = *reinterpret_cast<const float4 *>(&cs[rr * CLD + cc]);
-      float v[4] = {alpha * a4.x, alpha * a4.y, alpha * a4.z, alpha * a4.w};
+      float v[4] = {ldexpf(alpha * a4.x, aexp), ldexpf(alpha * a4.y, aexp), ldexpf(alpha * a4.z, aexp),
+                     ldexpf(alpha * a4.w, aexp)};
       JOLT_GLOBAL float *dst = gptr(P.C + (int64_t)row * P.ldc + col);
       if (vec && col + 4 <= P.N) {
         if (use_beta) {

@@ -346,8 +346,9 @@ __global__ void __launch_bounds__(NT) k_gemm16(const GemmProblem *__restrict__ p
     compute_at(0);
   }
 
-  float alpha = P.alpha;
-  if (P.alpha_exp2) alpha = ldexpf(alpha, (int)*gptr(P.alpha_exp2));
+  // alpha 2^e is applied as ldexp(alpha * acc, e): 2^e alone may lie outside fp32's range
+  const float alpha = P.alpha;
+  const int aexp = P.alpha_exp2 ? (int)*gptr(P.alpha_exp2) : 0;
   // epilogue through LDS, 32 rows per round: acc[a][b][q] is the output at row
   // wm*(BM/2) + a*32 + 8*(q/4) + 4*lh + q%4, column wn*64 + b*32 + lr of the tile
   float *cs = reinterpret_cast<float *>(&sm);
@@ -379,7 +380,7 @@ __global__ void __launch_bounds__(NT) k_gemm16(const GemmProblem *__restrict__ p
         if (col >= P.N || row >= P.M) continue;
         float v[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = alpha * cs[(rr + e) * CLD + cc];
+        for (int e = 0; e < 4; ++e) v[e] = ldexpf(alpha * cs[(rr + e) * CLD + cc], aexp);
         JOLT_GLOBAL float *dst = gptr(P.C + (int64_t)col * P.ldc + row);
         if (vec && row + 4 <= P.M) {
           if (use_beta) {
@@ -396,7 +397,8 @@ __global__ void __launch_bounds__(NT) k_gemm16(const GemmProblem *__restrict__ p
       } else {
         if (row >= P.M || col >= P.N) continue;
         const float4 a4 = *reinterpret_cast<const float4 *>(&cs[rr * CLD + cc]);
-        float v[4] = {alpha * a4.x, alpha * a4.y, alpha * a4.z, alpha * a4.w};
+        float v[4] = {ldexpf(alpha * a4.x, aexp), ldexpf(alpha * a4.y, aexp), ldexpf(alpha * a4.z, aexp),
+                     ldexpf(alpha * a4.w, aexp)};
         JOLT_GLOBAL float *dst = gptr(P.C + (int64_t)row * P.ldc + col);
         if (vec && col + 4 <= P.N) {
           if (use_beta) {

@@ -43,10 +43,10 @@ __global__ void __launch_bounds__(256) k_core_pack(SerCore a) {
   int e = 0;
   if (c.f16 && mx > 0.f) e = max(-128, ceil_log2_f(mx) - 15);
   if (threadIdx.x == 0) c.gexp[s] = (int8_t)e;
-  const float sc = ldexpf(1.f, -e);
+  // the power of two is applied to each value (2^-e itself may lie outside fp32's range)
   for (int q = threadIdx.x; q < rT * rd; q += 256) {
     const int r = q / rd, k = q % rd;
-    const float v = G[(int64_t)r * c.g_ld + k] * sc;
+    const float v = ldexpf(G[(int64_t)r * c.g_ld + k], -e);
     const int64_t o = ((int64_t)s * rT + r) * rd + k;
     if (c.f16) reinterpret_cast<uint16_t *>(c.G_out)[o] = f32_to_f16_bits(v);
     else reinterpret_cast<float *>(c.G_out)[o] = v;

@@ -7,44 +7,7 @@
 
 #include "../../include/jolt.h"
 
-// ----------------------------------------------------------------- residual / decode
-struct ResidCell {
-  const void *x;        // cell base pointer (bf16 or fp32)
-  const float *xt;      // X~ (m x T x d fp32, contiguous) or null (no backbone)
-  uint16_t *scales;     // fp16 bits, one per group
-  uint8_t *codes;       // packed codes
-  int32_t bits;
-  int32_t pad;
-};
-
-struct ResidArgs {
-  const ResidCell *cells;   // device array [n_cells]
-  const float *signs;       // device [n_cells][d]
-  int32_t n_cells, m, T, heads, group;
-  int64_t s_layer, s_head, s_tok;
-  float inv_sqrt_d;
-};
-
-struct DecodeCell {
-  const uint8_t *codes;
-  const uint16_t *scales;
-  const float *xt;          // X~ or null
-  void *out;                // output cell base (bf16 or fp32)
-  int32_t bits;
-  int32_t pad;
-};
-
-struct DecodeArgs {
-  const DecodeCell *cells;
-  const float *signs;
-  int32_t n_cells, m, T, heads, group;
-  int64_t s_layer, s_head, s_tok;
-  float inv_sqrt_d;
-  int32_t rope;             // 1: rotate feature pairs (j, j + d/2) by position t + rope_offset
-  int32_t rope_offset;
-  double rope_log2_base;    // log2 of the rotary base
-};
-
+// ----------------------------------------------------------------- residual calibration
 struct Eps2Args {
   uint64_t seed;
   int64_t n_samples;
@@ -53,8 +16,36 @@ struct Eps2Args {
   double *partials;         // [blocks][4]
 };
 
-hipError_t launch_residual_quant(const ResidArgs &a, int d, int in_dtype, hipStream_t st);
-hipError_t launch_decode(const DecodeArgs &a, int d, int out_dtype, hipStream_t st);
+
+// ----------------------------------------------------------------- fused reconstruction
+// X~_s = U^_T W_s rebuilt on the fp16 matrix cores inside the residual / decode passes.
+struct FusedCell {
+  const void *UT;           // blob U_T section: T x rT, fp16 or fp32 (the call's factor type)
+  const float *Wt;          // m slices of d x ldw fp32: W_s^T = 2^e_s U^_d G^_s^T
+  int32_t *wexp;            // m per-slice exponents k_s (written by launch_w_exponent)
+  const void *x;            // residual: cache cell base (strided, input type)
+  void *out;                // decode: output cell base (strided, output type)
+  uint8_t *codes;           // packed codes (written by the residual pass, read by decode)
+  uint16_t *scales;         // fp16 group scales
+  float *xt_out;            // export: X~ (m x T x d fp32, contiguous)
+  int32_t rT, bits, ldw, pad;
+};
+enum { FUSED_RESIDUAL = 0, FUSED_DECODE = 1, FUSED_XTILDE = 2 };
+struct FusedArgs {
+  const FusedCell *cells;   // device [n_cells]
+  const float *signs;       // device [n_cells][d]
+  int32_t n_cells, m, T, heads, group;
+  int32_t tiles_t, total, per_xcd;    // set by launch_fused
+  int64_t s_layer, s_head, s_tok;     // cell strides (input for the residual, output for decode)
+  float inv_sqrt_d;
+  int32_t rope, rope_offset, pad;
+  double rope_log2_base;
+};
+int fused_tile_tokens();
+hipError_t launch_w_exponent(const FusedCell *cells_dev, int n_cells, int m, int d, hipStream_t st);
+// io_dtype: the cache type (residual) or the output type (decode); split_factors: the
+// factors are fp32 (U_T split into two fp16 terms)
+hipError_t launch_fused(FusedArgs a, int mode, int d, int io_dtype, bool split_factors, hipStream_t st);
 hipError_t launch_rotation_signs(const uint64_t *seeds_dev, int n_cells, int d, float *signs,
                                  hipStream_t st);
 int eps2_blocks();

@@ -47,8 +47,8 @@ struct Ws {
   // tables
   GemmProblem *tab = nullptr;
   size_t tab_n = 0;
-  ResidCell *rcell = nullptr;
-  DecodeCell *dcell = nullptr;
+  FusedCell *fcell_r = nullptr;   // per-cell records of the fused reconstruction passes
+  int32_t *wexp = nullptr;         // [cell][slice] exponents of W_s
   FGramCell *fcell = nullptr;
   SerCell *scell = nullptr;
   SerFactorCell *sfcell = nullptr;
@@ -67,7 +67,8 @@ struct Ws {
   float *U = nullptr;  // token factor, T x kmaxT per cell
   int kmaxT = 0;
   // ST-HOSVD / reconstruction
-  float *Y = nullptr, *G = nullptr, *W = nullptr, *Xt = nullptr;
+  float *Y = nullptr, *G = nullptr, *W = nullptr;   // W: W_s^T (d x ldw) per slice
+  int ldw = 0;
   // FlashJoLT
   int ldo = 0, ldl = 0, g64_chunks = 0;
   uint16_t *Om = nullptr;                 // sketch, N x ldo bf16 per cell
@@ -113,8 +114,8 @@ void plan(Carver &cv, Ws &w, const SpecShape &sh, int nc) {
   // split-K Gram of up to kGramSplitMax chunks per cell)
   if (sh.method == JOLT_FLASH) w.tab_n += (size_t)nc * (160 + 33 * kGramSplitMax);
   w.tab = cv.take<GemmProblem>(w.tab_n);
-  w.rcell = cv.take<ResidCell>(nc);
-  w.dcell = cv.take<DecodeCell>(nc);
+  w.fcell_r = cv.take<FusedCell>(nc);
+  w.wexp = cv.take<int32_t>((size_t)nc * m);
   w.fcell = cv.take<FGramCell>(nc);
   w.scell = cv.take<SerCell>(nc);
   w.sfcell = cv.take<SerFactorCell>(2 * nc);
@@ -157,20 +158,23 @@ void plan(Carver &cv, Ws &w, const SpecShape &sh, int nc) {
   w.U = cv.take<float>((size_t)nc * T * std::max(w.kmaxT, 1));
   w.Y = cv.take<float>((size_t)nc * std::max(w.kmaxT, 1) * N);
   w.G = cv.take<float>((size_t)nc * m * std::max(w.kmaxT, 1) * d);
-  w.W = cv.take<float>((size_t)nc * m * std::max(w.kmaxT, 1) * d);
-  w.Xt = cv.take<float>((size_t)nc * m * T * d);
+  w.ldw = (std::max(w.kmaxT, 1) + 7) / 8 * 8;
+  w.W = cv.take<float>((size_t)nc * m * d * w.ldw);
 }
 
-// decode-only areas: problem table, per-cell records, rotation signs, W_s = G_s U_d^T and X~
+// decode-only areas: problem table, per-cell records, rotation signs, W_s^T = 2^e U_d G_s^T
+// and its exponents (X~ itself is never stored)
 void plan_decode(Carver &cv, Ws &w, int m, int T, int d, int nc, int kmax) {
+  (void)T;
   w.tab_n = 64 + 2 * (size_t)nc * m;
   w.tab = cv.take<GemmProblem>(w.tab_n);
-  w.dcell = cv.take<DecodeCell>(nc);
+  w.fcell_r = cv.take<FusedCell>(nc);
+  w.wexp = cv.take<int32_t>((size_t)nc * m);
   w.seeds = cv.take<uint64_t>(nc);
   w.signs = cv.take<float>((size_t)nc * d);
   w.kmaxT = std::max(kmax, 1);
-  w.W = cv.take<float>((size_t)nc * m * w.kmaxT * d);
-  w.Xt = kmax ? cv.take<float>((size_t)nc * m * T * d) : nullptr;
+  w.ldw = (w.kmaxT + 7) / 8 * 8;
+  w.W = cv.take<float>((size_t)nc * m * d * w.ldw);
 }
 
 int dtype_gt(int dt) { return dt == JOLT_BF16 ? GT_BF16 : GT_F32; }
@@ -414,6 +418,60 @@ int token_exact(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc,
 
 int spectrum_device(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, int nc,
                     const void *const *X, const uint64_t *seeds, const jolt_spectrum_opts *o);
+
+// Sections of one blob that the reconstruction reads.
+struct BlobView {
+  const uint8_t *b;
+  BlobLayout L;
+  int rT, rd, bits;
+};
+
+// W_s^T = 2^e_s U^_d G^_s^T (d x r_T per slice, leading dimension ldw) of every cell with a
+// backbone, from the stored factors, then the per-slice exponents k_s of the fused passes.
+// fc: the host records of the call (uploaded here); fb: bytes per stored factor scalar.
+int build_w(Run &R, int nc, int m, int d, const std::vector<BlobView> &bv, const std::vector<FusedCell> &fc,
+            int fb) {
+  const int ft = fb == 2 ? GT_F16 : GT_F32;
+  HIP_OK(hipMemcpyAsync(R.w.fcell_r, fc.data(), nc * sizeof(FusedCell), hipMemcpyHostToDevice, R.st));
+  std::vector<GemmProblem> P;
+  for (int c = 0; c < nc; ++c) {
+    const BlobView &v = bv[c];
+    if (!v.rT) continue;
+    for (int s = 0; s < m; ++s) {
+      GemmProblem p{};
+      p.A = plain(v.b + v.L.Ud, v.rd);                                     // A(f, j) = Ud[f][j]
+      p.B = plain(v.b + v.L.G + (int64_t)s * v.rT * v.rd * fb, v.rd);      // B(j, i) = G_s[i][j]
+      p.C = const_cast<float *>(fc[c].Wt) + (int64_t)s * d * R.w.ldw; p.ldc = R.w.ldw;
+      p.M = d; p.N = v.rT; p.K = v.rd; p.alpha = 1.f;
+      p.alpha_exp2 = reinterpret_cast<const int8_t *>(v.b + v.L.gexp + s);
+      P.push_back(p);
+    }
+  }
+  int rc = R.gemm(P, 1, ft, ft, true, true);
+  if (rc) return rc;
+  HIP_OK(launch_w_exponent(R.w.fcell_r, nc, m, d, R.st));
+  return JOLT_OK;
+}
+
+FusedCell fused_cell(Run &R, int c, int m, int d, const BlobView &v) {
+  FusedCell f{};
+  f.UT = v.b + v.L.UT;
+  f.Wt = R.w.W + (int64_t)c * m * d * R.w.ldw;
+  f.wexp = R.w.wexp + (int64_t)c * m;
+  f.codes = const_cast<uint8_t *>(v.b + v.L.codes);
+  f.scales = reinterpret_cast<uint16_t *>(const_cast<uint8_t *>(v.b + v.L.scales));
+  f.rT = v.rT; f.bits = v.bits; f.ldw = R.w.ldw;
+  return f;
+}
+
+FusedArgs fused_args(Run &R, int nc, int m, int T, int d, int group, const jolt_cell_desc *strides) {
+  FusedArgs a{};
+  a.cells = R.w.fcell_r; a.signs = R.w.signs;
+  a.n_cells = nc; a.m = m; a.T = T; a.heads = strides->n_heads; a.group = group;
+  a.s_layer = strides->stride_layer; a.s_head = strides->stride_head; a.s_tok = strides->stride_token;
+  a.inv_sqrt_d = (float)(1.0 / std::sqrt((double)d));
+  return a;
+}
 
 }  // namespace
 
@@ -793,7 +851,6 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
   const int64_t ldu = R.w.kmaxT, u_stride = (int64_t)T * R.w.kmaxT;
   const int64_t y_stride = (int64_t)R.w.kmaxT * N;
   const int64_t g_stride = (int64_t)m * R.w.kmaxT * d, g_slice = (int64_t)R.w.kmaxT * d;
-  const int64_t xt_stride = (int64_t)m * T * d;
   const bool f16 = params[0].factor_dtype == JOLT_FACTOR_F16;
   const int fb = f16 ? 2 : 4, ft = f16 ? GT_F16 : GT_F32;
   std::vector<BlobLayout> L(nc);
@@ -903,58 +960,28 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
   // zero exponents of cells without a backbone (the section is still present)
   for (int c = 0; c < nc; ++c)
     if (!rT[c]) HIP_OK(hipMemsetAsync(static_cast<uint8_t *>(blobs[c]) + L[c].gexp, 0, m, R.st));
-  // X~ from the stored factors: W_s = 2^e_s G^_s U^_d^T, X~_s = U^_T W_s
-  if (kmax > 0) {
-    StageTimer t(R.ctx, R.st, JOLT_STAGE_RECONSTRUCT);
-    std::vector<GemmProblem> P;
-    for (int c = 0; c < nc; ++c) {
-      if (!rT[c]) continue;
-      const uint8_t *b = static_cast<const uint8_t *>(blobs[c]);
-      for (int s = 0; s < m; ++s) {
-        GemmProblem p{};
-        p.A = plain(b + L[c].G + (int64_t)s * rT[c] * rd[c] * fb, rd[c]);   // k-contiguous
-        p.B = plain(b + L[c].Ud, rd[c]);                                    // B(k=j, n=f) = Ud[f][j]
-        p.C = R.w.W + c * g_stride + s * g_slice; p.ldc = d;
-        p.M = rT[c]; p.N = d; p.K = rd[c]; p.alpha = 1.f;
-        p.alpha_exp2 = reinterpret_cast<const int8_t *>(b + L[c].gexp + s);
-        P.push_back(p);
-      }
-    }
-    rc = R.gemm(P, 1, ft, ft, true, true);
-    if (rc) return rc;
-    P.clear();
-    for (int c = 0; c < nc; ++c) {
-      if (!rT[c]) continue;
-      const uint8_t *b = static_cast<const uint8_t *>(blobs[c]);
-      for (int s = 0; s < m; ++s) {
-        GemmProblem p{};
-        p.A = plain(b + L[c].UT, rT[c]);                                    // k-contiguous
-        p.B = plain(R.w.W + c * g_stride + s * g_slice, d);                 // n-contiguous
-        p.C = R.w.Xt + c * xt_stride + (int64_t)s * T * d; p.ldc = d;
-        p.M = T; p.N = d; p.K = rT[c]; p.alpha = 1.f;
-        P.push_back(p);
-      }
-    }
-    rc = R.gemm(P, 1, ft, GT_F32, true, false);
-    if (rc) return rc;
-  }
-  // residual + rotation + quantisation + packing
-  std::vector<ResidCell> rcells(nc);
+  // residual against X~ = U^_T W_s rebuilt from the stored factors inside the fused pass:
+  // W_s^T and its exponents first, then reconstruction + rotation + quantisation + packing
+  std::vector<BlobView> bv(nc);
+  std::vector<FusedCell> fc(nc);
   bool any_bits = false;
   for (int c = 0; c < nc; ++c) {
-    uint8_t *b = static_cast<uint8_t *>(blobs[c]);
-    rcells[c] = ResidCell{X[c], rT[c] ? R.w.Xt + c * xt_stride : nullptr,
-                          reinterpret_cast<uint16_t *>(b + L[c].scales), b + L[c].codes, params[c].bits, 0};
+    bv[c] = BlobView{static_cast<const uint8_t *>(blobs[c]), L[c], rT[c], rd[c], params[c].bits};
+    fc[c] = fused_cell(R, c, m, d, bv[c]);
+    fc[c].x = X[c];
     any_bits |= params[c].bits != 0;
   }
+  if (kmax > 0) {
+    StageTimer t(R.ctx, R.st, JOLT_STAGE_RECONSTRUCT);
+    rc = build_w(R, nc, m, d, bv, fc, fb);
+    if (rc) return rc;
+  } else {
+    HIP_OK(hipMemcpyAsync(R.w.fcell_r, fc.data(), nc * sizeof(FusedCell), hipMemcpyHostToDevice, R.st));
+  }
   if (any_bits) {
-    HIP_OK(hipMemcpyAsync(R.w.rcell, rcells.data(), nc * sizeof(ResidCell), hipMemcpyHostToDevice, R.st));
-    ResidArgs ra{};
-    ra.cells = R.w.rcell; ra.signs = R.w.signs; ra.n_cells = nc; ra.m = m; ra.T = T;
-    ra.heads = desc->n_heads; ra.group = params[0].group; ra.s_layer = desc->stride_layer;
-    ra.s_head = desc->stride_head; ra.s_tok = desc->stride_token; ra.inv_sqrt_d = (float)(1.0 / std::sqrt((double)d));
     StageTimer t(R.ctx, R.st, JOLT_STAGE_RESIDUAL);
-    HIP_OK(launch_residual_quant(ra, d, desc->dtype, R.st));
+    HIP_OK(launch_fused(fused_args(R, nc, m, T, d, params[0].group, desc), FUSED_RESIDUAL, d, desc->dtype,
+                        !f16, R.st));
   }
   // headers
   std::vector<uint8_t> hdr((size_t)nc * kHeaderBytes);
@@ -978,7 +1005,11 @@ extern "C" int jolt_compress(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
   dbg.rT = rT; dbg.rd = rd;
   dbg.U = R.w.U; dbg.u_stride = u_stride; dbg.ldu = ldu;
   dbg.Ud = R.w.Ud; dbg.ud_stride = (int64_t)d * d;
-  dbg.Xt = R.w.Xt; dbg.xt_stride = xt_stride;
+  // the X~ export re-runs the fused pass in its export mode on this call's W_s^T
+  dbg.fused = fc;
+  dbg.fcell_dev = R.w.fcell_r;
+  dbg.fargs = fused_args(R, nc, m, T, d, params[0].group, desc);
+  dbg.split = !f16;
   dbg.Omega = R.w.Om; dbg.om_stride = (int64_t)N * R.w.ldo; dbg.ldo = R.w.ldo;
   return JOLT_OK;
 }
@@ -1203,64 +1234,31 @@ extern "C" int jolt_decompress_rope(jolt_ctx *ctx, int n_cells, const void *cons
   for (int c = 0; c < n_cells; ++c) seeds[c] = bi[c].seed;
   rc = upload_seeds_and_signs(R, seeds.data(), n_cells, d);
   if (rc) return rc;
-  const int64_t g_stride = (int64_t)m * R.w.kmaxT * d, g_slice = (int64_t)R.w.kmaxT * d;
-  const int64_t xt_stride = (int64_t)m * T * d;
-  const int ft = bi[0].f16 ? GT_F16 : GT_F32, fb = bi[0].f16 ? 2 : 4;
-  if (kmax > 0) {
-    StageTimer t(ctx, st, JOLT_STAGE_RECONSTRUCT);
-    std::vector<GemmProblem> P;
-    for (int c = 0; c < n_cells; ++c) {
-      const BlobInfo &b = bi[c];
-      if (!b.rT) continue;
-      const uint8_t *p8 = static_cast<const uint8_t *>(blobs[c]);
-      for (int s = 0; s < m; ++s) {
-        GemmProblem p{};
-        p.A = plain(p8 + b.L.G + (int64_t)s * b.rT * b.rd * fb, b.rd);
-        p.B = plain(p8 + b.L.Ud, b.rd);
-        p.C = R.w.W + c * g_stride + s * g_slice; p.ldc = d;
-        p.M = b.rT; p.N = d; p.K = b.rd; p.alpha = 1.f;
-        p.alpha_exp2 = reinterpret_cast<const int8_t *>(p8 + b.L.gexp + s);
-        P.push_back(p);
-      }
-    }
-    rc = R.gemm(P, 1, ft, ft, true, true);
-    if (rc) return rc;
-    P.clear();
-    for (int c = 0; c < n_cells; ++c) {
-      const BlobInfo &b = bi[c];
-      if (!b.rT) continue;
-      const uint8_t *p8 = static_cast<const uint8_t *>(blobs[c]);
-      for (int s = 0; s < m; ++s) {
-        GemmProblem p{};
-        p.A = plain(p8 + b.L.UT, b.rT);
-        p.B = plain(R.w.W + c * g_stride + s * g_slice, d);
-        p.C = R.w.Xt + c * xt_stride + (int64_t)s * T * d; p.ldc = d;
-        p.M = T; p.N = d; p.K = b.rT; p.alpha = 1.f;
-        P.push_back(p);
-      }
-    }
-    rc = R.gemm(P, 1, ft, GT_F32, true, false);
-    if (rc) return rc;
-  }
-  std::vector<DecodeCell> dc(n_cells);
+  const int fb = bi[0].f16 ? 2 : 4;
+  // X^ = X~ + unrotated residual, X~ = U^_T W_s rebuilt inside the fused decode pass
+  std::vector<BlobView> bv(n_cells);
+  std::vector<FusedCell> fc(n_cells);
   for (int c = 0; c < n_cells; ++c) {
     const BlobInfo &b = bi[c];
-    const uint8_t *p8 = static_cast<const uint8_t *>(blobs[c]);
-    dc[c] = DecodeCell{p8 + b.L.codes, reinterpret_cast<const uint16_t *>(p8 + b.L.scales),
-                       b.rT ? R.w.Xt + c * xt_stride : nullptr, Xhat[c], (int32_t)b.bits, 0};
+    bv[c] = BlobView{static_cast<const uint8_t *>(blobs[c]), b.L, (int)b.rT, (int)b.rd, (int)b.bits};
+    fc[c] = fused_cell(R, c, m, d, bv[c]);
+    fc[c].out = Xhat[c];
   }
-  HIP_OK(hipMemcpyAsync(R.w.dcell, dc.data(), n_cells * sizeof(DecodeCell), hipMemcpyHostToDevice, st));
-  DecodeArgs da{};
-  da.cells = R.w.dcell; da.signs = R.w.signs; da.n_cells = n_cells; da.m = m; da.T = T;
-  da.heads = out->n_heads; da.group = bi[0].group; da.s_layer = out->stride_layer; da.s_head = out->stride_head;
-  da.s_tok = out->stride_token; da.inv_sqrt_d = (float)(1.0 / std::sqrt((double)d));
+  if (kmax > 0) {
+    StageTimer t(ctx, st, JOLT_STAGE_RECONSTRUCT);
+    rc = build_w(R, n_cells, m, d, bv, fc, fb);
+    if (rc) return rc;
+  } else {
+    HIP_OK(hipMemcpyAsync(R.w.fcell_r, fc.data(), n_cells * sizeof(FusedCell), hipMemcpyHostToDevice, st));
+  }
+  FusedArgs a = fused_args(R, n_cells, m, T, d, bi[0].group, out);
   if (rope) {
-    da.rope = 1;
-    da.rope_offset = rope->position_offset;
-    da.rope_log2_base = std::log2(rope->base);
+    a.rope = 1;
+    a.rope_offset = rope->position_offset;
+    a.rope_log2_base = std::log2(rope->base);
   }
   StageTimer t(ctx, st, JOLT_STAGE_DECODE);
-  HIP_OK(launch_decode(da, d, out->dtype, st));
+  HIP_OK(launch_fused(a, FUSED_DECODE, d, out->dtype, !bi[0].f16, st));
   return JOLT_OK;
 }
 
@@ -1498,11 +1496,16 @@ extern "C" int jolt_debug_export(jolt_ctx *ctx, int what, int cell, void *dst, s
   if (what == 2) {
     const size_t n = (size_t)g.m * g.T * g.d * sizeof(float);
     if (dst_bytes < n) return jolt_fail(JOLT_E_WORKSPACE, "dst too small");
-    if (g.rT[cell] == 0) {
-      HIP_OK(hipMemsetAsync(dst, 0, n, st));
-      return JOLT_OK;
-    }
-    HIP_OK(hipMemcpyAsync(dst, g.Xt + cell * g.xt_stride, n, hipMemcpyDeviceToDevice, st));
+    if (reinterpret_cast<uintptr_t>(dst) & 15) return jolt_fail(JOLT_E_INVAL, "dst must be 16-byte aligned");
+    // the recorded call's fused reconstruction, in its export mode, for this one cell
+    FusedCell fc = g.fused[cell];
+    fc.xt_out = static_cast<float *>(dst);
+    HIP_OK(hipMemcpyAsync(g.fcell_dev + cell, &fc, sizeof fc, hipMemcpyHostToDevice, st));
+    FusedArgs a = g.fargs;
+    a.cells = g.fcell_dev + cell;
+    a.signs = g.fargs.signs + (int64_t)cell * g.d;
+    a.n_cells = 1;
+    HIP_OK(launch_fused(a, FUSED_XTILDE, g.d, JOLT_F32, g.split, st));
     return JOLT_OK;
   }
   if (what == 3) {

@@ -3,8 +3,8 @@ against the oracle's softmax attention over the oracle's decode of the same blob
 
 Blobs come from the oracle's writer (any ranks and bits, including a residual-only key
 cell, a backbone-only value cell and fp32 factors) and from the GPU compressor.  The
-tolerance is fp32 arithmetic over at most a few hundred terms per sum: the relative
-Frobenius error of the outputs is at most 1e-4.  The fused path is also checked against
+tolerance is fp32 arithmetic over at most a few hundred terms per sum: every output
+entry of a query head is within 1e-4 of the norm of that head's output.  The fused path is also checked against
 the materialising path (jolt_decompress to fp32, then attention on the CPU).
 """
 import numpy as np
@@ -49,8 +49,13 @@ def _run(kblobs, vblobs, layers, Q, d):
 
 
 def _check(got, want):
-    err = np.linalg.norm(got - want) / np.linalg.norm(want)
-    assert err <= TOL, err
+    """Per query head j: every output entry within 1e-4 of that head's output norm."""
+    assert got.shape == want.shape
+    for j in range(want.shape[0]):
+        nj = np.linalg.norm(want[j])
+        err = np.abs(got[j] - want[j]).max()
+        assert err <= TOL * nj, (j, err, nj)
+    assert np.linalg.norm(got - want) <= TOL * np.linalg.norm(want)
 
 
 @pytest.mark.parametrize("case", ["gqa_ragged", "residual_only_keys", "single_token", "two_items_fp32_factors"])

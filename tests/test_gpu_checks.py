@@ -1,0 +1,136 @@
+"""GPU checks of the boundary's error paths and degenerate inputs, through the C-ABI.
+
+* non-finite input: every entry point that computes a spectrum reports JOLT_E_NONFINITE
+  (jolt_spectrum, jolt_compress without a reused spectrum, jolt_truncated_spectra), and
+  the context keeps working afterwards;
+* rank-deficient and all-zero cells are not solver failures (clamped CholeskyQR pivots of
+  a first pass and zero eigenvalues are the designed treatment) and still match the oracle;
+* JOLT_E_NOCONV: forced from the host with the inverse-iteration limit set to zero sweeps
+  (the growth check then fails on any input), never on the same input with the default;
+* the int8 core exponent: a core below 2^-113 stores the floor -128 (identically to the
+  oracle's serialisation rule), and the oracle's decode of that blob equals the GPU's.
+"""
+import numpy as np
+import pytest
+import torch
+
+import kvsynth
+import paper_2607_12550_amd as J
+from conftest import lowrank_cell
+from gpu_util import blob_bytes, ctx, decompress, device_cells, note, workspace
+from oracle import pipeline as opl, tucker as otk
+
+pytestmark = pytest.mark.gpu
+
+
+def keys(T=256, H=4, d=128, seed=0):
+    return kvsynth.layer_kv(layer=0, tensor=0, n_heads=H, T=T, d=d, alpha=1.5,
+                            data_seed=seed)[0].astype(np.float64)
+
+
+def blobs_for(desc, params):
+    return [torch.zeros(J.jolt_compressed_size(desc, p), dtype=torch.uint8, device="cuda") for p in params]
+
+
+@pytest.mark.parametrize("bad", [np.nan, np.inf])
+@pytest.mark.parametrize("method", ["exact", "flash"])
+def test_nonfinite_cell_is_reported(bad, method):
+    X = keys()
+    xs, ex, desc = device_cells([X, keys(seed=1)], "bf16")
+    bits = xs[1].view(torch.int16).clone()
+    v = torch.tensor([bad], dtype=torch.bfloat16).view(torch.int16)
+    bits[2, 100, 7] = v[0]
+    xs[1] = bits.view(torch.bfloat16)
+    o = None if method == "exact" else J.SpectrumOpts(J.JOLT_FLASH, 32, 0.0, 10, 1)
+    ws = workspace(desc, 2, o)
+    seeds = [1, 2]
+    note("non-finite", method, bad)
+    with pytest.raises(J.JoltError) as e:
+        J.jolt_spectrum(ctx(), desc, xs, seeds, o, ws)
+    assert e.value.code == J.JOLT_E_NONFINITE
+    params = [J.Params(16, 16, 4, 64, J.JOLT_FACTOR_F16, 0, s) for s in seeds]
+    with pytest.raises(J.JoltError) as e:
+        J.jolt_compress(ctx(), desc, xs, params, o, ws, blobs_for(desc, params))
+    assert e.value.code == J.JOLT_E_NONFINITE
+    nt = J.jolt_truncated_spectra_workspace_size(desc, 2, 8, 2, o)
+    wst = torch.empty(nt, dtype=torch.uint8, device="cuda")
+    with pytest.raises(J.JoltError) as e:
+        J.jolt_truncated_spectra(ctx(), desc, xs, 8, 2, seeds=seeds, opts=o, ws=wst)
+    assert e.value.code == J.JOLT_E_NONFINITE
+    # a failed call leaves no spectrum to reuse, and the context serves the next call
+    reuse = J.SpectrumOpts(o.method if o else J.JOLT_EXACT, o.q if o else 0, 0.0, o.oversample if o else 0,
+                           o.power_iters if o else 0, 1, 0)
+    with pytest.raises(J.JoltError) as e:
+        J.jolt_compress(ctx(), desc, xs, params, reuse, ws, blobs_for(desc, params))
+    assert e.value.code == J.JOLT_E_STATE
+    good, _, dgood = device_cells([X], "bf16")
+    E, lamT, _ = J.jolt_spectrum(ctx(), dgood, good, [1], o, workspace(dgood, 1, o))
+    assert np.isfinite(E).all() and np.isfinite(lamT).all()
+
+
+@pytest.mark.parametrize("method", ["exact", "flash"])
+def test_rank_deficient_and_zero_cells_are_not_solver_failures(method):
+    """Rank 3 < r_T and an all-zero cell: the spectra equal the oracle's, compression at
+    ranks above the cell's rank succeeds and reconstructs the low-rank cell exactly."""
+    rng = np.random.default_rng(7)
+    X = lowrank_cell(rng, 4, 300, 64, 3)
+    Z = np.zeros_like(X)
+    xs, ex, desc = device_cells([X, Z], "f32")
+    o = None if method == "exact" else J.SpectrumOpts(J.JOLT_FLASH, 20, 0.0, 10, 1)
+    ws = workspace(desc, 2, o)
+    note("rank-deficient", method)
+    E, lamT, lamd = J.jolt_spectrum(ctx(), desc, xs, [3, 4], o, ws)
+    lam_exact, _ = otk.token_spectrum_exact(ex[0])
+    n = 20 if method == "flash" else 300
+    np.testing.assert_allclose(lamT[0, :n], lam_exact[:n], rtol=0, atol=1e-5 * lam_exact[0])
+    assert E[1] == 0.0 and np.all(lamT[1] == 0.0) and np.all(lamd[1] == 0.0)
+    params = [J.Params(8, 8, 0, 64, J.JOLT_FACTOR_F32, 0, s) for s in (3, 4)]
+    blobs = blobs_for(desc, params)
+    J.jolt_compress(ctx(), desc, xs, params, o, ws, blobs)
+    torch.cuda.synchronize()
+    Xh = decompress(blobs, desc, "f32")
+    assert np.linalg.norm(Xh[0] - ex[0]) <= 1e-5 * np.linalg.norm(ex[0])
+    assert np.all(Xh[1] == 0.0)
+
+
+def test_inverse_iteration_limit_reports_noconv():
+    X = keys()
+    xs, ex, desc = device_cells([X], "bf16")
+    ws = workspace(desc, 1)
+    p = [J.Params(32, 32, 2, 64, J.JOLT_FACTOR_F16, 0, 1)]
+    c2 = J.jolt_create(0)
+    try:
+        J.jolt_debug_set(c2, J.JOLT_DBG_INVIT_ITERS, 0)
+        note("inverse iteration with zero sweeps")
+        with pytest.raises(J.JoltError) as e:
+            J.jolt_compress(c2, desc, xs, p, None, ws, blobs_for(desc, p))
+        assert e.value.code == J.JOLT_E_NOCONV
+        with pytest.raises(J.JoltError):
+            J.jolt_debug_set(c2, J.JOLT_DBG_INVIT_ITERS, 9)
+        J.jolt_debug_set(c2, J.JOLT_DBG_INVIT_ITERS, 2)
+        blobs = blobs_for(desc, p)
+        J.jolt_compress(c2, desc, xs, p, None, ws, blobs)
+        torch.cuda.synchronize()
+        assert np.isfinite(decompress(blobs, desc, "f32")[0]).all()
+    finally:
+        J.jolt_destroy(c2)
+
+
+def test_tiny_core_takes_the_exponent_floor():
+    """An fp32 cell of magnitude 2^-121 with fp16 factors: every core slice lies below
+    2^-113, so its exponent is the floor -128 and the stored values stay below 2^15; the
+    oracle's decode of the GPU's blob equals the GPU's decode."""
+    X = keys(H=2) * 2.0 ** -121
+    xs, ex, desc = device_cells([X], "f32")
+    p = [J.Params(8, 8, 4, 64, J.JOLT_FACTOR_F16, 0, 3)]
+    blobs = blobs_for(desc, p)
+    note("tiny core")
+    J.jolt_compress(ctx(), desc, xs, p, None, workspace(desc, 1), blobs)
+    torch.cuda.synchronize()
+    got = opl.read_blob(blob_bytes(blobs[0]))
+    assert got["gexp"].min() >= -128 and (got["gexp"] == -128).any()
+    assert np.abs(got["G_hat"]).max() < 2.0 ** 15
+    Xh = decompress(blobs, desc, "f32")[0]
+    want = opl.decode_blob(blob_bytes(blobs[0]))
+    assert np.isfinite(Xh).all()
+    assert np.linalg.norm(Xh - want) <= 1e-5 * np.linalg.norm(want)

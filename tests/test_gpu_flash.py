@@ -140,7 +140,8 @@ def test_flash_compress_matches_oracle(dtype, fdt):
                                 seed=seed, factor_bytes=fb, method="flash", q=40, p=10,
                                 power_iters=1)
         e_gpu, e_ref = opl.rel_error(ex[c], Xh[c]), opl.rel_error(ex[c], ref["Xhat"])
-        assert abs(e_gpu / e_ref - 1) < (1e-3 if dtype == "f32" else 1e-2), (c, e_gpu, e_ref)
+        note(f"flash e2e {dtype} cell {c}: gpu {e_gpu:.9g} oracle {e_ref:.9g}")
+        assert abs(e_gpu / e_ref - 1) < tol, (c, e_gpu, e_ref)
 
 
 def test_flash_sketch_covering_all_tokens_is_exact():

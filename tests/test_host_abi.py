@@ -227,8 +227,9 @@ def test_decode_workspace_fits_inside_the_compress_workspace():
         for n in (1, 16):
             dec = J.jolt_decompress_workspace_size(desc, n, rT_max)
             assert 0 < dec <= J.jolt_workspace_size(desc, n, opts)
-            # the reconstruction buffer dominates: m*T*d fp32 per cell
-            assert dec >= n * 32 * T * 128 * 4
+            # W_s^T (d x r_T fp32 per slice) dominates; X~ itself is never stored
+            assert dec >= n * 32 * 128 * rT_max * 4
+            assert dec < n * 32 * 128 * (rT_max + 8) * 4 + (1 << 20)
         assert J.jolt_decompress_workspace_size(desc, 2, 0) < 1 << 20   # residual-only blobs
     with pytest.raises(J.JoltError):
         J.jolt_decompress_workspace_size(desc, 0, 8)
@@ -268,3 +269,26 @@ def test_mode_summary_and_slice_spectrum_validation():
     rc = J.lib.jolt_slice_spectrum(None, C.byref(ok), 1, (C.c_void_p * 1)(0), None, 0,
                                    np.zeros(8).ctypes.data_as(C.POINTER(C.c_double)), None)
     assert rc == -1
+
+
+def test_r_max_caps_the_token_factor():
+    """jolt_spectrum_opts.r_max caps the admissible r_T (and the workspace), never the
+    eigenvalues returned; a negative cap is rejected."""
+    desc = _desc(T=4096)
+    full = J.jolt_workspace_size(desc, 2, None)
+    o = J.SpectrumOpts(J.JOLT_EXACT, 0, 0.0, 0, 0, 0, 512)
+    assert J.jolt_spectrum_len(desc, o) == (4096, 512)
+    assert J.jolt_workspace_size(desc, 2, o) < full
+    of = J.SpectrumOpts(J.JOLT_FLASH, 0, 2.0, 10, 1, 0, 64)
+    assert J.jolt_spectrum_len(desc, of) == (129, 64)
+    p = J.Params(520, 64, 2, 64, J.JOLT_FACTOR_F16, 0, 0)
+    with pytest.raises(J.JoltError) as e:
+        J.jolt_spectrum_len(desc, J.SpectrumOpts(J.JOLT_EXACT, 0, 0.0, 0, 0, 0, -1))
+    assert e.value.code == J.JOLT_E_INVAL
+    assert J.jolt_compressed_size(desc, p) > 0          # blob sizes do not depend on the cap
+
+
+def test_debug_set_validates_without_device_work():
+    with pytest.raises(J.JoltError) as e:
+        J.jolt_debug_set(None, J.JOLT_DBG_INVIT_ITERS, 2)
+    assert e.value.code == J.JOLT_E_INVAL
