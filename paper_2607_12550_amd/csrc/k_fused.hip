@@ -97,6 +97,44 @@ JOLT_DEV void load_run(const void *base, int64_t ld, int row, int rows, int k0, 
   }
 }
 
+// 8 cache entries of one row as loaded (converted to fp32 only when used)
+template <typename T> struct Raw8;
+template <> struct Raw8<bf16_t> { ju4 w; };
+template <> struct Raw8<float> { jf4 a, b; };
+JOLT_DEV void raw_load(const bf16_t *p, Raw8<bf16_t> &r) { r.w = gload_u4(p); }
+JOLT_DEV void raw_load(const float *p, Raw8<float> &r) { r.a = gload_f4(p); r.b = gload_f4(p + 4); }
+JOLT_DEV void raw_f32(const Raw8<bf16_t> &r, float (&v)[8]) {
+  const uint32_t w[4] = {r.w.x, r.w.y, r.w.z, r.w.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = bf16_to_f32((bf16_t)(w[i] & 0xffffu));
+    v[2 * i + 1] = bf16_to_f32((bf16_t)(w[i] >> 16));
+  }
+}
+JOLT_DEV void raw_f32(const Raw8<float> &r, float (&v)[8]) {
+  v[0] = r.a.x; v[1] = r.a.y; v[2] = r.a.z; v[3] = r.a.w; v[4] = r.b.x; v[5] = r.b.y; v[6] = r.b.z; v[7] = r.b.w;
+}
+// the b-bit codes of 8 entries (LSB first) as loaded: b = 2, 4 or 8 bytes
+typedef uint32_t ju2 __attribute__((ext_vector_type(2)));
+JOLT_DEV ju2 codes_load(const uint8_t *codes, int64_t elem, int bits) {
+  if (bits == 2) return ju2{(uint32_t)*gptr(reinterpret_cast<const uint16_t *>(codes + elem / 4)), 0u};
+  if (bits == 4) return ju2{*gptr(reinterpret_cast<const uint32_t *>(codes + elem / 2)), 0u};
+  return *gptr(reinterpret_cast<const ju2 *>(codes + elem));
+}
+JOLT_DEV void codes_unpack(ju2 w, int bits, uint32_t (&c)[8]) {
+  if (bits == 8) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      c[i] = (w.x >> (8 * i)) & 255u;
+      c[i + 4] = (w.y >> (8 * i)) & 255u;
+    }
+  } else {
+    const uint32_t mask = (1u << bits) - 1u;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) c[i] = (w.x >> (bits * i)) & mask;
+  }
+}
+
 template <int D, int MODE, typename TIO, bool USPLIT, bool ROPE>
 __global__ void __launch_bounds__(NT, 2) k_fused(FusedArgs a) {
   constexpr int WN = D >= 64 ? 2 : 1, WM = 4 / WN;
@@ -118,6 +156,35 @@ __global__ void __launch_bounds__(NT, 2) k_fused(FusedArgs a) {
   const int rT = c.rT, T = a.T;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN, lr = lane & 31, lh = lane >> 5;
+
+  // the epilogue's HBM operands (cache rows or codes and scales of the rows this lane
+  // finishes) are requested first, so that their latency overlaps the reconstruction
+  constexpr int NP = 32 / R;                  // epilogue passes: R rows per wave each
+  const int row_in_wave = lane / L, lane_in_row = lane % L;
+  const int64_t srow = (int64_t)(s / a.heads) * a.s_layer + (int64_t)(s % a.heads) * a.s_head;
+  Raw8<TIO> px[MODE == FUSED_RESIDUAL ? NP : 1];
+  ju2 pcode[MODE == FUSED_DECODE ? NP : 1];
+  uint16_t pscale[MODE == FUSED_DECODE ? NP : 1];
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const int t = t0 + wave * 32 + p * R + row_in_wave;
+    if (t >= T) continue;
+    const int64_t elem = ((int64_t)s * T + t) * D + lane_in_row * 8;
+    if constexpr (MODE == FUSED_RESIDUAL)
+      raw_load(reinterpret_cast<const TIO *>(c.x) + srow + (int64_t)t * a.s_tok + lane_in_row * 8, px[p]);
+    if constexpr (MODE == FUSED_DECODE) {
+      if (c.bits) {
+        pcode[p] = codes_load(c.codes, elem, c.bits);
+        pscale[p] = *gptr(c.scales + elem / a.group);
+      }
+    }
+  }
+  float sgv[8];
+  {
+    const float *sg = a.signs + (int64_t)cell * D + lane_in_row * 8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sgv[e] = sg[e];
+  }
 
   f32x16_t acc[MI][NI];
 #pragma unroll
@@ -220,11 +287,6 @@ __global__ void __launch_bounds__(NT, 2) k_fused(FusedArgs a) {
   __syncthreads();
 
   // epilogue: wave w finishes rows 32 w .. 32 w + 31 of the tile, R rows at a time
-  const int row_in_wave = lane / L, lane_in_row = lane % L;
-  const float *sg = a.signs + (int64_t)cell * D + lane_in_row * 8;
-  float sgv[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) sgv[e] = sg[e];
   double theta[8];
   if constexpr (ROPE) {
 #pragma unroll
@@ -234,9 +296,8 @@ __global__ void __launch_bounds__(NT, 2) k_fused(FusedArgs a) {
     }
   }
   const int gl = a.group / 8;
-  const int64_t srow = (int64_t)(s / a.heads) * a.s_layer + (int64_t)(s % a.heads) * a.s_head;
-#pragma unroll 2
-  for (int p = 0; p < 32 / R; ++p) {
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
     const int r = wave * 32 + p * R + row_in_wave, t = t0 + r;
     if (t >= T) continue;                  // whole rows (L lanes) drop out together
     float xt[8];
@@ -253,7 +314,7 @@ __global__ void __launch_bounds__(NT, 2) k_fused(FusedArgs a) {
       store8(c.xt_out + elem, xt);
     } else if constexpr (MODE == FUSED_RESIDUAL) {
       float v[8];
-      load8<TIO>(reinterpret_cast<const TIO *>(c.x) + srow + (int64_t)t * a.s_tok + lane_in_row * 8, v);
+      raw_f32(px[p], v);
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] = (v[e] - xt[e]) * sgv[e];
       fwht_row<D>(v, lane_in_row);
@@ -268,8 +329,8 @@ __global__ void __launch_bounds__(NT, 2) k_fused(FusedArgs a) {
       float v[8];
       if (c.bits) {
         uint32_t code[8];
-        load_codes(c.codes, elem, c.bits, code);
-        const float delta = h_val(c.scales[elem / a.group]);
+        codes_unpack(pcode[p], c.bits, code);
+        const float delta = h_val(pscale[p]);
         const float mid = 0.5f * (float)((1 << c.bits) - 1);
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = ((float)code[e] - mid) * delta;
