@@ -68,6 +68,9 @@ def parse():
     ap.add_argument("--power-iters", type=int, default=1)
     ap.add_argument("--oversample", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--gen-workers", type=int, default=16,
+                    help="processes generating the synthetic cache (1 = in this process, e.g. under a "
+                         "hardware-counter profiler; the values do not depend on it)")
     ap.add_argument("--cpu-sample-T", type=int, default=0,
                     help="tokens of the oracle sample cell (0 = the workload's T)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -484,7 +487,7 @@ def main():
     log("generating", args.workload)
     t0 = time.perf_counter()
     # generation runs in worker processes (the values do not depend on their number)
-    Knp, Vnp = kvsynth.make_cache(**cfg, workers=min(16, os.cpu_count() or 1))
+    Knp, Vnp = kvsynth.make_cache(**cfg, workers=max(1, min(args.gen_workers, os.cpu_count() or 1)))
     if args.rope_post > 1.0:
         for l in range(Knp.shape[0]):
             xr = kvsynth.apply_rope(kvsynth.bf16_bits_to_f32(Knp[l]) if cfg["dtype"] == "bf16" else Knp[l],
