@@ -371,6 +371,22 @@ int jolt_attend(jolt_ctx *ctx, int n_items, const void *const *k_blobs, const si
                 const void *v_hdr_host, const int32_t *layers, int n_q, const float *Q, float scale,
                 float *O, void *ws, size_t ws_bytes, jolt_stream stream);
 
+/* jolt_attend without a caller workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid allocation).
+ * Arguments, result and errors as jolt_attend; the workspace is a fixed scratch array of
+ * JOLT_ATTEND_SCRATCH_BYTES bytes that the library holds on every device it runs on until
+ * the process ends (its address is resolved once per device by jolt_create).  Calls whose
+ * jolt_attend_workspace_size exceeds it fail with JOLT_E_WORKSPACE before any device work
+ * (split the items over several calls).  The call allocates nothing.  Every call on a
+ * device shares that device's scratch and it keeps the last call's contents (each call
+ * writes every part it reads), so calls that overlap on one device race: serialise them
+ * (one stream, or events) across threads and contexts of the same device. */
+#define JOLT_ATTEND_SCRATCH_BYTES (64u << 20)
+int jolt_attend_noalloc(jolt_ctx *ctx, int n_items, const void *const *k_blobs, const size_t *k_bytes,
+                        const void *const *v_blobs, const size_t *v_bytes, const void *k_hdr_host,
+                        const void *v_hdr_host, const int32_t *layers, int n_q, const float *Q,
+                        float scale, float *O, jolt_stream stream);
+
 /* Test hook: copies an intermediate of the most recent jolt_compress on this
  * context for cell `cell` into dst (device memory, dst_bytes): 0 = U_T (T x r_T fp32),
  * 1 = U_d (d x r_d fp32), 2 = X~ (m x T x d fp32 from the stored factors, recomputed by

@@ -22,7 +22,7 @@ __all__ = ["JoltError", "lib", "CellDesc", "SpectrumOpts", "Params", "CellSpectr
            "jolt_compress", "jolt_decompress", "jolt_allocate", "jolt_eps2_workspace_size",
            "jolt_eps2_calibrate", "jolt_slice_spectrum_workspace_size", "jolt_slice_spectrum",
            "jolt_mode_summary", "jolt_truncated_spectra_workspace_size", "jolt_truncated_spectra",
-           "jolt_attend_workspace_size", "jolt_attend", "jolt_debug_export", "jolt_debug_set",
+           "jolt_attend_workspace_size", "jolt_attend", "jolt_attend_noalloc", "JOLT_ATTEND_SCRATCH_BYTES", "jolt_debug_export", "jolt_debug_set",
            "jolt_profile_enable", "jolt_profile_reset", "JOLT_E_NONFINITE", "JOLT_E_NOCONV",
            "JOLT_DBG_INVIT_ITERS",
            "jolt_profile_read", "STAGES", "cell_desc", "LIB_PATH", "HEADER_PATH"]
@@ -35,6 +35,7 @@ JOLT_OK, JOLT_F32, JOLT_BF16 = 0, 0, 1
 JOLT_E_INVAL, JOLT_E_UNSUPPORTED, JOLT_E_WORKSPACE, JOLT_E_BLOB = -1, -2, -3, -4
 JOLT_E_HIP, JOLT_E_NONFINITE, JOLT_E_STATE, JOLT_E_NOCONV = -5, -6, -7, -8
 JOLT_DBG_INVIT_ITERS = 0
+JOLT_ATTEND_SCRATCH_BYTES = 64 << 20
 JOLT_EXACT, JOLT_FLASH = 0, 1
 JOLT_FACTOR_F32, JOLT_FACTOR_F16 = 0, 1
 HEADER_BYTES = 128
@@ -129,6 +130,8 @@ _SIGS = {
                                          _P(SpectrumOpts), C.c_int, C.c_int, _vp, _sz, _P(_dbl), _vp]),
     "jolt_debug_export": (C.c_int, [_vp, C.c_int, C.c_int, _vp, _sz, _vp]),
     "jolt_debug_set": (C.c_int, [_vp, C.c_int, C.c_int64]),
+    "jolt_attend_noalloc": (C.c_int, [_vp, C.c_int, _P(_vp), _P(_sz), _P(_vp), _P(_sz), _vp, _vp, _P(_i32),
+                                      C.c_int, _vp, C.c_float, _vp, _vp]),
     "jolt_profile_enable": (C.c_int, [_vp, C.c_int]),
     "jolt_profile_reset": (C.c_int, [_vp]),
     "jolt_profile_read": (C.c_int, [_vp, C.c_int, _P(_dbl), _P(C.c_int64)]),
@@ -414,6 +417,20 @@ def jolt_attend(ctx, k_blobs, v_blobs, k_hdr, v_hdr, layers, Q, O, scale: float,
     _check(lib.jolt_attend(ctx, n, _ptrs(k_blobs), (_sz * n)(*kb), _ptrs(v_blobs), (_sz * n)(*vb),
                            kh.ctypes.data, vh.ctypes.data, lay, Q.shape[1], _addr(Q), float(scale),
                            _addr(O), _addr(ws), wsb, _stream(stream)))
+
+
+def jolt_attend_noalloc(ctx, k_blobs, v_blobs, k_hdr, v_hdr, layers, Q, O, scale: float, stream=None,
+                        k_bytes=None, v_bytes=None) -> None:
+    """jolt_attend on the library's fixed device scratch (no workspace argument)."""
+    n = len(k_blobs)
+    kb = k_bytes if k_bytes is not None else [b.numel() for b in k_blobs]
+    vb = v_bytes if v_bytes is not None else [b.numel() for b in v_blobs]
+    kh = np.ascontiguousarray(k_hdr, dtype=np.uint8)
+    vh = np.ascontiguousarray(v_hdr, dtype=np.uint8)
+    lay = (_i32 * n)(*layers)
+    _check(lib.jolt_attend_noalloc(ctx, n, _ptrs(k_blobs), (_sz * n)(*kb), _ptrs(v_blobs), (_sz * n)(*vb),
+                                   kh.ctypes.data, vh.ctypes.data, lay, Q.shape[1], _addr(Q), float(scale),
+                                   _addr(O), _stream(stream)))
 
 
 def jolt_debug_export(ctx, what: int, cell: int, dst, stream=None) -> None:

@@ -51,6 +51,12 @@ extern "C" int jolt_create(jolt_ctx **ctx, int device) {
   const std::string arch(c->prop.gcnArchName);
   if (arch.find("gfx950") == std::string::npos)
     return jolt_fail(JOLT_E_UNSUPPORTED, "jolt_create: device arch %s is not gfx950", arch.c_str());
+  {
+    // set-up of the allocation-free entry point: this device's scratch address, once per device
+    DeviceGuard dg;
+    HIP_OK(dg.enter(device));
+    HIP_OK(attend_scratch_address(device, &c->attend_scratch));
+  }
   *ctx = c.release();
   return JOLT_OK;
 }

@@ -75,6 +75,7 @@ struct jolt_ctx {
   hipGraphExec_t trd_exec = nullptr;
   std::vector<const void *> trd_key;
   int invit_iters = 2;            // inverse-iteration sweeps (test hook jolt_debug_set)
+  void *attend_scratch = nullptr; // this device's fixed attention scratch (device address)
   ~jolt_ctx();
 };
 

@@ -15,6 +15,7 @@
 // value factors and the inverse rotation once per query head.  Per token a query head
 // reads r_T factor values and d codes instead of d decoded values plus the decompression.
 #include <cmath>
+#include <mutex>
 
 #include "common.h"
 #include "kernels.h"
@@ -502,4 +503,31 @@ hipError_t launch_attend(const AttnArgs &a, int d, hipStream_t st) {
   L_(32) L_(64) L_(128)
 #undef L_
   return hipErrorInvalidValue;
+}
+
+// Fixed device scratch of jolt_attend_noalloc: the attention workspace of callers that
+// cannot allocate device memory.  One array per device that loads the library, held until
+// the process ends; every call on a device shares it.
+static __device__ __align__(256) uint8_t scratch[ATTN_SCRATCH_BYTES];
+
+namespace {
+std::mutex g_scratch_mu;
+void *g_scratch_dev[ATTN_SCRATCH_DEVICES] = {};
+}  // namespace
+
+// Device address of this device's scratch array, resolved once per device with
+// hipGetSymbolAddress while that device is current (the array's name in host code is not a
+// device address).
+hipError_t attend_scratch_address(int device, void **ptr) {
+  if (!ptr || device < 0 || device >= ATTN_SCRATCH_DEVICES) return hipErrorInvalidValue;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[device]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_dev[device] = p;
+  }
+  *ptr = g_scratch_dev[device];
+  return hipSuccess;
 }

@@ -193,6 +193,11 @@ constexpr int ATTN_QMAX = 64;       // query heads per item
 constexpr int ATTN_REP_MAX = 8;     // query heads per key-value head
 constexpr int ATTN_RT_MAX = 1024;   // largest value rank the combine kernel stages in LDS
 hipError_t launch_attend(const AttnArgs &a, int d, hipStream_t st);
+// fixed per-device scratch of the allocation-free attention entry point
+constexpr size_t ATTN_SCRATCH_BYTES = JOLT_ATTEND_SCRATCH_BYTES;
+constexpr int ATTN_SCRATCH_DEVICES = 64;
+// the calling thread must have `device` current
+hipError_t attend_scratch_address(int device, void **ptr);
 
 // ----------------------------------------------------------------- eigensolver
 struct EigBatch {

@@ -1401,10 +1401,13 @@ extern "C" int jolt_attend_workspace_size(int n_items, int n_q, int T, int d, in
   return JOLT_OK;
 }
 
-extern "C" int jolt_attend(jolt_ctx *ctx, int n_items, const void *const *k_blobs, const size_t *k_bytes,
-                           const void *const *v_blobs, const size_t *v_bytes, const void *k_hdr_host,
-                           const void *v_hdr_host, const int32_t *layers, int n_q, const float *Q,
-                           float scale, float *O, void *ws, size_t ws_bytes, jolt_stream stream) {
+namespace {
+// Decode attention on the factors with the workspace ws; caller_ws: the caller owns ws (a
+// recorded spectrum it overlaps is dropped), otherwise ws is the library's fixed scratch.
+int attend_impl(jolt_ctx *ctx, int n_items, const void *const *k_blobs, const size_t *k_bytes,
+                const void *const *v_blobs, const size_t *v_bytes, const void *k_hdr_host,
+                const void *v_hdr_host, const int32_t *layers, int n_q, const float *Q, float scale,
+                float *O, void *ws, size_t ws_bytes, bool caller_ws, jolt_stream stream) {
   if (!ctx || n_items < 1 || !k_blobs || !k_bytes || !v_blobs || !v_bytes || !k_hdr_host || !v_hdr_host ||
       !layers || n_q < 1 || !Q || !O || !ws)
     return jolt_fail(JOLT_E_INVAL, "jolt_attend: null argument or empty call");
@@ -1439,10 +1442,15 @@ extern "C" int jolt_attend(jolt_ctx *ctx, int n_items, const void *const *k_blob
   size_t need = 0;
   int rc = jolt_attend_workspace_size(n_items, n_q, T, d, rk, rv, &need);
   if (rc) return rc;
-  if (ws_bytes < need) return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  if (ws_bytes < need) {
+    if (!caller_ws)
+      return jolt_fail(JOLT_E_WORKSPACE, "jolt_attend_noalloc: the call needs %zu bytes of workspace, above the "
+                       "fixed scratch of %zu bytes (split the items over several calls)", need, ws_bytes);
+    return jolt_fail(JOLT_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  }
   DeviceGuard dg;
   HIP_OK(dg.enter(ctx->device));
-  forget_spectra(ctx, ws, ws_bytes);
+  if (caller_ws) forget_spectra(ctx, ws, ws_bytes);
   hipStream_t st = (hipStream_t)stream;
   Carver cv(ws);
   AttnItem *items; uint64_t *seeds; float *signs, *gk, *qr, *part;
@@ -1471,6 +1479,25 @@ extern "C" int jolt_attend(jolt_ctx *ctx, int n_items, const void *const *k_blob
   StageTimer t(ctx, st, JOLT_STAGE_ATTEND);
   HIP_OK(launch_attend(a, d, st));
   return JOLT_OK;
+}
+}  // namespace
+
+extern "C" int jolt_attend(jolt_ctx *ctx, int n_items, const void *const *k_blobs, const size_t *k_bytes,
+                           const void *const *v_blobs, const size_t *v_bytes, const void *k_hdr_host,
+                           const void *v_hdr_host, const int32_t *layers, int n_q, const float *Q,
+                           float scale, float *O, void *ws, size_t ws_bytes, jolt_stream stream) {
+  return attend_impl(ctx, n_items, k_blobs, k_bytes, v_blobs, v_bytes, k_hdr_host, v_hdr_host, layers, n_q,
+                     Q, scale, O, ws, ws_bytes, true, stream);
+}
+
+extern "C" int jolt_attend_noalloc(jolt_ctx *ctx, int n_items, const void *const *k_blobs,
+                                   const size_t *k_bytes, const void *const *v_blobs, const size_t *v_bytes,
+                                   const void *k_hdr_host, const void *v_hdr_host, const int32_t *layers,
+                                   int n_q, const float *Q, float scale, float *O, jolt_stream stream) {
+  if (!ctx) return jolt_fail(JOLT_E_INVAL, "jolt_attend_noalloc: ctx is null");
+  if (!ctx->attend_scratch) return jolt_fail(JOLT_E_STATE, "jolt_attend_noalloc: no scratch for this context");
+  return attend_impl(ctx, n_items, k_blobs, k_bytes, v_blobs, v_bytes, k_hdr_host, v_hdr_host, layers, n_q,
+                     Q, scale, O, ctx->attend_scratch, ATTN_SCRATCH_BYTES, false, stream);
 }
 
 // ------------------------------------------------------------------------ debug export
