@@ -2,9 +2,10 @@
 // rebuilt from the stored factors; decoding adds the dequantised, unrotated residual back).
 //
 // For slice s of a cell, X~_s = U^_T W_s with W_s = 2^e_s G^_s U^_d^T (r_T x d).  A small
-// GEMM forms W_s^T (d x r_T, fp32) in the workspace and k_w_exponent picks a power of two
-// 2^k_s with max |W_s| 2^-k_s <= 2^14.  The fused kernel then multiplies, per tile of 128
-// tokens x d features of one slice, on the fp16 matrix cores (v_mfma_f32_32x32x16_f16,
+// GEMM forms W_s^T (d x r_T, fp32) in the workspace; k_w_prepare picks a power of two
+// 2^k_s with max |W_s| 2^-k_s <= 2^14 and rewrites each entry in place as its fp16 hi and
+// lo terms, so tiles only separate them.  The fused kernel then multiplies, per tile of
+// 128 tokens x d features of one slice, on the fp16 matrix cores (v_mfma_f32_32x32x16_f16,
 // fp32 accumulation):
 //   * U^_T is an exact fp16 operand when the factors are stored in fp16; fp32 factors are
 //     scaled by 2^6 and split into hi + lo fp16 terms;
@@ -12,8 +13,9 @@
 //     |w - hi - lo| <= 2^-22 |w| for entries in the fp16 normal range;
 //   * X~ = 2^(k_s - u) (U_hi (W_hi + W_lo) [+ U_lo W_hi]), u = 6 for split factors, else 0:
 //     two MFMA passes per K step (three for fp32 factors), products exact in fp32.
-// The accumulator tile goes through LDS to the row layout of the residual kernels (a
-// feature row over d/8 lanes) and the epilogue finishes the row in registers:
+// The accumulator tile goes through LDS, 64 rows at a time, to the row layout of the
+// residual kernels (a feature row over d/8 lanes) and the epilogue finishes the row in
+// registers:
 //   residual: r = X - X~, rotate (FWHT), group max, fp16 scale, codes, pack;
 //   decode:   dequantise, inverse rotation, + X~, optional RoPE, cast, store;
 //   export:   X~ itself (fp32; the test hook of the closed loop).
@@ -36,11 +38,13 @@ using namespace rowops;
 
 constexpr int BT = 128, BK = 32, LDK = BK + 8, NT = 256;
 
+constexpr int EH = 64;                                         // epilogue rows per half
+
 template <int D, bool USPLIT>
 struct FusedLds {
   static constexpr int A = BT * LDK, B = D * LDK;              // halves per operand term
   static constexpr int OPER = (USPLIT ? 2 : 1) * A + 2 * B;     // A hi [A lo] B hi B lo
-  static constexpr int EPI = BT * (D + 4) * 2;                  // fp32 epilogue tile, in halves
+  static constexpr int EPI = EH * (D + 4) * 2;                  // fp32 epilogue half, in halves
   static constexpr int HALVES = OPER > EPI ? OPER : EPI;
 };
 
@@ -135,6 +139,18 @@ JOLT_DEV void codes_unpack(ju2 w, int bits, uint32_t (&c)[8]) {
   }
 }
 
+// 8 fp16 values of a run (k0 .. k0 + 7 of row `row`) as raw bits; zeros past the row count
+// or K (and for a partial run past K; `full` runs lie inside K)
+JOLT_DEV ju4 load_run_h(const uint16_t *base, int64_t ld, int row, int rows, int k0, int K) {
+  if (row >= rows || k0 >= K) return ju4{0u, 0u, 0u, 0u};
+  const uint16_t *p = base + (int64_t)row * ld + k0;
+  if (k0 + 8 <= K && (reinterpret_cast<uintptr_t>(p) & 15) == 0) return gload_u4(p);
+  uint16_t h[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) h[i] = k0 + i < K ? gptr(p)[i] : (uint16_t)0;
+  return ju4{pk2(h[0], h[1]), pk2(h[2], h[3]), pk2(h[4], h[5]), pk2(h[6], h[7])};
+}
+
 template <int D, int MODE, typename TIO, bool USPLIT, bool ROPE>
 __global__ void __launch_bounds__(NT, 2) k_fused(FusedArgs a) {
   constexpr int WN = D >= 64 ? 2 : 1, WM = 4 / WN;
@@ -158,27 +174,32 @@ __global__ void __launch_bounds__(NT, 2) k_fused(FusedArgs a) {
   const int wm = wave / WN, wn = wave % WN, lr = lane & 31, lh = lane >> 5;
 
   // the epilogue's HBM operands (cache rows or codes and scales of the rows this lane
-  // finishes) are requested first, so that their latency overlaps the reconstruction
-  constexpr int NP = 32 / R;                  // epilogue passes: R rows per wave each
+  // finishes) are requested first, so that their latency overlaps the reconstruction; those
+  // of the second half after the first half is done.  Wave w finishes rows
+  // h 64 + 16 w .. h 64 + 16 w + 15 of each half h, R at a time.
+  constexpr int NPH = (EH / 4) / R;                 // epilogue passes per half
   const int row_in_wave = lane / L, lane_in_row = lane % L;
   const int64_t srow = (int64_t)(s / a.heads) * a.s_layer + (int64_t)(s % a.heads) * a.s_head;
-  Raw8<TIO> px[MODE == FUSED_RESIDUAL ? NP : 1];
-  ju2 pcode[MODE == FUSED_DECODE ? NP : 1];
-  uint16_t pscale[MODE == FUSED_DECODE ? NP : 1];
+  Raw8<TIO> px[MODE == FUSED_RESIDUAL ? NPH : 1];
+  ju2 pcode[MODE == FUSED_DECODE ? NPH : 1];
+  uint16_t pscale[MODE == FUSED_DECODE ? NPH : 1];
+  auto prefetch = [&](int h) {
 #pragma unroll
-  for (int p = 0; p < NP; ++p) {
-    const int t = t0 + wave * 32 + p * R + row_in_wave;
-    if (t >= T) continue;
-    const int64_t elem = ((int64_t)s * T + t) * D + lane_in_row * 8;
-    if constexpr (MODE == FUSED_RESIDUAL)
-      raw_load(reinterpret_cast<const TIO *>(c.x) + srow + (int64_t)t * a.s_tok + lane_in_row * 8, px[p]);
-    if constexpr (MODE == FUSED_DECODE) {
-      if (c.bits) {
-        pcode[p] = codes_load(c.codes, elem, c.bits);
-        pscale[p] = *gptr(c.scales + elem / a.group);
+    for (int pp = 0; pp < NPH; ++pp) {
+      const int t = t0 + h * EH + wave * (EH / 4) + pp * R + row_in_wave;
+      if (t >= T) continue;
+      const int64_t elem = ((int64_t)s * T + t) * D + lane_in_row * 8;
+      if constexpr (MODE == FUSED_RESIDUAL)
+        raw_load(reinterpret_cast<const TIO *>(c.x) + srow + (int64_t)t * a.s_tok + lane_in_row * 8, px[pp]);
+      if constexpr (MODE == FUSED_DECODE) {
+        if (c.bits) {
+          pcode[pp] = codes_load(c.codes, elem, c.bits);
+          pscale[pp] = *gptr(c.scales + elem / a.group);
+        }
       }
     }
-  }
+  };
+  prefetch(0);
   float sgv[8];
   {
     const float *sg = a.signs + (int64_t)cell * D + lane_in_row * 8;
@@ -197,45 +218,54 @@ __global__ void __launch_bounds__(NT, 2) k_fused(FusedArgs a) {
   int ks = 0;                              // X~ = 2^(ks - u) acc, applied per value
   if (rT > 0) {
     ks = c.wexp[s];
-    const float *W = c.Wt + (int64_t)s * D * c.ldw;
+    // W_s^T as prepared: per entry the fp16 pair (hi, lo), zeros past r_T
+    const uint32_t *Wp = reinterpret_cast<const uint32_t *>(c.Wt + (int64_t)s * D * c.ldw);
     // operand units of 8 k values: A has BT rows x 4 units, B has D rows x 4 units
     constexpr int AU = BT * (BK / 8) / NT, BU = D * (BK / 8) / NT > 0 ? D * (BK / 8) / NT : 1;
-    float ra[AU][8], rb[BU][8];
+    float ra[USPLIT ? AU : 1][8];
+    ju4 rah[AU], rbh[BU], rbl[BU];
     auto fetch = [&](int k0) {
 #pragma unroll
       for (int q = 0; q < AU; ++q) {
         const int u = tid + NT * q, r = u >> 2, kc = (u & 3) * 8;
-        load_run<USPLIT>(c.UT, rT, t0 + r, T, k0 + kc, rT, ra[q]);
+        if constexpr (USPLIT) load_run<true>(c.UT, rT, t0 + r, T, k0 + kc, rT, ra[q]);
+        else rah[q] = load_run_h(reinterpret_cast<const uint16_t *>(c.UT), rT, t0 + r, T, k0 + kc, rT);
       }
 #pragma unroll
       for (int q = 0; q < BU; ++q) {
         const int u = tid + NT * q, r = u >> 2, kc = (u & 3) * 8;
-        if (u < D * (BK / 8)) load_run<true>(W, c.ldw, r, D, k0 + kc, rT, rb[q]);
+        const bool in = u < D * (BK / 8) && k0 + kc < rT;   // runs past r_T are zero
+        rbh[q] = in ? gload_u4(Wp + (int64_t)r * c.ldw + k0 + kc) : ju4{0u, 0u, 0u, 0u};
+        rbl[q] = in ? gload_u4(Wp + (int64_t)r * c.ldw + k0 + kc + 4) : ju4{0u, 0u, 0u, 0u};
       }
     };
     auto stash = [&]() {
 #pragma unroll
       for (int q = 0; q < AU; ++q) {
         const int u = tid + NT * q, r = u >> 2, kc = (u & 3) * 8;
-        uint16_t h[8], l[8];
+        if constexpr (USPLIT) {
+          uint16_t h[8], l[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          if constexpr (USPLIT) split_f16(ra[q][e] * 64.f, h[e], l[e]);
-          else h[e] = h_bits(ra[q][e]);        // exact: the value came from fp16
-        }
-        *reinterpret_cast<uint4 *>(sa + r * LDK + kc) = make_uint4(pk2(h[0], h[1]), pk2(h[2], h[3]), pk2(h[4], h[5]), pk2(h[6], h[7]));
-        if constexpr (USPLIT)
+          for (int e = 0; e < 8; ++e) split_f16(ra[q][e] * 64.f, h[e], l[e]);
+          *reinterpret_cast<uint4 *>(sa + r * LDK + kc) = make_uint4(pk2(h[0], h[1]), pk2(h[2], h[3]), pk2(h[4], h[5]), pk2(h[6], h[7]));
           *reinterpret_cast<uint4 *>(sa_lo + r * LDK + kc) = make_uint4(pk2(l[0], l[1]), pk2(l[2], l[3]), pk2(l[4], l[5]), pk2(l[6], l[7]));
+        } else {
+          *reinterpret_cast<ju4 *>(sa + r * LDK + kc) = rah[q];
+        }
       }
 #pragma unroll
       for (int q = 0; q < BU; ++q) {
         const int u = tid + NT * q, r = u >> 2, kc = (u & 3) * 8;
         if (u >= D * (BK / 8)) continue;
-        uint16_t h[8], l[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) split_f16(ldexpf(rb[q][e], -ks), h[e], l[e]);
-        *reinterpret_cast<uint4 *>(sb + r * LDK + kc) = make_uint4(pk2(h[0], h[1]), pk2(h[2], h[3]), pk2(h[4], h[5]), pk2(h[6], h[7]));
-        *reinterpret_cast<uint4 *>(sb_lo + r * LDK + kc) = make_uint4(pk2(l[0], l[1]), pk2(l[2], l[3]), pk2(l[4], l[5]), pk2(l[6], l[7]));
+        // 8 (hi, lo) pairs -> 8 hi terms and 8 lo terms
+        const uint32_t w[8] = {rbh[q].x, rbh[q].y, rbh[q].z, rbh[q].w, rbl[q].x, rbl[q].y, rbl[q].z, rbl[q].w};
+        ju4 hv, lv;
+        hv.x = __builtin_amdgcn_perm(w[1], w[0], 0x05040100u); lv.x = __builtin_amdgcn_perm(w[1], w[0], 0x07060302u);
+        hv.y = __builtin_amdgcn_perm(w[3], w[2], 0x05040100u); lv.y = __builtin_amdgcn_perm(w[3], w[2], 0x07060302u);
+        hv.z = __builtin_amdgcn_perm(w[5], w[4], 0x05040100u); lv.z = __builtin_amdgcn_perm(w[5], w[4], 0x07060302u);
+        hv.w = __builtin_amdgcn_perm(w[7], w[6], 0x05040100u); lv.w = __builtin_amdgcn_perm(w[7], w[6], 0x07060302u);
+        *reinterpret_cast<ju4 *>(sb + r * LDK + kc) = hv;
+        *reinterpret_cast<ju4 *>(sb_lo + r * LDK + kc) = lv;
       }
     };
     fetch(0);
@@ -272,97 +302,133 @@ __global__ void __launch_bounds__(NT, 2) k_fused(FusedArgs a) {
       }
     }
   }
-  // accumulators -> LDS tile [BT][D + 4] (fp32): acc[x][y][q] is row
-  // wm WR + x 32 + 8 (q / 4) + 4 lh + q % 4, column wn WC + y 32 + lr
+  const int gl = a.group / 8;
+  // accumulators -> LDS half tile [EH][D + 4] (fp32), half h holding tile rows h EH ..:
+  // acc[x][y][q] is row wm WR + x 32 + 8 (q / 4) + 4 lh + q % 4, column wn WC + y 32 + lr
   constexpr int ELD = D + 4;
   float *E = reinterpret_cast<float *>(lds);
-  __syncthreads();
 #pragma unroll
-  for (int x = 0; x < MI; ++x)
+  for (int h = 0; h < BT / EH; ++h) {
+    if (h > 0) prefetch(h);
+    __syncthreads();                       // operand tiles, or the previous half, are read
 #pragma unroll
-    for (int y = 0; y < NI; ++y)
+    for (int x = 0; x < MI; ++x) {
 #pragma unroll
-      for (int q = 0; q < 16; ++q)
-        E[(wm * WR + x * 32 + 8 * (q >> 2) + 4 * lh + (q & 3)) * ELD + wn * WC + y * 32 + lr] = acc[x][y][q];
-  __syncthreads();
-
-  // epilogue: wave w finishes rows 32 w .. 32 w + 31 of the tile, R rows at a time
-  double theta[8];
-  if constexpr (ROPE) {
+      for (int y = 0; y < NI; ++y) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int jj = (lane_in_row * 8 + e) % (D / 2);
-      theta[e] = exp2(-(2.0 * jj / D) * a.rope_log2_base);
+        for (int q = 0; q < 16; ++q) {
+          const int row = wm * WR + x * 32 + 8 * (q >> 2) + 4 * lh + (q & 3) - h * EH;
+          if (row >= 0 && row < EH) E[row * ELD + wn * WC + y * 32 + lr] = acc[x][y][q];
+        }
+      }
     }
-  }
-  const int gl = a.group / 8;
+    __syncthreads();
 #pragma unroll
-  for (int p = 0; p < NP; ++p) {
-    const int r = wave * 32 + p * R + row_in_wave, t = t0 + r;
-    if (t >= T) continue;                  // whole rows (L lanes) drop out together
-    float xt[8];
-    {
-      const jf4 u0 = *reinterpret_cast<const jf4 *>(E + r * ELD + lane_in_row * 8);
-      const jf4 u1 = *reinterpret_cast<const jf4 *>(E + r * ELD + lane_in_row * 8 + 4);
-      xt[0] = u0.x; xt[1] = u0.y; xt[2] = u0.z; xt[3] = u0.w; xt[4] = u1.x; xt[5] = u1.y; xt[6] = u1.z; xt[7] = u1.w;
-      const int xe = ks - (USPLIT ? 6 : 0);
+    for (int pp = 0; pp < NPH; ++pp) {
+      const int rr = wave * (EH / 4) + pp * R + row_in_wave, t = t0 + h * EH + rr;
+      if (t >= T) continue;                // whole rows (L lanes) drop out together
+      float xt[8];
+      {
+        const jf4 u0 = *reinterpret_cast<const jf4 *>(E + rr * ELD + lane_in_row * 8);
+        const jf4 u1 = *reinterpret_cast<const jf4 *>(E + rr * ELD + lane_in_row * 8 + 4);
+        xt[0] = u0.x; xt[1] = u0.y; xt[2] = u0.z; xt[3] = u0.w; xt[4] = u1.x; xt[5] = u1.y; xt[6] = u1.z; xt[7] = u1.w;
+        const int xe = ks - (USPLIT ? 6 : 0);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) xt[e] = rT > 0 ? ldexpf(xt[e], xe) : 0.f;   // exact
-    }
-    const int64_t elem = ((int64_t)s * T + t) * D + lane_in_row * 8;
-    if constexpr (MODE == FUSED_XTILDE) {
-      store8(c.xt_out + elem, xt);
-    } else if constexpr (MODE == FUSED_RESIDUAL) {
-      float v[8];
-      raw_f32(px[p], v);
+        for (int e = 0; e < 8; ++e) xt[e] = rT > 0 ? ldexpf(xt[e], xe) : 0.f;   // exact
+      }
+      const int64_t elem = ((int64_t)s * T + t) * D + lane_in_row * 8;
+      if constexpr (MODE == FUSED_XTILDE) {
+        store8(c.xt_out + elem, xt);
+      } else if constexpr (MODE == FUSED_RESIDUAL) {
+        float v[8];
+        raw_f32(px[pp], v);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = (v[e] - xt[e]) * sgv[e];
-      fwht_row<D>(v, lane_in_row);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] *= a.inv_sqrt_d;
-      uint32_t code[8];
-      float delta;
-      quantize8(v, c.bits, gl, code, delta);
-      store_codes(c.codes, elem, c.bits, code);
-      if ((lane_in_row % gl) == 0) c.scales[elem / a.group] = h_bits(delta);
-    } else {
-      float v[8];
-      if (c.bits) {
-        uint32_t code[8];
-        codes_unpack(pcode[p], c.bits, code);
-        const float delta = h_val(pscale[p]);
-        const float mid = 0.5f * (float)((1 << c.bits) - 1);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = ((float)code[e] - mid) * delta;
+        for (int e = 0; e < 8; ++e) v[e] = (v[e] - xt[e]) * sgv[e];
         fwht_row<D>(v, lane_in_row);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = xt[e] + sgv[e] * (v[e] * a.inv_sqrt_d);
+        for (int e = 0; e < 8; ++e) v[e] *= a.inv_sqrt_d;
+        uint32_t code[8];
+        float delta;
+        quantize8(v, c.bits, gl, lane_in_row, code, delta);
+        store_codes(c.codes, elem, c.bits, code);
+        if ((lane_in_row % gl) == 0) c.scales[elem / a.group] = h_bits(delta);
       } else {
+        float v[8];
+        if (c.bits) {
+          uint32_t code[8];
+          codes_unpack(pcode[pp], c.bits, code);
+          const float delta = h_val(pscale[pp]);
+          const float mid = 0.5f * (float)((1 << c.bits) - 1);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = xt[e];
+          for (int e = 0; e < 8; ++e) v[e] = ((float)code[e] - mid) * delta;
+          fwht_row<D>(v, lane_in_row);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = xt[e] + sgv[e] * (v[e] * a.inv_sqrt_d);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = xt[e];
+        }
+        if constexpr (ROPE) {
+          double theta[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int jj = (lane_in_row * 8 + e) % (D / 2);
+            theta[e] = exp2(-(2.0 * jj / D) * a.rope_log2_base);
+          }
+          rope_row<D>(v, lane_in_row, (double)(t + a.rope_offset), theta);
+        }
+        store8(reinterpret_cast<TIO *>(c.out) + srow + (int64_t)t * a.s_tok + lane_in_row * 8, v);
       }
-      if constexpr (ROPE) rope_row<D>(v, lane_in_row, (double)(t + a.rope_offset), theta);
-      store8(reinterpret_cast<TIO *>(c.out) + srow + (int64_t)t * a.s_tok + lane_in_row * 8, v);
     }
   }
 }
 
 // k_s of every (cell, slice): the smallest power of two with max |W_s| 2^-k_s <= 2^14
-// (0 for an all-zero slice or a cell without backbone); one workgroup per (slice, cell).
-__global__ void __launch_bounds__(256) k_w_exponent(const FusedCell *cells, int m, int d) {
+// (0 for an all-zero slice or a cell without backbone), then every entry of W_s^T up to
+// column round8(r_T) rewritten in place as the pair (hi, lo) of fp16 terms of W 2^-k_s, hi in
+// the low half-word (zeros from r_T on).  One workgroup per (slice, cell).
+__global__ void __launch_bounds__(256) k_w_prepare(const FusedCell *cells, int m, int d) {
   const int s = blockIdx.x, cell = blockIdx.y;
   const FusedCell &c = cells[cell];
-  if (s >= m) return;
+  if (s >= m || c.rT <= 0) return;
+  float *W = c.Wt + (int64_t)s * d * c.ldw;
+  // the columns the fused passes read, 0 .. round8(r_T) - 1 of each row (ldw may be far
+  // wider), as d * n4 chunks of 4 entries, four chunks in flight per thread; chunk q is
+  // row q / n4, entries 4 (q % n4) .. + 3
+  const int n4 = ((c.rT + 7) / 8) * 2, nq = d * n4;
+  const float inv_n4 = 1.f / (float)n4;
+  auto row_of = [&](int q) {                      // exact q / n4 for q < 2^24
+    int r = (int)((float)q * inv_n4);
+    if (r * n4 > q) --r;
+    if ((r + 1) * n4 <= q) ++r;
+    return r;
+  };
+  auto addr = [&](int q) {                        // float offset of chunk q in the slice
+    const int r = row_of(q);
+    return (int64_t)r * c.ldw + 4 * (q - r * n4);
+  };
+  constexpr int U4 = 4;
   float mx = 0.f;
-  if (c.rT > 0) {
-    const float *W = c.Wt + (int64_t)s * d * c.ldw;
-    for (int q = threadIdx.x; q < d * c.rT; q += 256) {
-      const int f = q / c.rT, k = q - f * c.rT;
-      mx = fmaxf(mx, fabsf(W[(int64_t)f * c.ldw + k]));
+  for (int q0 = threadIdx.x; q0 < nq; q0 += 256 * U4) {
+    jf4 v[U4];
+#pragma unroll
+    for (int u = 0; u < U4; ++u) {
+      const int q = q0 + 256 * u;
+      v[u] = q < nq ? gload_f4(W + addr(q)) : jf4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int u = 0; u < U4; ++u) {
+      const int q = q0 + 256 * u;
+      const int k = 4 * (q - row_of(q) * n4);
+      if (q < nq) {
+        mx = fmaxf(mx, fmaxf(fmaxf(k < c.rT ? fabsf(v[u].x) : 0.f, k + 1 < c.rT ? fabsf(v[u].y) : 0.f),
+                             fmaxf(k + 2 < c.rT ? fabsf(v[u].z) : 0.f, k + 3 < c.rT ? fabsf(v[u].w) : 0.f)));
+      }
     }
   }
   for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
   __shared__ float red[4];
+  __shared__ int ks_s;
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -374,6 +440,32 @@ __global__ void __launch_bounds__(256) k_w_exponent(const FusedCell *cells, int 
       e = (f == 0.5f ? ex - 1 : ex) - 14;          // ceil(log2 mx) - 14
     }
     c.wexp[s] = e;
+    ks_s = e;
+  }
+  __syncthreads();
+  const int ks = ks_s;
+  for (int q0 = threadIdx.x; q0 < nq; q0 += 256 * U4) {
+    jf4 v[U4];
+#pragma unroll
+    for (int u = 0; u < U4; ++u) {
+      const int q = q0 + 256 * u;
+      v[u] = q < nq ? gload_f4(W + addr(q)) : jf4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int u = 0; u < U4; ++u) {
+      const int q = q0 + 256 * u;
+      if (q >= nq) continue;
+      const int k = 4 * (q - row_of(q) * n4);
+      const float x[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+      uint32_t o[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        uint16_t hi = 0, lo = 0;
+        if (k + e < c.rT) split_f16(ldexpf(x[e], -ks), hi, lo);
+        o[e] = pk2(hi, lo);
+      }
+      *reinterpret_cast<ju4 *>(W + addr(q)) = ju4{o[0], o[1], o[2], o[3]};
+    }
   }
 }
 
@@ -411,9 +503,9 @@ hipError_t launch_m(const FusedArgs &a, int d, int io_dtype, bool split, bool ro
 
 int fused_tile_tokens() { return BT; }
 
-hipError_t launch_w_exponent(const FusedCell *cells_dev, int n_cells, int m, int d, hipStream_t st) {
+hipError_t launch_w_prepare(const FusedCell *cells_dev, int n_cells, int m, int d, hipStream_t st) {
   if (n_cells <= 0 || m <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_w_exponent, dim3(m, n_cells), dim3(256), 0, st, cells_dev, m, d);
+  hipLaunchKernelGGL(k_w_prepare, dim3(m, n_cells), dim3(256), 0, st, cells_dev, m, d);
   return hipGetLastError();
 }
 

@@ -67,7 +67,7 @@ __global__ void __launch_bounds__(256) k_eps2_partial(Eps2Args a) {
       const int bits = 2 << bi;
       uint32_t code[8];
       float delta;
-      quantize8(v, bits, gl, code, delta);
+      quantize8(v, bits, gl, lane_in_row, code, delta);
       const float mid = 0.5f * (float)((1 << bits) - 1);
       float y[8];
 #pragma unroll

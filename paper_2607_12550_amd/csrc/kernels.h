@@ -21,8 +21,10 @@ struct Eps2Args {
 // X~_s = U^_T W_s rebuilt on the fp16 matrix cores inside the residual / decode passes.
 struct FusedCell {
   const void *UT;           // blob U_T section: T x rT, fp16 or fp32 (the call's factor type)
-  const float *Wt;          // m slices of d x ldw fp32: W_s^T = 2^e_s U^_d G^_s^T
-  int32_t *wexp;            // m per-slice exponents k_s (written by launch_w_exponent)
+  float *Wt;                // m slices of d x ldw: W_s^T = 2^e_s U^_d G^_s^T in fp32, which
+                            // launch_w_prepare rewrites in place, entry by entry, as the fp16
+                            // pair (hi, lo) of W_s^T 2^-k_s (hi in the low half-word)
+  int32_t *wexp;            // m per-slice exponents k_s (written by launch_w_prepare)
   const void *x;            // residual: cache cell base (strided, input type)
   void *out;                // decode: output cell base (strided, output type)
   uint8_t *codes;           // packed codes (written by the residual pass, read by decode)
@@ -42,7 +44,9 @@ struct FusedArgs {
   double rope_log2_base;
 };
 int fused_tile_tokens();
-hipError_t launch_w_exponent(const FusedCell *cells_dev, int n_cells, int m, int d, hipStream_t st);
+// Per (cell, slice): k_s = the smallest power of two with max |W_s| 2^-k_s <= 2^14, then
+// every entry of W_s^T rewritten in place as its fp16 hi + lo split (zeros past r_T).
+hipError_t launch_w_prepare(const FusedCell *cells_dev, int n_cells, int m, int d, hipStream_t st);
 // io_dtype: the cache type (residual) or the output type (decode); split_factors: the
 // factors are fp32 (U_T split into two fp16 terms)
 hipError_t launch_fused(FusedArgs a, int mode, int d, int io_dtype, bool split_factors, hipStream_t st);

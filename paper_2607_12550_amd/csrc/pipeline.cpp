@@ -449,7 +449,7 @@ int build_w(Run &R, int nc, int m, int d, const std::vector<BlobView> &bv, const
   }
   int rc = R.gemm(P, 1, ft, ft, true, true);
   if (rc) return rc;
-  HIP_OK(launch_w_exponent(R.w.fcell_r, nc, m, d, R.st));
+  HIP_OK(launch_w_prepare(R.w.fcell_r, nc, m, d, R.st));
   return JOLT_OK;
 }
 

@@ -4,8 +4,8 @@
 // Layout on the wavefront: a feature row of D entries is held by D/8 consecutive lanes,
 // 8 contiguous entries per lane, so one wave64 processes 512/D rows at a time.  The
 // Walsh-Hadamard transform runs its first three butterfly stages inside the lane and the
-// remaining log2(D/8) stages across lanes with xor shuffles.  A quantiser group of g
-// entries spans g/8 lanes; its max is a shuffle reduction.
+// remaining log2(D/8) stages across lanes (DPP within the 16-lane row).  A quantiser group
+// of g entries spans g/8 lanes; its max is a reduction over them.
 #pragma once
 #include "common.h"
 
@@ -17,6 +17,47 @@ struct RowLayout {
   static constexpr int R = 64 / L;       // rows per wave
 };
 
+// Value held by lane `lane ^ M`.  For M < 16 the partner lies in the same row of 16 lanes and
+// DPP reads it inside the ALU (quad permutes for M = 1, 2; row shifts left / right by M,
+// picked by the lane's bit M, for M = 4, 8); wider distances go through the LDS crossbar.
+template <int M>
+JOLT_DEV float xor_lane(float v, int lane) {
+  const int x = __float_as_int(v);
+  if constexpr (M == 1) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, x, 0xB1, 0xf, 0xf, false));   // [1,0,3,2]
+  } else if constexpr (M == 2) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, x, 0x4E, 0xf, 0xf, false));   // [2,3,0,1]
+  } else if constexpr (M == 4 || M == 8) {
+    const int from_hi = __builtin_amdgcn_update_dpp(0, x, 0x100 + M, 0xf, 0xf, false);  // lane + M
+    const int from_lo = __builtin_amdgcn_update_dpp(0, x, 0x110 + M, 0xf, 0xf, false);  // lane - M
+    return __int_as_float((lane & M) ? from_lo : from_hi);
+  } else {
+    return __shfl_xor(v, M, 64);
+  }
+}
+
+// one butterfly stage across lanes at distance M: lower lane a + b, upper lane a' - b'
+template <int M>
+JOLT_DEV void xstage(float (&v)[8], int lane_in_row) {
+  const bool upper = (lane_in_row & M) != 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float p = xor_lane<M>(v[i], lane_in_row);
+    v[i] = upper ? (p - v[i]) : (v[i] + p);
+  }
+}
+
+// max over the gl lanes of a quantiser group (gl a power of two, at most 64)
+JOLT_DEV float group_max(float a, int gl, int lane) {
+  if (gl > 1) a = fmaxf(a, xor_lane<1>(a, lane));
+  if (gl > 2) a = fmaxf(a, xor_lane<2>(a, lane));
+  if (gl > 4) a = fmaxf(a, xor_lane<4>(a, lane));
+  if (gl > 8) a = fmaxf(a, xor_lane<8>(a, lane));
+  if (gl > 16) a = fmaxf(a, xor_lane<16>(a, lane));
+  if (gl > 32) a = fmaxf(a, xor_lane<32>(a, lane));
+  return a;
+}
+
 // Rotary embedding of one decoded row spread over L lanes (8 features each): features j and
 // j + D/2 sit in lanes l and l + L/2 and rotate together by the angle pos * theta_j, formed
 // and reduced in fp64.
@@ -26,7 +67,7 @@ JOLT_DEV void rope_row(float (&v)[8], int lane_in_row, double pos, const double 
   const bool upper = lane_in_row >= L / 2;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    const float partner = shfl_xor(v[i], L / 2);
+    const float partner = xor_lane<L / 2>(v[i], lane_in_row);
     double sn, cs;
     sincos(pos * theta[i], &sn, &cs);
     const float c = (float)cs, s = (float)sn;
@@ -48,15 +89,13 @@ JOLT_DEV void fwht_row(float (&v)[8], int lane_in_row) {
       }
     }
   }
-#pragma unroll
-  for (int lm = 1; lm < RowLayout<D>::L; lm <<= 1) {
-    const bool upper = (lane_in_row & lm) != 0;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      float p = shfl_xor(v[i], lm);
-      v[i] = upper ? (p - v[i]) : (v[i] + p);
-    }
-  }
+  constexpr int L = RowLayout<D>::L;
+  if constexpr (L > 1) xstage<1>(v, lane_in_row);
+  if constexpr (L > 2) xstage<2>(v, lane_in_row);
+  if constexpr (L > 4) xstage<4>(v, lane_in_row);
+  if constexpr (L > 8) xstage<8>(v, lane_in_row);
+  if constexpr (L > 16) xstage<16>(v, lane_in_row);
+  if constexpr (L > 32) xstage<32>(v, lane_in_row);
 }
 
 template <typename T>
@@ -95,23 +134,27 @@ JOLT_DEV void store8(float *p, const float (&v)[8]) {
 }
 
 // Quantise 8 rotated entries of one lane; group max over gl = g/8 lanes.
-JOLT_DEV void quantize8(const float (&r)[8], int bits, int gl, uint32_t (&code)[8], float &delta) {
+JOLT_DEV void quantize8(const float (&r)[8], int bits, int gl, int lane_in_row, uint32_t (&code)[8],
+                        float &delta) {
   float a = 0.f;
 #pragma unroll
   for (int i = 0; i < 8; ++i) a = fmaxf(a, fabsf(r[i]));
-  for (int m = 1; m < gl; m <<= 1) a = fmaxf(a, shfl_xor(a, m));
+  a = group_max(a, gl, lane_in_row);
   const int levels = (1 << bits) - 1;
   float dl = 2.f * a / (float)levels;
   dl = fminf(dl, 65504.f);
   delta = f16_round(dl);
   const float mid = 0.5f * (float)levels;
+  // r / delta as r * (1 / delta): within 1.5 ulp of the quotient, so a code moves only when
+  // the quotient lies that close to a rounding boundary
+  const float inv = delta == 0.f ? 0.f : 1.f / delta;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     float c;
     if (delta == 0.f) {
       c = (float)(1 << (bits - 1));
     } else {
-      c = __builtin_rintf(r[i] / delta + mid);
+      c = __builtin_rintf(fmaf(r[i], inv, mid));
       c = fminf(fmaxf(c, 0.f), (float)levels);
     }
     code[i] = (uint32_t)c;
