@@ -44,6 +44,7 @@ constexpr int LDS_BYTES = 160 * 1024;
 struct Grid {
   int tiles_m, tiles_n, per_prob, lower_only;
   int total, per_xcd;
+  int wide;                 // lower-triangle tables with 256-row tiles (two tile columns per row)
 };
 
 JOLT_DEV int64_t opoff(const GemmOperand &op, int row, int col) {
@@ -218,7 +219,14 @@ JOLT_DEV bool decode(const Grid &g, int j, int &z, int &tm, int &tn) {
   if (j >= g.total) return false;
   z = j / g.per_prob;
   int r = j - z * g.per_prob;
-  if (g.lower_only) {
+  if (g.lower_only && g.wide) {
+    // 256 x 128 tiles: row tm holds the 2 tm + 2 tiles tn <= 2 tm + 1 (the last row may
+    // hold fewer), so the r-th lower tile has tm (tm + 1) <= r
+    int t = (int)((sqrtf(4.f * (float)r + 1.f) - 1.f) * 0.5f);
+    while ((t + 1) * (t + 2) <= r) ++t;
+    while (t * (t + 1) > r) --t;
+    tm = t; tn = r - t * (t + 1);
+  } else if (g.lower_only) {
     // r-th lower tile in row-major order: tm (tm + 1) / 2 <= r
     int t = (int)((sqrtf(8.f * (float)r + 1.f) - 1.f) * 0.5f);
     while ((t + 1) * (t + 2) / 2 <= r) ++t;
@@ -496,10 +504,13 @@ bool gemm16_prepare(GemmProblem *probs, int n, int &ta, int &tb, bool &ak, bool 
   }
   if (swap) { std::swap(ta, tb); std::swap(ak, bk); }
   // 256-row tiles for split-operand products over long M whose bf16 operand is k-contiguous
-  // (two LDS buffers still fit); 128 otherwise (an m-contiguous bf16 operand is transposed
-  // on its way to LDS, and the 128-row tile then runs two workgroups per CU), and always for
-  // lower-triangle tables
-  bm = (tb == GT_F32 && ta == GT_BF16 && maxM >= 2048 && !lower && ak) ? 256 : 128;
+  // (two LDS buffers still fit) and for large lower-triangle bf16 tables (the token Gram:
+  // each K step then moves 384 operand rows for 256 x 128 outputs instead of 256 rows for
+  // 128 x 128); 128 otherwise (an m-contiguous bf16 operand is transposed on its way to LDS,
+  // and the 128-row tile then runs two workgroups per CU)
+  const bool bf_both = ta == GT_BF16 && tb == GT_BF16 && ak && bk;
+  bm = ((tb == GT_F32 && ta == GT_BF16 && maxM >= 2048 && !lower && ak) ||
+        (lower && bf_both && maxM >= 2048)) ? 256 : 128;
   return true;
 }
 
@@ -510,12 +521,18 @@ hipError_t launch_gemm16(const GemmProblem *probs_dev, int n_probs, int max_M, i
   const bool as = ta == GT_F32, bs = tb == GT_F32;
   if ((ta != GT_BF16 && !as) || (tb != GT_BF16 && !bs)) return hipErrorInvalidValue;
   if (bm != 128 && bm != 256) return hipErrorInvalidValue;
-  if (lower_only && bm != BN) return hipErrorInvalidValue;
+  if (lower_only && bm == 256 && (as || bs)) return hipErrorInvalidValue;
   Grid g;
   g.tiles_m = (max_M + bm - 1) / bm;
   g.tiles_n = (max_N + BN - 1) / BN;
   g.lower_only = lower_only ? 1 : 0;
-  g.per_prob = lower_only ? g.tiles_m * (g.tiles_m + 1) / 2 : g.tiles_m * g.tiles_n;
+  g.wide = lower_only && bm == 256 ? 1 : 0;
+  if (g.wide) {
+    // rows of 2 tm + 2 tiles; the last row is cut to the tile columns that exist
+    g.per_prob = g.tiles_m * (g.tiles_m + 1) - std::max(0, 2 * g.tiles_m - g.tiles_n);
+  } else {
+    g.per_prob = lower_only ? g.tiles_m * (g.tiles_m + 1) / 2 : g.tiles_m * g.tiles_n;
+  }
   g.total = g.per_prob * n_probs;
   g.per_xcd = (g.total + 7) / 8;
   if (bm == 256) {
