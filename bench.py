@@ -163,8 +163,8 @@ def roofline_report(model, prof_c, prof_d, step_ms):
 
 # kernel source of each pass whose HBM traffic was taken with hardware counters
 PASS_SOURCE = {"token_gram": "paper_2607_12550_amd/csrc/k_gemm16.hip",
-               "residual": "paper_2607_12550_amd/csrc/k_residual.hip",
-               "decode": "paper_2607_12550_amd/csrc/k_residual.hip"}
+               "residual": "paper_2607_12550_amd/csrc/k_fused.hip",
+               "decode": "paper_2607_12550_amd/csrc/k_fused.hip"}
 
 
 def measured_traffic(name, workload):
