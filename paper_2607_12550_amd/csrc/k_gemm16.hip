@@ -494,23 +494,26 @@ bool gemm16_prepare(GemmProblem *probs, int n, int &ta, int &tb, bool &ak, bool 
   }
   for (int i = 1; i < n; ++i)
     if ((probs[i].lower_only != 0) != (probs[0].lower_only != 0)) return false;
-  int maxM = 0;
+  int maxM = 0, minK = 1 << 30;
   bool lower = false;
   for (int i = 0; i < n; ++i) {
     GemmProblem &p = probs[i];
     if (swap) { std::swap(p.A, p.B); std::swap(p.M, p.N); p.c_trans = 1; }
     maxM = std::max(maxM, p.M);
+    minK = std::min(minK, p.K);
     lower = lower || p.lower_only;
   }
   if (swap) { std::swap(ta, tb); std::swap(ak, bk); }
   // 256-row tiles for split-operand products over long M whose bf16 operand is k-contiguous
-  // (two LDS buffers still fit) and for large lower-triangle bf16 tables (the token Gram:
-  // each K step then moves 384 operand rows for 256 x 128 outputs instead of 256 rows for
-  // 128 x 128); 128 otherwise (an m-contiguous bf16 operand is transposed on its way to LDS,
-  // and the 128-row tile then runs two workgroups per CU)
+  // (two LDS buffers still fit) and for large lower-triangle bf16 tables with a long K (the
+  // token Gram of wide cells: each K step then moves 384 operand rows for 256 x 128 outputs
+  // instead of 256 rows for 128 x 128; measured faster from K = 25600, slower at K = 4096,
+  // where the 128-row tiles keep two workgroups per CU busy); 128 otherwise (an m-contiguous
+  // bf16 operand is transposed on its way to LDS, and the 128-row tile then runs two
+  // workgroups per CU)
   const bool bf_both = ta == GT_BF16 && tb == GT_BF16 && ak && bk;
   bm = ((tb == GT_F32 && ta == GT_BF16 && maxM >= 2048 && !lower && ak) ||
-        (lower && bf_both && maxM >= 2048)) ? 256 : 128;
+        (lower && bf_both && maxM >= 2048 && minK >= 16384)) ? 256 : 128;
   return true;
 }
 
