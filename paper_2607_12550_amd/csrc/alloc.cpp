@@ -19,6 +19,14 @@
 // most 200 halvings) and returns the allocation at hi.  This file is compiled
 // without floating-point contraction so the arithmetic is plain IEEE double.
 //
+// Speed: the grids of the cells are built and sorted, and each bisection step evaluated,
+// on up to 16 host threads (each cell by one thread, totals summed in cell order, so the
+// result does not depend on the split), and each bisection step scans only the Pareto
+// frontier of a grid.  A point q off the frontier has an earlier
+// point p with s_p <= s_q and e_p <= e_q; rounding is monotone, so for every lambda >= 0
+// e_p + lambda s_p <= e_q + lambda s_q in floating point too, and q can never be the first
+// point of minimal value: the scan over the frontier returns what the full scan returns.
+//
 // The ablation allocators of section 7 (rank-only, greedy, uniform rank) use the same
 // grid, costs and model errors; their definitions are stated with JOLT_ALLOC_* in the
 // public header.
@@ -27,7 +35,12 @@
 #include <cstdint>
 #include <limits>
 #include <map>
+#include <atomic>
+#include <condition_variable>
+#include <functional>
+#include <mutex>
 #include <set>
+#include <thread>
 #include <tuple>
 #include <vector>
 
@@ -80,6 +93,70 @@ int64_t byte_cost(int64_t m, int64_t T, int64_t d, int64_t rT, int64_t rd, int64
   return s;
 }
 
+// Runs a per-cell task for cells 0 .. n-1 on the calling thread and nthr - 1 workers that
+// persist across run() calls; run() returns when every cell is done.
+class CellPool {
+ public:
+  CellPool(int nthr, int n) : n_(n) {
+    for (int t = 1; t < nthr; ++t) workers_.emplace_back([this] { loop(); });
+  }
+  ~CellPool() {
+    {
+      std::lock_guard<std::mutex> g(mu_);
+      stop_ = true;
+      ++gen_;
+    }
+    cv_.notify_all();
+    for (auto &w : workers_) w.join();
+  }
+  void run(const std::function<void(int)> &f) {
+    {
+      std::lock_guard<std::mutex> g(mu_);
+      task_ = &f;
+      next_ = 0;
+      busy_ = (int)workers_.size();
+      ++gen_;
+    }
+    cv_.notify_all();
+    drain(f);
+    std::unique_lock<std::mutex> g(mu_);
+    done_.wait(g, [this] { return busy_ == 0; });
+    task_ = nullptr;
+  }
+
+ private:
+  void drain(const std::function<void(int)> &f) {
+    for (int ci = next_++; ci < n_; ci = next_++) f(ci);
+  }
+  void loop() {
+    uint64_t seen = 0;
+    for (;;) {
+      const std::function<void(int)> *f;
+      {
+        std::unique_lock<std::mutex> g(mu_);
+        cv_.wait(g, [&] { return gen_ != seen; });
+        seen = gen_;
+        if (stop_) return;
+        f = task_;
+      }
+      drain(*f);
+      {
+        std::lock_guard<std::mutex> g(mu_);
+        if (--busy_ == 0) done_.notify_one();
+      }
+    }
+  }
+  const int n_;
+  std::vector<std::thread> workers_;
+  std::mutex mu_;
+  std::condition_variable cv_, done_;
+  const std::function<void(int)> *task_ = nullptr;
+  std::atomic<int> next_{0};
+  int busy_ = 0;
+  uint64_t gen_ = 0;
+  bool stop_ = false;
+};
+
 // Pareto frontier of a grid in grid order: the points whose error is below that of every
 // earlier (cheaper or equal-cost, earlier-ordered) point
 std::vector<int> pareto(const std::vector<Point> &pts) {
@@ -111,11 +188,16 @@ extern "C" int jolt_allocate(const jolt_cell_spectrum *cells, int n_cells, const
       return jolt_fail(JOLT_E_INVAL, "jolt_allocate: malformed cell spectrum %d", ci);
     if (c.n_mu < 0 || (c.n_mu > 0 && !c.mu))
       return jolt_fail(JOLT_E_INVAL, "jolt_allocate: malformed truncated spectra of cell %d", ci);
+  }
+  // grid of one cell, sorted in grid order
+  auto build = [&](int ci) {
+    const jolt_cell_spectrum &c = cells[ci];
     const std::vector<double> tT = tail_fractions(c.lam_T, c.n_lam_T, c.E);
     const std::vector<double> td = tail_fractions(c.lam_d, c.d, c.E);
     const std::vector<double> tx = exact_tau_table(c.mu, c.n_mu, c.d, c.E);
     const int rT_hi = c.n_mu > 0 ? std::min<int64_t>(c.rT_max, (int64_t)c.n_mu * o->step) : c.rT_max;
     std::vector<Point> &pts = grids[ci];
+    pts.reserve((size_t)4 * (rT_hi / o->step + 1) * (c.d / o->step + 1));
     for (int bi = 0; bi < 4; ++bi) {
       if (!(mask & (1 << bi))) continue;
       const int b = bit_values[bi];
@@ -141,11 +223,14 @@ extern "C" int jolt_allocate(const jolt_cell_spectrum *cells, int n_cells, const
         }
       }
     }
-    if (pts.empty()) return jolt_fail(JOLT_E_INVAL, "jolt_allocate: empty grid for cell %d", ci);
-    std::sort(pts.begin(), pts.end(), [](const Point &a, const Point &b) {
-      return std::make_tuple(a.s, a.b, a.rT, a.rd) < std::make_tuple(b.s, b.b, b.rT, b.rd);
-    });
-  }
+    // the points were made in (b, r_T, r_d) order, so a stable sort on s gives grid order
+    std::stable_sort(pts.begin(), pts.end(), [](const Point &a, const Point &b) { return a.s < b.s; });
+  };
+  const unsigned hw = std::max(1u, std::thread::hardware_concurrency());
+  CellPool pool(std::max(1, std::min<int>(n_cells, (int)std::min(16u, hw))), n_cells);
+  pool.run(build);
+  for (int ci = 0; ci < n_cells; ++ci)
+    if (grids[ci].empty()) return jolt_fail(JOLT_E_INVAL, "jolt_allocate: empty grid for cell %d", ci);
   std::vector<int> idx(n_cells), idx_hi(n_cells);
   auto emit = [&](const std::vector<int> &sel, double lam, int infeas) {
     double tb = 0.0, te = 0.0;
@@ -239,19 +324,33 @@ extern "C" int jolt_allocate(const jolt_cell_spectrum *cells, int n_cells, const
       idx[ci] = where[ci].at(std::make_tuple(cands[pick].b, cands[pick].rT, cands[pick].rd));
     return emit(idx, 0.0, infeas);
   }
-  auto choose = [&](double lam, std::vector<int> &out) {
-    double total = 0.0;
-    for (int ci = 0; ci < n_cells; ++ci) {
-      const std::vector<Point> &pts = grids[ci];
-      int best = 0;
-      double bv = pts[0].e + lam * (double)pts[0].s;
-      for (int k = 1; k < (int)pts.size(); ++k) {
-        const double v = pts[k].e + lam * (double)pts[k].s;
-        if (v < bv) { bv = v; best = k; }
-      }
-      out[ci] = best;
-      total += (double)pts[best].s;
+  // the frontier of each grid, led by its first point in every case (a NaN error there
+  // would make the full scan keep point 0)
+  std::vector<std::vector<int>> front(n_cells);
+  for (int ci = 0; ci < n_cells; ++ci) {
+    front[ci] = pareto(grids[ci]);
+    if (front[ci].empty() || front[ci][0] != 0) front[ci].insert(front[ci].begin(), 0);
+  }
+  double lam_cur = 0.0;
+  std::vector<int> *out_cur = nullptr;
+  const std::function<void(int)> pick = [&](int ci) {
+    const std::vector<Point> &pts = grids[ci];
+    const std::vector<int> &f = front[ci];
+    int best = 0;
+    double bv = pts[0].e + lam_cur * (double)pts[0].s;
+    for (size_t q = 1; q < f.size(); ++q) {
+      const Point &p = pts[f[q]];
+      const double v = p.e + lam_cur * (double)p.s;
+      if (v < bv) { bv = v; best = f[q]; }
     }
+    (*out_cur)[ci] = best;
+  };
+  auto choose = [&](double lam, std::vector<int> &out) {
+    lam_cur = lam;
+    out_cur = &out;
+    pool.run(pick);
+    double total = 0.0;
+    for (int ci = 0; ci < n_cells; ++ci) total += (double)grids[ci][out[ci]].s;
     return total;
   };
   if (choose(0.0, idx) <= B) return emit(idx, 0.0, 0);

@@ -262,8 +262,12 @@ StageTimer::~StageTimer() {
 }
 
 jolt_ctx::~jolt_ctx() {
-  if (trd_exec) (void)hipGraphExecDestroy(trd_exec);
-  if (cap_stream) (void)hipStreamDestroy(cap_stream);
+  for (int g = 0; g < kTrdLanes; ++g) {
+    if (trd_exec[g]) (void)hipGraphExecDestroy(trd_exec[g]);
+    if (cap_stream[g]) (void)hipStreamDestroy(cap_stream[g]);
+    if (trd_join[g]) (void)hipEventDestroy(trd_join[g]);
+  }
+  if (trd_fork) (void)hipEventDestroy(trd_fork);
   for (auto &r : prof_pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
   for (auto e : prof_pool) (void)hipEventDestroy(e);
 }

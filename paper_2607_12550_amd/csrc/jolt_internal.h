@@ -70,9 +70,15 @@ struct jolt_ctx {
   std::vector<hipEvent_t> prof_pool;
   double prof_ms[JOLT_STAGE_COUNT] = {};
   int64_t prof_n[JOLT_STAGE_COUNT] = {};
-  // replay of the fixed launch sequence of the blocked tridiagonalisation
-  hipStream_t cap_stream = nullptr;
-  hipGraphExec_t trd_exec = nullptr;
+  // replay of the fixed launch sequence of the blocked tridiagonalisation: the batch is
+  // split into kTrdLanes groups of matrices, each captured once and replayed on a stream
+  // of its own, so that one group's latency-bound column kernels run beside another
+  // group's bandwidth-bound mat-vec (all streams at the default priority)
+  static constexpr int kTrdLanes = 2;
+  hipStream_t cap_stream[kTrdLanes] = {};
+  hipGraphExec_t trd_exec[kTrdLanes] = {};
+  hipEvent_t trd_fork = nullptr, trd_join[kTrdLanes] = {};
+  int trd_lanes = 0;
   std::vector<const void *> trd_key;
   int invit_iters = 2;            // inverse-iteration sweeps (test hook jolt_debug_set)
   void *attend_scratch = nullptr; // this device's fixed attention scratch (device address)

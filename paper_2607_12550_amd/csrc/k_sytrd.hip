@@ -70,42 +70,16 @@ JOLT_DEV MatView view(const SytrdArgs &a, int mat) {
 // whose origin `base` is o rounded down to a multiple of 32 (so the 128-float row segment a
 // tile reads covers exactly four 128-byte cache lines);
 // entries with row or column < o are masked to zero.  Thread (ty, tx) of the 16 x 16 grid
-// holds an 8 x 8 sub-block in registers; row sums reduce across tx (lane shuffles), column
-// sums across ty (shuffles, then LDS across the four waves).  Tiles (I, 0) also produce the
+// holds 8 rows x 8 columns in registers, the columns being the two runs 4 tx .. 4 tx + 3 and
+// 64 + 4 tx .. 64 + 4 tx + 3 of the tile, so that each 16-byte load of a wave covers two
+// whole cache lines of a row; row sums reduce across tx (lane shuffles), column sums across
+// ty (shuffles, then LDS across the four waves).  Tiles (I, 0) also produce the
 // dot partials [sigma, W_p^T x, V_p^T x] over their 128 rows.
 JOLT_DEV void householder(float alpha, double sigma, double &beta, double &tv, double &scal) {
   if (sigma == 0.0) { tv = 0.0; beta = alpha; scal = 0.0; return; }
   beta = -copysign(sqrt((double)alpha * alpha + sigma), (double)alpha);
   tv = (beta - alpha) / beta;
   scal = 1.0 / (alpha - beta);
-}
-
-// sum_{b < nb_} x[b * stride] in the order b = 0, 1, ... (fp64), loads issued eight at a time
-JOLT_DEV double strided_sum(const float *x, int64_t stride, int nb_) {
-  double s = 0.0;
-  int b = 0;
-  for (; b + 8 <= nb_; b += 8) {
-    float t[8];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) t[q] = x[(int64_t)(b + q) * stride];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) s += (double)t[q];
-  }
-  for (; b < nb_; ++b) s += (double)x[(int64_t)b * stride];
-  return s;
-}
-
-// sum of the nt partial-slot entries of one row (slot s at s * n), in slot order; the
-// first 32 loads are issued together
-JOLT_DEV float slot_sum(const float *pp, int64_t n, int nt) {
-  float t[32];
-#pragma unroll
-  for (int s = 0; s < 32; ++s) t[s] = s < nt ? pp[(int64_t)s * n] : 0.f;
-  float y = 0.f;
-#pragma unroll
-  for (int s = 0; s < 32; ++s) y += t[s];
-  for (int s = 32; s < nt; ++s) y += pp[(int64_t)s * n];
-  return y;
 }
 
 __global__ void __launch_bounds__(RB) k_col_finish(SytrdArgs a, int i, int j, int jbw) {
@@ -121,28 +95,51 @@ __global__ void __launch_bounds__(RB) k_col_finish(SytrdArgs a, int i, int j, in
   float *Qv = M.Q + (int64_t)jbw * n;
   const int r = o + blockIdx.x * RB + tid;
   const int rr = r < n ? r : o;                 // in-range row for the loads
-  // Loads that do not depend on this column's Householder scalars go first, so their
-  // latency overlaps the reduction of sigma and the dots below.
-  const float ysl = slot_sum(M.part + (rr - base), n, nt);
+  // Every load that does not depend on this column's Householder scalars is issued before
+  // any is used and without a branch: entries past the live range read an entry this launch
+  // does not write and are masked afterwards.  The kernel then waits on one memory round
+  // trip before its barrier.
+  const float *pp = M.part + (rr - base);
+  float ts[32];
+#pragma unroll
+  for (int q = 0; q < 32; ++q) ts[q] = pp[(int64_t)min(q, nt - 1) * n];
   const float a_o = M.A[(int64_t)o * n + rr];   // A22[:, 0] (row o by symmetry)
   const float x_r = M.xt[rr];
+  // row f of V is not written by this launch (it writes row j only)
+  const int f = j == 0 ? 1 : 0;
   float vrow[32], wrow[32];
 #pragma unroll
   for (int p = 0; p < 32; ++p) {
-    vrow[p] = p < j ? V[(int64_t)p * n + rr] : 0.f;
-    wrow[p] = p < j ? W[(int64_t)p * n + rr] : 0.f;
+    vrow[p] = V[(int64_t)(p < j ? p : f) * n + rr];
+    wrow[p] = W[(int64_t)(p < j ? p : 0) * n + rr];
   }
-  float w_o = 0.f, v_o = 0.f;
-  if (tid < j) { w_o = W[(int64_t)tid * n + o]; v_o = V[(int64_t)tid * n + o]; }
-  // sigma and the dots, summed over the row blocks in a fixed order
+  float w_o = W[(int64_t)(tid < j ? tid : 0) * n + o];
+  float v_o = V[(int64_t)(tid < j ? tid : f) * n + o];
+  const float alpha = M.sc[0];
+  const int64_t dstride = 2 * nb + 1;
+  const float *dp = M.dpart + min(tid, 2 * j);  // dot of this thread: 0 sigma, then W, V
+  float td[32];
+#pragma unroll
+  for (int b = 0; b < 32; ++b) td[b] = dp[(int64_t)min(b, nprev - 1) * dstride];
+  float ysl = 0.f;
+#pragma unroll
+  for (int q = 0; q < 32; ++q) ysl += q < nt ? ts[q] : 0.f;
+  for (int q = 32; q < nt; ++q) ysl += pp[(int64_t)q * n];
+#pragma unroll
+  for (int p = 0; p < 32; ++p)
+    if (p >= j) { vrow[p] = 0.f; wrow[p] = 0.f; }
+  if (tid >= j) { w_o = 0.f; v_o = 0.f; }
+  // sigma and the dots, summed over the row blocks in the order b = 0, 1, ... (fp64)
   if (tid < 2 * j + 1) {
-    const double s = strided_sum(M.dpart + tid, 2 * nb + 1, nprev);
-    if (tid == 0) sh_sigma = s;
-    else if (tid <= j) pw[tid - 1] = (float)s;
-    else pv[tid - 1 - j] = (float)s;
+    double sd = 0.0;
+#pragma unroll
+    for (int b = 0; b < 32; ++b) sd += b < nprev ? (double)td[b] : 0.0;
+    for (int b = 32; b < nprev; ++b) sd += (double)dp[(int64_t)b * dstride];
+    if (tid == 0) sh_sigma = sd;
+    else if (tid <= j) pw[tid - 1] = (float)sd;
+    else pv[tid - 1 - j] = (float)sd;
   }
   __syncthreads();
-  const float alpha = M.sc[0];
   double beta, tv, scal;
   householder(alpha, sh_sigma, beta, tv, scal);
   const float sc = (float)scal, tf = (float)tv;
@@ -188,12 +185,14 @@ __global__ void __launch_bounds__(256) k_symv_tiles(SytrdArgs a, int i) {
   int I, J;
   tri_decode(rev ? gridDim.x - 1 - blockIdx.x : blockIdx.x, I, J);
   const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4, lane = tid & 63, wave = tid >> 6;
-  const int r0 = I * TB + ty * 8, c0 = J * TB + tx * 8;     // relative to base
+  const int r0 = I * TB + ty * 8;                             // relative to base
+  // column of register c (relative to base): two runs of four
+  auto ccol = [&](int c) { return J * TB + (c < 4 ? tx * 4 + c : 64 + tx * 4 + c - 4); };
   const float *xt = M.xt;
   float xr[8], xc[8];
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
-    const int gr = base + r0 + k, gc = base + c0 + k;
+    const int gr = base + r0 + k, gc = base + ccol(k);
     xr[k] = (gr >= o + 1 && gr < n) ? xt[gr] : 0.f;     // x_tail is zero at o and above it
     xc[k] = (gc >= o + 1 && gc < n) ? xt[gc] : 0.f;
   }
@@ -203,16 +202,16 @@ __global__ void __launch_bounds__(256) k_symv_tiles(SytrdArgs a, int i) {
   const bool diag = (I == J);
   // All 16 row loads are issued before any is consumed: rows outside [o, n) read a clamped
   // in-range row and are zeroed afterwards, so no load sits behind a branch.
-  const int gc0 = base + c0;
+  const int gc0 = base + ccol(0), gc4 = base + ccol(4);
   float v[8][8];
-  if (gc0 + 8 <= n) {
+  if (gc4 + 4 <= n) {
     float4 u[8][2];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const int gr = min(max(base + r0 + k, o), n - 1);
-      const float4 *p = reinterpret_cast<const float4 *>(M.A + (int64_t)gr * n + gc0);
-      u[k][0] = p[0];
-      u[k][1] = p[1];
+      const float *row = M.A + (int64_t)gr * n;
+      u[k][0] = *reinterpret_cast<const float4 *>(row + gc0);
+      u[k][1] = *reinterpret_cast<const float4 *>(row + gc4);
     }
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
@@ -226,19 +225,21 @@ __global__ void __launch_bounds__(256) k_symv_tiles(SytrdArgs a, int i) {
     for (int k = 0; k < 8; ++k) {
       const int gr = base + r0 + k;
 #pragma unroll
-      for (int c = 0; c < 8; ++c)
-        v[k][c] = (gr >= o && gr < n && gc0 + c < n) ? M.A[(int64_t)gr * n + gc0 + c] : 0.f;
+      for (int c = 0; c < 8; ++c) {
+        const int gc = base + ccol(c);
+        v[k][c] = (gr >= o && gr < n && gc < n) ? M.A[(int64_t)gr * n + gc] : 0.f;
+      }
     }
   }
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
 #pragma unroll
     for (int c = 0; c < 8; ++c) {
-      const int gc = gc0 + c;
+      const int gc = base + ccol(c);
       const float e = (gc >= o) ? v[k][c] : 0.f;
       if (diag) {
         // lower part only: row sums take col <= row, column sums take col < row
-        const bool le = (c0 + c) <= (r0 + k), lt = (c0 + c) < (r0 + k);
+        const bool le = ccol(c) <= (r0 + k), lt = ccol(c) < (r0 + k);
         rs[k] = fmaf(le ? e : 0.f, xc[c], rs[k]);
         cs[c] = fmaf(lt ? e : 0.f, xr[k], cs[c]);
       } else {
@@ -266,7 +267,7 @@ __global__ void __launch_bounds__(256) k_symv_tiles(SytrdArgs a, int i) {
   }
   if (lane < 16) {
 #pragma unroll
-    for (int c = 0; c < 8; ++c) csh[wave][tx * 8 + c] = cs[c];
+    for (int c = 0; c < 8; ++c) csh[wave][ccol(c) - J * TB] = cs[c];
   }
   if (tx == 0) {
 #pragma unroll
@@ -298,28 +299,51 @@ __global__ void __launch_bounds__(RB) k_col_next(SytrdArgs a, int i, int j, int 
   const int r = (prep_only ? ip : i + 1) + blockIdx.x * RB + tid;
   const int rr = r < n ? r : n - 1;             // in-range row for the loads
   const bool next = ip < n - 1;
-  // Loads that do not need alpha2 go first: panel rows p < j of V and W at this row and at
-  // row ip, the row ip of A, and what rebuilds w_j
+  // Every load that does not need alpha2 is issued before any is used and without a branch
+  // (panel rows p < j of V and W at this row and at row ip, row ip of A, what rebuilds w_j
+  // and the block partials of w^T v): entries past the live range read an entry this
+  // launch does not write and are masked afterwards.
+  const int ipc = min(ip, n - 1);
+  // row g of W is not written by this launch (it writes row j only, and none in prep_only)
+  const int g = j == 0 ? 1 : 0;
   float vrow[32], wrow[32];
 #pragma unroll
   for (int p = 0; p < 32; ++p) {
-    const bool ld = next && p < jp && (prep_only || p < j);
-    vrow[p] = ld ? V[(int64_t)p * n + rr] : 0.f;
-    wrow[p] = ld ? W[(int64_t)p * n + rr] : 0.f;
+    const bool ld = p < jp && (prep_only || p < j);
+    vrow[p] = V[(int64_t)(ld ? p : 0) * n + rr];
+    wrow[p] = W[(int64_t)(ld ? p : g) * n + rr];
   }
-  const float a_ip = next ? M.A[(int64_t)ip * n + rr] : 0.f;
-  float cw_t = 0.f, cv_t = 0.f;
-  if (next && tid < jp) {
-    cv_t = V[(int64_t)tid * n + ip];
-    if (prep_only || tid < j) cw_t = W[(int64_t)tid * n + ip];
+  float a_ip = M.A[(int64_t)ipc * n + rr];
+  const bool ldc = tid < jp, ldw = ldc && (prep_only || tid < j);
+  float cv_t = V[(int64_t)(ldc ? tid : 0) * n + ipc];
+  float cw_t = W[(int64_t)(ldw ? tid : g) * n + ipc];
+  float wpre_r = 0.f, vj_r = 0.f, wpre_ip = 0.f, vj_ip = 0.f, tau_i = 0.f, tw[32];
+  const int nblk = (n - (i + 1) + RB - 1) / RB;   // row blocks of column i's k_col_finish
+  if (!prep_only) {
+    wpre_r = M.wpre[rr];
+    vj_r = V[(int64_t)j * n + rr];
+    wpre_ip = M.wpre[ipc];
+    vj_ip = V[(int64_t)j * n + ipc];
+    tau_i = M.tau[i];
+#pragma unroll
+    for (int b = 0; b < 32; ++b) tw[b] = M.wpart[min(b, nblk - 1)];
   }
+#pragma unroll
+  for (int p = 0; p < 32; ++p)
+    if (!(next && p < jp && (prep_only || p < j))) { vrow[p] = 0.f; wrow[p] = 0.f; }
+  if (!next) a_ip = 0.f;
+  if (!(next && ldc)) cv_t = 0.f;
+  if (!(next && ldw)) cw_t = 0.f;
   float alpha2 = 0.f, w = 0.f;
   if (!prep_only) {
-    const int o = i + 1;
-    const float wpre_r = M.wpre[rr], vj_r = V[(int64_t)j * n + rr];
     vrow[j] = vj_r;
-    const int nblk = (n - o + RB - 1) / RB;          // row blocks of column i's k_col_finish
-    if (tid == 0) alpha2_s = (float)(-0.5 * (double)M.tau[i] * strided_sum(M.wpart, 1, nblk));
+    if (tid == 0) {
+      double sw = 0.0;
+#pragma unroll
+      for (int b = 0; b < 32; ++b) sw += b < nblk ? (double)tw[b] : 0.0;
+      for (int b = 32; b < nblk; ++b) sw += (double)M.wpart[b];
+      alpha2_s = (float)(-0.5 * (double)tau_i * sw);
+    }
     __syncthreads();
     alpha2 = alpha2_s;
     w = wpre_r + alpha2 * vj_r;
@@ -330,7 +354,7 @@ __global__ void __launch_bounds__(RB) k_col_next(SytrdArgs a, int i, int j, int 
     }
     if (!next) return;
     // reflector j's w[ip] is rebuilt here because another workgroup of this launch writes it
-    if (tid == j) cw_t = M.wpre[ip] + alpha2 * V[(int64_t)j * n + ip];
+    if (tid == j) cw_t = wpre_ip + alpha2 * vj_ip;
   }
   if (tid < jp) { cw[tid] = cw_t; cv[tid] = cv_t; }
   __syncthreads();
@@ -356,10 +380,13 @@ __global__ void __launch_bounds__(RB) k_col_next(SytrdArgs a, int i, int j, int 
     if (p < jp) { prod[1 + p][tid] = wrow[p] * xtail; prod[1 + jp + p][tid] = vrow[p] * xtail; }
   __syncthreads();
   if (tid < nk) {
-    float sum = 0.f;
-#pragma unroll 16
-    for (int t = 0; t < RB; ++t) sum += prod[tid][t];
-    M.dpart[(int64_t)blockIdx.x * (2 * a.nb + 1) + tid] = sum;
+    // four interleaved partial sums, combined in a fixed order
+    float s4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+    for (int t = 0; t < RB; t += 4)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) s4[q] += prod[tid][t + q];
+    M.dpart[(int64_t)blockIdx.x * (2 * a.nb + 1) + tid] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
   }
 }
 
