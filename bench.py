@@ -77,6 +77,9 @@ def parse():
                     help="before the run, one streaming pass (out = -in, fp32) that reads and "
                          "writes this many MiB: the reference dispatch for scaling HBM "
                          "traffic counters")
+    ap.add_argument("--trd-lanes", type=int, default=0,
+                    help="streams of the exact path's tridiagonalisation (library default 2); "
+                         "1 keeps every launch on one stream, for counter collection")
     ap.add_argument("--no-stage-profile", action="store_true",
                     help="skip the event-instrumented step; the stage and roofline fields are "
                          "then omitted")
@@ -510,6 +513,8 @@ def main():
     codec = CacheCodec(K, V, group_layers=gl, method=method, ratio=ratio,
                        oversample=args.oversample, power_iters=args.power_iters, tau=args.tau,
                        max_cells_per_call=args.cells_per_call)
+    if args.trd_lanes:
+        J.jolt_debug_set(codec.ctx, J.JOLT_DBG_TRD_LANES, args.trd_lanes)
     eps2 = codec.calibrate()
     log("eps2", eps2, "cells", len(codec.cells), "per call", codec.chunk)
     Kout, Vout = torch.empty_like(K), torch.empty_like(V)

@@ -396,11 +396,15 @@ int jolt_attend_noalloc(jolt_ctx *ctx, int n_items, const void *const *k_blobs, 
 int jolt_debug_export(jolt_ctx *ctx, int what, int cell, void *dst, size_t dst_bytes,
                       jolt_stream stream);
 
-/* Test hook: forces a solver condition from the host so that the JOLT_E_NOCONV path can be
- * exercised with inputs on which the solvers succeed.  JOLT_DBG_INVIT_ITERS sets the number
- * of inverse-iteration sweeps of later calls on this context (default 2, range 0..8; with
- * 0 no sweep runs and the growth check fails).  Errors: JOLT_E_INVAL. */
-enum { JOLT_DBG_INVIT_ITERS = 0 };
+/* Test and tuning hooks on a context.  JOLT_DBG_INVIT_ITERS forces a solver condition from
+ * the host so that the JOLT_E_NOCONV path can be exercised with inputs on which the solvers
+ * succeed: it sets the number of inverse-iteration sweeps of later calls on this context
+ * (default 2, range 0..8; with 0 no sweep runs and the growth check fails).
+ * JOLT_DBG_TRD_LANES sets how many streams the blocked tridiagonalisation of the exact token
+ * spectrum spreads its groups of matrices over (default 2, range 1..2; results do not
+ * depend on it): 1 keeps every launch on one stream, for counter collection.
+ * Errors: JOLT_E_INVAL. */
+enum { JOLT_DBG_INVIT_ITERS = 0, JOLT_DBG_TRD_LANES = 1 };
 int jolt_debug_set(jolt_ctx *ctx, int what, int64_t value);
 
 /* Benchmark instrumentation.  When enabled, the library brackets the kernels of each

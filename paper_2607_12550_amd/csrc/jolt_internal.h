@@ -78,7 +78,8 @@ struct jolt_ctx {
   hipStream_t cap_stream[kTrdLanes] = {};
   hipGraphExec_t trd_exec[kTrdLanes] = {};
   hipEvent_t trd_fork = nullptr, trd_join[kTrdLanes] = {};
-  int trd_lanes = 0;
+  int trd_lanes = 0;               // lanes of the captured graphs
+  int trd_lanes_max = kTrdLanes;   // JOLT_DBG_TRD_LANES
   std::vector<const void *> trd_key;
   int invit_iters = 2;            // inverse-iteration sweeps (test hook jolt_debug_set)
   void *attend_scratch = nullptr; // this device's fixed attention scratch (device address)

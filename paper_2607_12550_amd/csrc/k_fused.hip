@@ -26,6 +26,8 @@
 // WM x WN grid (2 x 2 for d >= 64), K = r_T in steps of 32 (zero-padded).  The 1-D grid
 // is remapped so that each XCD takes a contiguous run of tiles, ordered cell, slice, token
 // block: the token blocks of a slice share W_s, the slices of a cell share U^_T.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 #include "rowops.h"
@@ -469,6 +471,488 @@ __global__ void __launch_bounds__(256) k_w_prepare(const FusedCell *cells, int m
   }
 }
 
+// ------------------------------------------------------------------------- core path
+// Factors stored in fp16 (the default) take the reconstruction in the other order,
+// X~_s = 2^e_s (U^_T G^_s) U^_d^T, which costs 2 r_T r_d + 4 r_d d flops per token and slice
+// instead of the 4 r_T d of U^_T W_s:
+//   stage 1  Y_s^T = G^_s^T U^_T^T (r_d x tokens): fp16 operands as stored, products exact in
+//            fp32, fp32 accumulation;
+//   stage 2  X~_s^T 2^-(e_s + ky_s) = U^_d (Y_s^T 2^-ky_s): Y scaled by the power of two
+//            2^-ky_s that bounds it by 2^15 (|Y| <= |U^_T row| |G^_s column| <=
+//            1.01 sqrt(r_T) max|G^_s|) and split into fp16 hi + lo, two MFMA passes;
+//            U^_d is an exact fp16 operand.
+// k_core_prepare writes, per slice, G^_s^T zero-padded to RD = round32(r_d) rows of
+// K16 = round16(r_T) entries (in the slice's W area) and ky_s (in the exponent array), and
+// per cell U^_d with its columns permuted into the order of stage 2's k slots (below).
+//
+// Each wave owns 32 tokens of one slice (a workgroup 128 tokens, tiles ordered as in
+// k_fused).  Stage 1's accumulator block b holds Y^T rows 32 b + 8 (q / 4) + 4 h + q % 4 for
+// the lane's token (lane % 32) in its entry q, h = lane / 32; stage 2 takes entries
+// q = 8 c .. 8 c + 7 of block b as the B operand of k chunk kc = 2 b + c, so U^_d's columns are
+// permuted to match (slot s of lane half h is column 16 kc + 4 h + s % 4 + 8 (s / 4)).  Stage
+// 2's accumulator leaves token t's row split over the lane pair (t, t + 32): lane half h
+// holds features f = 8 u + 4 h + i for units u < d/8 and i < 4, value index 4 u + i.  The
+// epilogue works in that layout: the Walsh-Hadamard transform runs log2(d) - 1 butterfly
+// stages inside the lane and the stage of feature bit 2 across the pair (v_permlane32_swap);
+// a quantiser group of g features is g/8 units of one lane plus the same units of the other.
+constexpr int CORE_UDP_PAD = 8;                                 // halves per LDS row of U^_d
+
+// Across the lane pair (l, l + 32): v_permlane32_swap of two copies of v leaves the lower
+// lane's value in the first result and the upper lane's in the second, in both lanes.
+// Butterfly: the lower lane gets v_lo + v_hi, the upper v_lo - v_hi (sgn = +1 / -1).
+JOLT_DEV float pair_butterfly(float v, float sgn) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaf(sgn, __uint_as_float(r[1]), __uint_as_float(r[0]));
+}
+JOLT_DEV float pair_max(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__global__ void __launch_bounds__(256) k_core_prepare(const FusedCell *cells, const float *signs, int m, int d) {
+  const int s = blockIdx.x, cell = blockIdx.y;
+  const FusedCell &c = cells[cell];
+  if (s >= m || c.rT <= 0) return;
+  const int rT = c.rT, rd = c.rd, RD = (rd + 31) & ~31, K16 = (rT + 15) & ~15;
+  const uint16_t *G = c.G + (int64_t)s * rT * rd;
+  uint16_t *Gt = reinterpret_cast<uint16_t *>(c.Wt + (int64_t)s * d * c.ldw);
+  __shared__ uint16_t tile[64][130];
+  float mx = 0.f;
+  for (int i0 = 0; i0 < K16; i0 += 64) {
+    for (int q = threadIdx.x; q < 64 * RD; q += 256) {
+      const int r = q / RD, j = q - r * RD, i = i0 + r;
+      uint16_t v = 0;
+      if (i < rT && j < rd) {
+        v = G[(int64_t)i * rd + j];
+        mx = fmaxf(mx, fabsf(h_val(v)));
+      }
+      tile[r][j] = v;
+    }
+    __syncthreads();
+    for (int q = threadIdx.x; q < 64 * RD; q += 256) {
+      const int j = q / 64, r = q - j * 64;
+      if (i0 + r < K16) Gt[(int64_t)j * K16 + i0 + r] = tile[r][j];
+    }
+    __syncthreads();
+  }
+  for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  __shared__ float red[4];
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    int e = 0;
+    if (mx > 0.f) {
+      const double bound = 1.01 * sqrt((double)rT) * (double)mx;
+      int ex;
+      const double f = frexp(bound, &ex);         // bound = f 2^ex, 0.5 <= f < 1
+      e = (f == 0.5 ? ex - 1 : ex) - 15;          // ceil(log2 bound) - 15
+    }
+    c.wexp[s] = e;
+  }
+  if (s == 0) {
+    // s_f U^_d[f, :] (d x r_d, fp16, rotation sign s_f folded in: an exact sign flip) with
+    // columns in stage 2's slot order, zeros past r_d
+    for (int q = threadIdx.x; q < d * RD; q += 256) {
+      const int f = q / RD, p = q - f * RD;
+      const int kc = p >> 4, hh = (p >> 3) & 1, sl = p & 7;
+      const int jsrc = 16 * kc + 4 * hh + (sl & 3) + 8 * (sl >> 2);
+      const uint16_t flip = signs[(int64_t)cell * d + f] < 0.f ? 0x8000u : 0u;
+      c.udp[q] = jsrc < rd ? (uint16_t)(c.Ud[(int64_t)f * rd + jsrc] ^ flip) : (uint16_t)0;
+    }
+  }
+}
+
+JOLT_DEV f16x8_t as_f16x8(ju4 u) {
+  f16x8_t r;
+  __builtin_memcpy(&r, &u, 16);
+  return r;
+}
+
+// LDS of k_core: U^_d (permuted, rows padded), then one area shared in turn by the staged
+// cache rows of the tile (residual input), the staged codes and scales (decode input), the
+// K chunks of stage 1 (U^_T rows of the tile and G^_s^T rows, 32 k each, rows padded), and
+// the staged output (codes, or decoded rows).  All global traffic of the tile is in
+// 16-byte (cache rows, operands) or 4-byte (codes) pieces along contiguous memory.
+template <int D, typename TIO>
+struct CoreLds {
+  static constexpr int LDU = D + CORE_UDP_PAD;                  // halves per U^_d row
+  static constexpr int UD_BYTES = D * LDU * 2;
+  static constexpr int LDK = 40;                                // halves per K-chunk row
+  static constexpr int OPER = 2 * BT * LDK * 2;                 // U^_T chunk + G^T chunk
+  static constexpr int IO_ROW = D * (int)sizeof(TIO) + 16;      // bytes per staged cache row
+  static constexpr int IO = BT * IO_ROW;
+  static constexpr int CODE_ROW = D + 4;                        // bytes per staged code row (max)
+  static constexpr int CODES = BT * CODE_ROW + BT * (D / 8) * 2;
+  static constexpr int SHARED = OPER > IO ? (OPER > CODES ? OPER : CODES) : (IO > CODES ? IO : CODES);
+  static constexpr int BYTES = UD_BYTES + SHARED;
+};
+
+template <int D, int MODE, typename TIO, bool ROPE>
+__global__ void __launch_bounds__(NT, sizeof(TIO) == 2 ? 2 : 1) k_core(FusedArgs a) {
+  constexpr int FB = D / 32, NU = D / 8, NV = D / 2;     // feature blocks, units, values per lane
+  using L = CoreLds<D, TIO>;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[L::BYTES];
+  uint16_t *sud = reinterpret_cast<uint16_t *>(smem);
+  uint8_t *sh = smem + L::UD_BYTES;
+  uint16_t *sU = reinterpret_cast<uint16_t *>(sh), *sG = sU + BT * L::LDK;
+
+  const int bi = blockIdx.x, jt = (bi & 7) * a.per_xcd + (bi >> 3);
+  if (jt >= a.total) return;
+  const int per_cell = a.m * a.tiles_t;
+  const int cell = jt / per_cell, rem = jt - cell * per_cell;
+  const int s = rem / a.tiles_t, t0 = (rem - s * a.tiles_t) * BT;
+  const FusedCell c = a.cells[cell];
+  if (MODE == FUSED_RESIDUAL && c.bits == 0) return;
+  const int T = a.T, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, tl = lane & 31, h = lane >> 5;
+  const int trow = wave * 32 + tl;                         // tile row of this lane's token
+  const int t = t0 + trow;
+  const bool tin = t < T;
+  const int tc = tin ? t : T - 1;
+  const int nrows = T - t0 < BT ? T - t0 : BT;             // valid rows of the tile
+  const int64_t srow = (int64_t)(s / a.heads) * a.s_layer + (int64_t)(s % a.heads) * a.s_head;
+  const int64_t ebase = ((int64_t)s * T + tc) * D;         // element of (s, t, feature 0)
+  const int bits = c.bits, g = a.group, gw = g / 8;
+  const int rT = c.rT;
+  const int ky = rT > 0 ? c.wexp[s] : 0;
+  const int xe = rT > 0 ? ky + (int)c.gexp[s] : 0;         // X~ = 2^xe (stage-2 accumulator)
+  const int RD = rT > 0 ? (c.rd + 31) & ~31 : 0;
+
+  // U^_d in the permuted slot order to its LDS area (read after the next barrier)
+  for (int q = tid; q < D * RD / 8; q += NT) {
+    const int f = q / (RD / 8), p8 = q - f * (RD / 8);
+    *reinterpret_cast<ju4 *>(sud + f * L::LDU + 8 * p8) = gload_u4(c.udp + (int64_t)f * RD + 8 * p8);
+  }
+  // stage-1 operands: U^_T rows of the tile and G^_s^T rows, K chunks of 32; each thread moves
+  // two 16-byte pieces of each operand per chunk (128 rows x 4 pieces).  The first two
+  // chunks are requested here, ahead of the epilogue operands.
+  const int K16 = (rT + 15) & ~15, NB1 = RD / 32;
+  const uint16_t *Gt = reinterpret_cast<const uint16_t *>(c.Wt + (int64_t)s * D * c.ldw);
+  const uint16_t *UT = reinterpret_cast<const uint16_t *>(c.UT);
+  const bool whole = (rT & 7) == 0;                         // U^_T rows 16-byte aligned
+  ju4 pu[2][2], pg[2][2];
+  auto fetch = [&](int sl, int k0) {
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int q = tid + NT * e, r = q >> 2, k = k0 + 8 * (q & 3);
+      const int tr = t0 + r < T ? t0 + r : T - 1;
+      if (whole) pu[sl][e] = k < rT ? gload_u4(UT + (int64_t)tr * rT + k) : ju4{0u, 0u, 0u, 0u};
+      else pu[sl][e] = load_run_h(UT, rT, tr, T, k, rT);
+      pg[sl][e] = r < RD && k < K16 ? gload_u4(Gt + (int64_t)r * K16 + k) : ju4{0u, 0u, 0u, 0u};
+    }
+  };
+  if (rT > 0) {
+    fetch(0, 0);
+    if (32 < K16) fetch(1, 32);
+  }
+  const float *sgn = a.signs + (int64_t)cell * D;          // rotation signs s_f (+-1)
+  const int rows_bytes = D * bits / 8, code_row = rows_bytes + 4;       // codes per row, staged
+  const int lg = 31 - __builtin_clz(g), lgw = lg - 3;       // g and g / 8 are powers of two
+
+  // U^_d carries the rotation signs (k_core_prepare), so stage 2 adds s * X~ 2^-xe to the
+  // accumulator, which starts from (exact scalings):
+  //   residual: -s * X 2^-xe, so that it ends as -(s * r) 2^-xe, r = X - X~;
+  //   decode:   H r^ / sqrt(d) 2^-xe, so that it ends as s * X^ 2^-xe;
+  //   export:   zero, ending as s * X~ 2^-xe.
+  // acc2[fb][q] is value 16 fb + q: unit 4 fb + q / 4, entry q % 4.
+  f32x16_t acc2[FB];
+#pragma unroll
+  for (int fb = 0; fb < FB; ++fb)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) acc2[fb][q] = 0.f;
+  if constexpr (MODE == FUSED_RESIDUAL) {
+    // the tile's cache rows to LDS as -s * X: each thread moves the same 16-byte piece p of
+    // several rows and flips the sign bits of its entries by a mask (-s_f < 0 sets the bit)
+    constexpr int PR = D * (int)sizeof(TIO) / 16;           // 16-byte pieces per cache row
+    static_assert(NT % PR == 0, "piece index fixed per thread");
+    const int pp = tid % PR;
+    ju4 flip;
+    {
+      uint32_t m4[4];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        if constexpr (sizeof(TIO) == 2) {
+          const int f = 8 * pp + 2 * w;
+          m4[w] = (sgn[f] > 0.f ? 0x8000u : 0u) | (sgn[f + 1] > 0.f ? 0x80000000u : 0u);
+        } else {
+          m4[w] = sgn[4 * pp + w] > 0.f ? 0x80000000u : 0u;
+        }
+      }
+      flip = ju4{m4[0], m4[1], m4[2], m4[3]};
+    }
+    const uint8_t *xb = reinterpret_cast<const uint8_t *>(c.x);
+    for (int r = tid / PR; r < BT; r += NT / PR) {
+      const int tr = t0 + r < T ? t0 + r : T - 1;
+      *reinterpret_cast<ju4 *>(sh + r * L::IO_ROW + 16 * pp) =
+          gload_u4(xb + (srow + (int64_t)tr * a.s_tok) * (int64_t)sizeof(TIO) + 16 * pp) ^ flip;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      float x[4];
+      const uint8_t *src = sh + trow * L::IO_ROW + (8 * u + 4 * h) * (int)sizeof(TIO);
+      if constexpr (sizeof(TIO) == 2) {
+        const uint2 w = *reinterpret_cast<const uint2 *>(src);
+        x[0] = bf16_to_f32((bf16_t)(w.x & 0xffffu)); x[1] = bf16_to_f32((bf16_t)(w.x >> 16));
+        x[2] = bf16_to_f32((bf16_t)(w.y & 0xffffu)); x[3] = bf16_to_f32((bf16_t)(w.y >> 16));
+      } else {
+        const float4 w = *reinterpret_cast<const float4 *>(src);
+        x[0] = w.x; x[1] = w.y; x[2] = w.z; x[3] = w.w;
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc2[u >> 2][4 * (u & 3) + i] = ldexpf(x[i], -xe);
+    }
+    __syncthreads();                                        // the staging area is reused
+  } else if constexpr (MODE == FUSED_DECODE) {
+    if (bits) {
+      const int lng = 31 - __builtin_clz(D / g), ng = 1 << lng;              // scales per row
+      uint16_t *sS = reinterpret_cast<uint16_t *>(sh + BT * L::CODE_ROW);
+      const int lW = 31 - __builtin_clz(rows_bytes / 4), W = 1 << lW;        // code words per row
+      const uint8_t *cb = c.codes + ((int64_t)s * T + t0) * rows_bytes;
+      for (int q = tid; q < BT * W; q += NT) {
+        const int r = q >> lW, wi = q & (W - 1), rr = r < nrows ? r : nrows - 1;
+        *reinterpret_cast<uint32_t *>(sh + r * code_row + 4 * wi) =
+            *gptr(reinterpret_cast<const uint32_t *>(cb + (int64_t)rr * rows_bytes + 4 * wi));
+      }
+      const uint16_t *sb = c.scales + ((int64_t)s * T + t0) * ng;
+      for (int q = tid; q < BT * ng; q += NT) {
+        const int r = q >> lng, k = q & (ng - 1), rr = r < nrows ? r : nrows - 1;
+        sS[q] = *gptr(sb + (int64_t)rr * ng + k);
+      }
+      __syncthreads();
+      const int levels = (1 << bits) - 1;
+      const float mid = 0.5f * (float)levels;
+      float v[NV];
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        const uint8_t *src = sh + trow * code_row + (8 * u + 4 * h) * bits / 8;
+        uint32_t cw;
+        if (bits == 8) cw = *reinterpret_cast<const uint32_t *>(src);
+        else if (bits == 4) cw = *reinterpret_cast<const uint16_t *>(src);
+        else cw = *src;
+        const float dl = h_val(sS[(trow << lng) + ((8 * u) >> lg)]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[4 * u + i] = ((float)((cw >> (bits * i)) & (uint32_t)levels) - mid) * dl;
+      }
+      __syncthreads();                                      // the staging area is reused
+      // Walsh-Hadamard transform: value bits in the lane, feature bit 2 across the pair
+#pragma unroll
+      for (int w = 1; w < NV; w <<= 1)
+#pragma unroll
+        for (int k = 0; k < NV; ++k)
+          if ((k & w) == 0) {
+            const float p = v[k], q = v[k + w];
+            v[k] = p + q;
+            v[k + w] = p - q;
+          }
+#pragma unroll
+      for (int k = 0; k < NV; ++k) acc2[k >> 4][k & 15] = ldexpf(pair_butterfly(v[k], h ? -1.f : 1.f) * a.inv_sqrt_d, -xe);
+    }
+  }
+
+  if (rT > 0) {
+    f32x16_t acc1[FB];
+#pragma unroll
+    for (int b = 0; b < FB; ++b)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc1[b][q] = 0.f;
+    // stage 1 over K chunks of 32 staged in LDS, two chunks ahead in registers (slot 0 holds
+    // the even chunks, slot 1 the odd ones)
+    for (int k0 = 0; k0 < K16; k0 += 64) {
+#pragma unroll
+      for (int sl = 0; sl < 2; ++sl) {
+        const int kc0 = k0 + 32 * sl;
+        if (kc0 >= K16) break;
+        __syncthreads();                                    // the previous chunk has been read
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int q = tid + NT * e, r = q >> 2, p = q & 3;
+          *reinterpret_cast<ju4 *>(sU + r * L::LDK + 8 * p) = pu[sl][e];
+          *reinterpret_cast<ju4 *>(sG + r * L::LDK + 8 * p) = pg[sl][e];
+        }
+        __syncthreads();
+        if (kc0 + 64 < K16) fetch(sl, kc0 + 64);            // in flight during two chunks
+#pragma unroll
+        for (int kk = 0; kk < 32; kk += 16) {
+          if (kc0 + kk >= K16) break;
+          const f16x8_t ub = *reinterpret_cast<const f16x8_t *>(sU + trow * L::LDK + kk + 8 * h);
+#pragma unroll
+          for (int b = 0; b < FB; ++b)
+            if (b < NB1) {
+              const f16x8_t ga = *reinterpret_cast<const f16x8_t *>(sG + (32 * b + tl) * L::LDK + kk + 8 * h);
+              acc1[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ga, ub, acc1[b], 0, 0, 0);
+            }
+        }
+      }
+    }
+    // stage 2: acc2 += U^_d (Y^T 2^-ky), Y split into fp16 hi + lo; chunk kc = 2 b + cc takes
+    // entries 8 cc .. 8 cc + 7 of block b
+#pragma unroll
+    for (int kc = 0; kc < 2 * FB; ++kc) {
+      if (kc < RD / 16) {
+        const int b = kc >> 1, cc = kc & 1;
+        f16x8_t yh, yl;
+#pragma unroll
+        for (int sl = 0; sl < 8; ++sl) {
+          const float yv = ldexpf(acc1[b][8 * cc + sl], -ky);
+          const _Float16 hi = (_Float16)yv;
+          yh[sl] = hi;
+          yl[sl] = (_Float16)(yv - (float)hi);
+        }
+#pragma unroll
+        for (int fb = 0; fb < FB; ++fb) {
+          const f16x8_t ua = *reinterpret_cast<const f16x8_t *>(sud + (32 * fb + tl) * L::LDU + 16 * kc + 8 * h);
+          acc2[fb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ua, yh, acc2[fb], 0, 0, 0);
+          acc2[fb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ua, yl, acc2[fb], 0, 0, 0);
+        }
+      }
+    }
+  }
+  float v[NV];
+#pragma unroll
+  for (int fb = 0; fb < FB; ++fb)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) v[16 * fb + q] = ldexpf(acc2[fb][q], xe);     // exact
+
+  if constexpr (MODE == FUSED_XTILDE) {
+    if (tin) {
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        const jf4 sq = gload_f4(sgn + 8 * u + 4 * h);
+        *reinterpret_cast<jf4 *>(c.xt_out + ebase + 8 * u + 4 * h) =
+            jf4{v[4 * u] * sq.x, v[4 * u + 1] * sq.y, v[4 * u + 2] * sq.z, v[4 * u + 3] * sq.w};
+      }
+    }
+  } else if constexpr (MODE == FUSED_RESIDUAL) {
+    // v = -(s * r): r' = H (s * r) / sqrt(d) = -H v / sqrt(d)
+#pragma unroll
+    for (int w = 1; w < NV; w <<= 1)
+#pragma unroll
+      for (int k = 0; k < NV; ++k)
+        if ((k & w) == 0) {
+          const float p = v[k], q = v[k + w];
+          v[k] = p + q;
+          v[k + w] = p - q;
+        }
+#pragma unroll
+    for (int k = 0; k < NV; ++k) v[k] = pair_butterfly(v[k], h ? -1.f : 1.f) * -a.inv_sqrt_d;
+    // group max: units u / gw of the lane, then the pair
+    float am[NU];
+#pragma unroll
+    for (int u = 0; u < NU; ++u)
+      am[u] = fmaxf(fmaxf(fabsf(v[4 * u]), fabsf(v[4 * u + 1])), fmaxf(fabsf(v[4 * u + 2]), fabsf(v[4 * u + 3])));
+#pragma unroll
+    for (int w = 1; w < NU; w <<= 1)
+      if (w < gw) {
+#pragma unroll
+        for (int u = 0; u < NU; ++u)
+          if ((u & w) == 0) {
+            const float mm = fmaxf(am[u], am[u + w]);
+            am[u] = mm;
+            am[u + w] = mm;
+          }
+      }
+    const int levels = (1 << bits) - 1;
+    const float mid = 0.5f * (float)levels;
+    __syncthreads();                                        // stage 1's chunks have been read
+    float delta = 0.f, inv = 0.f;
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      if ((u & (gw - 1)) == 0) {                            // first unit of a group
+        const float aa = pair_max(am[u]);
+        float dl = 2.f * aa / (float)levels;
+        dl = fminf(dl, 65504.f);
+        delta = f16_round(dl);
+        // r / delta as r * (1 / delta): within 1.5 ulp of the quotient
+        inv = delta == 0.f ? 0.f : 1.f / delta;
+      }
+      uint32_t word = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float cq;
+        if (delta == 0.f) {
+          cq = (float)(1 << (bits - 1));
+        } else {
+          cq = __builtin_amdgcn_fmed3f(__builtin_rintf(fmaf(v[4 * u + i], inv, mid)), 0.f, (float)levels);
+        }
+        word |= (uint32_t)cq << (bits * i);
+      }
+      uint8_t *dst = sh + trow * code_row + (8 * u + 4 * h) * bits / 8;
+      if (bits == 8) *reinterpret_cast<uint32_t *>(dst) = word;
+      else if (bits == 4) *reinterpret_cast<uint16_t *>(dst) = (uint16_t)word;
+      else *dst = (uint8_t)word;
+      if (tin && h == 0 && (u & (gw - 1)) == 0) c.scales[(ebase + 8 * u) >> lg] = h_bits(delta);
+    }
+    __syncthreads();
+    // the tile's codes are one contiguous run of nrows rows
+    const int lW = 31 - __builtin_clz(rows_bytes / 4), W = 1 << lW;
+    uint8_t *cb = c.codes + ((int64_t)s * T + t0) * rows_bytes;
+    for (int q = tid; q < nrows * W; q += NT) {
+      const int r = q >> lW, wi = q & (W - 1);
+      *gptr(reinterpret_cast<uint32_t *>(cb + (int64_t)r * rows_bytes + 4 * wi)) =
+          *reinterpret_cast<const uint32_t *>(sh + r * code_row + 4 * wi);
+    }
+  } else {
+    if constexpr (ROPE) {
+      // X^ = s * v first
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        const jf4 sq = gload_f4(sgn + 8 * u + 4 * h);
+        v[4 * u] *= sq.x; v[4 * u + 1] *= sq.y; v[4 * u + 2] *= sq.z; v[4 * u + 3] *= sq.w;
+      }
+      // features f and f + D/2 (value indices k and k + NV/2) rotate together by pos theta_j
+      const double pos = (double)(t + a.rope_offset);
+#pragma unroll
+      for (int k = 0; k < NV / 2; ++k) {
+        const int f = 8 * (k / 4) + 4 * h + (k % 4);            // < D/2
+        const double theta = exp2(-(2.0 * f / D) * a.rope_log2_base);
+        double sn, cs;
+        sincos(pos * theta, &sn, &cs);
+        const float cf = (float)cs, sf = (float)sn;
+        const float lo = v[k], hi = v[k + NV / 2];
+        v[k] = fmaf(-hi, sf, lo * cf);
+        v[k + NV / 2] = fmaf(lo, sf, hi * cf);
+      }
+    }
+    __syncthreads();                                        // stage 1's chunks have been read
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      uint8_t *dst = sh + trow * L::IO_ROW + (8 * u + 4 * h) * (int)sizeof(TIO);
+      if constexpr (sizeof(TIO) == 2) {
+        const uint32_t w0 = (uint32_t)f32_to_bf16(v[4 * u]) | ((uint32_t)f32_to_bf16(v[4 * u + 1]) << 16);
+        const uint32_t w1 = (uint32_t)f32_to_bf16(v[4 * u + 2]) | ((uint32_t)f32_to_bf16(v[4 * u + 3]) << 16);
+        *reinterpret_cast<uint2 *>(dst) = make_uint2(w0, w1);
+      } else {
+        *reinterpret_cast<float4 *>(dst) = make_float4(v[4 * u], v[4 * u + 1], v[4 * u + 2], v[4 * u + 3]);
+      }
+    }
+    __syncthreads();
+    // the tile's rows, 8 bytes at a time along each row; each thread moves the same piece p
+    // of several rows and applies the rotation signs of its entries (X^ = s * v) by a mask,
+    // unless RoPE has applied them already
+    constexpr int P8 = D * (int)sizeof(TIO) / 8;
+    static_assert(NT % P8 == 0, "piece index fixed per thread");
+    const int pp = tid % P8;
+    ju2 flip{0u, 0u};
+    if constexpr (!ROPE) {
+#pragma unroll
+      for (int w = 0; w < 2; ++w) {
+        if constexpr (sizeof(TIO) == 2) {
+          const int f = 4 * pp + 2 * w;
+          flip[w] = (sgn[f] < 0.f ? 0x8000u : 0u) | (sgn[f + 1] < 0.f ? 0x80000000u : 0u);
+        } else {
+          flip[w] = sgn[2 * pp + w] < 0.f ? 0x80000000u : 0u;
+        }
+      }
+    }
+    uint8_t *ob = reinterpret_cast<uint8_t *>(c.out);
+    for (int r = tid / P8; r < nrows; r += NT / P8) {
+      *gptr(reinterpret_cast<ju2 *>(ob + (srow + (int64_t)(t0 + r) * a.s_tok) * (int64_t)sizeof(TIO) + 8 * pp)) =
+          *reinterpret_cast<const ju2 *>(sh + r * L::IO_ROW + 8 * pp) ^ flip;
+    }
+  }
+}
+
 template <int D, int MODE, typename TIO, bool USPLIT>
 hipError_t launch_mode(const FusedArgs &a, bool rope, hipStream_t st) {
   const dim3 grid((unsigned)(a.per_xcd * 8)), block(NT);
@@ -489,8 +973,32 @@ hipError_t launch_d(const FusedArgs &a, int io_dtype, bool split, bool rope, hip
   return split ? launch_mode<D, MODE, bf16_t, true>(a, rope, st) : launch_mode<D, MODE, bf16_t, false>(a, rope, st);
 }
 
+template <int D, int MODE>
+hipError_t launch_core(const FusedArgs &a, int io_dtype, bool rope, hipStream_t st) {
+  const dim3 grid((unsigned)(a.per_xcd * 8)), block(NT);
+  const bool f32 = MODE == FUSED_XTILDE || io_dtype == JOLT_F32;
+  if constexpr (MODE == FUSED_DECODE) {
+    if (rope) {
+      if (f32) hipLaunchKernelGGL((k_core<D, MODE, float, true>), grid, block, 0, st, a);
+      else hipLaunchKernelGGL((k_core<D, MODE, bf16_t, true>), grid, block, 0, st, a);
+      return hipGetLastError();
+    }
+  }
+  if (f32) hipLaunchKernelGGL((k_core<D, MODE, float, false>), grid, block, 0, st, a);
+  else hipLaunchKernelGGL((k_core<D, MODE, bf16_t, false>), grid, block, 0, st, a);
+  return hipGetLastError();
+}
+
 template <int MODE>
 hipError_t launch_m(const FusedArgs &a, int d, int io_dtype, bool split, bool rope, hipStream_t st) {
+  if (!split) {
+    switch (d) {
+      case 32: return launch_core<32, MODE>(a, io_dtype, rope, st);
+      case 64: return launch_core<64, MODE>(a, io_dtype, rope, st);
+      case 128: return launch_core<128, MODE>(a, io_dtype, rope, st);
+      default: return hipErrorInvalidValue;
+    }
+  }
   switch (d) {
     case 32: return launch_d<32, MODE>(a, io_dtype, split, rope, st);
     case 64: return launch_d<64, MODE>(a, io_dtype, split, rope, st);
@@ -506,6 +1014,13 @@ int fused_tile_tokens() { return BT; }
 hipError_t launch_w_prepare(const FusedCell *cells_dev, int n_cells, int m, int d, hipStream_t st) {
   if (n_cells <= 0 || m <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_w_prepare, dim3(m, n_cells), dim3(256), 0, st, cells_dev, m, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_core_prepare(const FusedCell *cells_dev, const float *signs_dev, int n_cells, int m, int d,
+                               hipStream_t st) {
+  if (n_cells <= 0 || m <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_core_prepare, dim3(m, n_cells), dim3(256), 0, st, cells_dev, signs_dev, m, d);
   return hipGetLastError();
 }
 

@@ -18,19 +18,26 @@ struct Eps2Args {
 
 
 // ----------------------------------------------------------------- fused reconstruction
-// X~_s = U^_T W_s rebuilt on the fp16 matrix cores inside the residual / decode passes.
+// X~_s rebuilt on the fp16 matrix cores inside the residual / decode passes: for fp16
+// factors as 2^e_s (U^_T G^_s) U^_d^T (launch_core_prepare), for fp32 factors as U^_T W_s.
 struct FusedCell {
   const void *UT;           // blob U_T section: T x rT, fp16 or fp32 (the call's factor type)
-  float *Wt;                // m slices of d x ldw: W_s^T = 2^e_s U^_d G^_s^T in fp32, which
-                            // launch_w_prepare rewrites in place, entry by entry, as the fp16
-                            // pair (hi, lo) of W_s^T 2^-k_s (hi in the low half-word)
-  int32_t *wexp;            // m per-slice exponents k_s (written by launch_w_prepare)
+  float *Wt;                // m slices of d x ldw floats.  fp32 factors: W_s^T = 2^e_s U^_d G^_s^T,
+                            // which launch_w_prepare rewrites in place, entry by entry, as the
+                            // fp16 pair (hi, lo) of W_s^T 2^-k_s (hi in the low half-word).
+                            // fp16 factors: G^_s^T as fp16, round32(r_d) rows of round16(r_T)
+                            // (launch_core_prepare)
+  int32_t *wexp;            // m per-slice exponents: k_s of W_s, or ky_s of Y_s = U^_T G^_s
+  const uint16_t *G;        // blob core section (m x rT x rd fp16) and its per-slice exponents
+  const int8_t *gexp;
+  const uint16_t *Ud;       // blob U_d section (d x rd fp16)
+  uint16_t *udp;            // d x round32(rd): U^_d with columns in the fused kernel's slot order
   const void *x;            // residual: cache cell base (strided, input type)
   void *out;                // decode: output cell base (strided, output type)
   uint8_t *codes;           // packed codes (written by the residual pass, read by decode)
   uint16_t *scales;         // fp16 group scales
   float *xt_out;            // export: X~ (m x T x d fp32, contiguous)
-  int32_t rT, bits, ldw, pad;
+  int32_t rT, bits, ldw, rd;
 };
 enum { FUSED_RESIDUAL = 0, FUSED_DECODE = 1, FUSED_XTILDE = 2 };
 struct FusedArgs {
@@ -47,6 +54,11 @@ int fused_tile_tokens();
 // Per (cell, slice): k_s = the smallest power of two with max |W_s| 2^-k_s <= 2^14, then
 // every entry of W_s^T rewritten in place as its fp16 hi + lo split (zeros past r_T).
 hipError_t launch_w_prepare(const FusedCell *cells_dev, int n_cells, int m, int d, hipStream_t st);
+// fp16 factors: per (cell, slice) G^_s^T zero-padded into the slice's W area and the exponent
+// ky_s with |U^_T G^_s| 2^-ky_s <= 2^15; per cell the permuted copy udp of U^_d with the
+// rotation signs (device [n_cells][d]) folded into its rows.
+hipError_t launch_core_prepare(const FusedCell *cells_dev, const float *signs_dev, int n_cells, int m, int d,
+                               hipStream_t st);
 // io_dtype: the cache type (residual) or the output type (decode); split_factors: the
 // factors are fp32 (U_T split into two fp16 terms)
 hipError_t launch_fused(FusedArgs a, int mode, int d, int io_dtype, bool split_factors, hipStream_t st);

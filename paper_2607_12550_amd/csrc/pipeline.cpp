@@ -48,7 +48,8 @@ struct Ws {
   GemmProblem *tab = nullptr;
   size_t tab_n = 0;
   FusedCell *fcell_r = nullptr;   // per-cell records of the fused reconstruction passes
-  int32_t *wexp = nullptr;         // [cell][slice] exponents of W_s
+  int32_t *wexp = nullptr;         // [cell][slice] exponents of W_s (or of U^_T G^_s)
+  uint16_t *udp = nullptr;         // [cell] d x d: U^_d in the fused kernel's slot order
   FGramCell *fcell = nullptr;
   SerCell *scell = nullptr;
   SerFactorCell *sfcell = nullptr;
@@ -160,6 +161,7 @@ void plan(Carver &cv, Ws &w, const SpecShape &sh, int nc) {
   w.G = cv.take<float>((size_t)nc * m * std::max(w.kmaxT, 1) * d);
   w.ldw = (std::max(w.kmaxT, 1) + 7) / 8 * 8;
   w.W = cv.take<float>((size_t)nc * m * d * w.ldw);
+  w.udp = cv.take<uint16_t>((size_t)nc * d * d);
 }
 
 // decode-only areas: problem table, per-cell records, rotation signs, W_s^T = 2^e U_d G_s^T
@@ -175,6 +177,7 @@ void plan_decode(Carver &cv, Ws &w, int m, int T, int d, int nc, int kmax) {
   w.kmaxT = std::max(kmax, 1);
   w.ldw = (w.kmaxT + 7) / 8 * 8;
   w.W = cv.take<float>((size_t)nc * m * d * w.ldw);
+  w.udp = cv.take<uint16_t>((size_t)nc * d * d);
 }
 
 int dtype_gt(int dt) { return dt == JOLT_BF16 ? GT_BF16 : GT_F32; }
@@ -251,7 +254,7 @@ int eig_values(Run &R, EigWs &e) {
       std::vector<const void *> key{e.b.A, e.trd, tab, e.b.d, e.b.e, e.b.tau,
                                     reinterpret_cast<const void *>((intptr_t)e.b.n),
                                     reinterpret_cast<const void *>((intptr_t)e.b.n_mat)};
-      const int lanes = std::min(jolt_ctx::kTrdLanes, e.b.n_mat);
+      const int lanes = std::min(c->trd_lanes_max, e.b.n_mat);
       if (c->trd_lanes != lanes || c->trd_key != key) {
         for (int g = 0; g < jolt_ctx::kTrdLanes; ++g)
           if (c->trd_exec[g]) { HIP_OK(hipGraphExecDestroy(c->trd_exec[g])); c->trd_exec[g] = nullptr; }
@@ -442,13 +445,19 @@ struct BlobView {
   int rT, rd, bits;
 };
 
-// W_s^T = 2^e_s U^_d G^_s^T (d x r_T per slice, leading dimension ldw) of every cell with a
-// backbone, from the stored factors, then the per-slice exponents k_s of the fused passes.
+// What the fused passes read besides the blobs, from the stored factors of every cell with
+// a backbone.  fp16 factors: G^_s^T per slice, the exponents ky_s and the permuted U^_d
+// (launch_core_prepare).  fp32 factors: W_s^T = 2^e_s U^_d G^_s^T (d x r_T per slice,
+// leading dimension ldw), then the per-slice exponents k_s.
 // fc: the host records of the call (uploaded here); fb: bytes per stored factor scalar.
 int build_w(Run &R, int nc, int m, int d, const std::vector<BlobView> &bv, const std::vector<FusedCell> &fc,
             int fb) {
   const int ft = fb == 2 ? GT_F16 : GT_F32;
   HIP_OK(hipMemcpyAsync(R.w.fcell_r, fc.data(), nc * sizeof(FusedCell), hipMemcpyHostToDevice, R.st));
+  if (fb == 2) {
+    HIP_OK(launch_core_prepare(R.w.fcell_r, R.w.signs, nc, m, d, R.st));
+    return JOLT_OK;
+  }
   std::vector<GemmProblem> P;
   for (int c = 0; c < nc; ++c) {
     const BlobView &v = bv[c];
@@ -476,7 +485,11 @@ FusedCell fused_cell(Run &R, int c, int m, int d, const BlobView &v) {
   f.wexp = R.w.wexp + (int64_t)c * m;
   f.codes = const_cast<uint8_t *>(v.b + v.L.codes);
   f.scales = reinterpret_cast<uint16_t *>(const_cast<uint8_t *>(v.b + v.L.scales));
-  f.rT = v.rT; f.bits = v.bits; f.ldw = R.w.ldw;
+  f.G = reinterpret_cast<const uint16_t *>(v.b + v.L.G);
+  f.gexp = reinterpret_cast<const int8_t *>(v.b + v.L.gexp);
+  f.Ud = reinterpret_cast<const uint16_t *>(v.b + v.L.Ud);
+  f.udp = R.w.udp + (int64_t)c * d * d;
+  f.rT = v.rT; f.bits = v.bits; f.ldw = R.w.ldw; f.rd = v.rd;
   return f;
 }
 
@@ -1568,6 +1581,12 @@ extern "C" int jolt_debug_set(jolt_ctx *ctx, int what, int64_t value) {
   if (what == JOLT_DBG_INVIT_ITERS) {
     if (value < 0 || value > 8) return jolt_fail(JOLT_E_INVAL, "jolt_debug_set: iterations must be in 0..8");
     ctx->invit_iters = (int)value;
+    return JOLT_OK;
+  }
+  if (what == JOLT_DBG_TRD_LANES) {
+    if (value < 1 || value > jolt_ctx::kTrdLanes)
+      return jolt_fail(JOLT_E_INVAL, "jolt_debug_set: tridiagonalisation lanes must be in 1..%d", jolt_ctx::kTrdLanes);
+    ctx->trd_lanes_max = (int)value;
     return JOLT_OK;
   }
   return jolt_fail(JOLT_E_INVAL, "jolt_debug_set: unknown setting %d", what);
