@@ -650,16 +650,20 @@ __global__ void __launch_bounds__(NT, sizeof(TIO) == 2 ? 2 : 1) k_core(FusedArgs
   const int lg = 31 - __builtin_clz(g), lgw = lg - 3;       // g and g / 8 are powers of two
 
   // U^_d carries the rotation signs (k_core_prepare), so stage 2 adds s * X~ 2^-xe to the
-  // accumulator, which starts from (exact scalings):
-  //   residual: -s * X 2^-xe, so that it ends as -(s * r) 2^-xe, r = X - X~;
-  //   decode:   H r^ / sqrt(d) 2^-xe, so that it ends as s * X^ 2^-xe;
-  //   export:   zero, ending as s * X~ 2^-xe.
+  // accumulator, which starts from (exact scaling):
+  //   residual and export: zero, ending as s * X~ 2^-xe; the residual pass keeps -s * X of
+  //             its entries in registers and forms -s * r = -s * X + s * X~ after the
+  //             reconstruction, a subtraction of close fp32 values that is exact, so r
+  //             carries the rounding of X~ only (the export mode returns the same X~);
+  //   decode:   H r^ / sqrt(d) 2^-xe, so that it ends as s * X^ 2^-xe.
   // acc2[fb][q] is value 16 fb + q: unit 4 fb + q / 4, entry q % 4.
   f32x16_t acc2[FB];
 #pragma unroll
   for (int fb = 0; fb < FB; ++fb)
 #pragma unroll
     for (int q = 0; q < 16; ++q) acc2[fb][q] = 0.f;
+  // residual: -s * X of the lane's entries as loaded (bf16 pairs, or fp32 in two words)
+  ju2 xw[MODE == FUSED_RESIDUAL ? NU : 1], xw2[MODE == FUSED_RESIDUAL && sizeof(TIO) == 4 ? NU : 1];
   if constexpr (MODE == FUSED_RESIDUAL) {
     // the tile's cache rows to LDS as -s * X: each thread moves the same 16-byte piece p of
     // several rows and flips the sign bits of its entries by a mask (-s_f < 0 sets the bit)
@@ -689,18 +693,15 @@ __global__ void __launch_bounds__(NT, sizeof(TIO) == 2 ? 2 : 1) k_core(FusedArgs
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < NU; ++u) {
-      float x[4];
       const uint8_t *src = sh + trow * L::IO_ROW + (8 * u + 4 * h) * (int)sizeof(TIO);
       if constexpr (sizeof(TIO) == 2) {
         const uint2 w = *reinterpret_cast<const uint2 *>(src);
-        x[0] = bf16_to_f32((bf16_t)(w.x & 0xffffu)); x[1] = bf16_to_f32((bf16_t)(w.x >> 16));
-        x[2] = bf16_to_f32((bf16_t)(w.y & 0xffffu)); x[3] = bf16_to_f32((bf16_t)(w.y >> 16));
+        xw[u] = ju2{w.x, w.y};
       } else {
         const float4 w = *reinterpret_cast<const float4 *>(src);
-        x[0] = w.x; x[1] = w.y; x[2] = w.z; x[3] = w.w;
+        xw[u] = ju2{__float_as_uint(w.x), __float_as_uint(w.y)};
+        xw2[u] = ju2{__float_as_uint(w.z), __float_as_uint(w.w)};
       }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) acc2[u >> 2][4 * (u & 3) + i] = ldexpf(x[i], -xe);
     }
     __syncthreads();                                        // the staging area is reused
   } else if constexpr (MODE == FUSED_DECODE) {
@@ -824,7 +825,20 @@ __global__ void __launch_bounds__(NT, sizeof(TIO) == 2 ? 2 : 1) k_core(FusedArgs
       }
     }
   } else if constexpr (MODE == FUSED_RESIDUAL) {
-    // v = -(s * r): r' = H (s * r) / sqrt(d) = -H v / sqrt(d)
+    // v = s * X~ - s * X = -(s * r), exact; r' = H (s * r) / sqrt(d) = -H v / sqrt(d)
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      float x[4];
+      if constexpr (sizeof(TIO) == 2) {
+        x[0] = bf16_to_f32((bf16_t)(xw[u].x & 0xffffu)); x[1] = bf16_to_f32((bf16_t)(xw[u].x >> 16));
+        x[2] = bf16_to_f32((bf16_t)(xw[u].y & 0xffffu)); x[3] = bf16_to_f32((bf16_t)(xw[u].y >> 16));
+      } else {
+        x[0] = __uint_as_float(xw[u].x); x[1] = __uint_as_float(xw[u].y);
+        x[2] = __uint_as_float(xw2[u].x); x[3] = __uint_as_float(xw2[u].y);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[4 * u + i] += x[i];
+    }
 #pragma unroll
     for (int w = 1; w < NV; w <<= 1)
 #pragma unroll

@@ -310,3 +310,37 @@ def test_decompress_reapplies_rope(out_dtype):
         assert (diff - np.abs(w16) * 2 ** -7).max() <= 1e-5 * float(np.sqrt(np.mean(X * X)))
     with pytest.raises(J.JoltError):
         J.jolt_decompress(ctx(), blobs, od, [out], ws, rope=(1.0, 0))
+
+
+@pytest.mark.parametrize("dtype,d,r,bits,group", [("bf16", 32, 13, 8, 8), ("f32", 64, 21, 2, 16),
+                                                  ("bf16", 128, 40, 4, 128), ("bf16", 128, 96, 8, 32)])
+def test_fused_passes_shape_variants(dtype, d, r, bits, group):
+    """The fused residual and decode passes (fp16 factors) over shapes their tiling treats
+    apart: d = 32 / 64 / 128, T = 300 (two full 128-token tiles and a ragged one), r_T not a
+    multiple of 8 (U_T rows read entry by entry) or up to three 32-row blocks of r_d,
+    quantiser groups of 8 to 128 entries, 2 / 4 / 8-bit codes, bf16 and fp32 cells.
+    Stage-wise against the oracle: X~ is the reconstruction of the blob's own factors, the
+    codes and scales are the oracle quantiser's on X - X~, the decode is the oracle's decode
+    of the blob."""
+    rng = np.random.default_rng(1000 + d + r)
+    X = lowrank_cell(rng, 4, 300, d, min(r, d), noise=0.02, decay=0.5)
+    xs, ex, desc = device_cells([X], dtype)
+    p = J.Params(r, min(r, d), bits, group, J.JOLT_FACTOR_F16, 0, 9)
+    blobs, ws = compress(xs, desc, [p])
+    got = opl.read_blob(blob_bytes(blobs[0]))
+    nX = np.linalg.norm(ex[0])
+    Xt_gpu = torch.empty((4, 300, d), device="cuda")
+    J.jolt_debug_export(ctx(), 2, 0, Xt_gpu)
+    Xt_gpu = Xt_gpu.cpu().numpy().astype(np.float64)
+    Xt_blob = opl.decode_parts_from_factors(got["U_hat"], got["Ud_hat"], got["G_hat"], got["gexp"],
+                                            None, None, T=300, d=d, bits=0, group=group, seed=9)
+    assert np.linalg.norm(Xt_gpu - Xt_blob) <= 1e-5 * nX
+    from oracle.philox import rotation_signs
+    from oracle.residual import quantize, rotate
+    codes_ref, scales_ref = quantize(rotate(ex[0] - Xt_gpu, rotation_signs(9, d)), bits, group)
+    frac, mx = code_mismatch(got["codes"], codes_ref)
+    assert frac <= 1e-4 and mx <= 1, (frac, mx)
+    np.testing.assert_allclose(got["scales"], scales_ref, rtol=2e-3)
+    Xh = decompress(blobs, desc, "f32")[0]
+    Xh_orc = opl.decode_blob(blob_bytes(blobs[0]))
+    assert np.linalg.norm(Xh - Xh_orc) <= 1e-5 * nX
