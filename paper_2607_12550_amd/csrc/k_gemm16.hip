@@ -9,8 +9,9 @@
 // (A hi * B + A lo * B, or the same for B); two fp32 operands take three
 // (hi*hi + lo*hi + hi*lo, dropping lo*lo, which is below 2^-16 of the product).
 //
-// Tile BM x 128 (BM = 128 or 256) per 256-thread workgroup, 4 waves in a 2 x 2 grid, each
-// (BM/2) x 64 = (BM/64) x 2 MFMA blocks; K tiles of 64.  Operands go global -> registers ->
+// Tile BM x BN (128 x 128, 256 x 128, or 256 x 256 for the token Gram of long rows) per
+// 256-thread workgroup, 4 waves in a 2 x 2 grid, each (BM/2) x (BN/2) = (BM/64) x (BN/64)
+// MFMA blocks; K tiles of 64.  Operands go global -> registers ->
 // LDS; the next K tile's loads are issued before the current tile is multiplied and their
 // registers are only read when they are stored to LDS, so the loads stay in flight during
 // the MFMAs.  With two LDS buffers (see Lds for when) the next tile is stored into the
@@ -38,7 +39,7 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 namespace {
 
-constexpr int BN = 128, BK = 64, NT = 256, LDK = BK + 8;
+constexpr int BK = 64, NT = 256, LDK = BK + 8;
 constexpr int LDS_BYTES = 160 * 1024;
 
 struct Grid {
@@ -206,7 +207,7 @@ struct Addr {
 // Two LDS buffers are used when they fit in half the LDS (two workgroups per CU), or, for
 // the 256-row tiles, in all of it: one workgroup per CU with double buffering measured
 // faster than two single-buffered ones there, slower for the 128-row split-operand tiles.
-template <int BM, bool AS, bool BS>
+template <int BM, int BN, bool AS, bool BS>
 struct Lds {
   static constexpr int LA = BM * LDK * (AS ? 2 : 1), LB = BN * LDK * (BS ? 2 : 1);
   static constexpr bool DB = 2 * 2 * (LA + LB) <= (BM == 256 ? LDS_BYTES : LDS_BYTES / 2);
@@ -242,8 +243,8 @@ JOLT_DEV bool decode(const Grid &g, int j, int &z, int &tm, int &tn) {
   return true;
 }
 
-// BM x 128 tile per 256-thread workgroup; waves in a 2 x 2 grid, each (BM/2) x 64.
-template <int BM, bool AK, bool BK_, bool AS, bool BS>
+// BM x BN tile per 256-thread workgroup; waves in a 2 x 2 grid, each (BM/2) x (BN/2).
+template <int BM, int BN, bool AK, bool BK_, bool AS, bool BS>
 __global__ void __launch_bounds__(NT) k_gemm16(const GemmProblem *__restrict__ probs, Grid g) {
   // blocks are dealt to the 8 XCDs round-robin; give each XCD a contiguous run of tiles
   const int i = blockIdx.x, j = (i & 7) * g.per_xcd + (i >> 3);
@@ -251,19 +252,19 @@ __global__ void __launch_bounds__(NT) k_gemm16(const GemmProblem *__restrict__ p
   if (!decode(g, j, z, tm, tn)) return;
   const GemmProblem P = probs[z];
   if (tm * BM >= P.M || tn * BN >= P.N) return;
-  constexpr int MI = BM / 64;      // 32-row MFMA blocks per wave
-  __shared__ __attribute__((aligned(16))) Lds<BM, AS, BS> sm;
+  constexpr int MI = BM / 64, NI = BN / 64;      // 32-row / 32-column MFMA blocks per wave
+  __shared__ __attribute__((aligned(16))) Lds<BM, BN, AS, BS> sm;
   constexpr int TA = BM * LDK, TB = BN * LDK;
-  constexpr int LA = Lds<BM, AS, BS>::LA, LB = Lds<BM, AS, BS>::LB;
+  constexpr int LA = Lds<BM, BN, AS, BS>::LA, LB = Lds<BM, BN, AS, BS>::LB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1, lr = lane & 31, lh = lane >> 5;
   const int m0 = tm * BM, n0 = tn * BN;
 
-  f32x16_t acc[MI][2];
+  f32x16_t acc[MI][NI];
 #pragma unroll
   for (int a = 0; a < MI; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < NI; ++b)
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[a][b][q] = 0.f;
 
@@ -279,10 +280,12 @@ __global__ void __launch_bounds__(NT) k_gemm16(const GemmProblem *__restrict__ p
     if (k_ < kfull) { ad_a.fetch_full(P.A, k_, sa[s]); ad_b.fetch_full(P.B, k_, sb[s]); } } while (0)
   auto compute_at = [&](int buf) {
     const uint16_t *la_ = sm.a + buf * LA, *lb_ = sm.b + buf * LB;
-#pragma unroll
+    // 16-wide k steps; with 256 x 256 tiles they are not unrolled, so that the fragments of
+    // one step only are live beside the 256 accumulator registers
+#pragma unroll (BN == 256 ? 1 : BK / 16)
     for (int s = 0; s < BK / 16; ++s) {
       const int ko = s * 16 + 8 * lh;
-      bf16x8_t fa[MI], fb[2], la[MI], lb[2];
+      bf16x8_t fa[MI], fb[NI], la[MI], lb[NI];
 #pragma unroll
       for (int a = 0; a < MI; ++a) {
         const int ra = (wm * (BM / 2) + a * 32 + lr) * LDK + ko;
@@ -290,22 +293,22 @@ __global__ void __launch_bounds__(NT) k_gemm16(const GemmProblem *__restrict__ p
         if constexpr (AS) la[a] = *reinterpret_cast<const bf16x8_t *>(la_ + TA + ra);
       }
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const int rb = (wn * 64 + b * 32 + lr) * LDK + ko;
+      for (int b = 0; b < NI; ++b) {
+        const int rb = (wn * (BN / 2) + b * 32 + lr) * LDK + ko;
         fb[b] = *reinterpret_cast<const bf16x8_t *>(lb_ + rb);
         if constexpr (BS) lb[b] = *reinterpret_cast<const bf16x8_t *>(lb_ + TB + rb);
       }
 #pragma unroll
       for (int a = 0; a < MI; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b) {
+        for (int b = 0; b < NI; ++b) {
           acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], acc[a][b], 0, 0, 0);
           if constexpr (AS) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(la[a], fb[b], acc[a][b], 0, 0, 0);
           if constexpr (BS) acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], lb[b], acc[a][b], 0, 0, 0);
         }
     }
   };
-  if constexpr (Lds<BM, AS, BS>::DB) {
+  if constexpr (Lds<BM, BN, AS, BS>::DB) {
   // two LDS buffers: tile k+1 is stored into one while tile k is multiplied out of the
   // other; one barrier per step
   
@@ -358,10 +361,10 @@ __global__ void __launch_bounds__(NT) k_gemm16(const GemmProblem *__restrict__ p
   const float alpha = P.alpha;
   const int aexp = P.alpha_exp2 ? (int)*gptr(P.alpha_exp2) : 0;
   // epilogue through LDS, 32 rows per round: acc[a][b][q] is the output at row
-  // wm*(BM/2) + a*32 + 8*(q/4) + 4*lh + q%4, column wn*64 + b*32 + lr of the tile
+  // wm*(BM/2) + a*32 + 8*(q/4) + 4*lh + q%4, column wn*(BN/2) + b*32 + lr of the tile
   float *cs = reinterpret_cast<float *>(&sm);
   constexpr int CLD = BN + 4;
-  static_assert(32 * CLD * sizeof(float) <= sizeof(Lds<BM, AS, BS>), "epilogue tile exceeds LDS");
+  static_assert(32 * CLD * sizeof(float) <= sizeof(Lds<BM, BN, AS, BS>), "epilogue tile exceeds LDS");
   const bool use_beta = P.beta != 0.f;
   const bool ct = P.c_trans != 0;   // store the transpose: C[col * ldc + row]
   const bool vec = ((reinterpret_cast<uintptr_t>(P.C) & 15) == 0) && (P.ldc % 4 == 0);
@@ -371,18 +374,19 @@ __global__ void __launch_bounds__(NT) k_gemm16(const GemmProblem *__restrict__ p
     if (wm == h / MI) {
       const int a = h % MI;
 #pragma unroll
-      for (int b = 0; b < 2; ++b)
+      for (int b = 0; b < NI; ++b)
 #pragma unroll
         for (int q = 0; q < 16; ++q)
-          cs[(8 * (q >> 2) + 4 * lh + (q & 3)) * CLD + wn * 64 + b * 32 + lr] = acc[a][b][q];
+          cs[(8 * (q >> 2) + 4 * lh + (q & 3)) * CLD + wn * (BN / 2) + b * 32 + lr] = acc[a][b][q];
     }
     __syncthreads();
+    // 32 rows x BN columns in runs of 4 (along the row, or along the column for C^T)
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < 8 * BN / NT; ++u) {
       const int idx = tid + u * NT;
       int rr, cc;
       if (ct) { cc = idx >> 3; rr = (idx & 7) * 4; }
-      else { rr = idx >> 5; cc = (idx & 31) * 4; }
+      else { rr = idx / (BN / 4); cc = (idx % (BN / 4)) * 4; }
       const int row = m0 + h * 32 + rr, col = n0 + cc;
       if (ct) {
         if (col >= P.N || row >= P.M) continue;
@@ -428,10 +432,10 @@ __global__ void __launch_bounds__(NT) k_gemm16(const GemmProblem *__restrict__ p
 template <int BM, bool AS, bool BS>
 hipError_t launch_bm(const GemmProblem *probs, const Grid &g, bool ak, bool bk, hipStream_t st) {
   const dim3 grid(g.per_xcd * 8);
-  if (ak && bk) hipLaunchKernelGGL((k_gemm16<BM, true, true, AS, BS>), grid, dim3(NT), 0, st, probs, g);
-  else if (ak) hipLaunchKernelGGL((k_gemm16<BM, true, false, AS, BS>), grid, dim3(NT), 0, st, probs, g);
-  else if (bk) hipLaunchKernelGGL((k_gemm16<BM, false, true, AS, BS>), grid, dim3(NT), 0, st, probs, g);
-  else hipLaunchKernelGGL((k_gemm16<BM, false, false, AS, BS>), grid, dim3(NT), 0, st, probs, g);
+  if (ak && bk) hipLaunchKernelGGL((k_gemm16<BM, 128, true, true, AS, BS>), grid, dim3(NT), 0, st, probs, g);
+  else if (ak) hipLaunchKernelGGL((k_gemm16<BM, 128, true, false, AS, BS>), grid, dim3(NT), 0, st, probs, g);
+  else if (bk) hipLaunchKernelGGL((k_gemm16<BM, 128, false, true, AS, BS>), grid, dim3(NT), 0, st, probs, g);
+  else hipLaunchKernelGGL((k_gemm16<BM, 128, false, false, AS, BS>), grid, dim3(NT), 0, st, probs, g);
   return hipGetLastError();
 }
 
@@ -505,15 +509,16 @@ bool gemm16_prepare(GemmProblem *probs, int n, int &ta, int &tb, bool &ak, bool 
   }
   if (swap) { std::swap(ta, tb); std::swap(ak, bk); }
   // 256-row tiles for split-operand products over long M whose bf16 operand is k-contiguous
-  // (two LDS buffers still fit) and for large lower-triangle bf16 tables with a long K (the
-  // token Gram of wide cells: each K step then moves 384 operand rows for 256 x 128 outputs
-  // instead of 256 rows for 128 x 128; measured faster from K = 25600, slower at K = 4096,
-  // where the 128-row tiles keep two workgroups per CU busy); 128 otherwise (an m-contiguous
-  // bf16 operand is transposed on its way to LDS, and the 128-row tile then runs two
-  // workgroups per CU)
+  // (two LDS buffers still fit); 256 x 256 tiles for large lower-triangle bf16 tables with a
+  // long K (the token Gram of wide cells: each K step moves 512 operand rows for 256 x 256
+  // outputs, and each wave's 128 x 128 block reads 8 fragments per 16 MFMAs, where the
+  // 128 x 128 tiles read 4 per 4 and leave the K loop bound by LDS bandwidth); 128 otherwise
+  // (an m-contiguous bf16 operand is transposed on its way to LDS, and the 128-row tile
+  // then runs two workgroups per CU; at K = 4096 the 128-row tiles also keep two
+  // workgroups per CU busy and measured faster)
   const bool bf_both = ta == GT_BF16 && tb == GT_BF16 && ak && bk;
-  bm = ((tb == GT_F32 && ta == GT_BF16 && maxM >= 2048 && !lower && ak) ||
-        (lower && bf_both && maxM >= 2048 && minK >= 16384)) ? 256 : 128;
+  if (lower && bf_both && maxM >= 2048 && minK >= 16384) bm = GEMM16_SQUARE256;
+  else bm = (tb == GT_F32 && ta == GT_BF16 && maxM >= 2048 && !lower && ak) ? 256 : 128;
   return true;
 }
 
@@ -523,11 +528,13 @@ hipError_t launch_gemm16(const GemmProblem *probs_dev, int n_probs, int max_M, i
   if (n_probs <= 0 || max_M <= 0 || max_N <= 0) return hipSuccess;
   const bool as = ta == GT_F32, bs = tb == GT_F32;
   if ((ta != GT_BF16 && !as) || (tb != GT_BF16 && !bs)) return hipErrorInvalidValue;
-  if (bm != 128 && bm != 256) return hipErrorInvalidValue;
-  if (lower_only && bm == 256 && (as || bs)) return hipErrorInvalidValue;
+  if (bm != 128 && bm != 256 && bm != GEMM16_SQUARE256) return hipErrorInvalidValue;
+  if (lower_only && bm != 128 && (as || bs)) return hipErrorInvalidValue;
+  const bool square = bm == GEMM16_SQUARE256;
+  const int tm_rows = square ? 256 : bm, tn_cols = square ? 256 : 128;
   Grid g;
-  g.tiles_m = (max_M + bm - 1) / bm;
-  g.tiles_n = (max_N + BN - 1) / BN;
+  g.tiles_m = (max_M + tm_rows - 1) / tm_rows;
+  g.tiles_n = (max_N + tn_cols - 1) / tn_cols;
   g.lower_only = lower_only ? 1 : 0;
   g.wide = lower_only && bm == 256 ? 1 : 0;
   if (g.wide) {
@@ -538,6 +545,13 @@ hipError_t launch_gemm16(const GemmProblem *probs_dev, int n_probs, int max_M, i
   }
   g.total = g.per_prob * n_probs;
   g.per_xcd = (g.total + 7) / 8;
+  if (square) {
+    // 256 x 256 tiles, bf16 x bf16 with both operands k-contiguous only
+    if (as || bs || !a_kcontig || !b_kcontig) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_gemm16<256, 256, true, true, false, false>), dim3(g.per_xcd * 8), dim3(NT), 0, st,
+                       probs_dev, g);
+    return hipGetLastError();
+  }
   if (bm == 256) {
     if (as && bs) return hipErrorInvalidValue;
     if (as) return launch_bm<256, true, false>(probs_dev, g, a_kcontig, b_kcontig, st);

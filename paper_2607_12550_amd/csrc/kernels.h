@@ -129,6 +129,8 @@ hipError_t launch_gemm(const GemmProblem *probs_dev, int n_probs, int max_M, int
 // false when a layout condition of the kernel is not met (use launch_gemm then), and may
 // rewrite the table and the type / layout arguments (an fp32 A is moved to the B side by
 // computing C^T) and picks the tile height bm for launch_gemm16.
+// tile code of launch_gemm16 besides the row counts 128 and 256: 256 x 256 tiles
+constexpr int GEMM16_SQUARE256 = 512;
 bool gemm16_prepare(GemmProblem *probs_host, int n_probs, int &ta, int &tb, bool &a_kcontig,
                     bool &b_kcontig, int &bm);
 hipError_t launch_gemm16(const GemmProblem *probs_dev, int n_probs, int max_M, int max_N, int ta,
