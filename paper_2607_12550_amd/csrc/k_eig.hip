@@ -629,7 +629,7 @@ size_t backtransform_table_entries(int n_mat, int n) {
   return panels * (size_t)n_mat * (1 + chunks + 2);
 }
 
-hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax, float *U,
+hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax, const int *k_host, float *U,
                                 int64_t ldu, int64_t u_stride, float *scratch, GemmProblem *tab_dev,
                                 GemmProblem *tab_host, hipStream_t st) {
   const int n = b.n, panels = (n + NB - 1) / NB, nm = b.n_mat;
@@ -652,6 +652,7 @@ hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax,
     GemmProblem *g = tab_host + (size_t)panels * nm + (size_t)p * per_panel;
     for (int m = 0; m < nm; ++m) {
       const float *A = b.A + (int64_t)m * b.mat_stride;
+      const int km = std::min(std::max(k_host[m], 0), kmax);   // this matrix's vectors
       GemmProblem S{};
       S.A = GemmOperand{A + (int64_t)(i0 + 1) * n + i0, n, 0, 0, 0, 1};
       S.B = GemmOperand{A + (int64_t)(i0 + 1) * n + i0, n, 0, 0, 0, 1};
@@ -665,7 +666,7 @@ hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax,
         P.A = GemmOperand{A + (int64_t)(i0 + 1 + r0) * n + i0, n, 0, 0, 0, 1};
         P.B = GemmOperand{U + (int64_t)m * u_stride + (int64_t)(i0 + 1 + r0) * ldu, ldu, 0, 0, 0, 1};
         P.C = W1 + m * w1_mat + (int64_t)c * NB * kmax; P.ldc = kmax;
-        P.M = (c < chunks) ? pw : 0; P.N = kmax; P.K = std::max(0, r1 - r0);
+        P.M = (c < chunks) ? pw : 0; P.N = km; P.K = std::max(0, r1 - r0);
         P.alpha = 1.f; P.beta = 0.f;
         g[(size_t)m * chunks_max + c] = P;
       }
@@ -675,13 +676,13 @@ hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax,
       Q.A = seg_operand(Tf + ((size_t)m * panels + p) * NB * NB, NB, 0, 0, NB, 1);
       Q.B = GemmOperand{W1 + m * w1_mat, kmax, 0, 0, 0, 1};
       Q.C = W2 + (size_t)m * NB * kmax; Q.ldc = kmax;
-      Q.M = pw; Q.N = kmax; Q.K = chunks * NB; Q.alpha = 1.f; Q.beta = 0.f;
+      Q.M = pw; Q.N = km; Q.K = chunks * NB; Q.alpha = 1.f; Q.beta = 0.f;
       g[(size_t)nm * chunks_max + m] = Q;
       GemmProblem R{};
       R.A = GemmOperand{A + (int64_t)(i0 + 1) * n + i0, n, 0, 0, 0, 1};
       R.B = GemmOperand{W2 + (size_t)m * NB * kmax, kmax, 0, 0, 0, 1};
       R.C = U + (int64_t)m * u_stride + (int64_t)(i0 + 1) * ldu; R.ldc = ldu;
-      R.M = rows; R.N = kmax; R.K = pw; R.alpha = -1.f; R.beta = 1.f;
+      R.M = rows; R.N = km; R.K = pw; R.alpha = -1.f; R.beta = 1.f;
       g[(size_t)nm * (chunks_max + 1) + m] = R;
     }
   }

@@ -266,13 +266,14 @@ hipError_t launch_tridiag_eigvecs(const EigBatch &b, const InvitWork &w, int kma
                                   hipStream_t st);
 // U = Q Z for the Householder vectors stored in A (Q = H_0 ... H_{n-2}), blocked into
 // panels of backtransform_nb() reflectors applied as I - V T V^T with GEMMs.  U fp32
-// [n_mat] x (n x ldu) at u_stride, first k[mat] columns written.  Needs
+// [n_mat] x (n x ldu) at u_stride, first k[mat] columns written (k_host: the host copy of
+// the per-matrix counts; each matrix's products run over its own k[mat] columns).  Needs
 // backtransform_scratch_floats() device floats and backtransform_table_entries()
 // GemmProblem slots on device (tab_dev) and host (tab_host).
 int backtransform_nb();
 size_t backtransform_scratch_floats(int n_mat, int n, int kmax);
 size_t backtransform_table_entries(int n_mat, int n);
-hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax, float *U,
+hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax, const int *k_host, float *U,
                                 int64_t ldu, int64_t u_stride, float *scratch, GemmProblem *tab_dev,
                                 GemmProblem *tab_host, hipStream_t st);
 

@@ -313,7 +313,7 @@ int eig_vectors(Run &R, EigWs &e, const std::vector<int> &k, float *U, int64_t l
   GemmProblem *tab = R.tab_slice(nt);
   if (!tab) return jolt_fail(JOLT_E_WORKSPACE, "GEMM problem table overflow");
   R.ctx->tab_host.resize(std::max(R.ctx->tab_host.size(), nt));
-  HIP_OK(launch_backtransform(e.b, iw, kmax, U, ldu, u_stride, e.bt, tab, R.ctx->tab_host.data(), R.st));
+  HIP_OK(launch_backtransform(e.b, iw, kmax, k.data(), U, ldu, u_stride, e.bt, tab, R.ctx->tab_host.data(), R.st));
   return JOLT_OK;
 }
 
