@@ -13,7 +13,7 @@
 
 namespace {
 
-constexpr int KC = 256;   // inverse-iteration columns per launch (bounds its scratch)
+constexpr int KC = 512;   // inverse-iteration columns per launch (bounds its scratch)
 constexpr int SYTRD_SMALL_MAX = 768;   // larger matrices use the blocked multi-workgroup kernel
 constexpr int SYTRD_NB = 32;
 constexpr int kG64Rows = 8192;          // rows per split-K chunk of the fp64 sketch Gram
