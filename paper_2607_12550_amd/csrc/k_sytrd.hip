@@ -16,9 +16,10 @@
 //   k_symv_tiles  lower-triangle 128 x 128 tiles of A22 (each read once; an off-diagonal
 //                 tile feeds two row blocks through per-slot partials, so row sums are
 //                 formed in a fixed order);
-//   k_col_finish  per 128-row block: tau, v, y, w_pre = tau y, partial w_pre^T v;
-//   k_col_next    per 128-row block: w = w_pre + alpha2 v, the next column's x and the
-//                 block partials of its sigma and dot products.
+//   k_col_step    per 128-row block: tau, v, y, w (y^T v assembled from global sums the
+//                 launch already has), then the next column's x and the block partials of
+//                 its sigma and dot products;
+//   k_col_first   the first column of a panel (x is column k0 of A).
 // Panels are stored twice, P = [V; W] and Q = [W; V] (rows = panel columns, packed to
 // the panel's width jb), so the rank-2jb update is the single product P^T Q.  Every row
 // a kernel or the update reads (rows >= the current column's o) has been written in
@@ -32,6 +33,8 @@ namespace {
 
 constexpr int TB = 128;   // mat-vec tile
 constexpr int RB = 128;   // rows per workgroup of the column kernels
+constexpr int TRD_MAX_N = 8192;
+static_assert(TRD_MAX_N / TB <= 64, "the slots of one row fit the lanes of a wavefront");
 
 JOLT_DEV void tri_decode(int t, int &I, int &J) {
   int i = (int)((sqrtf(8.f * (float)t + 1.f) - 1.f) * 0.5f);
@@ -42,7 +45,7 @@ JOLT_DEV void tri_decode(int t, int &I, int &J) {
 }
 
 struct MatView {
-  float *A, *P, *Q, *xt, *wpre, *part, *dpart, *wpart, *sc;
+  float *A, *P, *Q, *xt, *part, *dpart, *qpart, *sc;
   double *d, *e;
   float *tau;
 };
@@ -55,11 +58,10 @@ JOLT_DEV MatView view(const SytrdArgs &a, int mat) {
   m.P = base;
   m.Q = m.P + (int64_t)2 * nb * n;
   m.xt = m.Q + (int64_t)2 * nb * n;
-  m.wpre = m.xt + n;
-  m.part = m.wpre + n;
-  m.dpart = m.part + (int64_t)a.slots * n;
-  m.wpart = m.dpart + (int64_t)a.slots * (2 * nb + 1);
-  m.sc = m.wpart + a.slots;          // [0] alpha, [1] diagonal
+  m.part = m.xt + n;
+  m.dpart = m.part + (int64_t)a.slots * n;                  // two buffers (column parity)
+  m.qpart = m.dpart + (int64_t)2 * a.slots * (2 * nb + 1);
+  m.sc = m.qpart + (int64_t)a.slots * (a.slots + 1) / 2;   // per parity: [0] alpha, [1] diagonal
   m.d = a.d + (int64_t)mat * n;
   m.e = a.e + (int64_t)mat * n;
   m.tau = a.tau + (int64_t)mat * n;
@@ -73,8 +75,15 @@ JOLT_DEV MatView view(const SytrdArgs &a, int mat) {
 // holds 8 rows x 8 columns in registers, the columns being the two runs 4 tx .. 4 tx + 3 and
 // 64 + 4 tx .. 64 + 4 tx + 3 of the tile, so that each 16-byte load of a wave covers two
 // whole cache lines of a row; row sums reduce across tx (lane shuffles), column sums across
-// ty (shuffles, then LDS across the four waves).  Tiles (I, 0) also produce the
-// dot partials [sigma, W_p^T x, V_p^T x] over their 128 rows.
+// ty (shuffles, then LDS across the four waves).  Each tile also writes its term of
+// x_tail^T A22 x_tail (x_I^T A_II x_I on the diagonal, 2 x_I^T A_IJ x_J off it), which is
+// sum_r x_r (row sum)_r + sum_c x_c (column sum)_c over the tile in both cases.
+// base[byte offset]: with base uniform and the offset a 32-bit vector, the load takes the
+// scalar-base + vector-offset form
+JOLT_DEV float ld_off(const float *base, uint32_t boff) {
+  return *reinterpret_cast<const float *>(reinterpret_cast<const char *>(base) + boff);
+}
+
 JOLT_DEV void householder(float alpha, double sigma, double &beta, double &tv, double &scal) {
   if (sigma == 0.0) { tv = 0.0; beta = alpha; scal = 0.0; return; }
   beta = -copysign(sqrt((double)alpha * alpha + sigma), (double)alpha);
@@ -82,12 +91,29 @@ JOLT_DEV void householder(float alpha, double sigma, double &beta, double &tv, d
   scal = 1.0 / (alpha - beta);
 }
 
-__global__ void __launch_bounds__(RB) k_col_finish(SytrdArgs a, int i, int j, int jbw) {
+// Column i = k0 + j of a panel, after the mat-vec of its x_tail: reflector i from the block
+// partials, w_i, and, when the panel continues (more != 0), column i + 1 as updated by
+// reflectors k0 .. i together with the block partials of its sigma and dot products.
+// w_i = tau y - (tau^2 / 2)(y^T v) v needs the global y^T v; it is assembled from sums this
+// launch already has, so that no second launch per column is needed:
+//   y^T v     = v^T A22 v - 2 (V^T v).(W^T v),
+//   v^T A22 v = A22[o, o] + 2 scal (A22 x_tail)[o] + scal^2 x_tail^T A22 x_tail,
+// with (A22 x_tail)[o] summed from the slot partials of row o and the last term from the
+// mat-vec's per-tile partials.  Each workgroup also forms y[o] (hence w_i[o], which the
+// next column's update needs) by wave sums, and the owner of row o stores that same value.
+// The column scalars (alpha, diagonal) and the dot partials alternate between two
+// buffers by column parity: this launch reads column i's and writes column i + 1's.
+__global__ void __launch_bounds__(RB, 2) k_col_step(SytrdArgs a, int i, int j, int jbw, int more) {
   const int mat = blockIdx.y, n = a.n, nb = a.nb, o = i + 1;
-  const int base = o & ~31, nt = (n - base + TB - 1) / TB;
-  const int nprev = (n - i + RB - 1) / RB;     // row blocks of the k_col_next launch that made x
+  const int base = o & ~31, nt = (n - base + TB - 1) / TB, ntile = nt * (nt + 1) / 2;
+  const int nprev = (n - i + RB - 1) / RB;     // row blocks of the launch that made column i's x
   const MatView M = view(a, mat);
-  __shared__ float pw[64], pv[64];
+  const int64_t dstride = 2 * nb + 1, dbuf = (int64_t)a.slots * dstride;
+  const float *dcur = M.dpart + (i & 1) * dbuf;
+  float *dnext = M.dpart + ((i + 1) & 1) * dbuf;
+  const float *scur = M.sc + 2 * (i & 1);
+  float *snext = M.sc + 2 * ((i + 1) & 1);
+  __shared__ float pw[32], pv[32], cw[32], cv[32];
   __shared__ double red[RB / 64];
   __shared__ double sh_sigma;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -98,29 +124,40 @@ __global__ void __launch_bounds__(RB) k_col_finish(SytrdArgs a, int i, int j, in
   // Every load that does not depend on this column's Householder scalars is issued before
   // any is used and without a branch: entries past the live range read an entry this launch
   // does not write and are masked afterwards.  The kernel then waits on one memory round
-  // trip before its barrier.
+  // trip before its first barrier.  Each load is a uniform row base plus a per-thread byte
+  // offset shared by its group, so the addresses cost no 64-bit vector arithmetic.
+  const uint32_t off_r = 4u * (uint32_t)rr, off_p = 4u * (uint32_t)(rr - base);
   const float *pp = M.part + (rr - base);
   float ts[32];
 #pragma unroll
-  for (int q = 0; q < 32; ++q) ts[q] = pp[(int64_t)min(q, nt - 1) * n];
-  const float a_o = M.A[(int64_t)o * n + rr];   // A22[:, 0] (row o by symmetry)
-  const float x_r = M.xt[rr];
-  // row f of V is not written by this launch (it writes row j only)
+  for (int q = 0; q < 32; ++q) ts[q] = ld_off(M.part + (int64_t)min(q, nt - 1) * n, off_p);
+  const float a_o = ld_off(M.A + (int64_t)o * n, off_r);   // A22[:, 0] (row o by symmetry)
+  const float a_oo = M.A[(int64_t)o * n + o];
+  const float x_r = ld_off(M.xt, off_r);
+  // row f of V and W is not written by this launch (it writes row j only)
   const int f = j == 0 ? 1 : 0;
   float vrow[32], wrow[32];
 #pragma unroll
   for (int p = 0; p < 32; ++p) {
-    vrow[p] = V[(int64_t)(p < j ? p : f) * n + rr];
-    wrow[p] = W[(int64_t)(p < j ? p : 0) * n + rr];
+    vrow[p] = ld_off(V + (int64_t)(p < j ? p : f) * n, off_r);
+    wrow[p] = ld_off(W + (int64_t)(p < j ? p : f) * n, off_r);
   }
-  float w_o = W[(int64_t)(tid < j ? tid : 0) * n + o];
-  float v_o = V[(int64_t)(tid < j ? tid : f) * n + o];
-  const float alpha = M.sc[0];
-  const int64_t dstride = 2 * nb + 1;
-  const float *dp = M.dpart + min(tid, 2 * j);  // dot of this thread: 0 sigma, then W, V
+  const uint32_t off_c = 4u * (uint32_t)(tid < j ? tid : f) * (uint32_t)n;
+  float w_o = ld_off(W + o, off_c);
+  float v_o = ld_off(V + o, off_c);
+  const float alpha = scur[0];
+  const uint32_t off_d = 4u * (uint32_t)min(tid, 2 * j);   // dot of this thread: 0 sigma, then W, V
+  const float *dp = dcur + min(tid, 2 * j);
   float td[32];
 #pragma unroll
-  for (int b = 0; b < 32; ++b) td[b] = dp[(int64_t)min(b, nprev - 1) * dstride];
+  for (int b = 0; b < 32; ++b) td[b] = ld_off(dcur + (int64_t)min(b, nprev - 1) * dstride, off_d);
+  // slot `lane` of row o
+  const float pov = ld_off(M.part + (o - base), 4u * (uint32_t)min(lane, nt - 1) * (uint32_t)n);
+  constexpr int QU = 8;
+  float qv[QU];
+#pragma unroll
+  for (int k = 0; k < QU; ++k) qv[k] = ld_off(M.qpart, 4u * (uint32_t)min(tid + RB * k, ntile - 1));
+
   float ysl = 0.f;
 #pragma unroll
   for (int q = 0; q < 32; ++q) ysl += q < nt ? ts[q] : 0.f;
@@ -139,41 +176,93 @@ __global__ void __launch_bounds__(RB) k_col_finish(SytrdArgs a, int i, int j, in
     else if (tid <= j) pw[tid - 1] = (float)sd;
     else pv[tid - 1 - j] = (float)sd;
   }
+  if (tid < j) { cw[tid] = w_o; cv[tid] = v_o; }
+  // x_tail^T A22 x_tail: per-thread sums over tiles t = tid + RB k, then the block (fp64)
+  double qs = 0.0;
+#pragma unroll
+  for (int k = 0; k < QU; ++k) qs += tid + RB * k < ntile ? (double)qv[k] : 0.0;
+  for (int t = tid + RB * QU; t < ntile; t += RB) qs += (double)M.qpart[t];
+  qs = wave_sum(qs);
+  if (lane == 0) red[wave] = qs;
   __syncthreads();
+  const double qsum = red[0] + red[1];
   double beta, tv, scal;
   householder(alpha, sh_sigma, beta, tv, scal);
   const float sc = (float)scal, tf = (float)tv;
-  // W^T v = scal W^T x_tail + W[o, :]  (v = e_o + scal x_tail, x_tail[o] = 0)
-  if (tid < j) {
-    pw[tid] = sc * pw[tid] + w_o;
-    pv[tid] = sc * pv[tid] + v_o;
+  // W^T v = scal W^T x_tail + W[o, :] and V^T v = scal V^T x_tail + V[o, :] (v = e_o +
+  // scal x_tail, x_tail[o] = 0) are formed where used, from the raw dots and row o in LDS.
+  // y[o] (lane p < j takes correction p, lane q < nt slot q of row o; wave sums, so every
+  // wave has the same value) and alpha2 = -(tau^2 / 2) y^T v
+  float tcorr = 0.f;
+  double tpvw = 0.0;
+  if (lane < j) {
+    const float pwf = fmaf(sc, pw[lane], cw[lane]), pvf = fmaf(sc, pv[lane], cv[lane]);
+    tcorr = fmaf(cv[lane], pwf, cw[lane] * pvf);
+    tpvw = (double)pvf * (double)pwf;
   }
-  __syncthreads();
-  double dot = 0.0;
+  const float ysl_o = wave_sum(lane < nt ? pov : 0.f);
+  const float y_o = fmaf(sc, ysl_o, a_oo) - wave_sum(tcorr);
+  const double pvw = wave_sum(tpvw);
+  const double vav = (double)a_oo + 2.0 * scal * (double)ysl_o + scal * scal * qsum;
+  const float alpha2 = tv == 0.0 ? 0.f : (float)(-0.5 * (double)tf * (double)tf * (vav - 2.0 * pvw));
+  float vr = 0.f, w = 0.f;
   if (r < n) {
-    const float vr = (r == o) ? 1.f : (tv == 0.0 ? 0.f : sc * x_r);
-    float y = sc * ysl + a_o;
+    vr = (r == o) ? 1.f : (tv == 0.0 ? 0.f : sc * x_r);
+    float y = fmaf(sc, ysl, a_o);
 #pragma unroll
     for (int p = 0; p < 32; ++p)
-      if (p < j) y -= vrow[p] * pw[p] + wrow[p] * pv[p];
+      if (p < j) y -= fmaf(vrow[p], fmaf(sc, pw[p], cw[p]), wrow[p] * fmaf(sc, pv[p], cv[p]));
+    if (r == o) y = y_o;                          // row o: the value every workgroup uses
     const float wp = (tv == 0.0) ? 0.f : tf * y;
-    M.wpre[r] = wp;
+    w = fmaf(alpha2, vr, wp);
     V[(int64_t)j * n + r] = vr;
     Qv[(int64_t)j * n + r] = vr;
     M.A[(int64_t)r * n + i] = vr;                 // reflector kept for the back-transformation
-    dot = (double)wp * (double)vr;
+    W[(int64_t)j * n + r] = w;
+    M.Q[(int64_t)j * n + r] = w;
   }
-  dot = wave_sum(dot);
-  if (lane == 0) red[wave] = dot;
+  if (blockIdx.x == 0 && tid == 0) { M.d[i] = scur[1]; M.e[i] = beta; M.tau[i] = (float)tv; }
+  if (!more) return;
+
+  // column o = i + 1: x[r] = A[o][r] - sum_{p <= j} (V[p][r] W[p][o] + W[p][r] V[p][o]), r >= o,
+  // with V[j][o] = 1 and W[j][o] = tau y[o] + alpha2
+  const int jp = j + 1;
+  const float cw_j = fmaf(alpha2, 1.f, tv == 0.0 ? 0.f : tf * y_o);
+  float xtail = 0.f;
+  if (r < n) {
+    float x = a_o;
+#pragma unroll
+    for (int p = 0; p < 32; ++p)
+      if (p < j) x -= fmaf(vrow[p], cw[p], wrow[p] * cv[p]);
+    x -= fmaf(vr, cw_j, w);
+    if (r == o) snext[1] = x;
+    if (r == o + 1) snext[0] = x;
+    xtail = (r > o + 1) ? x : 0.f;
+    M.xt[r] = xtail;
+  }
+  // partials over this block's rows of the next column's sigma = x_tail^T x_tail and of
+  // W_p^T x_tail, V_p^T x_tail (p <= j), in that order
+  __shared__ float prod[2 * 32 + 1][RB];
+  const int nk = 2 * jp + 1;
+  prod[0][tid] = xtail * xtail;
+#pragma unroll
+  for (int p = 0; p < 32; ++p)
+    if (p < jp) {
+      const float vp = p == j ? vr : vrow[p], wq = p == j ? w : wrow[p];
+      prod[1 + p][tid] = wq * xtail;
+      prod[1 + jp + p][tid] = vp * xtail;
+    }
   __syncthreads();
-  if (tid == 0) {
-    double s = 0.0;
-    for (int w = 0; w < RB / 64; ++w) s += red[w];
-    M.wpart[blockIdx.x] = (float)s;
-    if (blockIdx.x == 0) { M.d[i] = M.sc[1]; M.e[i] = beta; M.tau[i] = (float)tv; }
+  if (tid < nk) {
+    // four interleaved partial sums, combined in a fixed order
+    float s4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+    for (int t = 0; t < RB; t += 4)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) s4[q] += prod[tid][t + q];
+    dnext[(int64_t)blockIdx.x * dstride + tid] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
   }
 }
-
 __global__ void __launch_bounds__(256) k_symv_tiles(SytrdArgs a, int i) {
   // odd columns walk the matrices and tiles in reverse, so a pass starts on the data the
   // previous pass touched last (still cache-resident when the matrices exceed the caches)
@@ -182,8 +271,9 @@ __global__ void __launch_bounds__(256) k_symv_tiles(SytrdArgs a, int i) {
   const int n = a.n, o = i + 1;
   const int base = o & ~31, Lb = n - base;
   const MatView M = view(a, mat);
+  const int tile = rev ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
   int I, J;
-  tri_decode(rev ? gridDim.x - 1 - blockIdx.x : blockIdx.x, I, J);
+  tri_decode(tile, I, J);
   const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4, lane = tid & 63, wave = tid >> 6;
   const int r0 = I * TB + ty * 8;                             // relative to base
   // column of register c (relative to base): two runs of four
@@ -259,11 +349,26 @@ __global__ void __launch_bounds__(256) k_symv_tiles(SytrdArgs a, int i) {
   // column sums: reduce over ty (lanes 16 apart in a wave, then the four waves)
   __shared__ float csh[4][TB];
   __shared__ float rsh[TB];
+  __shared__ float qsh[4];
 #pragma unroll
   for (int c = 0; c < 8; ++c) {
     float v = cs[c];
     v += __shfl_xor(v, 16, 64); v += __shfl_xor(v, 32, 64);
     cs[c] = v;
+  }
+  {
+    // this wave's term of x_tail^T A22 x_tail: its 32 rows' sums and its column partials
+    float qc = 0.f;
+    if (tx == 0) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) qc = fmaf(xr[k], rs[k], qc);
+    }
+    if (lane < 16) {
+#pragma unroll
+      for (int c = 0; c < 8; ++c) qc = fmaf(xc[c], cs[c], qc);
+    }
+    qc = wave_sum(qc);
+    if (lane == 0) qsh[wave] = qc;
   }
   if (lane < 16) {
 #pragma unroll
@@ -275,6 +380,7 @@ __global__ void __launch_bounds__(256) k_symv_tiles(SytrdArgs a, int i) {
   }
   __syncthreads();
   float *part = M.part;
+  if (tid == 0) M.qpart[tile] = (qsh[0] + qsh[1]) + (qsh[2] + qsh[3]);
   if (tid < TB) {
     const float colsum = csh[0][tid] + csh[1][tid] + csh[2][tid] + csh[3][tid];
     const int rr = I * TB + tid, cc = J * TB + tid;
@@ -287,106 +393,34 @@ __global__ void __launch_bounds__(256) k_symv_tiles(SytrdArgs a, int i) {
   }
 }
 
-__global__ void __launch_bounds__(RB) k_col_next(SytrdArgs a, int i, int j, int ip, int jp,
-                                                 int prep_only, int jbw) {
+// First column k0 of a panel (no reflector of the panel applies yet): x = A[k0][r] for
+// r >= k0, its scalars and the block partials of its sigma, into the buffers of column k0's
+// parity.
+__global__ void __launch_bounds__(RB) k_col_first(SytrdArgs a, int k0) {
   const int mat = blockIdx.y, n = a.n;
   const MatView M = view(a, mat);
-  float *V = M.P, *W = M.P + (int64_t)jbw * n;
-  __shared__ float cw[64], cv[64];
-  __shared__ float alpha2_s;
+  const int64_t dstride = 2 * a.nb + 1;
+  float *dnext = M.dpart + (k0 & 1) * (int64_t)a.slots * dstride;
+  float *snext = M.sc + 2 * (k0 & 1);
   const int tid = threadIdx.x;
-  // rows from ip (= i + 1 = o of column i unless prep_only) in blocks of 128, one per thread
-  const int r = (prep_only ? ip : i + 1) + blockIdx.x * RB + tid;
-  const int rr = r < n ? r : n - 1;             // in-range row for the loads
-  const bool next = ip < n - 1;
-  // Every load that does not need alpha2 is issued before any is used and without a branch
-  // (panel rows p < j of V and W at this row and at row ip, row ip of A, what rebuilds w_j
-  // and the block partials of w^T v): entries past the live range read an entry this
-  // launch does not write and are masked afterwards.
-  const int ipc = min(ip, n - 1);
-  // row g of W is not written by this launch (it writes row j only, and none in prep_only)
-  const int g = j == 0 ? 1 : 0;
-  float vrow[32], wrow[32];
-#pragma unroll
-  for (int p = 0; p < 32; ++p) {
-    const bool ld = p < jp && (prep_only || p < j);
-    vrow[p] = V[(int64_t)(ld ? p : 0) * n + rr];
-    wrow[p] = W[(int64_t)(ld ? p : g) * n + rr];
-  }
-  float a_ip = M.A[(int64_t)ipc * n + rr];
-  const bool ldc = tid < jp, ldw = ldc && (prep_only || tid < j);
-  float cv_t = V[(int64_t)(ldc ? tid : 0) * n + ipc];
-  float cw_t = W[(int64_t)(ldw ? tid : g) * n + ipc];
-  float wpre_r = 0.f, vj_r = 0.f, wpre_ip = 0.f, vj_ip = 0.f, tau_i = 0.f, tw[32];
-  const int nblk = (n - (i + 1) + RB - 1) / RB;   // row blocks of column i's k_col_finish
-  if (!prep_only) {
-    wpre_r = M.wpre[rr];
-    vj_r = V[(int64_t)j * n + rr];
-    wpre_ip = M.wpre[ipc];
-    vj_ip = V[(int64_t)j * n + ipc];
-    tau_i = M.tau[i];
-#pragma unroll
-    for (int b = 0; b < 32; ++b) tw[b] = M.wpart[min(b, nblk - 1)];
-  }
-#pragma unroll
-  for (int p = 0; p < 32; ++p)
-    if (!(next && p < jp && (prep_only || p < j))) { vrow[p] = 0.f; wrow[p] = 0.f; }
-  if (!next) a_ip = 0.f;
-  if (!(next && ldc)) cv_t = 0.f;
-  if (!(next && ldw)) cw_t = 0.f;
-  float alpha2 = 0.f, w = 0.f;
-  if (!prep_only) {
-    vrow[j] = vj_r;
-    if (tid == 0) {
-      double sw = 0.0;
-#pragma unroll
-      for (int b = 0; b < 32; ++b) sw += b < nblk ? (double)tw[b] : 0.0;
-      for (int b = 32; b < nblk; ++b) sw += (double)M.wpart[b];
-      alpha2_s = (float)(-0.5 * (double)tau_i * sw);
-    }
-    __syncthreads();
-    alpha2 = alpha2_s;
-    w = wpre_r + alpha2 * vj_r;
-    wrow[j] = w;
-    if (r < n) {
-      W[(int64_t)j * n + r] = w;
-      M.Q[(int64_t)j * n + r] = w;
-    }
-    if (!next) return;
-    // reflector j's w[ip] is rebuilt here because another workgroup of this launch writes it
-    if (tid == j) cw_t = wpre_ip + alpha2 * vj_ip;
-  }
-  if (tid < jp) { cw[tid] = cw_t; cv[tid] = cv_t; }
-  __syncthreads();
-  // x[r] = A[ip][r] - sum_p (V[p][r] W[p][ip] + W[p][r] V[p][ip]) for r >= ip (row ip = column ip)
+  const int r = k0 + blockIdx.x * RB + tid;
   float xtail = 0.f;
   if (r < n) {
-    float x = a_ip;
-#pragma unroll
-    for (int p = 0; p < 32; ++p)
-      if (p < jp) x -= vrow[p] * cw[p] + wrow[p] * cv[p];
-    if (r == ip) M.sc[1] = x;
-    if (r == ip + 1) M.sc[0] = x;
-    xtail = (r > ip + 1) ? x : 0.f;
+    const float x = M.A[(int64_t)k0 * n + r];
+    if (r == k0) snext[1] = x;
+    if (r == k0 + 1) snext[0] = x;
+    xtail = (r > k0 + 1) ? x : 0.f;
     M.xt[r] = xtail;
   }
-  // partials over this block's rows of the next column's sigma = x_tail^T x_tail and of
-  // W_p^T x_tail, V_p^T x_tail (p < jp), in that order; summed over blocks by k_col_finish
-  __shared__ float prod[2 * 32 + 1][RB];
-  const int nk = 2 * jp + 1;
-  prod[0][tid] = xtail * xtail;
-#pragma unroll
-  for (int p = 0; p < 32; ++p)
-    if (p < jp) { prod[1 + p][tid] = wrow[p] * xtail; prod[1 + jp + p][tid] = vrow[p] * xtail; }
+  __shared__ float prod[RB];
+  prod[tid] = xtail * xtail;
   __syncthreads();
-  if (tid < nk) {
-    // four interleaved partial sums, combined in a fixed order
+  if (tid == 0) {
     float s4[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 8
     for (int t = 0; t < RB; t += 4)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) s4[q] += prod[tid][t + q];
-    M.dpart[(int64_t)blockIdx.x * (2 * a.nb + 1) + tid] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
+      for (int q = 0; q < 4; ++q) s4[q] += prod[t + q];
+    dnext[(int64_t)blockIdx.x * dstride] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
   }
 }
 
@@ -437,7 +471,7 @@ __global__ void k_reflector_clean(SytrdArgs a) {
 
 size_t per_mat_floats(int n, int nb) {
   const size_t slots = (n + TB - 1) / TB;
-  return 4 * (size_t)nb * n + 2 * (size_t)n + slots * n + slots * (2 * nb + 1) + slots + 64;
+  return 4 * (size_t)nb * n + (size_t)n + slots * n + 2 * slots * (2 * nb + 1) + slots * (slots + 1) / 2 + 64;
 }
 
 }  // namespace
@@ -480,7 +514,8 @@ hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, const Gemm
   if (m1 < 0) m1 = b.n_mat;
   const int nm = m1 - m0;
   if (nm <= 0 || m0 < 0 || m1 > b.n_mat) return hipErrorInvalidValue;
-  if (nb > 32) return hipErrorInvalidValue;     // k_col_next's partial buffer holds 2 nb + 1 dots
+  if (nb > 32) return hipErrorInvalidValue;     // k_col_step holds the 2 nb + 1 dots of a block
+  if (n > TRD_MAX_N) return hipErrorInvalidValue;
   const int64_t wstride = (int64_t)((per_mat_floats(n, nb) + 63) / 64 * 64);
   SytrdArgs a{};
   a.A = b.A + (int64_t)m0 * b.mat_stride; a.mat_stride = b.mat_stride; a.n = n; a.nb = nb;
@@ -495,14 +530,12 @@ hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, const Gemm
   hipLaunchKernelGGL(k_mirror_strip, dim3((n + 63) / 64, nm), dim3(256), 0, st, a, 0);
   for (int p = 0; p < panels; ++p) {
     const int k0 = p * nb, jb = std::min(nb, n - 1 - k0);
-    hipLaunchKernelGGL(k_col_next, dim3((n - k0 + RB - 1) / RB, nm), dim3(RB), 0, st, a, -1, 0, k0, 0, 1, jb);
+    hipLaunchKernelGGL(k_col_first, dim3((n - k0 + RB - 1) / RB, nm), dim3(RB), 0, st, a, k0);
     for (int j = 0; j < jb; ++j) {
       const int i = k0 + j, o = i + 1, L = n - o;
       const int nt = (n - (o & ~31) + TB - 1) / TB, nblk = (L + RB - 1) / RB;
       hipLaunchKernelGGL(k_symv_tiles, dim3(nt * (nt + 1) / 2, nm), dim3(256), 0, st, a, i);
-      hipLaunchKernelGGL(k_col_finish, dim3(nblk, nm), dim3(RB), 0, st, a, i, j, jb);
-      const bool more = j + 1 < jb;
-      hipLaunchKernelGGL(k_col_next, dim3(nblk, nm), dim3(RB), 0, st, a, i, j, more ? i + 1 : n, j + 1, 0, jb);
+      hipLaunchKernelGGL(k_col_step, dim3(nblk, nm), dim3(RB), 0, st, a, i, j, jb, j + 1 < jb ? 1 : 0);
     }
     const int s = k0 + jb;
     if (s < n) {
