@@ -243,6 +243,83 @@ JOLT_DEV bool decode(const Grid &g, int j, int &z, int &tm, int &tn) {
   return true;
 }
 
+// Epilogue of a BM x BN tile through LDS (cs, at least 32 (BN + 4) floats; every wave has
+// finished with the operand buffers when it is called), 32 rows per round:
+// acc[a][b][q] is the output at row wm*(BM/2) + a*32 + 8*(q/4) + 4*lh + q%4, column
+// wn*(BN/2) + b*32 + lr of the tile.
+template <int BM, int BN>
+JOLT_DEV void store_tile(const GemmProblem &P, f32x16_t (&acc)[BM / 64][BN / 64], float *cs, int m0, int n0) {
+  constexpr int MI = BM / 64, NI = BN / 64;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1, lr = lane & 31, lh = lane >> 5;
+  // alpha 2^e is applied as ldexp(alpha * acc, e): 2^e alone may lie outside fp32's range
+  const float alpha = P.alpha;
+  const int aexp = P.alpha_exp2 ? (int)*gptr(P.alpha_exp2) : 0;
+  constexpr int CLD = BN + 4;
+  const bool use_beta = P.beta != 0.f;
+  const bool ct = P.c_trans != 0;   // store the transpose: C[col * ldc + row]
+  const bool vec = ((reinterpret_cast<uintptr_t>(P.C) & 15) == 0) && (P.ldc % 4 == 0);
+#pragma unroll
+  for (int h = 0; h < BM / 32; ++h) {
+    __syncthreads();
+    if (wm == h / MI) {
+      const int a = h % MI;
+#pragma unroll
+      for (int b = 0; b < NI; ++b)
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+          cs[(8 * (q >> 2) + 4 * lh + (q & 3)) * CLD + wn * (BN / 2) + b * 32 + lr] = acc[a][b][q];
+    }
+    __syncthreads();
+    // 32 rows x BN columns in runs of 4 (along the row, or along the column for C^T)
+#pragma unroll
+    for (int u = 0; u < 8 * BN / NT; ++u) {
+      const int idx = tid + u * NT;
+      int rr, cc;
+      if (ct) { cc = idx >> 3; rr = (idx & 7) * 4; }
+      else { rr = idx / (BN / 4); cc = (idx % (BN / 4)) * 4; }
+      const int row = m0 + h * 32 + rr, col = n0 + cc;
+      if (ct) {
+        if (col >= P.N || row >= P.M) continue;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = ldexpf(alpha * cs[(rr + e) * CLD + cc], aexp);
+        JOLT_GLOBAL float *dst = gptr(P.C + (int64_t)col * P.ldc + row);
+        if (vec && row + 4 <= P.M) {
+          if (use_beta) {
+            const jf4 o4 = *reinterpret_cast<const JOLT_GLOBAL jf4 *>(dst);
+            v[0] = fmaf(P.beta, o4.x, v[0]); v[1] = fmaf(P.beta, o4.y, v[1]);
+            v[2] = fmaf(P.beta, o4.z, v[2]); v[3] = fmaf(P.beta, o4.w, v[3]);
+          }
+          *reinterpret_cast<JOLT_GLOBAL jf4 *>(dst) = jf4{v[0], v[1], v[2], v[3]};
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (row + e < P.M) dst[e] = use_beta ? fmaf(P.beta, dst[e], v[e]) : v[e];
+        }
+      } else {
+        if (row >= P.M || col >= P.N) continue;
+        const float4 a4 = *reinterpret_cast<const float4 *>(&cs[rr * CLD + cc]);
+        float v[4] = {ldexpf(alpha * a4.x, aexp), ldexpf(alpha * a4.y, aexp), ldexpf(alpha * a4.z, aexp),
+                     ldexpf(alpha * a4.w, aexp)};
+        JOLT_GLOBAL float *dst = gptr(P.C + (int64_t)row * P.ldc + col);
+        if (vec && col + 4 <= P.N) {
+          if (use_beta) {
+            const jf4 o4 = *reinterpret_cast<const JOLT_GLOBAL jf4 *>(dst);
+            v[0] = fmaf(P.beta, o4.x, v[0]); v[1] = fmaf(P.beta, o4.y, v[1]);
+            v[2] = fmaf(P.beta, o4.z, v[2]); v[3] = fmaf(P.beta, o4.w, v[3]);
+          }
+          *reinterpret_cast<JOLT_GLOBAL jf4 *>(dst) = jf4{v[0], v[1], v[2], v[3]};
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (col + e < P.N) dst[e] = use_beta ? fmaf(P.beta, dst[e], v[e]) : v[e];
+        }
+      }
+    }
+  }
+}
+
 // BM x BN tile per 256-thread workgroup; waves in a 2 x 2 grid, each (BM/2) x (BN/2).
 template <int BM, int BN, bool AK, bool BK_, bool AS, bool BS>
 __global__ void __launch_bounds__(NT) k_gemm16(const GemmProblem *__restrict__ probs, Grid g) {
@@ -357,76 +434,124 @@ __global__ void __launch_bounds__(NT) k_gemm16(const GemmProblem *__restrict__ p
     compute_at(0);
   }
 
-  // alpha 2^e is applied as ldexp(alpha * acc, e): 2^e alone may lie outside fp32's range
-  const float alpha = P.alpha;
-  const int aexp = P.alpha_exp2 ? (int)*gptr(P.alpha_exp2) : 0;
-  // epilogue through LDS, 32 rows per round: acc[a][b][q] is the output at row
-  // wm*(BM/2) + a*32 + 8*(q/4) + 4*lh + q%4, column wn*(BN/2) + b*32 + lr of the tile
-  float *cs = reinterpret_cast<float *>(&sm);
-  constexpr int CLD = BN + 4;
-  static_assert(32 * CLD * sizeof(float) <= sizeof(Lds<BM, BN, AS, BS>), "epilogue tile exceeds LDS");
-  const bool use_beta = P.beta != 0.f;
-  const bool ct = P.c_trans != 0;   // store the transpose: C[col * ldc + row]
-  const bool vec = ((reinterpret_cast<uintptr_t>(P.C) & 15) == 0) && (P.ldc % 4 == 0);
+  static_assert(32 * (BN + 4) * sizeof(float) <= sizeof(Lds<BM, BN, AS, BS>), "epilogue tile exceeds LDS");
+  store_tile<BM, BN>(P, acc, reinterpret_cast<float *>(&sm), m0, n0);
+}
+
+// 256 x 256 tiles for bf16 x bf16 products whose operands are both k-contiguous and whose
+// K is a multiple of 64 (the token Gram of wide cells).  Operand tiles go from global
+// memory straight into LDS (global_load_lds_dwordx4: the 16 bytes of lane L land at the
+// instruction's LDS base + 16 L), so no registers hold them on the way and no vector work
+// repacks them.  An LDS row is one tile row's 64 k (128 bytes, unpadded) with its 16-byte
+// chunks permuted by row (chunk c of row r at position c ^ f(r), f(r) = (r & 7) ^ ((r >> 3)
+// & 1)), so that the fragment reads of any 8 consecutive rows, and of the even and of the odd
+// rows among 16, fall in distinct banks; lane L of a load instruction therefore fetches chunk
+// (L % 8) ^ f(r) of row r = (its 8-row group) + L / 8.  Two buffers: tile
+// k + 1 streams in while tile k is multiplied; the fragments of the next 16-wide k step
+// are read while the current one is multiplied.
+constexpr int SQ = 256, SQ_ROWB = BK * 2;             // tile rows, bytes per LDS row
+struct SqLds {
+  uint8_t a[2][SQ * SQ_ROWB], b[2][SQ * SQ_ROWB];     // 128 KB
+};
+
+JOLT_DEV void lds_dma16(const void *src, uint8_t *lds_row_base) {
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
+                                   (__attribute__((address_space(3))) void *)lds_row_base, 16, 0, 0);
+}
+
+__global__ void __launch_bounds__(NT) k_gemm16_sq(const GemmProblem *__restrict__ probs, Grid g) {
+  const int i = blockIdx.x, j = (i & 7) * g.per_xcd + (i >> 3);
+  int z, tm, tn;
+  if (!decode(g, j, z, tm, tn)) return;
+  const GemmProblem P = probs[z];
+  if (tm * SQ >= P.M || tn * SQ >= P.N) return;
+  constexpr int MI = 4, NI = 4, NQ = SQ / 8 / 4;      // load instructions per wave and operand
+  __shared__ __attribute__((aligned(16))) SqLds sm;
+  static_assert(32 * (SQ + 4) * sizeof(float) <= sizeof(SqLds), "epilogue tile exceeds LDS");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1, lr = lane & 31, lh = lane >> 5;
+  const int m0 = tm * SQ, n0 = tn * SQ;
+
+  f32x16_t acc[MI][NI];
 #pragma unroll
-  for (int h = 0; h < BM / 32; ++h) {
-    __syncthreads();
-    if (wm == h / MI) {
-      const int a = h % MI;
+  for (int a = 0; a < MI; ++a)
 #pragma unroll
-      for (int b = 0; b < NI; ++b)
+    for (int b = 0; b < NI; ++b)
 #pragma unroll
-        for (int q = 0; q < 16; ++q)
-          cs[(8 * (q >> 2) + 4 * lh + (q & 3)) * CLD + wn * (BN / 2) + b * 32 + lr] = acc[a][b][q];
+      for (int q = 0; q < 16; ++q) acc[a][b][q] = 0.f;
+
+  // byte offsets of this lane's chunk in instruction q (rows past the extent read row 0 of
+  // the operand and only feed outputs the epilogue does not store)
+  uint32_t offa[NQ], offb[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int r = 8 * (NQ * wave + q) + (lane >> 3), c = (lane & 7) ^ (r & 7) ^ ((r >> 3) & 1);
+    const int ra = m0 + r, rb = n0 + r;
+    offa[q] = 2u * (uint32_t)((ra < P.M ? ra : 0) * P.A.ld + 8 * c);
+    offb[q] = 2u * (uint32_t)((rb < P.N ? rb : 0) * P.B.ld + 8 * c);
+  }
+  auto dma = [&](int buf, int k0) {
+    const char *pa = reinterpret_cast<const char *>(P.A.ptr) + 2 * operand_col(P.A, k0);
+    const char *pb = reinterpret_cast<const char *>(P.B.ptr) + 2 * operand_col(P.B, k0);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      lds_dma16(pa + offa[q], sm.a[buf] + 8 * (NQ * wave + q) * SQ_ROWB);
+      lds_dma16(pb + offb[q], sm.b[buf] + 8 * (NQ * wave + q) * SQ_ROWB);
     }
-    __syncthreads();
-    // 32 rows x BN columns in runs of 4 (along the row, or along the column for C^T)
+  };
+  const int nk = P.K / BK, x = (lr & 7) ^ ((lr >> 3) & 1);
+  bf16x8_t fa[2][MI], fb[2][NI];
+  const uint8_t *la = sm.a[0], *lb = sm.b[0];
+  auto frag = [&](int s, int set) {
+    const int ch = ((2 * s + lh) ^ x) * 16;
 #pragma unroll
-    for (int u = 0; u < 8 * BN / NT; ++u) {
-      const int idx = tid + u * NT;
-      int rr, cc;
-      if (ct) { cc = idx >> 3; rr = (idx & 7) * 4; }
-      else { rr = idx / (BN / 4); cc = (idx % (BN / 4)) * 4; }
-      const int row = m0 + h * 32 + rr, col = n0 + cc;
-      if (ct) {
-        if (col >= P.N || row >= P.M) continue;
-        float v[4];
+    for (int a = 0; a < MI; ++a) fa[set][a] = *reinterpret_cast<const bf16x8_t *>(la + a * 32 * SQ_ROWB + ch);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = ldexpf(alpha * cs[(rr + e) * CLD + cc], aexp);
-        JOLT_GLOBAL float *dst = gptr(P.C + (int64_t)col * P.ldc + row);
-        if (vec && row + 4 <= P.M) {
-          if (use_beta) {
-            const jf4 o4 = *reinterpret_cast<const JOLT_GLOBAL jf4 *>(dst);
-            v[0] = fmaf(P.beta, o4.x, v[0]); v[1] = fmaf(P.beta, o4.y, v[1]);
-            v[2] = fmaf(P.beta, o4.z, v[2]); v[3] = fmaf(P.beta, o4.w, v[3]);
-          }
-          *reinterpret_cast<JOLT_GLOBAL jf4 *>(dst) = jf4{v[0], v[1], v[2], v[3]};
-        } else {
+    for (int b = 0; b < NI; ++b) fb[set][b] = *reinterpret_cast<const bf16x8_t *>(lb + b * 32 * SQ_ROWB + ch);
+  };
+  auto frag0 = [&](int buf) {
+    la = sm.a[buf] + (wm * (SQ / 2) + lr) * SQ_ROWB;
+    lb = sm.b[buf] + (wn * (SQ / 2) + lr) * SQ_ROWB;
+    frag(0, 0);
+  };
+  auto compute = [&](int buf) {
+    (void)buf;
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (row + e < P.M) dst[e] = use_beta ? fmaf(P.beta, dst[e], v[e]) : v[e];
-        }
-      } else {
-        if (row >= P.M || col >= P.N) continue;
-        const float4 a4 = *reinterpret_cast<const float4 *>(&cs[rr * CLD + cc]);
-        float v[4] = {ldexpf(alpha * a4.x, aexp), ldexpf(alpha * a4.y, aexp), ldexpf(alpha * a4.z, aexp),
-                     ldexpf(alpha * a4.w, aexp)};
-        JOLT_GLOBAL float *dst = gptr(P.C + (int64_t)row * P.ldc + col);
-        if (vec && col + 4 <= P.N) {
-          if (use_beta) {
-            const jf4 o4 = *reinterpret_cast<const JOLT_GLOBAL jf4 *>(dst);
-            v[0] = fmaf(P.beta, o4.x, v[0]); v[1] = fmaf(P.beta, o4.y, v[1]);
-            v[2] = fmaf(P.beta, o4.z, v[2]); v[3] = fmaf(P.beta, o4.w, v[3]);
-          }
-          *reinterpret_cast<JOLT_GLOBAL jf4 *>(dst) = jf4{v[0], v[1], v[2], v[3]};
-        } else {
+    for (int s = 0; s < BK / 16; ++s) {
+      // the next step's 8 fragment reads go out between this step's 16 products, one after
+      // every second product (scheduling groups; the barriers keep each step's region apart)
+      if (s + 1 < BK / 16) frag(s + 1, (s + 1) & 1);
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (col + e < P.N) dst[e] = use_beta ? fmaf(P.beta, dst[e], v[e]) : v[e];
+      for (int a = 0; a < MI; ++a)
+#pragma unroll
+        for (int b = 0; b < NI; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s & 1][a], fb[s & 1][b], acc[a][b], 0, 0, 0);
+      if (s + 1 < BK / 16) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
+  };
+  if (nk > 0) dma(0, 0);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    // this wave's loads of tile kt have landed; the barrier then covers every wave's, and
+    // every wave has finished reading the other buffer (tile kt - 1)
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    // the first step's fragment reads go out before the next tile's loads are issued
+    frag0(cur);
+    __builtin_amdgcn_sched_barrier(0);
+    if (kt + 1 < nk) dma(cur ^ 1, (kt + 1) * BK);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(cur);
   }
+  __syncthreads();
+  store_tile<SQ, SQ>(P, acc, reinterpret_cast<float *>(&sm), m0, n0);
 }
 
 template <int BM, bool AS, bool BS>
@@ -517,7 +642,9 @@ bool gemm16_prepare(GemmProblem *probs, int n, int &ta, int &tb, bool &ak, bool 
   // then runs two workgroups per CU; at K = 4096 the 128-row tiles also keep two
   // workgroups per CU busy and measured faster)
   const bool bf_both = ta == GT_BF16 && tb == GT_BF16 && ak && bk;
-  if (lower && bf_both && maxM >= 2048 && minK >= 16384) bm = GEMM16_SQUARE256;
+  bool k64 = true;
+  for (int i = 0; i < n; ++i) k64 = k64 && probs[i].K % BK == 0;
+  if (lower && bf_both && k64 && maxM >= 2048 && minK >= 16384) bm = GEMM16_SQUARE256;
   else bm = (tb == GT_F32 && ta == GT_BF16 && maxM >= 2048 && !lower && ak) ? 256 : 128;
   return true;
 }
@@ -548,8 +675,7 @@ hipError_t launch_gemm16(const GemmProblem *probs_dev, int n_probs, int max_M, i
   if (square) {
     // 256 x 256 tiles, bf16 x bf16 with both operands k-contiguous only
     if (as || bs || !a_kcontig || !b_kcontig) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_gemm16<256, 256, true, true, false, false>), dim3(g.per_xcd * 8), dim3(NT), 0, st,
-                       probs_dev, g);
+    hipLaunchKernelGGL(k_gemm16_sq, dim3(g.per_xcd * 8), dim3(NT), 0, st, probs_dev, g);
     return hipGetLastError();
   }
   if (bm == 256) {
