@@ -554,6 +554,182 @@ __global__ void __launch_bounds__(NT) k_gemm16_sq(const GemmProblem *__restrict_
   store_tile<SQ, SQ>(P, acc, reinterpret_cast<float *>(&sm), m0, n0);
 }
 
+// C = C + alpha A B for fp32 A (M x K) and B (K x N) stored mn-contiguous (the operands'
+// rows run along M and N), K <= 64, lower tiles only: the rank-2k update of the blocked
+// tridiagonalisation (A = [V W]^T, B = [W V]).  It runs on the bf16 matrix cores with each
+// operand element split into three bf16 terms, x = h + m + l (h = bf16(x), m = bf16(x - h),
+// l = bf16(x - h - m), so |x - h - m - l| <= 2^-27 |x|), keeping the six products of order
+// at most 2^-18 (hh, hm, mh, hl, mm, lh): what is dropped stays below 2^-25 of each product,
+// under fp32's own rounding of it.  128 x 128 tiles; K in halves of 32 through LDS (three
+// planes per operand, k-contiguous rows of 32 + 8: 61 KB, two workgroups per CU), all
+// operand loads issued at once; the epilogue requests the whole C tile before its first
+// round.
+constexpr int U3_BM = 128, U3_KH = 32, U3_LDK = U3_KH + 8;
+struct U3Lds {
+  uint16_t a[3][U3_BM * U3_LDK], b[3][U3_BM * U3_LDK];   // 61.4 KB
+};
+
+JOLT_DEV void split3_bf16(float x, uint16_t &h, uint16_t &m, uint16_t &l) {
+  h = f32_to_bf16(x);
+  const float r1 = x - bf16_to_f32(h);                   // exact
+  m = f32_to_bf16(r1);
+  l = f32_to_bf16(r1 - bf16_to_f32(m));                  // exact difference, rounded once
+}
+
+// the thread's 4 (k) x 8 (mn) block of an mn-contiguous operand, zero outside K x MN
+JOLT_DEV void load_block_mn(const GemmOperand &op, int k0, int mn0, int K, int MN, bool vec, float (&v)[4][8]) {
+  const float *base = reinterpret_cast<const float *>(op.ptr);
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    const int k = k0 + kk;
+    if (vec && k < K && mn0 + 8 <= MN) {
+      const float *p = base + (int64_t)k * op.ld + mn0;
+      const jf4 x0 = gload_f4(p), x1 = gload_f4(p + 4);
+      v[kk][0] = x0.x; v[kk][1] = x0.y; v[kk][2] = x0.z; v[kk][3] = x0.w;
+      v[kk][4] = x1.x; v[kk][5] = x1.y; v[kk][6] = x1.z; v[kk][7] = x1.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        v[kk][e] = (k < K && mn0 + e < MN) ? gptr(base)[(int64_t)k * op.ld + mn0 + e] : 0.f;
+    }
+  }
+}
+
+JOLT_DEV void stash3(const float (&v)[4][8], uint16_t *p0, uint16_t *p1, uint16_t *p2, int mn, int kb) {
+  // kb: the block's first k within the LDS half
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    uint16_t h[4], m[4], l[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) split3_bf16(v[kk][e], h[kk], m[kk], l[kk]);
+    const int o = (mn + e) * U3_LDK + kb;
+    *reinterpret_cast<uint2 *>(p0 + o) = make_uint2(pk(h[0], h[1]), pk(h[2], h[3]));
+    *reinterpret_cast<uint2 *>(p1 + o) = make_uint2(pk(m[0], m[1]), pk(m[2], m[3]));
+    *reinterpret_cast<uint2 *>(p2 + o) = make_uint2(pk(l[0], l[1]), pk(l[2], l[3]));
+  }
+}
+
+__global__ void __launch_bounds__(NT, 2) k_update3(const GemmProblem *__restrict__ probs, Grid g) {
+  const int i = blockIdx.x, j = (i & 7) * g.per_xcd + (i >> 3);
+  int z, tm, tn;
+  if (!decode(g, j, z, tm, tn)) return;
+  const GemmProblem P = probs[z];
+  if (tm * U3_BM >= P.M || tn * U3_BM >= P.N) return;
+  __shared__ __attribute__((aligned(16))) U3Lds sm;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1, lr = lane & 31, lh = lane >> 5;
+  const int m0 = tm * U3_BM, n0 = tn * U3_BM, K = P.K;
+
+  // operands: 4 (k) x 8 (mn) per thread, k = 4 (tid % 16) .., mn = 8 (tid / 16) ..
+  const int kb = 4 * (tid & 15), mb = 8 * (tid >> 4);
+  const bool avec = ((reinterpret_cast<uintptr_t>(P.A.ptr) & 15) == 0) && (P.A.ld % 4 == 0);
+  const bool bvec = ((reinterpret_cast<uintptr_t>(P.B.ptr) & 15) == 0) && (P.B.ld % 4 == 0);
+  float va[4][8], vb[4][8];
+  load_block_mn(P.A, kb, m0 + mb, K, P.M, avec, va);
+  load_block_mn(P.B, kb, n0 + mb, K, P.N, bvec, vb);
+
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[a][b][q] = 0.f;
+  const int ks = (K + 15) / 16;
+#pragma unroll
+  for (int s = 0; s < BK / 16; ++s) {
+    if (s >= ks) break;
+    if ((s & 1) == 0) {
+      // k half s / 2 to LDS (the threads whose block lies in it)
+      if (s) __syncthreads();
+      if ((kb >= U3_KH) == (s >= 2)) {
+        stash3(va, sm.a[0], sm.a[1], sm.a[2], mb, kb % U3_KH);
+        stash3(vb, sm.b[0], sm.b[1], sm.b[2], mb, kb % U3_KH);
+      }
+      __syncthreads();
+    }
+    const int ko = (s & 1) * 16 + 8 * lh;
+    bf16x8_t fa[3][2], fb[3][2];
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+#pragma unroll
+      for (int a = 0; a < 2; ++a) {
+        fa[t][a] = *reinterpret_cast<const bf16x8_t *>(sm.a[t] + (wm * 64 + a * 32 + lr) * U3_LDK + ko);
+        fb[t][a] = *reinterpret_cast<const bf16x8_t *>(sm.b[t] + (wn * 64 + a * 32 + lr) * U3_LDK + ko);
+      }
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        f32x16_t c = acc[a][b];
+        c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[2][a], fb[0][b], c, 0, 0, 0);   // l h
+        c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][a], fb[1][b], c, 0, 0, 0);   // m m
+        c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[0][a], fb[2][b], c, 0, 0, 0);   // h l
+        c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][a], fb[0][b], c, 0, 0, 0);   // m h
+        c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[0][a], fb[1][b], c, 0, 0, 0);   // h m
+        c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[0][a], fb[0][b], c, 0, 0, 0);   // h h
+        acc[a][b] = c;
+      }
+  }
+
+  // epilogue through LDS, 32 rows per round (acc[a][b][q] is the output at row
+  // wm*64 + a*32 + 8*(q/4) + 4*lh + q%4, column wn*64 + b*32 + lr of the tile)
+  // the C tile, all of it requested before the first round: round h, piece u covers row
+  // h * 32 + idx / 32, columns 4 (idx % 32) .. + 3, idx = tid + 256 u
+  const bool cvec = ((reinterpret_cast<uintptr_t>(P.C) & 15) == 0) && (P.ldc % 4 == 0);
+  jf4 cin[4][4];
+#pragma unroll
+  for (int h = 0; h < 4; ++h)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = tid + u * NT, row = m0 + h * 32 + (idx >> 5), col = n0 + (idx & 31) * 4;
+      const JOLT_GLOBAL float *src = gptr(P.C + (int64_t)row * P.ldc + col);
+      if (row < P.M && cvec && col + 4 <= P.N) {
+        cin[h][u] = *reinterpret_cast<const JOLT_GLOBAL jf4 *>(src);
+      } else {
+        float t[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) t[e] = (row < P.M && col + e < P.N) ? src[e] : 0.f;
+        cin[h][u] = jf4{t[0], t[1], t[2], t[3]};
+      }
+    }
+  float *cs = reinterpret_cast<float *>(&sm);
+  constexpr int CLD = U3_BM + 4;
+  static_assert(32 * CLD * sizeof(float) <= sizeof(U3Lds), "epilogue tile exceeds LDS");
+  const float alpha = P.alpha;
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    __syncthreads();
+    if (wm == (h >> 1)) {
+      const int a = h & 1;
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+          cs[(8 * (q >> 2) + 4 * lh + (q & 3)) * CLD + wn * 64 + b * 32 + lr] = acc[a][b][q];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = tid + u * NT, rr = idx >> 5, cc = (idx & 31) * 4;
+      const int row = m0 + h * 32 + rr, col = n0 + cc;
+      if (row >= P.M || col >= P.N) continue;
+      const float4 a4 = *reinterpret_cast<const float4 *>(&cs[rr * CLD + cc]);
+      const jf4 o4 = cin[h][u];
+      const float v[4] = {fmaf(alpha, a4.x, P.beta * o4.x), fmaf(alpha, a4.y, P.beta * o4.y),
+                          fmaf(alpha, a4.z, P.beta * o4.z), fmaf(alpha, a4.w, P.beta * o4.w)};
+      JOLT_GLOBAL float *dst = gptr(P.C + (int64_t)row * P.ldc + col);
+      if (cvec && col + 4 <= P.N) {
+        *reinterpret_cast<JOLT_GLOBAL jf4 *>(dst) = jf4{v[0], v[1], v[2], v[3]};
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (col + e < P.N) dst[e] = v[e];
+      }
+    }
+  }
+}
+
 template <int BM, bool AS, bool BS>
 hipError_t launch_bm(const GemmProblem *probs, const Grid &g, bool ak, bool bk, hipStream_t st) {
   const dim3 grid(g.per_xcd * 8);
@@ -688,4 +864,17 @@ hipError_t launch_gemm16(const GemmProblem *probs_dev, int n_probs, int max_M, i
   if (as) return launch_bm<128, true, false>(probs_dev, g, a_kcontig, b_kcontig, st);
   if (bs) return launch_bm<128, false, true>(probs_dev, g, a_kcontig, b_kcontig, st);
   return launch_bm<128, false, false>(probs_dev, g, a_kcontig, b_kcontig, st);
+}
+
+hipError_t launch_update3(const GemmProblem *probs_dev, int n_probs, int max_MN, hipStream_t st) {
+  if (n_probs <= 0 || max_MN <= 0) return hipSuccess;
+  Grid g;
+  g.tiles_m = g.tiles_n = (max_MN + U3_BM - 1) / U3_BM;
+  g.lower_only = 1;
+  g.wide = 0;
+  g.per_prob = g.tiles_m * (g.tiles_m + 1) / 2;
+  g.total = g.per_prob * n_probs;
+  g.per_xcd = (g.total + 7) / 8;
+  hipLaunchKernelGGL(k_update3, dim3(g.per_xcd * 8), dim3(NT), 0, st, probs_dev, g);
+  return hipGetLastError();
 }

@@ -539,7 +539,7 @@ hipError_t launch_sytrd_large(const EigBatch &b, float *work, int nb, const Gemm
     }
     const int s = k0 + jb;
     if (s < n) {
-      err = launch_gemm(tab_dev + (size_t)p * b.n_mat + m0, nm, n - s, n - s, 1, GT_F32, GT_F32, false, false, st);
+      err = launch_update3(tab_dev + (size_t)p * b.n_mat + m0, nm, n - s, st);
       if (err != hipSuccess) return err;
       hipLaunchKernelGGL(k_mirror_strip, dim3((n - s + 63) / 64, nm), dim3(256), 0, st, a, s);
     }

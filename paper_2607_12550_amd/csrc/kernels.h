@@ -133,6 +133,10 @@ hipError_t launch_gemm(const GemmProblem *probs_dev, int n_probs, int max_M, int
 constexpr int GEMM16_SQUARE256 = 512;
 bool gemm16_prepare(GemmProblem *probs_host, int n_probs, int &ta, int &tb, bool &a_kcontig,
                     bool &b_kcontig, int &bm);
+// C = alpha A B + beta C over the lower tiles for fp32 A, B stored mn-contiguous, K <= 64,
+// on the bf16 matrix cores with each operand split into three bf16 terms (fp32-level
+// accuracy): the rank-2k update of the blocked tridiagonalisation.
+hipError_t launch_update3(const GemmProblem *probs_dev, int n_probs, int max_MN, hipStream_t st);
 hipError_t launch_gemm16(const GemmProblem *probs_dev, int n_probs, int max_M, int max_N, int ta,
                          int tb, bool a_kcontig, bool b_kcontig, int bm, bool lower_only,
                          hipStream_t st);
