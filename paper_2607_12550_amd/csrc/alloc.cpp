@@ -19,9 +19,11 @@
 // most 200 halvings) and returns the allocation at hi.  This file is compiled
 // without floating-point contraction so the arithmetic is plain IEEE double.
 //
-// Speed: the grids of the cells are built and sorted, and each bisection step evaluated,
-// on up to 16 host threads (each cell by one thread, totals summed in cell order, so the
-// result does not depend on the split), and each bisection step scans only the Pareto
+// Speed: the grids of the cells are built and sorted (one 64-bit key per point holding the
+// cost and the generation index, so an unstable sort yields the stable order), and each
+// bisection step evaluated, on up to 16 host threads (each cell by one thread, totals summed
+// in cell order, so the result does not depend on the split; a bisection step over small
+// frontiers runs on the calling thread), and each bisection step scans only the Pareto
 // frontier of a grid.  A point q off the frontier has an earlier
 // point p with s_p <= s_q and e_p <= e_q; rounding is monotone, so for every lambda >= 0
 // e_p + lambda s_p <= e_q + lambda s_q in floating point too, and q can never be the first
@@ -157,6 +159,21 @@ class CellPool {
   bool stop_ = false;
 };
 
+// Ascending sort of keys below 2^bits (LSD radix, 11-bit digits).
+void radix_sort(std::vector<uint64_t> &key, int bits) {
+  constexpr int DB = 11, NB = 1 << DB;
+  std::vector<uint64_t> tmp(key.size());
+  uint32_t cnt[NB];
+  for (int sh = 0; sh < bits; sh += DB) {
+    std::fill(cnt, cnt + NB, 0u);
+    for (uint64_t k : key) ++cnt[(k >> sh) & (NB - 1)];
+    uint32_t pos = 0;
+    for (uint32_t &c : cnt) { const uint32_t n = c; c = pos; pos += n; }
+    for (uint64_t k : key) tmp[cnt[(k >> sh) & (NB - 1)]++] = k;
+    key.swap(tmp);
+  }
+}
+
 // Pareto frontier of a grid in grid order: the points whose error is below that of every
 // earlier (cheaper or equal-cost, earlier-ordered) point
 std::vector<int> pareto(const std::vector<Point> &pts) {
@@ -202,29 +219,47 @@ extern "C" int jolt_allocate(const jolt_cell_spectrum *cells, int n_cells, const
       if (!(mask & (1 << bi))) continue;
       const int b = bit_values[bi];
       if (b < o->floor_bits) continue;
+      const int step = o->step, rd0 = std::max(step, (o->floor_rd + step - 1) / step * step);
+      // the residual's cost, the same at every (r_T, r_d): s = backbone cost + res
+      const int64_t res = byte_cost(c.m, c.T, c.d, 0, 0, b, c.c, c.g, o->count_scale_bytes != 0);
       std::vector<int> rTs{0};
       for (int r = o->step; r <= rT_hi; r += o->step) rTs.push_back(r);
       for (int rT : rTs) {
         if (rT < o->floor_rT) continue;
         if (rT == 0) {
-          Point p{byte_cost(c.m, c.T, c.d, 0, 0, b, c.c, c.g, o->count_scale_bytes != 0), b, 0, 0, 0.0};
+          Point p{res, b, 0, 0, 0.0};
           const double tau = c.n_mu > 0 ? (c.E > 0.0 ? 1.0 : 0.0) : std::min(1.0, tT[0] + td[0]);
           p.e = o->eps2[bi] * tau;
           pts.push_back(p);
           continue;
         }
-        for (int rd = o->step; rd <= c.d; rd += o->step) {
-          if (rd < o->floor_rd) continue;
-          Point p{byte_cost(c.m, c.T, c.d, rT, rd, b, c.c, c.g, o->count_scale_bytes != 0), b, rT, rd, 0.0};
-          const double tau = c.n_mu > 0 ? tx[(size_t)(rT / o->step - 1) * (c.d + 1) + rd]
-                                        : std::min(1.0, tT[rT] + td[rd]);
-          p.e = o->eps2[bi] * tau;
-          pts.push_back(p);
+        const int64_t s_rT = (int64_t)c.T * rT, s_rd = (int64_t)c.m * rT + c.d;   // s = (s_rT + s_rd rd) c + res
+        const double eps = o->eps2[bi], tT_r = tT[rT];
+        const double *txr = c.n_mu > 0 ? tx.data() + (size_t)(rT / step - 1) * (c.d + 1) : nullptr;
+        for (int rd = rd0; rd <= c.d; rd += step) {
+          const double tau = txr ? txr[rd] : std::min(1.0, tT_r + td[rd]);
+          pts.push_back(Point{(s_rT + s_rd * rd) * c.c + res, b, rT, rd, eps * tau});
         }
       }
     }
-    // the points were made in (b, r_T, r_d) order, so a stable sort on s gives grid order
-    std::stable_sort(pts.begin(), pts.end(), [](const Point &a, const Point &b) { return a.s < b.s; });
+    // the points were made in (b, r_T, r_d) order, so ordering by (s, generation index) gives
+    // grid order; both go into one 64-bit key when s leaves room for the index
+    const size_t np = pts.size();
+    int gb = 1;
+    while (((size_t)1 << gb) < np) ++gb;
+    int64_t smax = 0;
+    for (const Point &q : pts) smax = std::max(smax, q.s);
+    if (smax >= 0 && gb < 40 && (uint64_t)smax < ((uint64_t)1 << (63 - gb))) {
+      std::vector<uint64_t> key(np);
+      for (size_t k = 0; k < np; ++k) key[k] = ((uint64_t)pts[k].s << gb) | (uint64_t)k;
+      radix_sort(key, 64 - __builtin_clzll(((uint64_t)smax << gb) | ((uint64_t)1 << gb)));
+      std::vector<Point> sorted(np);
+      const uint64_t low = ((uint64_t)1 << gb) - 1;
+      for (size_t k = 0; k < np; ++k) sorted[k] = pts[key[k] & low];
+      pts.swap(sorted);
+    } else {
+      std::stable_sort(pts.begin(), pts.end(), [](const Point &a, const Point &b) { return a.s < b.s; });
+    }
   };
   const unsigned hw = std::max(1u, std::thread::hardware_concurrency());
   CellPool pool(std::max(1, std::min<int>(n_cells, (int)std::min(16u, hw))), n_cells);
@@ -331,24 +366,41 @@ extern "C" int jolt_allocate(const jolt_cell_spectrum *cells, int n_cells, const
     front[ci] = pareto(grids[ci]);
     if (front[ci].empty() || front[ci][0] != 0) front[ci].insert(front[ci].begin(), 0);
   }
+  // each frontier's (e, s) pairs contiguous, so a bisection step streams through them
+  std::vector<std::vector<double>> fe(n_cells), fs(n_cells);
+  for (int ci = 0; ci < n_cells; ++ci) {
+    fe[ci].resize(front[ci].size());
+    fs[ci].resize(front[ci].size());
+    for (size_t q = 0; q < front[ci].size(); ++q) {
+      fe[ci][q] = grids[ci][front[ci][q]].e;
+      fs[ci][q] = (double)grids[ci][front[ci][q]].s;
+    }
+  }
   double lam_cur = 0.0;
   std::vector<int> *out_cur = nullptr;
   const std::function<void(int)> pick = [&](int ci) {
-    const std::vector<Point> &pts = grids[ci];
-    const std::vector<int> &f = front[ci];
-    int best = 0;
-    double bv = pts[0].e + lam_cur * (double)pts[0].s;
-    for (size_t q = 1; q < f.size(); ++q) {
-      const Point &p = pts[f[q]];
-      const double v = p.e + lam_cur * (double)p.s;
-      if (v < bv) { bv = v; best = f[q]; }
+    const double *e = fe[ci].data(), *sz = fs[ci].data();
+    const size_t nf = fe[ci].size();
+    size_t best = 0;
+    double bv = e[0] + lam_cur * sz[0];
+    for (size_t q = 1; q < nf; ++q) {
+      const double v = e[q] + lam_cur * sz[q];
+      if (v < bv) { bv = v; best = q; }
     }
-    (*out_cur)[ci] = best;
+    (*out_cur)[ci] = front[ci][best];
   };
+  // small frontiers are scanned on the calling thread (waking the pool would cost more)
+  size_t front_total = 0;
+  for (int ci = 0; ci < n_cells; ++ci) front_total += front[ci].size();
+  const bool serial = front_total < 50000;
   auto choose = [&](double lam, std::vector<int> &out) {
     lam_cur = lam;
     out_cur = &out;
-    pool.run(pick);
+    if (serial) {
+      for (int ci = 0; ci < n_cells; ++ci) pick(ci);
+    } else {
+      pool.run(pick);
+    }
     double total = 0.0;
     for (int ci = 0; ci < n_cells; ++ci) total += (double)grids[ci][out[ci]].s;
     return total;
