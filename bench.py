@@ -78,7 +78,7 @@ def parse():
                          "writes this many MiB: the reference dispatch for scaling HBM "
                          "traffic counters")
     ap.add_argument("--trd-lanes", type=int, default=0,
-                    help="streams of the exact path's tridiagonalisation (library default 2); "
+                    help="streams of the exact path's tridiagonalisation (library default 4); "
                          "1 keeps every launch on one stream, for counter collection")
     ap.add_argument("--no-stage-profile", action="store_true",
                     help="skip the event-instrumented step; the stage and roofline fields are "

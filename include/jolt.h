@@ -401,8 +401,8 @@ int jolt_debug_export(jolt_ctx *ctx, int what, int cell, void *dst, size_t dst_b
  * succeed: it sets the number of inverse-iteration sweeps of later calls on this context
  * (default 2, range 0..8; with 0 no sweep runs and the growth check fails).
  * JOLT_DBG_TRD_LANES sets how many streams the blocked tridiagonalisation of the exact token
- * spectrum spreads its groups of matrices over (default 2, range 1..2; results do not
- * depend on it): 1 keeps every launch on one stream, for counter collection.
+ * spectrum spreads its groups of matrices over (default 4, range 1..4; results do not
+ * depend on it): 1 keeps every launch on the call's stream, for counter collection.
  * Errors: JOLT_E_INVAL. */
 enum { JOLT_DBG_INVIT_ITERS = 0, JOLT_DBG_TRD_LANES = 1 };
 int jolt_debug_set(jolt_ctx *ctx, int what, int64_t value);

@@ -71,10 +71,11 @@ struct jolt_ctx {
   double prof_ms[JOLT_STAGE_COUNT] = {};
   int64_t prof_n[JOLT_STAGE_COUNT] = {};
   // replay of the fixed launch sequence of the blocked tridiagonalisation: the batch is
-  // split into kTrdLanes groups of matrices, each captured once and replayed on a stream
-  // of its own, so that one group's latency-bound column kernels run beside another
-  // group's bandwidth-bound mat-vec (all streams at the default priority)
-  static constexpr int kTrdLanes = 2;
+  // split into up to kTrdLanes groups of matrices, each captured once and replayed on a
+  // stream of its own (the first on the call's stream: with the private streams, four in
+  // all, the hardware queues of a process), so that one group's latency-bound column
+  // kernels run beside another group's bandwidth-bound mat-vec (default stream priority)
+  static constexpr int kTrdLanes = 4;
   hipStream_t cap_stream[kTrdLanes] = {};
   hipGraphExec_t trd_exec[kTrdLanes] = {};
   hipEvent_t trd_fork = nullptr, trd_join[kTrdLanes] = {};

@@ -248,9 +248,9 @@ int eig_values(Run &R, EigWs &e) {
     HIP_OK(hipMemcpyAsync(tab, c->tab_host.data(), nt * sizeof(GemmProblem), hipMemcpyHostToDevice, R.st));
     {
       // the launch sequence depends only on the shape and the buffers: capture it once per
-      // group of matrices on that group's private stream, and replay the groups side by side
-      // between a fork from and a join into the caller's stream (timed as one stage when
-      // profiling is on; its kernels are told apart by a kernel trace)
+      // group of matrices, and replay the groups side by side, the first on the caller's
+      // stream and the others on private streams between a fork from and a join into it
+      // (timed as one stage when profiling is on; its kernels are told apart by a kernel trace)
       std::vector<const void *> key{e.b.A, e.trd, tab, e.b.d, e.b.e, e.b.tau,
                                     reinterpret_cast<const void *>((intptr_t)e.b.n),
                                     reinterpret_cast<const void *>((intptr_t)e.b.n_mat)};
@@ -261,13 +261,16 @@ int eig_values(Run &R, EigWs &e) {
         c->trd_lanes = 0;
         if (!c->trd_fork) HIP_OK(hipEventCreateWithFlags(&c->trd_fork, hipEventDisableTiming));
         for (int g = 0; g < lanes; ++g) {
-          if (!c->cap_stream[g]) HIP_OK(hipStreamCreateWithFlags(&c->cap_stream[g], hipStreamNonBlocking));
+          // lane 0 replays on the caller's stream and is captured on lane 1's stream (no
+          // stream of its own, so that lanes + 1 streams never exceed the hardware queues)
+          const int cs = g > 0 ? g : 1;
+          if (!c->cap_stream[cs]) HIP_OK(hipStreamCreateWithFlags(&c->cap_stream[cs], hipStreamNonBlocking));
           if (!c->trd_join[g]) HIP_OK(hipEventCreateWithFlags(&c->trd_join[g], hipEventDisableTiming));
           const int m0 = (int)((int64_t)e.b.n_mat * g / lanes), m1 = (int)((int64_t)e.b.n_mat * (g + 1) / lanes);
           hipGraph_t gr = nullptr;
-          HIP_OK(hipStreamBeginCapture(c->cap_stream[g], hipStreamCaptureModeThreadLocal));
-          hipError_t le = launch_sytrd_large(e.b, e.trd, SYTRD_NB, tab, c->cap_stream[g], m0, m1);
-          hipError_t ce = hipStreamEndCapture(c->cap_stream[g], &gr);
+          HIP_OK(hipStreamBeginCapture(c->cap_stream[cs], hipStreamCaptureModeThreadLocal));
+          hipError_t le = launch_sytrd_large(e.b, e.trd, SYTRD_NB, tab, c->cap_stream[cs], m0, m1);
+          hipError_t ce = hipStreamEndCapture(c->cap_stream[cs], &gr);
           HIP_OK(le);
           HIP_OK(ce);
           hipError_t ie = hipGraphInstantiate(&c->trd_exec[g], gr, nullptr, nullptr, 0);
@@ -279,12 +282,13 @@ int eig_values(Run &R, EigWs &e) {
       }
       StageTimer t(R.ctx, R.st, JOLT_STAGE_TRIDIAG_LARGE);
       HIP_OK(hipEventRecord(c->trd_fork, R.st));
-      for (int g = 0; g < lanes; ++g) {
+      for (int g = 1; g < lanes; ++g) {
         HIP_OK(hipStreamWaitEvent(c->cap_stream[g], c->trd_fork, 0));
         HIP_OK(hipGraphLaunch(c->trd_exec[g], c->cap_stream[g]));
         HIP_OK(hipEventRecord(c->trd_join[g], c->cap_stream[g]));
-        HIP_OK(hipStreamWaitEvent(R.st, c->trd_join[g], 0));
       }
+      HIP_OK(hipGraphLaunch(c->trd_exec[0], R.st));
+      for (int g = 1; g < lanes; ++g) HIP_OK(hipStreamWaitEvent(R.st, c->trd_join[g], 0));
     }
   } else {
     StageTimer t(R.ctx, R.st, JOLT_STAGE_TRIDIAG_SMALL);

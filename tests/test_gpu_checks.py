@@ -138,24 +138,26 @@ def test_tiny_core_takes_the_exponent_floor():
 
 def test_tridiagonalisation_lanes_do_not_change_results():
     """The exact spectrum of a batch of cells is the same bit for bit whether the blocked
-    tridiagonalisation runs its matrices as one group on one stream or as two groups on two
-    streams (JOLT_DBG_TRD_LANES); the setting rejects values outside 1..2."""
+    tridiagonalisation runs its matrices as one group on one stream or as several groups on
+    up to four streams (JOLT_DBG_TRD_LANES; three cells, so 3 and 4 both give three groups);
+    the setting rejects values outside 1..4."""
     cells = [keys(T=1024, H=8, seed=s) for s in range(3)]      # T above the one-workgroup size
     xs, ex, desc = device_cells(cells, "bf16")
     ws = workspace(desc, 3)
     out = []
     c2 = J.jolt_create(0)
     try:
-        for lanes in (1, 2):
+        for lanes in (1, 2, 3, 4):
             J.jolt_debug_set(c2, J.JOLT_DBG_TRD_LANES, lanes)
             note("exact spectrum, tridiagonalisation lanes", lanes)
             E, lamT, lamd = J.jolt_spectrum(c2, desc, xs, None, None, ws)
             torch.cuda.synchronize()
             out.append((np.array(E), np.array(lamT), np.array(lamd)))
-        for bad in (0, 3):
+        for bad in (0, 5):
             with pytest.raises(J.JoltError):
                 J.jolt_debug_set(c2, J.JOLT_DBG_TRD_LANES, bad)
     finally:
         J.jolt_destroy(c2)
-    for a, b in zip(out[0], out[1]):
-        assert np.array_equal(a, b)
+    for other in out[1:]:
+        for a, b in zip(out[0], other):
+            assert np.array_equal(a, b)
