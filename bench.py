@@ -268,7 +268,6 @@ def diagnostics(args):
     # slice-mode Gram over every cell of the workload
     cfg = dict(kvsynth.CONFIGS[args.workload])
     gl = cfg.pop("group_layers")
-    cfg["workers"] = 8
     # generation runs in worker processes (the values do not depend on their number)
     Knp, Vnp = kvsynth.make_cache(**cfg, workers=min(16, os.cpu_count() or 1))
     to_dev = (lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()) \
@@ -319,7 +318,6 @@ def attend_bench(args):
     gl = cfg.pop("group_layers")
     method, ratio = WORKLOAD_RUN.get(args.workload, ("exact", 2.0))
     method, ratio = args.method or method, args.ratio or ratio
-    cfg["workers"] = 8
     log("generating", args.workload)
     # generation runs in worker processes (the values do not depend on their number)
     Knp, Vnp = kvsynth.make_cache(**cfg, workers=min(16, os.cpu_count() or 1))
