@@ -80,6 +80,10 @@ def parse():
     ap.add_argument("--trd-lanes", type=int, default=0,
                     help="streams of the exact path's tridiagonalisation (library default 4); "
                          "1 keeps every launch on one stream, for counter collection")
+    ap.add_argument("--trd-stages", type=int, default=-1, choices=[-1, 1, 2],
+                    help="reduction of the exact path's token Grams to tridiagonal form: 2 "
+                         "two-stage (band, then bulge chasing), 1 one-stage; -1 the library's "
+                         "choice (two stages once a call's matrices times T reach 32 * 4096)")
     ap.add_argument("--no-stage-profile", action="store_true",
                     help="skip the event-instrumented step; the stage and roofline fields are "
                          "then omitted")
@@ -461,6 +465,17 @@ def method_comparison(K, V, gl, ratio, args, exact_compress_ms):
     return out
 
 
+def trd_stages_used(args, cells_per_call, T):
+    """Reduction of the exact token Grams to tridiagonal form in this run: the forced one, or
+    the library's automatic choice (two stages once a call's matrices times T reach
+    32 * 4096; T up to 768 is reduced in one workgroup per matrix)."""
+    if T <= 768:
+        return "one-workgroup"
+    if args.trd_stages in (1, 2):
+        return "two-stage" if args.trd_stages == 2 else "one-stage"
+    return "two-stage" if cells_per_call * T >= 32 * 4096 else "one-stage"
+
+
 def main():
     args = parse()
     if args.attend:
@@ -513,6 +528,8 @@ def main():
                        max_cells_per_call=args.cells_per_call)
     if args.trd_lanes:
         J.jolt_debug_set(codec.ctx, J.JOLT_DBG_TRD_LANES, args.trd_lanes)
+    if args.trd_stages > 0:
+        J.jolt_debug_set(codec.ctx, J.JOLT_DBG_TRD_TWO_STAGE, 1 if args.trd_stages == 2 else 0)
     eps2 = codec.calibrate()
     log("eps2", eps2, "cells", len(codec.cells), "per call", codec.chunk)
     Kout, Vout = torch.empty_like(K), torch.empty_like(V)
@@ -594,6 +611,8 @@ def main():
                    "ratio": ratio, "allocator": args.allocator, "tau": args.tau,
                    **({"tau_rT_cap": codec.tau_cap_used} if args.tau == "exact" else {}),
                    "keys": "post-rope" if args.rope_post > 1.0 else "pre-rope",
+                   **({"tridiagonalisation": trd_stages_used(args, codec.chunk, cfg["T"])}
+                      if method == "exact" else {}),
                    "cache_bytes": cache_bytes},
         "compress_GBps": round(cache_bytes / (np.median(t_comp) * 1e-3) / 1e9, 3),
         "decompress_GBps": round(cache_bytes / (np.median(t_dec) * 1e-3) / 1e9, 3),

@@ -403,8 +403,14 @@ int jolt_debug_export(jolt_ctx *ctx, int what, int cell, void *dst, size_t dst_b
  * JOLT_DBG_TRD_LANES sets how many streams the blocked tridiagonalisation of the exact token
  * spectrum spreads its groups of matrices over (default 4, range 1..4; results do not
  * depend on it): 1 keeps every launch on the call's stream, for counter collection.
+ * JOLT_DBG_TRD_TWO_STAGE selects the reduction of those large matrices to tridiagonal form:
+ * 1 the two-stage reduction (dense to a band of half-bandwidth 32 by panel QR and
+ * matrix-core updates, then bulge chasing), 0 the one-stage blocked Householder reduction,
+ * -1 (default) two stages when the call's matrices times their order reach 32 * 4096, one
+ * otherwise; both give the same spectrum and projectors to rounding, and a compress that
+ * reuses a recorded spectrum back-transforms with the reduction that made it.
  * Errors: JOLT_E_INVAL. */
-enum { JOLT_DBG_INVIT_ITERS = 0, JOLT_DBG_TRD_LANES = 1 };
+enum { JOLT_DBG_INVIT_ITERS = 0, JOLT_DBG_TRD_LANES = 1, JOLT_DBG_TRD_TWO_STAGE = 2 };
 int jolt_debug_set(jolt_ctx *ctx, int what, int64_t value);
 
 /* Benchmark instrumentation.  When enabled, the library brackets the kernels of each

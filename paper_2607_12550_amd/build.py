@@ -18,7 +18,7 @@ OUT = os.path.join(HERE, "libjolt.so")
 BUILD = os.path.join(HERE, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-DEVICE_SOURCES = ["k_residual.hip", "k_gemm.hip", "k_gemm16.hip", "k_gram.hip", "k_eig.hip", "k_sytrd.hip", "k_serialize.hip", "k_flash.hip", "k_attend.hip", "k_fused.hip"]
+DEVICE_SOURCES = ["k_residual.hip", "k_gemm.hip", "k_gemm16.hip", "k_gram.hip", "k_eig.hip", "k_sytrd.hip", "k_sb.hip", "k_serialize.hip", "k_flash.hip", "k_attend.hip", "k_fused.hip"]
 HOST_SOURCES = ["api.cpp", "pipeline.cpp", "diag.cpp"]
 STRICT_FP_SOURCES = ["alloc.cpp"]
 

@@ -26,6 +26,9 @@ struct BlobInfo {
 };
 
 // State a jolt_compress call may reuse from the preceding jolt_spectrum call.
+// batch work (matrices x order) from which the automatic choice takes the two-stage reduction
+constexpr int64_t kTwoStageMinWork = 32 * 4096;
+
 struct SpecKey {
   bool valid = false;
   const void *ws = nullptr;
@@ -34,6 +37,7 @@ struct SpecKey {
   jolt_spectrum_opts opts{};
   std::vector<const void *> X;
   std::vector<uint64_t> seeds;
+  int32_t token_refl_off = 0;   // reduction that left the token reflectors (1 one-stage, else the band)
 };
 
 // Forget every recorded spectrum whose workspace overlaps [ws, ws + bytes), except `keep`.
@@ -82,6 +86,7 @@ struct jolt_ctx {
   int trd_lanes = 0;               // lanes of the captured graphs
   int trd_lanes_max = kTrdLanes;   // JOLT_DBG_TRD_LANES
   std::vector<const void *> trd_key;
+  int trd_two_stage = -1;          // JOLT_DBG_TRD_TWO_STAGE: 1 two-stage, 0 one-stage, -1 by batch size
   int invit_iters = 2;            // inverse-iteration sweeps (test hook jolt_debug_set)
   void *attend_scratch = nullptr; // this device's fixed attention scratch (device address)
   ~jolt_ctx();

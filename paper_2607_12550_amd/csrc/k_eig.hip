@@ -542,7 +542,7 @@ __global__ void __launch_bounds__(NB) k_larft(EigBatch b, const float *S_all, fl
   const int mat = blockIdx.y, p = blockIdx.x, n = b.n;
   const int panels = (n + NB - 1) / NB;
   const int i0 = p * NB;
-  const int pw = min(NB, n - 1 - i0);
+  const int pw = max(0, min(NB, n - refl_off(b) - i0));
   const float *tau = b.tau + (int64_t)mat * n;
   const float *S = S_all + ((int64_t)mat * panels + p) * NB * NB;
   __shared__ float T[NB][NB + 1];
@@ -631,12 +631,12 @@ size_t backtransform_table_entries(int n_mat, int n) {
 
 hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax, const int *k_host, float *U,
                                 int64_t ldu, int64_t u_stride, float *scratch, GemmProblem *tab_dev,
-                                GemmProblem *tab_host, hipStream_t st) {
-  const int n = b.n, panels = (n + NB - 1) / NB, nm = b.n_mat;
+                                GemmProblem *tab_host, hipStream_t st, bool u_ready) {
+  const int n = b.n, panels = (n + NB - 1) / NB, nm = b.n_mat, off = refl_off(b);
   const int chunks_max = (n + BT_KCHUNK - 1) / BT_KCHUNK;
   {
     dim3 g((unsigned)(((int64_t)n * kmax + 255) / 256), nm);
-    hipLaunchKernelGGL(k_z_to_f32, g, dim3(256), 0, st, b, w, kmax, U, ldu, u_stride);
+    if (!u_ready) hipLaunchKernelGGL(k_z_to_f32, g, dim3(256), 0, st, b, w, kmax, U, ldu, u_stride);
   }
   float *Sf = scratch;
   float *Tf = Sf + (size_t)nm * panels * NB * NB;
@@ -647,15 +647,15 @@ hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax,
   const size_t per_panel = (size_t)nm * (chunks_max + 2);
   GemmProblem *gS = tab_host;
   for (int p = 0; p < panels; ++p) {
-    const int i0 = p * NB, pw = std::min(NB, n - 1 - i0), rows = n - (i0 + 1);
+    const int i0 = p * NB, pw = std::max(0, std::min(NB, n - off - i0)), rows = std::max(0, n - (i0 + off));
     const int chunks = std::max(1, (rows + BT_KCHUNK - 1) / BT_KCHUNK);
     GemmProblem *g = tab_host + (size_t)panels * nm + (size_t)p * per_panel;
     for (int m = 0; m < nm; ++m) {
       const float *A = b.A + (int64_t)m * b.mat_stride;
       const int km = std::min(std::max(k_host[m], 0), kmax);   // this matrix's vectors
       GemmProblem S{};
-      S.A = GemmOperand{A + (int64_t)(i0 + 1) * n + i0, n, 0, 0, 0, 1};
-      S.B = GemmOperand{A + (int64_t)(i0 + 1) * n + i0, n, 0, 0, 0, 1};
+      S.A = GemmOperand{A + (int64_t)(i0 + off) * n + i0, n, 0, 0, 0, 1};
+      S.B = GemmOperand{A + (int64_t)(i0 + off) * n + i0, n, 0, 0, 0, 1};
       S.C = Sf + ((size_t)m * panels + p) * NB * NB; S.ldc = NB;
       S.M = std::max(pw, 0); S.N = std::max(pw, 0); S.K = rows; S.alpha = 1.f; S.beta = 0.f;
       gS[(size_t)p * nm + m] = S;
@@ -663,8 +663,8 @@ hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax,
       for (int c = 0; c < chunks_max; ++c) {
         GemmProblem P{};
         const int r0 = c * BT_KCHUNK, r1 = std::min(rows, r0 + BT_KCHUNK);
-        P.A = GemmOperand{A + (int64_t)(i0 + 1 + r0) * n + i0, n, 0, 0, 0, 1};
-        P.B = GemmOperand{U + (int64_t)m * u_stride + (int64_t)(i0 + 1 + r0) * ldu, ldu, 0, 0, 0, 1};
+        P.A = GemmOperand{A + (int64_t)(i0 + off + r0) * n + i0, n, 0, 0, 0, 1};
+        P.B = GemmOperand{U + (int64_t)m * u_stride + (int64_t)(i0 + off + r0) * ldu, ldu, 0, 0, 0, 1};
         P.C = W1 + m * w1_mat + (int64_t)c * NB * kmax; P.ldc = kmax;
         P.M = (c < chunks) ? pw : 0; P.N = km; P.K = std::max(0, r1 - r0);
         P.alpha = 1.f; P.beta = 0.f;
@@ -679,9 +679,9 @@ hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax,
       Q.M = pw; Q.N = km; Q.K = chunks * NB; Q.alpha = 1.f; Q.beta = 0.f;
       g[(size_t)nm * chunks_max + m] = Q;
       GemmProblem R{};
-      R.A = GemmOperand{A + (int64_t)(i0 + 1) * n + i0, n, 0, 0, 0, 1};
+      R.A = GemmOperand{A + (int64_t)(i0 + off) * n + i0, n, 0, 0, 0, 1};
       R.B = GemmOperand{W2 + (size_t)m * NB * kmax, kmax, 0, 0, 0, 1};
-      R.C = U + (int64_t)m * u_stride + (int64_t)(i0 + 1) * ldu; R.ldc = ldu;
+      R.C = U + (int64_t)m * u_stride + (int64_t)(i0 + off) * ldu; R.ldc = ldu;
       R.M = rows; R.N = km; R.K = pw; R.alpha = -1.f; R.beta = 1.f;
       g[(size_t)nm * (chunks_max + 1) + m] = R;
     }
@@ -699,9 +699,9 @@ hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax,
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   for (int p = panels - 1; p >= 0; --p) {
-    const int i0 = p * NB, pw = std::min(NB, n - 1 - i0);
+    const int i0 = p * NB, pw = std::max(0, std::min(NB, n - off - i0));
     if (pw <= 0) continue;
-    const int rows = n - (i0 + 1);
+    const int rows = n - (i0 + off);
     GemmProblem *g = tab_dev + (size_t)panels * nm + (size_t)p * per_panel;
     err = launch_gemm(g, nm * chunks_max, pw, kmax, 1, GT_F32, GT_F32, false, false, st);
     if (err != hipSuccess) return err;

@@ -230,7 +230,10 @@ struct EigBatch {
   double *d, *e;         // tridiagonal [n_mat][n]
   float *tau;            // [n_mat][n]
   double *lam;           // eigenvalues, descending [n_mat][n]
+  int32_t refl_off;      // row of reflector i's unit is i + refl_off (0 read as 1: one-stage)
+  int32_t pad_;
 };
+inline __host__ __device__ int refl_off(const EigBatch &b) { return b.refl_off > 0 ? b.refl_off : 1; }
 // Householder tridiagonalisation (lower): small n in one workgroup per matrix.
 hipError_t launch_sytrd_small(const EigBatch &b, hipStream_t st);
 // Blocked multi-workgroup tridiagonalisation for large n (panels of nb columns).
@@ -277,9 +280,36 @@ hipError_t launch_tridiag_eigvecs(const EigBatch &b, const InvitWork &w, int kma
 int backtransform_nb();
 size_t backtransform_scratch_floats(int n_mat, int n, int kmax);
 size_t backtransform_table_entries(int n_mat, int n);
+// u_ready: U already holds the vectors to transform (fp32), Z is not read.
 hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax, const int *k_host, float *U,
                                 int64_t ldu, int64_t u_stride, float *scratch, GemmProblem *tab_dev,
-                                GemmProblem *tab_host, hipStream_t st);
+                                GemmProblem *tab_host, hipStream_t st, bool u_ready = false);
+
+// Two-stage tridiagonalisation for large n (k_sb.hip): dense to band of half-bandwidth
+// sb_band() by panel QR and rank-2 sb_band() updates, then band to tridiagonal by bulge
+// chasing.  Leaves d, e, tau and the stage-1 reflectors in A (explicit, unit of reflector i
+// at row i + sb_band(), zeros above it within its block of 128) and the stage-2 reflectors
+// in work (sb_work_floats() floats).  The update problems come from sb_tables()
+// (sb_table_entries() entries).  Matrices m0 .. m1-1 of the batch.
+struct SbArgs {
+  float *A;
+  int64_t mat_stride;
+  int32_t n, pad;
+  float *work;
+  int64_t work_stride;
+  double *d, *e;
+  float *tau;
+};
+constexpr int SB_MAX_N = 8192;
+int sb_band();
+size_t sb_work_floats(int n_mat, int n);
+size_t sb_table_entries(int n_mat, int n);
+void sb_tables(const EigBatch &b, float *work, GemmProblem *tab_host);
+hipError_t launch_sb_reduce(const EigBatch &b, float *work, const GemmProblem *tab_dev, hipStream_t st,
+                            int m0 = 0, int m1 = -1);
+// U (fp32, first k[mat] columns) = Q2 Z for the tridiagonal's eigenvectors Z of w.
+hipError_t launch_sb_q2(const EigBatch &b, const float *work, const InvitWork &w, int kmax, float *U, int64_t ldu,
+                        int64_t u_stride, hipStream_t st);
 
 // ----------------------------------------------------------------- serialisation
 struct SerCell {

@@ -98,7 +98,8 @@ void carve_eig(Carver &cv, EigWs &e, int nmat, int n, int kmax, float *A) {
   e.kmax = kmax;
   e.k = cv.take<int32_t>(nmat);
   e.status = cv.take<int32_t>(nmat);
-  if (n > SYTRD_SMALL_MAX) e.trd = cv.take<float>(sytrd_large_work_floats(nmat, n, SYTRD_NB));
+  if (n > SYTRD_SMALL_MAX)
+    e.trd = cv.take<float>(std::max(sytrd_large_work_floats(nmat, n, SYTRD_NB), sb_work_floats(nmat, n)));
   if (kmax > 0) {
     e.Z = cv.take<double>((size_t)nmat * n * kmax);
     e.lu = cv.take<double>((size_t)nmat * 3 * n * std::min(kmax, KC));
@@ -239,12 +240,23 @@ struct Run {
 // symmetric eigenvalues (all) of the n x n matrices in e.b.A
 int eig_values(Run &R, EigWs &e) {
   if (e.b.n > SYTRD_SMALL_MAX) {
-    const size_t nt = sytrd_large_table_entries(e.b.n_mat, e.b.n, SYTRD_NB);
+    jolt_ctx *c = R.ctx;
+    // Two stages (band of half-bandwidth sb_band(), then bulge chasing) move the trailing
+    // matrix once per panel instead of once per column, but their bulge chase is a chain of
+    // about n^2 / 64 dependent steps per matrix; the one-stage reduction costs about n^3 / 6
+    // floats of trailing-matrix reads per matrix.  With the batch's matrices run side by side
+    // the chain is hidden once the batch holds n_mat * n >= 32 * 4096 (measured crossover at
+    // n = 4096: 16 matrices favour one stage, 64 two).  The eigenvector back-transform
+    // follows the choice.
+    const bool two = c->trd_two_stage == 1 ||
+                     (c->trd_two_stage < 0 && (int64_t)e.b.n_mat * e.b.n >= kTwoStageMinWork);
+    e.b.refl_off = two ? sb_band() : 1;
+    const size_t nt = two ? sb_table_entries(e.b.n_mat, e.b.n) : sytrd_large_table_entries(e.b.n_mat, e.b.n, SYTRD_NB);
     GemmProblem *tab = R.tab_slice(nt);
     if (!tab) return jolt_fail(JOLT_E_WORKSPACE, "GEMM problem table overflow");
-    jolt_ctx *c = R.ctx;
     c->tab_host.resize(std::max(c->tab_host.size(), nt));
-    sytrd_large_tables(e.b, e.trd, SYTRD_NB, c->tab_host.data());
+    if (two) sb_tables(e.b, e.trd, c->tab_host.data());
+    else sytrd_large_tables(e.b, e.trd, SYTRD_NB, c->tab_host.data());
     HIP_OK(hipMemcpyAsync(tab, c->tab_host.data(), nt * sizeof(GemmProblem), hipMemcpyHostToDevice, R.st));
     {
       // the launch sequence depends only on the shape and the buffers: capture it once per
@@ -253,7 +265,8 @@ int eig_values(Run &R, EigWs &e) {
       // (timed as one stage when profiling is on; its kernels are told apart by a kernel trace)
       std::vector<const void *> key{e.b.A, e.trd, tab, e.b.d, e.b.e, e.b.tau,
                                     reinterpret_cast<const void *>((intptr_t)e.b.n),
-                                    reinterpret_cast<const void *>((intptr_t)e.b.n_mat)};
+                                    reinterpret_cast<const void *>((intptr_t)e.b.n_mat),
+                                    reinterpret_cast<const void *>((intptr_t)(two ? 2 : 1))};
       const int lanes = std::min(c->trd_lanes_max, e.b.n_mat);
       if (c->trd_lanes != lanes || c->trd_key != key) {
         for (int g = 0; g < jolt_ctx::kTrdLanes; ++g)
@@ -269,7 +282,8 @@ int eig_values(Run &R, EigWs &e) {
           const int m0 = (int)((int64_t)e.b.n_mat * g / lanes), m1 = (int)((int64_t)e.b.n_mat * (g + 1) / lanes);
           hipGraph_t gr = nullptr;
           HIP_OK(hipStreamBeginCapture(c->cap_stream[cs], hipStreamCaptureModeThreadLocal));
-          hipError_t le = launch_sytrd_large(e.b, e.trd, SYTRD_NB, tab, c->cap_stream[cs], m0, m1);
+          hipError_t le = two ? launch_sb_reduce(e.b, e.trd, tab, c->cap_stream[cs], m0, m1)
+                              : launch_sytrd_large(e.b, e.trd, SYTRD_NB, tab, c->cap_stream[cs], m0, m1);
           hipError_t ce = hipStreamEndCapture(c->cap_stream[cs], &gr);
           HIP_OK(le);
           HIP_OK(ce);
@@ -317,7 +331,12 @@ int eig_vectors(Run &R, EigWs &e, const std::vector<int> &k, float *U, int64_t l
   GemmProblem *tab = R.tab_slice(nt);
   if (!tab) return jolt_fail(JOLT_E_WORKSPACE, "GEMM problem table overflow");
   R.ctx->tab_host.resize(std::max(R.ctx->tab_host.size(), nt));
-  HIP_OK(launch_backtransform(e.b, iw, kmax, k.data(), U, ldu, u_stride, e.bt, tab, R.ctx->tab_host.data(), R.st));
+  // two-stage reduction: the band-to-tridiagonal reflectors first (Z -> U), then the
+  // panel reflectors of the first stage by the blocked back-transform
+  const bool two = e.b.n > SYTRD_SMALL_MAX && e.b.refl_off == sb_band();
+  if (two) HIP_OK(launch_sb_q2(e.b, e.trd, iw, kmax, U, ldu, u_stride, R.st));
+  HIP_OK(launch_backtransform(e.b, iw, kmax, k.data(), U, ldu, u_stride, e.bt, tab, R.ctx->tab_host.data(), R.st,
+                              two));
   return JOLT_OK;
 }
 
@@ -798,6 +817,7 @@ extern "C" int jolt_spectrum(jolt_ctx *ctx, const jolt_cell_desc *desc, int n_ce
   k.opts = opts ? *opts : jolt_spectrum_opts{JOLT_EXACT, 0, 0.0, 0, 0, 0, 0};
   k.X.assign(X, X + n_cells);
   k.seeds.assign(seeds ? seeds : (const uint64_t *)nullptr, seeds ? seeds + n_cells : (const uint64_t *)nullptr);
+  k.token_refl_off = R.w.teig.b.refl_off;
   return JOLT_OK;
 }
 
@@ -821,6 +841,8 @@ int acquire_spectrum(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, in
     }
     if (!found)
       return jolt_fail(JOLT_E_STATE, "reuse requested but the workspace holds no spectrum of these cells");
+    // the eigenvector back-transform follows the reduction that stored the reflectors
+    R.w.teig.b.refl_off = found->token_refl_off;
     forget_spectra(ctx, ws, ws_bytes, found);
     return JOLT_OK;
   }
@@ -836,6 +858,7 @@ int acquire_spectrum(Run &R, const SpecShape &sh, const jolt_cell_desc *desc, in
   k.opts = o;
   k.X.assign(X, X + nc);
   k.seeds = seeds;
+  k.token_refl_off = R.w.teig.b.refl_off;
   return JOLT_OK;
 }
 
@@ -1591,6 +1614,12 @@ extern "C" int jolt_debug_set(jolt_ctx *ctx, int what, int64_t value) {
     if (value < 1 || value > jolt_ctx::kTrdLanes)
       return jolt_fail(JOLT_E_INVAL, "jolt_debug_set: tridiagonalisation lanes must be in 1..%d", jolt_ctx::kTrdLanes);
     ctx->trd_lanes_max = (int)value;
+    return JOLT_OK;
+  }
+  if (what == JOLT_DBG_TRD_TWO_STAGE) {
+    if (value < -1 || value > 1)
+      return jolt_fail(JOLT_E_INVAL, "jolt_debug_set: two-stage switch must be -1 (automatic), 0 or 1");
+    ctx->trd_two_stage = (int)value;
     return JOLT_OK;
   }
   return jolt_fail(JOLT_E_INVAL, "jolt_debug_set: unknown setting %d", what);

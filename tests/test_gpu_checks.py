@@ -161,3 +161,56 @@ def test_tridiagonalisation_lanes_do_not_change_results():
     for other in out[1:]:
         for a, b in zip(out[0], other):
             assert np.array_equal(a, b)
+
+
+def test_two_stage_and_one_stage_reductions_agree():
+    """JOLT_DBG_TRD_TWO_STAGE: for T > 768 (here T = 1100, a ragged last panel) the exact
+    token spectrum from the two-stage reduction (band of half-bandwidth 32 by panel QR and
+    rank-64 updates, then bulge chasing) and from the one-stage blocked reduction agree within
+    1e-5 of lambda_1 on fp32 cells, and the token factors at a gapped rank span the same
+    subspace (projectors within 1e-4).  A compress that reuses a spectrum recorded by
+    jolt_spectrum back-transforms with the reduction that made it, even after the setting
+    has changed in between: its blobs equal those of a direct compress in that mode.
+    Values outside -1..1 are rejected (-1, the default, chooses by batch size)."""
+    cells = [keys(T=1100, H=8, seed=s) for s in range(3)]
+    xs, ex, desc = device_cells(cells, "f32")
+    ws = workspace(desc, 3)
+    p = [J.Params(32, 32, 4, 64, J.JOLT_FACTOR_F32, 0, c) for c in range(3)]
+    reuse = J.SpectrumOpts(J.JOLT_EXACT, 0, 0.0, 0, 0, 1, 0)
+    lam, proj, direct = {}, {}, {}
+    c2 = J.jolt_create(0)
+    try:
+        for mode in (1, 0):
+            J.jolt_debug_set(c2, J.JOLT_DBG_TRD_TWO_STAGE, mode)
+            note("exact spectrum, two-stage switch", mode)
+            E, lamT, lamd = J.jolt_spectrum(c2, desc, xs, None, None, ws)
+            lam[mode] = np.array(lamT)
+            J.jolt_debug_set(c2, J.JOLT_DBG_TRD_TWO_STAGE, 1 - mode)
+            blobs = blobs_for(desc, p)
+            J.jolt_compress(c2, desc, xs, p, reuse, ws, blobs)
+            torch.cuda.synchronize()
+            U = torch.empty((1100, 32), device="cuda")
+            J.jolt_debug_export(c2, 0, 0, U)
+            U = U.cpu().numpy().astype(np.float64)
+            proj[mode] = U @ U.T
+            np.testing.assert_allclose(U.T @ U, np.eye(32), atol=1e-5)
+            J.jolt_debug_set(c2, J.JOLT_DBG_TRD_TWO_STAGE, mode)
+            ws2 = workspace(desc, 3)
+            blobs2 = blobs_for(desc, p)
+            J.jolt_compress(c2, desc, xs, p, None, ws2, blobs2)
+            torch.cuda.synchronize()
+            for a, b in zip(blobs, blobs2):
+                assert blob_bytes(a) == blob_bytes(b)
+        for bad in (-2, 2):
+            with pytest.raises(J.JoltError):
+                J.jolt_debug_set(c2, J.JOLT_DBG_TRD_TWO_STAGE, bad)
+        J.jolt_debug_set(c2, J.JOLT_DBG_TRD_TWO_STAGE, -1)
+    finally:
+        J.jolt_destroy(c2)
+    for c in range(3):
+        sp = opl.spectrum(ex[c])
+        for mode in (0, 1):
+            np.testing.assert_allclose(lam[mode][c], sp["lam_T"], rtol=0, atol=1e-5 * sp["lam_T"][0])
+    lam0 = opl.spectrum(ex[0])["lam_T"]
+    assert (lam0[31] - lam0[32]) / lam0[31] > 0.02
+    assert np.abs(proj[0] - proj[1]).max() < 1e-4

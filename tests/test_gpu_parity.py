@@ -186,9 +186,19 @@ def test_spectrum_then_compress_reuses_and_matches_direct():
         assert blob_bytes(a) == blob_bytes(b) == blob_bytes(c)
 
 
+@pytest.fixture(params=[0, 1], ids=["one_stage", "two_stage"])
+def reduction(request):
+    """Runs a test with the one-stage and with the two-stage reduction of the large token
+    Grams (JOLT_DBG_TRD_TWO_STAGE on the shared context), restoring the automatic choice."""
+    J.jolt_debug_set(ctx(), J.JOLT_DBG_TRD_TWO_STAGE, request.param)
+    yield request.param
+    J.jolt_debug_set(ctx(), J.JOLT_DBG_TRD_TWO_STAGE, -1)
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_blocked_tridiagonalisation_spectrum_and_subspace(dtype):
-    """T = 1024 > 768 takes the blocked multi-workgroup tridiagonalisation."""
+def test_blocked_tridiagonalisation_spectrum_and_subspace(dtype, reduction):
+    """T = 1024 > 768 takes the blocked multi-workgroup tridiagonalisation (one or two
+    stages)."""
     X = keys_cell(T=1024, H=4)
     xs, ex, desc = device_cells([X, keys_cell(T=1024, H=4, seed=5)], dtype)
     ws = workspace(desc, 2)
@@ -226,7 +236,7 @@ def test_blocked_tridiagonalisation_spectrum_and_subspace(dtype):
 
 
 @pytest.mark.parametrize("T,H", [(1001, 4), (900, 1)])
-def test_blocked_tridiagonalisation_ragged_and_rank_deficient(T, H):
+def test_blocked_tridiagonalisation_ragged_and_rank_deficient(T, H, reduction):
     """T = 1001: the last panel is ragged and rows are not 16-byte aligned; H = 1 with
     T = 900 > N = 128: the token Gram has rank 128, so the trailing columns of the
     reduction are numerically zero.  Spectrum within 1e-5 of lambda_1 (fp32 cell) and the
