@@ -43,7 +43,7 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 __host__ __device__ inline int steps_max(int n) { return n >= 3 ? (n - 3) / SB + 1 : 1; }
 
 struct SbView {
-  float *A, *P, *Q, *X, *Yp, *T, *AB, *V2;
+  float *A, *P, *Q, *X, *Yp, *T, *AB, *V2, *Tq;
   double *d, *e;
   float *tau;
 };
@@ -52,7 +52,7 @@ __host__ __device__ inline size_t sb_per_mat(int n) {
   const size_t km = n >= 3 ? (size_t)((n - 3) / SB + 1) : 1;
   const size_t nblk = (size_t)((n + SY_ROWS - 1) / SY_ROWS);
   const size_t f = 4 * (size_t)SB * n + (size_t)n * SB + nblk * SB * SB + SB * SB + (size_t)n * SBW +
-                   (size_t)n * km * SB + 64;
+                   (size_t)n * km * SB + km * (km + 1) / 2 * SB * SB + 64;
   return (f + 63) / 64 * 64;
 }
 
@@ -69,6 +69,7 @@ JOLT_DEV SbView sview(const SbArgs &a, int mat) {
   v.T = v.Yp + (int64_t)nblk * SB * SB;
   v.AB = v.T + SB * SB;
   v.V2 = v.AB + (int64_t)n * SBW;
+  v.Tq = v.V2 + (int64_t)n * steps_max(n) * SB;
   v.d = a.d + (int64_t)mat * n;
   v.e = a.e + (int64_t)mat * n;
   v.tau = a.tau + (int64_t)mat * n;
@@ -625,113 +626,265 @@ __global__ void __launch_bounds__(BG_WAVES * 64) k_sb_bulge(SbArgs a, int mat0) 
 }
 
 // ------------------------------------------- eigenvectors: U = Q2 Z (stage-2 reflectors)
-// One workgroup per matrix and slab of C columns of Z, the slab resident in LDS (fp32);
-// sweeps from the last to the first, the reflectors of one sweep (disjoint row blocks)
-// spread over the wavefronts (wavefront w takes k = w, w + 8, ...), one barrier per sweep.
-// A wavefront's reflectors of the next sweep are loaded while the current sweep is applied
-// (two register sets, one entry per lane and reflector).  Lane layout per reflector: column lane % C, rows
-// lane / C + (64 / C) q of its 32 (so that a wavefront's slab accesses spread over the LDS banks).
-constexpr int Q2_NT = 512;
-constexpr int Q2_WAVES = Q2_NT / 64;
+// The reflectors of the G = 32 sweeps s0 .. s0 + 31 at one step k act on the rows
+// s0 + g + 1 + 32 k .. + 31 (g = 0 .. 31): a parallelogram block of 63 rows whose product
+// H_{s0,k} H_{s0+1,k} ... H_{s0+31,k} is I - V T V^T (V 63 x 32, unit entry of column g in
+// row g; T upper triangular).  Applying Q2 = product of all reflectors in the order made to
+// the eigenvectors takes the groups from the last to the first and, within a group, the
+// blocks in increasing k: a reflector of a later sweep overlaps one of an earlier sweep only
+// at a step of the earlier one that is later (sweep s0 + g at step k meets sweep s0 + g' at
+// step k + 1 only for g > g'), and reflectors that do not overlap commute.
+constexpr int QG = SB;                 // sweeps per block
+constexpr int QH = SB + QG - 1;        // rows per block
+constexpr int QCW = 64;                // eigenvector columns per workgroup
+constexpr int QRING = 128;             // rows of the sliding window (63 in use + 32 prefetched), a power of 2
+constexpr int Q_NT = 256;
 
-// A wavefront's reflectors of one sweep: lane l holds entry l % 32 of each ([tau, v_1 ..]);
-// one load per reflector, the entries a lane needs come by lane exchange.
-template <int TMAX>
-struct Q2Set {
-  float e[TMAX];
-};
+__host__ __device__ inline int64_t q_group_offset(int gi, int km) {
+  return (int64_t)gi * km - (int64_t)gi * (gi - 1) / 2;    // blocks of groups 0 .. gi-1
+}
 
-template <int TMAX>
-JOLT_DEV void q2_fetch(Q2Set<TMAX> &f, const float *V2, int s, int km, int n, int wv, int lane) {
-  const int ks = (n - 3 - s) / SB + 1;
+JOLT_DEV bool refl_exists(int s, int k, int n) { return s <= n - 3 && k <= (n - 3 - s) / SB; }
+
+// T of every block, stored transposed (entry (a, b) of T at [b][a]); one wavefront per block.
+// Column g of V holds the entries 1 .. 31 of reflector (s0 + g, k) below its unit entry;
+// S = V^T V, then T[0:g, g] = -tau_g T[0:g, 0:g] S[0:g, g], T[g][g] = tau_g.
+__global__ void __launch_bounds__(512) k_sb_qt(SbArgs a, int mat0) {
+  const int mat = mat0 + blockIdx.y, n = a.n;
+  const SbView M = sview(a, mat);
+  const int km = steps_max(n);
+  const int64_t total = (int64_t)km * (km + 1) / 2;
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane & 31;
+  const int64_t blk = (int64_t)blockIdx.x * 8 + wv;
+  __shared__ float vs[8][QG][SB + 1];
+  __shared__ float ss[8][QG][QG + 1];
+  __shared__ float ts[8][QG];
+  if (blk >= total) return;
+  int gi = 0;
+  while (q_group_offset(gi + 1, km) <= blk) ++gi;
+  const int k = (int)(blk - q_group_offset(gi, km)), s0 = gi * QG;
+  const bool ex = refl_exists(s0 + g, k, n);
+  const uint32_t vb = ex ? (uint32_t)(((s0 + g) * km + k) * SB) : 0u;
+  if (lane < 32) {
+    for (int i = 0; i < SB; ++i) {
+      const float x = ldx(M.V2, vb + i);
+      vs[wv][g][i] = (i == 0) ? 1.f : (ex ? x : 0.f);
+      if (i == 0) ts[wv][g] = ex ? x : 0.f;
+    }
+  }
+  wave_sync();
+  // S[h][g] for h < g: rows of column h are offset by g - h from those of column g
+  if (lane < 32) {
+    for (int h = 0; h < QG; ++h) {
+      float acc = 0.f;
+      if (h < g)
+        for (int i = 0; i + (g - h) < SB; ++i) acc = fmaf(vs[wv][h][i + g - h], vs[wv][g][i], acc);
+      ss[wv][h][g] = acc;
+    }
+  }
+  wave_sync();
+  float t[QG];
 #pragma unroll
-  for (int t = 0; t < TMAX; ++t) {
-    const int k = wv + t * Q2_WAVES;
-    const bool live = s >= 0 && k < ks;
-    // unconditional load (a valid entry when not live; such entries are never applied), so
-    // that the loads stay in flight across the sweep's barrier until their first use
-    f.e[t] = ldx(V2, live ? (uint32_t)((s * km + k) * SB + (lane & 31)) : 0u);
+  for (int c = 0; c < QG; ++c) t[c] = 0.f;
+  const int i = g;
+#pragma unroll
+  for (int c = 0; c < QG; ++c) {
+    const float tc = ts[wv][c];
+    float acc = 0.f;
+#pragma unroll
+    for (int d = 0; d < c; ++d)
+      if (d >= i) acc = fmaf(t[d], ss[wv][d][c], acc);
+    t[c] = (i < c) ? -tc * acc : (i == c ? tc : 0.f);
+  }
+  if (lane < 32) {
+    float *To = M.Tq + (q_group_offset(gi, km) + k) * (QG * QG);
+#pragma unroll
+    for (int c = 0; c < QG; ++c) To[c * QG + i] = t[c];
   }
 }
 
-template <int C, int TMAX>
-__global__ void __launch_bounds__(Q2_NT) k_sb_q2(SbArgs a, int mat0, const double *Z, int ldz, const int32_t *kcnt,
-                                                 float *U, int64_t ldu, int64_t u_stride) {
-  constexpr int RPL = C / 2;                 // rows per lane
+// U (fp32) = Z (fp64) for the first k[mat] columns
+__global__ void k_sb_z2u(int n, const double *Z, int ldz, const int32_t *kcnt, float *U, int64_t ldu,
+                         int64_t u_stride, int kmax) {
+  const int mat = blockIdx.y, kc = kcnt[mat];
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= (int64_t)n * kmax) return;
+  const int r = (int)(q / kmax), c = (int)(q % kmax);
+  if (c < kc) U[(int64_t)mat * u_stride + (int64_t)r * ldu + c] = (float)Z[((int64_t)mat * n + r) * ldz + c];
+}
+
+// Blocks applied to a slab of QCW columns held in a sliding window of QRING rows; while a
+// block is applied the next block's 32 new rows, V entries and T are loaded into registers.
+struct QLds {
+  float z[QRING][QCW + 1];
+  float v[QH + 1][QG + 1];     // row QH stays zero (the products run over 64 rows)
+  float t[QG][QG + 1];
+  float w[QG][QCW + 1];
+  float w2[QG][QCW + 1];
+};
+
+__global__ void __launch_bounds__(Q_NT) k_sb_qapply(SbArgs a, int mat0, const int32_t *kcnt, float *U,
+                                                    int64_t ldu, int64_t u_stride) {
   const int mat = mat0 + blockIdx.y, n = a.n;
-  const int c0 = blockIdx.x * C;
-  const int kc = kcnt[mat];
+  const int c0 = blockIdx.x * QCW, kc = kcnt[mat];
   if (c0 >= kc) return;
   const SbView M = sview(a, mat);
   const int km = steps_max(n);
-  extern __shared__ float us[];
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const double *Zm = Z + (int64_t)mat * n * ldz;
-  for (int q = tid; q < n * C; q += Q2_NT) {
-    const int r = q / C, c = q % C;
-    us[q] = (c0 + c < kc) ? (float)Zm[(int64_t)r * ldz + c0 + c] : 0.f;
-  }
-  const int col = lane % C, rg = lane / C;
-  // the reflectors of one sweep touch disjoint rows: G at a time are read, reduced and
-  // written as a group, so that their LDS traffic and shuffles overlap
-  auto apply = [&](const Q2Set<TMAX> &g, int s) {
-    constexpr int G = C == 8 ? 8 : 4;
-    const int ks = (n - 3 - s) / SB + 1;
+  __shared__ QLds sm;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lr = lane & 31, lh = lane >> 5;
+  const int ct = wave & 1, kh = wave >> 1;
+  float *Um = U + (int64_t)mat * u_stride;
+  const int ncol = min(QCW, kc - c0);
+  for (int e = tid; e < QRING * (QCW + 1); e += Q_NT) (&sm.z[0][0])[e] = 0.f;
+  for (int e = tid; e < QG + 1; e += Q_NT) sm.v[QH][e] = 0.f;
+  // per-thread shares: rows (32 x QCW: 8 each), V (63 x 32: 8 each), T (32 x 32: 4 each)
+  float rz[8], rv[8], rt[4];
+  auto fetch = [&](int s0, int k, int row0, int nrows) {
+    // rows row0 .. row0 + nrows - 1 of the slab (nrows <= 32), V and T of block (s0, k)
 #pragma unroll
-    for (int t0 = 0; t0 < TMAX; t0 += G) {
-      if (wv + t0 * Q2_WAVES >= ks) break;
-      float u[G][RPL], vv[G][RPL], dot[G], tv[G];
-      int base[G], ln[G];
+    for (int u = 0; u < 8; ++u) {
+      const int e = tid + u * Q_NT, r = e / QCW, c = e % QCW;
+      rz[u] = (r < nrows && row0 + r < n && c < ncol) ? Um[(int64_t)(row0 + r) * ldu + c0 + c] : 0.f;
+    }
+    const int gi = s0 / QG;
 #pragma unroll
-      for (int e = 0; e < G; ++e) {
-        const int k = wv + (t0 + e) * Q2_WAVES;
-        const int r0 = s + 1 + k * SB;
-        ln[e] = (k < ks) ? min(SB, n - r0) : 0;
-        base[e] = r0 * C + col;
-        dot[e] = 0.f;
-#pragma unroll
-        for (int q = 0; q < RPL; ++q) {
-          const int i = rg + (64 / C) * q;
-          // every lane takes part in the exchange (its source lanes must be active)
-          const float vi = __shfl(g.e[t0 + e], i, 64);
-          vv[e][q] = (i == 0) ? 1.f : vi;
-          u[e][q] = (i < ln[e]) ? us[base[e] + i * C] : 0.f;
-          dot[e] = fmaf(vv[e][q], u[e][q], dot[e]);
-        }
-        tv[e] = __shfl(g.e[t0 + e], 0, 64);
+    for (int u = 0; u < 8; ++u) {
+      const int e = tid + u * Q_NT, j = e / QG, g = e % QG;
+      float x = 0.f;
+      if (j < QH) {
+        const int i = j - g, row = s0 + 1 + k * SB + j;
+        if (i == 0) x = 1.f;
+        else if (i > 0 && i < SB && row < n && refl_exists(s0 + g, k, n))
+          x = ldx(M.V2, (uint32_t)(((s0 + g) * km + k) * SB + i));
       }
+      rv[u] = x;
+    }
+    const float *Tb = M.Tq + (q_group_offset(gi, km) + k) * (QG * QG);
 #pragma unroll
-      for (int o = C; o < 64; o <<= 1)
+    for (int u = 0; u < 4; ++u) rt[u] = Tb[tid + u * Q_NT];
+  };
+  auto stash_vt = [&]() {
 #pragma unroll
-        for (int e = 0; e < G; ++e) dot[e] += shfl_xor(dot[e], o);
+    for (int u = 0; u < 8; ++u) {
+      const int e = tid + u * Q_NT, j = e / QG, g = e % QG;
+      if (j < QH) sm.v[j][g] = rv[u];
+    }
 #pragma unroll
-      for (int e = 0; e < G; ++e) {
-        const float td = tv[e] * dot[e];
-#pragma unroll
-        for (int q = 0; q < RPL; ++q) {
-          const int i = rg + (64 / C) * q;
-          if (i < ln[e]) us[base[e] + i * C] = fmaf(-td, vv[e][q], u[e][q]);
-        }
-      }
+    for (int u = 0; u < 4; ++u) {
+      const int e = tid + u * Q_NT;
+      sm.t[e % QG][e / QG] = rt[u];                 // T[a][b] at t[a][b]
     }
   };
-  Q2Set<TMAX> fa, fb;
-  q2_fetch<TMAX>(fa, M.V2, n - 3, km, n, wv, lane);
-  __syncthreads();
-  for (int s = n - 3; s >= 0; s -= 2) {
-    q2_fetch<TMAX>(fb, M.V2, s - 1, km, n, wv, lane);
-    apply(fa, s);
-    lds_barrier();
-    if (s == 0) break;
-    q2_fetch<TMAX>(fa, M.V2, s - 2, km, n, wv, lane);
-    apply(fb, s - 1);
-    lds_barrier();
-  }
-  __syncthreads();
-  float *Um = U + (int64_t)mat * u_stride;
-  for (int q = tid; q < n * C; q += Q2_NT) {
-    const int r = q / C, c = q % C;
-    if (c0 + c < kc) Um[(int64_t)r * ldu + c0 + c] = us[q];
+  auto stash_rows = [&](int row0) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = tid + u * Q_NT, r = e / QCW, c = e % QCW;
+      sm.z[(row0 + r) & (QRING - 1)][c] = rz[u];
+    }
+  };
+  auto store_rows = [&](int row0, int nrows) {
+    for (int e = tid; e < nrows * QCW; e += Q_NT) {
+      const int r = e / QCW, c = e % QCW;
+      if (row0 + r < n && c < ncol) Um[(int64_t)(row0 + r) * ldu + c0 + c] = sm.z[(row0 + r) & (QRING - 1)][c];
+    }
+  };
+  const int ng = km;
+  for (int gi = ng - 1; gi >= 0; --gi) {
+    const int s0 = gi * QG, kv = km - gi;
+    // window start: rows s0 + 1 .. s0 + 63 of block 0
+    fetch(s0, 0, s0 + 1, 32);
+    __syncthreads();
+    stash_rows(s0 + 1);
+    stash_vt();
+    fetch(s0, 0, s0 + 33, 31);
+    __syncthreads();
+    stash_rows(s0 + 33);
+    for (int k = 0; k < kv; ++k) {
+      const int r0 = s0 + 1 + k * SB;
+      if (k + 1 < kv) {
+        __syncthreads();
+        // next block: its V and T, and the 32 rows that enter the window
+        fetch(s0, k + 1, r0 + QH, 32);
+      }
+      __syncthreads();
+      // The block's products on the fp32 matrix cores (32x32x2; lane (lr, lh) supplies row or
+      // column lr at k = lh, acc[q] is element (8 (q / 4) + 4 lh + q % 4, lr) of the tile).
+      // W = V^T Z: tile of columns 32 ct, the 64 block rows split between two wavefronts.
+      {
+        f32x16_t acc;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+#pragma unroll
+        for (int st = 0; st < 16; ++st) {
+          const int j = 32 * kh + 2 * st + lh;
+          acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.v[j][lr], sm.z[(r0 + j) & (QRING - 1)][32 * ct + lr], acc, 0, 0, 0);
+        }
+        if (kh == 1) {
+#pragma unroll
+          for (int q = 0; q < 16; ++q) sm.w2[8 * (q >> 2) + 4 * lh + (q & 3)][32 * ct + lr] = acc[q];
+        }
+        __syncthreads();
+        if (kh == 0) {
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            const int g = 8 * (q >> 2) + 4 * lh + (q & 3);
+            sm.w[g][32 * ct + lr] = acc[q] + sm.w2[g][32 * ct + lr];
+          }
+        }
+      }
+      __syncthreads();
+      // W2 = T W (T upper triangular), the 32 inner indices split between two wavefronts
+      {
+        f32x16_t acc;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+#pragma unroll
+        for (int st = 0; st < 8; ++st) {
+          const int h = 16 * kh + 2 * st + lh;
+          acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.t[lr][h], sm.w[h][32 * ct + lr], acc, 0, 0, 0);
+        }
+        if (kh == 1) {
+#pragma unroll
+          for (int q = 0; q < 16; ++q) sm.w2[8 * (q >> 2) + 4 * lh + (q & 3)][32 * ct + lr] = acc[q];
+        }
+        __syncthreads();
+        if (kh == 0) {
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            const int g = 8 * (q >> 2) + 4 * lh + (q & 3);
+            sm.w2[g][32 * ct + lr] += acc[q];
+          }
+        }
+      }
+      __syncthreads();
+      // Z -= V W2: tile (rows 32 kh, columns 32 ct) per wavefront
+      {
+        f32x16_t acc;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+#pragma unroll
+        for (int st = 0; st < 16; ++st) {
+          const int g = 2 * st + lh;
+          acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.v[32 * kh + lr][g], sm.w2[g][32 * ct + lr], acc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int j = 32 * kh + 8 * (q >> 2) + 4 * lh + (q & 3);
+          if (j < QH) sm.z[(r0 + j) & (QRING - 1)][32 * ct + lr] -= acc[q];
+        }
+      }
+      __syncthreads();
+      if (k + 1 < kv) {
+        // rows r0 .. r0 + 31 leave the window; the prefetched rows and the next V, T enter
+        store_rows(r0, SB);
+        __syncthreads();
+        stash_rows(r0 + QH);
+        stash_vt();
+      } else {
+        store_rows(r0, min(QH, n - r0));
+      }
+    }
+    __syncthreads();
   }
 }
 
@@ -809,20 +962,11 @@ hipError_t launch_sb_q2(const EigBatch &b, const float *work, const InvitWork &w
   a.d = b.d;
   a.e = b.e;
   a.tau = b.tau;
-  if (n <= 4096) {
-    const size_t shm = (size_t)n * 8 * sizeof(float);
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_sb_q2<8, 16>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((k_sb_q2<8, 16>), dim3((kmax + 7) / 8, nm), dim3(Q2_NT), shm, st, a, 0, w.Z, w.ldz, w.k, U,
-                       ldu, u_stride);
-  } else {
-    const size_t shm = (size_t)n * 4 * sizeof(float);
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_sb_q2<4, 32>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((k_sb_q2<4, 32>), dim3((kmax + 3) / 4, nm), dim3(Q2_NT), shm, st, a, 0, w.Z, w.ldz, w.k, U,
-                       ldu, u_stride);
-  }
+  const int km = steps_max(n);
+  const int64_t blocks = (int64_t)km * (km + 1) / 2;
+  hipLaunchKernelGGL(k_sb_qt, dim3((unsigned)((blocks + 7) / 8), nm), dim3(512), 0, st, a, 0);
+  hipLaunchKernelGGL(k_sb_z2u, dim3((unsigned)(((int64_t)n * kmax + 255) / 256), nm), dim3(256), 0, st, n, w.Z, w.ldz,
+                     w.k, U, ldu, u_stride, kmax);
+  hipLaunchKernelGGL(k_sb_qapply, dim3((kmax + QCW - 1) / QCW, nm), dim3(Q_NT), 0, st, a, 0, w.k, U, ldu, u_stride);
   return hipGetLastError();
 }
