@@ -126,7 +126,7 @@ __global__ void __launch_bounds__(PQ_NT) k_sb_panel(SbArgs a, int p, int mat0) {
   const int k0 = p * SB, r0 = k0 + SB, w = min(SB, n - k0), m = n - r0;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   __shared__ float red[PQ_NT / 64][SB];
-  __shared__ float rowj[SB], dv[SB], Ts[SB][SB + 1];
+  __shared__ float rowj[SB], dv[SB], Ts[SB][SB + 1], Tw[SB][SB + 1];
   __shared__ float sc[4];
   for (int q = tid; q < SB * SBW; q += PQ_NT) {
     const int j = q / SBW, dd = q - j * SBW, row = k0 + j + dd;
@@ -228,21 +228,30 @@ __global__ void __launch_bounds__(PQ_NT) k_sb_panel(SbArgs a, int p, int mat0) {
       const float alpha = __shfl(rj, nj, 64), sig = __shfl(gsum, nj, 64);
       float t, b, sl;
       house(alpha, sig, t, b, sl);
-      if (lane < SB) dv[lane] = (lane == nj) ? 0.f : fmaf(sl, gsum, rj);
-      if (lane == 0) { sc[0] = t; sc[1] = b; sc[2] = sl; M.tau[k0 + nj] = t; }
-      wave_sync();
-      if (lane < nj) {
-        float acc = 0.f;
-        for (int c = lane; c < nj; ++c) acc = fmaf(Ts[lane][c], dv[c], acc);
-        Ts[lane][nj] = -t * acc;
+      if (lane < SB) {
+        const float dl = (lane == nj) ? 0.f : fmaf(sl, gsum, rj);
+        dv[lane] = dl;
+        Ts[lane][nj] = dl;                       // (V^T v_nj)_lane for lane < nj, kept for T
       }
-      if (lane == nj) Ts[nj][nj] = t;
+      if (lane == 0) { sc[0] = t; sc[1] = b; sc[2] = sl; M.tau[k0 + nj] = t; }
     }
     __syncthreads();
   }
   if (tid >= jmax && tid < SB) M.tau[k0 + tid] = 0.f;
   __syncthreads();
-  for (int q = tid; q < SB * SB; q += PQ_NT) M.T[q] = Ts[q / SB][q % SB];
+  // T by columns from the kept dot products D = Ts (strict upper part): lane i builds row i of T
+  // in Tw, reading only its own row, so the columns need no synchronisation
+  if (tid < SB) {
+    const int i = tid;
+    for (int c = 0; c < SB; ++c) {
+      const float tc = c < jmax ? M.tau[k0 + c] : 0.f;
+      float acc = 0.f;
+      for (int d = i; d < c; ++d) acc = fmaf(Tw[i][d], Ts[d][c], acc);
+      Tw[i][c] = (i < c) ? -tc * acc : (i == c ? tc : 0.f);
+    }
+  }
+  __syncthreads();
+  for (int q = tid; q < SB * SB; q += PQ_NT) M.T[q] = Tw[q / SB][q % SB];
   // zeros above the panel's reflectors inside their back-transform block
   const int z0 = (k0 / BT_BLOCK) * BT_BLOCK + SB;
   for (int q = tid; q < (r0 - z0) * SB; q += PQ_NT) {
@@ -715,6 +724,9 @@ __global__ void k_sb_z2u(int n, const double *Z, int ldz, const int32_t *kcnt, f
 
 // Blocks applied to a slab of QCW columns held in a sliding window of QRING rows; while a
 // block is applied the next block's 32 new rows, V entries and T are loaded into registers.
+// Inside a group the barriers wait for LDS traffic only (rows that leave the window are not
+// read again in the group, V and T are read-only), so those loads and the stores of the
+// leaving rows stay in flight; a full barrier separates the groups.
 struct QLds {
   float z[QRING][QCW + 1];
   float v[QH + 1][QG + 1];     // row QH stays zero (the products run over 64 rows)
@@ -802,28 +814,30 @@ __global__ void __launch_bounds__(Q_NT) k_sb_qapply(SbArgs a, int mat0, const in
     for (int k = 0; k < kv; ++k) {
       const int r0 = s0 + 1 + k * SB;
       if (k + 1 < kv) {
-        __syncthreads();
         // next block: its V and T, and the 32 rows that enter the window
         fetch(s0, k + 1, r0 + QH, 32);
       }
-      __syncthreads();
+      lds_barrier();
       // The block's products on the fp32 matrix cores (32x32x2; lane (lr, lh) supplies row or
       // column lr at k = lh, acc[q] is element (8 (q / 4) + 4 lh + q % 4, lr) of the tile).
       // W = V^T Z: tile of columns 32 ct, the 64 block rows split between two wavefronts.
       {
-        f32x16_t acc;
+        f32x16_t acc, acc1;
 #pragma unroll
-        for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+        for (int q = 0; q < 16; ++q) { acc[q] = 0.f; acc1[q] = 0.f; }
 #pragma unroll
-        for (int st = 0; st < 16; ++st) {
+        for (int st = 0; st < 16; st += 2) {          // two independent chains
           const int j = 32 * kh + 2 * st + lh;
           acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.v[j][lr], sm.z[(r0 + j) & (QRING - 1)][32 * ct + lr], acc, 0, 0, 0);
+          acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.v[j + 2][lr], sm.z[(r0 + j + 2) & (QRING - 1)][32 * ct + lr],
+                                                      acc1, 0, 0, 0);
         }
+        acc += acc1;
         if (kh == 1) {
 #pragma unroll
           for (int q = 0; q < 16; ++q) sm.w2[8 * (q >> 2) + 4 * lh + (q & 3)][32 * ct + lr] = acc[q];
         }
-        __syncthreads();
+        lds_barrier();
         if (kh == 0) {
 #pragma unroll
           for (int q = 0; q < 16; ++q) {
@@ -832,22 +846,24 @@ __global__ void __launch_bounds__(Q_NT) k_sb_qapply(SbArgs a, int mat0, const in
           }
         }
       }
-      __syncthreads();
+      lds_barrier();
       // W2 = T W (T upper triangular), the 32 inner indices split between two wavefronts
       {
-        f32x16_t acc;
+        f32x16_t acc, acc1;
 #pragma unroll
-        for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+        for (int q = 0; q < 16; ++q) { acc[q] = 0.f; acc1[q] = 0.f; }
 #pragma unroll
-        for (int st = 0; st < 8; ++st) {
+        for (int st = 0; st < 8; st += 2) {
           const int h = 16 * kh + 2 * st + lh;
           acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.t[lr][h], sm.w[h][32 * ct + lr], acc, 0, 0, 0);
+          acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.t[lr][h + 2], sm.w[h + 2][32 * ct + lr], acc1, 0, 0, 0);
         }
+        acc += acc1;
         if (kh == 1) {
 #pragma unroll
           for (int q = 0; q < 16; ++q) sm.w2[8 * (q >> 2) + 4 * lh + (q & 3)][32 * ct + lr] = acc[q];
         }
-        __syncthreads();
+        lds_barrier();
         if (kh == 0) {
 #pragma unroll
           for (int q = 0; q < 16; ++q) {
@@ -856,28 +872,31 @@ __global__ void __launch_bounds__(Q_NT) k_sb_qapply(SbArgs a, int mat0, const in
           }
         }
       }
-      __syncthreads();
+      lds_barrier();
       // Z -= V W2: tile (rows 32 kh, columns 32 ct) per wavefront
       {
-        f32x16_t acc;
+        f32x16_t acc, acc1;
 #pragma unroll
-        for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+        for (int q = 0; q < 16; ++q) { acc[q] = 0.f; acc1[q] = 0.f; }
 #pragma unroll
-        for (int st = 0; st < 16; ++st) {
+        for (int st = 0; st < 16; st += 2) {
           const int g = 2 * st + lh;
           acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.v[32 * kh + lr][g], sm.w2[g][32 * ct + lr], acc, 0, 0, 0);
+          acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.v[32 * kh + lr][g + 2], sm.w2[g + 2][32 * ct + lr], acc1, 0, 0,
+                                                      0);
         }
+        acc += acc1;
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
           const int j = 32 * kh + 8 * (q >> 2) + 4 * lh + (q & 3);
           if (j < QH) sm.z[(r0 + j) & (QRING - 1)][32 * ct + lr] -= acc[q];
         }
       }
-      __syncthreads();
+      lds_barrier();
       if (k + 1 < kv) {
         // rows r0 .. r0 + 31 leave the window; the prefetched rows and the next V, T enter
         store_rows(r0, SB);
-        __syncthreads();
+        lds_barrier();
         stash_rows(r0 + QH);
         stash_vt();
       } else {
