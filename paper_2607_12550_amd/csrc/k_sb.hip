@@ -93,6 +93,34 @@ JOLT_DEV void stx(float *base, uint32_t idx, float v) {
   *reinterpret_cast<float *>(reinterpret_cast<char *>(base) + 4u * idx) = v;
 }
 
+// Lane exchanges without LDS: the sum over the lane pair (l, l + 32) by v_permlane32_swap
+// (two copies of x leave the lower lane's value in r[0] and the upper's in r[1], in both
+// lanes), a lane's value as a wave-uniform scalar by readlane, and the sum over lanes
+// 0 .. 31 by DPP moves within rows of 16 (quad swaps, half-row and row mirrors) plus two
+// readlanes.
+JOLT_DEV float pair_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+JOLT_DEV float lane_value(float x, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l)); }
+JOLT_DEV float dpp_add(float x, int ctrl_sel) {
+  int y;
+  switch (ctrl_sel) {
+    case 0: y = __builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false); break;   // lanes ^ 1
+    case 1: y = __builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false); break;   // lanes ^ 2
+    case 2: y = __builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x141, 0xF, 0xF, false); break;  // half-row mirror
+    default: y = __builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x140, 0xF, 0xF, false); break; // row mirror
+  }
+  return x + __int_as_float(y);
+}
+JOLT_DEV float sum_lanes32(float x) {
+  x = dpp_add(x, 0);
+  x = dpp_add(x, 1);
+  x = dpp_add(x, 2);
+  x = dpp_add(x, 3);
+  return lane_value(x, 0) + lane_value(x, 16);
+}
+
 // Workgroup barrier for LDS traffic only: waits for this wavefront's LDS operations, not for
 // its global loads, so that loads issued before the barrier stay in flight across it.
 JOLT_DEV void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
@@ -514,8 +542,8 @@ __global__ void __launch_bounds__(BG_WAVES * 64) k_sb_bulge(SbArgs a, int mat0) 
         const int i = 16 * h + q;
         if (i >= 1) part = fmaf(L[q], L[q], part);
       }
-      const float sigma = __shfl(part, 0, 64) + __shfl(part, 32, 64);
-      const float alpha = __shfl(L[0], 0, 64);
+      const float sigma = lane_value(part, 0) + lane_value(part, 32);
+      const float alpha = lane_value(L[0], 0);
       float tau, beta, scal;
       house(alpha, sigma, tau, beta, scal);
       float *vbw = vb[wv], *wbw = wb[wv];
@@ -534,7 +562,7 @@ __global__ void __launch_bounds__(BG_WAVES * 64) k_sb_bulge(SbArgs a, int mat0) 
         float wc = 0.f;
 #pragma unroll
         for (int q = 0; q < 16; ++q) wc = fmaf(vbw[16 * h + q], L[q], wc);
-        wc += shfl_xor(wc, 32);
+        wc = pair_sum(wc);
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
           const int i = 16 * h + q;
@@ -577,12 +605,8 @@ __global__ void __launch_bounds__(BG_WAVES * 64) k_sb_bulge(SbArgs a, int mat0) 
       float pj = 0.f;
 #pragma unroll
       for (int q = 0; q < 16; ++q) pj = fmaf(tbw[(16 * h + q) * (SB + 1) + lj], vbw[16 * h + q], pj);
-      pj += shfl_xor(pj, 32);
-      pj *= tau;
-      float pv = (h == 0) ? pj * vl : 0.f;
-#pragma unroll
-      for (int o = 1; o < 32; o <<= 1) pv += shfl_xor(pv, o);
-      pv = __shfl(pv, 0, 64);
+      pj = pair_sum(pj) * tau;
+      const float pv = sum_lanes32(pj * vl);
       if (h == 0) wbw[lj] = fmaf(-0.5f * tau * pv, vl, pj);
       wave_sync();
 #pragma unroll
@@ -597,7 +621,7 @@ __global__ void __launch_bounds__(BG_WAVES * 64) k_sb_bulge(SbArgs a, int mat0) 
       float yi = 0.f;
 #pragma unroll
       for (int q = 0; q < 16; ++q) yi = fmaf(E[q], vbw[16 * h + q], yi);
-      yi += shfl_xor(yi, 32);
+      yi = pair_sum(yi);
 #pragma unroll
       for (int q = 0; q < 16; ++q) E[q] = fmaf(-tau * yi, vbw[16 * h + q], E[q]);
       if (ne >= 2) {
