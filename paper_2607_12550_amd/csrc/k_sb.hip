@@ -43,7 +43,7 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 __host__ __device__ inline int steps_max(int n) { return n >= 3 ? (n - 3) / SB + 1 : 1; }
 
 struct SbView {
-  float *A, *P, *Q, *X, *Yp, *T, *AB, *V2, *Tq;
+  float *A, *P, *Q, *X, *Yp, *Sp, *T, *AB, *V2, *Tq;
   double *d, *e;
   float *tau;
 };
@@ -51,7 +51,7 @@ struct SbView {
 __host__ __device__ inline size_t sb_per_mat(int n) {
   const size_t km = n >= 3 ? (size_t)((n - 3) / SB + 1) : 1;
   const size_t nblk = (size_t)((n + SY_ROWS - 1) / SY_ROWS);
-  const size_t f = 4 * (size_t)SB * n + (size_t)n * SB + nblk * SB * SB + SB * SB + (size_t)n * SBW +
+  const size_t f = 4 * (size_t)SB * n + (size_t)n * SB + 2 * nblk * SB * SB + SB * SB + (size_t)n * SBW +
                    (size_t)n * km * SB + km * (km + 1) / 2 * SB * SB + 64;
   return (f + 63) / 64 * 64;
 }
@@ -66,7 +66,8 @@ JOLT_DEV SbView sview(const SbArgs &a, int mat) {
   v.Q = v.P + (int64_t)2 * SB * n;
   v.X = v.Q + (int64_t)2 * SB * n;
   v.Yp = v.X + (int64_t)n * SB;
-  v.T = v.Yp + (int64_t)nblk * SB * SB;
+  v.Sp = v.Yp + (int64_t)nblk * SB * SB;
+  v.T = v.Sp + (int64_t)nblk * SB * SB;
   v.AB = v.T + SB * SB;
   v.V2 = v.AB + (int64_t)n * SBW;
   v.Tq = v.V2 + (int64_t)n * steps_max(n) * SB;
@@ -136,14 +137,14 @@ JOLT_DEV void wave_sync() {
 // reflector j and forms the sums the next column needs: with g_c = sum_{r > j+1} x_r[j+1] x_r[c]
 // (rows as updated by reflector j), sigma_{j+1} = g_{j+1} and
 //   d_c = v_{j+1}^T P[:, c] = scal g_c + P[j+1][c]   for every c != j + 1,
-// which are the apply-dots for c > j + 1 and the entries (V^T v_{j+1})_c of the T
-// recurrence T[0:j+1, j+1] = -tau T[0:j+1, 0:j+1] (V^T v_{j+1}) for c < j + 1.
+// which are the apply-dots for c > j + 1 (columns left of j are neither read nor written
+// by the pass; the block factor T is formed later from V^T V).
 // Eight lanes share a row (four columns each), so a wavefront reads eight whole rows per
 // load; the entries x_r[j] and x_r[j+1] are exchanged within the eight lanes.
 // Writes: the diagonal block and R into the band buffer (zeros past the band), V explicit
 // into the panel (unit at row j, zeros above, and zeros in the rows [blk + SB, r0) of the
-// panel's columns, blk = k0 rounded down to the back-transform's block of 128 reflectors),
-// tau and T.
+// panel's columns, blk = k0 rounded down to the back-transform's block of 128 reflectors)
+// and tau.
 JOLT_DEV float pick4(const float (&x)[4], int u) {
   return u == 0 ? x[0] : (u == 1 ? x[1] : (u == 2 ? x[2] : x[3]));
 }
@@ -154,7 +155,7 @@ __global__ void __launch_bounds__(PQ_NT) k_sb_panel(SbArgs a, int p, int mat0) {
   const int k0 = p * SB, r0 = k0 + SB, w = min(SB, n - k0), m = n - r0;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   __shared__ float red[PQ_NT / 64][SB];
-  __shared__ float rowj[SB], dv[SB], Ts[SB][SB + 1], Tw[SB][SB + 1];
+  __shared__ float rowj[SB], dv[SB];
   __shared__ float sc[4];
   for (int q = tid; q < SB * SBW; q += PQ_NT) {
     const int j = q / SBW, dd = q - j * SBW, row = k0 + j + dd;
@@ -162,7 +163,6 @@ __global__ void __launch_bounds__(PQ_NT) k_sb_panel(SbArgs a, int p, int mat0) {
     if (dd < SB - j) M.AB[(int64_t)(k0 + j) * SBW + dd] = M.A[(int64_t)row * n + k0 + j];
     else if (dd > SB) M.AB[(int64_t)(k0 + j) * SBW + dd] = 0.f;
   }
-  for (int q = tid; q < SB * (SB + 1); q += PQ_NT) (&Ts[0][0])[q] = 0.f;
   if (m <= 0) {
     if (tid < w) M.tau[k0 + tid] = 0.f;
     return;
@@ -182,55 +182,71 @@ __global__ void __launch_bounds__(PQ_NT) k_sb_panel(SbArgs a, int p, int mat0) {
       for (int u = 0; u < 4; ++u) d4[u] = dv[c4 + u];
     }
     float g4[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int r = rfirst; r < m; r += RSTEP) {
-      if (r < j) continue;                       // the eight lanes of a row agree
-      float *rp = M.A + (int64_t)(r0 + r) * n + k0 + c4;
-      float x[4];
-      if (vec) {
-        const jf4 v = gload_f4(rp);
-        x[0] = v[0]; x[1] = v[1]; x[2] = v[2]; x[3] = v[3];
-      } else {
+    // eight rows per batch: their loads are issued together (the rows a thread stores are
+    // never reloaded within the pass, but the compiler cannot prove it across iterations)
+    constexpr int RB8 = 8;
+    for (int rb = rfirst; rb < m; rb += RB8 * RSTEP) {
+      float xb[RB8][4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) x[u] = rp[u];
-      }
-      if (j >= 0) {
-        const float xj = __shfl(pick4(x, j & 3), grp0 | (j >> 2), 64);
-        const float vr = (r == j) ? 1.f : xj * sj;
-        const float tv = tj * vr;
+      for (int e = 0; e < RB8; ++e) {
+        const int r = rb + e * RSTEP;
+        const float *rp = M.A + (int64_t)(r0 + r) * n + k0 + c4;
+        xb[e][0] = xb[e][1] = xb[e][2] = xb[e][3] = 0.f;
+        if (r < m && r >= j && c4 + 3 >= j) {      // columns left of j take no part
+          if (vec) {
+            const jf4 v = gload_f4(rp);
+            xb[e][0] = v[0]; xb[e][1] = v[1]; xb[e][2] = v[2]; xb[e][3] = v[3];
+          } else {
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int c = c4 + u;
-          if (c > j) x[u] = fmaf(-tv, d4[u], x[u]);
-          if (c == j) x[u] = vr;
+            for (int u = 0; u < 4; ++u) xb[e][u] = rp[u];
+          }
         }
-        if (r == j) {
+      }
+#pragma unroll
+      for (int e = 0; e < RB8; ++e) {
+        const int r = rb + e * RSTEP;
+        if (r >= m || r < j) continue;             // the eight lanes of a row agree
+        float *rp = M.A + (int64_t)(r0 + r) * n + k0 + c4;
+        float (&x)[4] = xb[e];
+        if (j >= 0) {
+          const float xj = __shfl(pick4(x, j & 3), grp0 | (j >> 2), 64);
+          const float vr = (r == j) ? 1.f : xj * sj;
+          const float tv = tj * vr;
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
             const int c = c4 + u;
-            if (c == j) M.AB[(int64_t)(k0 + j) * SBW + SB] = bj;
-            if (c > j) { M.AB[(int64_t)(k0 + c) * SBW + SB + j - c] = x[u]; x[u] = 0.f; }
+            if (c > j) x[u] = fmaf(-tv, d4[u], x[u]);
+            if (c == j) x[u] = vr;
+          }
+          if (r == j) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const int c = c4 + u;
+              if (c == j) M.AB[(int64_t)(k0 + j) * SBW + SB] = bj;
+              if (c > j) { M.AB[(int64_t)(k0 + c) * SBW + SB + j - c] = x[u]; x[u] = 0.f; }
+            }
+          }
+          if (c4 + 3 >= j) {                       // columns left of j are unchanged
+            if (vec) {
+              jf4 v;
+              v[0] = x[0]; v[1] = x[1]; v[2] = x[2]; v[3] = x[3];
+              gstore_f4(rp, v);
+            } else {
+#pragma unroll
+              for (int u = 0; u < 4; ++u) rp[u] = x[u];
+            }
           }
         }
-        if (c4 + 3 >= j) {                       // columns left of j are unchanged
-          if (vec) {
-            jf4 v;
-            v[0] = x[0]; v[1] = x[1]; v[2] = x[2]; v[3] = x[3];
-            gstore_f4(rp, v);
-          } else {
+        if (nj < jmax) {
+          if (r == nj) {
 #pragma unroll
-            for (int u = 0; u < 4; ++u) rp[u] = x[u];
+            for (int u = 0; u < 4; ++u) rowj[c4 + u] = x[u];
           }
-        }
-      }
-      if (nj < jmax) {
-        if (r == nj) {
+          if (r > nj) {
+            const float xn = __shfl(pick4(x, nj & 3), grp0 | (nj >> 2), 64);
 #pragma unroll
-          for (int u = 0; u < 4; ++u) rowj[c4 + u] = x[u];
-        }
-        if (r > nj) {
-          const float xn = __shfl(pick4(x, nj & 3), grp0 | (nj >> 2), 64);
-#pragma unroll
-          for (int u = 0; u < 4; ++u) g4[u] = fmaf(xn, x[u], g4[u]);
+            for (int u = 0; u < 4; ++u) g4[u] = fmaf(xn, x[u], g4[u]);
+          }
         }
       }
     }
@@ -256,30 +272,13 @@ __global__ void __launch_bounds__(PQ_NT) k_sb_panel(SbArgs a, int p, int mat0) {
       const float alpha = __shfl(rj, nj, 64), sig = __shfl(gsum, nj, 64);
       float t, b, sl;
       house(alpha, sig, t, b, sl);
-      if (lane < SB) {
-        const float dl = (lane == nj) ? 0.f : fmaf(sl, gsum, rj);
-        dv[lane] = dl;
-        Ts[lane][nj] = dl;                       // (V^T v_nj)_lane for lane < nj, kept for T
-      }
+      if (lane < SB) dv[lane] = (lane == nj) ? 0.f : fmaf(sl, gsum, rj);
       if (lane == 0) { sc[0] = t; sc[1] = b; sc[2] = sl; M.tau[k0 + nj] = t; }
     }
     __syncthreads();
   }
   if (tid >= jmax && tid < SB) M.tau[k0 + tid] = 0.f;
   __syncthreads();
-  // T by columns from the kept dot products D = Ts (strict upper part): lane i builds row i of T
-  // in Tw, reading only its own row, so the columns need no synchronisation
-  if (tid < SB) {
-    const int i = tid;
-    for (int c = 0; c < SB; ++c) {
-      const float tc = c < jmax ? M.tau[k0 + c] : 0.f;
-      float acc = 0.f;
-      for (int d = i; d < c; ++d) acc = fmaf(Tw[i][d], Ts[d][c], acc);
-      Tw[i][c] = (i < c) ? -tc * acc : (i == c ? tc : 0.f);
-    }
-  }
-  __syncthreads();
-  for (int q = tid; q < SB * SB; q += PQ_NT) M.T[q] = Tw[q / SB][q % SB];
   // zeros above the panel's reflectors inside their back-transform block
   const int z0 = (k0 / BT_BLOCK) * BT_BLOCK + SB;
   for (int q = tid; q < (r0 - z0) * SB; q += PQ_NT) {
@@ -293,11 +292,11 @@ __global__ void __launch_bounds__(PQ_NT) k_sb_panel(SbArgs a, int p, int mat0) {
 // workgroup owns 128 rows of X and sweeps all columns of A22 in chunks of 32: chunks left
 // of its diagonal block are read as stored, chunks right of it transposed from the rows
 // below, the diagonal chunks entry by entry.  fp32 MFMA 32x32x2 (four wavefronts, 32 rows
-// each).  Epilogue: X = X1 T (T upper triangular), and this block's term of Y = V^T X.
+// each).  Epilogue: X1 stored, and this block's terms of V^T X1 and V^T V (the block
+// factor T and X = X1 T are formed by the Z kernel).
 struct SyLds {
   float As[SY_ROWS][SB + 1];
   float Vs[SB][SB + 1];
-  float Ts[SB][SB + 1];
   float Vb[SY_ROWS][SB + 1];
 };
 
@@ -374,41 +373,39 @@ __global__ void __launch_bounds__(SY_NT) k_sb_symm(SbArgs a, int p, int mat0) {
   __syncthreads();
 #pragma unroll
   for (int q = 0; q < 16; ++q) sm.As[32 * wave + 8 * (q >> 2) + 4 * lh + (q & 3)][lr] = acc[q];
-  for (int q = tid; q < SB * SB; q += SY_NT) sm.Ts[q / SB][q % SB] = M.T[q];
   for (int q = tid; q < SY_ROWS * SB; q += SY_NT) {
     const int i = q / SB, c = q % SB;
     sm.Vb[i][c] = (i0 + i < m) ? M.A[(int64_t)(r0 + i0 + i) * n + k0 + c] : 0.f;
   }
   __syncthreads();
-  const int xi = tid >> 1, xc = (tid & 1) * 16;
-  float xo[16];
+  {
+    const int xi = tid >> 1, xc = (tid & 1) * 16;
+    if (i0 + xi < m) {
 #pragma unroll
-  for (int u = 0; u < 16; ++u) {
-    const int c = xc + u;
-    float s = 0.f;
-    for (int k = 0; k <= c; ++k) s = fmaf(sm.As[xi][k], sm.Ts[k][c], s);
-    xo[u] = s;
+      for (int u = 0; u < 16; ++u) M.X[(int64_t)(i0 + xi) * SB + xc + u] = sm.As[xi][xc + u];
+    }
   }
-  __syncthreads();
-#pragma unroll
-  for (int u = 0; u < 16; ++u) sm.As[xi][xc + u] = xo[u];
-  if (i0 + xi < m) {
-#pragma unroll
-    for (int u = 0; u < 16; ++u) M.X[(int64_t)(i0 + xi) * SB + xc + u] = xo[u];
-  }
-  __syncthreads();
   const int ya = tid >> 3, yc = (tid & 7) * 4;
-  float yo[4] = {0.f, 0.f, 0.f, 0.f};
+  float yo[4] = {0.f, 0.f, 0.f, 0.f}, so[4] = {0.f, 0.f, 0.f, 0.f};
   for (int i = 0; i < SY_ROWS; ++i) {
     const float v = sm.Vb[i][ya];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) yo[u] = fmaf(v, sm.As[i][yc + u], yo[u]);
+    for (int u = 0; u < 4; ++u) {
+      yo[u] = fmaf(v, sm.As[i][yc + u], yo[u]);
+      so[u] = fmaf(v, sm.Vb[i][yc + u], so[u]);
+    }
   }
 #pragma unroll
-  for (int u = 0; u < 4; ++u) M.Yp[((int64_t)blockIdx.x * SB + ya) * SB + yc + u] = yo[u];
+  for (int u = 0; u < 4; ++u) {
+    M.Yp[((int64_t)blockIdx.x * SB + ya) * SB + yc + u] = yo[u];
+    M.Sp[((int64_t)blockIdx.x * SB + ya) * SB + yc + u] = so[u];
+  }
 }
 
 // ------------------------------------- stage 1: Z = X - (1/2) V (T^T Y) and the update panels
+// From the block terms: S = V^T V and Y1 = V^T X1 summed in a fixed order, T by the
+// recurrence T[0:c, c] = -tau_c T[0:c, 0:c] S[0:c, c] (one row per thread, in registers),
+// Y = Y1 T, M = T^T Y; then per row X = X1 T and Z = X - (1/2) V M.  Writes
 // P = [V; Z] and Q = [Z; V] (rows = panel columns, indexed by matrix row), so that the
 // rank-2SB update A22 -= V Z^T + Z V^T is the single product P^T Q.
 __global__ void __launch_bounds__(SY_NT) k_sb_zform(SbArgs a, int p, int mat0) {
@@ -418,39 +415,71 @@ __global__ void __launch_bounds__(SY_NT) k_sb_zform(SbArgs a, int p, int mat0) {
   const int i0 = blockIdx.x * SY_ROWS;
   if (m < 2 || i0 >= m) return;
   const int nblk = (m + SY_ROWS - 1) / SY_ROWS;
-  __shared__ float Ys[SB][SB + 1], Ts[SB][SB + 1], Ms[SB][SB + 1];
+  __shared__ float Ys[SB][SB + 1], Ss[SB][SB + 1], Tw[SB][SB + 1], Ms[SB][SB + 1];
   const int tid = threadIdx.x;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     const int e = tid * 4 + u;
-    float s = 0.f;
-    for (int b = 0; b < nblk; ++b) s += M.Yp[(int64_t)b * SB * SB + e];
-    Ys[e / SB][e % SB] = s;
-    Ts[e / SB][e % SB] = M.T[e];
+    float sy = 0.f, ss = 0.f;
+    for (int b = 0; b < nblk; ++b) {
+      sy += M.Yp[(int64_t)b * SB * SB + e];
+      ss += M.Sp[(int64_t)b * SB * SB + e];
+    }
+    Ys[e / SB][e % SB] = sy;
+    Ss[e / SB][e % SB] = ss;
+  }
+  __syncthreads();
+  if (tid < SB) {
+    // row i of T in registers (its entries left of the diagonal are zero, so every column
+    // sums over all earlier entries)
+    const int i = tid;
+    float trow[SB];
+#pragma unroll
+    for (int c = 0; c < SB; ++c) {
+      const float tc = M.tau[k0 + c];
+      float acc = 0.f;
+#pragma unroll
+      for (int d = 0; d < c; ++d) acc = fmaf(trow[d], Ss[d][c], acc);
+      trow[c] = (i < c) ? -tc * acc : (i == c ? tc : 0.f);
+    }
+#pragma unroll
+    for (int c = 0; c < SB; ++c) Tw[i][c] = trow[c];
+  }
+  __syncthreads();
+  // Y = Y1 T into Ms, then M = T^T Y into Ys
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int e = tid * 4 + u, ra = e / SB, c = e % SB;
+    float acc = 0.f;
+    for (int k = 0; k <= c; ++k) acc = fmaf(Ys[ra][k], Tw[k][c], acc);
+    Ms[ra][c] = acc;
   }
   __syncthreads();
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     const int e = tid * 4 + u, ra = e / SB, c = e % SB;
-    float s = 0.f;
-    for (int k = 0; k <= ra; ++k) s = fmaf(Ts[k][ra], Ys[k][c], s);
-    Ms[ra][c] = s;
+    float acc = 0.f;
+    for (int k = 0; k <= ra; ++k) acc = fmaf(Tw[k][ra], Ms[k][c], acc);
+    Ys[ra][c] = acc;
   }
   __syncthreads();
   const int i = tid >> 1, cb = (tid & 1) * 16;
   const int r = i0 + i;
   if (r >= m) return;
-  float v[SB];
+  float v[SB], x1[SB];
   const float *vp = M.A + (int64_t)(r0 + r) * n + k0;
 #pragma unroll
-  for (int c = 0; c < SB; ++c) v[c] = vp[c];
+  for (int c = 0; c < SB; ++c) { v[c] = vp[c]; x1[c] = M.X[(int64_t)r * SB + c]; }
 #pragma unroll
   for (int u = 0; u < 16; ++u) {
     const int c = cb + u;
-    float s = 0.f;
+    float sx = 0.f, sm_ = 0.f;
 #pragma unroll
-    for (int q = 0; q < SB; ++q) s = fmaf(v[q], Ms[q][c], s);
-    const float z = fmaf(-0.5f, s, M.X[(int64_t)r * SB + c]);
+    for (int q = 0; q < SB; ++q) {
+      sx = fmaf(x1[q], Tw[q][c], sx);
+      sm_ = fmaf(v[q], Ys[q][c], sm_);
+    }
+    const float z = fmaf(-0.5f, sm_, sx);
     float vc = 0.f;
 #pragma unroll
     for (int q = 0; q < SB; ++q) vc = (q == c) ? v[q] : vc;
