@@ -52,7 +52,7 @@ __host__ __device__ inline size_t sb_per_mat(int n) {
   const size_t km = n >= 3 ? (size_t)((n - 3) / SB + 1) : 1;
   const size_t nblk = (size_t)((n + SY_ROWS - 1) / SY_ROWS);
   const size_t f = 4 * (size_t)SB * n + (size_t)n * SB + 2 * nblk * SB * SB + SB * SB + (size_t)n * SBW +
-                   (size_t)n * km * SB + km * (km + 1) / 2 * SB * SB + 64;
+                   (size_t)n * km * SB + km * (km + 1) / 2 * 2 * SB * SB + 64;
   return (f + 63) / 64 * 64;
 }
 
@@ -708,9 +708,9 @@ __host__ __device__ inline int64_t q_group_offset(int gi, int km) {
 
 JOLT_DEV bool refl_exists(int s, int k, int n) { return s <= n - 3 && k <= (n - 3 - s) / SB; }
 
-// T of every block, stored transposed (entry (a, b) of T at [b][a]); one wavefront per block.
-// Column g of V holds the entries 1 .. 31 of reflector (s0 + g, k) below its unit entry;
-// S = V^T V, then T[0:g, g] = -tau_g T[0:g, 0:g] S[0:g, g], T[g][g] = tau_g.
+// V T of every block (64 x 32, row-major, row 63 zero); one wavefront per block.  Column g
+// of V holds the entries 1 .. 31 of reflector (s0 + g, k) below its unit entry;
+// S = V^T V, then T[0:g, g] = -tau_g T[0:g, 0:g] S[0:g, g], T[g][g] = tau_g, then V T.
 __global__ void __launch_bounds__(512) k_sb_qt(SbArgs a, int mat0) {
   const int mat = mat0 + blockIdx.y, n = a.n;
   const SbView M = sview(a, mat);
@@ -721,6 +721,7 @@ __global__ void __launch_bounds__(512) k_sb_qt(SbArgs a, int mat0) {
   __shared__ float vs[8][QG][SB + 1];
   __shared__ float ss[8][QG][QG + 1];
   __shared__ float ts[8][QG];
+  __shared__ float tt[8][QG][QG + 1];
   if (blk >= total) return;
   int gi = 0;
   while (q_group_offset(gi + 1, km) <= blk) ++gi;
@@ -735,14 +736,22 @@ __global__ void __launch_bounds__(512) k_sb_qt(SbArgs a, int mat0) {
     }
   }
   wave_sync();
-  // S[h][g] for h < g: rows of column h are offset by g - h from those of column g
-  if (lane < 32) {
-    for (int h = 0; h < QG; ++h) {
-      float acc = 0.f;
-      if (h < g)
-        for (int i = 0; i + (g - h) < SB; ++i) acc = fmaf(vs[wv][h][i + g - h], vs[wv][g][i], acc);
-      ss[wv][h][g] = acc;
+  // S = V^T V on the fp32 matrix cores (one 32 x 32 tile over the block's 64 rows): lane
+  // (lr, lh) supplies V[j][lr] at j = 2 st + lh as both operands
+  {
+    const int lr = lane & 31, lh = lane >> 5;
+    f32x16_t acc;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+#pragma unroll
+    for (int st = 0; st < 32; ++st) {
+      const int j = 2 * st + lh, dj = j - lr;
+      const float x = vs[wv][lr][min(max(dj, 0), SB - 1)];
+      const float vj = (dj == 0) ? 1.f : ((dj > 0 && dj < SB) ? x : 0.f);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(vj, vj, acc, 0, 0, 0);
     }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) ss[wv][8 * (q >> 2) + 4 * lh + (q & 3)][lr] = acc[q];
   }
   wave_sync();
   float t[QG];
@@ -759,9 +768,34 @@ __global__ void __launch_bounds__(512) k_sb_qt(SbArgs a, int mat0) {
     t[c] = (i < c) ? -tc * acc : (i == c ? tc : 0.f);
   }
   if (lane < 32) {
-    float *To = M.Tq + (q_group_offset(gi, km) + k) * (QG * QG);
 #pragma unroll
-    for (int c = 0; c < QG; ++c) To[c * QG + i] = t[c];
+    for (int c = 0; c < QG; ++c) tt[wv][i][c] = t[c];
+  }
+  wave_sync();
+  {
+    // V T on the fp32 matrix cores: two 32-row tiles, lane (lr, lh) supplies V[32 jt + lr][g]
+    // and T[g][lr] at g = 2 st + lh; V[j][g] is 1 at j = g and entry j - g of column g below it
+    const int lr = lane & 31, lh = lane >> 5;
+    float *To = M.Tq + (q_group_offset(gi, km) + k) * (2 * QG * QG);
+#pragma unroll
+    for (int jt = 0; jt < 2; ++jt) {
+      f32x16_t acc;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+      const int j = 32 * jt + lr;
+#pragma unroll
+      for (int st = 0; st < 16; ++st) {
+        const int gg = 2 * st + lh, dj = j - gg;
+        const float x = vs[wv][gg][min(max(dj, 0), SB - 1)];
+        const float vj = (dj == 0) ? 1.f : ((dj > 0 && dj < SB) ? x : 0.f);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(vj, tt[wv][gg][lr], acc, 0, 0, 0);
+      }
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int row = 32 * jt + 8 * (q >> 2) + 4 * lh + (q & 3);
+        To[row * QG + lr] = (row < QH) ? acc[q] : 0.f;
+      }
+    }
   }
 }
 
@@ -783,7 +817,7 @@ __global__ void k_sb_z2u(int n, const double *Z, int ldz, const int32_t *kcnt, f
 struct QLds {
   float z[QRING][QCW + 1];
   float v[QH + 1][QG + 1];     // row QH stays zero (the products run over 64 rows)
-  float t[QG][QG + 1];
+  float vt[QH + 1][QG + 1];    // V T of the block (row QH zero)
   float w[QG][QCW + 1];
   float w2[QG][QCW + 1];
 };
@@ -802,8 +836,8 @@ __global__ void __launch_bounds__(Q_NT) k_sb_qapply(SbArgs a, int mat0, const in
   const int ncol = min(QCW, kc - c0);
   for (int e = tid; e < QRING * (QCW + 1); e += Q_NT) (&sm.z[0][0])[e] = 0.f;
   for (int e = tid; e < QG + 1; e += Q_NT) sm.v[QH][e] = 0.f;
-  // per-thread shares: rows (32 x QCW: 8 each), V (63 x 32: 8 each), T (32 x 32: 4 each)
-  float rz[8], rv[8], rt[4];
+  // per-thread shares: rows (32 x QCW: 8 each), V (63 x 32: 8 each), V T (64 x 32: 8 each)
+  float rz[8], rv[8], rt[8];
   auto fetch = [&](int s0, int k, int row0, int nrows) {
     // rows row0 .. row0 + nrows - 1 of the slab (nrows <= 32), V and T of block (s0, k)
 #pragma unroll
@@ -824,9 +858,9 @@ __global__ void __launch_bounds__(Q_NT) k_sb_qapply(SbArgs a, int mat0, const in
       }
       rv[u] = x;
     }
-    const float *Tb = M.Tq + (q_group_offset(gi, km) + k) * (QG * QG);
+    const float *Tb = M.Tq + (q_group_offset(gi, km) + k) * (2 * QG * QG);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) rt[u] = Tb[tid + u * Q_NT];
+    for (int u = 0; u < 8; ++u) rt[u] = Tb[tid + u * Q_NT];
   };
   auto stash_vt = [&]() {
 #pragma unroll
@@ -835,9 +869,9 @@ __global__ void __launch_bounds__(Q_NT) k_sb_qapply(SbArgs a, int mat0, const in
       if (j < QH) sm.v[j][g] = rv[u];
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < 8; ++u) {
       const int e = tid + u * Q_NT;
-      sm.t[e % QG][e / QG] = rt[u];                 // T[a][b] at t[a][b]
+      sm.vt[e / QG][e % QG] = rt[u];
     }
   };
   auto stash_rows = [&](int row0) {
@@ -900,33 +934,7 @@ __global__ void __launch_bounds__(Q_NT) k_sb_qapply(SbArgs a, int mat0, const in
         }
       }
       lds_barrier();
-      // W2 = T W (T upper triangular), the 32 inner indices split between two wavefronts
-      {
-        f32x16_t acc, acc1;
-#pragma unroll
-        for (int q = 0; q < 16; ++q) { acc[q] = 0.f; acc1[q] = 0.f; }
-#pragma unroll
-        for (int st = 0; st < 8; st += 2) {
-          const int h = 16 * kh + 2 * st + lh;
-          acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.t[lr][h], sm.w[h][32 * ct + lr], acc, 0, 0, 0);
-          acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.t[lr][h + 2], sm.w[h + 2][32 * ct + lr], acc1, 0, 0, 0);
-        }
-        acc += acc1;
-        if (kh == 1) {
-#pragma unroll
-          for (int q = 0; q < 16; ++q) sm.w2[8 * (q >> 2) + 4 * lh + (q & 3)][32 * ct + lr] = acc[q];
-        }
-        lds_barrier();
-        if (kh == 0) {
-#pragma unroll
-          for (int q = 0; q < 16; ++q) {
-            const int g = 8 * (q >> 2) + 4 * lh + (q & 3);
-            sm.w2[g][32 * ct + lr] += acc[q];
-          }
-        }
-      }
-      lds_barrier();
-      // Z -= V W2: tile (rows 32 kh, columns 32 ct) per wavefront
+      // Z -= (V T) W: tile (rows 32 kh, columns 32 ct) per wavefront
       {
         f32x16_t acc, acc1;
 #pragma unroll
@@ -934,8 +942,8 @@ __global__ void __launch_bounds__(Q_NT) k_sb_qapply(SbArgs a, int mat0, const in
 #pragma unroll
         for (int st = 0; st < 16; st += 2) {
           const int g = 2 * st + lh;
-          acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.v[32 * kh + lr][g], sm.w2[g][32 * ct + lr], acc, 0, 0, 0);
-          acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.v[32 * kh + lr][g + 2], sm.w2[g + 2][32 * ct + lr], acc1, 0, 0,
+          acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.vt[32 * kh + lr][g], sm.w[g][32 * ct + lr], acc, 0, 0, 0);
+          acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.vt[32 * kh + lr][g + 2], sm.w[g + 2][32 * ct + lr], acc1, 0, 0,
                                                       0);
         }
         acc += acc1;
