@@ -16,12 +16,18 @@
 // column is annihilated by the next reflector of the sweep, and so on to the end of the
 // band.  Each step touches three SB x SB blocks (the previous bulge block, the diagonal
 // block and the block below) of a band buffer holding 2 SB entries per column; sweep s + 1
-// may run step k once sweep s has completed step k + 2.  One workgroup per matrix, one
-// wavefront per sweep in flight, the dependencies between wavefronts kept in LDS.
+// may run step k once sweep s has completed step k + 2 (k + 3 here, so that the next step's
+// blocks can be loaded during the current one).  One workgroup per matrix, one wavefront per
+// sweep in flight, the dependencies between wavefronts kept in LDS.
 //
-// Eigenvectors: z of the tridiagonal -> Q2 z (stage-2 reflectors, last sweep first; the
-// reflectors of one sweep act on disjoint rows) -> Q1 (Q2 z) (stage-1 reflectors by the
-// blocked WY back-transform, with the unit of reflector i at row i + SB).
+// Eigenvectors: z of the tridiagonal -> Q2 z (the stage-2 reflectors in blocks of 32 sweeps
+// at one step, groups of sweeps last to first, steps in increasing order within a group) ->
+// Q1 (Q2 z) (stage-1 reflectors by the blocked WY back-transform, with the unit of
+// reflector i at row i + SB).
+//
+// Which of this and the one-stage reduction runs is the caller's choice (by batch size:
+// the bulge chase is a chain of about n^2 / 64 dependent steps per matrix, hidden only when
+// enough matrices run side by side).
 #include <algorithm>
 
 #include "common.h"
@@ -43,7 +49,7 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 __host__ __device__ inline int steps_max(int n) { return n >= 3 ? (n - 3) / SB + 1 : 1; }
 
 struct SbView {
-  float *A, *P, *Q, *X, *Yp, *Sp, *T, *AB, *V2, *Tq;
+  float *A, *P, *Q, *X, *Yp, *Sp, *AB, *V2, *VTb;
   double *d, *e;
   float *tau;
 };
@@ -51,7 +57,7 @@ struct SbView {
 __host__ __device__ inline size_t sb_per_mat(int n) {
   const size_t km = n >= 3 ? (size_t)((n - 3) / SB + 1) : 1;
   const size_t nblk = (size_t)((n + SY_ROWS - 1) / SY_ROWS);
-  const size_t f = 4 * (size_t)SB * n + (size_t)n * SB + 2 * nblk * SB * SB + SB * SB + (size_t)n * SBW +
+  const size_t f = 4 * (size_t)SB * n + (size_t)n * SB + 2 * nblk * SB * SB + (size_t)n * SBW +
                    (size_t)n * km * SB + km * (km + 1) / 2 * 2 * SB * SB + 64;
   return (f + 63) / 64 * 64;
 }
@@ -67,10 +73,9 @@ JOLT_DEV SbView sview(const SbArgs &a, int mat) {
   v.X = v.Q + (int64_t)2 * SB * n;
   v.Yp = v.X + (int64_t)n * SB;
   v.Sp = v.Yp + (int64_t)nblk * SB * SB;
-  v.T = v.Sp + (int64_t)nblk * SB * SB;
-  v.AB = v.T + SB * SB;
+  v.AB = v.Sp + (int64_t)nblk * SB * SB;
   v.V2 = v.AB + (int64_t)n * SBW;
-  v.Tq = v.V2 + (int64_t)n * steps_max(n) * SB;
+  v.VTb = v.V2 + (int64_t)n * steps_max(n) * SB;     // V T of each block of 32 sweeps
   v.d = a.d + (int64_t)mat * n;
   v.e = a.e + (int64_t)mat * n;
   v.tau = a.tau + (int64_t)mat * n;
@@ -776,7 +781,7 @@ __global__ void __launch_bounds__(512) k_sb_qt(SbArgs a, int mat0) {
     // V T on the fp32 matrix cores: two 32-row tiles, lane (lr, lh) supplies V[32 jt + lr][g]
     // and T[g][lr] at g = 2 st + lh; V[j][g] is 1 at j = g and entry j - g of column g below it
     const int lr = lane & 31, lh = lane >> 5;
-    float *To = M.Tq + (q_group_offset(gi, km) + k) * (2 * QG * QG);
+    float *To = M.VTb + (q_group_offset(gi, km) + k) * (2 * QG * QG);
 #pragma unroll
     for (int jt = 0; jt < 2; ++jt) {
       f32x16_t acc;
@@ -858,7 +863,7 @@ __global__ void __launch_bounds__(Q_NT) k_sb_qapply(SbArgs a, int mat0, const in
       }
       rv[u] = x;
     }
-    const float *Tb = M.Tq + (q_group_offset(gi, km) + k) * (2 * QG * QG);
+    const float *Tb = M.VTb + (q_group_offset(gi, km) + k) * (2 * QG * QG);
 #pragma unroll
     for (int u = 0; u < 8; ++u) rt[u] = Tb[tid + u * Q_NT];
   };
