@@ -409,8 +409,11 @@ int jolt_debug_export(jolt_ctx *ctx, int what, int cell, void *dst, size_t dst_b
  * -1 (default) two stages when the call's matrices times their order reach 32 * 4096, one
  * otherwise; both give the same spectrum and projectors to rounding, and a compress that
  * reuses a recorded spectrum back-transforms with the reduction that made it.
+ * JOLT_DBG_BULGE_SPIN bounds each dependency wait of the two-stage reduction's bulge chase
+ * (default 2^24 polls, range 0..2^24; 0 makes the first wait give up): a chase that gives up
+ * ends normally and the call reports JOLT_E_NOCONV, which lets that path be exercised.
  * Errors: JOLT_E_INVAL. */
-enum { JOLT_DBG_INVIT_ITERS = 0, JOLT_DBG_TRD_LANES = 1, JOLT_DBG_TRD_TWO_STAGE = 2 };
+enum { JOLT_DBG_INVIT_ITERS = 0, JOLT_DBG_TRD_LANES = 1, JOLT_DBG_TRD_TWO_STAGE = 2, JOLT_DBG_BULGE_SPIN = 3 };
 int jolt_debug_set(jolt_ctx *ctx, int what, int64_t value);
 
 /* Benchmark instrumentation.  When enabled, the library brackets the kernels of each

@@ -24,7 +24,7 @@ __all__ = ["JoltError", "lib", "CellDesc", "SpectrumOpts", "Params", "CellSpectr
            "jolt_mode_summary", "jolt_truncated_spectra_workspace_size", "jolt_truncated_spectra",
            "jolt_attend_workspace_size", "jolt_attend", "jolt_attend_noalloc", "JOLT_ATTEND_SCRATCH_BYTES", "jolt_debug_export", "jolt_debug_set",
            "jolt_profile_enable", "jolt_profile_reset", "JOLT_E_NONFINITE", "JOLT_E_NOCONV",
-           "JOLT_DBG_INVIT_ITERS", "JOLT_DBG_TRD_LANES", "JOLT_DBG_TRD_TWO_STAGE",
+           "JOLT_DBG_INVIT_ITERS", "JOLT_DBG_TRD_LANES", "JOLT_DBG_TRD_TWO_STAGE", "JOLT_DBG_BULGE_SPIN",
            "jolt_profile_read", "STAGES", "cell_desc", "LIB_PATH", "HEADER_PATH"]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -37,6 +37,7 @@ JOLT_E_HIP, JOLT_E_NONFINITE, JOLT_E_STATE, JOLT_E_NOCONV = -5, -6, -7, -8
 JOLT_DBG_INVIT_ITERS = 0
 JOLT_DBG_TRD_LANES = 1
 JOLT_DBG_TRD_TWO_STAGE = 2
+JOLT_DBG_BULGE_SPIN = 3
 JOLT_ATTEND_SCRATCH_BYTES = 64 << 20
 JOLT_EXACT, JOLT_FLASH = 0, 1
 JOLT_FACTOR_F32, JOLT_FACTOR_F16 = 0, 1

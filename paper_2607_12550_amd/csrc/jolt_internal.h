@@ -87,6 +87,7 @@ struct jolt_ctx {
   int trd_lanes_max = kTrdLanes;   // JOLT_DBG_TRD_LANES
   std::vector<const void *> trd_key;
   int trd_two_stage = -1;          // JOLT_DBG_TRD_TWO_STAGE: 1 two-stage, 0 one-stage, -1 by batch size
+  int bulge_spin = SB_SPIN_DEFAULT; // JOLT_DBG_BULGE_SPIN: bound of the bulge chase's waits
   int invit_iters = 2;            // inverse-iteration sweeps (test hook jolt_debug_set)
   void *attend_scratch = nullptr; // this device's fixed attention scratch (device address)
   ~jolt_ctx();

@@ -42,7 +42,6 @@ constexpr int SY_ROWS = 128;      // rows of X per workgroup of the symmetric pr
 constexpr int SY_NT = 256;
 constexpr int BG_WAVES = 8;       // bulge chase: wavefronts (sweeps in flight) per matrix
 constexpr int BT_BLOCK = 128;     // reflectors per block of the stage-1 back-transform
-constexpr int SPIN_MAX = 1 << 24; // bound of one dependency wait of the bulge chase
 
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
@@ -545,10 +544,11 @@ __global__ void __launch_bounds__(BG_WAVES * 64) k_sb_bulge(SbArgs a, int mat0) 
       if (s > 0) {
         const int need = (s - 1) * 1024 + k + 4;
         int spins = 0;
-        for (;;) {
+        if (a.spin_max == 0) stop = true;
+        while (!stop) {
           const int v = __hip_atomic_load(&prog[(s - 1) % BG_WAVES], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
           if (v >= need) break;
-          if (++spins > SPIN_MAX || __hip_atomic_load(&abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) {
+          if (++spins > a.spin_max || __hip_atomic_load(&abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) {
             stop = true;
             break;
           }
@@ -1004,7 +1004,7 @@ void sb_tables(const EigBatch &b, float *work, GemmProblem *tab_host) {
 }
 
 hipError_t launch_sb_reduce(const EigBatch &b, float *work, const GemmProblem *tab_dev, hipStream_t st, int m0,
-                            int m1) {
+                            int m1, int spin_max) {
   const int n = b.n;
   if (m1 < 0) m1 = b.n_mat;
   const int nm = m1 - m0;
@@ -1018,6 +1018,7 @@ hipError_t launch_sb_reduce(const EigBatch &b, float *work, const GemmProblem *t
   a.d = b.d;
   a.e = b.e;
   a.tau = b.tau;
+  a.spin_max = spin_max < 0 ? 0 : spin_max;
   const int panels = (n + SB - 1) / SB;
   for (int p = 0; p < panels; ++p) {
     const int m = n - (p * SB + SB);

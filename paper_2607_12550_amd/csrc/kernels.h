@@ -294,19 +294,22 @@ hipError_t launch_backtransform(const EigBatch &b, const InvitWork &w, int kmax,
 struct SbArgs {
   float *A;
   int64_t mat_stride;
-  int32_t n, pad;
+  int32_t n;
+  int32_t spin_max;      // bound of one dependency wait of the bulge chase (0: the first wait
+                         // gives up); a chase that gives up leaves NaN on the diagonal
   float *work;
   int64_t work_stride;
   double *d, *e;
   float *tau;
 };
 constexpr int SB_MAX_N = 8192;
+constexpr int SB_SPIN_DEFAULT = 1 << 24;
 int sb_band();
 size_t sb_work_floats(int n_mat, int n);
 size_t sb_table_entries(int n_mat, int n);
 void sb_tables(const EigBatch &b, float *work, GemmProblem *tab_host);
 hipError_t launch_sb_reduce(const EigBatch &b, float *work, const GemmProblem *tab_dev, hipStream_t st,
-                            int m0 = 0, int m1 = -1);
+                            int m0 = 0, int m1 = -1, int spin_max = SB_SPIN_DEFAULT);
 // U (fp32, first k[mat] columns) = Q2 Z for the tridiagonal's eigenvectors Z of w.
 hipError_t launch_sb_q2(const EigBatch &b, const float *work, const InvitWork &w, int kmax, float *U, int64_t ldu,
                         int64_t u_stride, hipStream_t st);

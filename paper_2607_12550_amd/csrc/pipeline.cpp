@@ -266,7 +266,8 @@ int eig_values(Run &R, EigWs &e) {
       std::vector<const void *> key{e.b.A, e.trd, tab, e.b.d, e.b.e, e.b.tau,
                                     reinterpret_cast<const void *>((intptr_t)e.b.n),
                                     reinterpret_cast<const void *>((intptr_t)e.b.n_mat),
-                                    reinterpret_cast<const void *>((intptr_t)(two ? 2 : 1))};
+                                    reinterpret_cast<const void *>((intptr_t)(two ? 2 : 1)),
+                                    reinterpret_cast<const void *>((intptr_t)c->bulge_spin)};
       const int lanes = std::min(c->trd_lanes_max, e.b.n_mat);
       if (c->trd_lanes != lanes || c->trd_key != key) {
         for (int g = 0; g < jolt_ctx::kTrdLanes; ++g)
@@ -282,7 +283,7 @@ int eig_values(Run &R, EigWs &e) {
           const int m0 = (int)((int64_t)e.b.n_mat * g / lanes), m1 = (int)((int64_t)e.b.n_mat * (g + 1) / lanes);
           hipGraph_t gr = nullptr;
           HIP_OK(hipStreamBeginCapture(c->cap_stream[cs], hipStreamCaptureModeThreadLocal));
-          hipError_t le = two ? launch_sb_reduce(e.b, e.trd, tab, c->cap_stream[cs], m0, m1)
+          hipError_t le = two ? launch_sb_reduce(e.b, e.trd, tab, c->cap_stream[cs], m0, m1, c->bulge_spin)
                               : launch_sytrd_large(e.b, e.trd, SYTRD_NB, tab, c->cap_stream[cs], m0, m1);
           hipError_t ce = hipStreamEndCapture(c->cap_stream[cs], &gr);
           HIP_OK(le);
@@ -347,7 +348,7 @@ struct CallChecks {
   int nc = 0, n_orth = 0;
   bool spectrum = false;
   std::vector<int32_t> bad, clamp, tstat, fstat;
-  std::vector<double> E;
+  std::vector<double> E, d0;   // d0: first diagonal entry of each two-stage tridiagonal
 
   int queue(Run &R, int nc_, bool spectrum_computed, bool token_vecs, bool feature_vecs) {
     nc = nc_;
@@ -358,6 +359,13 @@ struct CallChecks {
       HIP_OK(hipMemcpyAsync(bad.data(), R.w.nonfinite, nc * sizeof(int32_t), hipMemcpyDeviceToHost, R.st));
       HIP_OK(hipMemcpyAsync(E.data(), R.w.E, nc * sizeof(double), hipMemcpyDeviceToHost, R.st));
       n_orth = R.orth_calls;
+      // a bulge chase that gave up leaves NaN on its diagonal
+      const EigBatch &tb = R.w.teig.b;
+      if (tb.d && tb.n > SYTRD_SMALL_MAX && tb.refl_off == sb_band()) {
+        d0.resize(tb.n_mat);
+        HIP_OK(hipMemcpy2DAsync(d0.data(), sizeof(double), tb.d, (size_t)tb.n * sizeof(double), sizeof(double),
+                                tb.n_mat, hipMemcpyDeviceToHost, R.st));
+      }
       if (n_orth) {
         clamp.resize((size_t)n_orth * 2 * nc);
         HIP_OK(hipMemcpyAsync(clamp.data(), R.w.orth_clamp, clamp.size() * sizeof(int32_t),
@@ -389,6 +397,9 @@ struct CallChecks {
                                           "pass (%d pivots clamped in the second)", c, o, second);
       }
     }
+    for (int c = 0; c < (int)d0.size(); ++c)
+      if (!std::isfinite(d0[c]))
+        return jolt_fail(JOLT_E_NOCONV, "cell %d: the band-to-tridiagonal reduction of the token Gram did not complete", c);
     for (int c = 0; c < (int)tstat.size(); ++c)
       if (tstat[c]) return jolt_fail(JOLT_E_NOCONV, "cell %d: token-mode inverse iteration did not converge", c);
     for (int c = 0; c < (int)fstat.size(); ++c)
@@ -1614,6 +1625,12 @@ extern "C" int jolt_debug_set(jolt_ctx *ctx, int what, int64_t value) {
     if (value < 1 || value > jolt_ctx::kTrdLanes)
       return jolt_fail(JOLT_E_INVAL, "jolt_debug_set: tridiagonalisation lanes must be in 1..%d", jolt_ctx::kTrdLanes);
     ctx->trd_lanes_max = (int)value;
+    return JOLT_OK;
+  }
+  if (what == JOLT_DBG_BULGE_SPIN) {
+    if (value < 0 || value > SB_SPIN_DEFAULT)
+      return jolt_fail(JOLT_E_INVAL, "jolt_debug_set: bulge-chase wait bound must be in 0..%d", SB_SPIN_DEFAULT);
+    ctx->bulge_spin = (int)value;
     return JOLT_OK;
   }
   if (what == JOLT_DBG_TRD_TWO_STAGE) {

@@ -6,7 +6,8 @@
 * rank-deficient and all-zero cells are not solver failures (clamped CholeskyQR pivots of
   a first pass and zero eigenvalues are the designed treatment) and still match the oracle;
 * JOLT_E_NOCONV: forced from the host with the inverse-iteration limit set to zero sweeps
-  (the growth check then fails on any input), never on the same input with the default;
+  (the growth check then fails on any input) and with the two-stage reduction's bulge-chase
+  wait bound set to zero, never on the same input with the defaults;
 * the int8 core exponent: a core below 2^-113 stores the floor -128 (identically to the
   oracle's serialisation rule), and the oracle's decode of that blob equals the GPU's.
 """
@@ -214,3 +215,32 @@ def test_two_stage_and_one_stage_reductions_agree():
     lam0 = opl.spectrum(ex[0])["lam_T"]
     assert (lam0[31] - lam0[32]) / lam0[31] > 0.02
     assert np.abs(proj[0] - proj[1]).max() < 1e-4
+
+
+def test_bulge_chase_that_gives_up_is_reported():
+    """JOLT_DBG_BULGE_SPIN = 0 makes the first dependency wait of the two-stage reduction's
+    bulge chase give up (forced from the host; the kernel still ends normally): the chase
+    leaves NaN on the diagonal and jolt_spectrum reports JOLT_E_NOCONV.  With the default
+    bound the same call on the same context succeeds again; values outside 0..2^24 are
+    rejected."""
+    cells = [keys(T=1024, H=4, seed=s) for s in range(2)]
+    xs, ex, desc = device_cells(cells, "f32")
+    ws = workspace(desc, 2)
+    c2 = J.jolt_create(0)
+    try:
+        J.jolt_debug_set(c2, J.JOLT_DBG_TRD_TWO_STAGE, 1)
+        J.jolt_debug_set(c2, J.JOLT_DBG_BULGE_SPIN, 0)
+        note("exact spectrum, bulge chase forced to give up")
+        with pytest.raises(J.JoltError) as e:
+            J.jolt_spectrum(c2, desc, xs, None, None, ws)
+        assert e.value.code == J.JOLT_E_NOCONV
+        J.jolt_debug_set(c2, J.JOLT_DBG_BULGE_SPIN, 1 << 24)
+        note("exact spectrum, default bound")
+        E, lamT, lamd = J.jolt_spectrum(c2, desc, xs, None, None, ws)
+        sp = opl.spectrum(ex[0])
+        np.testing.assert_allclose(np.array(lamT)[0], sp["lam_T"], rtol=0, atol=1e-5 * sp["lam_T"][0])
+        for bad in (-1, (1 << 24) + 1):
+            with pytest.raises(J.JoltError):
+                J.jolt_debug_set(c2, J.JOLT_DBG_BULGE_SPIN, bad)
+    finally:
+        J.jolt_destroy(c2)
