@@ -221,6 +221,7 @@ JOLT_DEV void gershgorin(const double *d, const double *e, int n, double &gl, do
                          double &pivmin) {
   gl = DBL_MAX; gu = -DBL_MAX;
   double emax2 = 0.0;
+#pragma unroll 8
   for (int i = 0; i < n; ++i) {
     const double r = (i > 0 ? fabs(e[i - 1]) : 0.0) + (i < n - 1 ? fabs(e[i]) : 0.0);
     gl = fmin(gl, d[i] - r);
@@ -362,20 +363,27 @@ __global__ void __launch_bounds__(64) k_tri_eigvecs(EigBatch b, InvitWork w, int
     return;
   }
   // deterministic start vector in [-1, 1]
-  for (int i = 0; i < n; ++i) {
+  auto start = [&](int i) {
     u32x4 r = philox4x32_10(u32x4{(uint32_t)i, (uint32_t)j, (uint32_t)mat, 4u}, 0x6a6f6c74u, 0u);
-    x[(int64_t)i * ld] = ((double)r.x + 0.5) * 0x1p-31 - 1.0;
-  }
+    return ((double)r.x + 0.5) * 0x1p-31 - 1.0;
+  };
+  if (w.iters == 0)
+    for (int i = 0; i < n; ++i) x[(int64_t)i * ld] = start(i);
   // Each sweep below walks the column serially; its steps are taken in blocks of IB whose
   // loads are issued one block ahead (they never touch an element the current block
   // stores), so the memory latency is paid once per block instead of once per step.  The
-  // arithmetic of every step is unchanged.
+  // arithmetic of every step is unchanged.  The first forward sweep draws the start vector
+  // itself, and the scaling of a solve's result by 1 / max|x| is applied where the next pass
+  // reads it (x holds the vector divided by `pend`), which saves two passes over the column
+  // per solve with the same values.
   constexpr int IB = 8;
   double growth = 0.0;                 // max |x| after the last solve (its input has max |x| <= 1)
+  double pend = 1.0;
   for (int it = 0; it < w.iters; ++it) {
+    const bool gen = it == 0;
     // forward: factor T - lam I = P L U while transforming the right-hand side in x
     double p = d[0] - lam, q = (n > 1) ? e[0] : 0.0;
-    double y = x[0];
+    double y = gen ? start(0) : x[0] * pend;
     double nc[IB], na1[IB], nb1[IB], ny1[IB];
     auto load_fwd = [&](int i0) {
 #pragma unroll
@@ -385,7 +393,7 @@ __global__ void __launch_bounds__(64) k_tri_eigvecs(EigBatch b, InvitWork w, int
         nc[s] = in ? e[i] : 0.0;
         na1[s] = in ? d[i + 1] - lam : 0.0;
         nb1[s] = (in && i + 1 < n - 1) ? e[i + 1] : 0.0;
-        ny1[s] = in ? x[(int64_t)(i + 1) * ld] : 0.0;
+        ny1[s] = in ? (gen ? start(i + 1) : x[(int64_t)(i + 1) * ld] * pend) : 0.0;
       }
     };
     load_fwd(0);
@@ -456,14 +464,7 @@ __global__ void __launch_bounds__(64) k_tri_eigvecs(EigBatch b, InvitWork w, int
       }
     }
     growth = amax;
-    const double sc = amax > 0.0 ? 1.0 / amax : 1.0;
-    for (int i0 = 0; i0 < n; i0 += IB) {
-      double v[IB];
-#pragma unroll
-      for (int s = 0; s < IB; ++s) v[s] = i0 + s < n ? x[(int64_t)(i0 + s) * ld] : 0.0;
-#pragma unroll
-      for (int s = 0; s < IB; ++s) if (i0 + s < n) x[(int64_t)(i0 + s) * ld] = v[s] * sc;
-    }
+    pend = amax > 0.0 ? 1.0 / amax : 1.0;
   }
   // convergence: the normalised vector z = y / |y| has residual |(T - lam I) z|_2 <=
   // sqrt(n) / |y|_inf, so a growth of at least 1e4 sqrt(n) / |T| bounds it by 1e-4 |T|
@@ -472,7 +473,7 @@ __global__ void __launch_bounds__(64) k_tri_eigvecs(EigBatch b, InvitWork w, int
   for (int i0 = 0; i0 < n; i0 += IB) {
     double v[IB];
 #pragma unroll
-    for (int s = 0; s < IB; ++s) v[s] = i0 + s < n ? x[(int64_t)(i0 + s) * ld] : 0.0;
+    for (int s = 0; s < IB; ++s) v[s] = i0 + s < n ? x[(int64_t)(i0 + s) * ld] * pend : 0.0;
 #pragma unroll
     for (int s = 0; s < IB; ++s) nrm += v[s] * v[s];
   }
@@ -480,7 +481,7 @@ __global__ void __launch_bounds__(64) k_tri_eigvecs(EigBatch b, InvitWork w, int
   for (int i0 = 0; i0 < n; i0 += IB) {
     double v[IB];
 #pragma unroll
-    for (int s = 0; s < IB; ++s) v[s] = i0 + s < n ? x[(int64_t)(i0 + s) * ld] : 0.0;
+    for (int s = 0; s < IB; ++s) v[s] = i0 + s < n ? x[(int64_t)(i0 + s) * ld] * pend : 0.0;
 #pragma unroll
     for (int s = 0; s < IB; ++s) if (i0 + s < n) x[(int64_t)(i0 + s) * ld] = v[s] * nrm;
   }
