@@ -335,7 +335,10 @@ __global__ void __launch_bounds__(EV_THREADS) k_tri_eigvals(EigBatch b) {
 }
 
 // inverse iteration on (T - lam I) with partial pivoting; per-thread vectors are laid
-// out [array][i][column] so neighbouring threads touch neighbouring addresses.
+// out [array][i][column] so neighbouring threads touch neighbouring addresses.  Each pivot is
+// inverted once by recip() (a few ulps) and its reciprocal multiplies in both sweeps: a
+// division on the serial chain of every step costs about twice as long, and inverse
+// iteration does not need correctly rounded steps.
 __global__ void __launch_bounds__(64) k_tri_eigvecs(EigBatch b, InvitWork w, int j0) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int n = b.n;
@@ -410,15 +413,17 @@ __global__ void __launch_bounds__(64) k_tri_eigvecs(EigBatch b, InvitWork w, int
         const double a1 = ca1[s], b1 = cb1[s], y1 = cy1[s];
         if (fabs(p) >= fabs(c)) {
           if (fabs(p) < tiny) p = copysign(tiny, p == 0.0 ? 1.0 : p);
-          const double l = c / p;
-          u0[(int64_t)(i) * ll] = p; u1[(int64_t)(i) * ll] = q; u2[(int64_t)(i) * ll] = 0.0;
+          const double rp = recip(p);
+          const double l = c * rp;
+          u0[(int64_t)(i) * ll] = rp; u1[(int64_t)(i) * ll] = q; u2[(int64_t)(i) * ll] = 0.0;
           x[(int64_t)i * ld] = y;
           y = y1 - l * y;
           p = a1 - l * q;
           q = b1;
         } else {
-          const double l = p / c;
-          u0[(int64_t)(i) * ll] = c; u1[(int64_t)(i) * ll] = a1; u2[(int64_t)(i) * ll] = b1;
+          const double rc = recip(c);
+          const double l = p * rc;
+          u0[(int64_t)(i) * ll] = rc; u1[(int64_t)(i) * ll] = a1; u2[(int64_t)(i) * ll] = b1;
           x[(int64_t)i * ld] = y1;
           const double ynew = y - l * y1;
           const double pnew = q - l * a1;
@@ -429,10 +434,10 @@ __global__ void __launch_bounds__(64) k_tri_eigvecs(EigBatch b, InvitWork w, int
       }
     }
     if (fabs(p) < tiny) p = copysign(tiny, p == 0.0 ? 1.0 : p);
-    u0[(int64_t)(n - 1) * ll] = p;
     x[(int64_t)(n - 1) * ld] = y;
-    // back substitution, blocks of rows n-2, n-3, ... loaded one block ahead
-    double xn1 = y / p, xn2 = 0.0;
+    // back substitution, blocks of rows n-2, n-3, ... loaded one block ahead; u0 holds the
+    // reciprocals of the pivots, so that no step divides
+    double xn1 = y * recip(p), xn2 = 0.0;
     x[(int64_t)(n - 1) * ld] = xn1;
     double amax = fabs(xn1);
     double bx[IB], b0[IB], b1v[IB], b2[IB];
@@ -457,7 +462,7 @@ __global__ void __launch_bounds__(64) k_tri_eigvecs(EigBatch b, InvitWork w, int
       for (int s = 0; s < IB; ++s) {
         const int i = i0 - s;
         if (i < 0) break;
-        const double xi = (cx[s] - c1[s] * xn1 - c2[s] * xn2) / c0[s];
+        const double xi = (cx[s] - c1[s] * xn1 - c2[s] * xn2) * c0[s];
         x[(int64_t)i * ld] = xi;
         xn2 = xn1; xn1 = xi;
         amax = fmax(amax, fabs(xi));
