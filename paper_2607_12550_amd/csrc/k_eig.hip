@@ -244,15 +244,22 @@ JOLT_DEV void gershgorin(const double *d, const double *e, int n, double &gl, do
 // independent of order).
 constexpr int EV_THREADS = 256;
 // 1/x from the hardware estimate refined by two Newton steps (each squares the relative
-// error, so the result is within a few units in the last place).  The Sturm count only
-// needs each step's quotient to that accuracy: it is then the exact count of a tridiagonal
-// within a few ulps of the given one (|x| >= pivmin > 0 here).
+// error, so the result is within a few units in the last place).
 JOLT_DEV double recip(double x) {
   double r = __builtin_amdgcn_rcp(x);
   double e = fma(-x, r, 1.0);
   r = fma(r, e, r);
   e = fma(-x, r, 1.0);
   return fma(r, e, r);
+}
+// 1/x to within 2^-48 relative: the gfx950 estimate is within 2^-24.4 (measured over 2^20
+// inputs of exponents -200..200), one Newton step squares that.  A Sturm step
+// q' = d - x - e^2 / q with such a quotient is the exact step for e^2 scaled by 1 + 2^-48,
+// so each count is that of a tridiagonal within about 2^-48 ||T|| of the given one, far
+// below the 1e-11 ||T|| to which the eigenvalues are resolved (|x| >= pivmin > 0 here).
+JOLT_DEV double recip_sturm(double x) {
+  const double r = __builtin_amdgcn_rcp(x);
+  return fma(r, fma(-x, r, 1.0), r);
 }
 
 __global__ void __launch_bounds__(EV_THREADS) k_tri_eigvals(EigBatch b) {
@@ -318,7 +325,7 @@ __global__ void __launch_bounds__(EV_THREADS) k_tri_eigvals(EigBatch b) {
       const double dj = dl[jj], ej2 = e2[jj - 1];
 #pragma unroll
       for (int q = 0; q < 3; ++q) {
-        double t = dj - x[q] - ej2 * recip(qv[q]);
+        double t = dj - x[q] - ej2 * recip_sturm(qv[q]);
         if (fabs(t) <= pivmin) t = -pivmin;
         qv[q] = t;
         cnt[q] += t < 0.0;
