@@ -241,7 +241,9 @@ JOLT_DEV void gershgorin(const double *d, const double *e, int n, double &gl, do
 // and gains two bits per sweep.  The interval is narrowed to the first quarter whose upper
 // point counts more than k eigenvalues, as three successive bisections on the same counts
 // would.  The Gershgorin interval and pivmin are reduced over the workgroup (min / max,
-// independent of order).
+// independent of order).  With NP = 1 the sweep is plain bisection at the midpoint: a third
+// fewer recurrence steps per bit, for batches large enough to keep the fp64 units busy
+// without the extra recurrences.
 constexpr int EV_THREADS = 256;
 // 1/x from the hardware estimate refined by two Newton steps (each squares the relative
 // error, so the result is within a few units in the last place).
@@ -262,7 +264,9 @@ JOLT_DEV double recip_sturm(double x) {
   return fma(r, fma(-x, r, 1.0), r);
 }
 
+template <int NP>
 __global__ void __launch_bounds__(EV_THREADS) k_tri_eigvals(EigBatch b) {
+  static_assert(NP == 1 || NP == 3, "bisection or quarter-point multisection");
   extern __shared__ double lds[];
   __shared__ double red[3][EV_THREADS / 64];
   const int mat = blockIdx.y, n = b.n, tid = threadIdx.x;
@@ -309,13 +313,16 @@ __global__ void __launch_bounds__(EV_THREADS) k_tri_eigvals(EigBatch b) {
                  mid == lo || mid == hi))
       live = false;
     if (!__any(live)) break;
-    // Sturm counts (eigenvalues below x) at the quarter points x[0] < x[1] < x[2]
+    // Sturm counts (eigenvalues below x) at the quarter points x[0] < x[1] < x[2], or at the
+    // midpoint alone
     const double h4 = 0.25 * (hi - lo);
-    const double x[3] = {lo + h4, mid, hi - h4};
-    double qv[3];
-    int cnt[3];
+    double x[NP];
+    if (NP == 1) x[0] = mid;
+    else { x[0] = lo + h4; x[1] = mid; x[2] = hi - h4; }
+    double qv[NP];
+    int cnt[NP];
 #pragma unroll
-    for (int q = 0; q < 3; ++q) {
+    for (int q = 0; q < NP; ++q) {
       qv[q] = dl[0] - x[q];
       if (fabs(qv[q]) <= pivmin) qv[q] = -pivmin;
       cnt[q] = qv[q] < 0.0;
@@ -324,7 +331,7 @@ __global__ void __launch_bounds__(EV_THREADS) k_tri_eigvals(EigBatch b) {
     for (int jj = 1; jj < n; ++jj) {
       const double dj = dl[jj], ej2 = e2[jj - 1];
 #pragma unroll
-      for (int q = 0; q < 3; ++q) {
+      for (int q = 0; q < NP; ++q) {
         double t = dj - x[q] - ej2 * recip_sturm(qv[q]);
         if (fabs(t) <= pivmin) t = -pivmin;
         qv[q] = t;
@@ -332,10 +339,15 @@ __global__ void __launch_bounds__(EV_THREADS) k_tri_eigvals(EigBatch b) {
       }
     }
     if (live) {
-      if (cnt[0] > k) hi = x[0];
-      else if (cnt[1] > k) { lo = x[0]; hi = x[1]; }
-      else if (cnt[2] > k) { lo = x[1]; hi = x[2]; }
-      else lo = x[2];
+      if (NP == 1) {
+        if (cnt[0] > k) hi = x[0];
+        else lo = x[0];
+      } else {
+        if (cnt[0] > k) hi = x[0];
+        else if (cnt[NP > 1 ? 1 : 0] > k) { lo = x[0]; hi = x[NP > 1 ? 1 : 0]; }
+        else if (cnt[NP - 1] > k) { lo = x[NP > 1 ? 1 : 0]; hi = x[NP - 1]; }
+        else lo = x[NP - 1];
+      }
     }
   }
   if (k < n) b.lam[(int64_t)mat * n + (n - 1 - k)] = 0.5 * (lo + hi);
@@ -602,12 +614,17 @@ hipError_t launch_tridiag_eigvals(const EigBatch &b, hipStream_t st) {
   const int per_block = EV_THREADS;
   dim3 grid((b.n + per_block - 1) / per_block, b.n_mat);
   const size_t shm = (size_t)2 * b.n * sizeof(double);
+  // bisection once the batch fills every SIMD with two wavefronts (32 matrices of order
+  // 4096), multisection below that
+  const bool bisect = (int64_t)b.n_mat * b.n >= (int64_t)32 * 4096;
+  const void *fn = bisect ? reinterpret_cast<const void *>(&k_tri_eigvals<1>)
+                          : reinterpret_cast<const void *>(&k_tri_eigvals<3>);
   if (shm > 65536) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_tri_eigvals),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(k_tri_eigvals, grid, dim3(EV_THREADS), shm, st, b);
+  if (bisect) hipLaunchKernelGGL(k_tri_eigvals<1>, grid, dim3(EV_THREADS), shm, st, b);
+  else hipLaunchKernelGGL(k_tri_eigvals<3>, grid, dim3(EV_THREADS), shm, st, b);
   return hipGetLastError();
 }
 

@@ -217,6 +217,41 @@ def test_two_stage_and_one_stage_reductions_agree():
     assert np.abs(proj[0] - proj[1]).max() < 1e-4
 
 
+def test_large_batch_eigenvalues_by_bisection():
+    """A call whose matrices times their order reach 32 * 4096 (here 120 token Grams of order
+    T = 1100) resolves the tridiagonal eigenvalues by plain bisection instead of quarter-point
+    multisection (and reduces by two stages): the token spectra of cells spread over the batch
+    match the oracle within 1e-5 of lambda_1 on fp32 cells, and equal those of the same cells
+    computed in a call of three (multisection, one stage) to the same bound.  The batch holds
+    three synthetic cells, each copy scaled by its own factor (so that a mix-up between
+    matrices would show)."""
+    n = 120
+    base = [keys(T=1100, H=8, seed=1000 + s) for s in range(3)]
+    cells = [base[s % 3] * (1.0 + s / 64.0) for s in range(n)]
+    xs, ex, desc = device_cells(cells, "f32")
+    ws = workspace(desc, n)
+    pick = [0, 57, 119]
+    xs3, ex3, desc3 = device_cells([cells[c] for c in pick], "f32")
+    ws3 = workspace(desc3, 3)
+    c2 = J.jolt_create(0)
+    try:
+        note("exact spectrum of", n, "cells at T = 1100")
+        E, lamT, lamd = J.jolt_spectrum(c2, desc, xs, None, None, ws)
+        torch.cuda.synchronize()
+        lam_big = [np.array(lamT[c]) for c in pick]
+        note("exact spectrum of 3 of them")
+        E3, lamT3, lamd3 = J.jolt_spectrum(c2, desc3, xs3, None, None, ws3)
+        torch.cuda.synchronize()
+        lam_small = [np.array(lamT3[i]) for i in range(3)]
+    finally:
+        J.jolt_destroy(c2)
+    for i, c in enumerate(pick):
+        sp = opl.spectrum(ex[c])
+        tol = 1e-5 * sp["lam_T"][0]
+        np.testing.assert_allclose(lam_big[i], sp["lam_T"], rtol=0, atol=tol)
+        np.testing.assert_allclose(lam_big[i], lam_small[i], rtol=0, atol=tol)
+
+
 def test_bulge_chase_that_gives_up_is_reported():
     """JOLT_DBG_BULGE_SPIN = 0 makes the first dependency wait of the two-stage reduction's
     bulge chase give up (forced from the host; the kernel still ends normally): the chase
